@@ -1,0 +1,232 @@
+"""CPU oracle for NLB forward recent sampling (arXiv 2402.01964).
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the CPU-baseline leg
+of the benchmark use it to check the GPU library.  The product path never
+imports it, and it imports nothing from the product package.
+
+The arithmetic lives in ``nlb_oracle.c`` (plain C, one link at a time, in
+stream order); this module only builds that file with gcc and wraps it with
+ctypes and numpy.  Which passage of the paper each function follows is stated
+in the C source:
+
+* ``slot``      -- eq. (2) (NLB-edge) / eq. (3) (NLB-node), Sec. 4.2
+* ``insert*``   -- replacement rule of Sec. 4.2 (empty slot: take; occupied:
+                   replace with probability alpha), both endpoints updated
+* ``sample``    -- eq. (1) strict ``t' < t`` mask; Sec. 4.4 retrieval of
+                   neighbour, link-feature and self rows; App. C T-encoding
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "nlb_oracle.c")
+_LIB = os.path.join(_HERE, "libnlb_oracle.so")
+
+DEFAULT_Q1 = 1000000007
+DEFAULT_Q2 = 998244353
+
+
+def build() -> str:
+    """Compile the oracle with gcc (-O2, no fp contraction, no fast-math)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+           "-Wall", "-Wextra", "-shared", "-fPIC", "-o", _LIB + ".tmp", _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    P = ctypes.c_void_p
+    i32, i64, u32, u64, dbl = (ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32,
+                               ctypes.c_uint64, ctypes.c_double)
+    lib.orc_create.restype = P
+    lib.orc_create.argtypes = [i64, i32, dbl, u64, u64, u64, i32]
+    lib.orc_destroy.argtypes = [P]
+    lib.orc_threshold.restype = u64
+    lib.orc_threshold.argtypes = [P]
+    lib.orc_count.restype = u64
+    lib.orc_count.argtypes = [P]
+    lib.orc_slot.restype = u32
+    lib.orc_slot.argtypes = [P, u32, u32]
+    lib.orc_coin.restype = u32
+    lib.orc_coin.argtypes = [P, u64, u32]
+    lib.orc_insert_at.restype = ctypes.c_int
+    lib.orc_insert_at.argtypes = [P, u64, i32, i32, u32]
+    lib.orc_insert_batch.restype = ctypes.c_int
+    lib.orc_insert_batch.argtypes = [P, P, P, P, i64]
+    lib.orc_insert_ids.restype = ctypes.c_int
+    lib.orc_insert_ids.argtypes = [P, P, P, P, P, i64]
+    lib.orc_export.argtypes = [P, P, P, P]
+    lib.orc_export_nodes.argtypes = [P, P, i64, P, P, P]
+    lib.orc_sample.restype = ctypes.c_int
+    lib.orc_sample.argtypes = [P, P, P, i64, i32, P, P, P, i64, P, i64,
+                               P, P, P, P, P, P, P]
+    lib.orc_tenc.argtypes = [P, i64, i32, P, P, P]
+    _lib = lib
+    return lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+class Oracle:
+    """Sequential NLB tables for ``num_nodes`` nodes with ``s`` slots each."""
+
+    def __init__(self, num_nodes: int, s: int, alpha: float, seed: int,
+                 q1: int = DEFAULT_Q1, q2: int = DEFAULT_Q2, key_mode: int = 0):
+        lib = _load()
+        self._lib = lib
+        self.N, self.s, self.alpha, self.seed = int(num_nodes), int(s), float(alpha), int(seed)
+        self.key_mode = int(key_mode)
+        self._h = lib.orc_create(self.N, self.s, self.alpha, self.seed & (2**64 - 1),
+                                 int(q1), int(q2), self.key_mode)
+        if not self._h:
+            raise ValueError("oracle: invalid parameters or out of memory")
+
+    def close(self):
+        if self._h:
+            self._lib.orc_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def threshold(self) -> int:
+        return int(self._lib.orc_threshold(self._h))
+
+    @property
+    def count(self) -> int:
+        return int(self._lib.orc_count(self._h))
+
+    def slot(self, x: int, t: int) -> int:
+        return int(self._lib.orc_slot(self._h, x, t))
+
+    def coin(self, e: int, k: int) -> int:
+        return int(self._lib.orc_coin(self._h, e, k))
+
+    def insert(self, src, dst, t):
+        src, dst, t = _c(src, np.int32), _c(dst, np.int32), _c(t, np.uint32)
+        if self._lib.orc_insert_batch(self._h, _ptr(src), _ptr(dst), _ptr(t), len(src)) != 0:
+            raise ValueError("oracle: node id out of range")
+
+    def insert_ids(self, eids, src, dst, t):
+        eids = _c(eids, np.uint64)
+        src, dst, t = _c(src, np.int32), _c(dst, np.int32), _c(t, np.uint32)
+        if self._lib.orc_insert_ids(self._h, _ptr(eids), _ptr(src), _ptr(dst), _ptr(t),
+                                    len(src)) != 0:
+            raise ValueError("oracle: node id out of range")
+
+    def export(self):
+        """Canonical table: (nbr int32, ts uint32, eid uint32), each [N, s]."""
+        n = self.N * self.s
+        nbr = np.empty(n, np.int32)
+        ts = np.empty(n, np.uint32)
+        eid = np.empty(n, np.uint32)
+        self._lib.orc_export(self._h, _ptr(nbr), _ptr(ts), _ptr(eid))
+        return nbr.reshape(self.N, self.s), ts.reshape(self.N, self.s), eid.reshape(self.N, self.s)
+
+    def export_nodes(self, nodes):
+        nodes = _c(nodes, np.int32)
+        c = len(nodes)
+        nbr = np.empty((c, self.s), np.int32)
+        ts = np.empty((c, self.s), np.uint32)
+        eid = np.empty((c, self.s), np.uint32)
+        self._lib.orc_export_nodes(self._h, _ptr(nodes), c, _ptr(nbr), _ptr(ts), _ptr(eid))
+        return nbr, ts, eid
+
+    def sample(self, node, tq, w=None, b=None, efeat=None, nfeat=None,
+               want=("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self")):
+        """Answer queries; returns a dict of numpy outputs (see nlb_oracle.c).
+
+        ``efeat``/``nfeat`` are 2-D arrays of any dtype (rows are copied as
+        bytes); outputs keep that dtype.
+        """
+        node, tq = _c(node, np.int32), _c(tq, np.uint32)
+        nq, s = len(node), self.s
+        d_t = 0 if w is None else len(w)
+        w = None if w is None else _c(w, np.float32)
+        b = None if b is None else _c(b, np.float32)
+        out = {}
+        if "nbr" in want:
+            out["nbr"] = np.empty((nq, s), np.int32)
+        if "eid" in want:
+            out["eid"] = np.empty((nq, s), np.uint32)
+        if "ts" in want:
+            out["ts"] = np.empty((nq, s), np.uint32)
+        if "tenc" in want and d_t > 0:
+            out["tenc"] = np.empty((nq, s, d_t), np.float32)
+        erb = nrb = 0
+        if efeat is not None:
+            efeat = np.ascontiguousarray(efeat)
+            erb = efeat.shape[1] * efeat.itemsize
+            if "efeat" in want:
+                out["efeat"] = np.empty((nq, s, efeat.shape[1]), efeat.dtype)
+        if nfeat is not None:
+            nfeat = np.ascontiguousarray(nfeat)
+            nrb = nfeat.shape[1] * nfeat.itemsize
+            if "nfeat" in want:
+                out["nfeat"] = np.empty((nq, s, nfeat.shape[1]), nfeat.dtype)
+            if "self" in want:
+                out["self"] = np.empty((nq, nfeat.shape[1]), nfeat.dtype)
+        rc = self._lib.orc_sample(
+            self._h, _ptr(node), _ptr(tq), nq, d_t, _ptr(w), _ptr(b),
+            _ptr(efeat), erb, _ptr(nfeat), nrb,
+            _ptr(out.get("nbr")), _ptr(out.get("eid")), _ptr(out.get("ts")),
+            _ptr(out.get("tenc")), _ptr(out.get("efeat")), _ptr(out.get("nfeat")),
+            _ptr(out.get("self")))
+        if rc != 0:
+            raise ValueError("oracle: query node out of range")
+        return out
+
+
+def tenc(dt, w, b):
+    """T-encoding of gaps ``dt`` (fp32) -> [len(dt), len(w)] fp32."""
+    lib = _load()
+    dt, w, b = _c(dt, np.float32), _c(w, np.float32), _c(b, np.float32)
+    out = np.empty((len(dt), len(w)), np.float32)
+    lib.orc_tenc(_ptr(dt), len(dt), len(w), _ptr(w), _ptr(b), _ptr(out))
+    return out
+
+
+def run_stream(oracle: Oracle, src, dst, t, neg, batch, w=None, b=None, efeat=None,
+               nfeat=None, batches=None, want=("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self")):
+    """Drive the oracle over a stream in batches (Sec. 4.2 timing: the queries
+    of a batch -- both endpoints and one negative, all at the link's time --
+    are answered from the tables as they stand before the batch is inserted).
+
+    Yields ``(batch_index, outputs)`` for the batches in ``batches`` (all when
+    None); every batch is inserted either way.
+    """
+    E = len(src)
+    nb = (E + batch - 1) // batch
+    wanted = None if batches is None else set(int(x) for x in batches)
+    for bi in range(nb):
+        lo, hi = bi * batch, min(E, (bi + 1) * batch)
+        if wanted is None or bi in wanted:
+            node = np.concatenate([src[lo:hi], dst[lo:hi], neg[lo:hi]])
+            tq = np.concatenate([t[lo:hi], t[lo:hi], t[lo:hi]])
+            yield bi, oracle.sample(node, tq, w, b, efeat, nfeat, want=want)
+        oracle.insert(src[lo:hi], dst[lo:hi], t[lo:hi])

@@ -1,0 +1,256 @@
+/*
+ * nlb_oracle.c -- plain, sequential CPU oracle for NLB forward recent sampling.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, loads or
+ * calls this file; it exists so that tests, the smoke check and the CPU leg of
+ * the benchmark can compare the GPU path against a slow, obviously correct
+ * restatement of the method.  It shares no code, header or constant table
+ * with the GPU path.
+ *
+ * What it follows (Luo & Li, "Scalable and Efficient Temporal Graph
+ * Representation Learning via Forward Recent Sampling", arXiv 2402.01964):
+ *   - Sec. 3, Def. "Temporal network": a time-ordered stream of undirected
+ *     links (u, v, t); the i-th link is identified here by its 0-based
+ *     arrival index e.
+ *   - Sec. 3, eq. (1): temporal neighbours of u at time t are the links of u
+ *     with timestamp strictly below t.
+ *   - Sec. 4.2: every node u owns a table S_u of s slots.  A new link
+ *     (u, v, t) is offered to S_u (neighbour v) and to S_v (neighbour u).  The
+ *     slot is hash(v, t) = (q1*v + q2*t) mod s for NLB-edge, eq. (2), or
+ *     hash(v) = q1*v mod s for NLB-node, eq. (3).  An empty slot always takes
+ *     the offer; an occupied one is overwritten with probability alpha.
+ *     Tables are updated after the queries of the current batch are answered.
+ *   - Sec. 4.4 and App. C: a query (u, t) returns the stored neighbours, their
+ *     link features, the neighbours' own feature rows, the self row and a
+ *     cosine time encoding of t - t'.
+ *
+ * Random draws: the replacement coin of offer (e, k) (k = 0 for the S_u
+ * offer, k = 1 for the S_v offer) is the high 32 bits of output number
+ * 2e+k+1 of SplitMix64 (Steele, Lea & Flood, OOPSLA 2014) started from state
+ * `seed`; the offer replaces an occupant when coin < floor(alpha * 2^32)
+ * (alpha = 1 gives 2^32, i.e. always).
+ *
+ * Precision: the time encoding is cos() in double of the fp32 argument
+ * fmaf(w, (float)(tq - t'), b), rounded to fp32.  Build with
+ * -ffp-contract=off and without fast-math.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef struct orc {
+    int64_t N;          /* number of nodes */
+    int32_t s;          /* slots per node */
+    int32_t key_mode;   /* 0: NLB-edge eq. (2); 1: NLB-node eq. (3) */
+    double alpha;
+    uint64_t thr;       /* floor(alpha * 2^32), 2^32 when alpha == 1 */
+    uint64_t seed;
+    uint64_t q1, q2;
+    int32_t *nbr;       /* [N*s], -1 = empty */
+    uint32_t *ts;       /* [N*s] */
+    uint32_t *eid;      /* [N*s] */
+    uint64_t next_e;    /* arrival index of the next link */
+} orc;
+
+/* n-th output (n >= 1) of SplitMix64 whose state starts at `state0`. */
+static uint64_t splitmix64_nth(uint64_t state0, uint64_t n)
+{
+    uint64_t z = state0 + n * 0x9E3779B97F4A7C15ULL;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+    return z ^ (z >> 31);
+}
+
+orc *orc_create(int64_t N, int32_t s, double alpha, uint64_t seed,
+                uint64_t q1, uint64_t q2, int32_t key_mode)
+{
+    if (N <= 0 || s <= 0 || !(alpha > 0.0 && alpha <= 1.0)) return NULL;
+    if (key_mode != 0 && key_mode != 1) return NULL;
+    /* q1*x + q2*t must not wrap in 64 bits: x < 2^31, t < 2^32. */
+    if (q1 >= (1ULL << 31) || q2 >= (1ULL << 31)) return NULL;
+    orc *o = (orc *)calloc(1, sizeof(orc));
+    if (!o) return NULL;
+    o->N = N; o->s = s; o->key_mode = key_mode; o->alpha = alpha;
+    o->seed = seed; o->q1 = q1; o->q2 = q2;
+    o->thr = (alpha >= 1.0) ? (1ULL << 32) : (uint64_t)floor(alpha * 4294967296.0);
+    size_t n = (size_t)N * (size_t)s;
+    o->nbr = (int32_t *)malloc(n * sizeof(int32_t));
+    o->ts = (uint32_t *)malloc(n * sizeof(uint32_t));
+    o->eid = (uint32_t *)malloc(n * sizeof(uint32_t));
+    if (!o->nbr || !o->ts || !o->eid) {
+        free(o->nbr); free(o->ts); free(o->eid); free(o);
+        return NULL;
+    }
+    for (size_t i = 0; i < n; i++) {
+        o->nbr[i] = -1; o->ts[i] = 0xFFFFFFFFu; o->eid[i] = 0xFFFFFFFFu;
+    }
+    return o;
+}
+
+void orc_destroy(orc *o)
+{
+    if (!o) return;
+    free(o->nbr); free(o->ts); free(o->eid); free(o);
+}
+
+uint64_t orc_threshold(const orc *o) { return o->thr; }
+uint64_t orc_count(const orc *o) { return o->next_e; }
+
+/* Slot of neighbour x seen at time t: eq. (2) (NLB-edge) or eq. (3) (NLB-node). */
+uint32_t orc_slot(const orc *o, uint32_t x, uint32_t t)
+{
+    uint64_t h = (o->key_mode == 0) ? o->q1 * (uint64_t)x + o->q2 * (uint64_t)t
+                                    : o->q1 * (uint64_t)x;
+    return (uint32_t)(h % (uint64_t)o->s);
+}
+
+uint32_t orc_coin(const orc *o, uint64_t e, uint32_t k)
+{
+    return (uint32_t)(splitmix64_nth(o->seed, 2 * e + k + 1) >> 32);
+}
+
+/* One offer: neighbour x of table n, from link (e, t).  Sec. 4.2: an empty
+ * slot takes it; an occupied slot is replaced with probability alpha. */
+static void offer(orc *o, int32_t n, int32_t x, uint32_t t, uint64_t e, uint32_t k)
+{
+    size_t idx = (size_t)n * (size_t)o->s + orc_slot(o, (uint32_t)x, t);
+    int empty = (o->nbr[idx] == -1);
+    if (empty || (uint64_t)orc_coin(o, e, k) < o->thr) {
+        o->nbr[idx] = x;
+        o->ts[idx] = t;
+        o->eid[idx] = (uint32_t)e;
+    }
+}
+
+/* Insert link (u, v, t) with explicit arrival index e.  Returns 0, or -1 when
+ * an endpoint is out of range (nothing is changed then). */
+int orc_insert_at(orc *o, uint64_t e, int32_t u, int32_t v, uint32_t t)
+{
+    if (u < 0 || v < 0 || u >= o->N || v >= o->N) return -1;
+    offer(o, u, v, t, e, 0);   /* S_u receives neighbour v */
+    offer(o, v, u, t, e, 1);   /* S_v receives neighbour u */
+    return 0;
+}
+
+/* Insert n links in stream order; their arrival indices continue the count. */
+int orc_insert_batch(orc *o, const int32_t *src, const int32_t *dst,
+                     const uint32_t *t, int64_t n)
+{
+    for (int64_t i = 0; i < n; i++) {
+        if (orc_insert_at(o, o->next_e, src[i], dst[i], t[i]) != 0) return -1;
+        o->next_e++;
+    }
+    return 0;
+}
+
+/* Insert n links whose arrival indices are given (a filtered sub-stream).
+ * The indices must increase; the count afterwards is eids[n-1] + 1. */
+int orc_insert_ids(orc *o, const uint64_t *eids, const int32_t *src,
+                   const int32_t *dst, const uint32_t *t, int64_t n)
+{
+    for (int64_t i = 0; i < n; i++) {
+        if (orc_insert_at(o, eids[i], src[i], dst[i], t[i]) != 0) return -1;
+        o->next_e = eids[i] + 1;
+    }
+    return 0;
+}
+
+void orc_export(const orc *o, int32_t *nbr, uint32_t *ts, uint32_t *eid)
+{
+    size_t n = (size_t)o->N * (size_t)o->s;
+    memcpy(nbr, o->nbr, n * sizeof(int32_t));
+    memcpy(ts, o->ts, n * sizeof(uint32_t));
+    memcpy(eid, o->eid, n * sizeof(uint32_t));
+}
+
+/* Export the slots of selected nodes: outputs are [count][s]. */
+void orc_export_nodes(const orc *o, const int32_t *nodes, int64_t count,
+                      int32_t *nbr, uint32_t *ts, uint32_t *eid)
+{
+    for (int64_t i = 0; i < count; i++) {
+        size_t src = (size_t)nodes[i] * (size_t)o->s;
+        size_t dst = (size_t)i * (size_t)o->s;
+        memcpy(nbr + dst, o->nbr + src, (size_t)o->s * sizeof(int32_t));
+        memcpy(ts + dst, o->ts + src, (size_t)o->s * sizeof(uint32_t));
+        memcpy(eid + dst, o->eid + src, (size_t)o->s * sizeof(uint32_t));
+    }
+}
+
+/* T-encoding of one time gap (App. C, with a phase b per dimension):
+ * cos(w_k * dt + b_k), the argument formed in fp32 by a single fused
+ * multiply-add, the cosine taken in double and rounded to fp32. */
+static float tenc_value(float w, float dt, float b)
+{
+    float arg = fmaf(w, dt, b);
+    return (float)cos((double)arg);
+}
+
+/*
+ * Answer nq queries (node[i], tq[i]) from the current tables (Sec. 4.4).
+ * Per query i and slot a (row-major [nq][s][...]):
+ *   valid    = slot non-empty and its timestamp t' < tq   (eq. (1), strict)
+ *   nbr/eid/ts = the stored entry, or -1 / 0xFFFFFFFF / 0xFFFFFFFF
+ *   tenc[k]  = tenc_value(w[k], (float)(tq - t'), b[k]) for k < d_t, else 0
+ *   efeat    = bytes of edge-feature row eid, else zero bytes
+ *   nfeat    = bytes of node-feature row nbr, else zero bytes
+ *   self     = bytes of node-feature row node[i]
+ * Any output pointer may be NULL.  Returns -1 on an out-of-range node.
+ */
+int orc_sample(const orc *o, const int32_t *node, const uint32_t *tq, int64_t nq,
+               int32_t d_t, const float *w, const float *b,
+               const uint8_t *efeat, int64_t e_row_bytes,
+               const uint8_t *nfeat, int64_t n_row_bytes,
+               int32_t *nbr_out, uint32_t *eid_out, uint32_t *ts_out,
+               float *tenc_out, uint8_t *efeat_out, uint8_t *nfeat_out,
+               uint8_t *self_out)
+{
+    const int64_t s = o->s;
+    for (int64_t i = 0; i < nq; i++) {
+        int32_t n = node[i];
+        if (n < 0 || n >= o->N) return -1;
+        for (int64_t a = 0; a < s; a++) {
+            size_t src = (size_t)n * (size_t)s + (size_t)a;
+            size_t out = (size_t)i * (size_t)s + (size_t)a;
+            int valid = (o->nbr[src] != -1) && (o->ts[src] < tq[i]);
+            if (nbr_out) nbr_out[out] = valid ? o->nbr[src] : -1;
+            if (eid_out) eid_out[out] = valid ? o->eid[src] : 0xFFFFFFFFu;
+            if (ts_out) ts_out[out] = valid ? o->ts[src] : 0xFFFFFFFFu;
+            if (tenc_out) {
+                float *row = tenc_out + out * (size_t)d_t;
+                if (valid) {
+                    float dt = (float)(uint32_t)(tq[i] - o->ts[src]);
+                    for (int32_t k = 0; k < d_t; k++) row[k] = tenc_value(w[k], dt, b[k]);
+                } else {
+                    for (int32_t k = 0; k < d_t; k++) row[k] = 0.0f;
+                }
+            }
+            if (efeat_out && e_row_bytes > 0) {
+                uint8_t *dst = efeat_out + out * (size_t)e_row_bytes;
+                if (valid)
+                    memcpy(dst, efeat + (size_t)o->eid[src] * (size_t)e_row_bytes, (size_t)e_row_bytes);
+                else
+                    memset(dst, 0, (size_t)e_row_bytes);
+            }
+            if (nfeat_out && n_row_bytes > 0) {
+                uint8_t *dst = nfeat_out + out * (size_t)n_row_bytes;
+                if (valid)
+                    memcpy(dst, nfeat + (size_t)o->nbr[src] * (size_t)n_row_bytes, (size_t)n_row_bytes);
+                else
+                    memset(dst, 0, (size_t)n_row_bytes);
+            }
+        }
+        if (self_out && n_row_bytes > 0)
+            memcpy(self_out + (size_t)i * (size_t)n_row_bytes,
+                   nfeat + (size_t)n * (size_t)n_row_bytes, (size_t)n_row_bytes);
+    }
+    return 0;
+}
+
+/* Stand-alone T-encoding of a list of gaps, for direct checks of App. C. */
+void orc_tenc(const float *dt, int64_t n, int32_t d_t, const float *w, const float *b, float *out)
+{
+    for (int64_t i = 0; i < n; i++)
+        for (int32_t k = 0; k < d_t; k++)
+            out[(size_t)i * (size_t)d_t + (size_t)k] = tenc_value(w[k], dt[i], b[k]);
+}

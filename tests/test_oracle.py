@@ -1,0 +1,459 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Each test checks the oracle against something other than itself: a
+hand-worked example, published known-answer values, a brute-force
+formulation that does not replay the sequential loop, a closed-form law or a
+textbook special case.  All run on the CPU.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import Oracle
+
+Q1, Q2 = oracle.DEFAULT_Q1, oracle.DEFAULT_Q2
+
+
+# ----------------------------------------------------------------------------- helpers
+def slot_residue(x, t, s, q1=Q1, q2=Q2, key_mode=0):
+    """eq. (2)/(3) evaluated through residues mod s (a different formulation
+    from the oracle's direct 64-bit product)."""
+    x = np.asarray(x, np.uint64) % np.uint64(s)
+    t = np.asarray(t, np.uint64) % np.uint64(s)
+    a = (np.uint64(q1 % s) * x) % np.uint64(s)
+    if key_mode == 0:
+        a = (a + (np.uint64(q2 % s) * t) % np.uint64(s)) % np.uint64(s)
+    return a.astype(np.int64)
+
+
+def offers_of(src, dst, t):
+    """Offer list in sequential order: (e, k, table n, neighbour x, t)."""
+    E = len(src)
+    e = np.repeat(np.arange(E, dtype=np.int64), 2)
+    k = np.tile(np.array([0, 1], np.int64), E)
+    n = np.stack([src, dst], 1).reshape(-1).astype(np.int64)
+    x = np.stack([dst, src], 1).reshape(-1).astype(np.int64)
+    tt = np.repeat(np.asarray(t, np.int64), 2)
+    return e, k, n, x, tt
+
+
+def random_stream(rng, N, E, tmax, self_loops=True):
+    src = rng.integers(0, N, E).astype(np.int32)
+    dst = rng.integers(0, N, E).astype(np.int32)
+    if not self_loops:
+        bad = src == dst
+        while bad.any():
+            dst[bad] = rng.integers(0, N, bad.sum())
+            bad = src == dst
+    t = np.sort(rng.integers(0, tmax, E)).astype(np.uint32)
+    return src, dst, t
+
+
+def table_from_winners(N, s, n, a, x, t, e):
+    nbr = np.full((N, s), -1, np.int32)
+    ts = np.full((N, s), 0xFFFFFFFF, np.uint32)
+    eid = np.full((N, s), 0xFFFFFFFF, np.uint32)
+    nbr[n, a] = x
+    ts[n, a] = t
+    eid[n, a] = e
+    return nbr, ts, eid
+
+
+def brute_force_table(N, s, src, dst, t, keep, pick_max=True, key_mode=0):
+    """Per (node, slot): the max-e (or min-e) offer among offers where
+    ``keep`` is True.  Group-by over the whole offer set; no sequential loop."""
+    e, k, n, x, tt = offers_of(src, dst, t)
+    a = slot_residue(x, tt, s, key_mode=key_mode)
+    m = keep
+    e, n, x, tt, a = e[m], n[m], x[m], tt[m], a[m]
+    cell = n * s + a
+    order = np.lexsort((e if pick_max else -e, cell))
+    cell_sorted = cell[order]
+    last = np.ones(len(order), bool)
+    last[:-1] = cell_sorted[1:] != cell_sorted[:-1]
+    w = order[last]
+    return table_from_winners(N, s, n[w], a[w], x[w], tt[w], e[w])
+
+
+def first_offer_mask(n, a, s):
+    cell = n * s + a
+    _, first_idx = np.unique(cell, return_index=True)
+    m = np.zeros(len(cell), bool)
+    m[first_idx] = True
+    return m
+
+
+def assert_tables_equal(got, want):
+    for g, w, name in zip(got, want, ("nbr", "ts", "eid")):
+        np.testing.assert_array_equal(g, w, err_msg=name)
+
+
+# ----------------------------------------------------------------------------- known answers
+def _read_golden(path):
+    rows = []
+    with open(path) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if line:
+                rows.append(line.split())
+    return rows
+
+
+def test_coin_matches_splitmix64_known_answers(golden_dir):
+    """coin(e, k) is the high half of SplitMix64 output 2e+k+1: pinned to the
+    published outputs for start states 0 and 1234567."""
+    for st, n, val in _read_golden(os.path.join(golden_dir, "splitmix64_vectors.txt")):
+        st, n, val = int(st), int(n), int(val, 0)
+        o = Oracle(4, 1, 0.5, seed=st)
+        e, k = (n - 1) // 2, (n - 1) % 2
+        assert o.coin(e, k) == val >> 32, (st, n)
+
+
+def test_handworked_tables(golden_dir):
+    """The hand-worked 6-link example (eq. (2), eq. (3), replacement rule)."""
+    rows = _read_golden(os.path.join(golden_dir, "handworked_tables.txt"))
+    params = dict(kv.split("=") for kv in rows[0][1:])
+    N, s, q1, q2 = (int(params[k]) for k in ("N", "s", "q1", "q2"))
+    links = np.array([[int(v) for v in r[1:]] for r in rows if r[0] == "link"])
+    assert (links[:, 0] == np.arange(len(links))).all()
+    src, dst, t = links[:, 1], links[:, 2], links[:, 3]
+    alphas = {"latest": 1.0, "first": 1e-12}
+    made = {}
+    for mode, km in (("edge", 0), ("node", 1)):
+        for rule, alpha in alphas.items():
+            o = Oracle(N, s, alpha, seed=99, q1=q1, q2=q2, key_mode=km)
+            o.insert(src, dst, t)
+            made[(mode, rule)] = o
+    assert made[("edge", "first")].threshold == 0
+    assert made[("edge", "latest")].threshold == 2**32
+    checked = 0
+    for r in rows:
+        if r[0] != "table":
+            continue
+        mode, rule, node, a, nbr = r[1], r[2], int(r[3]), int(r[4]), int(r[5])
+        got_nbr, got_ts, got_eid = made[(mode, rule)].export()
+        assert got_nbr[node, a] == nbr, r
+        if nbr >= 0:
+            assert got_ts[node, a] == int(r[6]) and got_eid[node, a] == int(r[7]), r
+        else:
+            assert got_ts[node, a] == 0xFFFFFFFF and got_eid[node, a] == 0xFFFFFFFF, r
+        checked += 1
+    assert checked == 4 * N * s
+    for r in rows:
+        if r[0] != "query":
+            continue
+        rule, node, tq, a, valid = r[1], int(r[2]), int(r[3]), int(r[4]), int(r[5])
+        out = made[("edge", rule)].sample([node], [tq])
+        assert (out["nbr"][0, a] >= 0) == bool(valid), r
+
+
+def test_slot_matches_eq2_bigint():
+    """64-bit evaluation of eq. (2)/(3) equals arbitrary-precision integers."""
+    rng = np.random.default_rng(1)
+    xs = rng.integers(0, 2**31, 3000)
+    ts = rng.integers(0, 2**32, 3000)
+    xs[:3] = [0, 2**31 - 1, 2**31 - 1]
+    ts[:3] = [0, 2**32 - 1, 0]
+    for s in (1, 2, 7, 10, 20, 64, 1000):
+        for km in (0, 1):
+            o = Oracle(2, s, 0.5, 0, key_mode=km)
+            for x, t in zip(xs[:400], ts[:400]):
+                want = (Q1 * int(x) + (Q2 * int(t) if km == 0 else 0)) % s
+                assert o.slot(int(x), int(t)) == want
+
+
+def test_threshold_values():
+    """floor(alpha * 2^32) in double (alpha = 1 -> 2^32)."""
+    assert Oracle(2, 1, 1.0, 0).threshold == 2**32
+    assert Oracle(2, 1, 0.5, 0).threshold == 2**31
+    assert Oracle(2, 1, 0.3, 0).threshold == 1288490188
+    assert Oracle(2, 1, 0.9, 0).threshold == math.floor(0.9 * 2**32)
+
+
+def test_rejects_bad_parameters():
+    for kw in (dict(num_nodes=0, s=1, alpha=0.5), dict(num_nodes=4, s=0, alpha=0.5),
+               dict(num_nodes=4, s=2, alpha=0.0), dict(num_nodes=4, s=2, alpha=1.5)):
+        with pytest.raises(ValueError):
+            Oracle(seed=0, **kw)
+    o = Oracle(4, 2, 0.5, 0)
+    with pytest.raises(ValueError):
+        o.insert([0], [4], [1])
+    with pytest.raises(ValueError):
+        o.sample([7], [1])
+
+
+# ----------------------------------------------------------------------------- coin statistics
+def test_coin_uniform_and_acceptance_rate():
+    """The coin is uniform on 32 bits (chi^2 over 256 bins of its top byte)
+    and passes thr = floor(alpha 2^32) with frequency alpha."""
+    o = Oracle(2, 1, 0.3, seed=12345)
+    n = 200000
+    r = np.array([o.coin(e, k) for e in range(n // 2) for k in (0, 1)], np.uint64)
+    hist = np.bincount((r >> np.uint64(24)).astype(np.int64), minlength=256)
+    expect = n / 256
+    chi2 = ((hist - expect) ** 2 / expect).sum()
+    # 255 dof: mean 255, sd ~22.6; 6 sd bound
+    assert chi2 < 255 + 6 * 22.6
+    for alpha in (0.1, 0.3, 0.5, 0.9):
+        thr = math.floor(alpha * 2**32)
+        p = (r < thr).mean()
+        assert abs(p - alpha) < 5 * math.sqrt(alpha * (1 - alpha) / n)
+
+
+# ----------------------------------------------------------------------------- brute force
+@pytest.mark.parametrize("s,key_mode", [(1, 0), (3, 0), (10, 0), (20, 0), (10, 1)])
+def test_alpha_one_each_slot_holds_latest(s, key_mode):
+    """alpha = 1: every slot holds the latest offer hashing to it."""
+    rng = np.random.default_rng(s + 10 * key_mode)
+    N, E = 50, 3000
+    src, dst, t = random_stream(rng, N, E, 10**6)
+    o = Oracle(N, s, 1.0, seed=5, key_mode=key_mode)
+    o.insert(src, dst, t)
+    keep = np.ones(2 * E, bool)
+    assert_tables_equal(o.export(), brute_force_table(N, s, src, dst, t, keep, True, key_mode))
+
+
+def test_threshold_zero_each_slot_holds_first():
+    """alpha below 2^-32 (threshold 0): only empty slots take offers, so
+    every slot holds the first offer hashing to it."""
+    rng = np.random.default_rng(3)
+    N, s, E = 40, 10, 3000
+    src, dst, t = random_stream(rng, N, E, 10**6)
+    o = Oracle(N, s, 1e-12, seed=5)
+    assert o.threshold == 0
+    o.insert(src, dst, t)
+    keep = np.ones(2 * E, bool)
+    assert_tables_equal(o.export(), brute_force_table(N, s, src, dst, t, keep, False))
+
+
+def test_single_slot_alpha_one_is_truncation_to_one():
+    """s = 1, alpha = 1: each node keeps exactly its most recent link
+    (truncation with one neighbour, Sec. 4.1)."""
+    rng = np.random.default_rng(4)
+    N, E = 30, 2000
+    src, dst, t = random_stream(rng, N, E, 10**5)
+    o = Oracle(N, 1, 1.0, seed=1)
+    o.insert(src, dst, t)
+    nbr, ts, eid = o.export()
+    for node in range(N):
+        touching = np.nonzero((src == node) | (dst == node))[0]
+        if len(touching) == 0:
+            assert nbr[node, 0] == -1
+            continue
+        last = touching[-1]
+        other = dst[last] if src[last] == node else src[last]
+        assert (nbr[node, 0], ts[node, 0], eid[node, 0]) == (other, t[last], last)
+
+
+@pytest.mark.parametrize("alpha,seed", [(0.3, 11), (0.5, 12), (0.9, 13)])
+def test_set_form_brute_force(alpha, seed):
+    """Any alpha: slot (n,a) holds the max-e offer of the set
+    {first offer to (n,a)} U {offers to (n,a) whose coin passes} --
+    a formulation that never replays the sequential loop."""
+    rng = np.random.default_rng(seed)
+    N, s, E = 60, 10, 4000
+    src, dst, t = random_stream(rng, N, E, 10**6)
+    o = Oracle(N, s, alpha, seed=seed * 7)
+    o.insert(src, dst, t)
+    e, k, n, x, tt = offers_of(src, dst, t)
+    a = slot_residue(x, tt, s)
+    coin = np.array([o.coin(int(ee), int(kk)) for ee, kk in zip(e, k)], np.uint64)
+    keep = first_offer_mask(n, a, s) | (coin < np.uint64(o.threshold))
+    assert_tables_equal(o.export(), brute_force_table(N, s, src, dst, t, keep, True))
+
+
+def test_batching_is_invisible_to_the_table():
+    """Inserting in batches of any size gives the one-at-a-time table."""
+    rng = np.random.default_rng(8)
+    N, s, E = 80, 10, 5000
+    src, dst, t = random_stream(rng, N, E, 10**6)
+    ref = Oracle(N, s, 0.5, seed=3)
+    for i in range(E):
+        ref.insert(src[i:i + 1], dst[i:i + 1], t[i:i + 1])
+    for B in (7, 200, 4999):
+        o = Oracle(N, s, 0.5, seed=3)
+        for lo in range(0, E, B):
+            o.insert(src[lo:lo + B], dst[lo:lo + B], t[lo:lo + B])
+        assert_tables_equal(o.export(), ref.export())
+
+
+def test_filtered_substream_gives_same_rows():
+    """Tables are per node: inserting only the links that touch a node set,
+    with their global arrival indices, gives those nodes' rows exactly."""
+    rng = np.random.default_rng(9)
+    N, s, E = 200, 10, 8000
+    src, dst, t = random_stream(rng, N, E, 10**6)
+    full = Oracle(N, s, 0.5, seed=21)
+    full.insert(src, dst, t)
+    nodes = np.array([0, 3, 17, 150, 199], np.int32)
+    sel = np.nonzero(np.isin(src, nodes) | np.isin(dst, nodes))[0]
+    part = Oracle(N, s, 0.5, seed=21)
+    part.insert_ids(sel, src[sel], dst[sel], t[sel])
+    for a, b in zip(part.export_nodes(nodes), full.export_nodes(nodes)):
+        np.testing.assert_array_equal(a, b)
+
+
+# ----------------------------------------------------------------------------- invariants
+def test_invariants_and_strict_query_mask():
+    rng = np.random.default_rng(10)
+    N, s, E = 100, 10, 6000
+    src, dst, t = random_stream(rng, N, E, 10**5)
+    o = Oracle(N, s, 0.5, seed=2)
+    o.insert(src, dst, t)
+    nbr, ts, eid = o.export()
+    for node in range(N):
+        for a in range(s):
+            if nbr[node, a] < 0:
+                continue
+            e_ = int(eid[node, a])
+            assert {int(src[e_]), int(dst[e_])} == {node, int(nbr[node, a])}
+            assert ts[node, a] == t[e_]
+            assert o.slot(int(nbr[node, a]), int(ts[node, a])) == a
+    nodes = rng.integers(0, N, 500).astype(np.int32)
+    tq = rng.integers(0, 10**5, 500).astype(np.uint32)
+    out = o.sample(nodes, tq)
+    for i in range(len(nodes)):
+        row_t = ts[nodes[i]]
+        valid = (nbr[nodes[i]] >= 0) & (row_t < tq[i])
+        assert ((out["nbr"][i] >= 0) == valid).all()
+        assert (out["ts"][i][valid] < tq[i]).all()
+        assert (out["eid"][i][~valid] == 0xFFFFFFFF).all()
+
+
+# ----------------------------------------------------------------------------- closed forms
+@pytest.mark.parametrize("alpha", [0.3, 0.5, 0.9])
+def test_survival_law_over_seeds(alpha):
+    """An offer followed by m later offers to its slot is present at the end
+    with probability alpha(1-alpha)^m if the slot was occupied when it
+    arrived, and (1-alpha)^m if it was empty (Sec. 4.2 rule; the per-link
+    replacement step used in the proof of Theorem 1)."""
+    rng = np.random.default_rng(100)
+    N, s, E = 6, 2, 30
+    src, dst, t = random_stream(rng, N, E, 1000, self_loops=False)
+    e, k, n, x, tt = offers_of(src, dst, t)
+    a = slot_residue(x, tt, s)
+    cell = n * s + a
+    m = np.array([(cell[i + 1:] == cell[i]).sum() for i in range(len(cell))])
+    occupied = np.array([(cell[:i] == cell[i]).any() for i in range(len(cell))])
+    p = np.where(occupied, alpha * (1 - alpha) ** m, (1 - alpha) ** m)
+    K = 20000
+    hits = np.zeros(len(cell))
+    for seed in range(1, K + 1):
+        o = Oracle(N, s, alpha, seed=seed)
+        o.insert(src, dst, t)
+        _, _, eid = o.export()
+        hits += eid[n, a] == e
+    freq = hits / K
+    sd = np.sqrt(np.maximum(p * (1 - p), 1e-12) / K)
+    z = np.abs(freq - p) / sd
+    assert z.max() < 4.5, (z.max(), freq[z.argmax()], p[z.argmax()])
+
+
+def test_theorem1_poisson_hub_survival():
+    """Theorem 1 (NLB-edge achieves recent sampling): with Poisson(lambda)
+    arrivals at a hub, a link that entered S_u at t_i is still there at t
+    with probability exp(-alpha lambda (t - t_i) / s).  Away from the start,
+    an offer enters with probability alpha, so presence = alpha * that."""
+    alpha, s, lam, T, H = 0.5, 10, 1.0, 200.0, 400
+    scale = 1000.0
+    pres, delta = [], []
+    for rep in range(4):
+        rng = np.random.default_rng(500 + rep)
+        times, hubs = [], []
+        for h in range(H):
+            n = rng.poisson(lam * T)
+            times.append(rng.uniform(0, T, n))
+            hubs.append(np.full(n, h))
+        times = np.concatenate(times)
+        hubs = np.concatenate(hubs)
+        order = np.argsort(times, kind="stable")
+        times, hubs = times[order], hubs[order]
+        E = len(times)
+        leaves = H + rng.permutation(E)          # every leaf appears once
+        tt = np.floor(times * scale).astype(np.uint32)
+        o = Oracle(H + E, s, alpha, seed=900 + rep)
+        o.insert(hubs.astype(np.int32), leaves.astype(np.int32), tt)
+        nbr, ts, eid = o.export_nodes(np.arange(H, dtype=np.int32))
+        present = np.zeros(E, bool)
+        got = eid[eid != 0xFFFFFFFF]
+        present[got] = True
+        keep = times > 60.0                       # tables long since full
+        pres.append(present[keep])
+        delta.append(T - times[keep])
+    pres = np.concatenate(pres)
+    delta = np.concatenate(delta)
+    expect = alpha * np.exp(-alpha * lam * delta / s)
+    edges = np.arange(0, 141, 10.0)
+    for lo, hi in zip(edges[:-1], edges[1:]):
+        m = (delta >= lo) & (delta < hi)
+        n = m.sum()
+        mu = expect[m].sum()
+        var = (expect[m] * (1 - expect[m])).sum()
+        assert abs(pres[m].sum() - mu) < 5 * math.sqrt(var) + 1, (lo, pres[m].sum(), mu, n)
+
+
+# ----------------------------------------------------------------------------- T-encoding
+def test_tenc_paper_form_cos_sin_pairs():
+    """App. C: with phases b in {0, -pi/2} the encoding is the
+    [cos(w t), sin(w t)] pairs of the paper.  Frequencies are powers of two
+    and gaps small integers, so w*dt is exact in fp32."""
+    d = 16
+    w = np.repeat(2.0 ** -np.arange(d // 2), 2).astype(np.float32)
+    b = np.tile(np.array([0.0, -np.pi / 2], np.float32), d // 2)
+    dt = np.array([0, 1, 2, 3, 5], np.float32)
+    out = oracle.tenc(dt, w, b)
+    for i, g in enumerate(dt):
+        for j in range(d // 2):
+            x = float(w[2 * j]) * float(g)
+            assert abs(out[i, 2 * j] - math.cos(x)) < 1e-7
+            assert abs(out[i, 2 * j + 1] - math.sin(x)) < 1e-6
+
+
+def test_tenc_zero_gap_and_exact_points():
+    w = np.array([1.0, 0.5, 1e-9, 3.0], np.float32)
+    b = np.array([0.0, np.float32(np.pi), 0.25, -1.0], np.float32)
+    out = oracle.tenc(np.array([0.0], np.float32), w, b)[0]
+    assert out[0] == 1.0
+    assert abs(out[1] + 1.0) < 1e-7
+    assert abs(out[2] - math.cos(0.25)) < 1e-7
+    assert abs(out[3] - math.cos(-1.0)) < 1e-7
+
+
+def test_sample_outputs_rows_and_zeros():
+    """Sec. 4.4 retrieval: valid slots carry the link's feature row, the
+    neighbour's node row and the T-encoding of tq - t'; invalid slots carry
+    -1 / 0xFFFFFFFF and all-zero rows; the self row is the query node's."""
+    rng = np.random.default_rng(20)
+    N, s, E = 40, 4, 500
+    src, dst, t = random_stream(rng, N, E, 10**4)
+    o = Oracle(N, s, 0.5, seed=4)
+    o.insert(src, dst, t)
+    efeat = rng.standard_normal((E, 6)).astype(np.float32)
+    nfeat = rng.integers(0, 2**16, (N, 5)).astype(np.uint16)
+    w = rng.uniform(0, 1, 7).astype(np.float32)
+    b = rng.uniform(-3, 3, 7).astype(np.float32)
+    nodes = rng.integers(0, N, 100).astype(np.int32)
+    tq = rng.integers(0, 10**4, 100).astype(np.uint32)
+    out = o.sample(nodes, tq, w, b, efeat, nfeat)
+    nbr, ts, eid = o.export()
+    for i in range(100):
+        np.testing.assert_array_equal(out["self"][i], nfeat[nodes[i]])
+        for a in range(s):
+            valid = nbr[nodes[i], a] >= 0 and ts[nodes[i], a] < tq[i]
+            if valid:
+                e_ = eid[nodes[i], a]
+                np.testing.assert_array_equal(out["efeat"][i, a], efeat[e_])
+                np.testing.assert_array_equal(out["nfeat"][i, a], nfeat[nbr[nodes[i], a]])
+                gap = np.float32(int(tq[i]) - int(ts[nodes[i], a]))
+                for kk in range(7):
+                    arg = np.float32(float(w[kk]) * float(gap) + float(b[kk]))  # fma, one rounding
+                    want = math.cos(float(arg))
+                    assert abs(out["tenc"][i, a, kk] - want) < 2e-6
+            else:
+                assert out["nbr"][i, a] == -1 and out["eid"][i, a] == 0xFFFFFFFF
+                assert out["ts"][i, a] == 0xFFFFFFFF
+                assert not out["efeat"][i, a].any() and not out["nfeat"][i, a].any()
+                assert not out["tenc"][i, a].any()
