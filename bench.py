@@ -1,0 +1,227 @@
+#!/usr/bin/env python3
+"""Benchmark of the NLB forward-recent-sampling hot path on one MI355X.
+
+A step is one batch of the stream through the whole hot path, in the
+paper's order (Sec. 4.2): nlb_sample answers the batch's queries (both
+endpoints and one negative per link, at the link's time) from the current
+tables, then nlb_insert_batch applies the batch's links.  Inputs (the whole
+stream in the batch-blocked layout, feature tables, time parameters) are
+resident in HBM before timing starts; the tables are first filled by
+inserting the stream up to the start batch.
+
+Prints one JSON line.  `value` is links per second through the whole step;
+queries/s and the kernel-only rates are extra fields.  `roofline` reports
+the sample kernel (the dominant one) against MI355X peak HBM bandwidth,
+timed with HIP events on the stream the kernels run on.  `cpu_baseline`
+times the CPU oracle on a bounded prefix of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", type=int, default=5)
+    ap.add_argument("--start-batch", type=int, default=None,
+                    help="first batch of the warmup (default: the middle of the stream)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    return ap.parse_args()
+
+
+def sample_bytes(w, valid_slots, queries):
+    """Algorithmic HBM bytes of one sample launch: what the method must move.
+    Reads: node id + query time (8 B), the s table slots (12 B each), the
+    link-feature and neighbour rows of valid slots and the self row.
+    Writes: nbr/eid/ts (12 B per slot), the fp32 time encoding (4*d_time per
+    slot), feature rows of every slot (zeros when invalid) and the self row."""
+    s, erb, nrb = w.s, w.row_bytes("edge"), w.row_bytes("node")
+    reads = queries * (8 + 12 * s + nrb) + valid_slots * (erb + nrb)
+    writes = queries * s * (12 + 4 * w.d_time + erb + nrb) + queries * nrb
+    return reads + writes
+
+
+def insert_bytes(links):
+    """Algorithmic bytes of one insert: 12 B of input per link, and per
+    offer an 8 B key read-modify-write plus a 4 B neighbour write."""
+    return links * (12 + 2 * (8 + 8 + 4))
+
+
+def cpu_baseline(w, budget_s, max_batches=400):
+    """The CPU oracle, single-threaded, over the first batches of the same
+    stream (sample then insert per batch) until the time budget is used.
+    Stream and feature rows are generated outside the timed region; the
+    oracle gathers rows from full-size host tables whose untouched rows stay
+    unmaterialised zero pages."""
+    import numpy as np
+
+    import oracle
+    import synth
+    o = oracle.Oracle(w.num_nodes, w.s, w.alpha, w.table_seed)
+    fw, fb = synth.time_params(w)
+    nb_max = min(w.batches, max_batches)
+    whole = None if w.stateless else synth.host_links(w)
+    ef = nf = None
+    if w.edge_dim:
+        ef = np.zeros((w.batch_range(nb_max - 1)[1], w.edge_dim),
+                      np.float32 if w.elem_bytes("edge") == 4 else np.uint16)
+    if w.node_dim:
+        nf = np.zeros((w.num_nodes, w.node_dim), np.float32 if w.elem_bytes("node") == 4 else np.uint16)
+        filled = np.zeros(w.num_nodes, bool)
+    links = queries = 0
+    spent = 0.0
+    b = 0
+    while b < nb_max and spent < budget_s:
+        lo, hi = w.batch_range(b)
+        if whole is None:
+            src, dst, t, neg = synth.host_links(w, lo, hi)
+        else:
+            src, dst, t, neg = (x[lo:hi] for x in whole)
+        q = np.concatenate([src, dst, neg])
+        tq = np.concatenate([t, t, t])
+        if ef is not None:
+            ef[lo:hi] = synth.host_feature_rows(w, "edge", np.arange(lo, hi))
+        if nf is not None:
+            new = np.unique(q)
+            new = new[~filled[new]]
+            if len(new):
+                nf[new] = synth.host_feature_rows(w, "node", new)
+                filled[new] = True
+        t0 = time.perf_counter()
+        o.sample(q, tq, fw, fb, ef, nf)
+        o.insert(src, dst, t)
+        spent += time.perf_counter() - t0
+        links += hi - lo
+        queries += len(q)
+        b += 1
+    return {"value": links / spent, "unit": "links/s", "cores": 1, "kind": "oracle",
+            "queries_per_s": queries / spent, "seconds": spent,
+            "sample": f"first {b} batches ({links} links, {queries} queries) of the same stream, "
+                      f"sample then insert per batch, one thread; early batches see emptier "
+                      f"tables than the GPU's timed window"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (asked for {args.gpus}); "
+              "the tables shard by node, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2402_01964_amd as nlb
+    import synth
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    w = synth.workload(args.workload)
+    K, W = args.steps, args.warmup
+    start = args.start_batch
+    if start is None:
+        start = max(0, min(w.batches // 2, w.batches - K - W))
+    if start + W + K > w.batches:
+        K = max(1, w.batches - start - W)
+
+    t_setup = time.perf_counter()
+    nodes, ts = synth.device_links(w, dev)
+    ef = synth.device_features(w, "edge", dev)
+    nf = synth.device_features(w, "node", dev)
+    fw, fb = synth.time_params(w)
+    tw, tb = torch.from_numpy(fw).to(dev), torch.from_numpy(fb).to(dev)
+    table = nlb.Table(w.num_nodes, w.s, w.alpha, w.table_seed, time_w=tw, time_b=tb,
+                      edge_feat=ef, node_feat=nf)
+    for b in range(start):
+        s_, d_, t_, _, _ = synth.batch_views(w, nodes, ts, b)
+        table.insert(s_, d_, t_)
+    torch.cuda.synchronize()
+    Qmax = 3 * w.batch
+    out = table.alloc_outputs(Qmax, want=("eid", "ts", "tenc", "efeat", "nfeat", "self"))
+    nbr_all = torch.empty((K, Qmax, w.s), dtype=torch.int32, device=dev)
+    setup_s = time.perf_counter() - t_setup
+
+    def step(b, nbr_out):
+        s_, d_, t_, q, tq = synth.batch_views(w, nodes, ts, b)
+        n = q.numel()
+        o = {k: v[:n] for k, v in out.items()}
+        o["nbr"] = nbr_out[:n]
+        table.sample_into(q, tq, o)
+        return s_, d_, t_, n
+
+    for k in range(W):
+        s_, d_, t_, _ = step(start + k, nbr_all[0])
+        table.insert(s_, d_, t_)
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    qcount = []
+    t0 = time.perf_counter()
+    for k in range(K):
+        b = start + W + k
+        ev[k][0].record()
+        s_, d_, t_, n = step(b, nbr_all[k])
+        ev[k][1].record()
+        table.insert(s_, d_, t_)
+        ev[k][2].record()
+        qcount.append(n)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    assert table.status() == nlb.NLB_OK
+
+    sample_ms = np.array([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)])
+    insert_ms = np.array([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)])
+    links = sum(n // 3 for n in qcount)
+    queries = sum(qcount)
+    valid = int(sum(int((nbr_all[k, :qcount[k]] >= 0).sum()) for k in range(K)))
+    s_bytes = sum(sample_bytes(w, 0, n) for n in qcount) + valid * (w.row_bytes("edge") + w.row_bytes("node"))
+    achieved = s_bytes / (sample_ms.sum() * 1e-3) / 1e9
+    full_bytes_per_query = sample_bytes(w, w.s, 1)
+    res = {
+        "metric": "interactions/s ingested + sampled queries/s; achieved HBM GB/s vs peak",
+        "value": links / elapsed,
+        "unit": "links/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": elapsed / K * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64+f32",
+        "data": "synthetic (seeded counter-based stream and features, generated in HBM)",
+        "config": {"workload": w.name, "nodes": w.num_nodes, "links": w.links, "s": w.s,
+                   "alpha": w.alpha, "batch": w.batch, "queries_per_batch": 3 * w.batch,
+                   "d_time": w.d_time, "edge_row_bytes": w.row_bytes("edge"),
+                   "node_row_bytes": w.row_bytes("node"), "start_batch": start,
+                   "timed_batches": [start + W, start + W + K - 1]},
+        "queries_per_s": queries / elapsed,
+        "sample_kernel_queries_per_s": queries / (sample_ms.sum() * 1e-3),
+        "insert_kernel_links_per_s": links / (insert_ms.sum() * 1e-3),
+        "sample_ms_avg": float(sample_ms.mean()),
+        "insert_ms_avg": float(insert_ms.mean()),
+        "valid_slot_fraction": valid / (queries * w.s),
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBPS, "traffic": None,
+                     "kernel": "sample_gather",
+                     "bytes_per_launch": s_bytes / K,
+                     "bytes_per_query_full_occupancy": full_bytes_per_query},
+        "setup_s": setup_s,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

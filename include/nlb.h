@@ -1,0 +1,183 @@
+/*
+ * nlb.h -- C ABI of the MI355X (gfx950) implementation of NLB forward recent
+ * sampling: per-node fixed-size hash tables of down-sampled temporal
+ * neighbours, maintained on the GPU batch by batch, and batched queries that
+ * gather the stored neighbours with their features and a cosine time
+ * encoding.
+ *
+ * Method: Luo & Li, "Scalable and Efficient Temporal Graph Representation
+ * Learning via Forward Recent Sampling", arXiv 2402.01964.
+ *   - Sec. 3, Def. "Temporal network": a time-ordered stream of undirected
+ *     links (u, v, t).  Here link i of the stream gets the 0-based arrival
+ *     index e = i (its "edge id"); later means larger e.
+ *   - Sec. 3, eq. (1): the temporal neighbours of u at time t are links of u
+ *     with timestamp t' < t (strict).
+ *   - Sec. 4.2: table S_u has s slots.  Link (u, v, t) offers (v, t, e) to
+ *     S_u at slot hash(v, t) and (u, t, e) to S_v at slot hash(u, t), with
+ *     hash(v, t) = (q1*v + q2*t) mod s (NLB-edge, eq. (2)) or
+ *     hash(v) = q1*v mod s (NLB-node, eq. (3)).  An empty slot takes the
+ *     offer; an occupied slot is replaced with probability alpha.  Tables are
+ *     updated after the current batch's queries are answered.
+ *   - Sec. 4.4: a query (u, t) retrieves S_u^t: each neighbour's status
+ *     (node feature row), the link's features and the encoded time.
+ *   - App. C: the time encoding is a vector of cosines of w_k * dt + b_k
+ *     (the paper's [cos, sin] pairs are the case b_k in {0, -pi/2}).
+ *
+ * Random draws.  The replacement coin of the offer of link e to its first
+ * endpoint (k = 0, table of src) or second endpoint (k = 1, table of dst) is
+ * the high 32 bits of output number 2e+k+1 of SplitMix64 (Steele, Lea &
+ * Flood, OOPSLA 2014) started from state `seed`.  The offer replaces an
+ * occupied slot iff coin < floor(alpha * 2^32) (always when alpha = 1).  The
+ * result of every call is therefore a deterministic function of the stream,
+ * the parameters and the seed, and equals inserting the links one at a time
+ * in stream order, whatever the batch sizes.
+ *
+ * Conventions for every entry point:
+ *   - Pointers named "device" are HIP device memory on the table's device;
+ *     the library never frees or retains them beyond what is stated.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Calls are asynchronous and ordered on that stream; use one stream (or
+ *     order streams yourself) per table.
+ *   - Return value: NLB_OK or an NLB_E* code.  Argument errors are detected
+ *     on the host before anything is enqueued and leave the table unchanged.
+ *     Errors found by kernels (out-of-range node ids, timestamps >= 2^30 or
+ *     out of order) are recorded on the device and reported by nlb_status.
+ *   - A table is used from one host thread at a time.  Distinct tables are
+ *     independent.  No C++ exception crosses this interface.
+ */
+#ifndef NLB_H
+#define NLB_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define NLB_OK 0
+#define NLB_EINVAL 1   /* bad argument (NULL pointer, size or parameter out of range) */
+#define NLB_ENOMEM 2   /* device allocation failed */
+#define NLB_EDEVICE 3  /* no usable GPU, or a HIP call failed */
+#define NLB_EORDER 4   /* (nlb_status) timestamps decreased, or a timestamp >= 2^30 */
+#define NLB_ERANGE 5   /* node id outside [0, num_nodes), or more than 2^32-1 links */
+
+/* Key choice of Sec. 4.2. */
+#define NLB_KEY_EDGE 0 /* key (neighbour, time): slot by eq. (2) */
+#define NLB_KEY_NODE 1 /* key neighbour: slot by eq. (3) */
+
+#define NLB_MAX_SLOTS 1024
+
+typedef struct nlb_table nlb_table;
+
+typedef struct nlb_config {
+    int64_t num_nodes;      /* N: node ids are 0..N-1; 1 <= N <= 2^31-1 */
+    int32_t s;              /* slots per node, 1..NLB_MAX_SLOTS */
+    int32_t key_mode;       /* NLB_KEY_EDGE or NLB_KEY_NODE */
+    double alpha;           /* replacement probability, 0 < alpha <= 1 */
+    uint64_t seed;          /* start state of the coin generator */
+    uint64_t q1, q2;        /* hash primes of eq. (2)/(3); 0 selects 1000000007 / 998244353;
+                               each must be < 2^31 */
+    int32_t d_time;         /* time-encoding width; 0 = no time encoding */
+    const float *time_w;    /* device fp32[d_time] frequencies, borrowed for the table's life */
+    const float *time_b;    /* device fp32[d_time] phases, borrowed for the table's life */
+    const void *edge_feat;  /* device [edge_rows][edge_row_bytes] link features indexed by
+                               arrival index, borrowed; NULL = none */
+    int64_t edge_rows;      /* rows of edge_feat; a stored link with e >= edge_rows gathers zeros */
+    int32_t edge_row_bytes; /* bytes per link-feature row, a multiple of 4 (0 with NULL) */
+    const void *node_feat;  /* device [num_nodes][node_row_bytes] node rows, borrowed; NULL = none */
+    int32_t node_row_bytes; /* bytes per node row, a multiple of 4 (0 with NULL) */
+    int32_t device;         /* HIP device ordinal that holds the table; -1 = current device */
+} nlb_config;
+
+/* Output buffers of nlb_sample (device pointers, row-major, in slot order).
+ * Any member may be NULL to skip that output.  For query i and slot a:
+ *   nbr  int32 [nq][s]                  stored neighbour id, -1 if not valid
+ *   eid  uint32[nq][s]                  stored arrival index, 0xFFFFFFFF if not valid
+ *   ts   uint32[nq][s]                  stored timestamp t', 0xFFFFFFFF if not valid
+ *   tenc fp32  [nq][s][d_time]          cos(fmaf(w_k, (float)(tq - t'), b_k)), 0 if not valid
+ *   efeat bytes[nq][s][edge_row_bytes]  edge_feat row eid, zero bytes if not valid
+ *   nfeat bytes[nq][s][node_row_bytes]  node_feat row nbr, zero bytes if not valid
+ *   self  bytes[nq][node_row_bytes]     node_feat row of the query node (zeros if the id is
+ *                                       out of range)
+ * A slot is valid when it is non-empty and its timestamp t' < tq (eq. (1)).
+ * tenc is within 1e-5 absolute of the cosine, taken in double, of the fp32
+ * argument fmaf(w_k, (float)(tq - t'), b_k); everything else is exact. */
+typedef struct nlb_sample_out {
+    int32_t *nbr;
+    uint32_t *eid;
+    uint32_t *ts;
+    float *tenc;
+    void *efeat;
+    void *nfeat;
+    void *self;
+} nlb_sample_out;
+
+typedef struct nlb_info {
+    int64_t num_nodes;
+    int32_t s;
+    int32_t key_mode;
+    uint64_t threshold;     /* floor(alpha * 2^32), or 2^32 for alpha == 1 */
+    uint64_t q1, q2;
+    uint64_t interactions;  /* links inserted so far = arrival index of the next link */
+    int64_t table_bytes;    /* device bytes owned by the table */
+    int32_t block_bytes;    /* bytes of one node's slot block */
+    int32_t device;
+} nlb_info;
+
+/* Create an empty table (Sec. 4.2: fixed-size GPU memory of s slots per
+ * node, all empty).  Validates `cfg`, allocates and zeroes the slot blocks on
+ * cfg->device, and stores *out only on success.  Errors: NLB_EINVAL (NULL
+ * argument, parameter out of range, row bytes not a multiple of 4, feature
+ * pointer and row bytes disagreeing), NLB_EDEVICE (no GPU), NLB_ENOMEM. */
+int nlb_create(const nlb_config *cfg, nlb_table **out);
+
+/* Insert the n links (src[i], dst[i], t[i]), i < n, as links
+ * interactions..interactions+n-1 of the stream (Sec. 4.2).  src, dst, t are
+ * device arrays of n elements, read during the call's kernels.  Each link
+ * offers to both endpoint tables; conflicts inside the batch resolve exactly
+ * as sequential insertion would.  Timestamps must be < 2^30 and
+ * non-decreasing across calls; node ids must be in [0, N).  Links with an
+ * out-of-range endpoint or timestamp are skipped and flagged for
+ * nlb_status, but still consume their arrival index.  n == 0 is a no-op.
+ * Errors: NLB_EINVAL (NULL table or array with n > 0), NLB_ERANGE (the
+ * arrival index would exceed 2^32-2), NLB_EDEVICE (launch failure). */
+int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst,
+                     const uint32_t *t, uint32_t n, void *stream);
+
+/* Answer nq queries (node[i], tq[i]) from the tables as they stand after the
+ * inserts enqueued before this call (Sec. 4.4 retrieval; eq. (1) strict
+ * mask; App. C time encoding).  node and tq are device arrays of nq
+ * elements; out holds device output pointers as described above and is read
+ * during the call only.  A query node outside [0, N) yields an all-invalid
+ * answer and is flagged for nlb_status.  nq == 0 is a no-op.
+ * Errors: NLB_EINVAL (NULL table, out or array with nq > 0; tenc/efeat/nfeat/
+ * self requested without the matching configuration), NLB_EDEVICE. */
+int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t nq,
+               const nlb_sample_out *out, void *stream);
+
+/* Free the table's device memory after synchronising its device.  NULL is a
+ * no-op.  Borrowed buffers are not touched. */
+int nlb_destroy(nlb_table *h);
+
+/* Sizes and counters of a table (host-side values; no synchronisation). */
+int nlb_get_info(const nlb_table *h, nlb_info *info);
+
+/* Write the canonical table into device arrays of N*s elements, node-major:
+ * nbr (-1 = empty), ts and eid (0xFFFFFFFF = empty).  Ordered on `stream`.
+ * For inspection and tests; the layout the kernels use is internal. */
+int nlb_export(nlb_table *h, int32_t *nbr, uint32_t *ts, uint32_t *eid, void *stream);
+
+/* Synchronise `stream`, then return and clear the errors kernels recorded
+ * since the last call: NLB_OK, NLB_ERANGE (node id out of range) or
+ * NLB_EORDER (timestamp >= 2^30 or decreasing); NLB_ERANGE wins when both. */
+int nlb_status(nlb_table *h, void *stream);
+
+/* Static description of a return code. */
+const char *nlb_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NLB_H */

@@ -1,0 +1,697 @@
+// nlb.hip -- gfx950 kernels and the C ABI (include/nlb.h) of NLB forward
+// recent sampling (Luo & Li, arXiv 2402.01964, Sec. 4.2 and Sec. 4.4).
+//
+// Table layout in HBM.  Node n owns one block of `block_bytes` bytes at
+// blocks + n * block_bytes: s 64-bit keys, then s 32-bit neighbour ids.
+// block_bytes is the smallest of 16, 32, 64, 128, 256, 384, ... that holds
+// 12*s bytes, so a block of s <= 10 sits in one 128-byte cache line and a
+// query reads its whole table with one line fetch.
+//
+// Key word (0 = empty slot):
+//   bits 63..62  class: 3 = offer whose coin passed, 1 = offer whose coin failed
+//   bits 61..30  arrival index e (class 3) or its complement ~e (class 1)
+//   bits 29..0   timestamp t (< 2^30)
+// Batch insertion must equal sequential insertion.  Sequentially, a slot
+// ends the batch holding the latest offer whose coin passed; if none passed,
+// it keeps its old entry, or, when it was empty, the first offer of the
+// batch (an empty slot always accepts).  With the encoding above this is a
+// plain unsigned maximum over the old word and all offer words: any passed
+// offer beats every class-1 word and older passed entries (larger e wins);
+// a failed offer can only win against an empty word, and among failed
+// offers the smallest e wins (largest ~e).  A stored class-1 word keeps
+// losing to later class-1 offers (smaller ~e), so stored words never need
+// rewriting.  Pass 1 (resolve) applies 64-bit atomicMax per offer; pass 2
+// (commit) lets the offer whose word survived write the neighbour id.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+
+#include "../../include/nlb.h"
+
+namespace {
+
+constexpr uint64_t kClassPass = 3ull << 62;
+constexpr uint64_t kClassFail = 1ull << 62;
+constexpr uint32_t kTimeBits = 30;
+constexpr uint32_t kTimeMask = (1u << kTimeBits) - 1u;
+constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;  // SplitMix64 state increment
+
+// Device status words, kept after the slot blocks.
+constexpr uint32_t kStatusRange = 1u;   // node id out of range
+constexpr uint32_t kStatusOrder = 2u;   // timestamp >= 2^30 or decreasing
+constexpr size_t kStatusBytes = 256;    // [0] flags, [1..2] last timestamp per batch parity
+
+constexpr int kWave = 64;
+constexpr int kSampleWaves = 4;         // queries per 256-thread workgroup
+constexpr int kInsertThreads = 256;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// ---------------------------------------------------------------- integer helpers
+// x mod d for 32-bit x and d, by Lemire, Kaser & Kurz, "Faster remainder by
+// direct computation" (2019): M = 2^64 / d + 1.
+__device__ __forceinline__ uint32_t fastmod_u32(uint32_t x, uint64_t M, uint32_t d) {
+    uint64_t low = M * x;
+    return (uint32_t)__umul64hi(low, d);
+}
+
+// floor(f / d) for f < 2^24, d < 2^16, with m = ceil(2^40 / d).
+__device__ __forceinline__ uint32_t div_small(uint32_t f, uint64_t m) {
+    return (uint32_t)(((uint64_t)f * m) >> 40);
+}
+
+// Output number n (n >= 1) of SplitMix64 started at `state0`; its mixing
+// function is the one published by Steele, Lea & Flood (OOPSLA 2014).
+__device__ __forceinline__ uint64_t splitmix64_nth(uint64_t state0, uint64_t n) {
+    uint64_t z = state0 + n * kGolden;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// ---------------------------------------------------------------- cosine
+// cos of an fp32 argument within ~5e-7 absolute.  For |x| < 2^30 the
+// argument is reduced by pi/2 in double with a two-constant Cody-Waite step
+// (Cody & Waite, "Software Manual for the Elementary Functions", 1980) whose
+// products are exact inside fused multiply-adds, leaving r accurate to
+// ~1e-16; cos(r) and sin(r) on [-pi/4, pi/4] are their Taylor polynomials
+// through r^8 and r^7 (truncation < 3.2e-7).  Larger arguments go to the
+// device libm's double cos, which reduces exactly.
+__device__ __forceinline__ float cos_fp32(float x) {
+    if (fabsf(x) < 1073741824.0f) {
+        const double xd = (double)x;
+        const double kd = __builtin_rint(xd * 0.63661977236758134308);
+        double r = __builtin_fma(-kd, 1.5707963267948965580e+00, xd);
+        r = __builtin_fma(-kd, 6.1232339957367658e-17, r);
+        const int k = (int)kd;
+        const float rf = (float)r;
+        const float z = rf * rf;
+        const float c = __builtin_fmaf(z, __builtin_fmaf(z, __builtin_fmaf(z, __builtin_fmaf(z,
+                            2.4801587301587302e-05f, -1.3888888888888889e-03f),
+                            4.1666666666666664e-02f), -0.5f), 1.0f);
+        const float sn = rf * __builtin_fmaf(z, __builtin_fmaf(z, __builtin_fmaf(z,
+                            -1.9841269841269841e-04f, 8.3333333333333332e-03f),
+                            -1.6666666666666666e-01f), 1.0f);
+        // cos(r + k*pi/2) = cos r, -sin r, -cos r, sin r for k mod 4 = 0..3
+        const float v = (k & 1) ? sn : c;
+        return ((k + 1) & 2) ? -v : v;
+    }
+    return (float)cos((double)x);
+}
+
+// ---------------------------------------------------------------- insert
+struct InsertParams {
+    const int32_t *src;
+    const int32_t *dst;
+    const uint32_t *t;
+    uint32_t n;
+    uint32_t e0;          // arrival index of link 0 of the batch
+    uint8_t *blocks;
+    uint32_t block_bytes;
+    uint32_t s;
+    int64_t num_nodes;
+    uint64_t seed;
+    uint64_t thr;         // replace when coin < thr
+    uint64_t mod_m;       // Lemire constant for mod s
+    uint32_t q1r, q2r;    // q1 mod s, q2 mod s
+    uint32_t key_mode;
+    uint32_t *status;
+    uint32_t parity;      // batch counter & 1
+};
+
+// Slot of neighbour x at time t: eq. (2) (q1*x + q2*t) mod s, or eq. (3)
+// q1*x mod s, evaluated on residues (exact: both products are < s^2).
+__device__ __forceinline__ uint32_t slot_of(const InsertParams &p, uint32_t x, uint32_t t) {
+    const uint32_t xr = fastmod_u32(x, p.mod_m, p.s);
+    uint32_t h = p.q1r * xr;
+    if (p.key_mode == NLB_KEY_EDGE) h += p.q2r * fastmod_u32(t, p.mod_m, p.s);
+    return fastmod_u32(h, p.mod_m, p.s);
+}
+
+__device__ __forceinline__ uint64_t offer_word(const InsertParams &p, uint32_t e, uint32_t k,
+                                               uint32_t t) {
+    const uint32_t coin = (uint32_t)(splitmix64_nth(p.seed, 2ull * e + k + 1) >> 32);
+    return ((uint64_t)coin < p.thr)
+               ? (kClassPass | ((uint64_t)e << kTimeBits) | t)
+               : (kClassFail | ((uint64_t)(~e) << kTimeBits) | t);
+}
+
+__device__ __forceinline__ bool link_ok(const InsertParams &p, int32_t u, int32_t v, uint32_t t) {
+    return u >= 0 && v >= 0 && (int64_t)u < p.num_nodes && (int64_t)v < p.num_nodes &&
+           t <= kTimeMask;
+}
+
+__global__ __launch_bounds__(kInsertThreads) void insert_resolve(InsertParams p) {
+    const uint32_t i = blockIdx.x * kInsertThreads + threadIdx.x;
+    if (i >= p.n) return;
+    const int32_t u = p.src[i];
+    const int32_t v = p.dst[i];
+    const uint32_t t = p.t[i];
+    // Validation: ranges, and timestamps non-decreasing inside the batch and
+    // against the last timestamp of the previous batch.
+    uint32_t flags = 0;
+    if (u < 0 || v < 0 || (int64_t)u >= p.num_nodes || (int64_t)v >= p.num_nodes) flags |= kStatusRange;
+    if (t > kTimeMask) flags |= kStatusOrder;
+    const uint32_t prev_t = (i > 0) ? p.t[i - 1] : p.status[1 + (p.parity ^ 1u)];
+    if (t < prev_t) flags |= kStatusOrder;
+    if (flags) atomicOr(p.status, flags);
+    if (i == p.n - 1) p.status[1 + p.parity] = t;
+    if (!link_ok(p, u, v, t)) return;
+
+    const uint32_t e = p.e0 + i;
+    // Sec. 4.2: S_u receives (v, t, e); S_v receives (u, t, e).
+    const uint32_t au = slot_of(p, (uint32_t)v, t);
+    const uint32_t av = slot_of(p, (uint32_t)u, t);
+    unsigned long long *ku =
+        (unsigned long long *)(p.blocks + (size_t)u * p.block_bytes) + au;
+    unsigned long long *kv =
+        (unsigned long long *)(p.blocks + (size_t)v * p.block_bytes) + av;
+    atomicMax(ku, (unsigned long long)offer_word(p, e, 0, t));
+    atomicMax(kv, (unsigned long long)offer_word(p, e, 1, t));
+}
+
+__global__ __launch_bounds__(kInsertThreads) void insert_commit(InsertParams p) {
+    const uint32_t i = blockIdx.x * kInsertThreads + threadIdx.x;
+    if (i >= p.n) return;
+    const int32_t u = p.src[i];
+    const int32_t v = p.dst[i];
+    const uint32_t t = p.t[i];
+    if (!link_ok(p, u, v, t)) return;
+    const uint32_t e = p.e0 + i;
+    const uint32_t au = slot_of(p, (uint32_t)v, t);
+    const uint32_t av = slot_of(p, (uint32_t)u, t);
+    uint8_t *bu = p.blocks + (size_t)u * p.block_bytes;
+    uint8_t *bv = p.blocks + (size_t)v * p.block_bytes;
+    const uint64_t wu = ((const uint64_t *)bu)[au];
+    const uint64_t wv = ((const uint64_t *)bv)[av];
+    // Exactly one offer owns each surviving word (a self-loop's two offers
+    // may share one; they write the same id).
+    if (wu == offer_word(p, e, 0, t)) ((int32_t *)(bu + 8u * p.s))[au] = v;
+    if (wv == offer_word(p, e, 1, t)) ((int32_t *)(bv + 8u * p.s))[av] = u;
+}
+
+// ---------------------------------------------------------------- sample
+struct SampleParams {
+    const uint8_t *blocks;
+    uint32_t block_bytes;
+    uint32_t s;
+    int64_t num_nodes;
+    const int32_t *node;
+    const uint32_t *tq;
+    uint32_t nq;
+    uint32_t d_time;
+    const float *w;
+    const float *b;
+    const uint8_t *efeat;
+    int64_t edge_rows;
+    uint32_t erb;         // bytes per edge row
+    const uint8_t *nfeat;
+    uint32_t nrb;         // bytes per node row
+    int32_t *o_nbr;
+    uint32_t *o_eid;
+    uint32_t *o_ts;
+    float *o_tenc;
+    uint8_t *o_efeat;
+    uint8_t *o_nfeat;
+    uint8_t *o_self;
+    uint32_t *status;
+    // copy geometry: units per row and ceil(2^40 / units)
+    uint32_t tenc_units, tenc_vec;  // tenc_vec = 4 (float4 stores) or 1
+    uint64_t tenc_m;
+    uint32_t e_units, e_width;
+    uint64_t e_m;
+    uint32_t n_units, n_width;
+    uint64_t n_m;
+};
+
+template <int W> struct VecOf;
+template <> struct VecOf<16> { typedef u32x4 T; };
+template <> struct VecOf<8> { typedef u32x2 T; };
+template <> struct VecOf<4> { typedef uint32_t T; };
+
+// Copy the rows selected by (row_i, ok_i) of the wave's lanes 0..sc-1 into
+// the contiguous output rows out_row0 .. out_row0+sc-1.  Lane L handles
+// units base+L of the flattened [sc][units] range; loads of four rounds are
+// issued before their stores.  Rows with ok == 0 are written as zeros.
+template <int W>
+__device__ __forceinline__ void gather_rows(const uint8_t *__restrict__ src, uint32_t row_bytes,
+                                            uint32_t units, uint64_t m, uint32_t sc,
+                                            int64_t row_i, int ok_i, uint8_t *__restrict__ out,
+                                            uint32_t lane) {
+    typedef typename VecOf<W>::T V;
+    constexpr int R = 4;
+    const uint32_t total = sc * units;
+    for (uint32_t base = 0; base < total; base += kWave * R) {
+        V val[R];
+        uint32_t fi[R];
+#pragma unroll
+        for (int r = 0; r < R; r++) {
+            const uint32_t f = base + r * kWave + lane;
+            const bool act = f < total;
+            const uint32_t j = act ? div_small(f, m) : 0u;
+            const int64_t row = __shfl(row_i, (int)j, kWave);
+            const int ok = __shfl(ok_i, (int)j, kWave);
+            fi[r] = f;
+            val[r] = V(0);
+            if (act && ok) {
+                const uint32_t c = f - j * units;
+                val[r] = *(const V *)(src + (size_t)row * row_bytes + (size_t)c * W);
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < R; r++) {
+            if (fi[r] < total) {
+                __builtin_nontemporal_store(val[r], (V *)(out + (size_t)fi[r] * W));
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void gather_rows_w(uint32_t width, const uint8_t *src,
+                                              uint32_t row_bytes, uint32_t units, uint64_t m,
+                                              uint32_t sc, int64_t row_i, int ok_i, uint8_t *out,
+                                              uint32_t lane) {
+    if (width == 16)
+        gather_rows<16>(src, row_bytes, units, m, sc, row_i, ok_i, out, lane);
+    else if (width == 8)
+        gather_rows<8>(src, row_bytes, units, m, sc, row_i, ok_i, out, lane);
+    else
+        gather_rows<4>(src, row_bytes, units, m, sc, row_i, ok_i, out, lane);
+}
+
+// One wavefront answers one query; four queries per workgroup.
+__global__ __launch_bounds__(kWave * kSampleWaves) void sample_gather(SampleParams p) {
+    const uint32_t lane = threadIdx.x & (kWave - 1);
+    const uint64_t q = (uint64_t)blockIdx.x * kSampleWaves + (threadIdx.x / kWave);
+    if (q >= p.nq) return;  // uniform across the wave
+    const int32_t node = p.node[q];
+    const uint32_t tq = p.tq[q];
+    const bool in_range = node >= 0 && (int64_t)node < p.num_nodes;
+    if (!in_range && lane == 0) atomicOr(p.status, kStatusRange);
+    const uint8_t *blk = p.blocks + (size_t)(in_range ? node : 0) * p.block_bytes;
+    const uint64_t *keys = (const uint64_t *)blk;
+    const int32_t *nbrs = (const int32_t *)(blk + 8u * p.s);
+
+    for (uint32_t c0 = 0; c0 < p.s; c0 += kWave) {
+        const uint32_t sc = min((uint32_t)kWave, p.s - c0);
+        // Lane j < sc owns slot c0 + j.
+        int valid = 0;
+        int32_t x = -1;
+        uint32_t e = 0xFFFFFFFFu, ts = 0xFFFFFFFFu;
+        float dt = 0.0f;
+        if (lane < sc && in_range) {
+            const uint64_t key = keys[c0 + lane];
+            const int32_t xv = nbrs[c0 + lane];  // same cache line; issued with the key
+            if (key != 0) {
+                const uint32_t t = (uint32_t)key & kTimeMask;
+                if (t < tq) {  // eq. (1): strictly earlier links only
+                    const uint32_t ef = (uint32_t)(key >> kTimeBits);
+                    valid = 1;
+                    e = ((key >> 62) == 3u) ? ef : ~ef;
+                    ts = t;
+                    x = xv;
+                    dt = (float)(tq - t);
+                }
+            }
+        }
+        const size_t row0 = (size_t)q * p.s + c0;  // first output row of this chunk
+        if (lane < sc) {
+            if (p.o_nbr) p.o_nbr[row0 + lane] = x;
+            if (p.o_eid) p.o_eid[row0 + lane] = e;
+            if (p.o_ts) p.o_ts[row0 + lane] = ts;
+        }
+
+        if (p.o_tenc) {
+            // T-encoding (App. C): cos(w_k * dt + b_k) with the argument
+            // formed by one fp32 fused multiply-add.
+            const uint32_t units = p.tenc_units;
+            const uint32_t total = sc * units;
+            float *out = p.o_tenc + row0 * p.d_time;
+            for (uint32_t base = 0; base < total; base += kWave) {
+                const uint32_t f = base + lane;
+                const bool act = f < total;
+                const uint32_t j = act ? div_small(f, p.tenc_m) : 0u;
+                const int ok = __shfl(valid, (int)j, kWave);
+                const float g = __shfl(dt, (int)j, kWave);
+                if (!act) continue;
+                const uint32_t c = f - j * units;
+                if (p.tenc_vec == 4) {
+                    f32x4 r = f32x4(0.0f);
+                    if (ok) {
+                        const f32x4 w4 = *(const f32x4 *)(p.w + 4 * c);
+                        const f32x4 b4 = *(const f32x4 *)(p.b + 4 * c);
+                        r.x = cos_fp32(__builtin_fmaf(w4.x, g, b4.x));
+                        r.y = cos_fp32(__builtin_fmaf(w4.y, g, b4.y));
+                        r.z = cos_fp32(__builtin_fmaf(w4.z, g, b4.z));
+                        r.w = cos_fp32(__builtin_fmaf(w4.w, g, b4.w));
+                    }
+                    __builtin_nontemporal_store(r, (f32x4 *)(out + (size_t)f * 4));
+                } else {
+                    float r = 0.0f;
+                    if (ok) r = cos_fp32(__builtin_fmaf(p.w[c], g, p.b[c]));
+                    __builtin_nontemporal_store(r, out + f);
+                }
+            }
+        }
+        if (p.o_efeat) {
+            const int ok = valid && (int64_t)e < p.edge_rows;
+            gather_rows_w(p.e_width, p.efeat, p.erb, p.e_units, p.e_m, sc, (int64_t)e, ok,
+                          p.o_efeat + row0 * p.erb, lane);
+        }
+        if (p.o_nfeat) {
+            gather_rows_w(p.n_width, p.nfeat, p.nrb, p.n_units, p.n_m, sc, (int64_t)x, valid,
+                          p.o_nfeat + row0 * p.nrb, lane);
+        }
+    }
+    if (p.o_self) {
+        gather_rows_w(p.n_width, p.nfeat, p.nrb, p.n_units, p.n_m, 1, (int64_t)node,
+                      in_range ? 1 : 0, p.o_self + (size_t)q * p.nrb, lane);
+    }
+}
+
+// ---------------------------------------------------------------- export
+__global__ __launch_bounds__(256) void export_table(const uint8_t *blocks, uint32_t block_bytes,
+                                                    uint32_t s, int64_t num_nodes, int32_t *nbr,
+                                                    uint32_t *ts, uint32_t *eid) {
+    const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (n >= num_nodes) return;
+    const uint8_t *blk = blocks + (size_t)n * block_bytes;
+    const uint64_t *keys = (const uint64_t *)blk;
+    const int32_t *nb = (const int32_t *)(blk + 8u * s);
+    for (uint32_t a = 0; a < s; a++) {
+        const uint64_t key = keys[a];
+        const size_t o = (size_t)n * s + a;
+        if (key == 0) {
+            nbr[o] = -1;
+            ts[o] = 0xFFFFFFFFu;
+            eid[o] = 0xFFFFFFFFu;
+        } else {
+            const uint32_t ef = (uint32_t)(key >> kTimeBits);
+            nbr[o] = nb[a];
+            ts[o] = (uint32_t)key & kTimeMask;
+            eid[o] = ((key >> 62) == 3u) ? ef : ~ef;
+        }
+    }
+}
+
+// ---------------------------------------------------------------- host side
+uint32_t block_bytes_for(uint32_t s) {
+    const uint32_t need = 12u * s;
+    if (need <= 128) {
+        uint32_t b = 16;
+        while (b < need) b *= 2;
+        return b;
+    }
+    return (need + 127u) / 128u * 128u;
+}
+
+uint64_t ceil_2_40_div(uint32_t d) { return ((1ull << 40) + d - 1) / d; }
+
+class DeviceGuard {
+  public:
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev_) != hipSuccess) prev_ = -1;
+        ok_ = hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard() {
+        if (prev_ >= 0) (void)hipSetDevice(prev_);
+    }
+    bool ok() const { return ok_; }
+
+  private:
+    int prev_ = -1;
+    bool ok_ = false;
+};
+
+// Widest copy unit (16, 8 or 4 bytes) that divides the row and keeps every
+// source and destination address aligned.
+uint32_t copy_width(uint32_t row_bytes, const void *src, const void *dst_or_null) {
+    const uintptr_t a = (uintptr_t)src | (uintptr_t)dst_or_null;
+    for (uint32_t w = 16; w >= 8; w /= 2)
+        if (row_bytes % w == 0 && a % w == 0) return w;
+    return 4;
+}
+
+}  // namespace
+
+struct nlb_table {
+    int device;
+    int64_t num_nodes;
+    uint32_t s;
+    int32_t key_mode;
+    double alpha;
+    uint64_t thr;
+    uint64_t seed;
+    uint64_t q1, q2;
+    uint32_t d_time;
+    const float *w;
+    const float *b;
+    const uint8_t *efeat;
+    int64_t edge_rows;
+    uint32_t erb;
+    const uint8_t *nfeat;
+    uint32_t nrb;
+    uint8_t *blocks;
+    size_t table_bytes;
+    uint32_t block_bytes;
+    uint32_t *status;
+    uint64_t interactions;
+    uint64_t batches;
+};
+
+extern "C" {
+
+const char *nlb_strerror(int code) {
+    switch (code) {
+        case NLB_OK: return "success";
+        case NLB_EINVAL: return "invalid argument";
+        case NLB_ENOMEM: return "out of device memory";
+        case NLB_EDEVICE: return "no usable GPU or HIP failure";
+        case NLB_EORDER: return "timestamp out of order or >= 2^30";
+        case NLB_ERANGE: return "node id or arrival index out of range";
+        default: return "unknown error";
+    }
+}
+
+int nlb_create(const nlb_config *cfg, nlb_table **out) {
+    if (!cfg || !out) return NLB_EINVAL;
+    if (cfg->num_nodes < 1 || cfg->num_nodes > INT32_MAX) return NLB_EINVAL;
+    if (cfg->s < 1 || cfg->s > NLB_MAX_SLOTS) return NLB_EINVAL;
+    if (cfg->key_mode != NLB_KEY_EDGE && cfg->key_mode != NLB_KEY_NODE) return NLB_EINVAL;
+    if (!(cfg->alpha > 0.0 && cfg->alpha <= 1.0)) return NLB_EINVAL;
+    const uint64_t q1 = cfg->q1 ? cfg->q1 : 1000000007ull;
+    const uint64_t q2 = cfg->q2 ? cfg->q2 : 998244353ull;
+    if (q1 >= (1ull << 31) || q2 >= (1ull << 31)) return NLB_EINVAL;
+    if (cfg->d_time < 0 || cfg->d_time > 65535) return NLB_EINVAL;
+    if (cfg->d_time > 0 && (!cfg->time_w || !cfg->time_b)) return NLB_EINVAL;
+    const bool has_e = cfg->edge_feat != nullptr;
+    const bool has_n = cfg->node_feat != nullptr;
+    if (has_e != (cfg->edge_row_bytes > 0) || has_n != (cfg->node_row_bytes > 0)) return NLB_EINVAL;
+    if (cfg->edge_row_bytes < 0 || cfg->node_row_bytes < 0) return NLB_EINVAL;
+    if (cfg->edge_row_bytes % 4 || cfg->node_row_bytes % 4) return NLB_EINVAL;
+    if (cfg->edge_row_bytes > (1 << 18) || cfg->node_row_bytes > (1 << 18)) return NLB_EINVAL;
+    if (has_e && cfg->edge_rows < 1) return NLB_EINVAL;
+    if ((uintptr_t)cfg->edge_feat % 4 || (uintptr_t)cfg->node_feat % 4) return NLB_EINVAL;
+
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return NLB_EDEVICE;
+    int dev = cfg->device;
+    if (dev < 0 && hipGetDevice(&dev) != hipSuccess) return NLB_EDEVICE;
+    if (dev >= ndev) return NLB_EINVAL;
+    DeviceGuard guard(dev);
+    if (!guard.ok()) return NLB_EDEVICE;
+
+    nlb_table *h = new (std::nothrow) nlb_table();
+    if (!h) return NLB_ENOMEM;
+    h->device = dev;
+    h->num_nodes = cfg->num_nodes;
+    h->s = (uint32_t)cfg->s;
+    h->key_mode = cfg->key_mode;
+    h->alpha = cfg->alpha;
+    h->thr = (cfg->alpha >= 1.0) ? (1ull << 32) : (uint64_t)std::floor(cfg->alpha * 4294967296.0);
+    h->seed = cfg->seed;
+    h->q1 = q1;
+    h->q2 = q2;
+    h->d_time = (uint32_t)cfg->d_time;
+    h->w = cfg->time_w;
+    h->b = cfg->time_b;
+    h->efeat = (const uint8_t *)cfg->edge_feat;
+    h->edge_rows = has_e ? cfg->edge_rows : 0;
+    h->erb = (uint32_t)cfg->edge_row_bytes;
+    h->nfeat = (const uint8_t *)cfg->node_feat;
+    h->nrb = (uint32_t)cfg->node_row_bytes;
+    h->block_bytes = block_bytes_for(h->s);
+    const size_t blocks_bytes = (size_t)h->num_nodes * h->block_bytes;
+    h->table_bytes = blocks_bytes + kStatusBytes;
+    if (hipMalloc((void **)&h->blocks, h->table_bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        delete h;
+        return NLB_ENOMEM;
+    }
+    if (hipMemset(h->blocks, 0, h->table_bytes) != hipSuccess) {
+        (void)hipFree(h->blocks);
+        delete h;
+        return NLB_EDEVICE;
+    }
+    h->status = (uint32_t *)(h->blocks + blocks_bytes);
+    *out = h;
+    return NLB_OK;
+}
+
+int nlb_destroy(nlb_table *h) {
+    if (!h) return NLB_OK;
+    int rc = NLB_OK;
+    {
+        DeviceGuard guard(h->device);
+        if (hipDeviceSynchronize() != hipSuccess) rc = NLB_EDEVICE;
+        if (hipFree(h->blocks) != hipSuccess) rc = NLB_EDEVICE;
+    }
+    delete h;
+    return rc;
+}
+
+int nlb_get_info(const nlb_table *h, nlb_info *info) {
+    if (!h || !info) return NLB_EINVAL;
+    info->num_nodes = h->num_nodes;
+    info->s = (int32_t)h->s;
+    info->key_mode = h->key_mode;
+    info->threshold = h->thr;
+    info->q1 = h->q1;
+    info->q2 = h->q2;
+    info->interactions = h->interactions;
+    info->table_bytes = (int64_t)h->table_bytes;
+    info->block_bytes = (int32_t)h->block_bytes;
+    info->device = h->device;
+    return NLB_OK;
+}
+
+int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const uint32_t *t,
+                     uint32_t n, void *stream) {
+    if (!h) return NLB_EINVAL;
+    if (n == 0) return NLB_OK;
+    if (!src || !dst || !t) return NLB_EINVAL;
+    if (h->interactions + n > 0xFFFFFFFFull) return NLB_ERANGE;
+    DeviceGuard guard(h->device);
+    if (!guard.ok()) return NLB_EDEVICE;
+    InsertParams p;
+    p.src = src;
+    p.dst = dst;
+    p.t = t;
+    p.n = n;
+    p.e0 = (uint32_t)h->interactions;
+    p.blocks = h->blocks;
+    p.block_bytes = h->block_bytes;
+    p.s = h->s;
+    p.num_nodes = h->num_nodes;
+    p.seed = h->seed;
+    p.thr = h->thr;
+    p.mod_m = UINT64_MAX / h->s + 1;
+    p.q1r = (uint32_t)(h->q1 % h->s);
+    p.q2r = (uint32_t)(h->q2 % h->s);
+    p.key_mode = (uint32_t)h->key_mode;
+    p.status = h->status;
+    p.parity = (uint32_t)(h->batches & 1);
+    const hipStream_t st = (hipStream_t)stream;
+    const dim3 grid((n + kInsertThreads - 1) / kInsertThreads);
+    hipLaunchKernelGGL(insert_resolve, grid, dim3(kInsertThreads), 0, st, p);
+    hipLaunchKernelGGL(insert_commit, grid, dim3(kInsertThreads), 0, st, p);
+    if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
+    h->interactions += n;
+    h->batches += 1;
+    return NLB_OK;
+}
+
+int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t nq,
+               const nlb_sample_out *out, void *stream) {
+    if (!h || !out) return NLB_EINVAL;
+    if (nq == 0) return NLB_OK;
+    if (!node || !tq) return NLB_EINVAL;
+    if (out->tenc && h->d_time == 0) return NLB_EINVAL;
+    if (out->efeat && !h->efeat) return NLB_EINVAL;
+    if ((out->nfeat || out->self) && !h->nfeat) return NLB_EINVAL;
+    if ((uintptr_t)out->nbr % 4 || (uintptr_t)out->eid % 4 || (uintptr_t)out->ts % 4 ||
+        (uintptr_t)out->tenc % 4 || (uintptr_t)out->efeat % 4 || (uintptr_t)out->nfeat % 4 ||
+        (uintptr_t)out->self % 4)
+        return NLB_EINVAL;
+    DeviceGuard guard(h->device);
+    if (!guard.ok()) return NLB_EDEVICE;
+    SampleParams p;
+    p.blocks = h->blocks;
+    p.block_bytes = h->block_bytes;
+    p.s = h->s;
+    p.num_nodes = h->num_nodes;
+    p.node = node;
+    p.tq = tq;
+    p.nq = nq;
+    p.d_time = h->d_time;
+    p.w = h->w;
+    p.b = h->b;
+    p.efeat = h->efeat;
+    p.edge_rows = h->edge_rows;
+    p.erb = h->erb;
+    p.nfeat = h->nfeat;
+    p.nrb = h->nrb;
+    p.o_nbr = out->nbr;
+    p.o_eid = out->eid;
+    p.o_ts = out->ts;
+    p.o_tenc = out->tenc;
+    p.o_efeat = (uint8_t *)out->efeat;
+    p.o_nfeat = (uint8_t *)out->nfeat;
+    p.o_self = (uint8_t *)out->self;
+    p.status = h->status;
+    const bool vec4 = h->d_time % 4 == 0 && (uintptr_t)out->tenc % 16 == 0 &&
+                      (uintptr_t)h->w % 16 == 0 && (uintptr_t)h->b % 16 == 0;
+    p.tenc_vec = vec4 ? 4 : 1;
+    p.tenc_units = h->d_time ? (vec4 ? h->d_time / 4 : h->d_time) : 1;
+    p.tenc_m = ceil_2_40_div(p.tenc_units);
+    p.e_width = h->erb ? copy_width(h->erb, h->efeat, out->efeat) : 4;
+    p.e_units = h->erb ? h->erb / p.e_width : 1;
+    p.e_m = ceil_2_40_div(p.e_units);
+    // the same width serves the neighbour rows and the self row
+    const uintptr_t nalign = (uintptr_t)out->nfeat | (uintptr_t)out->self;
+    p.n_width = h->nrb ? copy_width(h->nrb, h->nfeat, (const void *)nalign) : 4;
+    p.n_units = h->nrb ? h->nrb / p.n_width : 1;
+    p.n_m = ceil_2_40_div(p.n_units);
+    const hipStream_t st = (hipStream_t)stream;
+    const dim3 grid((nq + kSampleWaves - 1) / kSampleWaves);
+    hipLaunchKernelGGL(sample_gather, grid, dim3(kWave * kSampleWaves), 0, st, p);
+    if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
+    return NLB_OK;
+}
+
+int nlb_export(nlb_table *h, int32_t *nbr, uint32_t *ts, uint32_t *eid, void *stream) {
+    if (!h || !nbr || !ts || !eid) return NLB_EINVAL;
+    DeviceGuard guard(h->device);
+    if (!guard.ok()) return NLB_EDEVICE;
+    const dim3 grid((unsigned)((h->num_nodes + 255) / 256));
+    hipLaunchKernelGGL(export_table, grid, dim3(256), 0, (hipStream_t)stream, h->blocks,
+                       h->block_bytes, h->s, h->num_nodes, nbr, ts, eid);
+    if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
+    return NLB_OK;
+}
+
+int nlb_status(nlb_table *h, void *stream) {
+    if (!h) return NLB_EINVAL;
+    DeviceGuard guard(h->device);
+    if (!guard.ok()) return NLB_EDEVICE;
+    if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return NLB_EDEVICE;
+    uint32_t flags = 0;
+    if (hipMemcpy(&flags, h->status, sizeof(flags), hipMemcpyDeviceToHost) != hipSuccess)
+        return NLB_EDEVICE;
+    if (flags) {
+        const uint32_t zero = 0;
+        if (hipMemcpy(h->status, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess)
+            return NLB_EDEVICE;
+    }
+    if (flags & kStatusRange) return NLB_ERANGE;
+    if (flags & kStatusOrder) return NLB_EORDER;
+    return NLB_OK;
+}
+
+}  // extern "C"

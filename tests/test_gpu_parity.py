@@ -1,0 +1,280 @@
+"""GPU library vs CPU oracle, element by element, on seeded workloads.
+
+Indices, timestamps, arrival indices and feature rows must be bit-exact;
+the fp32 time encoding must be within 1e-5 absolute.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_helpers import (compare_sample, compare_tables, feat_to_dev, make_gpu_table,
+                               make_oracle, to_dev, u32)
+
+pytestmark = pytest.mark.gpu
+
+ALL = ("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self")
+
+
+def _run_stream(w, full_batches, index_batches="all", check_every=None):
+    """Drive GPU and oracle over workload w; compare the sample outputs of
+    `full_batches` fully, the indices of `index_batches`, and the tables at
+    the end (and every `check_every` batches)."""
+    import torch
+    src, dst, t, neg = synth.host_links(w)
+    nodes, ts = synth.blocked(w, src, dst, t, neg)
+    nodes_d, ts_d = to_dev(nodes), to_dev(ts)
+    ef = synth.host_features(w, "edge") if w.edge_dim else None
+    nf = synth.host_features(w, "node") if w.node_dim else None
+    ef_d = feat_to_dev(ef, w.edge_dtype) if ef is not None else None
+    nf_d = feat_to_dev(nf, w.node_dtype) if nf is not None else None
+    g = make_gpu_table(w, ef_d, nf_d)
+    o = make_oracle(w)
+    fw, fb = synth.time_params(w)
+    full = set(full_batches)
+    checked = 0
+    for b in range(w.batches):
+        s_, d_, t_, q, tq = synth.batch_views(w, nodes_d, ts_d, b)
+        lo, hi = w.batch_range(b)
+        qh = np.concatenate([src[lo:hi], dst[lo:hi], neg[lo:hi]])
+        tqh = np.concatenate([t[lo:hi]] * 3)
+        if b in full:
+            gout = g.sample(q, tq)
+            oout = o.sample(qh, tqh, fw, fb, ef, nf)
+            compare_sample(gout, oout, f"batch {b}")
+            checked += 1
+        elif index_batches == "all" or b in index_batches:
+            gout = g.sample(q, tq, want=("nbr", "eid", "ts"))
+            oout = o.sample(qh, tqh, want=("nbr", "eid", "ts"))
+            compare_sample(gout, oout, f"batch {b}")
+        g.insert(s_, d_, t_)
+        o.insert(src[lo:hi], dst[lo:hi], t[lo:hi])
+        if check_every and (b + 1) % check_every == 0:
+            compare_tables(g, o)
+    torch.cuda.synchronize()
+    assert g.status() == 0
+    compare_tables(g, o)
+    assert g.info()["interactions"] == w.links
+    return checked
+
+
+def test_tiny_bipartite_full_stream():
+    """Workload 1 at full size: every batch's outputs and the final table."""
+    w = synth.workload(1)
+    assert _run_stream(w, full_batches=range(w.batches), check_every=25) == w.batches
+
+
+def test_small_bipartite_full_stream():
+    """Workload 2 at full size: indices of every batch, all outputs on a
+    subset of batches (first 5, every 97th, last 5), tables at checkpoints."""
+    w = synth.workload(2)
+    nb = w.batches
+    full = set(range(5)) | set(range(0, nb, 97)) | set(range(nb - 5, nb))
+    _run_stream(w, full_batches=full, check_every=300)
+
+
+def test_medium_homogeneous_prefix():
+    """Workload 3 shape (s=64, alpha=0.3, bf16 edge+node rows) on its first
+    120 batches: tables at checkpoints and full outputs of some batches."""
+    w = synth.scaled(synth.workload(3), 120 * 4000)
+    _run_stream(w, full_batches={0, 1, 50, 119}, index_batches={10, 60, 100}, check_every=40)
+
+
+def test_dense_repeated_prefix():
+    """Workload 4 shape (bf16 186-dim edge rows = 372 B, 4-byte copy path)."""
+    w = synth.scaled(synth.workload(4), 60 * 10000)
+    _run_stream(w, full_batches={0, 30, 59}, index_batches={10, 20, 40, 50}, check_every=20)
+
+
+# ----------------------------------------------------------------------------- invariance
+def _insert_in_batches(w, src, dst, t, B, **kw):
+    g = make_gpu_table(w, time=False, **kw)
+    sd, dd, td = to_dev(src), to_dev(dst), to_dev(t)
+    for lo in range(0, len(src), B):
+        g.insert(sd[lo:lo + B], dd[lo:lo + B], td[lo:lo + B])
+    return g
+
+
+def test_batch_size_invariance_and_determinism():
+    """The table equals sequential insertion for any batch size, and repeated
+    runs give identical tables."""
+    import torch
+    w = synth.workload(2)
+    src, dst, t, _ = synth.host_links(w)
+    n = 60000
+    src, dst, t = src[:n], dst[:n], t[:n]
+    o = make_oracle(w)
+    o.insert(src, dst, t)
+    ref = None
+    for B in (1, 7, 600, 2400, n):
+        m = 3000 if B == 1 else n
+        g = _insert_in_batches(w, src[:m], dst[:m], t[:m], B)
+        if B == 1:
+            o1 = make_oracle(w)
+            o1.insert(src[:m], dst[:m], t[:m])
+            compare_tables(g, o1)
+            continue
+        compare_tables(g, o)
+        cur = [x.cpu() for x in g.export()]
+        if ref is not None:
+            assert all(torch.equal(a, b) for a, b in zip(cur, ref))
+        ref = cur
+
+
+@pytest.mark.parametrize("alpha", [1.0, 1e-12, 0.3, 0.9])
+def test_alpha_extremes(alpha):
+    import dataclasses
+    w = dataclasses.replace(synth.scaled(synth.workload(2), 30000), alpha=alpha)
+    src, dst, t, _ = synth.host_links(dataclasses.replace(w, repeat=0.0))
+    g = _insert_in_batches(w, src, dst, t, 600)
+    o = make_oracle(w)
+    o.insert(src, dst, t)
+    compare_tables(g, o)
+
+
+def test_single_hot_slot_batch():
+    """Every offer of a batch lands on the same slot of one hub table (all
+    links share the hub, the timestamp and a neighbour residue), plus
+    self-loops, ties and a ragged batch."""
+    N, s = 5000, 10
+    import dataclasses
+    w = dataclasses.replace(synth.workload(1), num_nodes=N, s=s)
+    rng = np.random.default_rng(3)
+    # neighbours congruent mod s, same t: eq. (2) gives one slot for all
+    nb = (rng.integers(1, N // s, 20000) * s).astype(np.int32)
+    src = np.zeros_like(nb)
+    t = np.full(len(nb), 777, np.uint32)
+    # self-loops and a second hub with ties
+    src[::97] = nb[::97]
+    t = np.sort(np.concatenate([t[:10000], np.full(10000, 778, np.uint32)]))
+    for B in (20000, 4096, 333):
+        g = _insert_in_batches(w, src, nb, t, B)
+        o = make_oracle(w)
+        o.insert(src, nb, t)
+        compare_tables(g, o)
+
+
+@pytest.mark.parametrize("key_mode", [0, 1])
+@pytest.mark.parametrize("s", [1, 3, 64, 100, 1024])
+def test_slot_counts_and_key_modes(s, key_mode):
+    """Table sizes across the layout classes (16-byte blocks up to multi-line
+    blocks and more than 64 slots per query) and both key choices."""
+    import dataclasses
+    w = dataclasses.replace(synth.scaled(synth.workload(3), 40000, num_nodes=3000), s=s,
+                            bursty=False, T=200000)
+    src, dst, t, neg = synth.host_links(w)
+    nf = synth.host_features(w, "node")
+    nf_d = feat_to_dev(nf, w.node_dtype)
+    g = make_gpu_table(w, None, nf_d, key_mode=key_mode)
+    o = make_oracle(w, key_mode=key_mode)
+    sd, dd, td = to_dev(src), to_dev(dst), to_dev(t)
+    fw, fb = synth.time_params(w)
+    nq = max(16, 20000 // s)   # keeps the oracle's cosine count bounded
+    for lo in range(0, len(src), 8000):
+        hi = lo + 8000
+        q = np.concatenate([src[lo:lo + nq], neg[lo:lo + nq]])
+        tq = np.concatenate([t[lo:lo + nq], t[lo:lo + nq] + 5])
+        gout = g.sample(to_dev(q), to_dev(tq), want=("nbr", "eid", "ts", "tenc", "nfeat", "self"))
+        oout = o.sample(q, tq, fw, fb, None, nf)
+        compare_sample(gout, oout, f"s={s} lo={lo}")
+        g.insert(sd[lo:hi], dd[lo:hi], td[lo:hi])
+        o.insert(src[lo:hi], dst[lo:hi], t[lo:hi])
+    compare_tables(g, o)
+
+
+# ----------------------------------------------------------------------------- edge cases
+def test_query_time_bounds_and_strictness():
+    """tq = 0 sees nothing; tq = 2^32-1 sees every stored entry; entries at
+    t' = tq are hidden (eq. (1) is strict)."""
+    w = synth.scaled(synth.workload(1), 5000)
+    src, dst, t, _ = synth.host_links(w)
+    g = _insert_in_batches(w, src, dst, t, 200)
+    o = make_oracle(w)
+    o.insert(src, dst, t)
+    nodes = np.arange(w.num_nodes, dtype=np.int32)
+    nbr_o, ts_o, eid_o = o.export()
+    for tq_val in (0, 2**32 - 1):
+        tq = np.full(len(nodes), tq_val, np.uint32)
+        gout = g.sample(to_dev(nodes), to_dev(tq), want=("nbr", "eid", "ts"))
+        oout = o.sample(nodes, tq, want=("nbr", "eid", "ts"))
+        compare_sample(gout, oout)
+    assert (g.sample(to_dev(nodes), to_dev(np.full(len(nodes), 2**32 - 1, np.uint32)),
+                     want=("nbr",))["nbr"].cpu().numpy() == nbr_o).all()
+    # query each node at the timestamp of its first stored entry
+    first_t = np.where(nbr_o[:, 0] >= 0, ts_o[:, 0], 0).astype(np.uint32)
+    gout = g.sample(to_dev(nodes), to_dev(first_t), want=("nbr", "eid", "ts"))
+    oout = o.sample(nodes, first_t, want=("nbr", "eid", "ts"))
+    compare_sample(gout, oout)
+    assert (gout["nbr"].cpu().numpy()[:, 0] == -1).all()
+
+
+def test_feature_row_widths_and_time_dims():
+    """Row sizes that take the 16-, 8- and 4-byte copy paths, a time
+    encoding width that is not a multiple of 4, and offset output buffers."""
+    import torch
+    rng = np.random.default_rng(5)
+    N, E, s = 300, 6000, 6
+    src = rng.integers(0, N, E).astype(np.int32)
+    dst = rng.integers(0, N, E).astype(np.int32)
+    t = np.sort(rng.integers(0, 10**6, E)).astype(np.uint32)
+    import paper_2402_01964_amd as nlb
+    for erb_elems, nrb_elems, d_t in ((4, 6, 7), (2, 3, 100), (1, 1, 1), (93, 64, 12)):
+        ef = rng.integers(0, 2**31, (E, erb_elems)).astype(np.int32)
+        nf = rng.integers(0, 2**31, (N, nrb_elems)).astype(np.int32)
+        fw = rng.uniform(0, 1, d_t).astype(np.float32)
+        fb = rng.uniform(-3, 3, d_t).astype(np.float32)
+        g = nlb.Table(N, s, 0.5, 9, time_w=to_dev(fw), time_b=to_dev(fb), edge_feat=to_dev(ef),
+                      node_feat=to_dev(nf))
+        o = oracle.Oracle(N, s, 0.5, 9)
+        g.insert(to_dev(src), to_dev(dst), to_dev(t))
+        o.insert(src, dst, t)
+        q = rng.integers(0, N, 777).astype(np.int32)
+        tq = rng.integers(0, 2 * 10**6, 777).astype(np.uint32)
+        gout = g.sample(to_dev(q), to_dev(tq))
+        compare_sample(gout, o.sample(q, tq, fw, fb, ef, nf), f"rows {erb_elems}/{nrb_elems}")
+        # outputs at a 4-byte offset inside larger buffers
+        big = torch.zeros(777 * s * erb_elems + 1, dtype=torch.int32, device="cuda")
+        out = {"efeat": big[1:].view(777, s, erb_elems)}
+        g.sample_into(to_dev(q), to_dev(tq), out)
+        np.testing.assert_array_equal(out["efeat"].cpu().numpy(),
+                                      o.sample(q, tq, None, None, ef, None)["efeat"])
+
+
+def test_errors_are_reported_not_faulted():
+    """Out-of-range ids, timestamps >= 2^30 and decreasing timestamps are
+    skipped/flagged; the rest of the batch is applied as usual."""
+    import paper_2402_01964_amd as nlb
+    N, s = 100, 4
+    g = nlb.Table(N, s, 0.5, 1)
+    src = np.array([1, 2, 500, 3, -4], np.int32)
+    dst = np.array([5, 6, 7, 8, 9], np.int32)
+    t = np.array([10, 11, 12, 13, 14], np.uint32)
+    g.insert(to_dev(src), to_dev(dst), to_dev(t))
+    assert g.status() == nlb.NLB_ERANGE
+    assert g.status() == nlb.NLB_OK  # cleared
+    g.insert(to_dev(np.array([1], np.int32)), to_dev(np.array([2], np.int32)),
+             to_dev(np.array([2**30], np.uint32)))
+    assert g.status() == nlb.NLB_EORDER
+    g.insert(to_dev(np.array([1], np.int32)), to_dev(np.array([2], np.int32)),
+             to_dev(np.array([3], np.uint32)))
+    assert g.status() == nlb.NLB_EORDER  # 3 < 14
+    out = g.sample(to_dev(np.array([0, 5, 100, -1], np.int32)),
+                   to_dev(np.array([99, 99, 99, 99], np.uint32)), want=("nbr",))
+    assert g.status() == nlb.NLB_ERANGE
+    nb = out["nbr"].cpu().numpy()
+    assert (nb[2:] == -1).all()
+    o = oracle.Oracle(N, s, 0.5, 1)
+    o.insert_ids([0, 1, 3], src[[0, 1, 3]], dst[[0, 1, 3]], t[[0, 1, 3]])
+    o.insert_ids([6], [1], [2], [3])
+    nbr, ts, eid = g.export()
+    on, ot, oe = o.export()
+    np.testing.assert_array_equal(nbr.cpu().numpy(), on)
+    np.testing.assert_array_equal(u32(eid), oe)
+    # empty calls are no-ops
+    g.insert(to_dev(np.zeros(0, np.int32)), to_dev(np.zeros(0, np.int32)),
+             to_dev(np.zeros(0, np.uint32)))
+    g.sample(to_dev(np.zeros(0, np.int32)), to_dev(np.zeros(0, np.uint32)), want=("nbr",))
+    assert g.info()["interactions"] == 6
+    with pytest.raises(nlb.NLBError):  # no time encoding configured
+        g.sample_into(to_dev(np.zeros(3, np.int32)), to_dev(np.zeros(3, np.uint32)),
+                      {"tenc": to_dev(np.zeros(300, np.float32))})
