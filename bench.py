@@ -37,6 +37,9 @@ def parse():
                     help="first batch of the warmup (default: the middle of the stream)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="before the benchmark, run a plain elementwise copy of this many MiB "
+                         "five times (a known-traffic kernel for calibrating HBM counters)")
     return ap.parse_args()
 
 
@@ -127,6 +130,14 @@ def main():
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     w = synth.workload(args.workload)
+    if args.copy_probe_mb:
+        n = args.copy_probe_mb * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device=dev)
+        c = torch.empty_like(a)
+        for _ in range(5):
+            torch.neg(a, out=c)   # reads and writes copy_probe_mb MiB each
+        torch.cuda.synchronize()
+        del a, c
     K, W = args.steps, args.warmup
     start = args.start_batch
     if start is None:

@@ -45,8 +45,6 @@ constexpr uint32_t kStatusRange = 1u;   // node id out of range
 constexpr uint32_t kStatusOrder = 2u;   // timestamp >= 2^30 or decreasing
 constexpr size_t kStatusBytes = 256;    // [0] flags, [1..2] last timestamp per batch parity
 
-constexpr int kWave = 64;
-constexpr int kSampleWaves = 4;         // queries per 256-thread workgroup
 constexpr int kInsertThreads = 256;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -76,33 +74,27 @@ __device__ __forceinline__ uint64_t splitmix64_nth(uint64_t state0, uint64_t n) 
 }
 
 // ---------------------------------------------------------------- cosine
-// cos of an fp32 argument within ~5e-7 absolute.  For |x| < 2^30 the
-// argument is reduced by pi/2 in double with a two-constant Cody-Waite step
-// (Cody & Waite, "Software Manual for the Elementary Functions", 1980) whose
-// products are exact inside fused multiply-adds, leaving r accurate to
-// ~1e-16; cos(r) and sin(r) on [-pi/4, pi/4] are their Taylor polynomials
-// through r^8 and r^7 (truncation < 3.2e-7).  Larger arguments go to the
-// device libm's double cos, which reduces exactly.
-__device__ __forceinline__ float cos_fp32(float x) {
-    if (fabsf(x) < 1073741824.0f) {
-        const double xd = (double)x;
-        const double kd = __builtin_rint(xd * 0.63661977236758134308);
-        double r = __builtin_fma(-kd, 1.5707963267948965580e+00, xd);
-        r = __builtin_fma(-kd, 6.1232339957367658e-17, r);
-        const int k = (int)kd;
-        const float rf = (float)r;
-        const float z = rf * rf;
-        const float c = __builtin_fmaf(z, __builtin_fmaf(z, __builtin_fmaf(z, __builtin_fmaf(z,
-                            2.4801587301587302e-05f, -1.3888888888888889e-03f),
-                            4.1666666666666664e-02f), -0.5f), 1.0f);
-        const float sn = rf * __builtin_fmaf(z, __builtin_fmaf(z, __builtin_fmaf(z,
-                            -1.9841269841269841e-04f, 8.3333333333333332e-03f),
-                            -1.6666666666666666e-01f), 1.0f);
-        // cos(r + k*pi/2) = cos r, -sin r, -cos r, sin r for k mod 4 = 0..3
-        const float v = (k & 1) ? sn : c;
-        return ((k + 1) & 2) ? -v : v;
-    }
+// Arguments beyond the fast path's range: the device libm's double cos,
+// which reduces exactly.  Kept out of line so that its registers do not
+// weigh on the kernels (time encodings never reach it in practice).
+__device__ __attribute__((noinline)) float cos_fp32_wide(float x) {
     return (float)cos((double)x);
+}
+
+// cos of an fp32 argument.  The argument is converted to revolutions in
+// double, y = x / (2 pi), and reduced to f = y - rint(y) in [-1/2, 1/2]; for
+// |x| < 2^33 the double product leaves f within 3e-7 revolutions of exact.
+// The hardware cosine (v_cos_f32, cos(2 pi f)) then evaluates the reduced
+// fraction; measured on gfx950 over a dense grid of [-1/2, 1/2] its error is
+// below 1.3e-7, and the whole function stays below 3e-7 absolute for
+// |x| < 1e9 against a double-precision cosine.
+__device__ __forceinline__ float cos_fp32(float x) {
+    if (fabsf(x) < 8589934592.0f) {
+        const double y = (double)x * 0.15915494309189533577;
+        const float f = (float)(y - __builtin_rint(y));
+        return __builtin_amdgcn_cosf(f);
+    }
+    return cos_fp32_wide(x);
 }
 
 // ---------------------------------------------------------------- insert
@@ -197,6 +189,17 @@ __global__ __launch_bounds__(kInsertThreads) void insert_commit(InsertParams p) 
 }
 
 // ---------------------------------------------------------------- sample
+// A 256-thread workgroup answers a tile of consecutive queries.  Its outputs
+// are contiguous ranges of every output array, so all stores are streamed
+// full lines.  Phase 1 reads the tile's table slots (one thread per slot
+// row), writes the id outputs and stages each slot's (neighbour, arrival
+// index, timestamp, gap) in LDS.  The later phases walk the flattened output
+// ranges (time encoding, link rows, neighbour rows, self rows) with every
+// thread taking consecutive 16-, 8- or 4-byte units; they look up their slot
+// in LDS and keep several row loads in flight before storing.
+constexpr int kTileThreads = 256;
+constexpr int kTileSlots = 1024;   // slot rows staged per tile (16 B each in LDS)
+
 struct SampleParams {
     const uint8_t *blocks;
     uint32_t block_bytes;
@@ -205,6 +208,8 @@ struct SampleParams {
     const int32_t *node;
     const uint32_t *tq;
     uint32_t nq;
+    uint32_t tile_q;      // queries per tile; tile_q * s <= kTileSlots
+    uint64_t s_m;         // ceil(2^40 / s)
     uint32_t d_time;
     const float *w;
     const float *b;
@@ -230,149 +235,158 @@ struct SampleParams {
     uint64_t n_m;
 };
 
+// One staged slot: x (-1 when the slot is not valid for its query), arrival
+// index, timestamp and the fp32 gap tq - t'.
+struct SlotLds {
+    int32_t x;
+    uint32_t e;
+    uint32_t t;
+    float dt;
+};
+
 template <int W> struct VecOf;
 template <> struct VecOf<16> { typedef u32x4 T; };
 template <> struct VecOf<8> { typedef u32x2 T; };
 template <> struct VecOf<4> { typedef uint32_t T; };
 
-// Copy the rows selected by (row_i, ok_i) of the wave's lanes 0..sc-1 into
-// the contiguous output rows out_row0 .. out_row0+sc-1.  Lane L handles
-// units base+L of the flattened [sc][units] range; loads of four rounds are
-// issued before their stores.  Rows with ok == 0 are written as zeros.
-template <int W>
-__device__ __forceinline__ void gather_rows(const uint8_t *__restrict__ src, uint32_t row_bytes,
-                                            uint32_t units, uint64_t m, uint32_t sc,
-                                            int64_t row_i, int ok_i, uint8_t *__restrict__ out,
-                                            uint32_t lane) {
+// Row source of output row j: the neighbour's node row (kind 0), the
+// link's row (kind 1) or the query node's row (kind 2).
+enum RowKind { kRowNeighbour = 0, kRowLink = 1, kRowSelf = 2 };
+
+// Copy `rows` output rows of `row_bytes` each, laid out contiguously at
+// `out`, from their source rows; unit f of the flattened range is
+// (row f / units, column f % units).  R loads per thread are issued before
+// their stores.  Rows without a valid source are written as zeros.
+template <int W, int KIND>
+__device__ __forceinline__ void gather_tile(const uint8_t *__restrict__ src, uint32_t row_bytes,
+                                            uint32_t units, uint64_t m, uint32_t rows,
+                                            int64_t src_rows, const SlotLds *slots,
+                                            const int32_t *tile_nodes, uint8_t *__restrict__ out,
+                                            uint32_t tid) {
     typedef typename VecOf<W>::T V;
-    constexpr int R = 4;
-    const uint32_t total = sc * units;
-    for (uint32_t base = 0; base < total; base += kWave * R) {
+    constexpr int R = (W == 16) ? 4 : (W == 8 ? 6 : 8);
+    const uint32_t total = rows * units;
+    for (uint32_t base = 0; base < total; base += kTileThreads * R) {
         V val[R];
-        uint32_t fi[R];
 #pragma unroll
         for (int r = 0; r < R; r++) {
-            const uint32_t f = base + r * kWave + lane;
-            const bool act = f < total;
-            const uint32_t j = act ? div_small(f, m) : 0u;
-            const int64_t row = __shfl(row_i, (int)j, kWave);
-            const int ok = __shfl(ok_i, (int)j, kWave);
-            fi[r] = f;
+            const uint32_t f = base + r * kTileThreads + tid;
             val[r] = V(0);
-            if (act && ok) {
+            if (f < total) {
+                const uint32_t j = div_small(f, m);
                 const uint32_t c = f - j * units;
-                val[r] = *(const V *)(src + (size_t)row * row_bytes + (size_t)c * W);
+                int64_t row;
+                if (KIND == kRowSelf) {
+                    row = tile_nodes[j];
+                } else {
+                    const SlotLds sl = slots[j];
+                    row = (sl.x < 0) ? -1 : (KIND == kRowNeighbour ? (int64_t)sl.x : (int64_t)sl.e);
+                }
+                if (row >= 0 && row < src_rows)
+                    val[r] = *(const V *)(src + (size_t)row * row_bytes + (size_t)c * W);
             }
         }
 #pragma unroll
         for (int r = 0; r < R; r++) {
-            if (fi[r] < total) {
-                __builtin_nontemporal_store(val[r], (V *)(out + (size_t)fi[r] * W));
-            }
+            const uint32_t f = base + r * kTileThreads + tid;
+            if (f < total) __builtin_nontemporal_store(val[r], (V *)(out + (size_t)f * W));
         }
     }
 }
 
-__device__ __forceinline__ void gather_rows_w(uint32_t width, const uint8_t *src,
-                                              uint32_t row_bytes, uint32_t units, uint64_t m,
-                                              uint32_t sc, int64_t row_i, int ok_i, uint8_t *out,
-                                              uint32_t lane) {
+template <int KIND>
+__device__ __forceinline__ void gather_tile_w(uint32_t width, const uint8_t *src, uint32_t row_bytes,
+                                              uint32_t units, uint64_t m, uint32_t rows,
+                                              int64_t src_rows, const SlotLds *slots,
+                                              const int32_t *tile_nodes, uint8_t *out,
+                                              uint32_t tid) {
     if (width == 16)
-        gather_rows<16>(src, row_bytes, units, m, sc, row_i, ok_i, out, lane);
+        gather_tile<16, KIND>(src, row_bytes, units, m, rows, src_rows, slots, tile_nodes, out, tid);
     else if (width == 8)
-        gather_rows<8>(src, row_bytes, units, m, sc, row_i, ok_i, out, lane);
+        gather_tile<8, KIND>(src, row_bytes, units, m, rows, src_rows, slots, tile_nodes, out, tid);
     else
-        gather_rows<4>(src, row_bytes, units, m, sc, row_i, ok_i, out, lane);
+        gather_tile<4, KIND>(src, row_bytes, units, m, rows, src_rows, slots, tile_nodes, out, tid);
 }
 
-// One wavefront answers one query; four queries per workgroup.
-__global__ __launch_bounds__(kWave * kSampleWaves) void sample_gather(SampleParams p) {
-    const uint32_t lane = threadIdx.x & (kWave - 1);
-    const uint64_t q = (uint64_t)blockIdx.x * kSampleWaves + (threadIdx.x / kWave);
-    if (q >= p.nq) return;  // uniform across the wave
-    const int32_t node = p.node[q];
-    const uint32_t tq = p.tq[q];
-    const bool in_range = node >= 0 && (int64_t)node < p.num_nodes;
-    if (!in_range && lane == 0) atomicOr(p.status, kStatusRange);
-    const uint8_t *blk = p.blocks + (size_t)(in_range ? node : 0) * p.block_bytes;
-    const uint64_t *keys = (const uint64_t *)blk;
-    const int32_t *nbrs = (const int32_t *)(blk + 8u * p.s);
+__global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
+    __shared__ SlotLds slots[kTileSlots];
+    __shared__ int32_t tile_nodes[kTileSlots];
+    const uint32_t tid = threadIdx.x;
+    const uint64_t q0 = (uint64_t)blockIdx.x * p.tile_q;
+    const uint32_t nqt = (uint32_t)min((uint64_t)p.tile_q, (uint64_t)p.nq - q0);
+    const uint32_t s = p.s;
+    const uint32_t ns = nqt * s;                 // slot rows of this tile
+    const size_t row0 = (size_t)q0 * s;          // first output slot row
 
-    for (uint32_t c0 = 0; c0 < p.s; c0 += kWave) {
-        const uint32_t sc = min((uint32_t)kWave, p.s - c0);
-        // Lane j < sc owns slot c0 + j.
-        int valid = 0;
-        int32_t x = -1;
-        uint32_t e = 0xFFFFFFFFu, ts = 0xFFFFFFFFu;
-        float dt = 0.0f;
-        if (lane < sc && in_range) {
-            const uint64_t key = keys[c0 + lane];
-            const int32_t xv = nbrs[c0 + lane];  // same cache line; issued with the key
-            if (key != 0) {
-                const uint32_t t = (uint32_t)key & kTimeMask;
-                if (t < tq) {  // eq. (1): strictly earlier links only
-                    const uint32_t ef = (uint32_t)(key >> kTimeBits);
-                    valid = 1;
-                    e = ((key >> 62) == 3u) ? ef : ~ef;
-                    ts = t;
-                    x = xv;
-                    dt = (float)(tq - t);
+    // Phase 1: table read, strict mask (eq. (1)), id outputs, LDS staging.
+    for (uint32_t j = tid; j < ns; j += kTileThreads) {
+        const uint32_t ql = div_small(j, p.s_m);
+        const uint32_t a = j - ql * s;
+        const int32_t node = p.node[q0 + ql];
+        const uint32_t tq = p.tq[q0 + ql];
+        const bool in_range = node >= 0 && (int64_t)node < p.num_nodes;
+        SlotLds sl = {-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
+        if (in_range) {
+            const uint8_t *blk = p.blocks + (size_t)node * p.block_bytes;
+            const uint64_t key = ((const uint64_t *)blk)[a];
+            const int32_t xv = ((const int32_t *)(blk + 8u * s))[a];
+            const uint32_t t = (uint32_t)key & kTimeMask;
+            if (key != 0 && t < tq) {
+                const uint32_t ef = (uint32_t)(key >> kTimeBits);
+                sl.x = xv;
+                sl.e = ((key >> 62) == 3u) ? ef : ~ef;
+                sl.t = t;
+                sl.dt = (float)(tq - t);
+            }
+        } else if (a == 0) {
+            atomicOr(p.status, kStatusRange);
+        }
+        if (a == 0) tile_nodes[ql] = in_range ? node : -1;
+        slots[j] = sl;
+        if (p.o_nbr) p.o_nbr[row0 + j] = sl.x;
+        if (p.o_eid) p.o_eid[row0 + j] = sl.e;
+        if (p.o_ts) p.o_ts[row0 + j] = sl.t;
+    }
+    __syncthreads();
+
+    // Phase 2: T-encoding (App. C): cos(w_k * dt + b_k), the argument formed
+    // by one fp32 fused multiply-add; zeros on invalid slots.
+    if (p.o_tenc) {
+        const uint32_t units = p.tenc_units;
+        const uint32_t total = ns * units;
+        float *out = p.o_tenc + row0 * p.d_time;
+        for (uint32_t f = tid; f < total; f += kTileThreads) {
+            const uint32_t j = div_small(f, p.tenc_m);
+            const uint32_t c = f - j * units;
+            const SlotLds sl = slots[j];
+            if (p.tenc_vec == 4) {
+                f32x4 r = f32x4(0.0f);
+                if (sl.x >= 0) {
+                    const f32x4 w4 = *(const f32x4 *)(p.w + 4 * c);
+                    const f32x4 b4 = *(const f32x4 *)(p.b + 4 * c);
+                    r.x = cos_fp32(__builtin_fmaf(w4.x, sl.dt, b4.x));
+                    r.y = cos_fp32(__builtin_fmaf(w4.y, sl.dt, b4.y));
+                    r.z = cos_fp32(__builtin_fmaf(w4.z, sl.dt, b4.z));
+                    r.w = cos_fp32(__builtin_fmaf(w4.w, sl.dt, b4.w));
                 }
+                __builtin_nontemporal_store(r, (f32x4 *)(out + (size_t)f * 4));
+            } else {
+                float r = 0.0f;
+                if (sl.x >= 0) r = cos_fp32(__builtin_fmaf(p.w[c], sl.dt, p.b[c]));
+                __builtin_nontemporal_store(r, out + f);
             }
         }
-        const size_t row0 = (size_t)q * p.s + c0;  // first output row of this chunk
-        if (lane < sc) {
-            if (p.o_nbr) p.o_nbr[row0 + lane] = x;
-            if (p.o_eid) p.o_eid[row0 + lane] = e;
-            if (p.o_ts) p.o_ts[row0 + lane] = ts;
-        }
-
-        if (p.o_tenc) {
-            // T-encoding (App. C): cos(w_k * dt + b_k) with the argument
-            // formed by one fp32 fused multiply-add.
-            const uint32_t units = p.tenc_units;
-            const uint32_t total = sc * units;
-            float *out = p.o_tenc + row0 * p.d_time;
-            for (uint32_t base = 0; base < total; base += kWave) {
-                const uint32_t f = base + lane;
-                const bool act = f < total;
-                const uint32_t j = act ? div_small(f, p.tenc_m) : 0u;
-                const int ok = __shfl(valid, (int)j, kWave);
-                const float g = __shfl(dt, (int)j, kWave);
-                if (!act) continue;
-                const uint32_t c = f - j * units;
-                if (p.tenc_vec == 4) {
-                    f32x4 r = f32x4(0.0f);
-                    if (ok) {
-                        const f32x4 w4 = *(const f32x4 *)(p.w + 4 * c);
-                        const f32x4 b4 = *(const f32x4 *)(p.b + 4 * c);
-                        r.x = cos_fp32(__builtin_fmaf(w4.x, g, b4.x));
-                        r.y = cos_fp32(__builtin_fmaf(w4.y, g, b4.y));
-                        r.z = cos_fp32(__builtin_fmaf(w4.z, g, b4.z));
-                        r.w = cos_fp32(__builtin_fmaf(w4.w, g, b4.w));
-                    }
-                    __builtin_nontemporal_store(r, (f32x4 *)(out + (size_t)f * 4));
-                } else {
-                    float r = 0.0f;
-                    if (ok) r = cos_fp32(__builtin_fmaf(p.w[c], g, p.b[c]));
-                    __builtin_nontemporal_store(r, out + f);
-                }
-            }
-        }
-        if (p.o_efeat) {
-            const int ok = valid && (int64_t)e < p.edge_rows;
-            gather_rows_w(p.e_width, p.efeat, p.erb, p.e_units, p.e_m, sc, (int64_t)e, ok,
-                          p.o_efeat + row0 * p.erb, lane);
-        }
-        if (p.o_nfeat) {
-            gather_rows_w(p.n_width, p.nfeat, p.nrb, p.n_units, p.n_m, sc, (int64_t)x, valid,
-                          p.o_nfeat + row0 * p.nrb, lane);
-        }
     }
-    if (p.o_self) {
-        gather_rows_w(p.n_width, p.nfeat, p.nrb, p.n_units, p.n_m, 1, (int64_t)node,
-                      in_range ? 1 : 0, p.o_self + (size_t)q * p.nrb, lane);
-    }
+    // Phase 3-5: row gathers (Sec. 4.4: link features, neighbour status, self).
+    if (p.o_efeat)
+        gather_tile_w<kRowLink>(p.e_width, p.efeat, p.erb, p.e_units, p.e_m, ns, p.edge_rows, slots,
+                                tile_nodes, p.o_efeat + row0 * p.erb, tid);
+    if (p.o_nfeat)
+        gather_tile_w<kRowNeighbour>(p.n_width, p.nfeat, p.nrb, p.n_units, p.n_m, ns, p.num_nodes,
+                                     slots, tile_nodes, p.o_nfeat + row0 * p.nrb, tid);
+    if (p.o_self)
+        gather_tile_w<kRowSelf>(p.n_width, p.nfeat, p.nrb, p.n_units, p.n_m, nqt, p.num_nodes, slots,
+                                tile_nodes, p.o_self + q0 * p.nrb, tid);
 }
 
 // ---------------------------------------------------------------- export
@@ -412,6 +426,15 @@ uint32_t block_bytes_for(uint32_t s) {
 }
 
 uint64_t ceil_2_40_div(uint32_t d) { return ((1ull << 40) + d - 1) / d; }
+
+// Queries per sample tile: as many as fit kTileSlots slot rows, rounded down
+// to a multiple of 16 when possible so that tiles start on whole cache lines
+// of every output array.
+uint32_t tile_queries(uint32_t s) {
+    uint32_t q = kTileSlots / s;
+    if (q >= 32) q = q / 16 * 16;
+    return q < 1 ? 1 : q;
+}
 
 class DeviceGuard {
   public:
@@ -658,9 +681,11 @@ int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t n
     p.n_width = h->nrb ? copy_width(h->nrb, h->nfeat, (const void *)nalign) : 4;
     p.n_units = h->nrb ? h->nrb / p.n_width : 1;
     p.n_m = ceil_2_40_div(p.n_units);
+    p.tile_q = tile_queries(h->s);
+    p.s_m = ceil_2_40_div(h->s);
     const hipStream_t st = (hipStream_t)stream;
-    const dim3 grid((nq + kSampleWaves - 1) / kSampleWaves);
-    hipLaunchKernelGGL(sample_gather, grid, dim3(kWave * kSampleWaves), 0, st, p);
+    const dim3 grid((unsigned)((nq + p.tile_q - 1) / p.tile_q));
+    hipLaunchKernelGGL(sample_gather, grid, dim3(kTileThreads), 0, st, p);
     if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
     return NLB_OK;
 }

@@ -274,7 +274,7 @@ def test_errors_are_reported_not_faulted():
     g.insert(to_dev(np.zeros(0, np.int32)), to_dev(np.zeros(0, np.int32)),
              to_dev(np.zeros(0, np.uint32)))
     g.sample(to_dev(np.zeros(0, np.int32)), to_dev(np.zeros(0, np.uint32)), want=("nbr",))
-    assert g.info()["interactions"] == 6
+    assert g.info()["interactions"] == 7   # flagged links still consume their index
     with pytest.raises(nlb.NLBError):  # no time encoding configured
         g.sample_into(to_dev(np.zeros(3, np.int32)), to_dev(np.zeros(3, np.uint32)),
                       {"tenc": to_dev(np.zeros(300, np.float32))})
