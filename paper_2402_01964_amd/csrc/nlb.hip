@@ -139,33 +139,93 @@ __device__ __forceinline__ bool link_ok(const InsertParams &p, int32_t u, int32_
            t <= kTimeMask;
 }
 
-__global__ __launch_bounds__(kInsertThreads) void insert_resolve(InsertParams p) {
-    const uint32_t i = blockIdx.x * kInsertThreads + threadIdx.x;
-    if (i >= p.n) return;
+// Pass 1.  Each link validates itself and turns into two offer words that
+// go to their slots with a 64-bit atomic maximum.  For large batches a
+// workgroup takes kResolveLinks consecutive links and first merges their
+// offers per slot in an LDS hash table (open addressing on the key word's
+// byte offset, 64-bit LDS atomics), so a slot that many of its offers hit --
+// the slots of a popular node -- costs one global atomic per workgroup
+// instead of one per offer; the maximum is associative, so the result is the
+// same.  Small batches skip the merge: they have few workgroups and little
+// same-slot traffic, and the plain atomics finish sooner.
+constexpr int kResolveLinks = 1024;
+constexpr int kAggBits = 12;                      // 2 * kResolveLinks offers: load <= 1/2
+constexpr int kAggEntries = 1 << kAggBits;
+constexpr uint32_t kAggMinBatch = 65536;          // batches from this size merge in LDS
+static_assert(kAggEntries >= 4 * kResolveLinks, "aggregation table size");
+
+__device__ __forceinline__ void agg_offer(unsigned long long *agg_off, unsigned long long *agg_word,
+                                          uint64_t off, uint64_t word) {
+    const unsigned long long tag = off + 1;  // 0 marks a free entry
+    uint32_t h = (uint32_t)(((off >> 3) * kGolden) >> (64 - kAggBits));
+    for (;;) {
+        const unsigned long long prev = atomicCAS(&agg_off[h], 0ull, tag);
+        if (prev == 0ull || prev == tag) {
+            atomicMax(&agg_word[h], (unsigned long long)word);
+            return;
+        }
+        h = (h + 1) & (kAggEntries - 1);
+    }
+}
+
+// Validation of link i (ranges; timestamps non-decreasing inside the batch
+// and against the last timestamp of the previous batch) and its two offers.
+// Returns false when the link is skipped.
+__device__ __forceinline__ bool link_offers(const InsertParams &p, uint32_t i, uint64_t &ou,
+                                            uint64_t &wu, uint64_t &ov, uint64_t &wv) {
     const int32_t u = p.src[i];
     const int32_t v = p.dst[i];
     const uint32_t t = p.t[i];
-    // Validation: ranges, and timestamps non-decreasing inside the batch and
-    // against the last timestamp of the previous batch.
     uint32_t flags = 0;
-    if (u < 0 || v < 0 || (int64_t)u >= p.num_nodes || (int64_t)v >= p.num_nodes) flags |= kStatusRange;
+    if (u < 0 || v < 0 || (int64_t)u >= p.num_nodes || (int64_t)v >= p.num_nodes)
+        flags |= kStatusRange;
     if (t > kTimeMask) flags |= kStatusOrder;
     const uint32_t prev_t = (i > 0) ? p.t[i - 1] : p.status[1 + (p.parity ^ 1u)];
     if (t < prev_t) flags |= kStatusOrder;
     if (flags) atomicOr(p.status, flags);
     if (i == p.n - 1) p.status[1 + p.parity] = t;
-    if (!link_ok(p, u, v, t)) return;
-
+    if (!link_ok(p, u, v, t)) return false;
     const uint32_t e = p.e0 + i;
     // Sec. 4.2: S_u receives (v, t, e); S_v receives (u, t, e).
-    const uint32_t au = slot_of(p, (uint32_t)v, t);
-    const uint32_t av = slot_of(p, (uint32_t)u, t);
-    unsigned long long *ku =
-        (unsigned long long *)(p.blocks + (size_t)u * p.block_bytes) + au;
-    unsigned long long *kv =
-        (unsigned long long *)(p.blocks + (size_t)v * p.block_bytes) + av;
-    atomicMax(ku, (unsigned long long)offer_word(p, e, 0, t));
-    atomicMax(kv, (unsigned long long)offer_word(p, e, 1, t));
+    ou = (uint64_t)u * p.block_bytes + 8u * slot_of(p, (uint32_t)v, t);
+    ov = (uint64_t)v * p.block_bytes + 8u * slot_of(p, (uint32_t)u, t);
+    wu = offer_word(p, e, 0, t);
+    wv = offer_word(p, e, 1, t);
+    return true;
+}
+
+__global__ __launch_bounds__(kInsertThreads) void insert_resolve(InsertParams p) {
+    const uint32_t i = blockIdx.x * kInsertThreads + threadIdx.x;
+    if (i >= p.n) return;
+    uint64_t ou, wu, ov, wv;
+    if (!link_offers(p, i, ou, wu, ov, wv)) return;
+    atomicMax((unsigned long long *)(p.blocks + ou), (unsigned long long)wu);
+    atomicMax((unsigned long long *)(p.blocks + ov), (unsigned long long)wv);
+}
+
+__global__ __launch_bounds__(kInsertThreads) void insert_resolve_merged(InsertParams p) {
+    __shared__ unsigned long long agg_off[kAggEntries];
+    __shared__ unsigned long long agg_word[kAggEntries];
+    for (int k = threadIdx.x; k < kAggEntries; k += kInsertThreads) {
+        agg_off[k] = 0ull;
+        agg_word[k] = 0ull;
+    }
+    __syncthreads();
+    const uint32_t first = blockIdx.x * kResolveLinks;
+    for (uint32_t r = 0; r < kResolveLinks; r += kInsertThreads) {
+        const uint32_t i = first + r + threadIdx.x;
+        if (i >= p.n) break;
+        uint64_t ou, wu, ov, wv;
+        if (link_offers(p, i, ou, wu, ov, wv)) {
+            agg_offer(agg_off, agg_word, ou, wu);
+            agg_offer(agg_off, agg_word, ov, wv);
+        }
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < kAggEntries; k += kInsertThreads) {
+        const unsigned long long tag = agg_off[k];
+        if (tag) atomicMax((unsigned long long *)(p.blocks + (tag - 1)), agg_word[k]);
+    }
 }
 
 __global__ __launch_bounds__(kInsertThreads) void insert_commit(InsertParams p) {
@@ -621,9 +681,14 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const
     p.status = h->status;
     p.parity = (uint32_t)(h->batches & 1);
     const hipStream_t st = (hipStream_t)stream;
-    const dim3 grid((n + kInsertThreads - 1) / kInsertThreads);
-    hipLaunchKernelGGL(insert_resolve, grid, dim3(kInsertThreads), 0, st, p);
-    hipLaunchKernelGGL(insert_commit, grid, dim3(kInsertThreads), 0, st, p);
+    if (n >= kAggMinBatch)
+        hipLaunchKernelGGL(insert_resolve_merged, dim3((n + kResolveLinks - 1) / kResolveLinks),
+                           dim3(kInsertThreads), 0, st, p);
+    else
+        hipLaunchKernelGGL(insert_resolve, dim3((n + kInsertThreads - 1) / kInsertThreads),
+                           dim3(kInsertThreads), 0, st, p);
+    hipLaunchKernelGGL(insert_commit, dim3((n + kInsertThreads - 1) / kInsertThreads),
+                       dim3(kInsertThreads), 0, st, p);
     if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
     h->interactions += n;
     h->batches += 1;

@@ -1,0 +1,159 @@
+"""Full-size parity: workloads 3, 4 and 5 at their real sizes, with the
+inputs resident in HBM and the batch / query launches the benchmark times.
+
+The GPU runs the whole stream.  At checkpoint batches a random subset of the
+batch's queries is kept; after the stream, the final table rows of those
+query nodes are kept too.  The oracle then replays, in stream order, only the
+links that touch those nodes (tables are per node, so this is exact -- pinned
+on the CPU by test_filtered_substream_gives_same_rows) and answers the same
+queries at the same points.  Indices and rows must match bit for bit, the
+time encoding within 1e-5.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_helpers import TENC_TOL, host_np, make_gpu_table
+
+pytestmark = pytest.mark.gpu
+
+
+def _host_filtered_links(w, mask, chunk=50_000_000):
+    """Links touching a masked node, with their arrival indices; also the
+    host copy of every query position asked for later is taken from the
+    same host generation."""
+    ids, S, D, T = [], [], [], []
+    if w.stateless:
+        for lo in range(0, w.links, chunk):
+            hi = min(w.links, lo + chunk)
+            src, dst, t, _ = synth.host_links(w, lo, hi)
+            sel = np.nonzero(mask[src] | mask[dst])[0]
+            ids.append(sel + lo)
+            S.append(src[sel]); D.append(dst[sel]); T.append(t[sel])
+    else:
+        src, dst, t, _ = synth.host_links(w)
+        sel = np.nonzero(mask[src] | mask[dst])[0]
+        ids.append(sel); S.append(src[sel]); D.append(dst[sel]); T.append(t[sel])
+    return (np.concatenate(ids).astype(np.uint64), np.concatenate(S), np.concatenate(D),
+            np.concatenate(T))
+
+
+def _host_queries(w, b, positions):
+    """Host-generated (node, tq) of query positions of batch b."""
+    lo, hi = w.batch_range(b)
+    src, dst, t, neg = synth.host_links(w, lo, hi) if w.stateless else \
+        (x[lo:hi] for x in synth.host_links(w))
+    q = np.concatenate([src, dst, neg])
+    tq = np.concatenate([t, t, t])
+    return q[positions], tq[positions]
+
+
+def _log(*a):
+    print("[full-size]", *a, flush=True)
+
+
+def _full_size(k, checks, per_check=400):
+    import torch
+    w = synth.workload(k)
+    _log(f"workload {w.name}: {w.links} links, {w.batches} batches, checks {sorted(checks)}")
+    dev = torch.device("cuda", 0)
+    nodes_d, ts_d = synth.device_links(w, dev)
+    ef_d = synth.device_features(w, "edge", dev)
+    nf_d = synth.device_features(w, "node", dev)
+    g = make_gpu_table(w, ef_d, nf_d)
+    out = g.alloc_outputs(3 * w.batch)
+    rng = np.random.default_rng(100 + k)
+    kept = {}
+    for b in range(w.batches):
+        s_, d_, t_, q, tq = synth.batch_views(w, nodes_d, ts_d, b)
+        if b in checks:
+            n = q.numel()
+            o = {kk: v[:n] for kk, v in out.items()}
+            g.sample_into(q, tq, o)
+            pos = np.sort(rng.choice(n, min(n, per_check), replace=False))
+            pos_d = torch.from_numpy(pos).to(dev)
+            kept[b] = (pos, host_np(q[pos_d]), {kk: host_np(v[pos_d]) for kk, v in o.items()})
+        g.insert(s_, d_, t_)
+        if b % 1000 == 0:
+            _log(f"gpu batch {b}")
+    torch.cuda.synchronize()
+    assert g.status() == 0
+    qnodes = np.unique(np.concatenate([kept[b][1] for b in kept]))
+    nbr_d, ts_dd, eid_d = g.export()
+    idx = torch.from_numpy(qnodes.astype(np.int64)).to(dev)
+    final_gpu = (host_np(nbr_d[idx]), host_np(ts_dd[idx]).view(np.uint32),
+                 host_np(eid_d[idx]).view(np.uint32))
+    del nbr_d, ts_dd, eid_d, out, g, ef_d, nf_d, nodes_d, ts_d
+    torch.cuda.empty_cache()
+
+    # ---- oracle side (host only from here)
+    mask = np.zeros(w.num_nodes, bool)
+    mask[qnodes] = True
+    _log(f"gpu done; filtering the host stream for {len(qnodes)} query nodes")
+    eids, S, D, T = _host_filtered_links(w, mask)
+    _log(f"{len(eids)} links touch them; oracle replay")
+    o = oracle.Oracle(w.num_nodes, w.s, w.alpha, w.table_seed)
+    fw, fb = synth.time_params(w)
+    nf = ef = None
+    if w.node_dim:
+        nf = np.zeros((w.num_nodes, w.node_dim), np.uint16 if w.elem_bytes("node") == 2 else np.float32)
+    if w.edge_dim:
+        ef = np.zeros((w.links, w.edge_dim), np.uint16 if w.elem_bytes("edge") == 2 else np.float32)
+    done = 0
+    for b in sorted(kept):
+        lo, _ = w.batch_range(b)
+        upto = int(np.searchsorted(eids, lo))
+        if upto > done:
+            o.insert_ids(eids[done:upto], S[done:upto], D[done:upto], T[done:upto])
+            done = upto
+        pos, gq, gout = kept[b]
+        hq, htq = _host_queries(w, b, pos)
+        np.testing.assert_array_equal(hq, gq)   # host and device streams agree
+        # materialise the feature rows the oracle will copy
+        rn, _, re = o.export_nodes(hq)
+        if nf is not None:
+            need = np.unique(np.concatenate([hq, rn[rn >= 0]]))
+            nf[need] = synth.host_feature_rows(w, "node", need)
+        if ef is not None:
+            need = np.unique(re[re != 0xFFFFFFFF]).astype(np.int64)
+            ef[need] = synth.host_feature_rows(w, "edge", need)
+        oout = o.sample(hq, htq, fw, fb, ef, nf)
+        for key, ov in oout.items():
+            gv = gout[key]
+            if key in ("eid", "ts"):
+                gv = gv.view(np.uint32)
+            if key == "tenc":
+                err = np.abs(gv.astype(np.float64) - ov)
+                assert err.max() <= TENC_TOL, (b, err.max())
+            else:
+                assert np.array_equal(gv, ov), (k, b, key, int((gv != ov).sum()))
+        _log(f"checkpoint batch {b} matches")
+    o.insert_ids(eids[done:], S[done:], D[done:], T[done:])
+    for gv, ov, name in zip(final_gpu, o.export_nodes(qnodes), ("nbr", "ts", "eid")):
+        assert np.array_equal(gv, ov), (k, "final", name)
+    return len(kept), len(qnodes), len(eids)
+
+
+@pytest.mark.timeout(600)
+def test_medium_homogeneous_full_size():
+    w = synth.workload(3)
+    nb = w.batches
+    checks = {0, 1, nb // 3, nb // 2, nb - 1}
+    assert _full_size(3, checks)[0] == len(checks)
+
+
+@pytest.mark.timeout(600)
+def test_dense_repeated_full_size():
+    w = synth.workload(4)
+    nb = w.batches
+    checks = {0, 5, nb // 2, nb - 2, nb - 1}
+    assert _full_size(4, checks)[0] == len(checks)
+
+
+@pytest.mark.timeout(900)
+def test_large_sparse_full_size():
+    w = synth.workload(5)
+    nb = w.batches
+    checks = {0, 1000, nb // 2, nb - 1}
+    assert _full_size(5, checks, per_check=300)[0] == len(checks)

@@ -101,19 +101,20 @@ def test_batch_size_invariance_and_determinism():
     import torch
     w = synth.workload(2)
     src, dst, t, _ = synth.host_links(w)
-    n = 60000
+    n = 200000
     src, dst, t = src[:n], dst[:n], t[:n]
     o = make_oracle(w)
     o.insert(src, dst, t)
     ref = None
-    for B in (1, 7, 600, 2400, n):
-        m = 3000 if B == 1 else n
-        g = _insert_in_batches(w, src[:m], dst[:m], t[:m], B)
-        if B == 1:
+    # batches below and above the size where insertion merges offers in LDS
+    for B in (1, 7, 600, 2400, 65535, 65536, 100000, n):
+        m = 3000 if B == 1 else (40000 if B == 7 else n)
+        if m != n:
             o1 = make_oracle(w)
             o1.insert(src[:m], dst[:m], t[:m])
-            compare_tables(g, o1)
+            compare_tables(_insert_in_batches(w, src[:m], dst[:m], t[:m], B), o1)
             continue
+        g = _insert_in_batches(w, src, dst, t, B)
         compare_tables(g, o)
         cur = [x.cpu() for x in g.export()]
         if ref is not None:
@@ -141,13 +142,12 @@ def test_single_hot_slot_batch():
     w = dataclasses.replace(synth.workload(1), num_nodes=N, s=s)
     rng = np.random.default_rng(3)
     # neighbours congruent mod s, same t: eq. (2) gives one slot for all
-    nb = (rng.integers(1, N // s, 20000) * s).astype(np.int32)
+    nb = (rng.integers(1, N // s, 140000) * s).astype(np.int32)
     src = np.zeros_like(nb)
-    t = np.full(len(nb), 777, np.uint32)
-    # self-loops and a second hub with ties
+    # self-loops, and timestamp ties throughout
     src[::97] = nb[::97]
-    t = np.sort(np.concatenate([t[:10000], np.full(10000, 778, np.uint32)]))
-    for B in (20000, 4096, 333):
+    t = np.sort(np.concatenate([np.full(70000, 777, np.uint32), np.full(70000, 778, np.uint32)]))
+    for B in (140000, 70000, 4096, 333):
         g = _insert_in_batches(w, src, nb, t, B)
         o = make_oracle(w)
         o.insert(src, nb, t)
