@@ -55,6 +55,25 @@ def sample_bytes(w, valid_slots, queries):
     return reads + writes
 
 
+def measured_traffic(w):
+    """HBM bytes per sample launch from the committed rocprofv3 counter
+    summary of this workload, or None when there is none or the kernel
+    source has changed since the counters were taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", f"sample_gather_{w.name}.md")
+    src = os.path.join(ROOT, "paper_2402_01964_amd", "csrc", "nlb.hip")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"counters: workload=(\S+) kernel=sample_gather traffic_bytes_per_launch=(\S+) "
+                  r"kernel_source_sha256=([0-9a-f]+)", open(path).read())
+    if not m or m.group(1) != w.name:
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != m.group(3):
+        return None
+    return float(m.group(2))
+
+
 def insert_bytes(links):
     """Algorithmic bytes of one insert: 12 B of input per link, and per
     offer an 8 B key read-modify-write plus a 4 B neighbour write."""
@@ -153,9 +172,14 @@ def main():
     tw, tb = torch.from_numpy(fw).to(dev), torch.from_numpy(fb).to(dev)
     table = nlb.Table(w.num_nodes, w.s, w.alpha, w.table_seed, time_w=tw, time_b=tb,
                       edge_feat=ef, node_feat=nf)
+    print(f"bench: {w.name}: inputs in HBM; inserting batches 0..{start - 1}", file=sys.stderr,
+          flush=True)
     for b in range(start):
         s_, d_, t_, _, _ = synth.batch_views(w, nodes, ts, b)
         table.insert(s_, d_, t_)
+        if (b + 1) % 1000 == 0:
+            torch.cuda.synchronize()
+            print(f"bench: inserted {b + 1} batches", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     Qmax = 3 * w.batch
     out = table.alloc_outputs(Qmax, want=("eid", "ts", "tenc", "efeat", "nfeat", "self"))
@@ -175,6 +199,7 @@ def main():
         table.insert(s_, d_, t_)
     torch.cuda.synchronize()
 
+    print(f"bench: warm-up done; timing {K} steps", file=sys.stderr, flush=True)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
     qcount = []
     t0 = time.perf_counter()
@@ -198,6 +223,7 @@ def main():
     s_bytes = sum(sample_bytes(w, 0, n) for n in qcount) + valid * (w.row_bytes("edge") + w.row_bytes("node"))
     achieved = s_bytes / (sample_ms.sum() * 1e-3) / 1e9
     full_bytes_per_query = sample_bytes(w, w.s, 1)
+    traffic = measured_traffic(w)
     res = {
         "metric": "interactions/s ingested + sampled queries/s; achieved HBM GB/s vs peak",
         "value": links / elapsed,
@@ -223,13 +249,18 @@ def main():
         "insert_ms_avg": float(insert_ms.mean()),
         "valid_slot_fraction": valid / (queries * w.s),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBPS, "traffic": None,
+                     "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic,
+                     "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
+                                     "scaled by a copy kernel)",
+                     "traffic_rate_gbps": (traffic / (sample_ms.mean() * 1e-3) / 1e9
+                                           if traffic else None),
                      "kernel": "sample_gather",
                      "bytes_per_launch": s_bytes / K,
                      "bytes_per_query_full_occupancy": full_bytes_per_query},
         "setup_s": setup_s,
     }
     if not args.no_cpu_baseline:
+        print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(res), flush=True)
 
