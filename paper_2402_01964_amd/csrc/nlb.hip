@@ -487,13 +487,21 @@ uint32_t block_bytes_for(uint32_t s) {
 
 uint64_t ceil_2_40_div(uint32_t d) { return ((1ull << 40) + d - 1) / d; }
 
-// Queries per sample tile: as many as fit kTileSlots slot rows, rounded down
-// to a multiple of 16 when possible so that tiles start on whole cache lines
+// Queries per sample tile.  Large launches use as many queries as fit
+// kTileSlots slot rows; smaller ones shrink the tile until the launch has
+// about kTargetTiles workgroups, so that every CU gets work.  Tiles of 32
+// queries or more are a multiple of 16, so they start on whole cache lines
 // of every output array.
-uint32_t tile_queries(uint32_t s) {
-    uint32_t q = kTileSlots / s;
-    if (q >= 32) q = q / 16 * 16;
-    return q < 1 ? 1 : q;
+constexpr uint32_t kTargetTiles = 4096;
+
+uint32_t tile_queries(uint32_t s, uint32_t nq) {
+    uint32_t cap = kTileSlots / s;
+    if (cap >= 32) cap = cap / 16 * 16;
+    if (cap < 1) cap = 1;
+    uint32_t want = (uint32_t)(((uint64_t)nq + kTargetTiles - 1) / kTargetTiles);
+    if (want >= 32) want = (want + 15) / 16 * 16;
+    if (want < 1) want = 1;
+    return want < cap ? want : cap;
 }
 
 class DeviceGuard {
@@ -746,7 +754,7 @@ int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t n
     p.n_width = h->nrb ? copy_width(h->nrb, h->nfeat, (const void *)nalign) : 4;
     p.n_units = h->nrb ? h->nrb / p.n_width : 1;
     p.n_m = ceil_2_40_div(p.n_units);
-    p.tile_q = tile_queries(h->s);
+    p.tile_q = tile_queries(h->s, nq);
     p.s_m = ceil_2_40_div(h->s);
     const hipStream_t st = (hipStream_t)stream;
     const dim3 grid((unsigned)((nq + p.tile_q - 1) / p.tile_q));
