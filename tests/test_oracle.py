@@ -457,3 +457,68 @@ def test_sample_outputs_rows_and_zeros():
                 assert out["ts"][i, a] == 0xFFFFFFFF
                 assert not out["efeat"][i, a].any() and not out["nfeat"][i, a].any()
                 assert not out["tenc"][i, a].any()
+
+
+def test_theorem2_nlb_node_product_form():
+    """Theorem 2 (NLB-node achieves recent node-wise sampling, App. B): when
+    each neighbour v_j meets the centre node as an independent Poisson
+    process of rate lambda_j, the latest link with v_i, entered at t_i, is
+    still stored at t with probability
+        prod_{j != i} ((s-1)/s + (1/s) exp(alpha lambda_j (t_i - t))),
+    the average over neighbour ids of the slot collisions of eq. (3).  Away
+    from the start an offer enters with probability alpha, so presence =
+    alpha * that product."""
+    alpha, s, T, H, M = 0.5, 10, 150.0, 300, 30
+    scale = 1000.0
+    pres, expect = [], []
+    for rep in range(4):
+        rng = np.random.default_rng(700 + rep)
+        hub_l, nbr_l, time_l = [], [], []
+        lam_all, ids_all = [], []
+        for h in range(H):
+            lam = rng.uniform(0.05, 0.3, M)
+            ids = H + rng.choice(10**6, M, replace=False)
+            lam_all.append(lam)
+            ids_all.append(ids)
+            for j in range(M):
+                n = rng.poisson(lam[j] * T)
+                time_l.append(rng.uniform(0, T, n))
+                hub_l.append(np.full(n, h))
+                nbr_l.append(np.full(n, ids[j]))
+        times = np.concatenate(time_l)
+        hubs = np.concatenate(hub_l)
+        nbrs = np.concatenate(nbr_l)
+        order = np.argsort(times, kind="stable")
+        times, hubs, nbrs = times[order], hubs[order], nbrs[order]
+        tt = np.floor(times * scale).astype(np.uint32)
+        o = Oracle(H + 10**6, s, alpha, seed=1700 + rep, key_mode=1)
+        o.insert(hubs.astype(np.int32), nbrs.astype(np.int32), tt)
+        _, _, eid = o.export_nodes(np.arange(H, dtype=np.int32))
+        stored = set(int(x) for x in eid[eid != 0xFFFFFFFF])
+        # latest link of every (hub, neighbour) pair
+        key = hubs.astype(np.int64) * (H + 10**6) + nbrs
+        last = {}
+        for e_, k_ in enumerate(key):
+            last[k_] = e_
+        for h in range(H):
+            lam, ids = lam_all[h], ids_all[h]
+            for j in range(M):
+                k_ = h * (H + 10**6) + ids[j]
+                if k_ not in last:
+                    continue
+                e_ = last[k_]
+                ti = times[e_]
+                if ti < 60.0:           # the table has long been full
+                    continue
+                d = T - ti
+                others = np.delete(lam, j)
+                p = np.prod((s - 1) / s + np.exp(-alpha * others * d) / s)
+                pres.append(e_ in stored)
+                expect.append(alpha * p)
+    pres = np.array(pres)
+    expect = np.array(expect)
+    delta_order = np.argsort(expect)
+    for chunk in np.array_split(delta_order, 8):
+        mu = expect[chunk].sum()
+        var = (expect[chunk] * (1 - expect[chunk])).sum()
+        assert abs(pres[chunk].sum() - mu) < 5 * math.sqrt(var) + 1, (pres[chunk].sum(), mu)
