@@ -37,6 +37,9 @@ def parse():
                     help="first batch of the warmup (default: the middle of the stream)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--hop2", action="store_true",
+                    help="also answer every step's second hop (Sec. 4.4) with nlb_sample_hop2, "
+                         "ids only, and report it separately")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="before the benchmark, run a plain elementwise copy of this many MiB "
                          "five times (a known-traffic kernel for calibrating HBM counters)")
@@ -72,6 +75,14 @@ def measured_traffic(w):
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != m.group(3):
         return None
     return float(m.group(2))
+
+
+def hop2_bytes(w, hop1_valid, queries):
+    """Algorithmic bytes of one ids-only second-hop launch over `queries`
+    first-hop queries: per first-hop entry its neighbour id and the query
+    time (8 B) and, when valid, the neighbour's s slots (12 B each); writes
+    nbr/eid/ts for s*s slots per query (12 B each)."""
+    return queries * w.s * 8 + hop1_valid * 12 * w.s + queries * w.s * w.s * 12
 
 
 def insert_bytes(links):
@@ -184,6 +195,9 @@ def main():
     Qmax = 3 * w.batch
     out = table.alloc_outputs(Qmax, want=("eid", "ts", "tenc", "efeat", "nfeat", "self"))
     nbr_all = torch.empty((K, Qmax, w.s), dtype=torch.int32, device=dev)
+    hop2_out = None
+    if args.hop2:
+        hop2_out = table.alloc_outputs(Qmax * w.s, want=("nbr", "eid", "ts"))
     setup_s = time.perf_counter() - t_setup
 
     def step(b, nbr_out):
@@ -200,7 +214,7 @@ def main():
     torch.cuda.synchronize()
 
     print(f"bench: warm-up done; timing {K} steps", file=sys.stderr, flush=True)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
     qcount = []
     t0 = time.perf_counter()
     for k in range(K):
@@ -208,15 +222,21 @@ def main():
         ev[k][0].record()
         s_, d_, t_, n = step(b, nbr_all[k])
         ev[k][1].record()
-        table.insert(s_, d_, t_)
+        if hop2_out is not None:
+            _, _, _, _, tq = synth.batch_views(w, nodes, ts, b)
+            o2 = {kk: v[:n * w.s] for kk, v in hop2_out.items()}
+            table.sample_hop2_into(nbr_all[k, :n], tq, o2)
         ev[k][2].record()
+        table.insert(s_, d_, t_)
+        ev[k][3].record()
         qcount.append(n)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     assert table.status() == nlb.NLB_OK
 
     sample_ms = np.array([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)])
-    insert_ms = np.array([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)])
+    hop2_ms = np.array([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)])
+    insert_ms = np.array([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)])
     links = sum(n // 3 for n in qcount)
     queries = sum(qcount)
     valid = int(sum(int((nbr_all[k, :qcount[k]] >= 0).sum()) for k in range(K)))
@@ -259,6 +279,19 @@ def main():
                      "bytes_per_query_full_occupancy": full_bytes_per_query},
         "setup_s": setup_s,
     }
+    if hop2_out is not None:
+        n_last = qcount[-1] * w.s
+        last_valid = int((hop2_out["nbr"][:n_last] >= 0).sum())   # last step, after timing
+        hb = sum(hop2_bytes(w, int((nbr_all[k, :qcount[k]] >= 0).sum()), qcount[k])
+                 for k in range(K))
+        hach = hb / (hop2_ms.sum() * 1e-3) / 1e9
+        res["hop2"] = {"kernel": "sample_gather (second hop, ids only)",
+                       "hop2_queries_per_s": queries * w.s / (hop2_ms.sum() * 1e-3),
+                       "ms_avg": float(hop2_ms.mean()), "valid_slot_fraction_last_step":
+                           last_valid / (n_last * w.s),
+                       "roofline": {"bound": "hbm", "achieved": hach, "peak": PEAK_HBM_GBPS,
+                                    "unit": "GB/s", "frac": hach / PEAK_HBM_GBPS}}
+        res["value_note"] = "value includes the second-hop launches (--hop2)"
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

@@ -156,6 +156,20 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst,
 int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t nq,
                const nlb_sample_out *out, void *stream);
 
+/* Second-hop retrieval (Sec. 4.4: if v is stored in S_u^t, S_v^t holds
+ * down-sampled second-hop neighbours of u).  hop1_nbr is the device nbr
+ * output [nq][s] of an nlb_sample call for queries (node[i], tq[i]); tq is
+ * the same device array of nq query times.  For every first-hop entry
+ * (i, a) with neighbour v = hop1_nbr[i*s + a], the call answers the query
+ * (v, tq[i]) exactly as nlb_sample would, into row i*s + a of each output:
+ * nbr/eid/ts [nq][s][s], tenc [nq][s][s][d_time], efeat/nfeat
+ * [nq][s][s][row bytes], self [nq][s][node_row_bytes] (v's node row).  An
+ * empty first-hop entry (v < 0) gives an all-invalid answer and a zero self
+ * row without an error; v >= N is flagged as in nlb_sample.  nq*s must be
+ * below 2^32.  nq == 0 is a no-op.  Errors: as nlb_sample. */
+int nlb_sample_hop2(nlb_table *h, const int32_t *hop1_nbr, const uint32_t *tq, uint32_t nq,
+                    const nlb_sample_out *out, void *stream);
+
 /* Free the table's device memory after synchronising its device.  NULL is a
  * no-op.  Borrowed buffers are not touched. */
 int nlb_destroy(nlb_table *h);

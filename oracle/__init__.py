@@ -14,6 +14,7 @@ in the C source:
                    replace with probability alpha), both endpoints updated
 * ``sample``    -- eq. (1) strict ``t' < t`` mask; Sec. 4.4 retrieval of
                    neighbour, link-feature and self rows; App. C T-encoding
+* ``sample_hop2`` -- Sec. 4.4 second-hop neighbours: S_v^t of each stored v
 """
 from __future__ import annotations
 
@@ -75,6 +76,9 @@ def _load():
     lib.orc_sample.restype = ctypes.c_int
     lib.orc_sample.argtypes = [P, P, P, i64, i32, P, P, P, i64, P, i64,
                                P, P, P, P, P, P, P]
+    lib.orc_sample_hop2.restype = ctypes.c_int
+    lib.orc_sample_hop2.argtypes = [P, P, P, i64, i32, P, P, P, i64, P, i64,
+                                    P, P, P, P, P, P, P]
     lib.orc_tenc.argtypes = [P, i64, i32, P, P, P]
     _lib = lib
     return lib
@@ -199,6 +203,52 @@ class Oracle:
             _ptr(out.get("self")))
         if rc != 0:
             raise ValueError("oracle: query node out of range")
+        return out
+
+
+    def sample_hop2(self, hop1_nbr, tq, w=None, b=None, efeat=None, nfeat=None,
+                    want=("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self")):
+        """Second-hop retrieval (Sec. 4.4): for every first-hop entry
+        (i, a) with neighbour v = hop1_nbr[i, a] >= 0, the answer to query
+        (v, tq[i]); empty entries (-1) give empty answers.  Outputs are shaped
+        [nq, s, s, ...] (self: [nq, s, ...])."""
+        hop1 = _c(hop1_nbr, np.int32).reshape(-1)
+        tq = _c(tq, np.uint32)
+        nq, s = len(tq), self.s
+        assert len(hop1) == nq * s
+        d_t = 0 if w is None else len(w)
+        w = None if w is None else _c(w, np.float32)
+        b = None if b is None else _c(b, np.float32)
+        out = {}
+        if "nbr" in want:
+            out["nbr"] = np.empty((nq, s, s), np.int32)
+        if "eid" in want:
+            out["eid"] = np.empty((nq, s, s), np.uint32)
+        if "ts" in want:
+            out["ts"] = np.empty((nq, s, s), np.uint32)
+        if "tenc" in want and d_t > 0:
+            out["tenc"] = np.empty((nq, s, s, d_t), np.float32)
+        erb = nrb = 0
+        if efeat is not None:
+            efeat = np.ascontiguousarray(efeat)
+            erb = efeat.shape[1] * efeat.itemsize
+            if "efeat" in want:
+                out["efeat"] = np.empty((nq, s, s, efeat.shape[1]), efeat.dtype)
+        if nfeat is not None:
+            nfeat = np.ascontiguousarray(nfeat)
+            nrb = nfeat.shape[1] * nfeat.itemsize
+            if "nfeat" in want:
+                out["nfeat"] = np.empty((nq, s, s, nfeat.shape[1]), nfeat.dtype)
+            if "self" in want:
+                out["self"] = np.empty((nq, s, nfeat.shape[1]), nfeat.dtype)
+        rc = self._lib.orc_sample_hop2(
+            self._h, _ptr(hop1), _ptr(tq), nq, d_t, _ptr(w), _ptr(b),
+            _ptr(efeat), erb, _ptr(nfeat), nrb,
+            _ptr(out.get("nbr")), _ptr(out.get("eid")), _ptr(out.get("ts")),
+            _ptr(out.get("tenc")), _ptr(out.get("efeat")), _ptr(out.get("nfeat")),
+            _ptr(out.get("self")))
+        if rc != 0:
+            raise ValueError("oracle: first-hop neighbour out of range")
         return out
 
 

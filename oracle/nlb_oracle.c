@@ -22,7 +22,8 @@
  *     Tables are updated after the queries of the current batch are answered.
  *   - Sec. 4.4 and App. C: a query (u, t) returns the stored neighbours, their
  *     link features, the neighbours' own feature rows, the self row and a
- *     cosine time encoding of t - t'.
+ *     cosine time encoding of t - t'.  Second-hop neighbours of u are the
+ *     entries of S_v^t for the stored neighbours v of u.
  *
  * Random draws: the replacement coin of offer (e, k) (k = 0 for the S_u
  * offer, k = 1 for the S_v offer) is the high 32 bits of output number
@@ -243,6 +244,57 @@ int orc_sample(const orc *o, const int32_t *node, const uint32_t *tq, int64_t nq
         if (self_out && n_row_bytes > 0)
             memcpy(self_out + (size_t)i * (size_t)n_row_bytes,
                    nfeat + (size_t)n * (size_t)n_row_bytes, (size_t)n_row_bytes);
+    }
+    return 0;
+}
+
+/*
+ * Second-hop retrieval (Sec. 4.4): if v is stored in S_u^t, then S_v^t holds
+ * down-sampled second-hop neighbours of u.  For every first-hop entry
+ * (i, a) with neighbour v = hop1_nbr[i*s + a], answer the query (v, tq[i])
+ * exactly as orc_sample does, into output row i*s + a; an empty first-hop
+ * entry (v = -1) gives an all-invalid answer with a zero self row.  Outputs
+ * are laid out as orc_sample's for nq*s queries.
+ */
+int orc_sample_hop2(const orc *o, const int32_t *hop1_nbr, const uint32_t *tq, int64_t nq,
+                    int32_t d_t, const float *w, const float *b,
+                    const uint8_t *efeat, int64_t e_row_bytes,
+                    const uint8_t *nfeat, int64_t n_row_bytes,
+                    int32_t *nbr_out, uint32_t *eid_out, uint32_t *ts_out,
+                    float *tenc_out, uint8_t *efeat_out, uint8_t *nfeat_out,
+                    uint8_t *self_out)
+{
+    const int64_t s = o->s;
+    for (int64_t i = 0; i < nq; i++) {
+        for (int64_t a = 0; a < s; a++) {
+            const int64_t r = i * s + a;         /* second-hop query index */
+            const int32_t v = hop1_nbr[r];
+            if (v >= 0) {
+                int rc = orc_sample(o, &v, &tq[i], 1, d_t, w, b, efeat, e_row_bytes, nfeat,
+                                    n_row_bytes,
+                                    nbr_out ? nbr_out + r * s : NULL,
+                                    eid_out ? eid_out + r * s : NULL,
+                                    ts_out ? ts_out + r * s : NULL,
+                                    tenc_out ? tenc_out + r * s * d_t : NULL,
+                                    efeat_out ? efeat_out + r * s * e_row_bytes : NULL,
+                                    nfeat_out ? nfeat_out + r * s * n_row_bytes : NULL,
+                                    self_out ? self_out + r * n_row_bytes : NULL);
+                if (rc != 0) return rc;
+                continue;
+            }
+            for (int64_t c = 0; c < s; c++) {
+                const int64_t out = r * s + c;
+                if (nbr_out) nbr_out[out] = -1;
+                if (eid_out) eid_out[out] = 0xFFFFFFFFu;
+                if (ts_out) ts_out[out] = 0xFFFFFFFFu;
+                if (tenc_out) memset(tenc_out + out * d_t, 0, (size_t)d_t * sizeof(float));
+                if (efeat_out && e_row_bytes > 0)
+                    memset(efeat_out + out * e_row_bytes, 0, (size_t)e_row_bytes);
+                if (nfeat_out && n_row_bytes > 0)
+                    memset(nfeat_out + out * n_row_bytes, 0, (size_t)n_row_bytes);
+            }
+            if (self_out && n_row_bytes > 0) memset(self_out + r * n_row_bytes, 0, (size_t)n_row_bytes);
+        }
     }
     return 0;
 }

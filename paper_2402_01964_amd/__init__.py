@@ -21,7 +21,7 @@ KEY_EDGE, KEY_NODE = 0, 1
 MAX_SLOTS = 1024
 
 # Symbols declared in include/nlb.h.
-ABI_SYMBOLS = ("nlb_create", "nlb_insert_batch", "nlb_sample", "nlb_destroy",
+ABI_SYMBOLS = ("nlb_create", "nlb_insert_batch", "nlb_sample", "nlb_sample_hop2", "nlb_destroy",
                "nlb_get_info", "nlb_export", "nlb_status", "nlb_strerror")
 
 
@@ -73,6 +73,8 @@ def load_library(path: str = LIB_PATH):
     lib.nlb_insert_batch.restype = I
     lib.nlb_sample.argtypes = [P, P, P, U32, ctypes.POINTER(_SampleOut), P]
     lib.nlb_sample.restype = I
+    lib.nlb_sample_hop2.argtypes = [P, P, P, U32, ctypes.POINTER(_SampleOut), P]
+    lib.nlb_sample_hop2.restype = I
     lib.nlb_destroy.argtypes = [P]
     lib.nlb_destroy.restype = I
     lib.nlb_get_info.argtypes = [P, ctypes.POINTER(_Info)]
@@ -199,6 +201,30 @@ class Table:
         _check(self._lib.nlb_sample(self._h, _dev_ptr(node, 4, "node"), _dev_ptr(tq, 4, "tq"), nq,
                                     ctypes.byref(so), _stream_ptr(stream)), "nlb_sample")
         return out
+
+    def sample_hop2_into(self, hop1_nbr, tq, out: dict, stream=None):
+        """Second-hop answers (Sec. 4.4) for the [nq, s] first-hop neighbours
+        ``hop1_nbr`` of queries with times ``tq``, into caller tensors shaped
+        for nq*s queries."""
+        nq = int(tq.numel())
+        if hop1_nbr.numel() != nq * self.s:
+            raise ValueError("hop1_nbr must hold s entries per query")
+        so = _SampleOut()
+        for k in ("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self"):
+            setattr(so, k, _dev_ptr(out.get(k), None, k))
+        _check(self._lib.nlb_sample_hop2(self._h, _dev_ptr(hop1_nbr, 4, "hop1_nbr"),
+                                         _dev_ptr(tq, 4, "tq"), nq, ctypes.byref(so),
+                                         _stream_ptr(stream)), "nlb_sample_hop2")
+        return out
+
+    def sample_hop2(self, hop1_nbr, tq, want=("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self"),
+                    stream=None):
+        """Second-hop answers as new tensors shaped [nq, s, s, ...] (self:
+        [nq, s, ...])."""
+        nq = int(tq.numel())
+        out = self.alloc_outputs(nq * self.s, want)
+        self.sample_hop2_into(hop1_nbr, tq, out, stream)
+        return {k: v.view(nq, self.s, *v.shape[1:]) for k, v in out.items()}
 
     def alloc_outputs(self, nq: int, want=("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self")):
         import torch

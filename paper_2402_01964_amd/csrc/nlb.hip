@@ -368,6 +368,9 @@ __device__ __forceinline__ void gather_tile_w(uint32_t width, const uint8_t *src
         gather_tile<4, KIND>(src, row_bytes, units, m, rows, src_rows, slots, tile_nodes, out, tid);
 }
 
+// HOP2: query i is (node[i], tq[i / s]) and a negative node is an empty
+// answer (second-hop retrieval over first-hop outputs).
+template <bool HOP2>
 __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
     __shared__ SlotLds slots[kTileSlots];
     __shared__ int32_t tile_nodes[kTileSlots];
@@ -382,9 +385,11 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
     for (uint32_t j = tid; j < ns; j += kTileThreads) {
         const uint32_t ql = div_small(j, p.s_m);
         const uint32_t a = j - ql * s;
-        const int32_t node = p.node[q0 + ql];
-        const uint32_t tq = p.tq[q0 + ql];
+        const uint64_t qg = q0 + ql;
+        const int32_t node = p.node[qg];
+        const uint32_t tq = p.tq[HOP2 ? (uint32_t)qg / s : qg];
         const bool in_range = node >= 0 && (int64_t)node < p.num_nodes;
+        const bool quiet = HOP2 && node < 0;   // empty first-hop slot
         SlotLds sl = {-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
         if (in_range) {
             const uint8_t *blk = p.blocks + (size_t)node * p.block_bytes;
@@ -398,7 +403,7 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
                 sl.t = t;
                 sl.dt = (float)(tq - t);
             }
-        } else if (a == 0) {
+        } else if (a == 0 && !quiet) {
             atomicOr(p.status, kStatusRange);
         }
         if (a == 0) tile_nodes[ql] = in_range ? node : -1;
@@ -703,11 +708,8 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const
     return NLB_OK;
 }
 
-int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t nq,
-               const nlb_sample_out *out, void *stream) {
-    if (!h || !out) return NLB_EINVAL;
-    if (nq == 0) return NLB_OK;
-    if (!node || !tq) return NLB_EINVAL;
+static int launch_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t nq,
+                         uint32_t hop2, const nlb_sample_out *out, void *stream) {
     if (out->tenc && h->d_time == 0) return NLB_EINVAL;
     if (out->efeat && !h->efeat) return NLB_EINVAL;
     if ((out->nfeat || out->self) && !h->nfeat) return NLB_EINVAL;
@@ -758,9 +760,29 @@ int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t n
     p.s_m = ceil_2_40_div(h->s);
     const hipStream_t st = (hipStream_t)stream;
     const dim3 grid((unsigned)((nq + p.tile_q - 1) / p.tile_q));
-    hipLaunchKernelGGL(sample_gather, grid, dim3(kTileThreads), 0, st, p);
+    if (hop2)
+        hipLaunchKernelGGL(sample_gather<true>, grid, dim3(kTileThreads), 0, st, p);
+    else
+        hipLaunchKernelGGL(sample_gather<false>, grid, dim3(kTileThreads), 0, st, p);
     if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
     return NLB_OK;
+}
+
+int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t nq,
+               const nlb_sample_out *out, void *stream) {
+    if (!h || !out) return NLB_EINVAL;
+    if (nq == 0) return NLB_OK;
+    if (!node || !tq) return NLB_EINVAL;
+    return launch_sample(h, node, tq, nq, 0, out, stream);
+}
+
+int nlb_sample_hop2(nlb_table *h, const int32_t *hop1_nbr, const uint32_t *tq, uint32_t nq,
+                    const nlb_sample_out *out, void *stream) {
+    if (!h || !out) return NLB_EINVAL;
+    if (nq == 0) return NLB_OK;
+    if (!hop1_nbr || !tq) return NLB_EINVAL;
+    if ((uint64_t)nq * h->s > 0xFFFFFFFFull) return NLB_EINVAL;
+    return launch_sample(h, hop1_nbr, tq, (uint32_t)(nq * h->s), 1, out, stream);
 }
 
 int nlb_export(nlb_table *h, int32_t *nbr, uint32_t *ts, uint32_t *eid, void *stream) {

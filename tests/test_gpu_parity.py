@@ -278,3 +278,35 @@ def test_errors_are_reported_not_faulted():
     with pytest.raises(nlb.NLBError):  # no time encoding configured
         g.sample_into(to_dev(np.zeros(3, np.int32)), to_dev(np.zeros(3, np.uint32)),
                       {"tenc": to_dev(np.zeros(300, np.float32))})
+
+
+@pytest.mark.parametrize("k", [1, 3])
+def test_second_hop_matches_oracle(k):
+    """Sec. 4.4 second-hop retrieval: nlb_sample_hop2 on the first-hop
+    neighbours of a batch equals the oracle's second hop, rows and time
+    encoding included, at several points of the stream."""
+    w = synth.scaled(synth.workload(k), 30 * synth.workload(k).batch)
+    src, dst, t, neg = synth.host_links(w)
+    nodes, ts = synth.blocked(w, src, dst, t, neg)
+    nodes_d, ts_d = to_dev(nodes), to_dev(ts)
+    ef = synth.host_features(w, "edge") if w.edge_dim else None
+    nf = synth.host_features(w, "node") if w.node_dim else None
+    g = make_gpu_table(w, feat_to_dev(ef, w.edge_dtype) if ef is not None else None,
+                       feat_to_dev(nf, w.node_dtype) if nf is not None else None)
+    o = make_oracle(w)
+    fw, fb = synth.time_params(w)
+    for b in range(w.batches):
+        s_, d_, t_, q, tq = synth.batch_views(w, nodes_d, ts_d, b)
+        lo, hi = w.batch_range(b)
+        if b in (3, 17, 29):
+            qh = np.concatenate([src[lo:hi], dst[lo:hi], neg[lo:hi]])[:600]
+            tqh = np.concatenate([t[lo:hi]] * 3)[:600]
+            first = g.sample(q[:600], tq[:600], want=("nbr",))["nbr"]
+            gout = g.sample_hop2(first, tq[:600])
+            ofirst = o.sample(qh, tqh, want=("nbr",))["nbr"]
+            np.testing.assert_array_equal(first.cpu().numpy(), ofirst)
+            oout = o.sample_hop2(ofirst, tqh, fw, fb, ef, nf)
+            compare_sample(gout, oout, f"hop2 batch {b}")
+        g.insert(s_, d_, t_)
+        o.insert(src[lo:hi], dst[lo:hi], t[lo:hi])
+    assert g.status() == 0   # empty first-hop entries are not errors

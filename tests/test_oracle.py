@@ -148,6 +148,16 @@ def test_handworked_tables(golden_dir):
         rule, node, tq, a, valid = r[1], int(r[2]), int(r[3]), int(r[4]), int(r[5])
         out = made[("edge", rule)].sample([node], [tq])
         assert (out["nbr"][0, a] >= 0) == bool(valid), r
+    hop2_rows = [r for r in rows if r[0] == "hop2"]
+    assert hop2_rows
+    for r in hop2_rows:
+        rule, node, tq, a, c, nbr = r[1], int(r[2]), int(r[3]), int(r[4]), int(r[5]), int(r[6])
+        o = made[("edge", rule)]
+        first = o.sample([node], [tq], want=("nbr",))["nbr"]
+        out = o.sample_hop2(first, [tq], want=("nbr", "eid", "ts"))
+        assert out["nbr"][0, a, c] == nbr, r
+        if nbr >= 0:
+            assert (out["ts"][0, a, c], out["eid"][0, a, c]) == (int(r[7]), int(r[8])), r
 
 
 def test_slot_matches_eq2_bigint():
@@ -522,3 +532,34 @@ def test_theorem2_nlb_node_product_form():
         mu = expect[chunk].sum()
         var = (expect[chunk] * (1 - expect[chunk])).sum()
         assert abs(pres[chunk].sum() - mu) < 5 * math.sqrt(var) + 1, (pres[chunk].sum(), mu)
+
+
+def test_hop2_entries_are_neighbours_of_neighbours():
+    """Sec. 4.4 second hop: every valid entry (i, a, c) is a stored link of
+    the first-hop neighbour v = hop1[i, a], earlier than tq[i]; empty
+    first-hop entries give empty second hops; rows follow the entries."""
+    rng = np.random.default_rng(31)
+    N, s, E = 60, 5, 3000
+    src, dst, t = random_stream(rng, N, E, 10**5)
+    o = Oracle(N, s, 0.5, seed=8)
+    o.insert(src, dst, t)
+    nfeat = rng.integers(0, 2**16, (N, 3)).astype(np.uint16)
+    nodes = rng.integers(0, N, 200).astype(np.int32)
+    tq = rng.integers(0, 10**5, 200).astype(np.uint32)
+    first = o.sample(nodes, tq, want=("nbr",))["nbr"]
+    out = o.sample_hop2(first, tq, nfeat=nfeat, want=("nbr", "eid", "ts", "nfeat", "self"))
+    for i in range(200):
+        for a in range(s):
+            v = first[i, a]
+            if v < 0:
+                assert (out["nbr"][i, a] == -1).all() and not out["self"][i, a].any()
+                continue
+            np.testing.assert_array_equal(out["self"][i, a], nfeat[v])
+            for c in range(s):
+                x = out["nbr"][i, a, c]
+                if x < 0:
+                    continue
+                e_ = out["eid"][i, a, c]
+                assert {int(src[e_]), int(dst[e_])} == {int(v), int(x)}
+                assert out["ts"][i, a, c] == t[e_] < tq[i]
+                np.testing.assert_array_equal(out["nfeat"][i, a, c], nfeat[x])
