@@ -15,6 +15,7 @@ in the C source:
 * ``sample``    -- eq. (1) strict ``t' < t`` mask; Sec. 4.4 retrieval of
                    neighbour, link-feature and self rows; App. C T-encoding
 * ``sample_hop2`` -- Sec. 4.4 second-hop neighbours: S_v^t of each stored v
+* ``aggregate`` -- eq. (4): attention over the retrieved neighbours, fp64
 """
 from __future__ import annotations
 
@@ -79,6 +80,9 @@ def _load():
     lib.orc_sample_hop2.restype = ctypes.c_int
     lib.orc_sample_hop2.argtypes = [P, P, P, i64, i32, P, P, P, i64, P, i64,
                                     P, P, P, P, P, P, P]
+    lib.orc_aggregate.restype = ctypes.c_int
+    lib.orc_aggregate.argtypes = [P, P, P, i64, i32, P, P, P, i32, i32, P, i32, i32, i32,
+                                  P, P, P, P, P, P, P, P, P, P]
     lib.orc_tenc.argtypes = [P, i64, i32, P, P, P]
     _lib = lib
     return lib
@@ -250,6 +254,36 @@ class Oracle:
         if rc != 0:
             raise ValueError("oracle: first-hop neighbour out of range")
         return out
+
+
+    def aggregate(self, node, tq, w, b, efeat, nfeat, weights):
+        """Eq. (4) attention aggregation (forward, fp64) for queries
+        (node[i], tq[i]); ``weights`` holds w1, b1, w2, b2, att, w3, b3, w4, b4
+        (bf16 matrices as uint16 bits in the padded layouts of
+        nlb_oracle.c).  ``efeat``/``nfeat``: 2-D float32 or bf16-bits (uint16)
+        arrays or None.  Returns z [nq, H] (float64)."""
+        node, tq = _c(node, np.int32), _c(tq, np.uint32)
+        w, b = _c(w, np.float32), _c(b, np.float32)
+        H = int(weights["b1"].shape[0])
+
+        def feat(a):
+            if a is None:
+                return None, 0, 1
+            a = np.ascontiguousarray(a)
+            return a, a.shape[1], (0 if a.dtype == np.float32 else 1)
+        ef, e_dim, e_dt = feat(efeat)
+        nf, n_dim, n_dt = feat(nfeat)
+        W = {k: np.ascontiguousarray(weights[k], np.uint16 if k[0] == "w" and k != "att" else np.float32)
+             for k in ("w1", "b1", "w2", "b2", "att", "w3", "b3", "w4", "b4")}
+        z = np.empty((len(node), H), np.float64)
+        rc = self._lib.orc_aggregate(
+            self._h, _ptr(node), _ptr(tq), len(node), len(w), _ptr(w), _ptr(b),
+            _ptr(ef), e_dim, e_dt, _ptr(nf), n_dim, n_dt, H,
+            _ptr(W["w1"]), _ptr(W["b1"]), _ptr(W["w2"]), _ptr(W["b2"]), _ptr(W["att"]),
+            _ptr(W["w3"]), _ptr(W["b3"]), _ptr(W["w4"]), _ptr(W["b4"]), _ptr(z))
+        if rc != 0:
+            raise ValueError("oracle: query node out of range")
+        return z
 
 
 def tenc(dt, w, b):

@@ -23,7 +23,8 @@
  *   - Sec. 4.4 and App. C: a query (u, t) returns the stored neighbours, their
  *     link features, the neighbours' own feature rows, the self row and a
  *     cosine time encoding of t - t'.  Second-hop neighbours of u are the
- *     entries of S_v^t for the stored neighbours v of u.
+ *     entries of S_v^t for the stored neighbours v of u.  Eq. (4) aggregates
+ *     the retrieved neighbours with attention into the representation Z_u.
  *
  * Random draws: the replacement coin of offer (e, k) (k = 0 for the S_u
  * offer, k = 1 for the S_v offer) is the high 32 bits of output number
@@ -297,6 +298,137 @@ int orc_sample_hop2(const orc *o, const int32_t *hop1_nbr, const uint32_t *tq, i
         }
     }
     return 0;
+}
+
+/* Value of element c of a feature row stored as fp32 (dtype 0) or bf16 (1). */
+static double feat_value(const uint8_t *row, int32_t dtype, int64_t c)
+{
+    if (dtype == 0) {
+        float f;
+        memcpy(&f, row + 4 * c, 4);
+        return (double)f;
+    }
+    uint16_t h;
+    memcpy(&h, row + 2 * c, 2);
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return (double)f;
+}
+
+static double bf16_value(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return (double)f;
+}
+
+static int64_t pad32(int64_t d) { return (d + 31) / 32 * 32; }
+
+/* out[j] = sum_k W[j][col0 + k] * x[k] + bias[j], j < rows, k < n (W: bf16 with
+ * row length ld). */
+static void affine(const uint16_t *W, int64_t ld, int64_t col0, const float *bias,
+                   const double *x, int64_t n, int64_t rows, double *out)
+{
+    for (int64_t j = 0; j < rows; j++) {
+        double acc = 0.0;
+        for (int64_t k = 0; k < n; k++) acc += bf16_value(W[j * ld + col0 + k]) * x[k];
+        out[j] = acc + (double)bias[j];
+    }
+}
+
+/*
+ * Attention aggregation of eq. (4) (Sec. 4.4), forward, in double:
+ *   Z_u = MLP_out(r_u, sum_i alpha_i MLP_in(r_v, e, t')),
+ *   {alpha_i} = softmax({w^T MLP_in(r_v, e, t')}) over the valid slots of S_u^t,
+ * with MLP(x) = W_b ReLU(W_a x + b_a) + b_b.  The neighbour status r_v is its
+ * node-feature row, e the stored link's feature row and t' enters through the
+ * T-encoding of tq - t' (as in orc_sample); r_u is the query node's row.
+ * A query with no valid slot aggregates the zero vector.
+ * Weights are bf16 (uint16 bits) in row-major [H][K] layouts whose input
+ * segments are each zero-padded to a multiple of 32 columns:
+ *   w1: [H][pad32(n_dim) + pad32(e_dim) + pad32(d_t)]  (r_v | e | T-enc)
+ *   w2: [H][H]; w3: [H][pad32(n_dim) + H]  (r_u | aggregate); w4: [H][H]
+ * Biases and att (the vector w) are fp32 [H].  Feature dtypes: 0 fp32, 1 bf16.
+ * z_out is [nq][H].  Returns -1 on an out-of-range query node.
+ */
+int orc_aggregate(const orc *o, const int32_t *node, const uint32_t *tq, int64_t nq,
+                  int32_t d_t, const float *w, const float *b,
+                  const uint8_t *efeat, int32_t e_dim, int32_t e_dtype,
+                  const uint8_t *nfeat, int32_t n_dim, int32_t n_dtype,
+                  int32_t H, const uint16_t *w1, const float *b1, const uint16_t *w2,
+                  const float *b2, const float *att, const uint16_t *w3, const float *b3,
+                  const uint16_t *w4, const float *b4, double *z_out)
+{
+    const int64_t s = o->s;
+    const int64_t e_bytes = (int64_t)e_dim * (e_dtype == 0 ? 4 : 2);
+    const int64_t n_bytes = (int64_t)n_dim * (n_dtype == 0 ? 4 : 2);
+    const int64_t k1 = pad32(n_dim) + pad32(e_dim) + pad32(d_t);
+    const int64_t k3 = pad32(n_dim) + H;
+    double *x = (double *)malloc(sizeof(double) * (size_t)(n_dim + e_dim + d_t + 1));
+    double *a = (double *)malloc(sizeof(double) * (size_t)H);
+    double *h = (double *)malloc(sizeof(double) * (size_t)(s * H));
+    double *logit = (double *)malloc(sizeof(double) * (size_t)s);
+    double *y = (double *)malloc(sizeof(double) * (size_t)(n_dim + H + 1));
+    int *valid = (int *)malloc(sizeof(int) * (size_t)s);
+    int rc = 0;
+    for (int64_t i = 0; i < nq && rc == 0; i++) {
+        const int32_t n = node[i];
+        if (n < 0 || n >= o->N) { rc = -1; break; }
+        int any = 0;
+        for (int64_t sl = 0; sl < s; sl++) {
+            const size_t idx = (size_t)n * (size_t)s + (size_t)sl;
+            valid[sl] = (o->nbr[idx] != -1) && (o->ts[idx] < tq[i]);
+            if (!valid[sl]) continue;
+            any = 1;
+            const int32_t v = o->nbr[idx];
+            const uint32_t e = o->eid[idx];
+            const float dt = (float)(uint32_t)(tq[i] - o->ts[idx]);
+            /* MLP_in on x = [r_v ; e ; T-enc(tq - t')] */
+            for (int64_t c = 0; c < n_dim; c++) x[c] = feat_value(nfeat + (size_t)v * n_bytes, n_dtype, c);
+            for (int64_t c = 0; c < e_dim; c++) x[n_dim + c] = feat_value(efeat + (size_t)e * e_bytes, e_dtype, c);
+            for (int64_t c = 0; c < d_t; c++) x[n_dim + e_dim + c] = (double)tenc_value(w[c], dt, b[c]);
+            for (int64_t j = 0; j < H; j++) {
+                double acc = 0.0;
+                for (int64_t c = 0; c < n_dim; c++) acc += bf16_value(w1[j * k1 + c]) * x[c];
+                for (int64_t c = 0; c < e_dim; c++)
+                    acc += bf16_value(w1[j * k1 + pad32(n_dim) + c]) * x[n_dim + c];
+                for (int64_t c = 0; c < d_t; c++)
+                    acc += bf16_value(w1[j * k1 + pad32(n_dim) + pad32(e_dim) + c]) * x[n_dim + e_dim + c];
+                acc += (double)b1[j];
+                a[j] = acc > 0.0 ? acc : 0.0;                  /* ReLU */
+            }
+            affine(w2, H, 0, b2, a, H, H, h + sl * H);
+            double l = 0.0;                                    /* attention logit w^T h */
+            for (int64_t j = 0; j < H; j++) l += (double)att[j] * h[sl * H + j];
+            logit[sl] = l;
+        }
+        /* softmax over the valid slots, then the weighted sum */
+        for (int64_t j = 0; j < H; j++) y[n_dim + j] = 0.0;
+        if (any) {
+            double m = -INFINITY, den = 0.0;
+            for (int64_t sl = 0; sl < s; sl++) if (valid[sl] && logit[sl] > m) m = logit[sl];
+            for (int64_t sl = 0; sl < s; sl++) if (valid[sl]) den += exp(logit[sl] - m);
+            for (int64_t sl = 0; sl < s; sl++) {
+                if (!valid[sl]) continue;
+                const double alpha = exp(logit[sl] - m) / den;
+                for (int64_t j = 0; j < H; j++) y[n_dim + j] += alpha * h[sl * H + j];
+            }
+        }
+        /* MLP_out on y = [r_u ; aggregate] */
+        for (int64_t c = 0; c < n_dim; c++) y[c] = feat_value(nfeat + (size_t)n * n_bytes, n_dtype, c);
+        for (int64_t j = 0; j < H; j++) {
+            double acc = 0.0;
+            for (int64_t c = 0; c < n_dim; c++) acc += bf16_value(w3[j * k3 + c]) * y[c];
+            for (int64_t c = 0; c < H; c++) acc += bf16_value(w3[j * k3 + pad32(n_dim) + c]) * y[n_dim + c];
+            acc += (double)b3[j];
+            a[j] = acc > 0.0 ? acc : 0.0;
+        }
+        affine(w4, H, 0, b4, a, H, H, z_out + i * H);
+    }
+    free(x); free(a); free(h); free(logit); free(y); free(valid);
+    return rc;
 }
 
 /* Stand-alone T-encoding of a list of gaps, for direct checks of App. C. */

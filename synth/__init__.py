@@ -364,3 +364,42 @@ def time_params(w: Workload):
     rng = np.random.default_rng(w.time_seed)
     phase = rng.uniform(-np.pi, np.pi, d).astype(np.float32)
     return freq, phase
+
+
+# ----------------------------------------------------------------------------- eq. (4) weights
+AGG_HIDDEN = 64
+
+
+def _pad32(d):
+    return (d + 31) // 32 * 32
+
+
+def _to_bf16_bits(x):
+    bits = np.ascontiguousarray(x, np.float32).view(np.uint32).astype(np.uint64)
+    return ((bits + 0x7FFF + ((bits >> 16) & 1)) >> 16).astype(np.uint16)   # nearest even
+
+
+def agg_weights(w: Workload, hidden: int = AGG_HIDDEN, seed: int | None = None):
+    """Random weights of the attention aggregation of eq. (4): bf16 matrices
+    (uint16 bits) in the padded layouts the library and the oracle take --
+    w1 [H][pad32(node_dim) + pad32(edge_dim) + pad32(d_time)] for (r_v | e |
+    T-enc), w2 [H][H], w3 [H][pad32(node_dim) + H] for (r_u | aggregate),
+    w4 [H][H] -- with zero pad columns; fp32 biases and attention vector.
+    Entries ~ N(0, 1/fan_in), biases ~ U(-0.1, 0.1)."""
+    rng = np.random.default_rng(5000 + w.key if seed is None else seed)
+    H, dn, de, dt = hidden, w.node_dim, w.edge_dim, w.d_time
+
+    def dense(rows, segs):
+        fan = sum(segs)
+        out = np.zeros((rows, sum(_pad32(s) for s in segs)), np.float32)
+        col = 0
+        for sgl in segs:
+            out[:, col:col + sgl] = rng.normal(0.0, 1.0 / np.sqrt(max(fan, 1)), (rows, sgl))
+            col += _pad32(sgl)
+        return _to_bf16_bits(out)
+
+    def vec(n, lo=-0.1, hi=0.1):
+        return rng.uniform(lo, hi, n).astype(np.float32)
+    return {"w1": dense(H, [dn, de, dt]), "b1": vec(H), "w2": dense(H, [H]), "b2": vec(H),
+            "att": rng.normal(0.0, 1.0 / np.sqrt(H), H).astype(np.float32),
+            "w3": dense(H, [dn, H]), "b3": vec(H), "w4": dense(H, [H]), "b4": vec(H)}

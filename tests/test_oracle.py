@@ -563,3 +563,97 @@ def test_hop2_entries_are_neighbours_of_neighbours():
                 assert {int(src[e_]), int(dst[e_])} == {int(v), int(x)}
                 assert out["ts"][i, a, c] == t[e_] < tq[i]
                 np.testing.assert_array_equal(out["nfeat"][i, a, c], nfeat[x])
+
+
+# ----------------------------------------------------------------------------- eq. (4)
+def _unit_weights(H, k1, k3):
+    z = lambda *shape: np.zeros(shape, np.float32)
+    return {"w1": z(H, k1), "b1": z(H), "w2": z(H, H), "b2": z(H), "att": z(H),
+            "w3": z(H, k3), "b3": z(H), "w4": z(H, H), "b4": z(H)}
+
+
+def _bits(wd):
+    import synth
+    return {k: (synth._to_bf16_bits(v) if k[0] == "w" else v) for k, v in wd.items()}
+
+
+def test_aggregate_handworked_two_slots():
+    """Eq. (4) by hand, H = 1: node 0 stores neighbours 1 (status 0) and 2
+    (status 1).  MLP_in passes the status through (W1 = 1 on r_v, ReLU,
+    W2 = 1) and the attention vector is 1, so the logits are 0 and 1 and
+    alpha = (1, e)/(1+e); the aggregate is e/(1+e).  MLP_out computes
+    ReLU(2*agg - 1) + 0.5 = tanh(1/2) + 0.5.  With no valid slot the
+    aggregate is 0 and Z = 0 + 0.5."""
+    o = Oracle(3, 2, 1.0, seed=0, q1=5, q2=2)
+    o.insert([0, 0], [1, 2], [1, 2])          # slots (5+2)%2 = 1 and (10+4)%2 = 0
+    nbr, _, _ = o.export()
+    assert sorted(nbr[0].tolist()) == [1, 2]
+    wd = _unit_weights(1, 64, 33)             # r_v in column 0, T-enc in column 32
+    wd["w1"][0, 0] = 1.0
+    wd["w2"][0, 0] = 1.0
+    wd["att"][0] = 1.0
+    wd["w3"][0, 32] = 2.0                     # coefficient of the aggregate
+    wd["b3"][0] = -1.0
+    wd["w4"][0, 0] = 1.0
+    wd["b4"][0] = 0.5
+    nfeat = np.array([[7.0], [0.0], [1.0]], np.float32)
+    w = np.zeros(1, np.float32)
+    b = np.zeros(1, np.float32)
+    z = o.aggregate([0, 0], [5, 0], w, b, None, nfeat, _bits(wd))
+    assert abs(z[0, 0] - (math.tanh(0.5) + 0.5)) < 1e-12
+    assert z[1, 0] == 0.5
+
+
+def test_aggregate_is_a_set_function():
+    """Eq. (4) sums over the set S_u^t: two tables holding the same entries
+    in different slots (different hash constants, no collisions) give the
+    same Z."""
+    import synth
+    rng = np.random.default_rng(3)
+    N, s, E = 400, 64, 120
+    src = rng.integers(0, 20, E).astype(np.int32)
+    dst = rng.integers(20, N, E).astype(np.int32)
+    t = np.sort(rng.choice(10**6, E, replace=False)).astype(np.uint32)
+    w = synth.scaled(synth.workload(3), 10)
+    W = synth.agg_weights(w)
+    nf = rng.integers(0, 2**15, (N, w.node_dim)).astype(np.uint16) & 0x3FFF   # finite bf16
+    fw, fb = synth.time_params(w)
+    zs, sets, slots = [], [], []
+    for q1, q2 in ((1000000007, 998244353), (999999937, 1000000009 % (2**31))):
+        o = Oracle(N, s, 1.0, seed=1, q1=q1, q2=q2)
+        o.insert(src, dst, t)
+        nbr, ts, eid = o.export_nodes(np.arange(20, dtype=np.int32))
+        sets.append([sorted(e for e in row if e != 0xFFFFFFFF) for row in eid])
+        slots.append(eid)
+        zs.append(o.aggregate(np.arange(20), np.full(20, 10**6 + 1), fw, fb, None, nf, W))
+    same = [i for i in range(20) if sets[0][i] == sets[1][i] and len(sets[0][i]) > 1
+            and not np.array_equal(slots[0][i], slots[1][i])]
+    assert len(same) >= 3
+    np.testing.assert_allclose(zs[0][same], zs[1][same], rtol=1e-12, atol=1e-12)
+
+
+def test_aggregate_constant_messages_ignore_attention():
+    """With W2 = 0 every message is b2, so the attention weights do not
+    matter: Z is the same for every query with at least one valid slot, and
+    for queries without one it is MLP_out of a zero aggregate."""
+    import synth
+    rng = np.random.default_rng(4)
+    N, s, E = 100, 8, 2000
+    src, dst, t = random_stream(rng, N, E, 10**5)
+    w = synth.scaled(synth.workload(1), 10)
+    W = synth.agg_weights(w)
+    W["w2"] = np.zeros_like(W["w2"])
+    ef = rng.standard_normal((E, w.edge_dim)).astype(np.float32)
+    fw, fb = synth.time_params(w)
+    o = Oracle(N, s, 0.5, seed=2)
+    o.insert(src, dst, t)
+    q = rng.integers(0, N, 300).astype(np.int32)
+    tq = rng.integers(0, 2 * 10**5, 300).astype(np.uint32)
+    z = o.aggregate(q, tq, fw, fb, ef, None, W)
+    any_valid = (o.sample(q, tq, want=("nbr",))["nbr"] >= 0).any(axis=1)
+    assert any_valid.any() and (~any_valid).any()
+    np.testing.assert_allclose(z[any_valid], np.broadcast_to(z[any_valid][0], z[any_valid].shape),
+                               rtol=0, atol=1e-12)
+    np.testing.assert_allclose(z[~any_valid], np.broadcast_to(z[~any_valid][0], z[~any_valid].shape),
+                               rtol=0, atol=1e-12)
+    assert np.abs(z[any_valid][0] - z[~any_valid][0]).max() > 1e-6
