@@ -21,8 +21,10 @@ KEY_EDGE, KEY_NODE = 0, 1
 MAX_SLOTS = 1024
 
 # Symbols declared in include/nlb.h.
-ABI_SYMBOLS = ("nlb_create", "nlb_insert_batch", "nlb_sample", "nlb_sample_hop2", "nlb_destroy",
-               "nlb_get_info", "nlb_export", "nlb_status", "nlb_strerror")
+ABI_SYMBOLS = ("nlb_create", "nlb_insert_batch", "nlb_sample", "nlb_sample_hop2", "nlb_aggregate",
+               "nlb_destroy", "nlb_get_info", "nlb_export", "nlb_status", "nlb_strerror")
+AGG_HIDDEN = 64
+DTYPE_F32, DTYPE_BF16 = 0, 1
 
 
 class NLBError(RuntimeError):
@@ -46,6 +48,12 @@ class _SampleOut(ctypes.Structure):
     _fields_ = [(k, ctypes.c_void_p) for k in ("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self")]
 
 
+class _AggWeights(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("node_dtype", ctypes.c_int32),
+                ("edge_dtype", ctypes.c_int32)] + \
+               [(k, ctypes.c_void_p) for k in ("w1", "b1", "w2", "b2", "att", "w3", "b3", "w4", "b4")]
+
+
 class _Info(ctypes.Structure):
     _fields_ = [("num_nodes", ctypes.c_int64), ("s", ctypes.c_int32), ("key_mode", ctypes.c_int32),
                 ("threshold", ctypes.c_uint64), ("q1", ctypes.c_uint64), ("q2", ctypes.c_uint64),
@@ -65,6 +73,11 @@ def load_library(path: str = LIB_PATH):
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with "
                           f"`python -m paper_2402_01964_amd.build` (hipcc, gfx950)")
+    # torch ships its own HIP runtime with the same soname as the system one
+    # the library links against.  Loading torch first makes the library bind
+    # to that copy, so one runtime owns the devices, streams and allocations
+    # that torch hands to the library.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     P, I, U32, U64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64
     lib.nlb_create.argtypes = [ctypes.POINTER(_Config), ctypes.POINTER(P)]
@@ -75,6 +88,8 @@ def load_library(path: str = LIB_PATH):
     lib.nlb_sample.restype = I
     lib.nlb_sample_hop2.argtypes = [P, P, P, U32, ctypes.POINTER(_SampleOut), P]
     lib.nlb_sample_hop2.restype = I
+    lib.nlb_aggregate.argtypes = [P, P, P, U32, ctypes.POINTER(_AggWeights), P, P]
+    lib.nlb_aggregate.restype = I
     lib.nlb_destroy.argtypes = [P]
     lib.nlb_destroy.restype = I
     lib.nlb_get_info.argtypes = [P, ctypes.POINTER(_Info)]
@@ -225,6 +240,32 @@ class Table:
         out = self.alloc_outputs(nq * self.s, want)
         self.sample_hop2_into(hop1_nbr, tq, out, stream)
         return {k: v.view(nq, self.s, *v.shape[1:]) for k, v in out.items()}
+
+    def aggregate(self, node, tq, weights: dict, out=None, stream=None):
+        """Eq. (4) attention aggregation for queries (node[i], tq[i]).
+        ``weights``: device tensors w1..w4 (bf16, or 16-bit ints holding bf16
+        bits, padded layouts of include/nlb.h) and b1..b4, att (fp32).
+        Returns (or fills) z, fp32 [nq, AGG_HIDDEN]."""
+        import torch
+        nq = int(node.numel())
+        if tq.numel() != nq:
+            raise ValueError("node and tq must have the same length")
+        aw = _AggWeights()
+        aw.hidden = AGG_HIDDEN
+
+        def dt(feat):
+            return DTYPE_F32 if feat is None or feat.dtype == torch.float32 else DTYPE_BF16
+        aw.node_dtype, aw.edge_dtype = dt(self.node_feat), dt(self.edge_feat)
+        for k in ("w1", "w2", "w3", "w4"):
+            setattr(aw, k, _dev_ptr(weights[k], 2, k))
+        for k in ("b1", "b2", "b3", "b4", "att"):
+            setattr(aw, k, _dev_ptr(weights[k], 4, k))
+        if out is None:
+            out = torch.empty((nq, AGG_HIDDEN), dtype=torch.float32, device=node.device)
+        _check(self._lib.nlb_aggregate(self._h, _dev_ptr(node, 4, "node"), _dev_ptr(tq, 4, "tq"), nq,
+                                       ctypes.byref(aw), _dev_ptr(out, 4, "z"), _stream_ptr(stream)),
+               "nlb_aggregate")
+        return out
 
     def alloc_outputs(self, nq: int, want=("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self")):
         import torch

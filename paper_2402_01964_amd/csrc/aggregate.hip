@@ -1,0 +1,463 @@
+// aggregate.hip -- the attention aggregation of eq. (4) (Luo & Li, arXiv
+// 2402.01964, Sec. 4.4) fused with retrieval:
+//   Z_u = MLP_out(r_u, sum_i alpha_i MLP_in(r_v, e, t')),
+//   {alpha_i} = softmax({w^T MLP_in(r_v, e, t')}) over the valid slots of S_u^t,
+// MLP(x) = W_b ReLU(W_a x + b_a) + b_b.  The retrieved rows and the time
+// encoding never leave the chip: a workgroup reads its tile's table slots,
+// builds the inputs in LDS and runs the four layers on bf16 matrix cores.
+//
+// Numerics.  Every activation is fp32 and enters a matrix product as a pair
+// of bf16 terms, hi = bf16(v) and lo = bf16(v - hi), which represent v to
+// 2^-18 relative; both terms multiply the same bf16 weights and accumulate
+// in fp32 (v_mfma_f32_16x16x32_bf16).  Inputs that are bf16 already (bf16
+// feature rows) have lo = 0, and their lo products are skipped.
+//
+// MFMA operand layout (v_mfma_f32_16x16x32_bf16, checked on gfx950): lane l
+// holds A[l % 16][8 (l / 16) + i], B[8 (l / 16) + i][l % 16] for i < 8, and
+// D[4 (l / 16) + i][l % 16] for i < 4.  A is a 16-row block of activations
+// in LDS (rows padded so 16-byte lane reads fall on distinct banks); B is a
+// 32 x 16 block of a weight matrix read straight from global memory, whose
+// rows (one per output column) are K-contiguous, so each lane reads 16
+// consecutive bytes.  Each of the four wavefronts owns 16 of the 64 output
+// columns and all row blocks of the tile.
+#include <cstring>
+
+#include "nlb_internal.h"
+
+namespace {
+
+constexpr int kAggThreads = 256;
+constexpr int kH = NLB_AGG_HIDDEN;      // hidden and output width
+constexpr int kHs = kH + 8;             // bf16 row stride of 64-wide activations in LDS
+constexpr int kHf = kH + 4;             // fp32 row stride of the messages in LDS
+constexpr int kMaxBlocks = 8;           // row blocks of 16: at most 128 slot rows per tile
+constexpr uint32_t kAggLdsBudget = 160 * 1024;   // gfx950: 160 KB of LDS per workgroup
+constexpr uint32_t kAggTargetTiles = 2048;
+static_assert(kH == 64, "the kernel maps four wavefronts onto 64 output columns");
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+struct AggParams {
+    const uint8_t *blocks;
+    uint32_t block_bytes;
+    uint32_t s;
+    int64_t num_nodes;
+    const int32_t *node;
+    const uint32_t *tq;
+    uint32_t nq;
+    uint32_t tile_q;      // queries per tile
+    uint32_t rows;        // slot rows per tile, padded to 16
+    uint32_t qrows;       // query rows per tile, padded to 16
+    uint64_t s_m;         // ceil(2^40 / s)
+    uint32_t d_time;
+    const float *w;
+    const float *b;
+    const uint8_t *efeat;
+    int64_t edge_rows;
+    uint32_t e_dim, e_bf16, erb, e_vec;
+    const uint8_t *nfeat;
+    uint32_t n_dim, n_bf16, nrb, n_vec;
+    uint32_t k1, off_e, off_t, k3;   // padded widths of w1 / w3 and segment offsets in w1
+    uint32_t xs, ys;                 // LDS row strides (bf16 elements) of X and Y
+    uint64_t g1_m, gq_m;             // ceil(2^40 / (k1 / 8)), ceil(2^40 / (pad32(n_dim) / 8))
+    uint32_t region_off, off_h, off_y, off_a3;
+    const __bf16 *w1, *w2, *w3, *w4;
+    const float *b1, *b2, *b3, *b4, *att;
+    float *z;
+    uint32_t *status;
+};
+
+__device__ __forceinline__ float bf16_bits_to_float(uint32_t bits) {
+    return __uint_as_float(bits << 16);
+}
+
+// Eight consecutive elements c0..c0+7 of a feature row (fp32 or bf16);
+// elements at or beyond `dim` read as zero.
+__device__ __forceinline__ void load8(const uint8_t *row, uint32_t dim, uint32_t is_bf16,
+                                      uint32_t vec_ok, uint32_t c0, float v[8]) {
+    if (vec_ok && c0 + 8 <= dim) {
+        if (is_bf16) {
+            const u32x4 q = *(const u32x4 *)(row + 2 * c0);
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                v[2 * i] = bf16_bits_to_float(q[i] & 0xFFFFu);
+                v[2 * i + 1] = bf16_bits_to_float(q[i] >> 16);
+            }
+        } else {
+            const f32x4 a = *(const f32x4 *)(row + 4 * c0);
+            const f32x4 b = *(const f32x4 *)(row + 4 * c0 + 16);
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                v[i] = a[i];
+                v[4 + i] = b[i];
+            }
+        }
+        return;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+        const uint32_t c = c0 + i;
+        v[i] = 0.0f;
+        if (c < dim)
+            v[i] = is_bf16 ? bf16_bits_to_float(((const uint16_t *)row)[c]) : ((const float *)row)[c];
+    }
+}
+
+// Store v as its bf16 pair (hi + lo) at hi[0..7] and lo[0..7] (16 bytes each).
+__device__ __forceinline__ void store_split8(const float v[8], __bf16 *hi, __bf16 *lo) {
+    bf16x8 h, l;
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+        const __bf16 t = (__bf16)v[i];
+        h[i] = t;
+        l[i] = (__bf16)(v[i] - (float)t);
+    }
+    *(bf16x8 *)hi = h;
+    *(bf16x8 *)lo = l;
+}
+
+__device__ __forceinline__ void store_split1(float v, __bf16 *hi, __bf16 *lo) {
+    const __bf16 t = (__bf16)v;
+    *hi = t;
+    *lo = (__bf16)(v - (float)t);
+}
+
+// acc[rb] += A_rb (16 x K, from the LDS pair Ah/Al with row stride `as`)
+//          * W^T (K x 16 columns col0.., W row-major [64][ld]) for rb < nrb.
+// lo products are skipped on K ranges whose lo terms are all zero.
+template <typename NeedLo>
+__device__ __forceinline__ void mfma_rows(f32x4 (&acc)[kMaxBlocks], uint32_t nrb, const __bf16 *Ah,
+                                          const __bf16 *Al, uint32_t as, const __bf16 *W,
+                                          uint32_t ld, uint32_t K, uint32_t col0, uint32_t lane,
+                                          NeedLo need_lo) {
+    const uint32_t lr = lane & 15, lk = (lane >> 4) * 8;
+    const __bf16 *wrow = W + (size_t)(col0 + lr) * ld + lk;
+    for (uint32_t k0 = 0; k0 < K; k0 += 32) {
+        const bf16x8 bv = *(const bf16x8 *)(wrow + k0);
+        const bool lo = need_lo(k0);
+#pragma unroll
+        for (int rb = 0; rb < kMaxBlocks; rb++) {
+            if ((uint32_t)rb < nrb) {
+                const uint32_t off = (16u * rb + lr) * as + k0 + lk;
+                acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8 *)(Ah + off), bv,
+                                                                  acc[rb], 0, 0, 0);
+                if (lo)
+                    acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8 *)(Al + off),
+                                                                      bv, acc[rb], 0, 0, 0);
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void zero_acc(f32x4 (&acc)[kMaxBlocks]) {
+#pragma unroll
+    for (int rb = 0; rb < kMaxBlocks; rb++) acc[rb] = f32x4(0.0f);
+}
+
+__global__ __launch_bounds__(kAggThreads) void aggregate_fused(AggParams p) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    SlotLds *slots = (SlotLds *)smem;
+    int32_t *tnodes = (int32_t *)(smem + 16u * p.rows);
+    uint8_t *region = smem + p.region_off;
+    __bf16 *Xh = (__bf16 *)region;
+    __bf16 *Xl = Xh + (size_t)p.rows * p.xs;
+    __bf16 *A1h = (__bf16 *)region;                 // after layer 1 (X consumed)
+    __bf16 *A1l = A1h + (size_t)p.rows * kHs;
+    float *Hf = (float *)(region + p.off_h);
+    float *logit = Hf + (size_t)p.rows * kHf;
+    __bf16 *Yh = (__bf16 *)(region + p.off_y);
+    __bf16 *Yl = Yh + (size_t)p.qrows * p.ys;
+    __bf16 *A3h = (__bf16 *)(region + p.off_a3);
+    __bf16 *A3l = A3h + (size_t)p.qrows * kHs;
+
+    const uint32_t tid = threadIdx.x;
+    const uint32_t lane = tid & 63, wave = tid >> 6;
+    const uint64_t q0 = (uint64_t)blockIdx.x * p.tile_q;
+    const uint32_t nqt = (uint32_t)min((uint64_t)p.tile_q, (uint64_t)p.nq - q0);
+    const uint32_t s = p.s;
+    const uint32_t ns = nqt * s;
+    const uint32_t col = 16u * wave + (lane & 15);   // output column of this lane
+
+    // Phase 1: table slots of the tile (eq. (1) strict mask).
+    for (uint32_t j = tid; j < p.rows; j += kAggThreads) {
+        SlotLds sl = {-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
+        if (j < ns) {
+            const uint32_t ql = div_small(j, p.s_m);
+            const uint32_t a = j - ql * s;
+            const int32_t node = p.node[q0 + ql];
+            const bool in_range = node >= 0 && (int64_t)node < p.num_nodes;
+            if (in_range)
+                sl = read_slot(p.blocks, p.block_bytes, s, node, a, p.tq[q0 + ql]);
+            else if (a == 0)
+                atomicOr(p.status, kStatusRange);
+            if (a == 0) tnodes[ql] = in_range ? node : -1;
+        }
+        slots[j] = sl;
+    }
+    __syncthreads();
+
+    // Phase 2: MLP_in inputs x = [r_v | e | T-enc(tq - t')], hi/lo pairs.
+    const uint32_t g1 = p.k1 / 8;
+    for (uint32_t u = tid; u < p.rows * g1; u += kAggThreads) {
+        const uint32_t j = div_small(u, p.g1_m);
+        const uint32_t c0 = (u - j * g1) * 8;
+        const SlotLds sl = slots[j];
+        float v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (sl.x >= 0) {
+            if (c0 < p.off_e) {
+                load8(p.nfeat + (size_t)sl.x * p.nrb, p.n_dim, p.n_bf16, p.n_vec, c0, v);
+            } else if (c0 < p.off_t) {
+                if ((int64_t)sl.e < p.edge_rows)
+                    load8(p.efeat + (size_t)sl.e * p.erb, p.e_dim, p.e_bf16, p.e_vec, c0 - p.off_e, v);
+            } else {
+                const uint32_t k = c0 - p.off_t;
+#pragma unroll
+                for (int i = 0; i < 8; i++)
+                    if (k + i < p.d_time)
+                        v[i] = cos_fp32(__builtin_fmaf(p.w[k + i], sl.dt, p.b[k + i]));
+            }
+        }
+        store_split8(v, Xh + (size_t)j * p.xs + c0, Xl + (size_t)j * p.xs + c0);
+    }
+    __syncthreads();
+
+    const uint32_t nrb = p.rows / 16;
+    const uint32_t nqb = p.qrows / 16;
+    f32x4 acc[kMaxBlocks];
+
+    // Layer 1: a1 = ReLU(W1 x + b1).
+    zero_acc(acc);
+    {
+        const uint32_t off_e = p.off_e, off_t = p.off_t, nb = p.n_bf16, eb = p.e_bf16;
+        mfma_rows(acc, nrb, Xh, Xl, p.xs, p.w1, p.k1, p.k1, 16u * wave, lane,
+                  [=](uint32_t k0) { return k0 < off_e ? !nb : (k0 < off_t ? !eb : true); });
+    }
+    __syncthreads();   // X is consumed; A1 reuses its space
+    {
+        const float bias = p.b1[col];
+#pragma unroll
+        for (int rb = 0; rb < kMaxBlocks; rb++)
+            if ((uint32_t)rb < nrb)
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const uint32_t row = 16u * rb + 4u * (lane >> 4) + i;
+                    store_split1(fmaxf(acc[rb][i] + bias, 0.0f), A1h + row * kHs + col,
+                                 A1l + row * kHs + col);
+                }
+    }
+    __syncthreads();
+
+    // Layer 2: messages h = W2 a1 + b2 (fp32 in LDS).
+    zero_acc(acc);
+    mfma_rows(acc, nrb, A1h, A1l, kHs, p.w2, kH, kH, 16u * wave, lane,
+              [](uint32_t) { return true; });
+    {
+        const float bias = p.b2[col];
+#pragma unroll
+        for (int rb = 0; rb < kMaxBlocks; rb++)
+            if ((uint32_t)rb < nrb)
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const uint32_t row = 16u * rb + 4u * (lane >> 4) + i;
+                    Hf[row * kHf + col] = acc[rb][i] + bias;
+                }
+    }
+    __syncthreads();
+
+    // Attention logits w^T h of the valid slots.
+    for (uint32_t j = tid; j < p.rows; j += kAggThreads) {
+        float l = 0.0f;
+        if (slots[j].x >= 0) {
+            const float *h = Hf + j * kHf;
+#pragma unroll 8
+            for (int n = 0; n < kH; n++) l = __builtin_fmaf(p.att[n], h[n], l);
+        }
+        logit[j] = l;
+    }
+    __syncthreads();
+
+    // MLP_out inputs y = [r_u | softmax-weighted sum of the messages].
+    const uint32_t kn = p.k3 - kH;   // pad32(node_dim)
+    for (uint32_t t = tid; t < p.qrows * kH; t += kAggThreads) {
+        const uint32_t q = t / kH, n = t % kH;
+        float value = 0.0f;
+        if (q < nqt) {
+            const uint32_t base = q * s;
+            float m = -INFINITY;
+            for (uint32_t a = 0; a < s; a++)
+                if (slots[base + a].x >= 0) m = fmaxf(m, logit[base + a]);
+            if (m > -INFINITY) {
+                float den = 0.0f, num = 0.0f;
+                for (uint32_t a = 0; a < s; a++) {
+                    if (slots[base + a].x < 0) continue;
+                    const float ex = expf(logit[base + a] - m);
+                    den += ex;
+                    num = __builtin_fmaf(ex, Hf[(base + a) * kHf + n], num);
+                }
+                value = num / den;
+            }
+        }
+        store_split1(value, Yh + q * p.ys + kn + n, Yl + q * p.ys + kn + n);
+    }
+    if (kn) {
+        const uint32_t gq = kn / 8;
+        for (uint32_t u = tid; u < p.qrows * gq; u += kAggThreads) {
+            const uint32_t q = div_small(u, p.gq_m);
+            const uint32_t c0 = (u - q * gq) * 8;
+            float v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            if (q < nqt && tnodes[q] >= 0)
+                load8(p.nfeat + (size_t)tnodes[q] * p.nrb, p.n_dim, p.n_bf16, p.n_vec, c0, v);
+            store_split8(v, Yh + q * p.ys + c0, Yl + q * p.ys + c0);
+        }
+    }
+    __syncthreads();
+
+    // Layer 3: a3 = ReLU(W3 y + b3).
+    zero_acc(acc);
+    {
+        const uint32_t nb = p.n_bf16;
+        mfma_rows(acc, nqb, Yh, Yl, p.ys, p.w3, p.k3, p.k3, 16u * wave, lane,
+                  [=](uint32_t k0) { return k0 < kn ? !nb : true; });
+        const float bias = p.b3[col];
+#pragma unroll
+        for (int rb = 0; rb < kMaxBlocks; rb++)
+            if ((uint32_t)rb < nqb)
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const uint32_t row = 16u * rb + 4u * (lane >> 4) + i;
+                    store_split1(fmaxf(acc[rb][i] + bias, 0.0f), A3h + row * kHs + col,
+                                 A3l + row * kHs + col);
+                }
+    }
+    __syncthreads();
+
+    // Layer 4: Z = W4 a3 + b4.
+    zero_acc(acc);
+    mfma_rows(acc, nqb, A3h, A3l, kHs, p.w4, kH, kH, 16u * wave, lane,
+              [](uint32_t) { return true; });
+    {
+        const float bias = p.b4[col];
+#pragma unroll
+        for (int rb = 0; rb < kMaxBlocks; rb++)
+            if ((uint32_t)rb < nqb)
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const uint32_t row = 16u * rb + 4u * (lane >> 4) + i;
+                    if (row < nqt) p.z[(q0 + row) * kH + col] = acc[rb][i] + bias;
+                }
+    }
+}
+
+uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u; }
+uint32_t pad32(uint32_t x) { return (x + 31u) & ~31u; }
+uint32_t align16(uint32_t x) { return (x + 15u) & ~15u; }
+
+// LDS layout of a tile with `rows` slot rows and `qrows` query rows.
+uint32_t agg_layout(AggParams &p, uint32_t rows, uint32_t qrows) {
+    p.rows = rows;
+    p.qrows = qrows;
+    p.region_off = align16(16u * rows + 4u * qrows);
+    const uint32_t x_bytes = 2u * rows * p.xs * 2u;
+    p.off_h = rows * kHs * 2u * 2u;
+    p.off_y = align16(p.off_h + rows * kHf * 4u + rows * 4u);
+    p.off_a3 = align16(p.off_y + 2u * qrows * p.ys * 2u);
+    const uint32_t late = p.off_a3 + 2u * qrows * kHs * 2u;
+    return p.region_off + (x_bytes > late ? x_bytes : late);
+}
+
+}  // namespace
+
+extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t nq,
+                             const nlb_agg_weights *wts, float *z, void *stream) {
+    if (!h || !wts) return NLB_EINVAL;
+    if (nq == 0) return NLB_OK;
+    if (!node || !tq || !z) return NLB_EINVAL;
+    if (wts->hidden != kH || h->s > 128) return NLB_EINVAL;
+    if (!wts->w1 || !wts->w2 || !wts->w3 || !wts->w4 || !wts->b1 || !wts->b2 || !wts->b3 ||
+        !wts->b4 || !wts->att)
+        return NLB_EINVAL;
+    if (((uintptr_t)wts->w1 | (uintptr_t)wts->w2 | (uintptr_t)wts->w3 | (uintptr_t)wts->w4) % 16)
+        return NLB_EINVAL;
+    if ((uintptr_t)z % 4) return NLB_EINVAL;
+    const int32_t nd = wts->node_dtype, ed = wts->edge_dtype;
+    if ((nd != NLB_DTYPE_F32 && nd != NLB_DTYPE_BF16) || (ed != NLB_DTYPE_F32 && ed != NLB_DTYPE_BF16))
+        return NLB_EINVAL;
+    const uint32_t n_es = nd == NLB_DTYPE_BF16 ? 2 : 4, e_es = ed == NLB_DTYPE_BF16 ? 2 : 4;
+    if (h->nrb % n_es || h->erb % e_es) return NLB_EINVAL;
+    DeviceGuard guard(h->device);
+    if (!guard.ok()) return NLB_EDEVICE;
+
+    AggParams p;
+    std::memset(&p, 0, sizeof(p));
+    p.blocks = h->blocks;
+    p.block_bytes = h->block_bytes;
+    p.s = h->s;
+    p.num_nodes = h->num_nodes;
+    p.node = node;
+    p.tq = tq;
+    p.nq = nq;
+    p.s_m = ceil_2_40_div(h->s);
+    p.d_time = h->d_time;
+    p.w = h->w;
+    p.b = h->b;
+    p.efeat = h->efeat;
+    p.edge_rows = h->edge_rows;
+    p.e_dim = h->erb / e_es;
+    p.e_bf16 = ed == NLB_DTYPE_BF16;
+    p.erb = h->erb;
+    p.e_vec = h->erb % 16 == 0 && (uintptr_t)h->efeat % 16 == 0;
+    p.nfeat = h->nfeat;
+    p.n_dim = h->nrb / n_es;
+    p.n_bf16 = nd == NLB_DTYPE_BF16;
+    p.nrb = h->nrb;
+    p.n_vec = h->nrb % 16 == 0 && (uintptr_t)h->nfeat % 16 == 0;
+    p.off_e = pad32(p.n_dim);
+    p.off_t = p.off_e + pad32(p.e_dim);
+    p.k1 = p.off_t + pad32(h->d_time);
+    p.k3 = pad32(p.n_dim) + kH;
+    if (p.k1 == 0) return NLB_EINVAL;   // no inputs at all
+    p.xs = p.k1 + 8;
+    p.ys = p.k3 + 8;
+    p.g1_m = ceil_2_40_div(p.k1 / 8);
+    p.gq_m = ceil_2_40_div(pad32(p.n_dim) / 8 ? pad32(p.n_dim) / 8 : 1);
+    p.w1 = (const __bf16 *)wts->w1;
+    p.w2 = (const __bf16 *)wts->w2;
+    p.w3 = (const __bf16 *)wts->w3;
+    p.w4 = (const __bf16 *)wts->w4;
+    p.b1 = wts->b1;
+    p.b2 = wts->b2;
+    p.b3 = wts->b3;
+    p.b4 = wts->b4;
+    p.att = wts->att;
+    p.z = z;
+    p.status = h->status;
+
+    // Tile: as many queries as fit the LDS budget (at most 128 slot rows),
+    // fewer when that leaves too few workgroups to fill the GPU.
+    uint32_t tile_q = 0, lds = 0;
+    for (uint32_t rows = 128; rows >= 16; rows -= 16) {
+        const uint32_t tq_cap = rows / h->s;
+        if (tq_cap == 0) continue;
+        const uint32_t want = (uint32_t)(((uint64_t)nq + kAggTargetTiles - 1) / kAggTargetTiles);
+        const uint32_t t = tq_cap < (want ? want : 1) ? tq_cap : (want ? want : 1);
+        AggParams trial = p;
+        const uint32_t bytes = agg_layout(trial, pad16(t * h->s), pad16(t));
+        if (bytes <= kAggLdsBudget) {
+            tile_q = t;
+            lds = bytes;
+            break;
+        }
+    }
+    if (tile_q == 0) return NLB_EINVAL;   // one query does not fit the LDS budget
+    p.tile_q = tile_q;
+    agg_layout(p, pad16(tile_q * h->s), pad16(tile_q));
+    // Dynamic LDS beyond 64 KB has to be allowed per kernel before launch.
+    if (lds > 64u * 1024u &&
+        hipFuncSetAttribute((const void *)aggregate_fused, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)kAggLdsBudget) != hipSuccess)
+        return NLB_EDEVICE;
+    const dim3 grid((unsigned)((nq + tile_q - 1) / tile_q));
+    hipLaunchKernelGGL(aggregate_fused, grid, dim3(kAggThreads), lds, (hipStream_t)stream, p);
+    if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
+    return NLB_OK;
+}

@@ -1,55 +1,16 @@
 // nlb.hip -- gfx950 kernels and the C ABI (include/nlb.h) of NLB forward
-// recent sampling (Luo & Li, arXiv 2402.01964, Sec. 4.2 and Sec. 4.4).
-//
-// Table layout in HBM.  Node n owns one block of `block_bytes` bytes at
-// blocks + n * block_bytes: s 64-bit keys, then s 32-bit neighbour ids.
-// block_bytes is the smallest of 16, 32, 64, 128, 256, 384, ... that holds
-// 12*s bytes, so a block of s <= 10 sits in one 128-byte cache line and a
-// query reads its whole table with one line fetch.
-//
-// Key word (0 = empty slot):
-//   bits 63..62  class: 3 = offer whose coin passed, 1 = offer whose coin failed
-//   bits 61..30  arrival index e (class 3) or its complement ~e (class 1)
-//   bits 29..0   timestamp t (< 2^30)
-// Batch insertion must equal sequential insertion.  Sequentially, a slot
-// ends the batch holding the latest offer whose coin passed; if none passed,
-// it keeps its old entry, or, when it was empty, the first offer of the
-// batch (an empty slot always accepts).  With the encoding above this is a
-// plain unsigned maximum over the old word and all offer words: any passed
-// offer beats every class-1 word and older passed entries (larger e wins);
-// a failed offer can only win against an empty word, and among failed
-// offers the smallest e wins (largest ~e).  A stored class-1 word keeps
-// losing to later class-1 offers (smaller ~e), so stored words never need
-// rewriting.  Pass 1 (resolve) applies 64-bit atomicMax per offer; pass 2
-// (commit) lets the offer whose word survived write the neighbour id.
-#include <hip/hip_runtime.h>
-
+// recent sampling (Luo & Li, arXiv 2402.01964, Sec. 4.2 and Sec. 4.4): table
+// creation, batch insertion, first- and second-hop sampling, export.  The
+// table layout and key-word format are described in nlb_internal.h.
 #include <climits>
-#include <cmath>
-#include <cstdint>
 #include <cstring>
 #include <new>
 
-#include "../../include/nlb.h"
+#include "nlb_internal.h"
 
 namespace {
 
-constexpr uint64_t kClassPass = 3ull << 62;
-constexpr uint64_t kClassFail = 1ull << 62;
-constexpr uint32_t kTimeBits = 30;
-constexpr uint32_t kTimeMask = (1u << kTimeBits) - 1u;
-constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;  // SplitMix64 state increment
-
-// Device status words, kept after the slot blocks.
-constexpr uint32_t kStatusRange = 1u;   // node id out of range
-constexpr uint32_t kStatusOrder = 2u;   // timestamp >= 2^30 or decreasing
-constexpr size_t kStatusBytes = 256;    // [0] flags, [1..2] last timestamp per batch parity
-
 constexpr int kInsertThreads = 256;
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------- integer helpers
 // x mod d for 32-bit x and d, by Lemire, Kaser & Kurz, "Faster remainder by
@@ -59,11 +20,6 @@ __device__ __forceinline__ uint32_t fastmod_u32(uint32_t x, uint64_t M, uint32_t
     return (uint32_t)__umul64hi(low, d);
 }
 
-// floor(f / d) for f < 2^24, d < 2^16, with m = ceil(2^40 / d).
-__device__ __forceinline__ uint32_t div_small(uint32_t f, uint64_t m) {
-    return (uint32_t)(((uint64_t)f * m) >> 40);
-}
-
 // Output number n (n >= 1) of SplitMix64 started at `state0`; its mixing
 // function is the one published by Steele, Lea & Flood (OOPSLA 2014).
 __device__ __forceinline__ uint64_t splitmix64_nth(uint64_t state0, uint64_t n) {
@@ -71,30 +27,6 @@ __device__ __forceinline__ uint64_t splitmix64_nth(uint64_t state0, uint64_t n) 
     z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
     z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
     return z ^ (z >> 31);
-}
-
-// ---------------------------------------------------------------- cosine
-// Arguments beyond the fast path's range: the device libm's double cos,
-// which reduces exactly.  Kept out of line so that its registers do not
-// weigh on the kernels (time encodings never reach it in practice).
-__device__ __attribute__((noinline)) float cos_fp32_wide(float x) {
-    return (float)cos((double)x);
-}
-
-// cos of an fp32 argument.  The argument is converted to revolutions in
-// double, y = x / (2 pi), and reduced to f = y - rint(y) in [-1/2, 1/2]; for
-// |x| < 2^33 the double product leaves f within 3e-7 revolutions of exact.
-// The hardware cosine (v_cos_f32, cos(2 pi f)) then evaluates the reduced
-// fraction; measured on gfx950 over a dense grid of [-1/2, 1/2] its error is
-// below 1.3e-7, and the whole function stays below 3e-7 absolute for
-// |x| < 1e9 against a double-precision cosine.
-__device__ __forceinline__ float cos_fp32(float x) {
-    if (fabsf(x) < 8589934592.0f) {
-        const double y = (double)x * 0.15915494309189533577;
-        const float f = (float)(y - __builtin_rint(y));
-        return __builtin_amdgcn_cosf(f);
-    }
-    return cos_fp32_wide(x);
 }
 
 // ---------------------------------------------------------------- insert
@@ -295,15 +227,6 @@ struct SampleParams {
     uint64_t n_m;
 };
 
-// One staged slot: x (-1 when the slot is not valid for its query), arrival
-// index, timestamp and the fp32 gap tq - t'.
-struct SlotLds {
-    int32_t x;
-    uint32_t e;
-    uint32_t t;
-    float dt;
-};
-
 template <int W> struct VecOf;
 template <> struct VecOf<16> { typedef u32x4 T; };
 template <> struct VecOf<8> { typedef u32x2 T; };
@@ -392,17 +315,7 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
         const bool quiet = HOP2 && node < 0;   // empty first-hop slot
         SlotLds sl = {-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
         if (in_range) {
-            const uint8_t *blk = p.blocks + (size_t)node * p.block_bytes;
-            const uint64_t key = ((const uint64_t *)blk)[a];
-            const int32_t xv = ((const int32_t *)(blk + 8u * s))[a];
-            const uint32_t t = (uint32_t)key & kTimeMask;
-            if (key != 0 && t < tq) {
-                const uint32_t ef = (uint32_t)(key >> kTimeBits);
-                sl.x = xv;
-                sl.e = ((key >> 62) == 3u) ? ef : ~ef;
-                sl.t = t;
-                sl.dt = (float)(tq - t);
-            }
+            sl = read_slot(p.blocks, p.block_bytes, s, node, a, tq);
         } else if (a == 0 && !quiet) {
             atomicOr(p.status, kStatusRange);
         }
@@ -490,8 +403,6 @@ uint32_t block_bytes_for(uint32_t s) {
     return (need + 127u) / 128u * 128u;
 }
 
-uint64_t ceil_2_40_div(uint32_t d) { return ((1ull << 40) + d - 1) / d; }
-
 // Queries per sample tile.  Large launches use as many queries as fit
 // kTileSlots slot rows; smaller ones shrink the tile until the launch has
 // about kTargetTiles workgroups, so that every CU gets work.  Tiles of 32
@@ -509,57 +420,7 @@ uint32_t tile_queries(uint32_t s, uint32_t nq) {
     return want < cap ? want : cap;
 }
 
-class DeviceGuard {
-  public:
-    explicit DeviceGuard(int dev) {
-        if (hipGetDevice(&prev_) != hipSuccess) prev_ = -1;
-        ok_ = hipSetDevice(dev) == hipSuccess;
-    }
-    ~DeviceGuard() {
-        if (prev_ >= 0) (void)hipSetDevice(prev_);
-    }
-    bool ok() const { return ok_; }
-
-  private:
-    int prev_ = -1;
-    bool ok_ = false;
-};
-
-// Widest copy unit (16, 8 or 4 bytes) that divides the row and keeps every
-// source and destination address aligned.
-uint32_t copy_width(uint32_t row_bytes, const void *src, const void *dst_or_null) {
-    const uintptr_t a = (uintptr_t)src | (uintptr_t)dst_or_null;
-    for (uint32_t w = 16; w >= 8; w /= 2)
-        if (row_bytes % w == 0 && a % w == 0) return w;
-    return 4;
-}
-
 }  // namespace
-
-struct nlb_table {
-    int device;
-    int64_t num_nodes;
-    uint32_t s;
-    int32_t key_mode;
-    double alpha;
-    uint64_t thr;
-    uint64_t seed;
-    uint64_t q1, q2;
-    uint32_t d_time;
-    const float *w;
-    const float *b;
-    const uint8_t *efeat;
-    int64_t edge_rows;
-    uint32_t erb;
-    const uint8_t *nfeat;
-    uint32_t nrb;
-    uint8_t *blocks;
-    size_t table_bytes;
-    uint32_t block_bytes;
-    uint32_t *status;
-    uint64_t interactions;
-    uint64_t batches;
-};
 
 extern "C" {
 

@@ -165,6 +165,8 @@ def _load():
         return _lib
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: run synth.build()")
+    # bind to torch's HIP runtime (same soname as the system one): one runtime per process
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     P, I64, I32, U32, U64, D = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32,
                                 ctypes.c_uint64, ctypes.c_double)

@@ -98,3 +98,20 @@ def test_product_path_never_reaches_the_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 assert not re.search(r"\boracle\b", text), f
                 assert "nlb_oracle" not in text and "orc_" not in text, f
+
+
+def test_one_hip_runtime_per_process():
+    """The library and the input generator bind to torch's HIP runtime
+    whatever the import order, so torch's streams and allocations belong to
+    the same runtime as the library's kernels."""
+    import subprocess
+    import sys
+    code = (
+        "import sys; sys.path.insert(0, %r)\n"
+        "import synth; synth._load()\n"
+        "import paper_2402_01964_amd as nlb; nlb.load_library()\n"
+        "print(len(set(l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l)))\n"
+    ) % ROOT
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip() == "1"

@@ -310,3 +310,50 @@ def test_second_hop_matches_oracle(k):
         g.insert(s_, d_, t_)
         o.insert(src[lo:hi], dst[lo:hi], t[lo:hi])
     assert g.status() == 0   # empty first-hop entries are not errors
+
+
+def _agg_dev(W):
+    import torch
+    return {k: (to_dev(v.view(np.int16)) if v.dtype == np.uint16 else to_dev(v)) for k, v in W.items()}
+
+
+def agg_error(gz, oz):
+    """Max over elements of |z_gpu - z_oracle| / (|z_oracle| + rms(z_oracle))."""
+    scale = np.sqrt(np.mean(oz ** 2))
+    return float(np.max(np.abs(gz.astype(np.float64) - oz) / (np.abs(oz) + scale)))
+
+
+AGG_TOL = 2e-4   # see nlb_aggregate in include/nlb.h for the derivation
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_aggregate_matches_oracle(k):
+    """Eq. (4) forward on every workload shape (fp32 or bf16 rows, 372-byte
+    unaligned rows, s = 10 / 20 / 64) at several points of a stream prefix,
+    against the fp64 oracle; also queries with no valid slot."""
+    base = synth.workload(k)
+    w = synth.scaled(base, 12 * base.batch, num_nodes=min(base.num_nodes, 200000))
+    src, dst, t, neg = synth.host_links(w)
+    ef = synth.host_features(w, "edge") if w.edge_dim else None
+    nf = synth.host_features(w, "node") if w.node_dim else None
+    g = make_gpu_table(w, feat_to_dev(ef, w.edge_dtype) if ef is not None else None,
+                       feat_to_dev(nf, w.node_dtype) if nf is not None else None)
+    o = make_oracle(w)
+    W = synth.agg_weights(w)
+    Wd = _agg_dev(W)
+    fw, fb = synth.time_params(w)
+    worst = 0.0
+    for b in range(w.batches):
+        lo, hi = w.batch_range(b)
+        if b in (2, 7, 11):
+            q = np.concatenate([src[lo:hi], dst[lo:hi], neg[lo:hi]])[:3000]
+            tq = np.concatenate([t[lo:hi]] * 3)[:3000]
+            tq[::7] = 0                      # no valid slot for these
+            gz = g.aggregate(to_dev(q), to_dev(tq), Wd).cpu().numpy()
+            oz = o.aggregate(q, tq, fw, fb, ef, nf, W)
+            worst = max(worst, agg_error(gz, oz))
+        g.insert(to_dev(src[lo:hi]), to_dev(dst[lo:hi]), to_dev(t[lo:hi]))
+        o.insert(src[lo:hi], dst[lo:hi], t[lo:hi])
+    print(f"aggregate workload {k}: max scaled error {worst:.3e}")
+    assert g.status() == 0
+    assert worst <= AGG_TOL
