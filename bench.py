@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--hop2", action="store_true",
                     help="also answer every step's second hop (Sec. 4.4) with nlb_sample_hop2, "
                          "ids only, and report it separately")
+    ap.add_argument("--aggregate", action="store_true",
+                    help="retrieve with the fused eq. (4) attention aggregation (nlb_aggregate, "
+                         "random weights) instead of nlb_sample, and report that kernel")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="before the benchmark, run a plain elementwise copy of this many MiB "
                          "five times (a known-traffic kernel for calibrating HBM counters)")
@@ -83,6 +86,26 @@ def hop2_bytes(w, hop1_valid, queries):
     time (8 B) and, when valid, the neighbour's s slots (12 B each); writes
     nbr/eid/ts for s*s slots per query (12 B each)."""
     return queries * w.s * 8 + hop1_valid * 12 * w.s + queries * w.s * w.s * 12
+
+
+PEAK_BF16_TFLOPS = 2500.0
+
+
+def aggregate_flops(w, valid_slots, queries, hidden=64):
+    """Algorithmic matrix FLOPs of eq. (4) (no padding, one product per
+    weight): MLP_in's two layers for every valid slot, MLP_out's two layers
+    for every query, and the attention logits."""
+    d_in = w.node_dim + w.edge_dim + w.d_time
+    per_slot = 2 * (d_in * hidden + hidden * hidden + hidden)
+    per_query = 2 * ((w.node_dim + hidden) * hidden + hidden * hidden)
+    return valid_slots * per_slot + queries * per_query
+
+
+def aggregate_bytes(w, valid_slots, queries, hidden=64):
+    """Algorithmic HBM bytes of one aggregation launch: query ids and times,
+    the table slots, the rows of valid slots and the self row; Z written."""
+    erb, nrb = w.row_bytes("edge"), w.row_bytes("node")
+    return queries * (8 + 12 * w.s + nrb + 4 * hidden) + valid_slots * (erb + nrb)
 
 
 def insert_bytes(links):
@@ -195,6 +218,11 @@ def main():
     Qmax = 3 * w.batch
     out = table.alloc_outputs(Qmax, want=("eid", "ts", "tenc", "efeat", "nfeat", "self"))
     nbr_all = torch.empty((K, Qmax, w.s), dtype=torch.int32, device=dev)
+    agg_w = agg_z = None
+    if args.aggregate:
+        agg_w = {k: (torch.from_numpy(v.view(np.int16)) if v.dtype == np.uint16 else
+                     torch.from_numpy(v)).to(dev) for k, v in synth.agg_weights(w).items()}
+        agg_z = torch.empty((Qmax, nlb.AGG_HIDDEN), dtype=torch.float32, device=dev)
     hop2_out = None
     if args.hop2:
         hop2_out = table.alloc_outputs(Qmax * w.s, want=("nbr", "eid", "ts"))
@@ -203,6 +231,9 @@ def main():
     def step(b, nbr_out):
         s_, d_, t_, q, tq = synth.batch_views(w, nodes, ts, b)
         n = q.numel()
+        if agg_w is not None:
+            table.aggregate(q, tq, agg_w, out=agg_z[:n])
+            return s_, d_, t_, n
         o = {k: v[:n] for k, v in out.items()}
         o["nbr"] = nbr_out[:n]
         table.sample_into(q, tq, o)
@@ -239,6 +270,17 @@ def main():
     insert_ms = np.array([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)])
     links = sum(n // 3 for n in qcount)
     queries = sum(qcount)
+    if agg_w is not None:
+        # The aggregation writes no ids; its valid-slot counts come from a
+        # replay of the timed batches' first-hop ids on a fresh table (not timed).
+        replay = nlb.Table(w.num_nodes, w.s, w.alpha, w.table_seed)
+        for b in range(start + W + K):
+            s_, d_, t_, q, tq = synth.batch_views(w, nodes, ts, b)
+            if b >= start + W:
+                replay.sample_into(q, tq, {"nbr": nbr_all[b - start - W, :q.numel()]})
+            replay.insert(s_, d_, t_)
+        torch.cuda.synchronize()
+        replay.close()
     valid = int(sum(int((nbr_all[k, :qcount[k]] >= 0).sum()) for k in range(K)))
     s_bytes = sum(sample_bytes(w, 0, n) for n in qcount) + valid * (w.row_bytes("edge") + w.row_bytes("node"))
     achieved = s_bytes / (sample_ms.sum() * 1e-3) / 1e9
@@ -279,6 +321,18 @@ def main():
                      "bytes_per_query_full_occupancy": full_bytes_per_query},
         "setup_s": setup_s,
     }
+    if agg_w is not None:
+        fl = aggregate_flops(w, valid, queries)
+        ab = aggregate_bytes(w, valid, queries)
+        t_s = sample_ms.sum() * 1e-3
+        res["roofline"] = {"bound": "mfma", "achieved": fl / t_s / 1e12, "peak": PEAK_BF16_TFLOPS,
+                           "unit": "TFLOP/s", "frac": fl / t_s / 1e12 / PEAK_BF16_TFLOPS,
+                           "traffic": None, "kernel": "aggregate_fused",
+                           "flops_per_launch": fl / K, "hbm_gbps_algorithmic": ab / t_s / 1e9}
+        res["aggregate_ms_avg"] = res.pop("sample_ms_avg")
+        res["aggregate_kernel_queries_per_s"] = res.pop("sample_kernel_queries_per_s")
+        res["value_note"] = "steps retrieve with nlb_aggregate (eq. (4), random weights)"
+        res["dtype"] = "bf16-mfma+f32"
     if hop2_out is not None:
         n_last = qcount[-1] * w.s
         last_valid = int((hop2_out["nbr"][:n_last] >= 0).sum())   # last step, after timing

@@ -192,7 +192,7 @@ int nlb_sample_hop2(nlb_table *h, const int32_t *hop1_nbr, const uint32_t *tq, u
  * (relative error ~2.5e-5 of the sum of magnitudes); through four layers and
  * the softmax, Z is within 2e-4 * (|Z| + the root mean square of Z over the
  * launch) of the same function evaluated in double (measured: <= 3.3e-5).
- * z is device fp32 [nq][H].  Tables with s > 128 are not supported
+ * z is device fp32 [nq][H].  Tables with s > 64 are not supported
  * (NLB_EINVAL).  nq == 0 is a no-op.  Errors: as nlb_sample, and NLB_EINVAL
  * for a bad weight set. */
 #define NLB_AGG_HIDDEN 64

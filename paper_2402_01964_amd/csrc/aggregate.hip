@@ -30,8 +30,10 @@ constexpr int kAggThreads = 256;
 constexpr int kH = NLB_AGG_HIDDEN;      // hidden and output width
 constexpr int kHs = kH + 8;             // bf16 row stride of 64-wide activations in LDS
 constexpr int kHf = kH + 4;             // fp32 row stride of the messages in LDS
-constexpr int kMaxBlocks = 8;           // row blocks of 16: at most 128 slot rows per tile
-constexpr uint32_t kAggLdsBudget = 160 * 1024;   // gfx950: 160 KB of LDS per workgroup
+constexpr int kMaxBlocks = 4;           // row blocks of 16: at most 64 slot rows per tile
+constexpr uint32_t kAggLdsBudget = 40 * 1024;    // four workgroups per CU
+constexpr uint32_t kAggLdsMax = 160 * 1024;      // gfx950: LDS of one workgroup at most
+constexpr int kFillUnroll = 4;                   // input units whose loads are in flight together
 constexpr uint32_t kAggTargetTiles = 2048;
 static_assert(kH == 64, "the kernel maps four wavefronts onto 64 output columns");
 
@@ -196,28 +198,44 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_fused(AggParams p) {
     }
     __syncthreads();
 
-    // Phase 2: MLP_in inputs x = [r_v | e | T-enc(tq - t')], hi/lo pairs.
+    // Phase 2: MLP_in inputs x = [r_v | e | T-enc(tq - t')], hi/lo pairs;
+    // the row loads of kFillUnroll units are issued before their stores.
     const uint32_t g1 = p.k1 / 8;
-    for (uint32_t u = tid; u < p.rows * g1; u += kAggThreads) {
-        const uint32_t j = div_small(u, p.g1_m);
-        const uint32_t c0 = (u - j * g1) * 8;
-        const SlotLds sl = slots[j];
-        float v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        if (sl.x >= 0) {
+    const uint32_t units = p.rows * g1;
+    for (uint32_t base = tid; base < units; base += kAggThreads * kFillUnroll) {
+        float v[kFillUnroll][8];
+#pragma unroll
+        for (int r = 0; r < kFillUnroll; r++) {
+            const uint32_t u = base + r * kAggThreads;
+#pragma unroll
+            for (int i = 0; i < 8; i++) v[r][i] = 0.0f;
+            if (u >= units) continue;
+            const uint32_t j = div_small(u, p.g1_m);
+            const uint32_t c0 = (u - j * g1) * 8;
+            const SlotLds sl = slots[j];
+            if (sl.x < 0) continue;
             if (c0 < p.off_e) {
-                load8(p.nfeat + (size_t)sl.x * p.nrb, p.n_dim, p.n_bf16, p.n_vec, c0, v);
+                load8(p.nfeat + (size_t)sl.x * p.nrb, p.n_dim, p.n_bf16, p.n_vec, c0, v[r]);
             } else if (c0 < p.off_t) {
                 if ((int64_t)sl.e < p.edge_rows)
-                    load8(p.efeat + (size_t)sl.e * p.erb, p.e_dim, p.e_bf16, p.e_vec, c0 - p.off_e, v);
+                    load8(p.efeat + (size_t)sl.e * p.erb, p.e_dim, p.e_bf16, p.e_vec, c0 - p.off_e,
+                          v[r]);
             } else {
                 const uint32_t k = c0 - p.off_t;
 #pragma unroll
                 for (int i = 0; i < 8; i++)
                     if (k + i < p.d_time)
-                        v[i] = cos_fp32(__builtin_fmaf(p.w[k + i], sl.dt, p.b[k + i]));
+                        v[r][i] = cos_fp32(__builtin_fmaf(p.w[k + i], sl.dt, p.b[k + i]));
             }
         }
-        store_split8(v, Xh + (size_t)j * p.xs + c0, Xl + (size_t)j * p.xs + c0);
+#pragma unroll
+        for (int r = 0; r < kFillUnroll; r++) {
+            const uint32_t u = base + r * kAggThreads;
+            if (u >= units) continue;
+            const uint32_t j = div_small(u, p.g1_m);
+            const uint32_t c0 = (u - j * g1) * 8;
+            store_split8(v[r], Xh + (size_t)j * p.xs + c0, Xl + (size_t)j * p.xs + c0);
+        }
     }
     __syncthreads();
 
@@ -372,7 +390,7 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
     if (!h || !wts) return NLB_EINVAL;
     if (nq == 0) return NLB_OK;
     if (!node || !tq || !z) return NLB_EINVAL;
-    if (wts->hidden != kH || h->s > 128) return NLB_EINVAL;
+    if (wts->hidden != kH || h->s > 16u * kMaxBlocks) return NLB_EINVAL;
     if (!wts->w1 || !wts->w2 || !wts->w3 || !wts->w4 || !wts->b1 || !wts->b2 || !wts->b3 ||
         !wts->b4 || !wts->att)
         return NLB_EINVAL;
@@ -434,18 +452,20 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
 
     // Tile: as many queries as fit the LDS budget (at most 128 slot rows),
     // fewer when that leaves too few workgroups to fill the GPU.
+    // A tile larger than one query must fit the budget that keeps four
+    // workgroups per CU (the kernel is latency-bound: concurrency beats tile
+    // size); a single query may use a workgroup's whole LDS.
     uint32_t tile_q = 0, lds = 0;
-    for (uint32_t rows = 128; rows >= 16; rows -= 16) {
+    const uint32_t want = (uint32_t)(((uint64_t)nq + kAggTargetTiles - 1) / kAggTargetTiles);
+    for (uint32_t rows = 16u * kMaxBlocks; rows >= 16 && tile_q == 0; rows -= 16) {
         const uint32_t tq_cap = rows / h->s;
         if (tq_cap == 0) continue;
-        const uint32_t want = (uint32_t)(((uint64_t)nq + kAggTargetTiles - 1) / kAggTargetTiles);
         const uint32_t t = tq_cap < (want ? want : 1) ? tq_cap : (want ? want : 1);
         AggParams trial = p;
         const uint32_t bytes = agg_layout(trial, pad16(t * h->s), pad16(t));
-        if (bytes <= kAggLdsBudget) {
+        if (bytes <= (t == 1 ? kAggLdsMax : kAggLdsBudget)) {
             tile_q = t;
             lds = bytes;
-            break;
         }
     }
     if (tile_q == 0) return NLB_EINVAL;   // one query does not fit the LDS budget
@@ -454,7 +474,7 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
     // Dynamic LDS beyond 64 KB has to be allowed per kernel before launch.
     if (lds > 64u * 1024u &&
         hipFuncSetAttribute((const void *)aggregate_fused, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)kAggLdsBudget) != hipSuccess)
+                            (int)kAggLdsMax) != hipSuccess)
         return NLB_EDEVICE;
     const dim3 grid((unsigned)((nq + tile_q - 1) / tile_q));
     hipLaunchKernelGGL(aggregate_fused, grid, dim3(kAggThreads), lds, (hipStream_t)stream, p);
