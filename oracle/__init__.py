@@ -16,6 +16,7 @@ in the C source:
                    neighbour, link-feature and self rows; App. C T-encoding
 * ``sample_hop2`` -- Sec. 4.4 second-hop neighbours: S_v^t of each stored v
 * ``aggregate`` -- eq. (4): attention over the retrieved neighbours, fp64
+* ``gru_update`` -- Sec. 4.4 node-status RNN update after each event, fp64
 """
 from __future__ import annotations
 
@@ -83,6 +84,9 @@ def _load():
     lib.orc_aggregate.restype = ctypes.c_int
     lib.orc_aggregate.argtypes = [P, P, P, i64, i32, P, P, P, i32, i32, P, i32, i32, i32,
                                   P, P, P, P, P, P, P, P, P, P]
+    lib.orc_gru_update.restype = ctypes.c_int
+    lib.orc_gru_update.argtypes = [i64, i32, P, i32, P, P, P, i64, u64, i32, P, P, P, i32, i32,
+                                   P, P, P, P]
     lib.orc_tenc.argtypes = [P, i64, i32, P, P, P]
     _lib = lib
     return lib
@@ -284,6 +288,32 @@ class Oracle:
         if rc != 0:
             raise ValueError("oracle: query node out of range")
         return z
+
+
+def gru_update(status, src, dst, t, e0, w, b, efeat, weights):
+    """Node-status update of Sec. 4.4 (GRU, batch semantics: updates read
+    the statuses from before the batch, the latest link of a node wins), in
+    place on ``status`` ([N, d] float32, or uint16 bf16 bits).  ``weights``:
+    w_ih, w_hh (uint16 bf16 bits, padded layouts of nlb_oracle.c), b_ih, b_hh
+    (float32).  ``efeat``: [E, e_dim] float32 / bf16 bits, or None."""
+    lib = _load()
+    assert status.flags.c_contiguous
+    src, dst, t = _c(src, np.int32), _c(dst, np.int32), _c(t, np.uint32)
+    w, b = _c(w, np.float32), _c(b, np.float32)
+    s_dt = 0 if status.dtype == np.float32 else 1
+    if efeat is None:
+        ef, e_dim, e_dt = None, 0, 1
+    else:
+        ef = np.ascontiguousarray(efeat)
+        e_dim, e_dt = ef.shape[1], (0 if ef.dtype == np.float32 else 1)
+    W = {k: np.ascontiguousarray(weights[k], np.uint16 if k.startswith("w_") else np.float32)
+         for k in ("w_ih", "w_hh", "b_ih", "b_hh")}
+    rc = lib.orc_gru_update(status.shape[0], status.shape[1], _ptr(status), s_dt, _ptr(src), _ptr(dst),
+                            _ptr(t), len(src), int(e0), len(w), _ptr(w), _ptr(b), _ptr(ef), e_dim, e_dt,
+                            _ptr(W["w_ih"]), _ptr(W["w_hh"]), _ptr(W["b_ih"]), _ptr(W["b_hh"]))
+    if rc != 0:
+        raise ValueError("oracle: node id out of range")
+    return status
 
 
 def tenc(dt, w, b):

@@ -24,7 +24,8 @@
  *     link features, the neighbours' own feature rows, the self row and a
  *     cosine time encoding of t - t'.  Second-hop neighbours of u are the
  *     entries of S_v^t for the stored neighbours v of u.  Eq. (4) aggregates
- *     the retrieved neighbours with attention into the representation Z_u.
+ *     the retrieved neighbours with attention into the representation Z_u,
+ *     and an RNN updates the node statuses after each event.
  *
  * Random draws: the replacement coin of offer (e, k) (k = 0 for the S_u
  * offer, k = 1 for the S_v offer) is the high 32 bits of output number
@@ -429,6 +430,113 @@ int orc_aggregate(const orc *o, const int32_t *node, const uint32_t *tq, int64_t
     }
     free(x); free(a); free(h); free(logit); free(y); free(valid);
     return rc;
+}
+
+static double sigmoid(double a) { return 1.0 / (1.0 + exp(-a)); }
+
+static uint16_t bf16_round(double v)
+{
+    /* double -> fp32 (nearest) -> bf16 (nearest even), as a bf16 store of
+     * an fp32 result rounds */
+    float f = (float)v;
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    u = u + 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+/*
+ * Node-status update of Sec. 4.4: after a link (u, v, t) with features e,
+ * r_u <- RNN([r_u, r_v, t, e]) and r_v <- RNN([r_v, r_u, t, e]).  The RNN is
+ * a GRU cell (Cho et al., 2014) with input x = [r_other ; T-enc(t) ; e] and
+ * hidden state h = r_self:
+ *   r = sigmoid(W_ir x + b_ir + W_hr h + b_hr)
+ *   z = sigmoid(W_iz x + b_iz + W_hz h + b_hz)
+ *   n = tanh(W_in x + b_in + r * (W_hn h + b_hn))
+ *   h' = (1 - z) * n + z * h
+ * T-enc(t) is the table's time encoding of the link's timestamp,
+ * cos(w_k * t + b_k) with the fp32 argument fmaf(w_k, (float)t, b_k).
+ * A batch of n links (arrival indices e0 .. e0+n-1, link rows efeat[e]) is
+ * applied with batch semantics: every update reads the statuses as they were
+ * before the batch, and a node that several links of the batch touch takes
+ * the update of the latest one (larger arrival index; the second endpoint's
+ * update after the first's on a self-loop).
+ * status: [N][d] fp32 (dtype 0) or bf16 bits (1), updated in place.
+ * Weights (bf16 bits, row-major, input segments zero-padded to 32 columns):
+ *   w_ih [3d][pad32(d) + pad32(d_t) + pad32(e_dim)]  rows r | z | n
+ *   w_hh [3d][pad32(d)]
+ * b_ih, b_hh: fp32 [3d].  Returns -1 on an out-of-range endpoint.
+ */
+int orc_gru_update(int64_t N, int32_t d, void *status, int32_t status_dtype,
+                   const int32_t *src, const int32_t *dst, const uint32_t *t, int64_t n,
+                   uint64_t e0, int32_t d_t, const float *w, const float *b,
+                   const uint8_t *efeat, int32_t e_dim, int32_t e_dtype,
+                   const uint16_t *w_ih, const uint16_t *w_hh, const float *b_ih,
+                   const float *b_hh)
+{
+    const int64_t kx = pad32(d) + pad32(d_t) + pad32(e_dim);
+    const int64_t kh = pad32(d);
+    const int64_t e_bytes = (int64_t)e_dim * (e_dtype == 0 ? 4 : 2);
+    const int64_t s_bytes = (int64_t)d * (status_dtype == 0 ? 4 : 2);
+    for (int64_t i = 0; i < n; i++)
+        if (src[i] < 0 || dst[i] < 0 || src[i] >= N || dst[i] >= N) return -1;
+    /* candidates of every touched node; the last write per node wins */
+    double *cand = (double *)malloc(sizeof(double) * (size_t)(2 * n) * (size_t)d);
+    int32_t *who = (int32_t *)malloc(sizeof(int32_t) * (size_t)(2 * n));
+    double *x = (double *)malloc(sizeof(double) * (size_t)(d + d_t + e_dim + 1));
+    double *hv = (double *)malloc(sizeof(double) * (size_t)d);
+    for (int64_t i = 0; i < n; i++) {
+        for (int k = 0; k < 2; k++) {
+            const int32_t self = k == 0 ? src[i] : dst[i];
+            const int32_t other = k == 0 ? dst[i] : src[i];
+            const uint8_t *rs = (const uint8_t *)status + (size_t)self * (size_t)s_bytes;
+            const uint8_t *ro = (const uint8_t *)status + (size_t)other * (size_t)s_bytes;
+            for (int64_t c = 0; c < d; c++) x[c] = feat_value(ro, status_dtype, c);
+            for (int64_t c = 0; c < d_t; c++)
+                x[d + c] = (double)tenc_value(w[c], (float)t[i], b[c]);
+            for (int64_t c = 0; c < e_dim; c++)
+                x[d + d_t + c] = feat_value(efeat + (size_t)(e0 + (uint64_t)i) * (size_t)e_bytes, e_dtype, c);
+            for (int64_t c = 0; c < d; c++) hv[c] = feat_value(rs, status_dtype, c);
+            double *out = cand + (size_t)(2 * i + k) * (size_t)d;
+            for (int64_t j = 0; j < d; j++) {
+                double gi[3], gh[3];
+                for (int g = 0; g < 3; g++) {
+                    const int64_t row = g * d + j;
+                    double acc = 0.0;
+                    for (int64_t c = 0; c < d; c++) acc += bf16_value(w_ih[row * kx + c]) * x[c];
+                    for (int64_t c = 0; c < d_t; c++)
+                        acc += bf16_value(w_ih[row * kx + pad32(d) + c]) * x[d + c];
+                    for (int64_t c = 0; c < e_dim; c++)
+                        acc += bf16_value(w_ih[row * kx + pad32(d) + pad32(d_t) + c]) * x[d + d_t + c];
+                    gi[g] = acc + (double)b_ih[row];
+                    double acc2 = 0.0;
+                    for (int64_t c = 0; c < d; c++) acc2 += bf16_value(w_hh[row * kh + c]) * hv[c];
+                    gh[g] = acc2 + (double)b_hh[row];
+                }
+                const double r = sigmoid(gi[0] + gh[0]);
+                const double z = sigmoid(gi[1] + gh[1]);
+                const double nn = tanh(gi[2] + r * gh[2]);
+                out[j] = (1.0 - z) * nn + z * hv[j];
+            }
+            who[2 * i + k] = self;
+        }
+    }
+    /* apply in stream order: the latest update of a node is written last */
+    for (int64_t r = 0; r < 2 * n; r++) {
+        uint8_t *dstrow = (uint8_t *)status + (size_t)who[r] * (size_t)s_bytes;
+        const double *c = cand + (size_t)r * (size_t)d;
+        for (int64_t j = 0; j < d; j++) {
+            if (status_dtype == 0) {
+                const float f = (float)c[j];
+                memcpy(dstrow + 4 * j, &f, 4);
+            } else {
+                const uint16_t hb = bf16_round(c[j]);
+                memcpy(dstrow + 2 * j, &hb, 2);
+            }
+        }
+    }
+    free(cand); free(who); free(x); free(hv);
+    return 0;
 }
 
 /* Stand-alone T-encoding of a list of gaps, for direct checks of App. C. */

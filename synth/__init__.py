@@ -405,3 +405,44 @@ def agg_weights(w: Workload, hidden: int = AGG_HIDDEN, seed: int | None = None):
     return {"w1": dense(H, [dn, de, dt]), "b1": vec(H), "w2": dense(H, [H]), "b2": vec(H),
             "att": rng.normal(0.0, 1.0 / np.sqrt(H), H).astype(np.float32),
             "w3": dense(H, [dn, H]), "b3": vec(H), "w4": dense(H, [H]), "b4": vec(H)}
+
+
+STATUS_DIM_DEFAULT = 100
+
+
+def status_spec(w: Workload):
+    """Width and element type of the node statuses r_u that the RNN update
+    maintains: a workload with node-feature rows updates those rows in place
+    (so later queries gather the updated statuses); one without keeps an fp32
+    status table of width 100 (the paper tunes status widths from 50 to 100)."""
+    if w.node_dim:
+        return w.node_dim, w.node_dtype
+    return STATUS_DIM_DEFAULT, "f32"
+
+
+def gru_weights(w: Workload, seed: int | None = None):
+    """Random weights of the node-status GRU for workload ``w`` (see
+    ``gru_weights_for``), seeded by the workload."""
+    d, _ = status_spec(w)
+    return gru_weights_for(d, w.d_time, w.edge_dim, 6000 + w.key if seed is None else seed)
+
+
+def gru_weights_for(d: int, d_time: int, edge_dim: int, seed: int):
+    """Random weights of a node-status GRU of width d: bf16 (uint16 bits)
+    w_ih [3d][pad32(d) + pad32(d_time) + pad32(edge_dim)] for (r_other |
+    T-enc(t) | e) and w_hh [3d][pad32(d)], gate rows r | z | n, zero pad
+    columns; fp32 biases b_ih, b_hh [3d].  Entries ~ U(-1/sqrt(d),
+    1/sqrt(d)), the usual GRU initialisation."""
+    rng = np.random.default_rng(seed)
+    k = 1.0 / np.sqrt(d)
+
+    def dense(segs):
+        out = np.zeros((3 * d, sum(_pad32(s) for s in segs)), np.float32)
+        col = 0
+        for sgl in segs:
+            out[:, col:col + sgl] = rng.uniform(-k, k, (3 * d, sgl))
+            col += _pad32(sgl)
+        return _to_bf16_bits(out)
+    return {"w_ih": dense([d, d_time, edge_dim]), "w_hh": dense([d]),
+            "b_ih": rng.uniform(-k, k, 3 * d).astype(np.float32),
+            "b_hh": rng.uniform(-k, k, 3 * d).astype(np.float32)}

@@ -657,3 +657,152 @@ def test_aggregate_constant_messages_ignore_attention():
     np.testing.assert_allclose(z[~any_valid], np.broadcast_to(z[~any_valid][0], z[~any_valid].shape),
                                rtol=0, atol=1e-12)
     assert np.abs(z[any_valid][0] - z[~any_valid][0]).max() > 1e-6
+
+
+# ----------------------------------------------------------------------------- status RNN (Sec. 4.4)
+def _gru_zero(d, d_t, e_dim):
+    kx = oracle_pad32(d) + oracle_pad32(d_t) + oracle_pad32(e_dim)
+    return {"w_ih": np.zeros((3 * d, kx), np.uint16), "w_hh": np.zeros((3 * d, oracle_pad32(d)), np.uint16),
+            "b_ih": np.zeros(3 * d, np.float32), "b_hh": np.zeros(3 * d, np.float32)}
+
+
+def oracle_pad32(x):
+    return (x + 31) // 32 * 32
+
+
+def test_gru_handworked_bias_only():
+    """d = 1, all weights zero: r = sigmoid(b_ir + b_hr), z = sigmoid(b_iz +
+    b_hz) and n = tanh(b_in + r * b_hn), so the new status is (1 - z) n + z h.
+    With b_iz = ln 3 (z = 3/4), b_ir = 0 (r = 1/2), b_in = 0 and b_hn =
+    2 atanh(0.6) (n = 0.6): h' = 0.15 + 0.75 h.  Node 2 is not touched."""
+    W = _gru_zero(1, 0, 0)
+    W["b_ih"][1] = math.log(3.0)
+    W["b_hh"][2] = 2.0 * math.atanh(0.6)
+    st = np.array([[0.5], [-1.0], [4.0]], np.float32)
+    oracle.gru_update(st, [0], [1], [7], 0, np.zeros(0, np.float32), np.zeros(0, np.float32), None, W)
+    n = math.tanh(0.5 * np.float32(2.0 * math.atanh(0.6)))
+    assert abs(st[0, 0] - (0.25 * n + 0.75 * 0.5)) < 1e-7
+    assert abs(st[1, 0] - (0.25 * n - 0.75)) < 1e-7
+    assert st[2, 0] == 4.0
+
+
+def _gru_cell_reference(W, d, d_t, e_dim, x, h):
+    """torch.nn.GRUCell in float64 with the given bf16 weights (pad columns
+    dropped): the textbook GRU of a library."""
+    import torch
+    f = lambda bits: torch.from_numpy(bf16_to_f32(bits).astype(np.float64))
+    w_ih = f(W["w_ih"])
+    cols = list(range(d)) + [oracle_pad32(d) + c for c in range(d_t)] + \
+        [oracle_pad32(d) + oracle_pad32(d_t) + c for c in range(e_dim)]
+    cell = torch.nn.GRUCell(d + d_t + e_dim, d).double()
+    with torch.no_grad():
+        cell.weight_ih.copy_(w_ih[:, cols])
+        cell.weight_hh.copy_(f(W["w_hh"])[:, :d])
+        cell.bias_ih.copy_(torch.from_numpy(W["b_ih"].astype(np.float64)))
+        cell.bias_hh.copy_(torch.from_numpy(W["b_hh"].astype(np.float64)))
+        return cell(torch.from_numpy(x), torch.from_numpy(h)).numpy()
+
+
+@pytest.mark.parametrize("edge_dtype", ["f32", "bf16"])
+def test_gru_matches_library_gru_cell(edge_dtype):
+    """Links with pairwise distinct endpoints: each endpoint's new status is
+    torch's GRUCell (float64) on x = [r_other ; T-enc(t) ; e] with hidden
+    state r_self, both endpoints reading pre-batch statuses.  The time
+    weights are dyadic with few bits, so w * t is exact in fp32 and the
+    fused argument w * t + b is one fp32 addition."""
+    import synth
+    rng = np.random.default_rng(21)
+    N, d, d_t, e_dim, E = 64, 20, 12, 9, 16
+    W = synth.gru_weights_for(d, d_t, e_dim, seed=3)
+    perm = rng.permutation(N)[:2 * E]
+    src, dst = perm[:E].astype(np.int32), perm[E:].astype(np.int32)
+    t = np.sort(rng.integers(0, 2**20, E)).astype(np.uint32)
+    st = rng.standard_normal((N, d)).astype(np.float32)
+    ef32 = rng.standard_normal((E + 5, e_dim)).astype(np.float32)
+    ef = synth._to_bf16_bits(ef32) if edge_dtype == "bf16" else ef32
+    efv = bf16_to_f32(ef) if edge_dtype == "bf16" else ef32
+    fw = (rng.integers(1, 16, d_t) * 2.0**-22).astype(np.float32)
+    fb = rng.uniform(-3, 3, d_t).astype(np.float32)
+    before = st.copy()
+    oracle.gru_update(st, src, dst, t, 5, fw, fb, ef, W)   # link i uses row 5 + i
+    arg = fw[None, :] * t[:, None].astype(np.float32) + fb[None, :]
+    assert arg.dtype == np.float32
+    te = np.cos(arg.astype(np.float64)).astype(np.float32).astype(np.float64)
+    e = efv[5:5 + E].astype(np.float64)
+    b64 = before.astype(np.float64)
+    want_u = _gru_cell_reference(W, d, d_t, e_dim, np.concatenate([b64[dst], te, e], 1), b64[src])
+    want_v = _gru_cell_reference(W, d, d_t, e_dim, np.concatenate([b64[src], te, e], 1), b64[dst])
+    np.testing.assert_allclose(st[src], want_u.astype(np.float32), rtol=0, atol=2e-7)
+    np.testing.assert_allclose(st[dst], want_v.astype(np.float32), rtol=0, atol=2e-7)
+    untouched = np.setdiff1d(np.arange(N), perm[:2 * E])
+    np.testing.assert_array_equal(st[untouched], before[untouched])
+
+
+def bf16_to_f32(bits):
+    return (np.asarray(bits, np.uint32) << 16).view(np.float32)
+
+
+def test_gru_batch_reads_pre_batch_statuses_and_latest_link_wins():
+    """Batch semantics of the status update: in one batch, link 0 (0, 1),
+    link 1 (1, 2), link 2 (3, 0).  Node 1's final status is its update from
+    link 1, node 0's from link 2, and both read the statuses from before the
+    batch -- so each equals the single-link update applied to the initial
+    statuses.  A self-loop (4, 4) gives the same status either way."""
+    import synth
+    rng = np.random.default_rng(5)
+    N, d = 6, 40
+    W = synth.gru_weights_for(d, 0, 0, seed=9)
+    init = rng.standard_normal((N, d)).astype(np.float32)
+    no = np.zeros(0, np.float32)
+    batch = init.copy()
+    oracle.gru_update(batch, [0, 1, 3, 4], [1, 2, 0, 4], [1, 2, 3, 4], 0, no, no, None, W)
+    single = {}
+    for i, (u, v) in enumerate([(0, 1), (1, 2), (3, 0), (4, 4)]):
+        st = init.copy()
+        oracle.gru_update(st, [u], [v], [i + 1], i, no, no, None, W)
+        single[i] = st
+    np.testing.assert_array_equal(batch[0], single[2][0])
+    np.testing.assert_array_equal(batch[1], single[1][1])
+    np.testing.assert_array_equal(batch[2], single[1][2])
+    np.testing.assert_array_equal(batch[3], single[2][3])
+    np.testing.assert_array_equal(batch[4], single[3][4])
+    np.testing.assert_array_equal(batch[5], init[5])
+    # sequential application would differ: link 1 would see node 1's new status
+    seq = init.copy()
+    for i, (u, v) in enumerate([(0, 1), (1, 2), (3, 0), (4, 4)]):
+        oracle.gru_update(seq, [u], [v], [i + 1], i, no, no, None, W)
+    assert np.abs(seq[2] - batch[2]).max() > 1e-4
+
+
+def test_gru_bf16_status_rounds_to_nearest_even():
+    """A bf16 status table stores the update rounded to nearest even (as
+    torch's fp32 -> bf16 conversion); with d = 1 and zero weights the update
+    is (1 - z) n + z h with n = 0.6, z = 3/4 (see the hand-worked case)."""
+    import torch
+    W = _gru_zero(1, 0, 0)
+    W["b_ih"][1] = math.log(3.0)
+    W["b_hh"][2] = 2.0 * math.atanh(0.6)
+    no = np.zeros(0, np.float32)
+    h = np.array([0.5, -1.0, 0.3125, 2.0], np.float32)
+    st = np.ascontiguousarray(synth_bits(h)[:, None])
+    oracle.gru_update(st, [0, 2], [1, 3], [1, 2], 0, no, no, None, W)
+    n = math.tanh(0.5 * np.float32(2.0 * math.atanh(0.6)))
+    exact = torch.tensor([0.25 * n + 0.75 * float(bf16_to_f32(synth_bits(np.array([x], np.float32)))[0])
+                          for x in h], dtype=torch.float64)
+    want = exact.float().bfloat16().view(torch.int16).numpy().astype(np.uint16)
+    np.testing.assert_array_equal(st[:, 0], want)
+
+
+def synth_bits(x):
+    import synth
+    return synth._to_bf16_bits(x)
+
+
+def test_gru_rejects_out_of_range_endpoint():
+    import synth
+    W = synth.gru_weights_for(4, 0, 0, seed=1)
+    st = np.zeros((3, 4), np.float32)
+    no = np.zeros(0, np.float32)
+    with pytest.raises(ValueError):
+        oracle.gru_update(st, [0], [3], [1], 0, no, no, None, W)
+    assert not st.any()
