@@ -217,6 +217,54 @@ typedef struct nlb_agg_weights {
 int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t nq,
                   const nlb_agg_weights *wts, float *z, void *stream);
 
+/* Node-status update of Sec. 4.4: after a link (u, v, t) with features e,
+ * r_u <- RNN([r_u, r_v, t, e]) and r_v <- RNN([r_v, r_u, t, e]), for a batch
+ * of n links (src, dst, t: device arrays of n elements) whose link-feature
+ * rows are first_eid .. first_eid + n - 1 of the table's link rows (rows at
+ * or past edge_rows read as zeros).  The RNN is a GRU cell with input
+ * x = [r_other ; T-enc(t) ; e] and hidden state h = r_self:
+ *   r = sigmoid(W_ir x + b_ir + W_hr h + b_hr)
+ *   z = sigmoid(W_iz x + b_iz + W_hz h + b_hz)
+ *   n = tanh(W_in x + b_in + r * (W_hn h + b_hn))
+ *   h' = (1 - z) n + z h
+ * with T-enc(t) the table's time encoding cos(w_k t + b_k) of the link time
+ * (argument fmaf(w_k, (float)t, b_k)).  Batch semantics: every update reads
+ * the statuses as they were before the call, and a node that several links
+ * of the batch touch takes the update of the latest one (larger index; on a
+ * self-loop the dst side's).  status is a device array [N][status_dim] of
+ * status_dtype elements, updated in place (it may be the table's node_feat
+ * buffer, so later queries gather the new statuses); rows of nodes that no
+ * link touches are not written.  A link with an endpoint outside [0, N) is
+ * skipped and flagged for nlb_status.  Weights (device, read during the
+ * call, bf16 rows 16-byte aligned, each input segment zero-padded to a
+ * multiple of 32 columns, gate rows in the order r | z | n):
+ *   w_ih: [3 d][pad32(d) + pad32(d_time) + pad32(edge_dim)]  (r_other | T-enc | e)
+ *   w_hh: [3 d][pad32(d)];  b_ih, b_hh: fp32 [3 d]
+ * with d = status_dim and edge_dim the table's link row bytes over the size
+ * of edge_dtype.  Numerics: fp32 activations enter bf16 matrix cores as
+ * hi + lo pairs (2^-18 relative), bf16 ones as one term, with fp32
+ * accumulation; an fp32 status is within 1e-4 of the same cell evaluated in
+ * double, a bf16 one within one bf16 rounding of it.  Calls on one table
+ * must be ordered (same stream): they share the table's working buffers,
+ * which the first call (and a larger batch) allocates.  n == 0 is a no-op.
+ * Errors: NLB_EINVAL (NULL table, weights or array with n > 0; n >= 2^31;
+ * bad dtype or dimension; misaligned pointers; a 16-row tile that does not
+ * fit the LDS), NLB_ENOMEM, NLB_EDEVICE. */
+#define NLB_RNN_MAX_DIM 1024
+
+typedef struct nlb_gru_weights {
+    int32_t status_dim;      /* d, 1 .. NLB_RNN_MAX_DIM */
+    int32_t status_dtype;    /* NLB_DTYPE_F32 / _BF16 */
+    int32_t edge_dtype;      /* element type of the table's link rows */
+    const uint16_t *w_ih;    /* bf16 bits */
+    const uint16_t *w_hh;
+    const float *b_ih;
+    const float *b_hh;
+} nlb_gru_weights;
+
+int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, const uint32_t *t, uint32_t n,
+                   uint64_t first_eid, const nlb_gru_weights *wts, void *status, void *stream);
+
 /* Free the table's device memory after synchronising its device.  NULL is a
  * no-op.  Borrowed buffers are not touched. */
 int nlb_destroy(nlb_table *h);

@@ -6,7 +6,8 @@ kernels of the library.  torch is used for device memory and streams.
 
 Method: Luo & Li, "Scalable and Efficient Temporal Graph Representation
 Learning via Forward Recent Sampling", arXiv 2402.01964 (Sec. 4.2 table
-maintenance, Sec. 4.4 retrieval, App. C time encoding).
+maintenance, Sec. 4.4 retrieval, attention aggregation and status update,
+App. C time encoding).
 """
 from __future__ import annotations
 
@@ -22,8 +23,10 @@ MAX_SLOTS = 1024
 
 # Symbols declared in include/nlb.h.
 ABI_SYMBOLS = ("nlb_create", "nlb_insert_batch", "nlb_sample", "nlb_sample_hop2", "nlb_aggregate",
-               "nlb_destroy", "nlb_get_info", "nlb_export", "nlb_status", "nlb_strerror")
+               "nlb_rnn_update", "nlb_destroy", "nlb_get_info", "nlb_export", "nlb_status",
+               "nlb_strerror")
 AGG_HIDDEN = 64
+RNN_MAX_DIM = 1024
 DTYPE_F32, DTYPE_BF16 = 0, 1
 
 
@@ -52,6 +55,12 @@ class _AggWeights(ctypes.Structure):
     _fields_ = [("hidden", ctypes.c_int32), ("node_dtype", ctypes.c_int32),
                 ("edge_dtype", ctypes.c_int32)] + \
                [(k, ctypes.c_void_p) for k in ("w1", "b1", "w2", "b2", "att", "w3", "b3", "w4", "b4")]
+
+
+class _GruWeights(ctypes.Structure):
+    _fields_ = [("status_dim", ctypes.c_int32), ("status_dtype", ctypes.c_int32),
+                ("edge_dtype", ctypes.c_int32)] + \
+               [(k, ctypes.c_void_p) for k in ("w_ih", "w_hh", "b_ih", "b_hh")]
 
 
 class _Info(ctypes.Structure):
@@ -90,6 +99,8 @@ def load_library(path: str = LIB_PATH):
     lib.nlb_sample_hop2.restype = I
     lib.nlb_aggregate.argtypes = [P, P, P, U32, ctypes.POINTER(_AggWeights), P, P]
     lib.nlb_aggregate.restype = I
+    lib.nlb_rnn_update.argtypes = [P, P, P, P, U32, U64, ctypes.POINTER(_GruWeights), P, P]
+    lib.nlb_rnn_update.restype = I
     lib.nlb_destroy.argtypes = [P]
     lib.nlb_destroy.restype = I
     lib.nlb_get_info.argtypes = [P, ctypes.POINTER(_Info)]
@@ -266,6 +277,35 @@ class Table:
                                        ctypes.byref(aw), _dev_ptr(out, 4, "z"), _stream_ptr(stream)),
                "nlb_aggregate")
         return out
+
+    def rnn_update(self, src, dst, t, first_eid: int, weights: dict, status, stream=None):
+        """Node-status GRU update of Sec. 4.4 after the links (src[i], dst[i],
+        t[i]) whose link rows are first_eid + i, in place on ``status`` (a
+        CUDA tensor [N, d], fp32 or bf16 -- e.g. this table's node_feat).
+        ``weights``: w_ih, w_hh (bf16, or 16-bit ints holding bf16 bits, padded
+        layouts of include/nlb.h) and b_ih, b_hh (fp32)."""
+        import torch
+        n = int(src.numel())
+        if dst.numel() != n or t.numel() != n:
+            raise ValueError("src, dst and t must have the same length")
+        if status.dim() != 2:
+            raise ValueError("status must be [N, d]")
+        gw = _GruWeights()
+        gw.status_dim = int(status.shape[1])
+        gw.status_dtype = DTYPE_F32 if status.dtype == torch.float32 else DTYPE_BF16
+        if status.dtype not in (torch.float32, torch.bfloat16, torch.int16):
+            raise TypeError("status must be float32 or bfloat16 (int16 bits)")
+        gw.edge_dtype = DTYPE_F32 if self.edge_feat is None or self.edge_feat.dtype == torch.float32 \
+            else DTYPE_BF16
+        for k in ("w_ih", "w_hh"):
+            setattr(gw, k, _dev_ptr(weights[k], 2, k))
+        for k in ("b_ih", "b_hh"):
+            setattr(gw, k, _dev_ptr(weights[k], 4, k))
+        _check(self._lib.nlb_rnn_update(self._h, _dev_ptr(src, 4, "src"), _dev_ptr(dst, 4, "dst"),
+                                        _dev_ptr(t, 4, "t"), n, int(first_eid), ctypes.byref(gw),
+                                        _dev_ptr(status, None, "status"), _stream_ptr(stream)),
+               "nlb_rnn_update")
+        return status
 
     def alloc_outputs(self, nq: int, want=("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self")):
         import torch

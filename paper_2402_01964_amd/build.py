@@ -4,7 +4,7 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRCS = [os.path.join(HERE, "csrc", f) for f in ("nlb.hip", "aggregate.hip")]
+SRCS = [os.path.join(HERE, "csrc", f) for f in ("nlb.hip", "aggregate.hip", "rnn.hip")]
 LIB = os.path.join(HERE, "libnlb.so")
 
 HIPCC_FLAGS = [

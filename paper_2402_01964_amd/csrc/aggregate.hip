@@ -37,8 +37,6 @@ constexpr int kFillUnroll = 4;                   // input units whose loads are 
 constexpr uint32_t kAggTargetTiles = 2048;
 static_assert(kH == 64, "the kernel maps four wavefronts onto 64 output columns");
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-
 struct AggParams {
     const uint8_t *blocks;
     uint32_t block_bytes;
@@ -68,61 +66,6 @@ struct AggParams {
     float *z;
     uint32_t *status;
 };
-
-__device__ __forceinline__ float bf16_bits_to_float(uint32_t bits) {
-    return __uint_as_float(bits << 16);
-}
-
-// Eight consecutive elements c0..c0+7 of a feature row (fp32 or bf16);
-// elements at or beyond `dim` read as zero.
-__device__ __forceinline__ void load8(const uint8_t *row, uint32_t dim, uint32_t is_bf16,
-                                      uint32_t vec_ok, uint32_t c0, float v[8]) {
-    if (vec_ok && c0 + 8 <= dim) {
-        if (is_bf16) {
-            const u32x4 q = *(const u32x4 *)(row + 2 * c0);
-#pragma unroll
-            for (int i = 0; i < 4; i++) {
-                v[2 * i] = bf16_bits_to_float(q[i] & 0xFFFFu);
-                v[2 * i + 1] = bf16_bits_to_float(q[i] >> 16);
-            }
-        } else {
-            const f32x4 a = *(const f32x4 *)(row + 4 * c0);
-            const f32x4 b = *(const f32x4 *)(row + 4 * c0 + 16);
-#pragma unroll
-            for (int i = 0; i < 4; i++) {
-                v[i] = a[i];
-                v[4 + i] = b[i];
-            }
-        }
-        return;
-    }
-#pragma unroll
-    for (int i = 0; i < 8; i++) {
-        const uint32_t c = c0 + i;
-        v[i] = 0.0f;
-        if (c < dim)
-            v[i] = is_bf16 ? bf16_bits_to_float(((const uint16_t *)row)[c]) : ((const float *)row)[c];
-    }
-}
-
-// Store v as its bf16 pair (hi + lo) at hi[0..7] and lo[0..7] (16 bytes each).
-__device__ __forceinline__ void store_split8(const float v[8], __bf16 *hi, __bf16 *lo) {
-    bf16x8 h, l;
-#pragma unroll
-    for (int i = 0; i < 8; i++) {
-        const __bf16 t = (__bf16)v[i];
-        h[i] = t;
-        l[i] = (__bf16)(v[i] - (float)t);
-    }
-    *(bf16x8 *)hi = h;
-    *(bf16x8 *)lo = l;
-}
-
-__device__ __forceinline__ void store_split1(float v, __bf16 *hi, __bf16 *lo) {
-    const __bf16 t = (__bf16)v;
-    *hi = t;
-    *lo = (__bf16)(v - (float)t);
-}
 
 // acc[rb] += A_rb (16 x K, from the LDS pair Ah/Al with row stride `as`)
 //          * W^T (K x 16 columns col0.., W row-major [64][ld]) for rb < nrb.
@@ -365,10 +308,6 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_fused(AggParams p) {
                 }
     }
 }
-
-uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u; }
-uint32_t pad32(uint32_t x) { return (x + 31u) & ~31u; }
-uint32_t align16(uint32_t x) { return (x + 15u) & ~15u; }
 
 // LDS layout of a tile with `rows` slot rows and `qrows` query rows.
 uint32_t agg_layout(AggParams &p, uint32_t rows, uint32_t qrows) {

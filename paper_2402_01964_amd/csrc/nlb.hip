@@ -79,26 +79,8 @@ __device__ __forceinline__ bool link_ok(const InsertParams &p, int32_t u, int32_
 // the slots of a popular node -- costs one global atomic per workgroup
 // instead of one per offer; the maximum is associative, so the result is the
 // same.  Small batches skip the merge: they have few workgroups and little
-// same-slot traffic, and the plain atomics finish sooner.
-constexpr int kResolveLinks = 1024;
-constexpr int kAggBits = 12;                      // 2 * kResolveLinks offers: load <= 1/2
-constexpr int kAggEntries = 1 << kAggBits;
-constexpr uint32_t kAggMinBatch = 65536;          // batches from this size merge in LDS
-static_assert(kAggEntries >= 4 * kResolveLinks, "aggregation table size");
-
-__device__ __forceinline__ void agg_offer(unsigned long long *agg_off, unsigned long long *agg_word,
-                                          uint64_t off, uint64_t word) {
-    const unsigned long long tag = off + 1;  // 0 marks a free entry
-    uint32_t h = (uint32_t)(((off >> 3) * kGolden) >> (64 - kAggBits));
-    for (;;) {
-        const unsigned long long prev = atomicCAS(&agg_off[h], 0ull, tag);
-        if (prev == 0ull || prev == tag) {
-            atomicMax(&agg_word[h], (unsigned long long)word);
-            return;
-        }
-        h = (h + 1) & (kAggEntries - 1);
-    }
-}
+// same-slot traffic, and the plain atomics finish sooner.  The merge table
+// is merge_max of nlb_internal.h.
 
 // Validation of link i (ranges; timestamps non-decreasing inside the batch
 // and against the last timestamp of the previous batch) and its two offers.
@@ -136,11 +118,11 @@ __global__ __launch_bounds__(kInsertThreads) void insert_resolve(InsertParams p)
 }
 
 __global__ __launch_bounds__(kInsertThreads) void insert_resolve_merged(InsertParams p) {
-    __shared__ unsigned long long agg_off[kAggEntries];
-    __shared__ unsigned long long agg_word[kAggEntries];
-    for (int k = threadIdx.x; k < kAggEntries; k += kInsertThreads) {
-        agg_off[k] = 0ull;
-        agg_word[k] = 0ull;
+    __shared__ unsigned long long merge_off[kMergeEntries];
+    __shared__ unsigned long long merge_word[kMergeEntries];
+    for (int k = threadIdx.x; k < kMergeEntries; k += kInsertThreads) {
+        merge_off[k] = 0ull;
+        merge_word[k] = 0ull;
     }
     __syncthreads();
     const uint32_t first = blockIdx.x * kResolveLinks;
@@ -149,14 +131,14 @@ __global__ __launch_bounds__(kInsertThreads) void insert_resolve_merged(InsertPa
         if (i >= p.n) break;
         uint64_t ou, wu, ov, wv;
         if (link_offers(p, i, ou, wu, ov, wv)) {
-            agg_offer(agg_off, agg_word, ou, wu);
-            agg_offer(agg_off, agg_word, ov, wv);
+            merge_max(merge_off, merge_word, ou, wu);
+            merge_max(merge_off, merge_word, ov, wv);
         }
     }
     __syncthreads();
-    for (int k = threadIdx.x; k < kAggEntries; k += kInsertThreads) {
-        const unsigned long long tag = agg_off[k];
-        if (tag) atomicMax((unsigned long long *)(p.blocks + (tag - 1)), agg_word[k]);
+    for (int k = threadIdx.x; k < kMergeEntries; k += kInsertThreads) {
+        const unsigned long long tag = merge_off[k];
+        if (tag) atomicMax((unsigned long long *)(p.blocks + (tag - 1)), merge_word[k]);
     }
 }
 
@@ -508,6 +490,9 @@ int nlb_destroy(nlb_table *h) {
         DeviceGuard guard(h->device);
         if (hipDeviceSynchronize() != hipSuccess) rc = NLB_EDEVICE;
         if (hipFree(h->blocks) != hipSuccess) rc = NLB_EDEVICE;
+        if (h->rnn_winner && hipFree(h->rnn_winner) != hipSuccess) rc = NLB_EDEVICE;
+        if (h->rnn_cand && hipFree(h->rnn_cand) != hipSuccess) rc = NLB_EDEVICE;
+        if (h->rnn_cand_node && hipFree(h->rnn_cand_node) != hipSuccess) rc = NLB_EDEVICE;
     }
     delete h;
     return rc;
@@ -555,7 +540,7 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const
     p.status = h->status;
     p.parity = (uint32_t)(h->batches & 1);
     const hipStream_t st = (hipStream_t)stream;
-    if (n >= kAggMinBatch)
+    if (n >= kMergeMinBatch)
         hipLaunchKernelGGL(insert_resolve_merged, dim3((n + kResolveLinks - 1) / kResolveLinks),
                            dim3(kInsertThreads), 0, st, p);
     else

@@ -106,6 +106,93 @@ __device__ __forceinline__ SlotLds read_slot(const uint8_t *blocks, uint32_t blo
     return sl;
 }
 
+// ---------------------------------------------------------------- LDS max-merge
+// Open-addressing LDS table that merges 64-bit maxima per global address
+// (byte offset `off`): merge_max records max(word) for off, so one global
+// atomicMax per distinct address can replace many.  kMergeEntries entries
+// hold up to half as many distinct addresses.
+constexpr int kResolveLinks = 1024;               // links merged per workgroup (two addresses each)
+constexpr int kMergeBits = 12;                    // 2 * kResolveLinks addresses: load <= 1/2
+constexpr int kMergeEntries = 1 << kMergeBits;
+constexpr uint32_t kMergeMinBatch = 65536;        // batches from this size merge in LDS
+static_assert(kMergeEntries >= 4 * kResolveLinks, "merge table size");
+
+__device__ __forceinline__ void merge_max(unsigned long long *merge_off, unsigned long long *merge_word,
+                                          uint64_t off, uint64_t word) {
+    const unsigned long long tag = off + 1;  // 0 marks a free entry
+    uint32_t h = (uint32_t)(((off >> 3) * kGolden) >> (64 - kMergeBits));
+    for (;;) {
+        const unsigned long long prev = atomicCAS(&merge_off[h], 0ull, tag);
+        if (prev == 0ull || prev == tag) {
+            atomicMax(&merge_word[h], (unsigned long long)word);
+            return;
+        }
+        h = (h + 1) & (kMergeEntries - 1);
+    }
+}
+
+// ---------------------------------------------------------------- feature rows, bf16 pairs
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float bf16_bits_to_float(uint32_t bits) {
+    return __uint_as_float(bits << 16);
+}
+
+// Eight consecutive elements c0..c0+7 of a feature row (fp32 or bf16);
+// elements at or beyond `dim` read as zero.
+__device__ __forceinline__ void load8(const uint8_t *row, uint32_t dim, uint32_t is_bf16,
+                                      uint32_t vec_ok, uint32_t c0, float v[8]) {
+    if (vec_ok && c0 + 8 <= dim) {
+        if (is_bf16) {
+            const u32x4 q = *(const u32x4 *)(row + 2 * c0);
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                v[2 * i] = bf16_bits_to_float(q[i] & 0xFFFFu);
+                v[2 * i + 1] = bf16_bits_to_float(q[i] >> 16);
+            }
+        } else {
+            const f32x4 a = *(const f32x4 *)(row + 4 * c0);
+            const f32x4 b = *(const f32x4 *)(row + 4 * c0 + 16);
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                v[i] = a[i];
+                v[4 + i] = b[i];
+            }
+        }
+        return;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+        const uint32_t c = c0 + i;
+        v[i] = 0.0f;
+        if (c < dim)
+            v[i] = is_bf16 ? bf16_bits_to_float(((const uint16_t *)row)[c]) : ((const float *)row)[c];
+    }
+}
+
+// Store v as its bf16 pair (hi + lo) at hi[0..7] and lo[0..7] (16 bytes each).
+__device__ __forceinline__ void store_split8(const float v[8], __bf16 *hi, __bf16 *lo) {
+    bf16x8 h, l;
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+        const __bf16 t = (__bf16)v[i];
+        h[i] = t;
+        l[i] = (__bf16)(v[i] - (float)t);
+    }
+    *(bf16x8 *)hi = h;
+    *(bf16x8 *)lo = l;
+}
+
+__device__ __forceinline__ void store_split1(float v, __bf16 *hi, __bf16 *lo) {
+    const __bf16 t = (__bf16)v;
+    *hi = t;
+    *lo = (__bf16)(v - (float)t);
+}
+
+inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u; }
+inline uint32_t pad32(uint32_t x) { return (x + 31u) & ~31u; }
+inline uint32_t align16(uint32_t x) { return (x + 15u) & ~15u; }
+
 uint64_t ceil_2_40_div(uint32_t d) { return ((1ull << 40) + d - 1) / d; }
 
 class DeviceGuard {
@@ -158,5 +245,12 @@ struct nlb_table {
     uint32_t *status;
     uint64_t interactions;
     uint64_t batches;
+    // Node-status update (rnn.hip), allocated on first use.
+    unsigned long long *rnn_winner;   // [N] latest pair-row code per node
+    uint32_t rnn_epoch;               // calls since the winner array was cleared
+    uint8_t *rnn_cand;                // candidate status rows by pair row
+    size_t rnn_cand_bytes;
+    int32_t *rnn_cand_node;           // winner node per pair row, else -1
+    uint64_t rnn_cand_rows;
 };
 

@@ -1,0 +1,530 @@
+// rnn.hip -- the node-status update of Sec. 4.4 (Luo & Li, arXiv 2402.01964):
+// after a link (u, v, t) with features e, each endpoint's status is updated
+// by an RNN over [r_u, r_v, t, e].  The cell is a GRU with input
+// x = [r_other ; T-enc(t) ; e] and hidden state h = r_self:
+//   r = sigmoid(W_ir x + W_hr h + b_ir + b_hr)
+//   z = sigmoid(W_iz x + W_hz h + b_iz + b_hz)
+//   n = tanh(W_in x + b_in + r * (W_hn h + b_hn))
+//   h' = (1 - z) n + z h
+// A batch is applied at once: every update reads the statuses from before
+// the batch, and a node that several links of the batch touch takes the
+// update of its latest one (larger arrival index; on a self-loop the second
+// endpoint's).
+//
+// Four launches per batch:
+//   resolve  each endpoint offers the code epoch << 32 | (2i + k + 1) of its
+//            pair row (link i, endpoint k) to winner[node] with a 64-bit
+//            atomic maximum; codes of earlier calls are smaller, so the array
+//            is never cleared.  Large batches merge their offers per node in
+//            LDS first (merge_max), as the table insertion does.
+//   gru      a workgroup takes a tile of consecutive pair rows, keeps the
+//            winners (wavefront ballot + prefix count), builds their inputs
+//            in LDS and runs both GRU products on bf16 matrix cores; the
+//            gates, the blend with h and the rounding to the status type
+//            happen in registers, and the new status goes to a candidate
+//            buffer indexed by pair row.
+//   scatter  copies each winner's candidate row over its node's status.
+// The candidate buffer is what lets the gru pass read only pre-batch
+// statuses: no status is written until every workgroup has read its inputs.
+//
+// Numerics.  fp32 activations (fp32 statuses, the time encoding, fp32 link
+// rows) enter the products as bf16 pairs hi + lo (2^-18 relative), bf16 ones
+// as a single term; the weights are bf16 and the products accumulate in fp32.
+//
+// Matrix-core mapping (v_mfma_f32_16x16x32_bf16; lane layout as in
+// aggregate.hip).  Wavefront w computes the output units 16 ub .. 16 ub + 15
+// for ub = w, w + 4, ...; for each it keeps four accumulators per 16-row
+// block -- r and z (input and hidden products summed), the input part of n
+// and the hidden part of n -- so a unit's three gates meet in one lane and
+// the cell finishes without another LDS round trip.
+#include <cstring>
+
+#include "nlb_internal.h"
+
+namespace {
+
+constexpr int kRnnThreads = 256;
+constexpr int kGruMaxBlocks = 4;                  // 16-row blocks per tile: at most 64 pair rows
+constexpr uint32_t kGruMeta = 1024;               // LDS bytes of the tile's row list
+constexpr uint32_t kGruLdsBudget = 80 * 1024;     // two workgroups per CU
+constexpr uint32_t kGruLdsMax = 160 * 1024;       // gfx950: LDS of one workgroup at most
+constexpr uint32_t kGruTargetTiles = 2048;
+constexpr int kFill = 4;                          // input units whose loads are in flight together
+
+struct ResolveParams {
+    const int32_t *src;
+    const int32_t *dst;
+    uint32_t n;
+    int64_t num_nodes;
+    unsigned long long *winner;
+    uint64_t epoch_hi;
+    uint32_t *status;
+};
+
+__device__ __forceinline__ bool endpoints_ok(int32_t u, int32_t v, int64_t num_nodes) {
+    return u >= 0 && v >= 0 && (int64_t)u < num_nodes && (int64_t)v < num_nodes;
+}
+
+__global__ __launch_bounds__(kRnnThreads) void rnn_resolve(ResolveParams p) {
+    const uint32_t i = blockIdx.x * kRnnThreads + threadIdx.x;
+    if (i >= p.n) return;
+    const int32_t u = p.src[i], v = p.dst[i];
+    if (!endpoints_ok(u, v, p.num_nodes)) {
+        atomicOr(p.status, kStatusRange);
+        return;
+    }
+    atomicMax(&p.winner[u], (unsigned long long)(p.epoch_hi | (2ull * i + 1)));
+    atomicMax(&p.winner[v], (unsigned long long)(p.epoch_hi | (2ull * i + 2)));
+}
+
+__global__ __launch_bounds__(kRnnThreads) void rnn_resolve_merged(ResolveParams p) {
+    __shared__ unsigned long long merge_off[kMergeEntries];
+    __shared__ unsigned long long merge_word[kMergeEntries];
+    for (int k = threadIdx.x; k < kMergeEntries; k += kRnnThreads) {
+        merge_off[k] = 0ull;
+        merge_word[k] = 0ull;
+    }
+    __syncthreads();
+    const uint32_t first = blockIdx.x * kResolveLinks;
+    for (uint32_t r = 0; r < kResolveLinks; r += kRnnThreads) {
+        const uint32_t i = first + r + threadIdx.x;
+        if (i >= p.n) break;
+        const int32_t u = p.src[i], v = p.dst[i];
+        if (!endpoints_ok(u, v, p.num_nodes)) {
+            atomicOr(p.status, kStatusRange);
+            continue;
+        }
+        merge_max(merge_off, merge_word, 8ull * (uint32_t)u, p.epoch_hi | (2ull * i + 1));
+        merge_max(merge_off, merge_word, 8ull * (uint32_t)v, p.epoch_hi | (2ull * i + 2));
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < kMergeEntries; k += kRnnThreads) {
+        const unsigned long long tag = merge_off[k];
+        if (tag) atomicMax(&p.winner[(tag - 1) >> 3], merge_word[k]);
+    }
+}
+
+struct GruParams {
+    const int32_t *src;
+    const int32_t *dst;
+    const uint32_t *t;
+    uint32_t n;
+    int64_t num_nodes;
+    const unsigned long long *winner;
+    uint64_t epoch_hi;
+    uint64_t first_eid;                 // arrival index (link-row index) of link 0
+    uint32_t d, d_time;
+    const float *tw, *tb;               // time encoding
+    const uint8_t *efeat;
+    int64_t edge_rows;
+    uint32_t e_dim, e_bf16, erb, e_vec;
+    const uint8_t *st;                  // statuses [N][d]
+    uint32_t s_bf16, srb, s_vec;
+    uint8_t *cand;                      // [2n][srb] candidate rows by pair row
+    int32_t *cand_node;                 // [2n] node of a winning pair row, else -1
+    uint32_t kd, off_e, kx;             // X = [r_other | T-enc | e]: columns [0,kd) [kd,off_e) [off_e,kx)
+    uint32_t lo_begin, lo_end;          // X columns with a stored lo plane
+    uint32_t h_lo;                      // fp32 statuses: H has a lo plane
+    uint32_t xs, ls, hs;                // LDS row strides (bf16 elements)
+    uint32_t rows;                      // pair rows per tile (multiple of 16, <= 64)
+    uint32_t off_xl, off_h, off_hl;     // LDS byte offsets
+    uint64_t gx_m, gh_m;                // ceil(2^40 / (kx / 8)), ceil(2^40 / (kd / 8))
+    const __bf16 *w_ih, *w_hh;
+    const float *b_ih, *b_hh;
+};
+
+__device__ __forceinline__ void store_hi8(const float v[8], __bf16 *hi) {
+    bf16x8 h;
+#pragma unroll
+    for (int i = 0; i < 8; i++) h[i] = (__bf16)v[i];
+    *(bf16x8 *)hi = h;
+}
+
+__device__ __forceinline__ float sigmoid_f32(float a) { return 1.0f / (1.0f + expf(-a)); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+// acc[g'][rb] += A_rb (16 x K from the LDS pair Ah/Al, row stride `as`; the
+// lo plane covers columns [lo_b, lo_e) with its own stride `ls`)
+//              * W_g^T for the three gate row blocks W_g = W + g * d * ld,
+// where g' = g for the r and z gates and g' = NIDX for the n gate.
+template <int NIDX>
+__device__ __forceinline__ void gate_products(f32x4 (&acc)[4][kGruMaxBlocks], uint32_t nrb,
+                                              const __bf16 *Ah, const __bf16 *Al, uint32_t as,
+                                              uint32_t ls, uint32_t lo_b, uint32_t lo_e,
+                                              const __bf16 *W, uint32_t ld, uint32_t K, uint32_t d,
+                                              uint32_t unit, uint32_t lane) {
+    const uint32_t lr = lane & 15, lk = (lane >> 4) * 8;
+    const __bf16 *w0 = W + (size_t)unit * ld + lk;
+    const size_t gstep = (size_t)d * ld;
+    for (uint32_t k0 = 0; k0 < K; k0 += 32) {
+        bf16x8 b[3];
+#pragma unroll
+        for (int g = 0; g < 3; g++) b[g] = *(const bf16x8 *)(w0 + g * gstep + k0);
+        const bool lo = k0 >= lo_b && k0 < lo_e;
+#pragma unroll
+        for (int rb = 0; rb < kGruMaxBlocks; rb++) {
+            if ((uint32_t)rb >= nrb) continue;
+            const bf16x8 a = *(const bf16x8 *)(Ah + (16u * rb + lr) * as + k0 + lk);
+#pragma unroll
+            for (int g = 0; g < 3; g++) {
+                const int gi = g == 2 ? NIDX : g;
+                acc[gi][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[g], acc[gi][rb], 0, 0, 0);
+            }
+            if (lo) {
+                const bf16x8 al = *(const bf16x8 *)(Al + (16u * rb + lr) * ls + (k0 - lo_b) + lk);
+#pragma unroll
+                for (int g = 0; g < 3; g++) {
+                    const int gi = g == 2 ? NIDX : g;
+                    acc[gi][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b[g], acc[gi][rb], 0, 0, 0);
+                }
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    uint32_t *m_row = (uint32_t *)smem;          // pair row of compacted row j
+    int32_t *m_self = (int32_t *)(m_row + 64);
+    int32_t *m_other = m_self + 64;
+    uint32_t *m_count = (uint32_t *)(m_other + 64);
+    __bf16 *Xh = (__bf16 *)(smem + kGruMeta);
+    __bf16 *Xl = (__bf16 *)(smem + p.off_xl);
+    __bf16 *Hh = (__bf16 *)(smem + p.off_h);
+    __bf16 *Hl = (__bf16 *)(smem + p.off_hl);
+
+    const uint32_t tid = threadIdx.x;
+    const uint32_t lane = tid & 63, wave = tid >> 6;
+    const uint64_t r0 = (uint64_t)blockIdx.x * p.rows;
+    const uint64_t total = 2ull * p.n;
+
+    // Winners of the tile's pair rows, compacted in order.
+    if (wave == 0) {
+        const uint64_t r = r0 + lane;
+        bool win = false;
+        int32_t self = -1, other = -1;
+        if (lane < p.rows && r < total) {
+            const uint32_t i = (uint32_t)(r >> 1);
+            const int32_t u = p.src[i], v = p.dst[i];
+            if (endpoints_ok(u, v, p.num_nodes)) {
+                self = (r & 1) ? v : u;
+                other = (r & 1) ? u : v;
+                win = p.winner[self] == (p.epoch_hi | (r + 1));
+            }
+            p.cand_node[r] = win ? self : -1;
+        }
+        const uint64_t mask = __ballot(win);
+        if (win) {
+            const uint32_t pos = (uint32_t)__popcll(mask & ((1ull << lane) - 1ull));
+            m_row[pos] = (uint32_t)r;
+            m_self[pos] = self;
+            m_other[pos] = other;
+        }
+        if (lane == 0) *m_count = (uint32_t)__popcll(mask);
+    }
+    __syncthreads();
+    const uint32_t m = *m_count;
+    if (m == 0) return;
+    const uint32_t nrb = (m + 15) / 16;
+    const uint32_t rows_p = 16 * nrb;
+
+    // Inputs: X = [r_other | T-enc(t) | e] and H = r_self; pad rows are zero.
+    const uint32_t gx = p.kx / 8;
+    const uint32_t ux = rows_p * gx;
+    for (uint32_t base = tid; base < ux; base += kRnnThreads * kFill) {
+        float v[kFill][8];
+#pragma unroll
+        for (int f = 0; f < kFill; f++) {
+            const uint32_t u = base + f * kRnnThreads;
+#pragma unroll
+            for (int i = 0; i < 8; i++) v[f][i] = 0.0f;
+            if (u >= ux) continue;
+            const uint32_t j = div_small(u, p.gx_m);
+            const uint32_t c0 = (u - j * gx) * 8;
+            if (j >= m) continue;
+            const uint32_t link = m_row[j] >> 1;
+            if (c0 < p.kd) {
+                load8(p.st + (size_t)m_other[j] * p.srb, p.d, p.s_bf16, p.s_vec, c0, v[f]);
+            } else if (c0 < p.off_e) {
+                const uint32_t k = c0 - p.kd;
+                const float tf = (float)p.t[link];
+#pragma unroll
+                for (int i = 0; i < 8; i++)
+                    if (k + i < p.d_time) v[f][i] = cos_fp32(__builtin_fmaf(p.tw[k + i], tf, p.tb[k + i]));
+            } else {
+                const uint64_t e = p.first_eid + link;
+                if (e < (uint64_t)p.edge_rows)
+                    load8(p.efeat + (size_t)e * p.erb, p.e_dim, p.e_bf16, p.e_vec, c0 - p.off_e, v[f]);
+            }
+        }
+#pragma unroll
+        for (int f = 0; f < kFill; f++) {
+            const uint32_t u = base + f * kRnnThreads;
+            if (u >= ux) continue;
+            const uint32_t j = div_small(u, p.gx_m);
+            const uint32_t c0 = (u - j * gx) * 8;
+            if (c0 >= p.lo_begin && c0 < p.lo_end)
+                store_split8(v[f], Xh + (size_t)j * p.xs + c0, Xl + (size_t)j * p.ls + (c0 - p.lo_begin));
+            else
+                store_hi8(v[f], Xh + (size_t)j * p.xs + c0);
+        }
+    }
+    const uint32_t gh = p.kd / 8;
+    const uint32_t uh = rows_p * gh;
+    for (uint32_t u = tid; u < uh; u += kRnnThreads) {
+        const uint32_t j = div_small(u, p.gh_m);
+        const uint32_t c0 = (u - j * gh) * 8;
+        float v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (j < m) load8(p.st + (size_t)m_self[j] * p.srb, p.d, p.s_bf16, p.s_vec, c0, v);
+        if (p.h_lo)
+            store_split8(v, Hh + (size_t)j * p.hs + c0, Hl + (size_t)j * p.hs + c0);
+        else
+            store_hi8(v, Hh + (size_t)j * p.hs + c0);
+    }
+    __syncthreads();
+
+    const uint32_t d = p.d;
+    const uint32_t units = (d + 15) / 16;
+    for (uint32_t ub = wave; ub < units; ub += kRnnThreads / 64) {
+        const uint32_t j = 16 * ub + (lane & 15);
+        const uint32_t jr = j < d ? j : d - 1;   // rows past d are read, never used
+        f32x4 acc[4][kGruMaxBlocks];   // r, z, input part of n, hidden part of n
+#pragma unroll
+        for (int g = 0; g < 4; g++)
+#pragma unroll
+            for (int rb = 0; rb < kGruMaxBlocks; rb++) acc[g][rb] = f32x4(0.0f);
+        gate_products<2>(acc, nrb, Xh, Xl, p.xs, p.ls, p.lo_begin, p.lo_end, p.w_ih, p.kx, p.kx, d, jr,
+                         lane);
+        gate_products<3>(acc, nrb, Hh, Hl, p.hs, p.hs, 0, p.h_lo ? p.kd : 0, p.w_hh, p.kd, p.kd, d, jr,
+                         lane);
+        if (j >= d) continue;
+        const float br = p.b_ih[j] + p.b_hh[j];
+        const float bz = p.b_ih[d + j] + p.b_hh[d + j];
+        const float bin = p.b_ih[2 * d + j];
+        const float bhn = p.b_hh[2 * d + j];
+#pragma unroll
+        for (int rb = 0; rb < kGruMaxBlocks; rb++) {
+            if ((uint32_t)rb >= nrb) continue;
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const uint32_t row = 16u * rb + 4u * (lane >> 4) + i;
+                if (row >= m) continue;
+                const float rg = sigmoid_f32(acc[0][rb][i] + br);
+                const float zg = sigmoid_f32(acc[1][rb][i] + bz);
+                const float ng = tanhf(acc[2][rb][i] + bin + rg * (acc[3][rb][i] + bhn));
+                const uint8_t *srow = p.st + (size_t)m_self[row] * p.srb;
+                const float h = p.s_bf16 ? bf16_bits_to_float(((const uint16_t *)srow)[j])
+                                         : ((const float *)srow)[j];
+                const float out = (1.0f - zg) * ng + zg * h;
+                uint8_t *crow = p.cand + (size_t)m_row[row] * p.srb;
+                if (p.s_bf16)
+                    ((uint16_t *)crow)[j] = f32_to_bf16_rne(out);
+                else
+                    ((float *)crow)[j] = out;
+            }
+        }
+    }
+}
+
+// Status rows of the winners: cand row r -> status row cand_node[r], in
+// units of `w` bytes (upr units per row), grid-stride.
+__global__ __launch_bounds__(kRnnThreads) void rnn_scatter(const uint8_t *cand, const int32_t *cand_node,
+                                                          uint8_t *st, uint64_t rows, uint32_t srb,
+                                                          uint32_t w, uint32_t upr) {
+    const uint64_t units = rows * upr;
+    for (uint64_t u = (uint64_t)blockIdx.x * kRnnThreads + threadIdx.x; u < units;
+         u += (uint64_t)gridDim.x * kRnnThreads) {
+        const uint64_t r = u / upr;
+        const int32_t node = cand_node[r];
+        if (node < 0) continue;
+        const uint32_t c = (uint32_t)(u - r * upr) * w;
+        const uint8_t *from = cand + r * srb + c;
+        uint8_t *to = st + (size_t)node * srb + c;
+        if (w == 16)
+            *(u32x4 *)to = *(const u32x4 *)from;
+        else if (w == 8)
+            *(u32x2 *)to = *(const u32x2 *)from;
+        else if (w == 4)
+            *(uint32_t *)to = *(const uint32_t *)from;
+        else
+            *(uint16_t *)to = *(const uint16_t *)from;
+    }
+}
+
+// Zero fill of the winner array (on the rare wrap of the call counter).
+__global__ __launch_bounds__(kRnnThreads) void rnn_clear(unsigned long long *a, uint64_t n) {
+    for (uint64_t i = (uint64_t)blockIdx.x * kRnnThreads + threadIdx.x; i < n;
+         i += (uint64_t)gridDim.x * kRnnThreads)
+        a[i] = 0ull;
+}
+
+// LDS layout of a tile of `rows` pair rows; returns its size in bytes.
+uint32_t gru_layout(GruParams &p, uint32_t rows) {
+    p.rows = rows;
+    p.off_xl = align16(kGruMeta + rows * p.xs * 2u);
+    p.off_h = align16(p.off_xl + (p.lo_end > p.lo_begin ? rows * p.ls * 2u : 0u));
+    p.off_hl = align16(p.off_h + rows * p.hs * 2u);
+    return p.off_hl + (p.h_lo ? rows * p.hs * 2u : 0u);
+}
+
+// Per-table working memory of the update, grown on demand.
+int rnn_reserve(nlb_table *h, uint64_t pair_rows, uint32_t srb) {
+    if (!h->rnn_winner) {
+        const size_t bytes = (size_t)h->num_nodes * 8u;
+        if (hipMalloc((void **)&h->rnn_winner, bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            h->rnn_winner = nullptr;
+            return NLB_ENOMEM;
+        }
+        if (hipMemset(h->rnn_winner, 0, bytes) != hipSuccess) return NLB_EDEVICE;
+        h->rnn_epoch = 0;
+    }
+    const size_t cbytes = (size_t)pair_rows * srb;
+    if (cbytes > h->rnn_cand_bytes || pair_rows > h->rnn_cand_rows) {
+        // Earlier updates may still read the old buffers.
+        if (hipDeviceSynchronize() != hipSuccess) return NLB_EDEVICE;
+        (void)hipFree(h->rnn_cand);
+        (void)hipFree(h->rnn_cand_node);
+        h->rnn_cand = nullptr;
+        h->rnn_cand_node = nullptr;
+        h->rnn_cand_bytes = 0;
+        h->rnn_cand_rows = 0;
+        if (hipMalloc((void **)&h->rnn_cand, cbytes) != hipSuccess ||
+            hipMalloc((void **)&h->rnn_cand_node, (size_t)pair_rows * 4u) != hipSuccess) {
+            (void)hipGetLastError();
+            (void)hipFree(h->rnn_cand);
+            h->rnn_cand = nullptr;
+            h->rnn_cand_node = nullptr;
+            return NLB_ENOMEM;
+        }
+        h->rnn_cand_bytes = cbytes;
+        h->rnn_cand_rows = pair_rows;
+    }
+    return NLB_OK;
+}
+
+}  // namespace
+
+extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, const uint32_t *t,
+                              uint32_t n, uint64_t first_eid, const nlb_gru_weights *wts, void *status,
+                              void *stream) {
+    if (!h || !wts) return NLB_EINVAL;
+    if (n == 0) return NLB_OK;
+    if (!src || !dst || !t || !status) return NLB_EINVAL;
+    if (n >= (1u << 31)) return NLB_EINVAL;
+    const int32_t sd = wts->status_dtype, ed = wts->edge_dtype;
+    if ((sd != NLB_DTYPE_F32 && sd != NLB_DTYPE_BF16) || (ed != NLB_DTYPE_F32 && ed != NLB_DTYPE_BF16))
+        return NLB_EINVAL;
+    if (wts->status_dim < 1 || wts->status_dim > NLB_RNN_MAX_DIM) return NLB_EINVAL;
+    if (!wts->w_ih || !wts->w_hh || !wts->b_ih || !wts->b_hh) return NLB_EINVAL;
+    if (((uintptr_t)wts->w_ih | (uintptr_t)wts->w_hh) % 16 || ((uintptr_t)wts->b_ih | (uintptr_t)wts->b_hh) % 4)
+        return NLB_EINVAL;
+    const uint32_t s_es = sd == NLB_DTYPE_BF16 ? 2 : 4, e_es = ed == NLB_DTYPE_BF16 ? 2 : 4;
+    if ((uintptr_t)status % s_es || h->erb % e_es) return NLB_EINVAL;
+    DeviceGuard guard(h->device);
+    if (!guard.ok()) return NLB_EDEVICE;
+
+    GruParams p;
+    std::memset(&p, 0, sizeof(p));
+    p.src = src;
+    p.dst = dst;
+    p.t = t;
+    p.n = n;
+    p.num_nodes = h->num_nodes;
+    p.first_eid = first_eid;
+    p.d = (uint32_t)wts->status_dim;
+    p.d_time = h->d_time;
+    p.tw = h->w;
+    p.tb = h->b;
+    p.efeat = h->efeat;
+    p.edge_rows = h->edge_rows;
+    p.e_dim = h->erb / e_es;
+    p.e_bf16 = ed == NLB_DTYPE_BF16;
+    p.erb = h->erb;
+    p.e_vec = h->erb % 16 == 0 && (uintptr_t)h->efeat % 16 == 0;
+    p.st = (const uint8_t *)status;
+    p.s_bf16 = sd == NLB_DTYPE_BF16;
+    p.srb = p.d * s_es;
+    p.s_vec = p.srb % 16 == 0 && (uintptr_t)status % 16 == 0;
+    p.kd = pad32(p.d);
+    p.off_e = p.kd + pad32(p.d_time);
+    p.kx = p.off_e + pad32(p.e_dim);
+    // Columns whose values are not bf16 already: fp32 statuses, the time
+    // encoding, fp32 link rows.  They form one range because the time
+    // encoding sits between the other two segments.
+    const bool lo_s = !p.s_bf16, lo_t = p.d_time > 0, lo_e = p.e_dim > 0 && !p.e_bf16;
+    p.lo_begin = lo_s ? 0 : (lo_t ? p.kd : (lo_e ? p.off_e : 0));
+    p.lo_end = lo_e ? p.kx : (lo_t ? p.off_e : (lo_s ? p.kd : 0));
+    p.h_lo = lo_s;
+    p.xs = p.kx + 8;
+    p.ls = (p.lo_end - p.lo_begin) + 8;
+    p.hs = p.kd + 8;
+    p.gx_m = ceil_2_40_div(p.kx / 8);
+    p.gh_m = ceil_2_40_div(p.kd / 8);
+    p.w_ih = (const __bf16 *)wts->w_ih;
+    p.w_hh = (const __bf16 *)wts->w_hh;
+    p.b_ih = wts->b_ih;
+    p.b_hh = wts->b_hh;
+
+    // Tile: enough tiles to fill the GPU, at most 64 pair rows, within the
+    // LDS budget of two workgroups per CU (a 16-row tile may use more).
+    const uint64_t pairs = 2ull * n;
+    uint32_t want = (uint32_t)pad16((uint32_t)((pairs + kGruTargetTiles - 1) / kGruTargetTiles));
+    if (want > 16u * kGruMaxBlocks) want = 16u * kGruMaxBlocks;
+    uint32_t rows = 0, lds = 0;
+    for (uint32_t r = want; r >= 16 && rows == 0; r -= 16) {
+        GruParams trial = p;
+        const uint32_t bytes = gru_layout(trial, r);
+        if (bytes <= (r == 16 ? kGruLdsMax : kGruLdsBudget)) {
+            rows = r;
+            lds = bytes;
+        }
+    }
+    if (rows == 0) return NLB_EINVAL;   // one 16-row tile does not fit the LDS
+    gru_layout(p, rows);
+
+    int rc = rnn_reserve(h, pairs, p.srb);
+    if (rc != NLB_OK) return rc;
+    if (h->rnn_epoch == 0xFFFFFFFFu) {
+        hipLaunchKernelGGL(rnn_clear, dim3(4096), dim3(kRnnThreads), 0, (hipStream_t)stream, h->rnn_winner,
+                           (uint64_t)h->num_nodes);
+        h->rnn_epoch = 0;
+    }
+    h->rnn_epoch++;
+    const uint64_t epoch_hi = (uint64_t)h->rnn_epoch << 32;
+    p.winner = h->rnn_winner;
+    p.epoch_hi = epoch_hi;
+    p.cand = h->rnn_cand;
+    p.cand_node = h->rnn_cand_node;
+
+    ResolveParams rp = {src, dst, n, h->num_nodes, h->rnn_winner, epoch_hi, h->status};
+    if (n >= kMergeMinBatch)
+        hipLaunchKernelGGL(rnn_resolve_merged, dim3((n + kResolveLinks - 1) / kResolveLinks),
+                           dim3(kRnnThreads), 0, (hipStream_t)stream, rp);
+    else
+        hipLaunchKernelGGL(rnn_resolve, dim3((n + kRnnThreads - 1) / kRnnThreads), dim3(kRnnThreads), 0,
+                           (hipStream_t)stream, rp);
+    if (lds > 64u * 1024u &&
+        hipFuncSetAttribute((const void *)rnn_gru, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)kGruLdsMax) != hipSuccess)
+        return NLB_EDEVICE;
+    hipLaunchKernelGGL(rnn_gru, dim3((unsigned)((pairs + rows - 1) / rows)), dim3(kRnnThreads), lds,
+                       (hipStream_t)stream, p);
+    uint32_t w = 2;
+    for (uint32_t c = 16; c >= 4; c /= 2)
+        if (p.srb % c == 0 && (uintptr_t)status % c == 0 && (uintptr_t)h->rnn_cand % c == 0) {
+            w = c;
+            break;
+        }
+    const uint32_t upr = p.srb / w;
+    const uint64_t blocks = (pairs * upr + kRnnThreads - 1) / kRnnThreads;
+    hipLaunchKernelGGL(rnn_scatter, dim3((unsigned)(blocks < 65536 ? blocks : 65536)),
+                       dim3(kRnnThreads), 0, (hipStream_t)stream, (const uint8_t *)h->rnn_cand,
+                       (const int32_t *)h->rnn_cand_node, (uint8_t *)status, pairs, p.srb, w, upr);
+    if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
+    return NLB_OK;
+}

@@ -1,0 +1,297 @@
+"""Node-status GRU update (Sec. 4.4) on the GPU vs the fp64 oracle.
+
+Each comparison starts both sides from the same statuses (the GPU's, copied
+to the host) and applies one batch: an fp32 status must be within 1e-4 of
+the oracle's, a bf16 status within 1e-4 plus one bf16 rounding (2^-7
+relative) -- see nlb_rnn_update in include/nlb.h.  Batch semantics
+(pre-batch reads, latest link wins) are exercised by hubs, repeats and
+self-loops; the large-sparse shape at its full batch and node count is
+checked on sampled nodes against single-link oracle updates of their
+winning links, found on the host.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_helpers import feat_to_dev, host_np, make_gpu_table, to_dev
+
+pytestmark = pytest.mark.gpu
+
+RNN_TOL = 1e-4          # fp32 status, absolute
+BF16_REL = 2.0 ** -7    # one bf16 rounding
+
+
+def _log(*a):
+    print("[rnn]", *a, flush=True)
+
+
+def bf16_to_f32(bits):
+    return (np.asarray(bits, np.uint32) << 16).view(np.float32)
+
+
+def compare_status(g, o, what=""):
+    """g, o: host arrays (float32, or uint16 bf16 bits) of the same rows."""
+    if g.dtype == np.uint16:
+        gf, of = bf16_to_f32(g).astype(np.float64), bf16_to_f32(o).astype(np.float64)
+        diff = np.abs(gf - of)
+        bound = RNN_TOL + BF16_REL * np.abs(of)
+        assert (diff <= bound).all(), f"{what}: bf16 status off by {diff.max():.3e}"
+        frac = float(np.mean(g != o))
+        assert frac < 0.02, f"{what}: {frac:.3%} of bf16 statuses differ"
+        return float(diff.max()), frac
+    err = float(np.abs(g.astype(np.float64) - o.astype(np.float64)).max()) if g.size else 0.0
+    assert err <= RNN_TOL, f"{what}: fp32 status off by {err:.3e}"
+    return err, 0.0
+
+
+def _weights_dev(W):
+    return {k: (to_dev(v.view(np.int16)) if v.dtype == np.uint16 else to_dev(v)) for k, v in W.items()}
+
+
+def _initial_status(w, d, dtype, seed):
+    if w.node_dim and d == w.node_dim and dtype == w.node_dtype:
+        return synth.host_features(w, "node")
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((w.num_nodes, d)).astype(np.float32)
+    return synth._to_bf16_bits(x) if dtype == "bf16" else x
+
+
+def _setup(w, d=None, dtype=None, status_seed=7):
+    """GPU table (time encoding and link rows of w), status tensor, host
+    copies of the link rows, and weights for a status of width d."""
+    sd, sdt = synth.status_spec(w)
+    d, dtype = d or sd, dtype or sdt
+    ef = synth.host_features(w, "edge") if w.edge_dim else None
+    ef_d = feat_to_dev(ef, w.edge_dtype) if ef is not None else None
+    g = make_gpu_table(w, ef_d, None)
+    st = feat_to_dev(_initial_status(w, d, dtype, status_seed), dtype)
+    W = synth.gru_weights_for(d, w.d_time, w.edge_dim, 6000 + w.key)
+    return g, st, ef, W, _weights_dev(W)
+
+
+def _check_batch(g, st, ef, W, Wd, fw, fb, src, dst, t, e0, what):
+    """One batch on both sides from the GPU's current statuses."""
+    import torch
+    pre = host_np(st).copy()
+    g.rnn_update(to_dev(src), to_dev(dst), to_dev(t), e0, Wd, st)
+    torch.cuda.synchronize()
+    want = oracle.gru_update(pre.copy(), src, dst, t, e0, fw, fb, ef, W)
+    got = host_np(st)
+    touched = np.unique(np.concatenate([src, dst]))
+    untouched = np.setdiff1d(np.arange(len(pre)), touched)
+    assert np.array_equal(got[untouched], pre[untouched]), f"{what}: untouched rows changed"
+    return compare_status(got[touched], want[touched], what)
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_rnn_matches_oracle(k):
+    """Every workload shape (fp32 status of width 100 with fp32 / bf16 link
+    rows, bf16 node-feature statuses of width 128), several consecutive
+    batches of the workload's batch size (at most 4000 links), restarted
+    from the GPU's statuses before each."""
+    base = synth.workload(k)
+    w = dataclasses.replace(synth.scaled(base, 4 * min(base.batch, 4000),
+                                         num_nodes=min(base.num_nodes, 200000)),
+                            batch=min(base.batch, 4000))
+    src, dst, t, _ = synth.host_links(w)
+    g, st, ef, W, Wd = _setup(w)
+    fw, fb = synth.time_params(w)
+    for b in range(w.batches):
+        lo, hi = w.batch_range(b)
+        err, frac = _check_batch(g, st, ef, W, Wd, fw, fb, src[lo:hi], dst[lo:hi], t[lo:hi], lo,
+                                 f"workload {k} batch {b}")
+        _log(f"workload {k} batch {b}: max err {err:.3e}, bf16 mismatches {frac:.3%}")
+    assert g.status() == 0
+
+
+def test_rnn_continuous_fp32_stream():
+    """Small-bipartite shape, 20 batches in a row on both sides without
+    restarting: the per-batch differences stay bounded (the cell contracts
+    them: |dh'/dh| < 1 on average)."""
+    import torch
+    base = synth.workload(2)
+    w = synth.scaled(base, 20 * base.batch)
+    src, dst, t, _ = synth.host_links(w)
+    g, st, ef, W, Wd = _setup(w)
+    fw, fb = synth.time_params(w)
+    host = host_np(st).copy()
+    for b in range(w.batches):
+        lo, hi = w.batch_range(b)
+        g.rnn_update(to_dev(src[lo:hi]), to_dev(dst[lo:hi]), to_dev(t[lo:hi]), lo, Wd, st)
+        oracle.gru_update(host, src[lo:hi], dst[lo:hi], t[lo:hi], lo, fw, fb, ef, W)
+    torch.cuda.synchronize()
+    err = float(np.abs(host_np(st).astype(np.float64) - host).max())
+    _log(f"continuous 20 batches: max err {err:.3e}")
+    assert err <= 2 * RNN_TOL
+
+
+def _small_table(N, d_time=12, edge=None, seed=3):
+    import paper_2402_01964_amd as nlb
+    rng = np.random.default_rng(seed)
+    fw = (10.0 ** -rng.uniform(0, 6, d_time)).astype(np.float32)
+    fb = rng.uniform(-np.pi, np.pi, d_time).astype(np.float32)
+    tw, tb = (to_dev(fw), to_dev(fb)) if d_time else (None, None)
+    return nlb.Table(N, 4, 0.5, 1, time_w=tw, time_b=tb, edge_feat=edge), fw, fb
+
+
+@pytest.mark.parametrize("n", [1000, 70000])
+def test_rnn_hub_repeats_and_self_loops(n):
+    """50 nodes, half of all endpoints on node 0, 5% self-loops: nearly
+    every node is touched many times per batch and the latest link must
+    win.  70000 links take the LDS-merged resolve path."""
+    rng = np.random.default_rng(n)
+    N, d = 50, 40
+    src = np.where(rng.random(n) < 0.5, 0, rng.integers(0, N, n)).astype(np.int32)
+    dst = rng.integers(0, N, n).astype(np.int32)
+    loops = rng.random(n) < 0.05
+    dst[loops] = src[loops]
+    t = np.sort(rng.integers(0, 10**7, n)).astype(np.uint32)
+    ef32 = rng.standard_normal((n + 10, 24)).astype(np.float32)
+    g, fw, fb = _small_table(N, edge=to_dev(ef32))
+    st = to_dev(rng.standard_normal((N, d)).astype(np.float32))
+    W = synth.gru_weights_for(d, 12, 24, seed=5)
+    Wd = _weights_dev(W)
+    for call in range(3):   # later calls must not see earlier calls' winners
+        err, _ = _check_batch(g, st, ef32, W, Wd, fw, fb, src, dst, t, 10, f"hub n={n} call {call}")
+        _log(f"hub n={n} call {call}: max err {err:.3e}")
+    assert g.status() == 0
+
+
+@pytest.mark.parametrize("d,dtype", [(1, "f32"), (17, "bf16"), (17, "f32"), (100, "bf16"),
+                                     (160, "f32"), (300, "bf16")])
+def test_rnn_status_widths_and_types(d, dtype):
+    """Widths that are not multiples of 16 or 32, odd bf16 rows (2-byte
+    copies), wide statuses (several output blocks per wavefront); bf16 link
+    rows of width 10 (20-byte rows: no 16-byte loads)."""
+    rng = np.random.default_rng(d)
+    N, n = 3000, 2500
+    ebits = synth._to_bf16_bits(rng.standard_normal((n, 10)).astype(np.float32))
+    g, fw, fb = _small_table(N, d_time=20, edge=feat_to_dev(ebits, "bf16"))
+    x = rng.standard_normal((N, d)).astype(np.float32)
+    host = synth._to_bf16_bits(x) if dtype == "bf16" else x
+    st = feat_to_dev(host, dtype)
+    W = synth.gru_weights_for(d, 20, 10, seed=d + 1)
+    Wd = _weights_dev(W)
+    src = rng.integers(0, N, n).astype(np.int32)
+    dst = rng.integers(0, N, n).astype(np.int32)
+    t = np.sort(rng.integers(0, 2**30, n)).astype(np.uint32)
+    err, frac = _check_batch(g, st, ebits, W, Wd, fw, fb, src, dst, t, 0, f"d={d} {dtype}")
+    _log(f"d={d} {dtype}: max err {err:.3e}, bf16 mismatches {frac:.3%}")
+
+
+def test_rnn_without_time_or_link_rows_and_rows_past_the_end():
+    """A table with no time encoding and no link rows (x = r_other only); and
+    link rows past the end of the link table read as zeros."""
+    import torch
+    rng = np.random.default_rng(11)
+    N, d, n = 500, 33, 400
+    g, fw, fb = _small_table(N, d_time=0)
+    st = to_dev(rng.standard_normal((N, d)).astype(np.float32))
+    W = synth.gru_weights_for(d, 0, 0, seed=2)
+    src = rng.integers(0, N, n).astype(np.int32)
+    dst = rng.integers(0, N, n).astype(np.int32)
+    t = np.arange(n, dtype=np.uint32)
+    _check_batch(g, st, None, W, _weights_dev(W), fw, fb, src, dst, t, 0, "no time, no rows")
+
+    ef32 = rng.standard_normal((100, 8)).astype(np.float32)
+    g2, fw2, fb2 = _small_table(N, d_time=4, edge=to_dev(ef32))
+    st2 = to_dev(rng.standard_normal((N, d)).astype(np.float32))
+    W2 = synth.gru_weights_for(d, 4, 8, seed=3)
+    padded = np.zeros((60 + n, 8), np.float32)   # rows 60 .. 99 real, the rest zero
+    padded[60:100] = ef32[60:100]
+    pre = host_np(st2).copy()
+    g2.rnn_update(to_dev(src), to_dev(dst), to_dev(t), 60, _weights_dev(W2), st2)
+    torch.cuda.synchronize()
+    want = oracle.gru_update(pre, src, dst, t, 60, fw2, fb2, padded, W2)
+    touched = np.unique(np.concatenate([src, dst]))
+    compare_status(host_np(st2)[touched], want[touched], "rows past the end")
+
+
+def test_rnn_out_of_range_link_is_skipped_and_flagged():
+    import torch
+    rng = np.random.default_rng(12)
+    N, d, n = 200, 16, 100
+    g, fw, fb = _small_table(N, d_time=8)
+    st = to_dev(rng.standard_normal((N, d)).astype(np.float32))
+    W = synth.gru_weights_for(d, 8, 0, seed=4)
+    src = rng.integers(0, N, n).astype(np.int32)
+    dst = rng.integers(0, N, n).astype(np.int32)
+    dst[-1] = N   # last link out of range
+    t = np.arange(n, dtype=np.uint32)
+    pre = host_np(st).copy()
+    g.rnn_update(to_dev(src), to_dev(dst), to_dev(t), 0, _weights_dev(W), st)
+    torch.cuda.synchronize()
+    want = oracle.gru_update(pre.copy(), src[:-1], dst[:-1], t[:-1], 0, fw, fb, None, W)
+    compare_status(host_np(st), want, "out of range")
+    import paper_2402_01964_amd as nlb
+    assert g.status() == nlb.NLB_ERANGE
+    assert g.status() == 0
+
+
+def test_rnn_argument_errors():
+    import torch
+    import paper_2402_01964_amd as nlb
+    g, _, _ = _small_table(10, d_time=4)
+    W = _weights_dev(synth.gru_weights_for(8, 4, 0, seed=1))
+    z = torch.zeros(3, dtype=torch.int32, device="cuda")
+    st = torch.zeros((10, 8), dtype=torch.float32, device="cuda")
+    g.rnn_update(z[:0], z[:0], z[:0], 0, W, st)   # empty batch: no-op
+    with pytest.raises(nlb.NLBError) as e:
+        g.rnn_update(z, z, z, 0, W, torch.zeros((10, 2000), dtype=torch.float32, device="cuda"))
+    assert e.value.code == nlb.NLB_EINVAL
+    bad = dict(W)
+    bad["w_ih"] = torch.zeros(W["w_ih"].numel() + 8, dtype=torch.int16, device="cuda")[1:1 + W["w_ih"].numel()]
+    with pytest.raises(nlb.NLBError) as e:
+        g.rnn_update(z, z, z, 0, bad, st)
+    assert e.value.code == nlb.NLB_EINVAL
+    torch.cuda.synchronize()
+    assert not st.any()
+
+
+def test_rnn_large_sparse_full_batch_sampled():
+    """Large-sparse shape at full size: 120M nodes with bf16 node-feature
+    statuses of width 128, one batch of 100,000 links from mid-stream.  For
+    600 sampled touched nodes the winning link is found on the host (the
+    latest occurrence among the batch's endpoints) and the oracle applies
+    that single link to the node's pre-batch rows."""
+    import torch
+    w = synth.workload(5)
+    b = w.batches // 2
+    lo, hi = w.batch_range(b)
+    src, dst, t, _ = synth.host_links(w, lo, hi)
+    _log(f"large-sparse batch {b}: {hi - lo} links, {w.num_nodes} nodes")
+    st = synth.device_features(w, "node")
+    g = make_gpu_table(w, None, st)
+    d = w.node_dim
+    W = synth.gru_weights(w)
+    fw, fb = synth.time_params(w)
+    rng = np.random.default_rng(13)
+    ends = np.stack([src, dst], 1).reshape(-1)              # pair row r = 2i + k
+    last = {}
+    for r, node in enumerate(ends.tolist()):
+        last[node] = r
+    nodes = rng.choice(np.array(sorted(last)), 600, replace=False)
+    rows = np.array([last[x] for x in nodes])
+    links = rows // 2
+    others = np.where(rows % 2 == 0, dst[links], src[links])
+    idx = torch.from_numpy(np.concatenate([nodes, others]).astype(np.int64)).cuda()
+    pre = host_np(st[idx]).copy()
+    g.rnn_update(to_dev(src), to_dev(dst), to_dev(t), lo, _weights_dev(W), st)
+    torch.cuda.synchronize()
+    got = host_np(st[idx[:len(nodes)]])
+    want = np.empty_like(got)
+    for j in range(len(nodes)):
+        i = int(links[j])
+        mini = np.stack([pre[j], pre[len(nodes) + j]])        # [self, other]
+        if nodes[j] == others[j]:
+            mini = mini[:1].copy()
+            oracle.gru_update(mini, [0], [0], t[i:i + 1], 0, fw, fb, None, W)
+        else:
+            oracle.gru_update(mini, [0], [1], t[i:i + 1], 0, fw, fb, None, W)
+        want[j] = mini[0]
+    err, frac = compare_status(got, want, "large-sparse sampled")
+    _log(f"large-sparse sampled: max err {err:.3e}, bf16 mismatches {frac:.3%}")
+    assert g.status() == 0
