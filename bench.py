@@ -43,6 +43,10 @@ def parse():
     ap.add_argument("--aggregate", action="store_true",
                     help="retrieve with the fused eq. (4) attention aggregation (nlb_aggregate, "
                          "random weights) instead of nlb_sample, and report that kernel")
+    ap.add_argument("--rnn", action="store_true",
+                    help="also update the node statuses after every batch (Sec. 4.4 GRU, "
+                         "nlb_rnn_update, random weights): the node-feature rows when the workload "
+                         "has them, else an fp32 status table of width 100")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="before the benchmark, run a plain elementwise copy of this many MiB "
                          "five times (a known-traffic kernel for calibrating HBM counters)")
@@ -106,6 +110,21 @@ def aggregate_bytes(w, valid_slots, queries, hidden=64):
     the table slots, the rows of valid slots and the self row; Z written."""
     erb, nrb = w.row_bytes("edge"), w.row_bytes("node")
     return queries * (8 + 12 * w.s + nrb + 4 * hidden) + valid_slots * (erb + nrb)
+
+
+def rnn_flops(w, d, winners):
+    """Algorithmic matrix FLOPs of one status update: for each node updated
+    (the winners: distinct endpoints of the batch), the GRU's input and
+    hidden products, 2 * 3d * (d + d_time + edge_dim) + 2 * 3d * d."""
+    return winners * 2 * 3 * d * (2 * d + w.d_time + w.edge_dim)
+
+
+def rnn_bytes(w, d, status_bytes, links, winners):
+    """Algorithmic HBM bytes of one status update: link ids and times; per
+    winner its own and its partner's status row and its link row read, and
+    its new row written."""
+    srb = d * status_bytes
+    return links * 12 + winners * (3 * srb + w.row_bytes("edge"))
 
 
 def insert_bytes(links):
@@ -226,6 +245,16 @@ def main():
     hop2_out = None
     if args.hop2:
         hop2_out = table.alloc_outputs(Qmax * w.s, want=("nbr", "eid", "ts"))
+    gru_w = status = None
+    if args.rnn:
+        d_r, dt_r = synth.status_spec(w)
+        gru_w = {k: (torch.from_numpy(v.view(np.int16)) if v.dtype == np.uint16 else
+                     torch.from_numpy(v)).to(dev) for k, v in synth.gru_weights(w).items()}
+        if nf is not None:
+            status = nf                     # the gathered node rows are the statuses
+        else:
+            status = torch.empty((w.num_nodes, d_r), dtype=torch.float32, device=dev)
+            status.normal_(generator=torch.Generator(device=dev).manual_seed(7000 + w.key))
     setup_s = time.perf_counter() - t_setup
 
     def step(b, nbr_out):
@@ -239,13 +268,18 @@ def main():
         table.sample_into(q, tq, o)
         return s_, d_, t_, n
 
+    def update(b, s_, d_, t_):
+        if status is not None:
+            table.rnn_update(s_, d_, t_, b * w.batch, gru_w, status)
+
     for k in range(W):
         s_, d_, t_, _ = step(start + k, nbr_all[0])
         table.insert(s_, d_, t_)
+        update(start + k, s_, d_, t_)
     torch.cuda.synchronize()
 
     print(f"bench: warm-up done; timing {K} steps", file=sys.stderr, flush=True)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
     qcount = []
     t0 = time.perf_counter()
     for k in range(K):
@@ -260,6 +294,8 @@ def main():
         ev[k][2].record()
         table.insert(s_, d_, t_)
         ev[k][3].record()
+        update(b, s_, d_, t_)
+        ev[k][4].record()
         qcount.append(n)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
@@ -268,6 +304,7 @@ def main():
     sample_ms = np.array([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)])
     hop2_ms = np.array([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)])
     insert_ms = np.array([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)])
+    rnn_ms = np.array([ev[k][3].elapsed_time(ev[k][4]) for k in range(K)])
     links = sum(n // 3 for n in qcount)
     queries = sum(qcount)
     if agg_w is not None:
@@ -346,6 +383,26 @@ def main():
                        "roofline": {"bound": "hbm", "achieved": hach, "peak": PEAK_HBM_GBPS,
                                     "unit": "GB/s", "frac": hach / PEAK_HBM_GBPS}}
         res["value_note"] = "value includes the second-hop launches (--hop2)"
+    if status is not None:
+        # Winners per timed batch (distinct endpoints), counted after timing.
+        winners = 0
+        for k in range(K):
+            s_, d_, _, _, _ = synth.batch_views(w, nodes, ts, start + W + k)
+            winners += int(torch.unique(torch.cat([s_, d_])).numel())
+        d_r = status.shape[1]
+        fl = rnn_flops(w, d_r, winners)
+        rb = rnn_bytes(w, d_r, status.element_size(), links, winners)
+        t_s = rnn_ms.sum() * 1e-3
+        res["rnn"] = {"kernels": "rnn_resolve(_merged) + rnn_gru + rnn_scatter",
+                      "status": f"{d_r} x {str(status.dtype).replace('torch.', '')}",
+                      "links_per_s": links / t_s, "node_updates_per_s": winners / t_s,
+                      "ms_avg": float(rnn_ms.mean()), "updates_per_batch": winners / K,
+                      "roofline": {"bound": "mfma", "achieved": fl / t_s / 1e12,
+                                   "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                                   "frac": fl / t_s / 1e12 / PEAK_BF16_TFLOPS,
+                                   "flops_per_launch": fl / K,
+                                   "hbm_gbps_algorithmic": rb / t_s / 1e9}}
+        res["value_note"] = "value includes the node-status updates (--rnn)"
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

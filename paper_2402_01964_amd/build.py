@@ -12,6 +12,9 @@ HIPCC_FLAGS = [
     "-ffp-contract=off",
     # packed fp32 instructions are kept out of all device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core accumulators in ordinary VGPRs: the accumulate chains then
+    # stay in place instead of being copied between register files
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-Wall",
 ]
 

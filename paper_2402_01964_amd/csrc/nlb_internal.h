@@ -251,6 +251,7 @@ struct nlb_table {
     uint8_t *rnn_cand;                // candidate status rows by pair row
     size_t rnn_cand_bytes;
     int32_t *rnn_cand_node;           // winner node per pair row, else -1
+    uint32_t *rnn_list;               // winner count, then the winners' pair rows
     uint64_t rnn_cand_rows;
 };
 

@@ -17,12 +17,15 @@
 //            atomic maximum; codes of earlier calls are smaller, so the array
 //            is never cleared.  Large batches merge their offers per node in
 //            LDS first (merge_max), as the table insertion does.
-//   gru      a workgroup takes a tile of consecutive pair rows, keeps the
-//            winners (wavefront ballot + prefix count), builds their inputs
-//            in LDS and runs both GRU products on bf16 matrix cores; the
-//            gates, the blend with h and the rounding to the status type
-//            happen in registers, and the new status goes to a candidate
-//            buffer indexed by pair row.
+//   select   each pair row checks whether it won; the winners are appended
+//            to a dense list (one atomic per wavefront).  The list order
+//            varies from run to run; the results do not, because every row
+//            of a matrix product depends on its own inputs only.
+//   gru      a workgroup takes a tile of 16, 32 or 64 listed rows, builds
+//            their inputs in LDS and runs both GRU products on bf16 matrix
+//            cores; the gates, the blend with h and the rounding to the
+//            status type happen in registers, and the new status goes to a
+//            candidate buffer indexed by pair row.
 //   scatter  copies each winner's candidate row over its node's status.
 // The candidate buffer is what lets the gru pass read only pre-batch
 // statuses: no status is written until every workgroup has read its inputs.
@@ -36,7 +39,10 @@
 // for ub = w, w + 4, ...; for each it keeps four accumulators per 16-row
 // block -- r and z (input and hidden products summed), the input part of n
 // and the hidden part of n -- so a unit's three gates meet in one lane and
-// the cell finishes without another LDS round trip.
+// the cell finishes without another LDS round trip.  The weight fragments
+// (read from global memory, where the whole weight set stays L2-resident)
+// go through a three-slot register ring, so each k-step's loads are issued
+// two steps before their products.
 #include <cstring>
 
 #include "nlb_internal.h"
@@ -44,12 +50,10 @@
 namespace {
 
 constexpr int kRnnThreads = 256;
-constexpr int kGruMaxBlocks = 4;                  // 16-row blocks per tile: at most 64 pair rows
 constexpr uint32_t kGruMeta = 1024;               // LDS bytes of the tile's row list
 constexpr uint32_t kGruLdsBudget = 80 * 1024;     // two workgroups per CU
 constexpr uint32_t kGruLdsMax = 160 * 1024;       // gfx950: LDS of one workgroup at most
-constexpr uint32_t kGruTargetTiles = 2048;
-constexpr int kFill = 4;                          // input units whose loads are in flight together
+constexpr uint32_t kGruTargetTiles = 1024;      // tiles wanted per launch (counted on 2n rows)
 
 struct ResolveParams {
     const int32_t *src;
@@ -59,6 +63,7 @@ struct ResolveParams {
     unsigned long long *winner;
     uint64_t epoch_hi;
     uint32_t *status;
+    uint32_t *count;      // winners listed by select; zeroed here
 };
 
 __device__ __forceinline__ bool endpoints_ok(int32_t u, int32_t v, int64_t num_nodes) {
@@ -67,6 +72,7 @@ __device__ __forceinline__ bool endpoints_ok(int32_t u, int32_t v, int64_t num_n
 
 __global__ __launch_bounds__(kRnnThreads) void rnn_resolve(ResolveParams p) {
     const uint32_t i = blockIdx.x * kRnnThreads + threadIdx.x;
+    if (i == 0) *p.count = 0;
     if (i >= p.n) return;
     const int32_t u = p.src[i], v = p.dst[i];
     if (!endpoints_ok(u, v, p.num_nodes)) {
@@ -84,6 +90,7 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_resolve_merged(ResolveParams 
         merge_off[k] = 0ull;
         merge_word[k] = 0ull;
     }
+    if (blockIdx.x == 0 && threadIdx.x == 0) *p.count = 0;
     __syncthreads();
     const uint32_t first = blockIdx.x * kResolveLinks;
     for (uint32_t r = 0; r < kResolveLinks; r += kRnnThreads) {
@@ -104,17 +111,72 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_resolve_merged(ResolveParams 
     }
 }
 
+struct SelectParams {
+    const int32_t *src;
+    const int32_t *dst;
+    uint32_t n;
+    int64_t num_nodes;
+    const unsigned long long *winner;
+    uint64_t epoch_hi;
+    int32_t *cand_node;   // [2n]: winner node of pair row r, else -1
+    u32x4 *list;          // winners, dense: {pair row, self, other, 0}
+    uint32_t *count;
+};
+
+// A workgroup checks kSelectRows consecutive pair rows, collects its
+// winners in LDS (one LDS atomic per wavefront and pass) and appends them to
+// the list with a single global atomic.
+constexpr uint32_t kSelectRows = 1024;
+
+__global__ __launch_bounds__(kRnnThreads) void rnn_select(SelectParams p) {
+    __shared__ u32x4 rows[kSelectRows];
+    __shared__ uint32_t n_local, base;
+    const uint32_t lane = threadIdx.x & 63;
+    if (threadIdx.x == 0) n_local = 0;
+    __syncthreads();
+    const uint64_t r0 = (uint64_t)blockIdx.x * kSelectRows;
+    for (uint32_t k = threadIdx.x; k < kSelectRows; k += kRnnThreads) {
+        const uint64_t r = r0 + k;
+        bool win = false;
+        int32_t self = -1, other = -1;
+        if (r < 2ull * p.n) {
+            const uint32_t i = (uint32_t)(r >> 1);
+            const int32_t u = p.src[i], v = p.dst[i];
+            if (endpoints_ok(u, v, p.num_nodes)) {
+                self = (r & 1) ? v : u;
+                other = (r & 1) ? u : v;
+                win = p.winner[self] == (p.epoch_hi | (r + 1));
+            }
+            p.cand_node[r] = win ? self : -1;
+        }
+        const uint64_t mask = __ballot(win);
+        if (mask == 0) continue;
+        const uint32_t leader = (uint32_t)__ffsll((long long)mask) - 1u;
+        uint32_t off = 0;
+        if (lane == leader) off = atomicAdd(&n_local, (uint32_t)__popcll(mask));
+        off = __shfl(off, (int)leader);
+        if (win)
+            rows[off + (uint32_t)__popcll(mask & ((1ull << lane) - 1ull))] =
+                u32x4{(uint32_t)r, (uint32_t)self, (uint32_t)other, 0u};
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) base = n_local ? atomicAdd(p.count, n_local) : 0;
+    __syncthreads();
+    for (uint32_t k = threadIdx.x; k < n_local; k += kRnnThreads) p.list[base + k] = rows[k];
+}
+
 struct GruParams {
     const int32_t *src;
     const int32_t *dst;
     const uint32_t *t;
     uint32_t n;
     int64_t num_nodes;
-    const unsigned long long *winner;
-    uint64_t epoch_hi;
+    const u32x4 *list;                  // winners {pair row, self, other, 0} (select)
+    const uint32_t *count;
     uint64_t first_eid;                 // arrival index (link-row index) of link 0
     uint32_t d, d_time;
     const float *tw, *tb;               // time encoding
+    uint32_t t_vec;                     // tw, tb 16-byte aligned
     const uint8_t *efeat;
     int64_t edge_rows;
     uint32_t e_dim, e_bf16, erb, e_vec;
@@ -126,7 +188,7 @@ struct GruParams {
     uint32_t lo_begin, lo_end;          // X columns with a stored lo plane
     uint32_t h_lo;                      // fp32 statuses: H has a lo plane
     uint32_t xs, ls, hs;                // LDS row strides (bf16 elements)
-    uint32_t rows;                      // pair rows per tile (multiple of 16, <= 64)
+    uint32_t rows;                      // listed rows per tile (16, 32 or 64)
     uint32_t off_xl, off_h, off_hl;     // LDS byte offsets
     uint64_t gx_m, gh_m;                // ceil(2^40 / (kx / 8)), ceil(2^40 / (kd / 8))
     const __bf16 *w_ih, *w_hh;
@@ -140,58 +202,103 @@ __device__ __forceinline__ void store_hi8(const float v[8], __bf16 *hi) {
     *(bf16x8 *)hi = h;
 }
 
-__device__ __forceinline__ float sigmoid_f32(float a) { return 1.0f / (1.0f + expf(-a)); }
+// Gates from the hardware base-2 exponential and reciprocal (each within a
+// few ulp): sigmoid(a) = 1 / (1 + 2^(-a log2 e)), tanh(a) = 1 - 2 / (1 +
+// 2^(2 a log2 e)).  Both saturate correctly when the exponential overflows
+// to infinity or underflows to zero; tanh near 0 is accurate to ~1e-7
+// absolute.
+constexpr float kLog2e = 1.44269504088896340736f;
+
+__device__ __forceinline__ float sigmoid_f32(float a) {
+    return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-a * kLog2e));
+}
+
+__device__ __forceinline__ float tanh_f32(float a) {
+    return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(2.0f * kLog2e * a));
+}
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     const uint32_t u = __float_as_uint(f);
     return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
-// acc[g'][rb] += A_rb (16 x K from the LDS pair Ah/Al, row stride `as`; the
-// lo plane covers columns [lo_b, lo_e) with its own stride `ls`)
-//              * W_g^T for the three gate row blocks W_g = W + g * d * ld,
-// where g' = g for the r and z gates and g' = NIDX for the n gate.
-template <int NIDX>
-__device__ __forceinline__ void gate_products(f32x4 (&acc)[4][kGruMaxBlocks], uint32_t nrb,
-                                              const __bf16 *Ah, const __bf16 *Al, uint32_t as,
-                                              uint32_t ls, uint32_t lo_b, uint32_t lo_e,
-                                              const __bf16 *W, uint32_t ld, uint32_t K, uint32_t d,
-                                              uint32_t unit, uint32_t lane) {
-    const uint32_t lr = lane & 15, lk = (lane >> 4) * 8;
-    const __bf16 *w0 = W + (size_t)unit * ld + lk;
-    const size_t gstep = (size_t)d * ld;
-    for (uint32_t k0 = 0; k0 < K; k0 += 32) {
-        bf16x8 b[3];
+// acc[g'][rb] += A_rb (16 x 32 blocks of the LDS pair Ah/Al, row stride
+// `as`; the lo plane starts at column lo_b with its own stride `ls`)
+//              * W_g^T for the three gate row blocks W_g = w0 + g * gstep,
+// over the k-steps kb, kb + 32, .. < ke; g' = g for the r and z gates and
+// g' = NIDX for the n gate.  LO adds the lo-plane products.
+template <int NB, bool LO, int NIDX>
+__device__ __forceinline__ void gate_seg(f32x4 (&acc)[4][NB], const __bf16 *Ah, const __bf16 *Al,
+                                         uint32_t as, uint32_t ls, uint32_t lo_b, const __bf16 *w0,
+                                         size_t gstep, uint32_t kb, uint32_t ke, uint32_t lr,
+                                         uint32_t lk) {
+    if (kb >= ke) return;
+    const uint32_t last = ke - 32;
+    bf16x8 r0[3], r1[3], r2[3];
+    auto load = [&](bf16x8 (&b)[3], uint32_t k) {
 #pragma unroll
-        for (int g = 0; g < 3; g++) b[g] = *(const bf16x8 *)(w0 + g * gstep + k0);
-        const bool lo = k0 >= lo_b && k0 < lo_e;
+        for (int g = 0; g < 3; g++) b[g] = *(const bf16x8 *)(w0 + g * gstep + k);
+    };
+    auto step = [&](const bf16x8 (&b)[3], uint32_t k0) {
+        bf16x8 a[NB], al[NB];
 #pragma unroll
-        for (int rb = 0; rb < kGruMaxBlocks; rb++) {
-            if ((uint32_t)rb >= nrb) continue;
-            const bf16x8 a = *(const bf16x8 *)(Ah + (16u * rb + lr) * as + k0 + lk);
+        for (int rb = 0; rb < NB; rb++) a[rb] = *(const bf16x8 *)(Ah + (16u * rb + lr) * as + k0 + lk);
+        if (LO) {
+#pragma unroll
+            for (int rb = 0; rb < NB; rb++)
+                al[rb] = *(const bf16x8 *)(Al + (16u * rb + lr) * ls + (k0 - lo_b) + lk);
+        }
+#pragma unroll
+        for (int rb = 0; rb < NB; rb++)
 #pragma unroll
             for (int g = 0; g < 3; g++) {
                 const int gi = g == 2 ? NIDX : g;
-                acc[gi][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[g], acc[gi][rb], 0, 0, 0);
+                acc[gi][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], b[g], acc[gi][rb], 0, 0, 0);
             }
-            if (lo) {
-                const bf16x8 al = *(const bf16x8 *)(Al + (16u * rb + lr) * ls + (k0 - lo_b) + lk);
+        if (LO) {
+#pragma unroll
+            for (int rb = 0; rb < NB; rb++)
 #pragma unroll
                 for (int g = 0; g < 3; g++) {
                     const int gi = g == 2 ? NIDX : g;
-                    acc[gi][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b[g], acc[gi][rb], 0, 0, 0);
+                    acc[gi][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[rb], b[g], acc[gi][rb], 0, 0, 0);
                 }
-            }
         }
+        // All LDS reads of the step first, then its products.
+        __builtin_amdgcn_sched_group_barrier(0x0100, LO ? 2 * NB : NB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x0008, LO ? 6 * NB : 3 * NB, 0);
+    };
+    // Three-slot ring: the loads of step k + 64 are issued before the
+    // products of step k (the scheduling barriers keep them there).
+    // Prefetches past the segment re-read its last step (in bounds, unused).
+    load(r0, kb);
+    load(r1, kb + 32 < ke ? kb + 32 : last);
+    uint32_t k0 = kb;
+    for (; k0 + 64 < ke; k0 += 96) {
+        load(r2, k0 + 64);
+        __builtin_amdgcn_sched_barrier(0);
+        step(r0, k0);
+        load(r0, k0 + 96 < ke ? k0 + 96 : last);
+        __builtin_amdgcn_sched_barrier(0);
+        step(r1, k0 + 32);
+        load(r1, k0 + 128 < ke ? k0 + 128 : last);
+        __builtin_amdgcn_sched_barrier(0);
+        step(r2, k0 + 64);
     }
+    if (k0 < ke) step(r0, k0);
+    if (k0 + 32 < ke) step(r1, k0 + 32);
 }
 
+template <int NB>
 __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
+    constexpr uint32_t R = 16 * NB;
+    // Input units (8 columns each) whose loads a thread keeps in flight
+    // together: about all of its units for the common widths.
+    constexpr int kFill = NB == 4 ? 12 : (NB == 2 ? 8 : 4);
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-    uint32_t *m_row = (uint32_t *)smem;          // pair row of compacted row j
+    uint32_t *m_row = (uint32_t *)smem;          // pair row of tile row j
     int32_t *m_self = (int32_t *)(m_row + 64);
     int32_t *m_other = m_self + 64;
-    uint32_t *m_count = (uint32_t *)(m_other + 64);
     __bf16 *Xh = (__bf16 *)(smem + kGruMeta);
     __bf16 *Xl = (__bf16 *)(smem + p.off_xl);
     __bf16 *Hh = (__bf16 *)(smem + p.off_h);
@@ -199,50 +306,38 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
 
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63, wave = tid >> 6;
-    const uint64_t r0 = (uint64_t)blockIdx.x * p.rows;
-    const uint64_t total = 2ull * p.n;
-
-    // Winners of the tile's pair rows, compacted in order.
-    if (wave == 0) {
-        const uint64_t r = r0 + lane;
-        bool win = false;
-        int32_t self = -1, other = -1;
-        if (lane < p.rows && r < total) {
-            const uint32_t i = (uint32_t)(r >> 1);
-            const int32_t u = p.src[i], v = p.dst[i];
-            if (endpoints_ok(u, v, p.num_nodes)) {
-                self = (r & 1) ? v : u;
-                other = (r & 1) ? u : v;
-                win = p.winner[self] == (p.epoch_hi | (r + 1));
-            }
-            p.cand_node[r] = win ? self : -1;
-        }
-        const uint64_t mask = __ballot(win);
-        if (win) {
-            const uint32_t pos = (uint32_t)__popcll(mask & ((1ull << lane) - 1ull));
-            m_row[pos] = (uint32_t)r;
-            m_self[pos] = self;
-            m_other[pos] = other;
-        }
-        if (lane == 0) *m_count = (uint32_t)__popcll(mask);
+    const uint32_t count = *p.count;
+    const uint64_t j0 = (uint64_t)blockIdx.x * R;
+    if (j0 >= count) return;
+    const uint32_t m = (uint32_t)min((uint64_t)R, (uint64_t)count - j0);
+    if (tid < m) {
+        const u32x4 e = p.list[j0 + tid];
+        m_row[tid] = e[0];
+        m_self[tid] = (int32_t)e[1];
+        m_other[tid] = (int32_t)e[2];
     }
     __syncthreads();
-    const uint32_t m = *m_count;
-    if (m == 0) return;
-    const uint32_t nrb = (m + 15) / 16;
-    const uint32_t rows_p = 16 * nrb;
 
-    // Inputs: X = [r_other | T-enc(t) | e] and H = r_self; pad rows are zero.
-    const uint32_t gx = p.kx / 8;
-    const uint32_t ux = rows_p * gx;
-    for (uint32_t base = tid; base < ux; base += kRnnThreads * kFill) {
+    // Inputs: X = [r_other | T-enc(t) | e] and H = r_self; rows m .. R-1
+    // are zero.  Units of 8 columns: X's R * kx / 8 first, then H's; the
+    // loads of kFill units per thread are in flight together.
+    const uint32_t gx = p.kx / 8, gh = p.kd / 8;
+    const uint32_t ux = R * gx;
+    const uint32_t ut = ux + R * gh;
+    for (uint32_t base = tid; base < ut; base += kRnnThreads * kFill) {
         float v[kFill][8];
 #pragma unroll
         for (int f = 0; f < kFill; f++) {
             const uint32_t u = base + f * kRnnThreads;
 #pragma unroll
             for (int i = 0; i < 8; i++) v[f][i] = 0.0f;
-            if (u >= ux) continue;
+            if (u >= ut) continue;
+            if (u >= ux) {
+                const uint32_t j = div_small(u - ux, p.gh_m);
+                const uint32_t c0 = (u - ux - j * gh) * 8;
+                if (j < m) load8(p.st + (size_t)m_self[j] * p.srb, p.d, p.s_bf16, p.s_vec, c0, v[f]);
+                continue;
+            }
             const uint32_t j = div_small(u, p.gx_m);
             const uint32_t c0 = (u - j * gx) * 8;
             if (j >= m) continue;
@@ -252,9 +347,27 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
             } else if (c0 < p.off_e) {
                 const uint32_t k = c0 - p.kd;
                 const float tf = (float)p.t[link];
+                float wk[8], bk[8];
+                if (p.t_vec && k + 8 <= p.d_time) {
+                    const f32x4 w0 = *(const f32x4 *)(p.tw + k), w1 = *(const f32x4 *)(p.tw + k + 4);
+                    const f32x4 b0 = *(const f32x4 *)(p.tb + k), b1 = *(const f32x4 *)(p.tb + k + 4);
+#pragma unroll
+                    for (int i = 0; i < 4; i++) {
+                        wk[i] = w0[i];
+                        wk[4 + i] = w1[i];
+                        bk[i] = b0[i];
+                        bk[4 + i] = b1[i];
+                    }
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 8; i++) {
+                        wk[i] = k + i < p.d_time ? p.tw[k + i] : 0.0f;
+                        bk[i] = k + i < p.d_time ? p.tb[k + i] : 0.0f;
+                    }
+                }
 #pragma unroll
                 for (int i = 0; i < 8; i++)
-                    if (k + i < p.d_time) v[f][i] = cos_fp32(__builtin_fmaf(p.tw[k + i], tf, p.tb[k + i]));
+                    if (k + i < p.d_time) v[f][i] = cos_fp32(__builtin_fmaf(wk[i], tf, bk[i]));
             } else {
                 const uint64_t e = p.first_eid + link;
                 if (e < (uint64_t)p.edge_rows)
@@ -264,7 +377,16 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
 #pragma unroll
         for (int f = 0; f < kFill; f++) {
             const uint32_t u = base + f * kRnnThreads;
-            if (u >= ux) continue;
+            if (u >= ut) continue;
+            if (u >= ux) {
+                const uint32_t j = div_small(u - ux, p.gh_m);
+                const uint32_t c0 = (u - ux - j * gh) * 8;
+                if (p.h_lo)
+                    store_split8(v[f], Hh + (size_t)j * p.hs + c0, Hl + (size_t)j * p.hs + c0);
+                else
+                    store_hi8(v[f], Hh + (size_t)j * p.hs + c0);
+                continue;
+            }
             const uint32_t j = div_small(u, p.gx_m);
             const uint32_t c0 = (u - j * gx) * 8;
             if (c0 >= p.lo_begin && c0 < p.lo_end)
@@ -273,53 +395,58 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
                 store_hi8(v[f], Xh + (size_t)j * p.xs + c0);
         }
     }
-    const uint32_t gh = p.kd / 8;
-    const uint32_t uh = rows_p * gh;
-    for (uint32_t u = tid; u < uh; u += kRnnThreads) {
-        const uint32_t j = div_small(u, p.gh_m);
-        const uint32_t c0 = (u - j * gh) * 8;
-        float v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        if (j < m) load8(p.st + (size_t)m_self[j] * p.srb, p.d, p.s_bf16, p.s_vec, c0, v);
-        if (p.h_lo)
-            store_split8(v, Hh + (size_t)j * p.hs + c0, Hl + (size_t)j * p.hs + c0);
-        else
-            store_hi8(v, Hh + (size_t)j * p.hs + c0);
-    }
     __syncthreads();
 
     const uint32_t d = p.d;
     const uint32_t units = (d + 15) / 16;
+    const uint32_t lr = lane & 15, lk = (lane >> 4) * 8;
     for (uint32_t ub = wave; ub < units; ub += kRnnThreads / 64) {
-        const uint32_t j = 16 * ub + (lane & 15);
+        const uint32_t j = 16 * ub + lr;
         const uint32_t jr = j < d ? j : d - 1;   // rows past d are read, never used
-        f32x4 acc[4][kGruMaxBlocks];   // r, z, input part of n, hidden part of n
+        // The epilogue's h values, loaded before the products so that
+        // their latency overlaps them.
+        float hv[NB][4];
+#pragma unroll
+        for (int rb = 0; rb < NB; rb++)
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const uint32_t row = 16u * rb + 4u * (lane >> 4) + i;
+                const uint8_t *srow = p.st + (size_t)m_self[row < m ? row : 0] * p.srb;
+                hv[rb][i] = p.s_bf16 ? bf16_bits_to_float(((const uint16_t *)srow)[jr])
+                                     : ((const float *)srow)[jr];
+            }
+        f32x4 acc[4][NB];   // r, z, input part of n, hidden part of n
 #pragma unroll
         for (int g = 0; g < 4; g++)
 #pragma unroll
-            for (int rb = 0; rb < kGruMaxBlocks; rb++) acc[g][rb] = f32x4(0.0f);
-        gate_products<2>(acc, nrb, Xh, Xl, p.xs, p.ls, p.lo_begin, p.lo_end, p.w_ih, p.kx, p.kx, d, jr,
-                         lane);
-        gate_products<3>(acc, nrb, Hh, Hl, p.hs, p.hs, 0, p.h_lo ? p.kd : 0, p.w_hh, p.kd, p.kd, d, jr,
-                         lane);
+            for (int rb = 0; rb < NB; rb++) acc[g][rb] = f32x4(0.0f);
+        const __bf16 *wx = p.w_ih + (size_t)jr * p.kx + lk;
+        const size_t gx_step = (size_t)d * p.kx;
+        gate_seg<NB, false, 2>(acc, Xh, Xl, p.xs, p.ls, p.lo_begin, wx, gx_step, 0, p.lo_begin, lr, lk);
+        gate_seg<NB, true, 2>(acc, Xh, Xl, p.xs, p.ls, p.lo_begin, wx, gx_step, p.lo_begin, p.lo_end, lr,
+                              lk);
+        gate_seg<NB, false, 2>(acc, Xh, Xl, p.xs, p.ls, p.lo_begin, wx, gx_step, p.lo_end, p.kx, lr, lk);
+        const __bf16 *wh = p.w_hh + (size_t)jr * p.kd + lk;
+        const size_t gh_step = (size_t)d * p.kd;
+        if (p.h_lo)
+            gate_seg<NB, true, 3>(acc, Hh, Hl, p.hs, p.hs, 0, wh, gh_step, 0, p.kd, lr, lk);
+        else
+            gate_seg<NB, false, 3>(acc, Hh, Hl, p.hs, p.hs, 0, wh, gh_step, 0, p.kd, lr, lk);
         if (j >= d) continue;
         const float br = p.b_ih[j] + p.b_hh[j];
         const float bz = p.b_ih[d + j] + p.b_hh[d + j];
         const float bin = p.b_ih[2 * d + j];
         const float bhn = p.b_hh[2 * d + j];
 #pragma unroll
-        for (int rb = 0; rb < kGruMaxBlocks; rb++) {
-            if ((uint32_t)rb >= nrb) continue;
+        for (int rb = 0; rb < NB; rb++) {
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 const uint32_t row = 16u * rb + 4u * (lane >> 4) + i;
                 if (row >= m) continue;
                 const float rg = sigmoid_f32(acc[0][rb][i] + br);
                 const float zg = sigmoid_f32(acc[1][rb][i] + bz);
-                const float ng = tanhf(acc[2][rb][i] + bin + rg * (acc[3][rb][i] + bhn));
-                const uint8_t *srow = p.st + (size_t)m_self[row] * p.srb;
-                const float h = p.s_bf16 ? bf16_bits_to_float(((const uint16_t *)srow)[j])
-                                         : ((const float *)srow)[j];
-                const float out = (1.0f - zg) * ng + zg * h;
+                const float ng = tanh_f32(acc[2][rb][i] + bin + rg * (acc[3][rb][i] + bhn));
+                const float out = (1.0f - zg) * ng + zg * hv[rb][i];
                 uint8_t *crow = p.cand + (size_t)m_row[row] * p.srb;
                 if (p.s_bf16)
                     ((uint16_t *)crow)[j] = f32_to_bf16_rne(out);
@@ -389,14 +516,19 @@ int rnn_reserve(nlb_table *h, uint64_t pair_rows, uint32_t srb) {
         if (hipDeviceSynchronize() != hipSuccess) return NLB_EDEVICE;
         (void)hipFree(h->rnn_cand);
         (void)hipFree(h->rnn_cand_node);
+        (void)hipFree(h->rnn_list);
         h->rnn_cand = nullptr;
         h->rnn_cand_node = nullptr;
+        h->rnn_list = nullptr;
         h->rnn_cand_bytes = 0;
         h->rnn_cand_rows = 0;
+        // list: the winner count in word 0, the winners (4 words each) from word 64 on
         if (hipMalloc((void **)&h->rnn_cand, cbytes) != hipSuccess ||
-            hipMalloc((void **)&h->rnn_cand_node, (size_t)pair_rows * 4u) != hipSuccess) {
+            hipMalloc((void **)&h->rnn_cand_node, (size_t)pair_rows * 4u) != hipSuccess ||
+            hipMalloc((void **)&h->rnn_list, ((size_t)pair_rows * 4u + 64u) * 4u) != hipSuccess) {
             (void)hipGetLastError();
             (void)hipFree(h->rnn_cand);
+            (void)hipFree(h->rnn_cand_node);
             h->rnn_cand = nullptr;
             h->rnn_cand_node = nullptr;
             return NLB_ENOMEM;
@@ -440,6 +572,7 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     p.d_time = h->d_time;
     p.tw = h->w;
     p.tb = h->b;
+    p.t_vec = ((uintptr_t)h->w | (uintptr_t)h->b) % 16 == 0;
     p.efeat = h->efeat;
     p.edge_rows = h->edge_rows;
     p.e_dim = h->erb / e_es;
@@ -470,22 +603,21 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     p.b_ih = wts->b_ih;
     p.b_hh = wts->b_hh;
 
-    // Tile: enough tiles to fill the GPU, at most 64 pair rows, within the
-    // LDS budget of two workgroups per CU (a 16-row tile may use more).
+    // Tile of 16 * nb listed rows: as large as the LDS budget of two
+    // workgroups per CU allows, smaller when the batch would give fewer than
+    // kGruTargetTiles tiles (counting all 2n pair rows; the winners are
+    // fewer); a 16-row tile may use a workgroup's whole LDS.
     const uint64_t pairs = 2ull * n;
-    uint32_t want = (uint32_t)pad16((uint32_t)((pairs + kGruTargetTiles - 1) / kGruTargetTiles));
-    if (want > 16u * kGruMaxBlocks) want = 16u * kGruMaxBlocks;
-    uint32_t rows = 0, lds = 0;
-    for (uint32_t r = want; r >= 16 && rows == 0; r -= 16) {
+    uint32_t nb = 4;
+    while (nb > 1 && pairs < (uint64_t)kGruTargetTiles * 16u * nb) nb /= 2;
+    uint32_t lds = 0;
+    for (;; nb /= 2) {
         GruParams trial = p;
-        const uint32_t bytes = gru_layout(trial, r);
-        if (bytes <= (r == 16 ? kGruLdsMax : kGruLdsBudget)) {
-            rows = r;
-            lds = bytes;
-        }
+        lds = gru_layout(trial, 16u * nb);
+        if (lds <= (nb == 1 ? kGruLdsMax : kGruLdsBudget)) break;
+        if (nb == 1) return NLB_EINVAL;   // one 16-row tile does not fit the LDS
     }
-    if (rows == 0) return NLB_EINVAL;   // one 16-row tile does not fit the LDS
-    gru_layout(p, rows);
+    gru_layout(p, 16u * nb);
 
     int rc = rnn_reserve(h, pairs, p.srb);
     if (rc != NLB_OK) return rc;
@@ -496,24 +628,35 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     }
     h->rnn_epoch++;
     const uint64_t epoch_hi = (uint64_t)h->rnn_epoch << 32;
-    p.winner = h->rnn_winner;
-    p.epoch_hi = epoch_hi;
+    uint32_t *count = h->rnn_list;
+    u32x4 *list = (u32x4 *)(h->rnn_list + 64);
+    p.list = list;
+    p.count = count;
     p.cand = h->rnn_cand;
     p.cand_node = h->rnn_cand_node;
 
-    ResolveParams rp = {src, dst, n, h->num_nodes, h->rnn_winner, epoch_hi, h->status};
+    ResolveParams rp = {src, dst, n, h->num_nodes, h->rnn_winner, epoch_hi, h->status, count};
     if (n >= kMergeMinBatch)
         hipLaunchKernelGGL(rnn_resolve_merged, dim3((n + kResolveLinks - 1) / kResolveLinks),
                            dim3(kRnnThreads), 0, (hipStream_t)stream, rp);
     else
         hipLaunchKernelGGL(rnn_resolve, dim3((n + kRnnThreads - 1) / kRnnThreads), dim3(kRnnThreads), 0,
                            (hipStream_t)stream, rp);
+    SelectParams sp = {src, dst, n, h->num_nodes, h->rnn_winner, epoch_hi, h->rnn_cand_node, list, count};
+    hipLaunchKernelGGL(rnn_select, dim3((unsigned)((pairs + kSelectRows - 1) / kSelectRows)),
+                       dim3(kRnnThreads), 0, (hipStream_t)stream, sp);
+    const void *kern = nb == 4 ? (const void *)rnn_gru<4>
+                     : nb == 2 ? (const void *)rnn_gru<2> : (const void *)rnn_gru<1>;
     if (lds > 64u * 1024u &&
-        hipFuncSetAttribute((const void *)rnn_gru, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)kGruLdsMax) != hipSuccess)
+        hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGruLdsMax) != hipSuccess)
         return NLB_EDEVICE;
-    hipLaunchKernelGGL(rnn_gru, dim3((unsigned)((pairs + rows - 1) / rows)), dim3(kRnnThreads), lds,
-                       (hipStream_t)stream, p);
+    const dim3 grid((unsigned)((pairs + 16u * nb - 1) / (16u * nb)));
+    if (nb == 4)
+        hipLaunchKernelGGL(rnn_gru<4>, grid, dim3(kRnnThreads), lds, (hipStream_t)stream, p);
+    else if (nb == 2)
+        hipLaunchKernelGGL(rnn_gru<2>, grid, dim3(kRnnThreads), lds, (hipStream_t)stream, p);
+    else
+        hipLaunchKernelGGL(rnn_gru<1>, grid, dim3(kRnnThreads), lds, (hipStream_t)stream, p);
     uint32_t w = 2;
     for (uint32_t c = 16; c >= 4; c /= 2)
         if (p.srb % c == 0 && (uintptr_t)status % c == 0 && (uintptr_t)h->rnn_cand % c == 0) {
