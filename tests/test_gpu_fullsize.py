@@ -2,19 +2,23 @@
 inputs resident in HBM and the batch / query launches the benchmark times.
 
 The GPU runs the whole stream.  At checkpoint batches a random subset of the
-batch's queries is kept; after the stream, the final table rows of those
-query nodes are kept too.  The oracle then replays, in stream order, only the
+batch's queries is kept -- the sampled outputs, and the eq. (4) aggregates
+of the same launch of all the batch's queries (random weights); after the
+stream, the final table rows of those query nodes are kept too.  The oracle then replays, in stream order, only the
 links that touch those nodes (tables are per node, so this is exact -- pinned
 on the CPU by test_filtered_substream_gives_same_rows) and answers the same
 queries at the same points.  Indices and rows must match bit for bit, the
-time encoding within 1e-5.
+time encoding within 1e-5, the aggregates within the scaled tolerance of
+nlb_aggregate.
 """
 import numpy as np
 import pytest
 
 import oracle
 import synth
-from tests.gpu_helpers import TENC_TOL, host_np, make_gpu_table
+from tests.gpu_helpers import TENC_TOL, host_np, make_gpu_table, to_dev
+
+AGG_TOL = 2e-4   # see nlb_aggregate in include/nlb.h
 
 pytestmark = pytest.mark.gpu
 
@@ -63,6 +67,10 @@ def _full_size(k, checks, per_check=400):
     nf_d = synth.device_features(w, "node", dev)
     g = make_gpu_table(w, ef_d, nf_d)
     out = g.alloc_outputs(3 * w.batch)
+    W = synth.agg_weights(w) if w.s <= 64 else None
+    Wd = {kk: (to_dev(v.view(np.int16)) if v.dtype == np.uint16 else to_dev(v)) for kk, v in W.items()} \
+        if W is not None else None
+    z = torch.empty((3 * w.batch, 64), dtype=torch.float32, device=dev) if W is not None else None
     rng = np.random.default_rng(100 + k)
     kept = {}
     for b in range(w.batches):
@@ -73,13 +81,18 @@ def _full_size(k, checks, per_check=400):
             g.sample_into(q, tq, o)
             pos = np.sort(rng.choice(n, min(n, per_check), replace=False))
             pos_d = torch.from_numpy(pos).to(dev)
-            kept[b] = (pos, host_np(q[pos_d]), {kk: host_np(v[pos_d]) for kk, v in o.items()})
+            zk = None
+            if W is not None:
+                g.aggregate(q, tq, Wd, out=z[:n])
+                zk = host_np(z[pos_d])
+            kept[b] = (pos, host_np(q[pos_d]), {kk: host_np(v[pos_d]) for kk, v in o.items()}, zk)
         g.insert(s_, d_, t_)
         if b % 1000 == 0:
             _log(f"gpu batch {b}")
     torch.cuda.synchronize()
     assert g.status() == 0
     qnodes = np.unique(np.concatenate([kept[b][1] for b in kept]))
+    del z
     nbr_d, ts_dd, eid_d = g.export()
     idx = torch.from_numpy(qnodes.astype(np.int64)).to(dev)
     final_gpu = (host_np(nbr_d[idx]), host_np(ts_dd[idx]).view(np.uint32),
@@ -107,7 +120,7 @@ def _full_size(k, checks, per_check=400):
         if upto > done:
             o.insert_ids(eids[done:upto], S[done:upto], D[done:upto], T[done:upto])
             done = upto
-        pos, gq, gout = kept[b]
+        pos, gq, gout, gz = kept[b]
         hq, htq = _host_queries(w, b, pos)
         np.testing.assert_array_equal(hq, gq)   # host and device streams agree
         # materialise the feature rows the oracle will copy
@@ -128,6 +141,12 @@ def _full_size(k, checks, per_check=400):
                 assert err.max() <= TENC_TOL, (b, err.max())
             else:
                 assert np.array_equal(gv, ov), (k, b, key, int((gv != ov).sum()))
+        if gz is not None:
+            oz = o.aggregate(hq, htq, fw, fb, ef, nf, W)
+            scale = np.sqrt(np.mean(oz ** 2))
+            err = float(np.max(np.abs(gz.astype(np.float64) - oz) / (np.abs(oz) + scale)))
+            assert err <= AGG_TOL, (k, b, "aggregate", err)
+            _log(f"checkpoint batch {b}: aggregate scaled error {err:.2e}")
         _log(f"checkpoint batch {b} matches")
     o.insert_ids(eids[done:], S[done:], D[done:], T[done:])
     for gv, ov, name in zip(final_gpu, o.export_nodes(qnodes), ("nbr", "ts", "eid")):
