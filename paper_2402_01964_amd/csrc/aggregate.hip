@@ -309,6 +309,335 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_fused(AggParams p) {
     }
 }
 
+// ---------------------------------------------------------------- wavefront-per-query kernel
+// A second formulation of the same computation that keeps every
+// intermediate in registers.  The matrix cores take the weights as the A
+// operand (16 output units x 32 inputs) and the activations as the B operand
+// (32 inputs x 16 rows): then lane l holds output units 4 (l / 16) + i of
+// row l % 16 (i < 4), and two such blocks (units 32 ks + 4 (l / 16) + i and
+// 32 ks + 16 + 4 (l / 16) + i) are exactly the eight inputs lane l supplies
+// for k-step ks of the next layer -- with the next layer's weight columns
+// permuted to that order when they are staged.  So ReLU, the bf16 split and
+// the next product follow without an LDS round trip.
+//
+// Each wavefront takes one query at a time, one 16-row block of its slots
+// at a time (s <= 16: one block): layer 1, layer 2, the attention logits
+// (a reduction over the four lanes of a row) and an online softmax with the
+// weighted sum of the messages (reductions over the 16 rows of a block,
+// combined across blocks with a running maximum).  A group of 16 queries
+// then runs MLP_out as one 16-row block.  The weights of all four layers are
+// staged in LDS once per persistent workgroup; the only other LDS is each
+// wavefront's 16 aggregate vectors.  Wavefronts never wait for each other
+// after the staging, so the latency of one query's gathers is covered by
+// the other wavefronts of the CU.
+constexpr int kRowThreads = 512;    // 8 wavefronts per workgroup
+constexpr int kGroupQ = 16;         // queries per MLP_out block
+constexpr int kRuSteps = 4;         // k-steps of r_u held in registers: node rows up to 128 wide
+constexpr uint32_t kRowsMinQueries = 65536;
+constexpr uint32_t kRowsMinQueriesWide = 4096;
+
+struct RowParams {
+    const uint8_t *blocks;
+    uint32_t block_bytes;
+    uint32_t s;
+    int64_t num_nodes;
+    const int32_t *node;
+    const uint32_t *tq;
+    uint32_t nq;
+    uint32_t nbq;                    // 16-row blocks per query
+    uint32_t d_time;
+    const float *w;
+    const float *b;
+    const uint8_t *efeat;
+    int64_t edge_rows;
+    uint32_t e_dim, e_bf16, erb, e_vec;
+    const uint8_t *nfeat;
+    uint32_t n_dim, n_bf16, nrb, n_vec;
+    uint32_t k1, off_e, off_t, kn, k3;   // layer-1 segments [0,off_e) r_v, [off_e,off_t) e, [off_t,k1) T-enc
+    const __bf16 *w1, *w2, *w3, *w4;
+    const float *b1, *b2, *b3, *b4, *att;
+    float *z;
+    uint32_t *status;
+    uint32_t ls1, ls3;                   // LDS row strides (elements) of w1 and w3
+    uint32_t o_w1, o_w2, o_w3, o_w4, o_vec, o_y;   // LDS byte offsets
+};
+
+constexpr uint32_t kPs = kH + 8;        // LDS row stride of the permuted w2 / w4
+
+// Input unit feeding slot (ks, g, i) of a chained layer's B operand.
+__device__ __forceinline__ uint32_t chain_unit(uint32_t c) {
+    const uint32_t ks = c >> 5, r = c & 31, g = r >> 3, i = r & 7;
+    return 32u * ks + (i < 4 ? 4u * g + i : 16u + 4u * g + (i - 4u));
+}
+
+__device__ __forceinline__ void split8(const float v[8], bf16x8 &hi, bf16x8 &lo) {
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+        const __bf16 t = (__bf16)v[i];
+        hi[i] = t;
+        lo[i] = (__bf16)(v[i] - (float)t);
+    }
+}
+
+// acc[ub] += W[16 ub .. 16 ub + 15][k-step] x (hi + lo) for the four unit blocks.
+__device__ __forceinline__ void mfma4(f32x4 (&acc)[4], const __bf16 *W, uint32_t ls, uint32_t k0,
+                                      uint32_t r16, uint32_t g, const bf16x8 &hi, const bf16x8 &lo,
+                                      bool use_lo) {
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++) {
+        const bf16x8 a = *(const bf16x8 *)(W + (16u * ub + r16) * ls + k0 + 8u * g);
+        acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, hi, acc[ub], 0, 0, 0);
+        if (use_lo) acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, lo, acc[ub], 0, 0, 0);
+    }
+}
+
+// acc (layer input in the D layout, 64 units) -> next layer through the
+// permuted weights Wp: acc_out[ub] += Wp x act.
+__device__ __forceinline__ void chain64(f32x4 (&out)[4], const f32x4 (&act)[4], const __bf16 *Wp,
+                                        uint32_t r16, uint32_t g) {
+#pragma unroll
+    for (int ks = 0; ks < 2; ks++) {
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            v[i] = act[2 * ks][i];
+            v[4 + i] = act[2 * ks + 1][i];
+        }
+        bf16x8 hi, lo;
+        split8(v, hi, lo);
+        mfma4(out, Wp, kPs, 32u * ks, r16, g, hi, lo, true);
+    }
+}
+
+// Reductions over the 16 lanes of a DPP row (the 16 rows of a block), with
+// the result in every lane: pair lanes by quad permutations (swap
+// neighbours, then pairs), then mirror within each half-row and the row.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppSwap1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kDppSwap2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;  // row_half_mirror
+constexpr int kDppMirror = 0x140;      // row_mirror
+
+__device__ __forceinline__ float xor16_sum(float v) {
+    v += dpp<kDppSwap1>(v);
+    v += dpp<kDppSwap2>(v);
+    v += dpp<kDppHalfMirror>(v);
+    v += dpp<kDppMirror>(v);
+    return v;
+}
+
+__device__ __forceinline__ float xor16_max(float v) {
+    v = fmaxf(v, dpp<kDppSwap1>(v));
+    v = fmaxf(v, dpp<kDppSwap2>(v));
+    v = fmaxf(v, dpp<kDppHalfMirror>(v));
+    v = fmaxf(v, dpp<kDppMirror>(v));
+    return v;
+}
+
+template <int GS>
+__global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    __bf16 *W1 = (__bf16 *)(smem + p.o_w1);
+    __bf16 *W2 = (__bf16 *)(smem + p.o_w2);
+    __bf16 *W3 = (__bf16 *)(smem + p.o_w3);
+    __bf16 *W4 = (__bf16 *)(smem + p.o_w4);
+    float *vec = (float *)(smem + p.o_vec);   // b1 | b2 | b3 | b4 | att, 64 each
+
+    // Stage the weights (w2, w4 with columns in chained order).
+    const uint32_t tid = threadIdx.x;
+    for (uint32_t u = tid; u < kH * (p.k1 / 8); u += kRowThreads) {
+        const uint32_t r = u / (p.k1 / 8), c = (u % (p.k1 / 8)) * 8;
+        *(bf16x8 *)(W1 + r * p.ls1 + c) = *(const bf16x8 *)(p.w1 + (size_t)r * p.k1 + c);
+    }
+    for (uint32_t u = tid; u < kH * (p.k3 / 8); u += kRowThreads) {
+        const uint32_t r = u / (p.k3 / 8), c = (u % (p.k3 / 8)) * 8;
+        *(bf16x8 *)(W3 + r * p.ls3 + c) = *(const bf16x8 *)(p.w3 + (size_t)r * p.k3 + c);
+    }
+    for (uint32_t u = tid; u < kH * kH; u += kRowThreads) {
+        const uint32_t r = u / kH, c = u % kH;
+        W2[r * kPs + c] = p.w2[r * kH + chain_unit(c)];
+        W4[r * kPs + c] = p.w4[r * kH + chain_unit(c)];
+    }
+    for (uint32_t u = tid; u < 5u * kH; u += kRowThreads) {
+        const uint32_t k = u / kH, c = u % kH;
+        const float *src = k == 0 ? p.b1 : k == 1 ? p.b2 : k == 2 ? p.b3 : k == 3 ? p.b4 : p.att;
+        vec[u] = src[c];
+    }
+    __syncthreads();
+
+    const uint32_t lane = tid & 63, wave = tid >> 6;
+    const uint32_t r16 = lane & 15, g = lane >> 4;
+    float *Y = (float *)(smem + p.o_y) + (size_t)wave * (kGroupQ * kH);
+    const float *b1 = vec, *b2 = vec + kH, *b3 = vec + 2 * kH, *b4 = vec + 3 * kH, *att = vec + 4 * kH;
+    const uint32_t gs = p.off_t / 32, k1s = p.k1 / 32, k3s = p.k3 / 32, kns = p.kn / 32;
+    const uint64_t groups = ((uint64_t)p.nq + kGroupQ - 1) / kGroupQ;
+    const uint32_t waves = gridDim.x * (kRowThreads / 64);
+
+    for (uint64_t grp = (uint64_t)blockIdx.x * (kRowThreads / 64) + wave; grp < groups; grp += waves) {
+        const uint64_t qb = grp * kGroupQ;
+        const uint32_t nqg = (uint32_t)min((uint64_t)kGroupQ, (uint64_t)p.nq - qb);
+        for (uint32_t qi = 0; qi < nqg; qi++) {
+            const uint64_t q = qb + qi;
+            const int32_t node = p.node[q];
+            const uint32_t tq = p.tq[q];
+            const bool in_range = node >= 0 && (int64_t)node < p.num_nodes;
+            if (!in_range && lane == 0) atomicOr(p.status, kStatusRange);
+            float m = -INFINITY, den = 0.0f;
+            f32x4 agg[4];
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++) agg[ub] = f32x4(0.0f);
+            for (uint32_t blk = 0; blk < p.nbq; blk++) {
+                // Keeps the LDS-resident biases from being hoisted into
+                // long-lived registers.
+                asm volatile("" ::: "memory");
+                const uint32_t a = 16u * blk + r16;
+                SlotLds sl = {-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
+                if (in_range && a < p.s) sl = read_slot(p.blocks, p.block_bytes, p.s, node, a, tq);
+                const bool valid = sl.x >= 0;
+                // Gathered inputs (r_v and e) of this lane's row, all issued first.
+                float v[GS][8];
+#pragma unroll
+                for (int ks = 0; ks < GS; ks++) {
+#pragma unroll
+                    for (int i = 0; i < 8; i++) v[ks][i] = 0.0f;
+                    if ((uint32_t)ks >= gs || !valid) continue;
+                    const uint32_t c0 = 32u * ks + 8u * g;
+                    if (c0 < p.off_e)
+                        load8(p.nfeat + (size_t)sl.x * p.nrb, p.n_dim, p.n_bf16, p.n_vec, c0, v[ks]);
+                    else if ((int64_t)sl.e < p.edge_rows)
+                        load8(p.efeat + (size_t)sl.e * p.erb, p.e_dim, p.e_bf16, p.e_vec, c0 - p.off_e, v[ks]);
+                }
+                // Layer 1: a1 = ReLU(W1 x + b1).
+                f32x4 acc[4];
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++) acc[ub] = f32x4(0.0f);
+#pragma unroll
+                for (int ks = 0; ks < GS; ks++) {
+                    if ((uint32_t)ks >= gs) continue;
+                    const uint32_t c0 = 32u * ks;
+                    bf16x8 hi, lo;
+                    split8(v[ks], hi, lo);
+                    const bool use_lo = c0 < p.off_e ? !p.n_bf16 : !p.e_bf16;
+                    mfma4(acc, W1, p.ls1, c0, r16, g, hi, lo, use_lo);
+                }
+                for (uint32_t ks = gs; ks < k1s; ks++) {
+                    const uint32_t k = 32u * ks + 8u * g - p.off_t;
+                    float t[8];
+#pragma unroll
+                    for (int i = 0; i < 8; i++)
+                        t[i] = (valid && k + i < p.d_time)
+                                   ? cos_fp32(__builtin_fmaf(p.w[k + i], sl.dt, p.b[k + i]))
+                                   : 0.0f;
+                    bf16x8 hi, lo;
+                    split8(t, hi, lo);
+                    mfma4(acc, W1, p.ls1, 32u * ks, r16, g, hi, lo, true);
+                }
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+                    for (int i = 0; i < 4; i++) acc[ub][i] = fmaxf(acc[ub][i] + b1[16 * ub + 4 * g + i], 0.0f);
+                // Layer 2: messages h = W2 a1 + b2, and the logit w^T h of the row.
+                f32x4 h[4];
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++) h[ub] = f32x4(0.0f);
+                chain64(h, acc, W2, r16, g);
+                float part = 0.0f;
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+                    for (int i = 0; i < 4; i++) {
+                        h[ub][i] += b2[16 * ub + 4 * g + i];
+                        part = __builtin_fmaf(att[16 * ub + 4 * g + i], h[ub][i], part);
+                    }
+                part += __shfl_xor(part, 16);
+                part += __shfl_xor(part, 32);
+                // Online softmax over the query's valid rows.
+                const float lg = valid ? part : -INFINITY;
+                const float mb = xor16_max(lg);
+                if (mb == -INFINITY) continue;   // no valid row in this block (wave-uniform)
+                const float mn = fmaxf(m, mb);
+                const float sc = (m == -INFINITY) ? 0.0f : expf(m - mn);
+                const float e = valid ? expf(lg - mn) : 0.0f;
+                den = den * sc + xor16_sum(e);
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+                    for (int i = 0; i < 4; i++) agg[ub][i] = agg[ub][i] * sc + xor16_sum(e * h[ub][i]);
+                m = mn;
+            }
+            if (r16 == 0) {
+                const float inv = den > 0.0f ? 1.0f / den : 0.0f;
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++) {
+                    f32x4 o;
+#pragma unroll
+                    for (int i = 0; i < 4; i++) o[i] = den > 0.0f ? agg[ub][i] * inv : 0.0f;
+                    *(f32x4 *)(Y + qi * kH + 16 * ub + 4 * g) = o;
+                }
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+        asm volatile("" ::: "memory");
+        // MLP_out for the group: row r16 = query qb + r16, input [r_u | aggregate].
+        const bool vq = r16 < nqg;
+        int32_t nr = vq ? p.node[qb + r16] : -1;
+        if (nr >= 0 && (int64_t)nr >= p.num_nodes) nr = -1;
+        float ru[kRuSteps][8];
+#pragma unroll
+        for (int ks = 0; ks < kRuSteps; ks++) {
+#pragma unroll
+            for (int i = 0; i < 8; i++) ru[ks][i] = 0.0f;
+            if ((uint32_t)ks < kns && nr >= 0)
+                load8(p.nfeat + (size_t)nr * p.nrb, p.n_dim, p.n_bf16, p.n_vec, 32u * ks + 8u * g, ru[ks]);
+        }
+        f32x4 acc3[4];
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) acc3[ub] = f32x4(0.0f);
+#pragma unroll
+        for (int ks = 0; ks < kRuSteps; ks++) {
+            if ((uint32_t)ks >= kns) continue;
+            bf16x8 hi, lo;
+            split8(ru[ks], hi, lo);
+            mfma4(acc3, W3, p.ls3, 32u * ks, r16, g, hi, lo, !p.n_bf16);
+        }
+        for (uint32_t ks = kns; ks < k3s; ks++) {
+            const uint32_t c = 32u * ks + 8u * g - p.kn;
+            float y[8];
+#pragma unroll
+            for (int i = 0; i < 8; i++) y[i] = vq ? Y[r16 * kH + c + i] : 0.0f;
+            bf16x8 hi, lo;
+            split8(y, hi, lo);
+            mfma4(acc3, W3, p.ls3, 32u * ks, r16, g, hi, lo, true);
+        }
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+            for (int i = 0; i < 4; i++) acc3[ub][i] = fmaxf(acc3[ub][i] + b3[16 * ub + 4 * g + i], 0.0f);
+        f32x4 zo[4];
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) zo[ub] = f32x4(0.0f);
+        chain64(zo, acc3, W4, r16, g);
+        if (vq) {
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++) {
+#pragma unroll
+                for (int i = 0; i < 4; i++) zo[ub][i] += b4[16 * ub + 4 * g + i];
+                *(f32x4 *)(p.z + (qb + r16) * kH + 16 * ub + 4 * g) = zo[ub];
+            }
+        }
+        // Y is rewritten by the next group of this wavefront only.
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+}
+
 // LDS layout of a tile with `rows` slot rows and `qrows` query rows.
 uint32_t agg_layout(AggParams &p, uint32_t rows, uint32_t qrows) {
     p.rows = rows;
@@ -388,6 +717,85 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
     p.att = wts->att;
     p.z = z;
     p.status = h->status;
+
+    // The wavefront-per-query kernel for launches large enough to give every
+    // wavefront of the GPU several query groups (or queries of several row
+    // blocks, where the tiled kernel's LDS staging is largest), when its
+    // operands fit: node rows up to 128 wide, at most 8 gathered k-steps (r_v
+    // and e), all four weight matrices plus the aggregate staging within one
+    // workgroup's LDS.  Small launches keep the tiled kernel, whose many
+    // short tiles start more work in parallel.
+    if (nq >= kRowsMinQueries || (h->s > 16 && nq >= kRowsMinQueriesWide)) {
+        RowParams r;
+        std::memset(&r, 0, sizeof(r));
+        r.blocks = p.blocks;
+        r.block_bytes = p.block_bytes;
+        r.s = p.s;
+        r.num_nodes = p.num_nodes;
+        r.node = node;
+        r.tq = tq;
+        r.nq = nq;
+        r.nbq = (h->s + 15u) / 16u;
+        r.d_time = p.d_time;
+        r.w = p.w;
+        r.b = p.b;
+        r.efeat = p.efeat;
+        r.edge_rows = p.edge_rows;
+        r.e_dim = p.e_dim;
+        r.e_bf16 = p.e_bf16;
+        r.erb = p.erb;
+        r.e_vec = p.e_vec;
+        r.nfeat = p.nfeat;
+        r.n_dim = p.n_dim;
+        r.n_bf16 = p.n_bf16;
+        r.nrb = p.nrb;
+        r.n_vec = p.n_vec;
+        r.k1 = p.k1;
+        r.off_e = p.off_e;
+        r.off_t = p.off_t;
+        r.kn = pad32(p.n_dim);
+        r.k3 = p.k3;
+        r.w1 = p.w1;
+        r.w2 = p.w2;
+        r.w3 = p.w3;
+        r.w4 = p.w4;
+        r.b1 = p.b1;
+        r.b2 = p.b2;
+        r.b3 = p.b3;
+        r.b4 = p.b4;
+        r.att = p.att;
+        r.z = z;
+        r.status = h->status;
+        r.ls1 = p.k1 + 8;
+        r.ls3 = p.k3 + 8;
+        r.o_w1 = 0;
+        r.o_w2 = align16(r.o_w1 + kH * r.ls1 * 2u);
+        r.o_w3 = align16(r.o_w2 + kH * kPs * 2u);
+        r.o_w4 = align16(r.o_w3 + kH * r.ls3 * 2u);
+        r.o_vec = align16(r.o_w4 + kH * kPs * 2u);
+        r.o_y = align16(r.o_vec + 5u * kH * 4u);
+        const uint32_t bytes = r.o_y + (kRowThreads / 64) * kGroupQ * kH * 4u;
+        const uint32_t gs = r.off_t / 32;
+        if (r.kn <= 32u * kRuSteps && gs <= 8 && bytes <= kAggLdsMax) {
+            const void *kern = gs <= 4 ? (const void *)aggregate_rows<4> : (const void *)aggregate_rows<8>;
+            if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kAggLdsMax) !=
+                hipSuccess)
+                return NLB_EDEVICE;
+            int cus = 0;
+            if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess ||
+                cus < 1)
+                return NLB_EDEVICE;
+            const uint64_t groups = ((uint64_t)nq + kGroupQ - 1) / kGroupQ;
+            const uint64_t wgs = (groups + kRowThreads / 64 - 1) / (kRowThreads / 64);
+            const dim3 grid((unsigned)(wgs < (uint64_t)cus ? wgs : (uint64_t)cus));
+            if (gs <= 4)
+                hipLaunchKernelGGL(aggregate_rows<4>, grid, dim3(kRowThreads), bytes, (hipStream_t)stream, r);
+            else
+                hipLaunchKernelGGL(aggregate_rows<8>, grid, dim3(kRowThreads), bytes, (hipStream_t)stream, r);
+            if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
+            return NLB_OK;
+        }
+    }
 
     // Tile: as many queries as fit the LDS budget (at most 128 slot rows),
     // fewer when that leaves too few workgroups to fill the GPU.

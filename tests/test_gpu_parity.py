@@ -357,3 +357,39 @@ def test_aggregate_matches_oracle(k):
     print(f"aggregate workload {k}: max scaled error {worst:.3e}")
     assert g.status() == 0
     assert worst <= AGG_TOL
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_aggregate_large_launch_matches_oracle(k):
+    """Launches of 70 001 queries (the size class that takes the
+    wavefront-per-query kernel, with a partial last group of queries) on every
+    workload shape; 1 500 sampled queries are compared with the oracle,
+    including queries without a valid slot and repeated query nodes."""
+    import torch
+    base = synth.workload(k)
+    w = synth.scaled(base, 12 * base.batch, num_nodes=min(base.num_nodes, 200000))
+    src, dst, t, _ = synth.host_links(w)
+    ef = synth.host_features(w, "edge") if w.edge_dim else None
+    nf = synth.host_features(w, "node") if w.node_dim else None
+    g = make_gpu_table(w, feat_to_dev(ef, w.edge_dtype) if ef is not None else None,
+                       feat_to_dev(nf, w.node_dtype) if nf is not None else None)
+    o = make_oracle(w)
+    lo, hi = 0, w.links
+    g.insert(to_dev(src[lo:hi]), to_dev(dst[lo:hi]), to_dev(t[lo:hi]))
+    o.insert(src[lo:hi], dst[lo:hi], t[lo:hi])
+    rng = np.random.default_rng(70 + k)
+    nq = 70001
+    ends = np.concatenate([src, dst])
+    q = ends[rng.integers(0, len(ends), nq)].astype(np.int32)
+    tq = rng.integers(0, int(t[-1]) + 2, nq).astype(np.uint32)
+    tq[::11] = 0                                   # no valid slot
+    W = synth.agg_weights(w)
+    gz = g.aggregate(to_dev(q), to_dev(tq), _agg_dev(W)).cpu().numpy()
+    pos = np.sort(rng.choice(nq, 1500, replace=False))
+    pos[-1] = nq - 1                               # the partial last group
+    fw, fb = synth.time_params(w)
+    oz = o.aggregate(q[pos], tq[pos], fw, fb, ef, nf, W)
+    err = agg_error(gz[pos], oz)
+    print(f"aggregate large launch, workload {k}: max scaled error {err:.3e}")
+    assert g.status() == 0
+    assert err <= AGG_TOL
