@@ -479,85 +479,108 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
     for (uint64_t grp = (uint64_t)blockIdx.x * (kRowThreads / 64) + wave; grp < groups; grp += waves) {
         const uint64_t qb = grp * kGroupQ;
         const uint32_t nqg = (uint32_t)min((uint64_t)kGroupQ, (uint64_t)p.nq - qb);
-        for (uint32_t qi = 0; qi < nqg; qi++) {
-            const uint64_t q = qb + qi;
-            const int32_t node = p.node[q];
-            const uint32_t tq = p.tq[q];
-            const bool in_range = node >= 0 && (int64_t)node < p.num_nodes;
-            if (!in_range && lane == 0) atomicOr(p.status, kStatusRange);
-            float m = -INFINITY, den = 0.0f;
-            f32x4 agg[4];
+        // Software pipeline over the group's (query, row block) units: the
+        // query node and time are read two queries ahead, each block's table
+        // slots one block ahead, so only the row gathers of a block are
+        // waited for when it starts.
+        auto slot_at = [&](int32_t nd, uint32_t t, uint32_t blk) {
+            SlotLds r = {-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
+            const uint32_t a = 16u * blk + r16;
+            if (nd >= 0 && (int64_t)nd < p.num_nodes && a < p.s)
+                r = read_slot(p.blocks, p.block_bytes, p.s, nd, a, t);
+            return r;
+        };
+        int32_t nd_cur = p.node[qb], nd_nxt = nqg > 1 ? p.node[qb + 1] : -1;
+        uint32_t t_cur = p.tq[qb], t_nxt = nqg > 1 ? p.tq[qb + 1] : 0u;
+        SlotLds sl_next = slot_at(nd_cur, t_cur, 0);
+        uint32_t qi = 0, blk = 0;
+        float m = -INFINITY, den = 0.0f;
+        f32x4 agg[4];
 #pragma unroll
-            for (int ub = 0; ub < 4; ub++) agg[ub] = f32x4(0.0f);
-            for (uint32_t blk = 0; blk < p.nbq; blk++) {
-                // Keeps the LDS-resident biases from being hoisted into
-                // long-lived registers.
-                asm volatile("" ::: "memory");
-                const uint32_t a = 16u * blk + r16;
-                SlotLds sl = {-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
-                if (in_range && a < p.s) sl = read_slot(p.blocks, p.block_bytes, p.s, node, a, tq);
-                const bool valid = sl.x >= 0;
-                // Gathered inputs (r_v and e) of this lane's row, all issued first.
-                float v[GS][8];
-#pragma unroll
-                for (int ks = 0; ks < GS; ks++) {
-#pragma unroll
-                    for (int i = 0; i < 8; i++) v[ks][i] = 0.0f;
-                    if ((uint32_t)ks >= gs || !valid) continue;
-                    const uint32_t c0 = 32u * ks + 8u * g;
-                    if (c0 < p.off_e)
-                        load8(p.nfeat + (size_t)sl.x * p.nrb, p.n_dim, p.n_bf16, p.n_vec, c0, v[ks]);
-                    else if ((int64_t)sl.e < p.edge_rows)
-                        load8(p.efeat + (size_t)sl.e * p.erb, p.e_dim, p.e_bf16, p.e_vec, c0 - p.off_e, v[ks]);
+        for (int ub = 0; ub < 4; ub++) agg[ub] = f32x4(0.0f);
+        while (qi < nqg) {
+            // Keeps the LDS-resident biases from being hoisted into
+            // long-lived registers.
+            asm volatile("" ::: "memory");
+            const SlotLds sl = sl_next;
+            const bool last_blk = blk + 1 == p.nbq;
+            if (blk == 0 && (nd_cur < 0 || (int64_t)nd_cur >= p.num_nodes) && lane == 0)
+                atomicOr(p.status, kStatusRange);
+            // Issue the next unit's slot read (and the query after next's ids).
+            int32_t nd_after = -1;
+            uint32_t t_after = 0;
+            if (last_blk) {
+                if (qi + 2 < nqg) {
+                    nd_after = p.node[qb + qi + 2];
+                    t_after = p.tq[qb + qi + 2];
                 }
-                // Layer 1: a1 = ReLU(W1 x + b1).
-                f32x4 acc[4];
+                sl_next = qi + 1 < nqg ? slot_at(nd_nxt, t_nxt, 0) : SlotLds{-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
+            } else {
+                sl_next = slot_at(nd_cur, t_cur, blk + 1);
+            }
+            const bool valid = sl.x >= 0;
+            // Gathered inputs (r_v and e) of this lane's row, all issued first.
+            float v[GS][8];
 #pragma unroll
-                for (int ub = 0; ub < 4; ub++) acc[ub] = f32x4(0.0f);
+            for (int ks = 0; ks < GS; ks++) {
 #pragma unroll
-                for (int ks = 0; ks < GS; ks++) {
-                    if ((uint32_t)ks >= gs) continue;
-                    const uint32_t c0 = 32u * ks;
-                    bf16x8 hi, lo;
-                    split8(v[ks], hi, lo);
-                    const bool use_lo = c0 < p.off_e ? !p.n_bf16 : !p.e_bf16;
-                    mfma4(acc, W1, p.ls1, c0, r16, g, hi, lo, use_lo);
+                for (int i = 0; i < 8; i++) v[ks][i] = 0.0f;
+                if ((uint32_t)ks >= gs || !valid) continue;
+                const uint32_t c0 = 32u * ks + 8u * g;
+                if (c0 < p.off_e)
+                    load8(p.nfeat + (size_t)sl.x * p.nrb, p.n_dim, p.n_bf16, p.n_vec, c0, v[ks]);
+                else if ((int64_t)sl.e < p.edge_rows)
+                    load8(p.efeat + (size_t)sl.e * p.erb, p.e_dim, p.e_bf16, p.e_vec, c0 - p.off_e, v[ks]);
+            }
+            // Layer 1: a1 = ReLU(W1 x + b1).
+            f32x4 acc[4];
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++) acc[ub] = f32x4(0.0f);
+#pragma unroll
+            for (int ks = 0; ks < GS; ks++) {
+                if ((uint32_t)ks >= gs) continue;
+                const uint32_t c0 = 32u * ks;
+                bf16x8 hi, lo;
+                split8(v[ks], hi, lo);
+                const bool use_lo = c0 < p.off_e ? !p.n_bf16 : !p.e_bf16;
+                mfma4(acc, W1, p.ls1, c0, r16, g, hi, lo, use_lo);
+            }
+            for (uint32_t ks = gs; ks < k1s; ks++) {
+                const uint32_t k = 32u * ks + 8u * g - p.off_t;
+                float t[8];
+#pragma unroll
+                for (int i = 0; i < 8; i++)
+                    t[i] = (valid && k + i < p.d_time)
+                               ? cos_fp32(__builtin_fmaf(p.w[k + i], sl.dt, p.b[k + i]))
+                               : 0.0f;
+                bf16x8 hi, lo;
+                split8(t, hi, lo);
+                mfma4(acc, W1, p.ls1, 32u * ks, r16, g, hi, lo, true);
+            }
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+                for (int i = 0; i < 4; i++) acc[ub][i] = fmaxf(acc[ub][i] + b1[16 * ub + 4 * g + i], 0.0f);
+            // Layer 2: messages h = W2 a1 + b2, and the logit w^T h of the row.
+            f32x4 h[4];
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++) h[ub] = f32x4(0.0f);
+            chain64(h, acc, W2, r16, g);
+            float part = 0.0f;
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    h[ub][i] += b2[16 * ub + 4 * g + i];
+                    part = __builtin_fmaf(att[16 * ub + 4 * g + i], h[ub][i], part);
                 }
-                for (uint32_t ks = gs; ks < k1s; ks++) {
-                    const uint32_t k = 32u * ks + 8u * g - p.off_t;
-                    float t[8];
-#pragma unroll
-                    for (int i = 0; i < 8; i++)
-                        t[i] = (valid && k + i < p.d_time)
-                                   ? cos_fp32(__builtin_fmaf(p.w[k + i], sl.dt, p.b[k + i]))
-                                   : 0.0f;
-                    bf16x8 hi, lo;
-                    split8(t, hi, lo);
-                    mfma4(acc, W1, p.ls1, 32u * ks, r16, g, hi, lo, true);
-                }
-#pragma unroll
-                for (int ub = 0; ub < 4; ub++)
-#pragma unroll
-                    for (int i = 0; i < 4; i++) acc[ub][i] = fmaxf(acc[ub][i] + b1[16 * ub + 4 * g + i], 0.0f);
-                // Layer 2: messages h = W2 a1 + b2, and the logit w^T h of the row.
-                f32x4 h[4];
-#pragma unroll
-                for (int ub = 0; ub < 4; ub++) h[ub] = f32x4(0.0f);
-                chain64(h, acc, W2, r16, g);
-                float part = 0.0f;
-#pragma unroll
-                for (int ub = 0; ub < 4; ub++)
-#pragma unroll
-                    for (int i = 0; i < 4; i++) {
-                        h[ub][i] += b2[16 * ub + 4 * g + i];
-                        part = __builtin_fmaf(att[16 * ub + 4 * g + i], h[ub][i], part);
-                    }
-                part += __shfl_xor(part, 16);
-                part += __shfl_xor(part, 32);
-                // Online softmax over the query's valid rows.
-                const float lg = valid ? part : -INFINITY;
-                const float mb = xor16_max(lg);
-                if (mb == -INFINITY) continue;   // no valid row in this block (wave-uniform)
+            part += __shfl_xor(part, 16);
+            part += __shfl_xor(part, 32);
+            // Online softmax over the query's valid rows (a block without a
+            // valid row changes nothing; the test is wave-uniform).
+            const float lg = valid ? part : -INFINITY;
+            const float mb = xor16_max(lg);
+            if (mb != -INFINITY) {
                 const float mn = fmaxf(m, mb);
                 const float sc = (m == -INFINITY) ? 0.0f : expf(m - mn);
                 const float e = valid ? expf(lg - mn) : 0.0f;
@@ -568,15 +591,29 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
                     for (int i = 0; i < 4; i++) agg[ub][i] = agg[ub][i] * sc + xor16_sum(e * h[ub][i]);
                 m = mn;
             }
-            if (r16 == 0) {
-                const float inv = den > 0.0f ? 1.0f / den : 0.0f;
+            if (last_blk) {
+                if (r16 == 0) {
+                    const float inv = den > 0.0f ? 1.0f / den : 0.0f;
 #pragma unroll
-                for (int ub = 0; ub < 4; ub++) {
-                    f32x4 o;
+                    for (int ub = 0; ub < 4; ub++) {
+                        f32x4 o;
 #pragma unroll
-                    for (int i = 0; i < 4; i++) o[i] = den > 0.0f ? agg[ub][i] * inv : 0.0f;
-                    *(f32x4 *)(Y + qi * kH + 16 * ub + 4 * g) = o;
+                        for (int i = 0; i < 4; i++) o[i] = den > 0.0f ? agg[ub][i] * inv : 0.0f;
+                        *(f32x4 *)(Y + qi * kH + 16 * ub + 4 * g) = o;
+                    }
                 }
+                m = -INFINITY;
+                den = 0.0f;
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++) agg[ub] = f32x4(0.0f);
+                nd_cur = nd_nxt;
+                t_cur = t_nxt;
+                nd_nxt = nd_after;
+                t_nxt = t_after;
+                qi++;
+                blk = 0;
+            } else {
+                blk++;
             }
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
