@@ -349,6 +349,35 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
                                 tile_nodes, p.o_self + q0 * p.nrb, tid);
 }
 
+// Time encoding of a large first-hop launch as its own stream, after
+// sample_gather has written the timestamp output: one float4 of output per
+// thread in short workgroups.  A tile-looping kernel's write streams reach
+// about 5 TB/s on gfx950; this shape writes at the fill rate (~6.9 TB/s).
+// Slot row j = f / units belongs to query j / s; ts[j] = 0xFFFFFFFF marks an
+// invalid slot (zeros).  Divisions by multiply-high with M = 2^64 / d + 1,
+// exact for 32-bit numerators.
+__global__ __launch_bounds__(256) void tenc_stream(const uint32_t *ts, const uint32_t *tq, uint64_t s_M,
+                                                   uint32_t units, uint64_t u_M, uint32_t total,
+                                                   const float *w, const float *b, float *out) {
+    const uint32_t f = blockIdx.x * 256u + threadIdx.x;
+    if (f >= total) return;
+    const uint32_t j = (uint32_t)__umul64hi(u_M, f);
+    const uint32_t c = f - j * units;
+    const uint32_t t = ts[j];
+    f32x4 r = f32x4(0.0f);
+    if (t != 0xFFFFFFFFu) {
+        const uint32_t i = (uint32_t)__umul64hi(s_M, j);
+        const float dt = (float)(tq[i] - t);
+        const f32x4 w4 = *(const f32x4 *)(w + 4 * c);
+        const f32x4 b4 = *(const f32x4 *)(b + 4 * c);
+        r.x = cos_fp32(__builtin_fmaf(w4.x, dt, b4.x));
+        r.y = cos_fp32(__builtin_fmaf(w4.y, dt, b4.y));
+        r.z = cos_fp32(__builtin_fmaf(w4.z, dt, b4.z));
+        r.w = cos_fp32(__builtin_fmaf(w4.w, dt, b4.w));
+    }
+    __builtin_nontemporal_store(r, (f32x4 *)(out + (size_t)f * 4));
+}
+
 // ---------------------------------------------------------------- export
 __global__ __launch_bounds__(256) void export_table(const uint8_t *blocks, uint32_t block_bytes,
                                                     uint32_t s, int64_t num_nodes, int32_t *nbr,
@@ -391,6 +420,7 @@ uint32_t block_bytes_for(uint32_t s) {
 // queries or more are a multiple of 16, so they start on whole cache lines
 // of every output array.
 constexpr uint32_t kTargetTiles = 4096;
+constexpr uint64_t kTencStreamMin = 1u << 20;   // float4 outputs from which tenc_stream is used
 
 uint32_t tile_queries(uint32_t s, uint32_t nq) {
     uint32_t cap = kTileSlots / s;
@@ -607,10 +637,22 @@ static int launch_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, 
     p.s_m = ceil_2_40_div(h->s);
     const hipStream_t st = (hipStream_t)stream;
     const dim3 grid((unsigned)((nq + p.tile_q - 1) / p.tile_q));
+    // Large first-hop launches that also write timestamps take the time
+    // encoding out of sample_gather into tenc_stream.
+    const uint64_t tenc_total = (uint64_t)nq * h->s * p.tenc_units;
+    const bool split = !hop2 && out->tenc && out->ts && vec4 && tenc_total >= kTencStreamMin &&
+                       tenc_total < (1ull << 32);
+    if (split) p.o_tenc = nullptr;
     if (hop2)
         hipLaunchKernelGGL(sample_gather<true>, grid, dim3(kTileThreads), 0, st, p);
     else
         hipLaunchKernelGGL(sample_gather<false>, grid, dim3(kTileThreads), 0, st, p);
+    if (split) {
+        const uint64_t sM = ~0ull / h->s + 1, uM = ~0ull / p.tenc_units + 1;
+        hipLaunchKernelGGL(tenc_stream, dim3((unsigned)((tenc_total + 255) / 256)), dim3(256), 0, st,
+                           (const uint32_t *)out->ts, tq, sM, p.tenc_units, uM, (uint32_t)tenc_total, h->w,
+                           h->b, out->tenc);
+    }
     if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
     return NLB_OK;
 }

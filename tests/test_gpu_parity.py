@@ -86,6 +86,31 @@ def test_dense_repeated_prefix():
     _run_stream(w, full_batches={0, 30, 59}, index_batches={10, 20, 40, 50}, check_every=20)
 
 
+def test_time_encoding_launch_paths_agree():
+    """A large first-hop launch that also writes timestamps computes the time
+    encoding in a separate streaming kernel; without the timestamp output
+    (or in a small launch) sample_gather computes it.  Both paths give
+    bit-identical values, and both match the oracle within 1e-5."""
+    import torch
+    w = synth.scaled(synth.workload(4), 20 * 10000)
+    src, dst, t, neg = synth.host_links(w)
+    g = make_gpu_table(w)
+    g.insert(to_dev(src), to_dev(dst), to_dev(t))
+    o = make_oracle(w)
+    o.insert(src, dst, t)
+    rng = np.random.default_rng(8)
+    for nq in (30000, 500):                   # 7.5M and 125k float4 outputs
+        q = np.concatenate([src, dst])[rng.integers(0, 2 * len(src), nq)].astype(np.int32)
+        tq = rng.integers(0, int(t[-1]) + 2, nq).astype(np.uint32)
+        a = g.sample(to_dev(q), to_dev(tq), want=("nbr", "eid", "ts", "tenc"))
+        b = g.sample(to_dev(q), to_dev(tq), want=("tenc",))
+        assert torch.equal(a["tenc"], b["tenc"]), nq
+        fw, fb = synth.time_params(w)
+        oo = o.sample(q[:400], tq[:400], fw, fb, None, None, want=("nbr", "ts", "tenc"))
+        compare_sample({"nbr": a["nbr"][:400], "ts": a["ts"][:400], "tenc": a["tenc"][:400]},
+                       {"nbr": oo["nbr"], "ts": oo["ts"], "tenc": oo["tenc"]}, f"nq={nq}")
+
+
 # ----------------------------------------------------------------------------- invariance
 def _insert_in_batches(w, src, dst, t, B, **kw):
     g = make_gpu_table(w, time=False, **kw)
