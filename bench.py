@@ -11,8 +11,9 @@ inserting the stream up to the start batch.
 
 Prints one JSON line.  `value` is links per second through the whole step;
 queries/s and the kernel-only rates are extra fields.  `roofline` reports
-the sample kernel (the dominant one) against MI355X peak HBM bandwidth,
-timed with HIP events on the stream the kernels run on.  `cpu_baseline`
+the sample call (the dominant work: sample_gather, plus tenc_stream on
+large launches) against MI355X peak HBM bandwidth, timed with HIP events on
+the stream the kernels run on.  `cpu_baseline`
 times the CPU oracle on a bounded prefix of the same workload.
 """
 import argparse
@@ -65,21 +66,29 @@ def sample_bytes(w, valid_slots, queries):
     return reads + writes
 
 
-def measured_traffic(w):
-    """HBM bytes per sample launch from the committed rocprofv3 counter
-    summary of this workload, or None when there is none or the kernel
-    source has changed since the counters were taken."""
+def kernel_source_hash():
+    """sha256 over the sources of the sample kernels (nlb.hip and the shared
+    header), the key under which counter summaries stay valid."""
     import hashlib
+    hs = hashlib.sha256()
+    for f in ("nlb.hip", "nlb_internal.h"):
+        hs.update(open(os.path.join(ROOT, "paper_2402_01964_amd", "csrc", f), "rb").read())
+    return hs.hexdigest()
+
+
+def measured_traffic(w):
+    """HBM bytes per nlb_sample call (all its launches) from the committed
+    rocprofv3 counter summary of this workload, or None when there is none
+    or the kernel sources have changed since the counters were taken."""
     import re
     path = os.path.join(ROOT, "profiles", f"sample_gather_{w.name}.md")
-    src = os.path.join(ROOT, "paper_2402_01964_amd", "csrc", "nlb.hip")
     if not os.path.exists(path):
         return None
-    m = re.search(r"counters: workload=(\S+) kernel=sample_gather traffic_bytes_per_launch=(\S+) "
+    m = re.search(r"counters: workload=(\S+) call=nlb_sample traffic_bytes_per_call=(\S+) "
                   r"kernel_source_sha256=([0-9a-f]+)", open(path).read())
     if not m or m.group(1) != w.name:
         return None
-    if hashlib.sha256(open(src, "rb").read()).hexdigest() != m.group(3):
+    if kernel_source_hash() != m.group(3):
         return None
     return float(m.group(2))
 
@@ -349,11 +358,12 @@ def main():
         "valid_slot_fraction": valid / (queries * w.s),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic,
-                     "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
-                                     "scaled by a copy kernel)",
+                     "traffic_unit": "bytes per nlb_sample call (rocprofv3 FETCH_SIZE + WRITE_SIZE "
+                                     "of its launches, scaled by a copy kernel)",
                      "traffic_rate_gbps": (traffic / (sample_ms.mean() * 1e-3) / 1e9
                                            if traffic else None),
-                     "kernel": "sample_gather",
+                     "kernel": "nlb_sample: sample_gather (+ tenc_stream on large launches "
+                               "that write timestamps)",
                      "bytes_per_launch": s_bytes / K,
                      "bytes_per_query_full_occupancy": full_bytes_per_query},
         "setup_s": setup_s,
