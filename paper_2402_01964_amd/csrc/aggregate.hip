@@ -350,16 +350,13 @@ struct RowParams {
     const float *b;
     const uint8_t *efeat;
     int64_t edge_rows;
-    uint32_t e_dim, e_bf16, erb, e_vec;
+    uint32_t e_dim, erb;
     const uint8_t *nfeat;
-    uint32_t n_dim, n_bf16, nrb, n_vec;
-    uint32_t k1, off_e, off_t, kn, k3;   // layer-1 segments [0,off_e) r_v, [off_e,off_t) e, [off_t,k1) T-enc
+    uint32_t n_dim, nrb;
     const __bf16 *w1, *w2, *w3, *w4;
     const float *b1, *b2, *b3, *b4, *att;
     float *z;
     uint32_t *status;
-    uint32_t ls1, ls3;                   // LDS row strides (elements) of w1 and w3
-    uint32_t o_w1, o_w2, o_w3, o_w4, o_vec, o_y;   // LDS byte offsets
 };
 
 constexpr uint32_t kPs = kH + 8;        // LDS row stride of the permuted w2 / w4
@@ -437,24 +434,95 @@ __device__ __forceinline__ float xor16_max(float v) {
     return v;
 }
 
-template <int GS>
+// LDS layout of aggregate_rows for K1S / K3S k-steps of layers 1 and 3 and
+// TKS k-steps of time encoding.
+template <int K1S, int K3S, int TKS>
+struct RowsLayout {
+    static constexpr uint32_t ls1 = 32u * K1S + 8u, ls3 = 32u * K3S + 8u;
+    static constexpr uint32_t o_w1 = 0;
+    static constexpr uint32_t o_w2 = o_w1 + kH * ls1 * 2u;
+    static constexpr uint32_t o_w3 = o_w2 + kH * kPs * 2u;
+    static constexpr uint32_t o_w4 = o_w3 + kH * ls3 * 2u;
+    static constexpr uint32_t o_vec = o_w4 + kH * kPs * 2u;
+    static constexpr uint32_t o_tenc = o_vec + 5u * kH * 4u;   // w | b, 32 TKS each, zero-padded
+    static constexpr uint32_t o_y = o_tenc + 2u * 32u * TKS * 4u;
+    static constexpr uint32_t bytes = o_y + (kRowThreads / 64) * kGroupQ * kH * 4u;
+};
+
+// One lane's eight consecutive elements c..c+7 of a gathered row, for rows
+// whose size and base address are 16-byte aligned (bf16: one 16-byte load,
+// fp32: two).  The width of such a row is a multiple of 8 (bf16) or 4
+// (fp32), so each 16-byte piece lies wholly inside or wholly past the row;
+// a piece past it is read from the row's start (in bounds) and zeroed when
+// used.  Loading and use are separate steps so that a caller can put all of
+// a block's loads in flight before it waits for the first.
+template <bool BF>
+struct Piece8 {
+    u32x4 w[BF ? 1 : 2];
+};
+
+template <bool BF>
+__device__ __forceinline__ void load_piece(const uint8_t *row, uint32_t dim, uint32_t c, Piece8<BF> &r) {
+    if constexpr (BF) {
+        r.w[0] = *(const u32x4 *)(row + (c + 8u <= dim ? 2u * c : 0u));
+    } else {
+        r.w[0] = *(const u32x4 *)(row + (c + 4u <= dim ? 4u * c : 0u));
+        r.w[1] = *(const u32x4 *)(row + (c + 8u <= dim ? 4u * c + 16u : 0u));
+    }
+}
+
+// The piece as a matrix-core B operand, hi + lo (lo is not formed for bf16
+// rows, whose values are exact in bf16), zero where `ok` is false or past
+// the row.
+template <bool BF>
+__device__ __forceinline__ void piece_operand(const Piece8<BF> &r, uint32_t dim, uint32_t c, bool ok,
+                                              bf16x8 &hi, bf16x8 &lo) {
+    if constexpr (BF) {
+        const bool in = ok && c + 8u <= dim;
+        u32x4 w;
+#pragma unroll
+        for (int i = 0; i < 4; i++) w[i] = in ? r.w[0][i] : 0u;
+        hi = __builtin_bit_cast(bf16x8, w);
+        lo = hi;
+    } else {
+        const bool in0 = ok && c + 4u <= dim, in1 = ok && c + 8u <= dim;
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            v[i] = in0 ? __uint_as_float(r.w[0][i]) : 0.0f;
+            v[4 + i] = in1 ? __uint_as_float(r.w[1][i]) : 0.0f;
+        }
+        split8(v, hi, lo);
+    }
+}
+
+// Specialised per input shape: NKS, EKS and TKS k-steps of layer 1 hold r_v,
+// e and the time encoding, NB / EB say whether the node / link rows are
+// bf16 (else fp32); layer 3 has NKS + 2 k-steps (r_u, then the aggregate).
+// With the shape fixed at compile time every LDS address is a base plus an
+// immediate offset, all k-loops unroll and each segment's loads have one
+// fixed form.
+template <int NKS, int EKS, int TKS, bool NB, bool EB>
 __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
+    constexpr int GS = NKS + EKS, K1S = GS + TKS, K3S = NKS + 2;
+    using L = RowsLayout<K1S, K3S, TKS>;
+    static_assert(NKS <= kRuSteps, "shape");
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-    __bf16 *W1 = (__bf16 *)(smem + p.o_w1);
-    __bf16 *W2 = (__bf16 *)(smem + p.o_w2);
-    __bf16 *W3 = (__bf16 *)(smem + p.o_w3);
-    __bf16 *W4 = (__bf16 *)(smem + p.o_w4);
-    float *vec = (float *)(smem + p.o_vec);   // b1 | b2 | b3 | b4 | att, 64 each
+    __bf16 *W1 = (__bf16 *)(smem + L::o_w1);
+    __bf16 *W2 = (__bf16 *)(smem + L::o_w2);
+    __bf16 *W3 = (__bf16 *)(smem + L::o_w3);
+    __bf16 *W4 = (__bf16 *)(smem + L::o_w4);
+    float *vec = (float *)(smem + L::o_vec);   // b1 | b2 | b3 | b4 | att, 64 each
 
     // Stage the weights (w2, w4 with columns in chained order).
     const uint32_t tid = threadIdx.x;
-    for (uint32_t u = tid; u < kH * (p.k1 / 8); u += kRowThreads) {
-        const uint32_t r = u / (p.k1 / 8), c = (u % (p.k1 / 8)) * 8;
-        *(bf16x8 *)(W1 + r * p.ls1 + c) = *(const bf16x8 *)(p.w1 + (size_t)r * p.k1 + c);
+    for (uint32_t u = tid; u < kH * (K1S * 4u); u += kRowThreads) {
+        const uint32_t r = u / (K1S * 4u), c = (u % (K1S * 4u)) * 8;
+        *(bf16x8 *)(W1 + r * L::ls1 + c) = *(const bf16x8 *)(p.w1 + (size_t)r * (32u * K1S) + c);
     }
-    for (uint32_t u = tid; u < kH * (p.k3 / 8); u += kRowThreads) {
-        const uint32_t r = u / (p.k3 / 8), c = (u % (p.k3 / 8)) * 8;
-        *(bf16x8 *)(W3 + r * p.ls3 + c) = *(const bf16x8 *)(p.w3 + (size_t)r * p.k3 + c);
+    for (uint32_t u = tid; u < kH * (K3S * 4u); u += kRowThreads) {
+        const uint32_t r = u / (K3S * 4u), c = (u % (K3S * 4u)) * 8;
+        *(bf16x8 *)(W3 + r * L::ls3 + c) = *(const bf16x8 *)(p.w3 + (size_t)r * (32u * K3S) + c);
     }
     for (uint32_t u = tid; u < kH * kH; u += kRowThreads) {
         const uint32_t r = u / kH, c = u % kH;
@@ -466,212 +534,287 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
         const float *src = k == 0 ? p.b1 : k == 1 ? p.b2 : k == 2 ? p.b3 : k == 3 ? p.b4 : p.att;
         vec[u] = src[c];
     }
+    float *tw = (float *)(smem + L::o_tenc), *tb = tw + 32 * TKS;
+    for (uint32_t u = tid; u < 32u * TKS; u += kRowThreads) {
+        tw[u] = u < p.d_time ? p.w[u] : 0.0f;
+        tb[u] = u < p.d_time ? p.b[u] : 0.0f;
+    }
     __syncthreads();
 
-    const uint32_t lane = tid & 63, wave = tid >> 6;
+    // The wavefront index as a uniform value, so that all the cursor state
+    // below lives in scalar registers and its branches are scalar.
+    const uint32_t lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint32_t r16 = lane & 15, g = lane >> 4;
-    float *Y = (float *)(smem + p.o_y) + (size_t)wave * (kGroupQ * kH);
+    float *Y = (float *)(smem + L::o_y) + (size_t)wave * (kGroupQ * kH);
     const float *b1 = vec, *b2 = vec + kH, *b3 = vec + 2 * kH, *b4 = vec + 3 * kH, *att = vec + 4 * kH;
-    const uint32_t gs = p.off_t / 32, k1s = p.k1 / 32, k3s = p.k3 / 32, kns = p.kn / 32;
     const uint64_t groups = ((uint64_t)p.nq + kGroupQ - 1) / kGroupQ;
-    const uint32_t waves = gridDim.x * (kRowThreads / 64);
+    const uint64_t gstep = (uint64_t)gridDim.x * (kRowThreads / 64);
+    const uint64_t g0 = (uint64_t)blockIdx.x * (kRowThreads / 64) + wave;
+    if (g0 >= groups) return;   // no workgroup barrier follows
 
-    for (uint64_t grp = (uint64_t)blockIdx.x * (kRowThreads / 64) + wave; grp < groups; grp += waves) {
-        const uint64_t qb = grp * kGroupQ;
-        const uint32_t nqg = (uint32_t)min((uint64_t)kGroupQ, (uint64_t)p.nq - qb);
-        // Software pipeline over the group's (query, row block) units: the
-        // query node and time are read two queries ahead, each block's table
-        // slots one block ahead, so only the row gathers of a block are
-        // waited for when it starts.
-        auto slot_at = [&](int32_t nd, uint32_t t, uint32_t blk) {
-            SlotLds r = {-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
-            const uint32_t a = 16u * blk + r16;
-            if (nd >= 0 && (int64_t)nd < p.num_nodes && a < p.s)
-                r = read_slot(p.blocks, p.block_bytes, p.s, nd, a, t);
-            return r;
-        };
-        int32_t nd_cur = p.node[qb], nd_nxt = nqg > 1 ? p.node[qb + 1] : -1;
-        uint32_t t_cur = p.tq[qb], t_nxt = nqg > 1 ? p.tq[qb + 1] : 0u;
-        SlotLds sl_next = slot_at(nd_cur, t_cur, 0);
-        uint32_t qi = 0, blk = 0;
-        float m = -INFINITY, den = 0.0f;
-        f32x4 agg[4];
-#pragma unroll
-        for (int ub = 0; ub < 4; ub++) agg[ub] = f32x4(0.0f);
-        while (qi < nqg) {
-            // Keeps the LDS-resident biases from being hoisted into
-            // long-lived registers.
-            asm volatile("" ::: "memory");
-            const SlotLds sl = sl_next;
-            const bool last_blk = blk + 1 == p.nbq;
-            if (blk == 0 && (nd_cur < 0 || (int64_t)nd_cur >= p.num_nodes) && lane == 0)
-                atomicOr(p.status, kStatusRange);
-            // Issue the next unit's slot read (and the query after next's ids).
-            int32_t nd_after = -1;
-            uint32_t t_after = 0;
-            if (last_blk) {
-                if (qi + 2 < nqg) {
-                    nd_after = p.node[qb + qi + 2];
-                    t_after = p.tq[qb + qi + 2];
+    auto group_size = [&](uint64_t grp) -> uint32_t {
+        return (uint32_t)min((uint64_t)kGroupQ, (uint64_t)p.nq - grp * kGroupQ);
+    };
+    // Query ids of a group: query i of it in the lanes with r16 == i.  Lanes
+    // past the last query read the last (in bounds; never used), so the loads
+    // are unconditional and land in their final registers.
+    auto load_ids = [&](uint64_t grp, int32_t &nd, uint32_t &t) {
+        const uint64_t q = min(grp * kGroupQ + r16, (uint64_t)p.nq - 1);
+        nd = p.node[q];
+        t = p.tq[q];
+    };
+
+    // The wavefront's units, (group, query, 16-row block) in order over its
+    // groups, run as a software pipeline: a unit's two slot words are read
+    // two units ahead of its computation, its rows are gathered one unit
+    // ahead, and the query ids of the group after next are read when a
+    // group starts.  Only the computation waits, for loads issued a whole
+    // unit earlier.
+    struct SlotRaw {
+        uint64_t key;
+        int32_t x;
+        uint32_t tq;
+        bool ok;   // node in range and slot inside the table
+    };
+    uint64_t ig = g0;   // issue cursor (slot words)
+    uint32_t iq = 0, ib = 0, inq = group_size(g0);
+    int32_t id_nd, pre_nd;
+    uint32_t id_t, pre_t;
+    load_ids(g0, id_nd, id_t);
+    load_ids(g0 + gstep, pre_nd, pre_t);
+    // A unit's two slot words, read unconditionally (a unit past the end, an
+    // out-of-range node or a slot past s reads slot 0 of node 0 and is
+    // marked not ok).
+    auto issue_slot = [&]() {
+        SlotRaw r;
+        const bool live = ig < groups;
+        const int32_t nd = __builtin_amdgcn_readlane(id_nd, (int)iq);
+        r.tq = (uint32_t)__builtin_amdgcn_readlane((int)id_t, (int)iq);
+        const uint32_t a = 16u * ib + r16;
+        r.ok = live && nd >= 0 && (int64_t)nd < p.num_nodes && a < p.s;
+        const uint8_t *bp = p.blocks + (size_t)(r.ok ? nd : 0) * p.block_bytes;
+        const uint32_t aa = r.ok ? a : 0u;
+        r.key = ((const uint64_t *)bp)[aa];
+        r.x = ((const int32_t *)(bp + 8u * p.s))[aa];
+        if (live) {
+            if (++ib == p.nbq) {
+                ib = 0;
+                if (++iq == inq) {
+                    iq = 0;
+                    ig += gstep;
+                    id_nd = pre_nd;
+                    id_t = pre_t;
+                    if (ig < groups) inq = group_size(ig);
+                    load_ids(ig + gstep, pre_nd, pre_t);
                 }
-                sl_next = qi + 1 < nqg ? slot_at(nd_nxt, t_nxt, 0) : SlotLds{-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
-            } else {
-                sl_next = slot_at(nd_cur, t_cur, blk + 1);
-            }
-            const bool valid = sl.x >= 0;
-            // Gathered inputs (r_v and e) of this lane's row, all issued first.
-            float v[GS][8];
-#pragma unroll
-            for (int ks = 0; ks < GS; ks++) {
-#pragma unroll
-                for (int i = 0; i < 8; i++) v[ks][i] = 0.0f;
-                if ((uint32_t)ks >= gs || !valid) continue;
-                const uint32_t c0 = 32u * ks + 8u * g;
-                if (c0 < p.off_e)
-                    load8(p.nfeat + (size_t)sl.x * p.nrb, p.n_dim, p.n_bf16, p.n_vec, c0, v[ks]);
-                else if ((int64_t)sl.e < p.edge_rows)
-                    load8(p.efeat + (size_t)sl.e * p.erb, p.e_dim, p.e_bf16, p.e_vec, c0 - p.off_e, v[ks]);
-            }
-            // Layer 1: a1 = ReLU(W1 x + b1).
-            f32x4 acc[4];
-#pragma unroll
-            for (int ub = 0; ub < 4; ub++) acc[ub] = f32x4(0.0f);
-#pragma unroll
-            for (int ks = 0; ks < GS; ks++) {
-                if ((uint32_t)ks >= gs) continue;
-                const uint32_t c0 = 32u * ks;
-                bf16x8 hi, lo;
-                split8(v[ks], hi, lo);
-                const bool use_lo = c0 < p.off_e ? !p.n_bf16 : !p.e_bf16;
-                mfma4(acc, W1, p.ls1, c0, r16, g, hi, lo, use_lo);
-            }
-            for (uint32_t ks = gs; ks < k1s; ks++) {
-                const uint32_t k = 32u * ks + 8u * g - p.off_t;
-                float t[8];
-#pragma unroll
-                for (int i = 0; i < 8; i++)
-                    t[i] = (valid && k + i < p.d_time)
-                               ? cos_fp32(__builtin_fmaf(p.w[k + i], sl.dt, p.b[k + i]))
-                               : 0.0f;
-                bf16x8 hi, lo;
-                split8(t, hi, lo);
-                mfma4(acc, W1, p.ls1, 32u * ks, r16, g, hi, lo, true);
-            }
-#pragma unroll
-            for (int ub = 0; ub < 4; ub++)
-#pragma unroll
-                for (int i = 0; i < 4; i++) acc[ub][i] = fmaxf(acc[ub][i] + b1[16 * ub + 4 * g + i], 0.0f);
-            // Layer 2: messages h = W2 a1 + b2, and the logit w^T h of the row.
-            f32x4 h[4];
-#pragma unroll
-            for (int ub = 0; ub < 4; ub++) h[ub] = f32x4(0.0f);
-            chain64(h, acc, W2, r16, g);
-            float part = 0.0f;
-#pragma unroll
-            for (int ub = 0; ub < 4; ub++)
-#pragma unroll
-                for (int i = 0; i < 4; i++) {
-                    h[ub][i] += b2[16 * ub + 4 * g + i];
-                    part = __builtin_fmaf(att[16 * ub + 4 * g + i], h[ub][i], part);
-                }
-            part += __shfl_xor(part, 16);
-            part += __shfl_xor(part, 32);
-            // Online softmax over the query's valid rows (a block without a
-            // valid row changes nothing; the test is wave-uniform).
-            const float lg = valid ? part : -INFINITY;
-            const float mb = xor16_max(lg);
-            if (mb != -INFINITY) {
-                const float mn = fmaxf(m, mb);
-                const float sc = (m == -INFINITY) ? 0.0f : expf(m - mn);
-                const float e = valid ? expf(lg - mn) : 0.0f;
-                den = den * sc + xor16_sum(e);
-#pragma unroll
-                for (int ub = 0; ub < 4; ub++)
-#pragma unroll
-                    for (int i = 0; i < 4; i++) agg[ub][i] = agg[ub][i] * sc + xor16_sum(e * h[ub][i]);
-                m = mn;
-            }
-            if (last_blk) {
-                if (r16 == 0) {
-                    const float inv = den > 0.0f ? 1.0f / den : 0.0f;
-#pragma unroll
-                    for (int ub = 0; ub < 4; ub++) {
-                        f32x4 o;
-#pragma unroll
-                        for (int i = 0; i < 4; i++) o[i] = den > 0.0f ? agg[ub][i] * inv : 0.0f;
-                        *(f32x4 *)(Y + qi * kH + 16 * ub + 4 * g) = o;
-                    }
-                }
-                m = -INFINITY;
-                den = 0.0f;
-#pragma unroll
-                for (int ub = 0; ub < 4; ub++) agg[ub] = f32x4(0.0f);
-                nd_cur = nd_nxt;
-                t_cur = t_nxt;
-                nd_nxt = nd_after;
-                t_nxt = t_after;
-                qi++;
-                blk = 0;
-            } else {
-                blk++;
             }
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        return r;
+    };
+    // Gathered inputs (r_v and e) of this lane's row of a unit; invalid rows
+    // read row 0 and are zeroed when used.
+    struct Rows {
+        Piece8<NB> n[NKS > 0 ? NKS : 1];
+        Piece8<EB> e[EKS > 0 ? EKS : 1];
+    };
+    auto issue_rows = [&](const SlotLds &sl, Rows &r) {
+        const bool valid = sl.x >= 0;
+        if constexpr (NKS > 0) {
+            const uint8_t *nrow = p.nfeat + (size_t)(valid ? sl.x : 0) * p.nrb;
+#pragma unroll
+            for (int ks = 0; ks < NKS; ks++) load_piece<NB>(nrow, p.n_dim, 32u * ks + 8u * g, r.n[ks]);
+        }
+        if constexpr (EKS > 0) {
+            const bool ev = valid && (int64_t)sl.e < p.edge_rows;
+            const uint8_t *erow = p.efeat + (size_t)(ev ? sl.e : 0u) * p.erb;
+#pragma unroll
+            for (int ks = 0; ks < EKS; ks++) load_piece<EB>(erow, p.e_dim, 32u * ks + 8u * g, r.e[ks]);
+        }
+    };
 
+    SlotRaw raw_n = issue_slot();
+    SlotLds sl_c = decode_slot(raw_n.ok ? raw_n.key : 0ull, raw_n.x, raw_n.tq);
+    Rows rows_c;
+    issue_rows(sl_c, rows_c);
+    raw_n = issue_slot();
+    uint64_t cg = g0;   // compute cursor
+    uint32_t cq = 0, cb = 0, cnq = group_size(g0);
+    // Query ids of the compute group for MLP_out (lanes r16 >= cnq unused).
+    int32_t mo_nd = p.node[min(g0 * kGroupQ + r16, (uint64_t)p.nq - 1)];
+    float m = -INFINITY, den = 0.0f;
+    f32x4 agg[4];
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++) agg[ub] = f32x4(0.0f);
+    while (cg < groups) {
+        // Keeps the LDS-resident biases from being hoisted into long-lived
+        // registers.
         asm volatile("" ::: "memory");
-        // MLP_out for the group: row r16 = query qb + r16, input [r_u | aggregate].
-        const bool vq = r16 < nqg;
-        int32_t nr = vq ? p.node[qb + r16] : -1;
-        if (nr >= 0 && (int64_t)nr >= p.num_nodes) nr = -1;
-        float ru[kRuSteps][8];
+        const bool last_blk = cb + 1 == p.nbq;
+        const bool group_end = last_blk && cq + 1 == cnq;
+        // The next unit's rows, the slot words of the one after, and at a
+        // group's last unit its MLP_out rows r_u.
+        const SlotLds sl_n = decode_slot(raw_n.ok ? raw_n.key : 0ull, raw_n.x, raw_n.tq);
+        Rows rows_n;
+        issue_rows(sl_n, rows_n);
+        raw_n = issue_slot();
+        const bool vq = r16 < cnq;
+        const int32_t nr = (vq && mo_nd >= 0 && (int64_t)mo_nd < p.num_nodes) ? mo_nd : -1;
+        Piece8<NB> ru[NKS > 0 ? NKS : 1];
+        if constexpr (NKS > 0) {
+            if (group_end) {
+                const uint8_t *urow = p.nfeat + (size_t)(nr >= 0 ? nr : 0) * p.nrb;
 #pragma unroll
-        for (int ks = 0; ks < kRuSteps; ks++) {
-#pragma unroll
-            for (int i = 0; i < 8; i++) ru[ks][i] = 0.0f;
-            if ((uint32_t)ks < kns && nr >= 0)
-                load8(p.nfeat + (size_t)nr * p.nrb, p.n_dim, p.n_bf16, p.n_vec, 32u * ks + 8u * g, ru[ks]);
+                for (int ks = 0; ks < NKS; ks++) load_piece<NB>(urow, p.n_dim, 32u * ks + 8u * g, ru[ks]);
+            }
         }
-        f32x4 acc3[4];
+        // Keep the scheduler from sinking the loads to their uses.
+        __builtin_amdgcn_sched_barrier(0);
+
+        const SlotLds sl = sl_c;
+        const bool valid = sl.x >= 0;
+        const bool ev = valid && (int64_t)sl.e < p.edge_rows;
+        // Layer 1: a1 = ReLU(W1 x + b1).
+        f32x4 acc[4];
 #pragma unroll
-        for (int ub = 0; ub < 4; ub++) acc3[ub] = f32x4(0.0f);
+        for (int ub = 0; ub < 4; ub++) acc[ub] = f32x4(0.0f);
 #pragma unroll
-        for (int ks = 0; ks < kRuSteps; ks++) {
-            if ((uint32_t)ks >= kns) continue;
+        for (int ks = 0; ks < NKS; ks++) {
             bf16x8 hi, lo;
-            split8(ru[ks], hi, lo);
-            mfma4(acc3, W3, p.ls3, 32u * ks, r16, g, hi, lo, !p.n_bf16);
+            piece_operand<NB>(rows_c.n[ks], p.n_dim, 32u * ks + 8u * g, valid, hi, lo);
+            mfma4(acc, W1, L::ls1, 32u * ks, r16, g, hi, lo, !NB);
         }
-        for (uint32_t ks = kns; ks < k3s; ks++) {
-            const uint32_t c = 32u * ks + 8u * g - p.kn;
-            float y[8];
 #pragma unroll
-            for (int i = 0; i < 8; i++) y[i] = vq ? Y[r16 * kH + c + i] : 0.0f;
+        for (int ks = 0; ks < EKS; ks++) {
             bf16x8 hi, lo;
-            split8(y, hi, lo);
-            mfma4(acc3, W3, p.ls3, 32u * ks, r16, g, hi, lo, true);
+            piece_operand<EB>(rows_c.e[ks], p.e_dim, 32u * ks + 8u * g, ev, hi, lo);
+            mfma4(acc, W1, L::ls1, 32u * (NKS + ks), r16, g, hi, lo, !EB);
+        }
+#pragma unroll 1
+        for (int ks = 0; ks < TKS; ks++) {
+            const uint32_t k = 32u * ks + 8u * g;
+            float t[8];
+#pragma unroll
+            for (int i = 0; i < 8; i++) {
+                const float c = cos_fp32(__builtin_fmaf(tw[k + i], sl.dt, tb[k + i]));
+                t[i] = (valid && k + i < p.d_time) ? c : 0.0f;
+            }
+            bf16x8 hi, lo;
+            split8(t, hi, lo);
+            mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
         }
 #pragma unroll
         for (int ub = 0; ub < 4; ub++)
 #pragma unroll
-            for (int i = 0; i < 4; i++) acc3[ub][i] = fmaxf(acc3[ub][i] + b3[16 * ub + 4 * g + i], 0.0f);
-        f32x4 zo[4];
+            for (int i = 0; i < 4; i++) acc[ub][i] = fmaxf(acc[ub][i] + b1[16 * ub + 4 * g + i], 0.0f);
+        // Layer 2: messages h = W2 a1 + b2, and the logit w^T h of the row.
+        f32x4 h[4];
 #pragma unroll
-        for (int ub = 0; ub < 4; ub++) zo[ub] = f32x4(0.0f);
-        chain64(zo, acc3, W4, r16, g);
-        if (vq) {
+        for (int ub = 0; ub < 4; ub++) h[ub] = f32x4(0.0f);
+        chain64(h, acc, W2, r16, g);
+        float part = 0.0f;
 #pragma unroll
-            for (int ub = 0; ub < 4; ub++) {
+        for (int ub = 0; ub < 4; ub++)
 #pragma unroll
-                for (int i = 0; i < 4; i++) zo[ub][i] += b4[16 * ub + 4 * g + i];
-                *(f32x4 *)(p.z + (qb + r16) * kH + 16 * ub + 4 * g) = zo[ub];
+            for (int i = 0; i < 4; i++) {
+                h[ub][i] += b2[16 * ub + 4 * g + i];
+                part = __builtin_fmaf(att[16 * ub + 4 * g + i], h[ub][i], part);
             }
+        part += __shfl_xor(part, 16);
+        part += __shfl_xor(part, 32);
+        // Online softmax over the query's valid rows (a block without a valid
+        // row changes nothing; the test is wave-uniform).
+        const float lg = valid ? part : -INFINITY;
+        const float mb = xor16_max(lg);
+        if (mb != -INFINITY) {
+            const float mn = fmaxf(m, mb);
+            const float sc = (m == -INFINITY) ? 0.0f : expf(m - mn);
+            const float e = valid ? expf(lg - mn) : 0.0f;
+            den = den * sc + xor16_sum(e);
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+                for (int i = 0; i < 4; i++) agg[ub][i] = agg[ub][i] * sc + xor16_sum(e * h[ub][i]);
+            m = mn;
         }
-        // Y is rewritten by the next group of this wavefront only.
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (last_blk) {
+            if (r16 == 0) {
+                const float inv = den > 0.0f ? 1.0f / den : 0.0f;
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++) {
+                    f32x4 o;
+#pragma unroll
+                    for (int i = 0; i < 4; i++) o[i] = den > 0.0f ? agg[ub][i] * inv : 0.0f;
+                    *(f32x4 *)(Y + cq * kH + 16 * ub + 4 * g) = o;
+                }
+            }
+            m = -INFINITY;
+            den = 0.0f;
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++) agg[ub] = f32x4(0.0f);
+        }
+        if (group_end) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            asm volatile("" ::: "memory");
+            // MLP_out for the group: row r16 = query qb + r16, input
+            // [r_u | aggregate].
+            const uint64_t qb = cg * kGroupQ;
+            if (vq && g == 0 && nr < 0) atomicOr(p.status, kStatusRange);   // an out-of-range query
+            f32x4 acc3[4];
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++) acc3[ub] = f32x4(0.0f);
+#pragma unroll
+            for (int ks = 0; ks < NKS; ks++) {
+                bf16x8 hi, lo;
+                piece_operand<NB>(ru[ks], p.n_dim, 32u * ks + 8u * g, nr >= 0, hi, lo);
+                mfma4(acc3, W3, L::ls3, 32u * ks, r16, g, hi, lo, !NB);
+            }
+#pragma unroll
+            for (int ks = 0; ks < 2; ks++) {
+                const uint32_t c = 32u * ks + 8u * g;
+                float y[8];
+#pragma unroll
+                for (int i = 0; i < 8; i++) y[i] = vq ? Y[r16 * kH + c + i] : 0.0f;
+                bf16x8 hi, lo;
+                split8(y, hi, lo);
+                mfma4(acc3, W3, L::ls3, 32u * (NKS + ks), r16, g, hi, lo, true);
+            }
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+                for (int i = 0; i < 4; i++) acc3[ub][i] = fmaxf(acc3[ub][i] + b3[16 * ub + 4 * g + i], 0.0f);
+            f32x4 zo[4];
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++) zo[ub] = f32x4(0.0f);
+            chain64(zo, acc3, W4, r16, g);
+            if (vq) {
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++) {
+#pragma unroll
+                    for (int i = 0; i < 4; i++) zo[ub][i] += b4[16 * ub + 4 * g + i];
+                    *(f32x4 *)(p.z + (qb + r16) * kH + 16 * ub + 4 * g) = zo[ub];
+                }
+            }
+            // Y is rewritten by the next group of this wavefront only.
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            cg += gstep;
+            cq = 0;
+            cb = 0;
+            if (cg < groups) {
+                cnq = group_size(cg);
+                mo_nd = p.node[min(cg * kGroupQ + r16, (uint64_t)p.nq - 1)];
+            }
+        } else if (last_blk) {
+            cq++;
+            cb = 0;
+        } else {
+            cb++;
+        }
+        sl_c = sl_n;
+        rows_c = rows_n;
     }
 }
 
@@ -757,11 +900,11 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
 
     // The wavefront-per-query kernel for launches large enough to give every
     // wavefront of the GPU several query groups (or queries of several row
-    // blocks, where the tiled kernel's LDS staging is largest), when its
-    // operands fit: node rows up to 128 wide, at most 8 gathered k-steps (r_v
-    // and e), all four weight matrices plus the aggregate staging within one
-    // workgroup's LDS.  Small launches keep the tiled kernel, whose many
-    // short tiles start more work in parallel.
+    // blocks, where the tiled kernel's LDS staging is largest), for the input
+    // shapes it is instantiated for, with 16-byte aligned rows, and when all
+    // four weight matrices plus the aggregate staging fit one workgroup's
+    // LDS.  Small launches keep the tiled kernel, whose many short tiles
+    // start more work in parallel; other shapes take it at every size.
     if (nq >= kRowsMinQueries || (h->s > 16 && nq >= kRowsMinQueriesWide)) {
         RowParams r;
         std::memset(&r, 0, sizeof(r));
@@ -779,19 +922,10 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
         r.efeat = p.efeat;
         r.edge_rows = p.edge_rows;
         r.e_dim = p.e_dim;
-        r.e_bf16 = p.e_bf16;
         r.erb = p.erb;
-        r.e_vec = p.e_vec;
         r.nfeat = p.nfeat;
         r.n_dim = p.n_dim;
-        r.n_bf16 = p.n_bf16;
         r.nrb = p.nrb;
-        r.n_vec = p.n_vec;
-        r.k1 = p.k1;
-        r.off_e = p.off_e;
-        r.off_t = p.off_t;
-        r.kn = pad32(p.n_dim);
-        r.k3 = p.k3;
         r.w1 = p.w1;
         r.w2 = p.w2;
         r.w3 = p.w3;
@@ -803,18 +937,29 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
         r.att = p.att;
         r.z = z;
         r.status = h->status;
-        r.ls1 = p.k1 + 8;
-        r.ls3 = p.k3 + 8;
-        r.o_w1 = 0;
-        r.o_w2 = align16(r.o_w1 + kH * r.ls1 * 2u);
-        r.o_w3 = align16(r.o_w2 + kH * kPs * 2u);
-        r.o_w4 = align16(r.o_w3 + kH * r.ls3 * 2u);
-        r.o_vec = align16(r.o_w4 + kH * kPs * 2u);
-        r.o_y = align16(r.o_vec + 5u * kH * 4u);
-        const uint32_t bytes = r.o_y + (kRowThreads / 64) * kGroupQ * kH * 4u;
-        const uint32_t gs = r.off_t / 32;
-        if (r.kn <= 32u * kRuSteps && gs <= 8 && bytes <= kAggLdsMax) {
-            const void *kern = gs <= 4 ? (const void *)aggregate_rows<4> : (const void *)aggregate_rows<8>;
+        const uint32_t nks = p.off_e / 32, eks = (p.off_t - p.off_e) / 32, tks = (p.k1 - p.off_t) / 32;
+        const bool n_ok = nks == 0 || p.n_vec, e_ok = eks == 0 || p.e_vec;
+        const void *kern = nullptr;
+        uint32_t bytes = 0;
+        void (*launch)(dim3, uint32_t, hipStream_t, const RowParams &) = nullptr;
+#define NLB_ROWS_SHAPE(A, B, C, NB, EB)                                                              \
+    if (!kern && n_ok && e_ok && nks == A && eks == B && tks == C && (A == 0 || p.n_bf16 == NB) &&     \
+        (B == 0 || p.e_bf16 == EB)) {                                                                 \
+        kern = (const void *)aggregate_rows<A, B, C, NB, EB>;                                         \
+        bytes = RowsLayout<A + B + C, A + 2, C>::bytes;                                                  \
+        launch = [](dim3 gr, uint32_t l, hipStream_t st, const RowParams &rp) {                       \
+            hipLaunchKernelGGL((aggregate_rows<A, B, C, NB, EB>), gr, dim3(kRowThreads), l, st, rp);  \
+        };                                                                                            \
+    }
+        // The input shapes of the synthetic workloads with 16-byte aligned
+        // rows (100 time dims; bf16 node rows 128 wide with bf16 link rows
+        // 128 wide or none; fp32 link rows 100 or 172 wide and no node rows).
+        NLB_ROWS_SHAPE(4, 0, 4, true, false)
+        NLB_ROWS_SHAPE(4, 4, 4, true, true)
+        NLB_ROWS_SHAPE(0, 6, 4, false, false)
+        NLB_ROWS_SHAPE(0, 4, 4, false, false)
+#undef NLB_ROWS_SHAPE
+        if (kern && bytes <= kAggLdsMax) {
             if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kAggLdsMax) !=
                 hipSuccess)
                 return NLB_EDEVICE;
@@ -824,11 +969,7 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
                 return NLB_EDEVICE;
             const uint64_t groups = ((uint64_t)nq + kGroupQ - 1) / kGroupQ;
             const uint64_t wgs = (groups + kRowThreads / 64 - 1) / (kRowThreads / 64);
-            const dim3 grid((unsigned)(wgs < (uint64_t)cus ? wgs : (uint64_t)cus));
-            if (gs <= 4)
-                hipLaunchKernelGGL(aggregate_rows<4>, grid, dim3(kRowThreads), bytes, (hipStream_t)stream, r);
-            else
-                hipLaunchKernelGGL(aggregate_rows<8>, grid, dim3(kRowThreads), bytes, (hipStream_t)stream, r);
+            launch(dim3((unsigned)(wgs < (uint64_t)cus ? wgs : (uint64_t)cus)), bytes, (hipStream_t)stream, r);
             if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
             return NLB_OK;
         }

@@ -87,14 +87,11 @@ struct SlotLds {
     float dt;
 };
 
-// Slot a of node `node`'s block, seen by a query at time tq: eq. (1) keeps
-// only entries stored strictly before tq.
-__device__ __forceinline__ SlotLds read_slot(const uint8_t *blocks, uint32_t block_bytes, uint32_t s,
-                                             int32_t node, uint32_t a, uint32_t tq) {
+// A slot as a query at time tq sees it, from its two stored words (the
+// class-encoded key and x): eq. (1) keeps only entries stored strictly
+// before tq.
+__device__ __forceinline__ SlotLds decode_slot(uint64_t key, int32_t xv, uint32_t tq) {
     SlotLds sl = {-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
-    const uint8_t *blk = blocks + (size_t)node * block_bytes;
-    const uint64_t key = ((const uint64_t *)blk)[a];
-    const int32_t xv = ((const int32_t *)(blk + 8u * s))[a];
     const uint32_t t = (uint32_t)key & kTimeMask;
     if (key != 0 && t < tq) {
         const uint32_t ef = (uint32_t)(key >> kTimeBits);
@@ -104,6 +101,13 @@ __device__ __forceinline__ SlotLds read_slot(const uint8_t *blocks, uint32_t blo
         sl.dt = (float)(tq - t);
     }
     return sl;
+}
+
+// Slot a of node `node`'s block, seen by a query at time tq.
+__device__ __forceinline__ SlotLds read_slot(const uint8_t *blocks, uint32_t block_bytes, uint32_t s,
+                                             int32_t node, uint32_t a, uint32_t tq) {
+    const uint8_t *blk = blocks + (size_t)node * block_bytes;
+    return decode_slot(((const uint64_t *)blk)[a], ((const int32_t *)(blk + 8u * s))[a], tq);
 }
 
 // ---------------------------------------------------------------- LDS max-merge
