@@ -367,13 +367,23 @@ __device__ __forceinline__ uint32_t chain_unit(uint32_t c) {
     return 32u * ks + (i < 4 ? 4u * g + i : 16u + 4u * g + (i - 4u));
 }
 
+// v = hi + lo (bf16 each, hi rounded to nearest).  Pairs are converted
+// together and the fp32 value of each hi is taken from the packed bits.
 __device__ __forceinline__ void split8(const float v[8], bf16x8 &hi, bf16x8 &lo) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    u32x4 hw, lw;
 #pragma unroll
-    for (int i = 0; i < 8; i++) {
-        const __bf16 t = (__bf16)v[i];
-        hi[i] = t;
-        lo[i] = (__bf16)(v[i] - (float)t);
+    for (int j = 0; j < 4; j++) {
+        const uint32_t hb =
+            __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){v[2 * j], v[2 * j + 1]}, bf16x2));
+        const float h0 = __uint_as_float(hb << 16), h1 = __uint_as_float(hb & 0xFFFF0000u);
+        hw[j] = hb;
+        lw[j] = __builtin_bit_cast(uint32_t,
+                                   __builtin_convertvector((f32x2){v[2 * j] - h0, v[2 * j + 1] - h1}, bf16x2));
     }
+    hi = __builtin_bit_cast(bf16x8, hw);
+    lo = __builtin_bit_cast(bf16x8, lw);
 }
 
 // acc[ub] += W[16 ub .. 16 ub + 15][k-step] x (hi + lo) for the four unit blocks.
@@ -516,9 +526,15 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
 
     // Stage the weights (w2, w4 with columns in chained order).
     const uint32_t tid = threadIdx.x;
+    // The time-encoding columns past d_time are staged as zeros: the rows'
+    // time encodings are then used unmasked (finite values, zero weight).
     for (uint32_t u = tid; u < kH * (K1S * 4u); u += kRowThreads) {
         const uint32_t r = u / (K1S * 4u), c = (u % (K1S * 4u)) * 8;
-        *(bf16x8 *)(W1 + r * L::ls1 + c) = *(const bf16x8 *)(p.w1 + (size_t)r * (32u * K1S) + c);
+        bf16x8 v = *(const bf16x8 *)(p.w1 + (size_t)r * (32u * K1S) + c);
+#pragma unroll
+        for (int i = 0; i < 8; i++)
+            if (c + i >= 32u * GS + p.d_time) v[i] = (__bf16)0.0f;
+        *(bf16x8 *)(W1 + r * L::ls1 + c) = v;
     }
     for (uint32_t u = tid; u < kH * (K3S * 4u); u += kRowThreads) {
         const uint32_t r = u / (K3S * 4u), c = (u % (K3S * 4u)) * 8;
@@ -540,6 +556,20 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
         tb[u] = u < p.d_time ? p.b[u] : 0.0f;
     }
     __syncthreads();
+    // max |w| and max |b| of the time encoding, for the per-unit test that
+    // every argument w dt + b is inside the fast cosine's range.
+    float wmax = 0.0f, bmax = 0.0f;
+    for (uint32_t u = tid & 63; u < 32u * TKS; u += 64) {
+        wmax = fmaxf(wmax, fabsf(tw[u]));
+        bmax = fmaxf(bmax, fabsf(tb[u]));
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        wmax = fmaxf(wmax, __shfl_xor(wmax, o));
+        bmax = fmaxf(bmax, __shfl_xor(bmax, o));
+    }
+    wmax = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(wmax)));
+    bmax = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(bmax)));
 
     // The wavefront index as a uniform value, so that all the cursor state
     // below lives in scalar registers and its branches are scalar.
@@ -673,6 +703,8 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
         const SlotLds sl = sl_c;
         const bool valid = sl.x >= 0;
         const bool ev = valid && (int64_t)sl.e < p.edge_rows;
+        // A block without a valid row changes nothing (wave-uniform test).
+        if (__builtin_amdgcn_ballot_w64(valid) != 0) {
         // Layer 1: a1 = ReLU(W1 x + b1).
         f32x4 acc[4];
 #pragma unroll
@@ -689,18 +721,38 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
             piece_operand<EB>(rows_c.e[ks], p.e_dim, 32u * ks + 8u * g, ev, hi, lo);
             mfma4(acc, W1, L::ls1, 32u * (NKS + ks), r16, g, hi, lo, !EB);
         }
+        // Time encoding of every row, unmasked: an invalid row has dt = 0
+        // and its result is never used, padding columns have zero weight.
+        // The fast cosine serves the whole block when max |w| max dt + max |b|
+        // (with margin for the rounding of the bound) is inside its range.
+        const float dtmax = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(xor16_max(sl.dt))));
+        if (wmax * dtmax + bmax < 0.5f * kCosFastLimit) {
 #pragma unroll 1
-        for (int ks = 0; ks < TKS; ks++) {
-            const uint32_t k = 32u * ks + 8u * g;
-            float t[8];
+            for (int ks = 0; ks < TKS; ks++) {
+                const uint32_t k = 32u * ks + 8u * g;
+                const f32x4 w0 = *(const f32x4 *)(tw + k), w1 = *(const f32x4 *)(tw + k + 4);
+                const f32x4 c0 = *(const f32x4 *)(tb + k), c1 = *(const f32x4 *)(tb + k + 4);
+                float t[8];
 #pragma unroll
-            for (int i = 0; i < 8; i++) {
-                const float c = cos_fp32(__builtin_fmaf(tw[k + i], sl.dt, tb[k + i]));
-                t[i] = (valid && k + i < p.d_time) ? c : 0.0f;
+                for (int i = 0; i < 4; i++) {
+                    t[i] = cos_fp32_small(__builtin_fmaf(w0[i], sl.dt, c0[i]));
+                    t[4 + i] = cos_fp32_small(__builtin_fmaf(w1[i], sl.dt, c1[i]));
+                }
+                bf16x8 hi, lo;
+                split8(t, hi, lo);
+                mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
             }
-            bf16x8 hi, lo;
-            split8(t, hi, lo);
-            mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
+        } else {
+#pragma unroll 1
+            for (int ks = 0; ks < TKS; ks++) {
+                const uint32_t k = 32u * ks + 8u * g;
+                float t[8];
+#pragma unroll
+                for (int i = 0; i < 8; i++) t[i] = cos_fp32(__builtin_fmaf(tw[k + i], sl.dt, tb[k + i]));
+                bf16x8 hi, lo;
+                split8(t, hi, lo);
+                mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
+            }
         }
 #pragma unroll
         for (int ub = 0; ub < 4; ub++)
@@ -735,6 +787,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
 #pragma unroll
                 for (int i = 0; i < 4; i++) agg[ub][i] = agg[ub][i] * sc + xor16_sum(e * h[ub][i]);
             m = mn;
+        }
         }
         if (last_blk) {
             if (r16 == 0) {

@@ -69,12 +69,17 @@ __device__ __attribute__((noinline)) float cos_fp32_wide(float x) {
 // fraction; measured on gfx950 over a dense grid of [-1/2, 1/2] its error is
 // below 1.3e-7, and the whole function stays below 3e-7 absolute for
 // |x| < 1e9 against a double-precision cosine.
+constexpr float kCosFastLimit = 8589934592.0f;   // 2^33
+
+// The fast path alone, for a caller that has checked |x| < kCosFastLimit.
+__device__ __forceinline__ float cos_fp32_small(float x) {
+    const double y = (double)x * 0.15915494309189533577;
+    const float f = (float)(y - __builtin_rint(y));
+    return __builtin_amdgcn_cosf(f);
+}
+
 __device__ __forceinline__ float cos_fp32(float x) {
-    if (fabsf(x) < 8589934592.0f) {
-        const double y = (double)x * 0.15915494309189533577;
-        const float f = (float)(y - __builtin_rint(y));
-        return __builtin_amdgcn_cosf(f);
-    }
+    if (fabsf(x) < kCosFastLimit) return cos_fp32_small(x);
     return cos_fp32_wide(x);
 }
 
