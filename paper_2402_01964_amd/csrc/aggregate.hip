@@ -398,10 +398,11 @@ __device__ __forceinline__ void mfma4(f32x4 (&acc)[4], const __bf16 *W, uint32_t
     }
 }
 
-// acc (layer input in the D layout, 64 units) -> next layer through the
-// permuted weights Wp: acc_out[ub] += Wp x act.
+// act (a layer's output in the D layout, 64 units) -> next layer through
+// weights whose 64 columns from k0 on are in chained order (row stride ls):
+// out[ub] += Wp x act.
 __device__ __forceinline__ void chain64(f32x4 (&out)[4], const f32x4 (&act)[4], const __bf16 *Wp,
-                                        uint32_t r16, uint32_t g) {
+                                        uint32_t ls, uint32_t k0, uint32_t r16, uint32_t g) {
 #pragma unroll
     for (int ks = 0; ks < 2; ks++) {
         float v[8];
@@ -412,7 +413,7 @@ __device__ __forceinline__ void chain64(f32x4 (&out)[4], const f32x4 (&act)[4], 
         }
         bf16x8 hi, lo;
         split8(v, hi, lo);
-        mfma4(out, Wp, kPs, 32u * ks, r16, g, hi, lo, true);
+        mfma4(out, Wp, ls, k0 + 32u * ks, r16, g, hi, lo, true);
     }
 }
 
@@ -455,8 +456,7 @@ struct RowsLayout {
     static constexpr uint32_t o_w4 = o_w3 + kH * ls3 * 2u;
     static constexpr uint32_t o_vec = o_w4 + kH * kPs * 2u;
     static constexpr uint32_t o_tenc = o_vec + 5u * kH * 4u;   // w | b, 32 TKS each, zero-padded
-    static constexpr uint32_t o_y = o_tenc + 2u * 32u * TKS * 4u;
-    static constexpr uint32_t bytes = o_y + (kRowThreads / 64) * kGroupQ * kH * 4u;
+    static constexpr uint32_t bytes = o_tenc + 2u * 32u * TKS * 4u;
 };
 
 // One lane's eight consecutive elements c..c+7 of a gathered row, for rows
@@ -522,9 +522,10 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
     __bf16 *W2 = (__bf16 *)(smem + L::o_w2);
     __bf16 *W3 = (__bf16 *)(smem + L::o_w3);
     __bf16 *W4 = (__bf16 *)(smem + L::o_w4);
-    float *vec = (float *)(smem + L::o_vec);   // b1 | b2 | b3 | b4 | att, 64 each
+    float *vec = (float *)(smem + L::o_vec);   // b1 | b2 | b3 | b4 | v, 64 each
 
-    // Stage the weights (w2, w4 with columns in chained order).
+    // Stage the weights: w2, w4 and the aggregate columns of w3 in chained
+    // order.
     const uint32_t tid = threadIdx.x;
     // The time-encoding columns past d_time are staged as zeros: the rows'
     // time encodings are then used unmasked (finite values, zero weight).
@@ -536,19 +537,32 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
             if (c + i >= 32u * GS + p.d_time) v[i] = (__bf16)0.0f;
         *(bf16x8 *)(W1 + r * L::ls1 + c) = v;
     }
-    for (uint32_t u = tid; u < kH * (K3S * 4u); u += kRowThreads) {
-        const uint32_t r = u / (K3S * 4u), c = (u % (K3S * 4u)) * 8;
-        *(bf16x8 *)(W3 + r * L::ls3 + c) = *(const bf16x8 *)(p.w3 + (size_t)r * (32u * K3S) + c);
+    if constexpr (NKS > 0) {
+        for (uint32_t u = tid; u < kH * (NKS * 4u); u += kRowThreads) {
+            const uint32_t r = u / (NKS * 4u), c = (u % (NKS * 4u)) * 8;
+            *(bf16x8 *)(W3 + r * L::ls3 + c) = *(const bf16x8 *)(p.w3 + (size_t)r * (32u * K3S) + c);
+        }
     }
     for (uint32_t u = tid; u < kH * kH; u += kRowThreads) {
         const uint32_t r = u / kH, c = u % kH;
         W2[r * kPs + c] = p.w2[r * kH + chain_unit(c)];
         W4[r * kPs + c] = p.w4[r * kH + chain_unit(c)];
+        W3[r * L::ls3 + 32u * NKS + c] = p.w3[(size_t)r * (32u * K3S) + 32u * NKS + chain_unit(c)];
     }
+    // Layer 2 is affine, so the logit att . (w2 a1 + b2) of a row is
+    // v . a1 up to a shift common to all rows (which the softmax cancels),
+    // with v = w2^T att; and the aggregate sum_s alpha_s (w2 a1_s + b2) is
+    // w2 (sum_s alpha_s a1_s) + b2.  So layer 2 runs once per query.
     for (uint32_t u = tid; u < 5u * kH; u += kRowThreads) {
         const uint32_t k = u / kH, c = u % kH;
-        const float *src = k == 0 ? p.b1 : k == 1 ? p.b2 : k == 2 ? p.b3 : k == 3 ? p.b4 : p.att;
-        vec[u] = src[c];
+        float val;
+        if (k < 4) {
+            val = (k == 0 ? p.b1 : k == 1 ? p.b2 : k == 2 ? p.b3 : p.b4)[c];
+        } else {
+            val = 0.0f;
+            for (uint32_t r = 0; r < kH; r++) val = __builtin_fmaf(p.att[r], (float)p.w2[r * kH + c], val);
+        }
+        vec[u] = val;
     }
     float *tw = (float *)(smem + L::o_tenc), *tb = tw + 32 * TKS;
     for (uint32_t u = tid; u < 32u * TKS; u += kRowThreads) {
@@ -575,8 +589,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
     // below lives in scalar registers and its branches are scalar.
     const uint32_t lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint32_t r16 = lane & 15, g = lane >> 4;
-    float *Y = (float *)(smem + L::o_y) + (size_t)wave * (kGroupQ * kH);
-    const float *b1 = vec, *b2 = vec + kH, *b3 = vec + 2 * kH, *b4 = vec + 3 * kH, *att = vec + 4 * kH;
+    const float *b1 = vec, *b2 = vec + kH, *b3 = vec + 2 * kH, *b4 = vec + 3 * kH, *va = vec + 4 * kH;
     const uint64_t groups = ((uint64_t)p.nq + kGroupQ - 1) / kGroupQ;
     const uint64_t gstep = (uint64_t)gridDim.x * (kRowThreads / 64);
     const uint64_t g0 = (uint64_t)blockIdx.x * (kRowThreads / 64) + wave;
@@ -672,9 +685,14 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
     // Query ids of the compute group for MLP_out (lanes r16 >= cnq unused).
     int32_t mo_nd = p.node[min(g0 * kGroupQ + r16, (uint64_t)p.nq - 1)];
     float m = -INFINITY, den = 0.0f;
-    f32x4 agg[4];
+    // Running softmax sums of the current query, and the group's finished
+    // aggregates sum_s alpha_s a1_s: query q's in the lanes with r16 == q, in
+    // the D layout (units 16 ub + 4 g + i), with ne = 1 where the query had a
+    // valid row (else its aggregate is zero).
+    f32x4 agg[4], aggq[4];
+    float ne = 0.0f;
 #pragma unroll
-    for (int ub = 0; ub < 4; ub++) agg[ub] = f32x4(0.0f);
+    for (int ub = 0; ub < 4; ub++) agg[ub] = aggq[ub] = f32x4(0.0f);
     while (cg < groups) {
         // Keeps the LDS-resident biases from being hoisted into long-lived
         // registers.
@@ -758,19 +776,12 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
         for (int ub = 0; ub < 4; ub++)
 #pragma unroll
             for (int i = 0; i < 4; i++) acc[ub][i] = fmaxf(acc[ub][i] + b1[16 * ub + 4 * g + i], 0.0f);
-        // Layer 2: messages h = W2 a1 + b2, and the logit w^T h of the row.
-        f32x4 h[4];
-#pragma unroll
-        for (int ub = 0; ub < 4; ub++) h[ub] = f32x4(0.0f);
-        chain64(h, acc, W2, r16, g);
+        // The row's logit v . a1 (up to the common shift att . b2).
         float part = 0.0f;
 #pragma unroll
         for (int ub = 0; ub < 4; ub++)
 #pragma unroll
-            for (int i = 0; i < 4; i++) {
-                h[ub][i] += b2[16 * ub + 4 * g + i];
-                part = __builtin_fmaf(att[16 * ub + 4 * g + i], h[ub][i], part);
-            }
+            for (int i = 0; i < 4; i++) part = __builtin_fmaf(va[16 * ub + 4 * g + i], acc[ub][i], part);
         part += __shfl_xor(part, 16);
         part += __shfl_xor(part, 32);
         // Online softmax over the query's valid rows (a block without a valid
@@ -785,20 +796,20 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
 #pragma unroll
             for (int ub = 0; ub < 4; ub++)
 #pragma unroll
-                for (int i = 0; i < 4; i++) agg[ub][i] = agg[ub][i] * sc + xor16_sum(e * h[ub][i]);
+                for (int i = 0; i < 4; i++) agg[ub][i] = agg[ub][i] * sc + xor16_sum(e * acc[ub][i]);
             m = mn;
         }
         }
         if (last_blk) {
-            if (r16 == 0) {
+            // The sums are the same in every lane of a row group: the lanes
+            // of row cq keep them, normalised.
+            if (r16 == cq) {
                 const float inv = den > 0.0f ? 1.0f / den : 0.0f;
 #pragma unroll
-                for (int ub = 0; ub < 4; ub++) {
-                    f32x4 o;
+                for (int ub = 0; ub < 4; ub++)
 #pragma unroll
-                    for (int i = 0; i < 4; i++) o[i] = den > 0.0f ? agg[ub][i] * inv : 0.0f;
-                    *(f32x4 *)(Y + cq * kH + 16 * ub + 4 * g) = o;
-                }
+                    for (int i = 0; i < 4; i++) aggq[ub][i] = agg[ub][i] * inv;
+                ne = den > 0.0f ? 1.0f : 0.0f;
             }
             m = -INFINITY;
             den = 0.0f;
@@ -806,12 +817,9 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
             for (int ub = 0; ub < 4; ub++) agg[ub] = f32x4(0.0f);
         }
         if (group_end) {
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            asm volatile("" ::: "memory");
             // MLP_out for the group: row r16 = query qb + r16, input
-            // [r_u | aggregate].
+            // [r_u | aggregate], the aggregate w2 aggq + b2 (zero for a query
+            // without valid rows).
             const uint64_t qb = cg * kGroupQ;
             if (vq && g == 0 && nr < 0) atomicOr(p.status, kStatusRange);   // an out-of-range query
             f32x4 acc3[4];
@@ -823,16 +831,15 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
                 piece_operand<NB>(ru[ks], p.n_dim, 32u * ks + 8u * g, nr >= 0, hi, lo);
                 mfma4(acc3, W3, L::ls3, 32u * ks, r16, g, hi, lo, !NB);
             }
+            f32x4 hq[4];
 #pragma unroll
-            for (int ks = 0; ks < 2; ks++) {
-                const uint32_t c = 32u * ks + 8u * g;
-                float y[8];
+            for (int ub = 0; ub < 4; ub++) hq[ub] = f32x4(0.0f);
+            chain64(hq, aggq, W2, kPs, 0, r16, g);
 #pragma unroll
-                for (int i = 0; i < 8; i++) y[i] = vq ? Y[r16 * kH + c + i] : 0.0f;
-                bf16x8 hi, lo;
-                split8(y, hi, lo);
-                mfma4(acc3, W3, L::ls3, 32u * (NKS + ks), r16, g, hi, lo, true);
-            }
+            for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+                for (int i = 0; i < 4; i++) hq[ub][i] = ne * (hq[ub][i] + b2[16 * ub + 4 * g + i]);
+            chain64(acc3, hq, W3, L::ls3, 32u * NKS, r16, g);
 #pragma unroll
             for (int ub = 0; ub < 4; ub++)
 #pragma unroll
@@ -840,7 +847,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
             f32x4 zo[4];
 #pragma unroll
             for (int ub = 0; ub < 4; ub++) zo[ub] = f32x4(0.0f);
-            chain64(zo, acc3, W4, r16, g);
+            chain64(zo, acc3, W4, kPs, 0, r16, g);
             if (vq) {
 #pragma unroll
                 for (int ub = 0; ub < 4; ub++) {
@@ -849,10 +856,9 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
                     *(f32x4 *)(p.z + (qb + r16) * kH + 16 * ub + 4 * g) = zo[ub];
                 }
             }
-            // Y is rewritten by the next group of this wavefront only.
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++) aggq[ub] = f32x4(0.0f);
+            ne = 0.0f;
             cg += gstep;
             cq = 0;
             cb = 0;
