@@ -331,10 +331,9 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_fused(AggParams p) {
 // after the staging, so the latency of one query's gathers is covered by
 // the other wavefronts of the CU.
 constexpr int kRowThreads = 512;    // 8 wavefronts per workgroup
-constexpr int kGroupQ = 16;         // queries per MLP_out block
+constexpr uint32_t kMaxGroupQ = 16;  // queries per MLP_out block at most
 constexpr int kRuSteps = 4;         // k-steps of r_u held in registers: node rows up to 128 wide
-constexpr uint32_t kRowsMinQueries = 65536;
-constexpr uint32_t kRowsMinQueriesWide = 4096;
+constexpr uint32_t kRowsMinQueries = 1;
 
 struct RowParams {
     const uint8_t *blocks;
@@ -344,6 +343,7 @@ struct RowParams {
     const int32_t *node;
     const uint32_t *tq;
     uint32_t nq;
+    uint32_t gq;                     // queries per group (1..16)
     uint32_t nbq;                    // 16-row blocks per query
     uint32_t d_time;
     const float *w;
@@ -459,22 +459,30 @@ struct RowsLayout {
     static constexpr uint32_t bytes = o_tenc + 2u * 32u * TKS * 4u;
 };
 
-// One lane's eight consecutive elements c..c+7 of a gathered row, for rows
-// whose size and base address are 16-byte aligned (bf16: one 16-byte load,
-// fp32: two).  The width of such a row is a multiple of 8 (bf16) or 4
-// (fp32), so each 16-byte piece lies wholly inside or wholly past the row;
-// a piece past it is read from the row's start (in bounds) and zeroed when
-// used.  Loading and use are separate steps so that a caller can put all of
-// a block's loads in flight before it waits for the first.
-template <bool BF>
+// One lane's eight consecutive elements c..c+7 of a gathered row, in one of
+// three forms fixed per row matrix:
+//   kBf16Vec  bf16 rows, size and base 16-byte aligned: one 16-byte load;
+//   kBf16Word bf16 rows, size and base 4-byte aligned: four 4-byte loads;
+//   kF32Vec   fp32 rows, size and base 16-byte aligned: two 16-byte loads.
+// Each load then lies wholly inside or wholly past the row (the width is a
+// multiple of 8, 2 or 4 elements respectively); a load past it reads the
+// row's start instead (in bounds) and is zeroed when used.  Loading and use
+// are separate steps so that a caller can put all of a block's loads in
+// flight before it waits for the first.
+constexpr int kBf16Vec = 0, kBf16Word = 1, kF32Vec = 2;
+
+template <int KIND>
 struct Piece8 {
-    u32x4 w[BF ? 1 : 2];
+    u32x4 w[KIND == kF32Vec ? 2 : 1];
 };
 
-template <bool BF>
-__device__ __forceinline__ void load_piece(const uint8_t *row, uint32_t dim, uint32_t c, Piece8<BF> &r) {
-    if constexpr (BF) {
+template <int KIND>
+__device__ __forceinline__ void load_piece(const uint8_t *row, uint32_t dim, uint32_t c, Piece8<KIND> &r) {
+    if constexpr (KIND == kBf16Vec) {
         r.w[0] = *(const u32x4 *)(row + (c + 8u <= dim ? 2u * c : 0u));
+    } else if constexpr (KIND == kBf16Word) {
+#pragma unroll
+        for (int j = 0; j < 4; j++) r.w[0][j] = *(const uint32_t *)(row + (c + 2u * j + 2u <= dim ? 2u * (c + 2u * j) : 0u));
     } else {
         r.w[0] = *(const u32x4 *)(row + (c + 4u <= dim ? 4u * c : 0u));
         r.w[1] = *(const u32x4 *)(row + (c + 8u <= dim ? 4u * c + 16u : 0u));
@@ -484,14 +492,16 @@ __device__ __forceinline__ void load_piece(const uint8_t *row, uint32_t dim, uin
 // The piece as a matrix-core B operand, hi + lo (lo is not formed for bf16
 // rows, whose values are exact in bf16), zero where `ok` is false or past
 // the row.
-template <bool BF>
-__device__ __forceinline__ void piece_operand(const Piece8<BF> &r, uint32_t dim, uint32_t c, bool ok,
+template <int KIND>
+__device__ __forceinline__ void piece_operand(const Piece8<KIND> &r, uint32_t dim, uint32_t c, bool ok,
                                               bf16x8 &hi, bf16x8 &lo) {
-    if constexpr (BF) {
-        const bool in = ok && c + 8u <= dim;
+    if constexpr (KIND != kF32Vec) {
         u32x4 w;
 #pragma unroll
-        for (int i = 0; i < 4; i++) w[i] = in ? r.w[0][i] : 0u;
+        for (int j = 0; j < 4; j++) {
+            const bool in = ok && (KIND == kBf16Vec ? c + 8u <= dim : c + 2u * j + 2u <= dim);
+            w[j] = in ? r.w[0][j] : 0u;
+        }
         hi = __builtin_bit_cast(bf16x8, w);
         lo = hi;
     } else {
@@ -507,12 +517,12 @@ __device__ __forceinline__ void piece_operand(const Piece8<BF> &r, uint32_t dim,
 }
 
 // Specialised per input shape: NKS, EKS and TKS k-steps of layer 1 hold r_v,
-// e and the time encoding, NB / EB say whether the node / link rows are
-// bf16 (else fp32); layer 3 has NKS + 2 k-steps (r_u, then the aggregate).
-// With the shape fixed at compile time every LDS address is a base plus an
-// immediate offset, all k-loops unroll and each segment's loads have one
-// fixed form.
-template <int NKS, int EKS, int TKS, bool NB, bool EB>
+// e and the time encoding, NK / EK are the piece forms of the node / link
+// rows; layer 3 has NKS + 2 k-steps (r_u, then the aggregate).  With the
+// shape fixed at compile time every LDS address is a base plus an immediate
+// offset, all k-loops unroll and each segment's loads have one fixed form.
+// Queries are taken in groups of p.gq <= 16 (one MLP_out block each).
+template <int NKS, int EKS, int TKS, int NK, int EK>
 __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
     constexpr int GS = NKS + EKS, K1S = GS + TKS, K3S = NKS + 2;
     using L = RowsLayout<K1S, K3S, TKS>;
@@ -590,19 +600,22 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
     const uint32_t lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint32_t r16 = lane & 15, g = lane >> 4;
     const float *b1 = vec, *b2 = vec + kH, *b3 = vec + 2 * kH, *b4 = vec + 3 * kH, *va = vec + 4 * kH;
-    const uint64_t groups = ((uint64_t)p.nq + kGroupQ - 1) / kGroupQ;
+    const uint32_t gq = p.gq;
+    const uint64_t groups = ((uint64_t)p.nq + gq - 1) / gq;
     const uint64_t gstep = (uint64_t)gridDim.x * (kRowThreads / 64);
-    const uint64_t g0 = (uint64_t)blockIdx.x * (kRowThreads / 64) + wave;
+    // Consecutive groups go to different workgroups first, so a launch with
+    // few groups spreads over the CUs.
+    const uint64_t g0 = (uint64_t)wave * gridDim.x + blockIdx.x;
     if (g0 >= groups) return;   // no workgroup barrier follows
 
     auto group_size = [&](uint64_t grp) -> uint32_t {
-        return (uint32_t)min((uint64_t)kGroupQ, (uint64_t)p.nq - grp * kGroupQ);
+        return (uint32_t)min((uint64_t)gq, (uint64_t)p.nq - grp * gq);
     };
     // Query ids of a group: query i of it in the lanes with r16 == i.  Lanes
     // past the last query read the last (in bounds; never used), so the loads
     // are unconditional and land in their final registers.
     auto load_ids = [&](uint64_t grp, int32_t &nd, uint32_t &t) {
-        const uint64_t q = min(grp * kGroupQ + r16, (uint64_t)p.nq - 1);
+        const uint64_t q = min(grp * gq + r16, (uint64_t)p.nq - 1);
         nd = p.node[q];
         t = p.tq[q];
     };
@@ -657,21 +670,21 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
     // Gathered inputs (r_v and e) of this lane's row of a unit; invalid rows
     // read row 0 and are zeroed when used.
     struct Rows {
-        Piece8<NB> n[NKS > 0 ? NKS : 1];
-        Piece8<EB> e[EKS > 0 ? EKS : 1];
+        Piece8<NK> n[NKS > 0 ? NKS : 1];
+        Piece8<EK> e[EKS > 0 ? EKS : 1];
     };
     auto issue_rows = [&](const SlotLds &sl, Rows &r) {
         const bool valid = sl.x >= 0;
         if constexpr (NKS > 0) {
             const uint8_t *nrow = p.nfeat + (size_t)(valid ? sl.x : 0) * p.nrb;
 #pragma unroll
-            for (int ks = 0; ks < NKS; ks++) load_piece<NB>(nrow, p.n_dim, 32u * ks + 8u * g, r.n[ks]);
+            for (int ks = 0; ks < NKS; ks++) load_piece<NK>(nrow, p.n_dim, 32u * ks + 8u * g, r.n[ks]);
         }
         if constexpr (EKS > 0) {
             const bool ev = valid && (int64_t)sl.e < p.edge_rows;
             const uint8_t *erow = p.efeat + (size_t)(ev ? sl.e : 0u) * p.erb;
 #pragma unroll
-            for (int ks = 0; ks < EKS; ks++) load_piece<EB>(erow, p.e_dim, 32u * ks + 8u * g, r.e[ks]);
+            for (int ks = 0; ks < EKS; ks++) load_piece<EK>(erow, p.e_dim, 32u * ks + 8u * g, r.e[ks]);
         }
     };
 
@@ -683,7 +696,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
     uint64_t cg = g0;   // compute cursor
     uint32_t cq = 0, cb = 0, cnq = group_size(g0);
     // Query ids of the compute group for MLP_out (lanes r16 >= cnq unused).
-    int32_t mo_nd = p.node[min(g0 * kGroupQ + r16, (uint64_t)p.nq - 1)];
+    int32_t mo_nd = p.node[min(g0 * gq + r16, (uint64_t)p.nq - 1)];
     float m = -INFINITY, den = 0.0f;
     // Running softmax sums of the current query, and the group's finished
     // aggregates sum_s alpha_s a1_s: query q's in the lanes with r16 == q, in
@@ -707,12 +720,12 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
         raw_n = issue_slot();
         const bool vq = r16 < cnq;
         const int32_t nr = (vq && mo_nd >= 0 && (int64_t)mo_nd < p.num_nodes) ? mo_nd : -1;
-        Piece8<NB> ru[NKS > 0 ? NKS : 1];
+        Piece8<NK> ru[NKS > 0 ? NKS : 1];
         if constexpr (NKS > 0) {
             if (group_end) {
                 const uint8_t *urow = p.nfeat + (size_t)(nr >= 0 ? nr : 0) * p.nrb;
 #pragma unroll
-                for (int ks = 0; ks < NKS; ks++) load_piece<NB>(urow, p.n_dim, 32u * ks + 8u * g, ru[ks]);
+                for (int ks = 0; ks < NKS; ks++) load_piece<NK>(urow, p.n_dim, 32u * ks + 8u * g, ru[ks]);
             }
         }
         // Keep the scheduler from sinking the loads to their uses.
@@ -730,14 +743,14 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
 #pragma unroll
         for (int ks = 0; ks < NKS; ks++) {
             bf16x8 hi, lo;
-            piece_operand<NB>(rows_c.n[ks], p.n_dim, 32u * ks + 8u * g, valid, hi, lo);
-            mfma4(acc, W1, L::ls1, 32u * ks, r16, g, hi, lo, !NB);
+            piece_operand<NK>(rows_c.n[ks], p.n_dim, 32u * ks + 8u * g, valid, hi, lo);
+            mfma4(acc, W1, L::ls1, 32u * ks, r16, g, hi, lo, NK == kF32Vec);
         }
 #pragma unroll
         for (int ks = 0; ks < EKS; ks++) {
             bf16x8 hi, lo;
-            piece_operand<EB>(rows_c.e[ks], p.e_dim, 32u * ks + 8u * g, ev, hi, lo);
-            mfma4(acc, W1, L::ls1, 32u * (NKS + ks), r16, g, hi, lo, !EB);
+            piece_operand<EK>(rows_c.e[ks], p.e_dim, 32u * ks + 8u * g, ev, hi, lo);
+            mfma4(acc, W1, L::ls1, 32u * (NKS + ks), r16, g, hi, lo, EK == kF32Vec);
         }
         // Time encoding of every row, unmasked: an invalid row has dt = 0
         // and its result is never used, padding columns have zero weight.
@@ -820,7 +833,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
             // MLP_out for the group: row r16 = query qb + r16, input
             // [r_u | aggregate], the aggregate w2 aggq + b2 (zero for a query
             // without valid rows).
-            const uint64_t qb = cg * kGroupQ;
+            const uint64_t qb = cg * gq;
             if (vq && g == 0 && nr < 0) atomicOr(p.status, kStatusRange);   // an out-of-range query
             f32x4 acc3[4];
 #pragma unroll
@@ -828,8 +841,8 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
 #pragma unroll
             for (int ks = 0; ks < NKS; ks++) {
                 bf16x8 hi, lo;
-                piece_operand<NB>(ru[ks], p.n_dim, 32u * ks + 8u * g, nr >= 0, hi, lo);
-                mfma4(acc3, W3, L::ls3, 32u * ks, r16, g, hi, lo, !NB);
+                piece_operand<NK>(ru[ks], p.n_dim, 32u * ks + 8u * g, nr >= 0, hi, lo);
+                mfma4(acc3, W3, L::ls3, 32u * ks, r16, g, hi, lo, NK == kF32Vec);
             }
             f32x4 hq[4];
 #pragma unroll
@@ -864,7 +877,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
             cb = 0;
             if (cg < groups) {
                 cnq = group_size(cg);
-                mo_nd = p.node[min(cg * kGroupQ + r16, (uint64_t)p.nq - 1)];
+                mo_nd = p.node[min(cg * gq + r16, (uint64_t)p.nq - 1)];
             }
         } else if (last_blk) {
             cq++;
@@ -957,14 +970,19 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
     p.z = z;
     p.status = h->status;
 
-    // The wavefront-per-query kernel for launches large enough to give every
-    // wavefront of the GPU several query groups (or queries of several row
-    // blocks, where the tiled kernel's LDS staging is largest), for the input
-    // shapes it is instantiated for, with 16-byte aligned rows, and when all
-    // four weight matrices plus the aggregate staging fit one workgroup's
-    // LDS.  Small launches keep the tiled kernel, whose many short tiles
-    // start more work in parallel; other shapes take it at every size.
-    if (nq >= kRowsMinQueries || (h->s > 16 && nq >= kRowsMinQueriesWide)) {
+    // The wavefront-per-query kernel, for the input shapes it is instantiated
+    // for (those of the synthetic workloads) when its weights fit one
+    // workgroup's LDS; other shapes take the tiled kernel.
+    const uint32_t nks = p.off_e / 32, eks = (p.off_t - p.off_e) / 32, tks = (p.k1 - p.off_t) / 32;
+    auto piece_kind = [](uint32_t row_bytes, const void *base, bool bf16) -> int {
+        const uintptr_t a = (uintptr_t)base;
+        if (row_bytes % 16 == 0 && a % 16 == 0) return bf16 ? kBf16Vec : kF32Vec;
+        if (bf16 && row_bytes % 4 == 0 && a % 4 == 0) return kBf16Word;
+        return -1;
+    };
+    const int nkind = nks ? piece_kind(p.nrb, p.nfeat, p.n_bf16) : 0;
+    const int ekind = eks ? piece_kind(p.erb, p.efeat, p.e_bf16) : 0;
+    if (nq >= kRowsMinQueries && nkind >= 0 && ekind >= 0) {
         RowParams r;
         std::memset(&r, 0, sizeof(r));
         r.blocks = p.blocks;
@@ -996,27 +1014,25 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
         r.att = p.att;
         r.z = z;
         r.status = h->status;
-        const uint32_t nks = p.off_e / 32, eks = (p.off_t - p.off_e) / 32, tks = (p.k1 - p.off_t) / 32;
-        const bool n_ok = nks == 0 || p.n_vec, e_ok = eks == 0 || p.e_vec;
         const void *kern = nullptr;
         uint32_t bytes = 0;
         void (*launch)(dim3, uint32_t, hipStream_t, const RowParams &) = nullptr;
-#define NLB_ROWS_SHAPE(A, B, C, NB, EB)                                                              \
-    if (!kern && n_ok && e_ok && nks == A && eks == B && tks == C && (A == 0 || p.n_bf16 == NB) &&     \
-        (B == 0 || p.e_bf16 == EB)) {                                                                 \
-        kern = (const void *)aggregate_rows<A, B, C, NB, EB>;                                         \
-        bytes = RowsLayout<A + B + C, A + 2, C>::bytes;                                                  \
+#define NLB_ROWS_SHAPE(A, B, C, NK, EK)                                                              \
+    if (!kern && nks == A && eks == B && tks == C && (A == 0 || nkind == NK) && (B == 0 || ekind == EK)) { \
+        kern = (const void *)aggregate_rows<A, B, C, NK, EK>;                                         \
+        bytes = RowsLayout<A + B + C, A + 2, C>::bytes;                                               \
         launch = [](dim3 gr, uint32_t l, hipStream_t st, const RowParams &rp) {                       \
-            hipLaunchKernelGGL((aggregate_rows<A, B, C, NB, EB>), gr, dim3(kRowThreads), l, st, rp);  \
+            hipLaunchKernelGGL((aggregate_rows<A, B, C, NK, EK>), gr, dim3(kRowThreads), l, st, rp);  \
         };                                                                                            \
     }
-        // The input shapes of the synthetic workloads with 16-byte aligned
-        // rows (100 time dims; bf16 node rows 128 wide with bf16 link rows
-        // 128 wide or none; fp32 link rows 100 or 172 wide and no node rows).
-        NLB_ROWS_SHAPE(4, 0, 4, true, false)
-        NLB_ROWS_SHAPE(4, 4, 4, true, true)
-        NLB_ROWS_SHAPE(0, 6, 4, false, false)
-        NLB_ROWS_SHAPE(0, 4, 4, false, false)
+        // 100 time dims with: bf16 node rows 128 wide and bf16 link rows 128
+        // wide or none; no node rows and fp32 link rows 100 or 172 wide, or
+        // bf16 link rows 186 wide (4-byte aligned).
+        NLB_ROWS_SHAPE(4, 0, 4, kBf16Vec, kBf16Vec)
+        NLB_ROWS_SHAPE(4, 4, 4, kBf16Vec, kBf16Vec)
+        NLB_ROWS_SHAPE(0, 6, 4, kBf16Vec, kF32Vec)
+        NLB_ROWS_SHAPE(0, 4, 4, kBf16Vec, kF32Vec)
+        NLB_ROWS_SHAPE(0, 6, 4, kBf16Vec, kBf16Word)
 #undef NLB_ROWS_SHAPE
         if (kern && bytes <= kAggLdsMax) {
             if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kAggLdsMax) !=
@@ -1026,9 +1042,12 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
             if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess ||
                 cus < 1)
                 return NLB_EDEVICE;
-            const uint64_t groups = ((uint64_t)nq + kGroupQ - 1) / kGroupQ;
-            const uint64_t wgs = (groups + kRowThreads / 64 - 1) / (kRowThreads / 64);
-            launch(dim3((unsigned)(wgs < (uint64_t)cus ? wgs : (uint64_t)cus)), bytes, (hipStream_t)stream, r);
+            // One persistent workgroup per CU; groups of up to 16 queries,
+            // fewer when that leaves wavefronts without one.
+            const uint64_t waves = (uint64_t)cus * (kRowThreads / 64);
+            r.gq = (uint32_t)std::min<uint64_t>(kMaxGroupQ, std::max<uint64_t>(1, (nq + waves - 1) / waves));
+            const uint64_t groups = ((uint64_t)nq + r.gq - 1) / r.gq;
+            launch(dim3((unsigned)std::min<uint64_t>(groups, (uint64_t)cus)), bytes, (hipStream_t)stream, r);
             if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
             return NLB_OK;
         }

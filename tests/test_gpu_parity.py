@@ -384,11 +384,53 @@ def test_aggregate_matches_oracle(k):
     assert worst <= AGG_TOL
 
 
+# Input shapes that no wavefront-per-query instance covers (they take the
+# tiled kernel): fp32 node rows 36 wide with bf16 link rows 90 wide and a
+# 50-dim time encoding; bf16 node rows 200 wide (more than four k-steps).
+TILED_SHAPES = {
+    "f32node36-bf16edge90-t50": dict(node_dim=36, node_dtype="f32", edge_dim=90, edge_dtype="bf16", d_time=50),
+    "bf16node200": dict(node_dim=200, node_dtype="bf16", edge_dim=0),
+}
+
+
+@pytest.mark.parametrize("shape", sorted(TILED_SHAPES))
+def test_aggregate_tiled_shapes_match_oracle(shape):
+    """Eq. (4) forward for input shapes outside the per-query kernel's
+    instances, at 3 000 and 70 001 queries, against the fp64 oracle."""
+    import dataclasses
+    base = synth.workload(1)
+    w = dataclasses.replace(synth.scaled(base, 12 * base.batch), **TILED_SHAPES[shape])
+    src, dst, t, neg = synth.host_links(w)
+    ef = synth.host_features(w, "edge") if w.edge_dim else None
+    nf = synth.host_features(w, "node") if w.node_dim else None
+    g = make_gpu_table(w, feat_to_dev(ef, w.edge_dtype) if ef is not None else None,
+                       feat_to_dev(nf, w.node_dtype) if nf is not None else None)
+    o = make_oracle(w)
+    g.insert(to_dev(src), to_dev(dst), to_dev(t))
+    o.insert(src, dst, t)
+    W = synth.agg_weights(w)
+    fw, fb = synth.time_params(w)
+    rng = np.random.default_rng(7)
+    ends = np.concatenate([src, dst, neg])
+    worst = 0.0
+    for nq in (3000, 70001):
+        q = ends[rng.integers(0, len(ends), nq)].astype(np.int32)
+        tq = rng.integers(0, int(t[-1]) + 2, nq).astype(np.uint32)
+        tq[::9] = 0                                # no valid slot
+        gz = g.aggregate(to_dev(q), to_dev(tq), _agg_dev(W)).cpu().numpy()
+        pos = np.sort(rng.choice(nq, min(nq, 1500), replace=False))
+        oz = o.aggregate(q[pos], tq[pos], fw, fb, ef, nf, W)
+        worst = max(worst, agg_error(gz[pos], oz))
+    print(f"aggregate tiled shape {shape}: max scaled error {worst:.3e}")
+    assert g.status() == 0
+    assert worst <= AGG_TOL
+
+
 @pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
 def test_aggregate_large_launch_matches_oracle(k):
-    """Launches of 70 001 queries (the size class that takes the
-    wavefront-per-query kernel, with a partial last group of queries) on every
-    workload shape; 1 500 sampled queries are compared with the oracle,
+    """Launches of 70 001 queries (full groups of 16 queries in the
+    wavefront-per-query kernel, with a partial last group) on every workload
+    shape; 1 500 sampled queries are compared with the oracle,
     including queries without a valid slot and repeated query nodes."""
     import torch
     base = synth.workload(k)
