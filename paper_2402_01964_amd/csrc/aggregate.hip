@@ -334,6 +334,9 @@ constexpr int kRowThreads = 512;    // 8 wavefronts per workgroup
 constexpr uint32_t kMaxGroupQ = 16;  // queries per MLP_out block at most
 constexpr int kRuSteps = 4;         // k-steps of r_u held in registers: node rows up to 128 wide
 constexpr uint32_t kRowsMinQueries = 1;
+// Blocks with at least this many valid rows compute the time encoding of
+// every row in registers; sparser blocks compute their valid rows only.
+constexpr uint32_t kDenseRows = 12;
 
 struct RowParams {
     const uint8_t *blocks;
@@ -346,6 +349,8 @@ struct RowParams {
     uint32_t gq;                     // queries per group (1..16)
     uint32_t nbq;                    // 16-row blocks per query
     uint32_t d_time;
+    uint32_t nch;                    // 4-column chunks of the time encoding
+    uint64_t nch_m;                  // ceil(2^32 / nch): i / nch = (i nch_m) >> 32 for i < 2^16
     const float *w;
     const float *b;
     const uint8_t *efeat;
@@ -359,7 +364,9 @@ struct RowParams {
     uint32_t *status;
 };
 
-constexpr uint32_t kPs = kH + 8;        // LDS row stride of the permuted w2 / w4
+// LDS row stride of the permuted w2 / w4: unpadded, as they are read once
+// per query group only.
+constexpr uint32_t kPs = kH;
 
 // Input unit feeding slot (ks, g, i) of a chained layer's B operand.
 __device__ __forceinline__ uint32_t chain_unit(uint32_t c) {
@@ -384,6 +391,21 @@ __device__ __forceinline__ void split8(const float v[8], bf16x8 &hi, bf16x8 &lo)
     }
     hi = __builtin_bit_cast(bf16x8, hw);
     lo = __builtin_bit_cast(bf16x8, lw);
+}
+
+// The same split for four values, as packed bf16 pairs.
+__device__ __forceinline__ void split4(const float v[4], u32x2 &hw, u32x2 &lw) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+        const uint32_t hb =
+            __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){v[2 * j], v[2 * j + 1]}, bf16x2));
+        const float h0 = __uint_as_float(hb << 16), h1 = __uint_as_float(hb & 0xFFFF0000u);
+        hw[j] = hb;
+        lw[j] = __builtin_bit_cast(uint32_t,
+                                   __builtin_convertvector((f32x2){v[2 * j] - h0, v[2 * j + 1] - h1}, bf16x2));
+    }
 }
 
 // acc[ub] += W[16 ub .. 16 ub + 15][k-step] x (hi + lo) for the four unit blocks.
@@ -456,7 +478,13 @@ struct RowsLayout {
     static constexpr uint32_t o_w4 = o_w3 + kH * ls3 * 2u;
     static constexpr uint32_t o_vec = o_w4 + kH * kPs * 2u;
     static constexpr uint32_t o_tenc = o_vec + 5u * kH * 4u;   // w | b, 32 TKS each, zero-padded
-    static constexpr uint32_t bytes = o_tenc + 2u * 32u * TKS * 4u;
+    // Per wavefront: the time encodings of a block's 16 rows, bf16 hi | lo
+    // (32 TKS each) plus 8 elements of padding per row, and the list of the
+    // block's valid rows (row, dt).
+    static constexpr uint32_t ts = 64u * TKS + 8u;
+    static constexpr uint32_t o_t = o_tenc + 2u * 32u * TKS * 4u;
+    static constexpr uint32_t o_rl = o_t + (kRowThreads / 64) * 16u * ts * 2u;
+    static constexpr uint32_t bytes = o_rl + (kRowThreads / 64) * 16u * 8u;
 };
 
 // One lane's eight consecutive elements c..c+7 of a gathered row, in one of
@@ -579,6 +607,10 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
         tw[u] = u < p.d_time ? p.w[u] : 0.0f;
         tb[u] = u < p.d_time ? p.b[u] : 0.0f;
     }
+    // The time-encoding tiles start as zeros: rows and columns a block does
+    // not write keep finite values.
+    for (uint32_t u = tid; u < (L::o_rl - L::o_t) / 16u; u += kRowThreads)
+        *(u32x4 *)(smem + L::o_t + 16u * u) = u32x4(0u);
     __syncthreads();
     // max |w| and max |b| of the time encoding, for the per-unit test that
     // every argument w dt + b is inside the fast cosine's range.
@@ -599,6 +631,8 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
     // below lives in scalar registers and its branches are scalar.
     const uint32_t lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint32_t r16 = lane & 15, g = lane >> 4;
+    __bf16 *Tt = (__bf16 *)(smem + L::o_t) + (size_t)wave * 16u * L::ts;
+    u32x2 *rl = (u32x2 *)(smem + L::o_rl) + wave * 16u;
     const float *b1 = vec, *b2 = vec + kH, *b3 = vec + 2 * kH, *b4 = vec + 3 * kH, *va = vec + 4 * kH;
     const uint32_t gq = p.gq;
     const uint64_t groups = ((uint64_t)p.nq + gq - 1) / gq;
@@ -752,37 +786,80 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
             piece_operand<EK>(rows_c.e[ks], p.e_dim, 32u * ks + 8u * g, ev, hi, lo);
             mfma4(acc, W1, L::ls1, 32u * (NKS + ks), r16, g, hi, lo, EK == kF32Vec);
         }
-        // Time encoding of every row, unmasked: an invalid row has dt = 0
-        // and its result is never used, padding columns have zero weight.
+        // Time encodings.  A block with few valid rows computes only those:
+        // its (valid row, 4-column chunk) items are spread over the 64 lanes,
+        // their bf16 hi / lo pairs go to the wavefront's LDS tile, and the
+        // tile's rows are read back as matrix-core operands (rows the block
+        // does not write hold earlier finite values and are excluded by the
+        // softmax).  A block with many valid rows, or with an argument
+        // outside the fast cosine's range, computes every row in registers
+        // (an invalid row has dt = 0).  Columns past d_time have zero weight.
         // The fast cosine serves the whole block when max |w| max dt + max |b|
         // (with margin for the rounding of the bound) is inside its range.
-        const float dtmax = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(xor16_max(sl.dt))));
-        if (wmax * dtmax + bmax < 0.5f * kCosFastLimit) {
-#pragma unroll 1
-            for (int ks = 0; ks < TKS; ks++) {
-                const uint32_t k = 32u * ks + 8u * g;
-                const f32x4 w0 = *(const f32x4 *)(tw + k), w1 = *(const f32x4 *)(tw + k + 4);
-                const f32x4 c0 = *(const f32x4 *)(tb + k), c1 = *(const f32x4 *)(tb + k + 4);
-                float t[8];
+        {
+            const uint32_t vm = (uint32_t)__builtin_amdgcn_ballot_w64(valid) & 0xFFFFu;
+            const uint32_t nv = (uint32_t)__builtin_popcount(vm);
+            const float dtmax =
+                __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(xor16_max(sl.dt))));
+            const bool fast = wmax * dtmax + bmax < 0.5f * kCosFastLimit;
+            if (fast && nv < kDenseRows) {
+                if (g == 0 && valid) rl[__builtin_popcount(vm & ((1u << r16) - 1u))] = u32x2{r16, __float_as_uint(sl.dt)};
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+                const uint32_t items = nv * p.nch;
+                for (uint32_t base = 0; base < items; base += 64) {
+                    const uint32_t it = base + lane;
+                    if (it < items) {
+                        const uint32_t j = (uint32_t)(((uint64_t)it * p.nch_m) >> 32), c = it - j * p.nch;
+                        const u32x2 e = rl[j];
+                        const float dt = __uint_as_float(e[1]);
+                        const f32x4 wv = *(const f32x4 *)(tw + 4u * c), bv = *(const f32x4 *)(tb + 4u * c);
+                        float t[4];
 #pragma unroll
-                for (int i = 0; i < 4; i++) {
-                    t[i] = cos_fp32_small(__builtin_fmaf(w0[i], sl.dt, c0[i]));
-                    t[4 + i] = cos_fp32_small(__builtin_fmaf(w1[i], sl.dt, c1[i]));
+                        for (int i = 0; i < 4; i++) t[i] = cos_fp32_small(__builtin_fmaf(wv[i], dt, bv[i]));
+                        u32x2 hw, lw;
+                        split4(t, hw, lw);
+                        *(u32x2 *)(Tt + e[0] * L::ts + 4u * c) = hw;
+                        *(u32x2 *)(Tt + e[0] * L::ts + 32u * TKS + 4u * c) = lw;
+                    }
                 }
-                bf16x8 hi, lo;
-                split8(t, hi, lo);
-                mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
-            }
-        } else {
-#pragma unroll 1
-            for (int ks = 0; ks < TKS; ks++) {
-                const uint32_t k = 32u * ks + 8u * g;
-                float t[8];
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
-                for (int i = 0; i < 8; i++) t[i] = cos_fp32(__builtin_fmaf(tw[k + i], sl.dt, tb[k + i]));
-                bf16x8 hi, lo;
-                split8(t, hi, lo);
-                mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
+                for (int ks = 0; ks < TKS; ks++) {
+                    const bf16x8 hi = *(const bf16x8 *)(Tt + r16 * L::ts + 32u * ks + 8u * g);
+                    const bf16x8 lo = *(const bf16x8 *)(Tt + r16 * L::ts + 32u * TKS + 32u * ks + 8u * g);
+                    mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
+                }
+            } else if (fast) {
+#pragma unroll 1
+                for (int ks = 0; ks < TKS; ks++) {
+                    const uint32_t k = 32u * ks + 8u * g;
+                    const f32x4 w0 = *(const f32x4 *)(tw + k), w1 = *(const f32x4 *)(tw + k + 4);
+                    const f32x4 c0 = *(const f32x4 *)(tb + k), c1 = *(const f32x4 *)(tb + k + 4);
+                    float t[8];
+#pragma unroll
+                    for (int i = 0; i < 4; i++) {
+                        t[i] = cos_fp32_small(__builtin_fmaf(w0[i], sl.dt, c0[i]));
+                        t[4 + i] = cos_fp32_small(__builtin_fmaf(w1[i], sl.dt, c1[i]));
+                    }
+                    bf16x8 hi, lo;
+                    split8(t, hi, lo);
+                    mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
+                }
+            } else {
+#pragma unroll 1
+                for (int ks = 0; ks < TKS; ks++) {
+                    const uint32_t k = 32u * ks + 8u * g;
+                    float t[8];
+#pragma unroll
+                    for (int i = 0; i < 8; i++) t[i] = cos_fp32(__builtin_fmaf(tw[k + i], sl.dt, tb[k + i]));
+                    bf16x8 hi, lo;
+                    split8(t, hi, lo);
+                    mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
+                }
             }
         }
 #pragma unroll
@@ -994,6 +1071,8 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
         r.nq = nq;
         r.nbq = (h->s + 15u) / 16u;
         r.d_time = p.d_time;
+        r.nch = (p.d_time + 3u) / 4u;
+        r.nch_m = r.nch ? ((1ull << 32) + r.nch - 1) / r.nch : 0u;
         r.w = p.w;
         r.b = p.b;
         r.efeat = p.efeat;
