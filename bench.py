@@ -105,12 +105,15 @@ PEAK_BF16_TFLOPS = 2500.0
 
 
 def aggregate_flops(w, valid_slots, queries, hidden=64):
-    """Algorithmic matrix FLOPs of eq. (4) (no padding, one product per
-    weight): MLP_in's two layers for every valid slot, MLP_out's two layers
-    for every query, and the attention logits."""
+    """Algorithmic matrix FLOPs of eq. (4) as computed (no padding, one
+    product per weight): MLP_in's first layer and the attention logit for
+    every valid slot; MLP_in's second layer, which is affine, once on each
+    query's softmax-weighted sum, and MLP_out's two layers, for every query.
+    (Applying the second layer to every slot, in the order the equation is
+    written, would add 2 H^2 per valid slot.)"""
     d_in = w.node_dim + w.edge_dim + w.d_time
-    per_slot = 2 * (d_in * hidden + hidden * hidden + hidden)
-    per_query = 2 * ((w.node_dim + hidden) * hidden + hidden * hidden)
+    per_slot = 2 * (d_in * hidden + hidden)
+    per_query = 2 * (hidden * hidden + (w.node_dim + hidden) * hidden + hidden * hidden)
     return valid_slots * per_slot + queries * per_query
 
 
@@ -374,7 +377,7 @@ def main():
         t_s = sample_ms.sum() * 1e-3
         res["roofline"] = {"bound": "mfma", "achieved": fl / t_s / 1e12, "peak": PEAK_BF16_TFLOPS,
                            "unit": "TFLOP/s", "frac": fl / t_s / 1e12 / PEAK_BF16_TFLOPS,
-                           "traffic": None, "kernel": "aggregate_fused",
+                           "traffic": None, "kernel": "nlb_aggregate: aggregate_rows",
                            "flops_per_launch": fl / K, "hbm_gbps_algorithmic": ab / t_s / 1e9}
         res["aggregate_ms_avg"] = res.pop("sample_ms_avg")
         res["aggregate_kernel_queries_per_s"] = res.pop("sample_kernel_queries_per_s")
