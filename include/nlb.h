@@ -191,7 +191,10 @@ int nlb_sample_hop2(nlb_table *h, const int32_t *hop1_nbr, const uint32_t *tq, u
  * relative error 2^-18), accumulating in fp32 over at most ~400 terms
  * (relative error ~2.5e-5 of the sum of magnitudes); through four layers and
  * the softmax, Z is within 2e-4 * (|Z| + the root mean square of Z over the
- * launch) of the same function evaluated in double (measured: <= 3.3e-5).
+ * launch) of the same function evaluated in double (measured: <= 3.9e-5).
+ * MLP_in's second layer is affine, so the library may apply it once to the
+ * softmax-weighted sum of the first layer's outputs instead of to every
+ * slot (the logits then use W_b^T w); only the rounding order differs.
  * z is device fp32 [nq][H].  Tables with s > 64 are not supported
  * (NLB_EINVAL).  nq == 0 is a no-op.  Errors: as nlb_sample, and NLB_EINVAL
  * for a bad weight set. */
