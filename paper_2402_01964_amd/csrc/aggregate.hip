@@ -23,6 +23,7 @@
 #include <cstring>
 
 #include "nlb_internal.h"
+#include "nlb_pieces.h"
 
 namespace {
 
@@ -487,59 +488,18 @@ struct RowsLayout {
     static constexpr uint32_t bytes = o_rl + (kRowThreads / 64) * 16u * 8u;
 };
 
-// One lane's eight consecutive elements c..c+7 of a gathered row, in one of
-// three forms fixed per row matrix:
-//   kBf16Vec  bf16 rows, size and base 16-byte aligned: one 16-byte load;
-//   kBf16Word bf16 rows, size and base 4-byte aligned: four 4-byte loads;
-//   kF32Vec   fp32 rows, size and base 16-byte aligned: two 16-byte loads.
-// Each load then lies wholly inside or wholly past the row (the width is a
-// multiple of 8, 2 or 4 elements respectively); a load past it reads the
-// row's start instead (in bounds) and is zeroed when used.  Loading and use
-// are separate steps so that a caller can put all of a block's loads in
-// flight before it waits for the first.
-constexpr int kBf16Vec = 0, kBf16Word = 1, kF32Vec = 2;
-
-template <int KIND>
-struct Piece8 {
-    u32x4 w[KIND == kF32Vec ? 2 : 1];
-};
-
-template <int KIND>
-__device__ __forceinline__ void load_piece(const uint8_t *row, uint32_t dim, uint32_t c, Piece8<KIND> &r) {
-    if constexpr (KIND == kBf16Vec) {
-        r.w[0] = *(const u32x4 *)(row + (c + 8u <= dim ? 2u * c : 0u));
-    } else if constexpr (KIND == kBf16Word) {
-#pragma unroll
-        for (int j = 0; j < 4; j++) r.w[0][j] = *(const uint32_t *)(row + (c + 2u * j + 2u <= dim ? 2u * (c + 2u * j) : 0u));
-    } else {
-        r.w[0] = *(const u32x4 *)(row + (c + 4u <= dim ? 4u * c : 0u));
-        r.w[1] = *(const u32x4 *)(row + (c + 8u <= dim ? 4u * c + 16u : 0u));
-    }
-}
-
-// The piece as a matrix-core B operand, hi + lo (lo is not formed for bf16
+// A piece as a matrix-core B operand, hi + lo (lo is not formed for bf16
 // rows, whose values are exact in bf16), zero where `ok` is false or past
 // the row.
 template <int KIND>
 __device__ __forceinline__ void piece_operand(const Piece8<KIND> &r, uint32_t dim, uint32_t c, bool ok,
                                               bf16x8 &hi, bf16x8 &lo) {
     if constexpr (KIND != kF32Vec) {
-        u32x4 w;
-#pragma unroll
-        for (int j = 0; j < 4; j++) {
-            const bool in = ok && (KIND == kBf16Vec ? c + 8u <= dim : c + 2u * j + 2u <= dim);
-            w[j] = in ? r.w[0][j] : 0u;
-        }
-        hi = __builtin_bit_cast(bf16x8, w);
+        hi = __builtin_bit_cast(bf16x8, piece_bf16_bits<KIND>(r, dim, c, ok));
         lo = hi;
     } else {
-        const bool in0 = ok && c + 4u <= dim, in1 = ok && c + 8u <= dim;
         float v[8];
-#pragma unroll
-        for (int i = 0; i < 4; i++) {
-            v[i] = in0 ? __uint_as_float(r.w[0][i]) : 0.0f;
-            v[4 + i] = in1 ? __uint_as_float(r.w[1][i]) : 0.0f;
-        }
+        piece_floats<KIND>(r, dim, c, ok, v);
         split8(v, hi, lo);
     }
 }
@@ -1051,12 +1011,6 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
     // for (those of the synthetic workloads) when its weights fit one
     // workgroup's LDS; other shapes take the tiled kernel.
     const uint32_t nks = p.off_e / 32, eks = (p.off_t - p.off_e) / 32, tks = (p.k1 - p.off_t) / 32;
-    auto piece_kind = [](uint32_t row_bytes, const void *base, bool bf16) -> int {
-        const uintptr_t a = (uintptr_t)base;
-        if (row_bytes % 16 == 0 && a % 16 == 0) return bf16 ? kBf16Vec : kF32Vec;
-        if (bf16 && row_bytes % 4 == 0 && a % 4 == 0) return kBf16Word;
-        return -1;
-    };
     const int nkind = nks ? piece_kind(p.nrb, p.nfeat, p.n_bf16) : 0;
     const int ekind = eks ? piece_kind(p.erb, p.efeat, p.e_bf16) : 0;
     if (nq >= kRowsMinQueries && nkind >= 0 && ekind >= 0) {

@@ -46,11 +46,12 @@
 #include <cstring>
 
 #include "nlb_internal.h"
+#include "nlb_pieces.h"
 
 namespace {
 
 constexpr int kRnnThreads = 256;
-constexpr uint32_t kGruMeta = 1024;               // LDS bytes of the tile's row list
+constexpr uint32_t kGruMetaRows = 1024;           // LDS bytes of the tile's row list (4 words per row)
 constexpr uint32_t kGruLdsBudget = 80 * 1024;     // two workgroups per CU
 constexpr uint32_t kGruLdsMax = 160 * 1024;       // gfx950: LDS of one workgroup at most
 constexpr uint32_t kGruTargetTiles = 1024;      // tiles wanted per launch (counted on 2n rows)
@@ -191,6 +192,9 @@ struct GruParams {
     uint32_t rows;                      // listed rows per tile (16, 32 or 64)
     uint32_t off_xl, off_h, off_hl;     // LDS byte offsets
     uint64_t gx_m, gh_m;                // ceil(2^40 / (kx / 8)), ceil(2^40 / (kd / 8))
+    uint64_t gt_m, ge_m;                // ceil(2^40 / ((off_e - kd) / 8)), ceil(2^40 / ((kx - off_e) / 8))
+    int32_t s_kind, e_kind;             // piece forms of status / link rows (-1: none applies)
+    uint32_t meta;                      // LDS bytes before X: row list, then T-enc w | b (pad32(d_time) each)
     const __bf16 *w_ih, *w_hh;
     const float *b_ih, *b_hh;
 };
@@ -289,6 +293,32 @@ __device__ __forceinline__ void gate_seg(f32x4 (&acc)[4][NB], const __bf16 *Ah, 
     if (k0 + 32 < ke) step(r1, k0 + 32);
 }
 
+// One input segment of a tile: `units` pieces of 8 columns, piece u of tile
+// row j = u / g at column c0 = 8 (u - j g), from the row row_of(j) (a valid
+// address for every j < R); store(j, c0, piece) writes it to LDS.  F pieces
+// per thread are loaded before any is stored.
+template <int KIND, int F, typename RowOf, typename Store>
+__device__ __forceinline__ void fill_seg(uint32_t units, uint32_t g, uint64_t g_m, uint32_t dim, RowOf row_of,
+                                         Store store) {
+    for (uint32_t base = threadIdx.x; base < units; base += kRnnThreads * F) {
+        Piece8<KIND> pc[F];
+#pragma unroll
+        for (int f = 0; f < F; f++) {
+            const uint32_t u = min(base + f * kRnnThreads, units - 1u);
+            const uint32_t j = div_small(u, g_m), c0 = (u - j * g) * 8u;
+            load_piece<KIND>(row_of(j), dim, c0, pc[f]);
+        }
+#pragma unroll
+        for (int f = 0; f < F; f++) {
+            const uint32_t u = base + f * kRnnThreads;
+            if (u < units) {
+                const uint32_t j = div_small(u, g_m), c0 = (u - j * g) * 8u;
+                store(j, c0, pc[f]);
+            }
+        }
+    }
+}
+
 template <int NB>
 __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
     constexpr uint32_t R = 16 * NB;
@@ -299,7 +329,9 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
     uint32_t *m_row = (uint32_t *)smem;          // pair row of tile row j
     int32_t *m_self = (int32_t *)(m_row + 64);
     int32_t *m_other = m_self + 64;
-    __bf16 *Xh = (__bf16 *)(smem + kGruMeta);
+    float *m_t = (float *)(m_other + 64);        // its link's time, as fp32
+    float *s_tw = (float *)(smem + kGruMetaRows), *s_tb = s_tw + ((p.d_time + 31u) & ~31u);
+    __bf16 *Xh = (__bf16 *)(smem + p.meta);
     __bf16 *Xl = (__bf16 *)(smem + p.off_xl);
     __bf16 *Hh = (__bf16 *)(smem + p.off_h);
     __bf16 *Hl = (__bf16 *)(smem + p.off_hl);
@@ -315,8 +347,107 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
         m_row[tid] = e[0];
         m_self[tid] = (int32_t)e[1];
         m_other[tid] = (int32_t)e[2];
+        m_t[tid] = (float)p.t[e[0] >> 1];
+    }
+    for (uint32_t u = tid; u < ((p.d_time + 31u) & ~31u); u += kRnnThreads) {
+        s_tw[u] = u < p.d_time ? p.tw[u] : 0.0f;
+        s_tb[u] = u < p.d_time ? p.tb[u] : 0.0f;
     }
     __syncthreads();
+
+    if (p.s_kind >= 0 && (p.e_kind >= 0 || p.kx == p.off_e)) {
+        // Inputs segment by segment, each with its rows' fixed piece form:
+        // statuses (H = r_self, then X's r_other), the time encoding, link
+        // rows.  Rows m .. R-1 of the tile read row 0 of the list and are
+        // stored as zeros.
+        const uint32_t d = p.d, gh = p.kd / 8, us = R * gh;
+        auto status_fill = [&](auto kind) {
+            constexpr int K = decltype(kind)::value;
+            // Pieces u < us: H rows (self); us <= u < 2 us: X rows (other),
+            // by tile row j = u / gh over 2R rows.
+            fill_seg<K, 8>(
+                2u * us, gh, p.gh_m, d,
+                [&](uint32_t jj) {
+                    const uint32_t j = jj < R ? jj : jj - R;
+                    const int32_t node = (jj < R ? m_self : m_other)[j < m ? j : 0];
+                    return p.st + (size_t)node * p.srb;
+                },
+                [&](uint32_t jj, uint32_t c0, const Piece8<K> &pc) {
+                    const uint32_t j = jj < R ? jj : jj - R;
+                    const bool ok = j < m;
+                    if constexpr (K == kF32Vec) {
+                        float v[8];
+                        piece_floats<K>(pc, d, c0, ok, v);
+                        if (jj < R)
+                            store_split8(v, Hh + (size_t)j * p.hs + c0, Hl + (size_t)j * p.hs + c0);
+                        else
+                            store_split8(v, Xh + (size_t)j * p.xs + c0,
+                                         Xl + (size_t)j * p.ls + (c0 - p.lo_begin));
+                    } else {
+                        const u32x4 w = piece_bf16_bits<K>(pc, d, c0, ok);
+                        *(u32x4 *)(jj < R ? Hh + (size_t)j * p.hs + c0 : Xh + (size_t)j * p.xs + c0) = w;
+                    }
+                });
+        };
+        if (p.s_kind == kF32Vec)
+            status_fill(std::integral_constant<int, kF32Vec>{});
+        else if (p.s_kind == kBf16Word)
+            status_fill(std::integral_constant<int, kBf16Word>{});
+        else
+            status_fill(std::integral_constant<int, kBf16Vec>{});
+
+        // Time encoding cos(w_k t + b_k) of each row's link time.
+        const uint32_t gt = (p.off_e - p.kd) / 8;
+        for (uint32_t u = tid; u < R * gt; u += kRnnThreads) {
+            const uint32_t j = div_small(u, p.gt_m), k = (u - j * gt) * 8u;
+            const float tf = m_t[j < m ? j : 0];
+            const f32x4 w0 = *(const f32x4 *)(s_tw + k), w1 = *(const f32x4 *)(s_tw + k + 4);
+            const f32x4 b0 = *(const f32x4 *)(s_tb + k), b1 = *(const f32x4 *)(s_tb + k + 4);
+            float v[8];
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                v[i] = cos_fp32(__builtin_fmaf(w0[i], tf, b0[i]));
+                v[4 + i] = cos_fp32(__builtin_fmaf(w1[i], tf, b1[i]));
+            }
+#pragma unroll
+            for (int i = 0; i < 8; i++) v[i] = (j < m && k + i < p.d_time) ? v[i] : 0.0f;
+            store_split8(v, Xh + (size_t)j * p.xs + p.kd + k, Xl + (size_t)j * p.ls + (p.kd + k - p.lo_begin));
+        }
+
+        // Link rows (rows at or past edge_rows are zeros).
+        if (p.kx > p.off_e) {
+            const uint32_t ge = (p.kx - p.off_e) / 8;
+            auto edge_fill = [&](auto kind) {
+                constexpr int K = decltype(kind)::value;
+                auto eid_of = [&](uint32_t j) { return p.first_eid + (m_row[j < m ? j : 0] >> 1); };
+                fill_seg<K, 8>(
+                    R * ge, ge, p.ge_m, p.e_dim,
+                    [&](uint32_t j) {
+                        const uint64_t e = eid_of(j);
+                        return p.efeat + (size_t)(e < (uint64_t)p.edge_rows ? e : 0u) * p.erb;
+                    },
+                    [&](uint32_t j, uint32_t c0, const Piece8<K> &pc) {
+                        const bool ok = j < m && eid_of(j) < (uint64_t)p.edge_rows;
+                        if constexpr (K == kF32Vec) {
+                            float v[8];
+                            piece_floats<K>(pc, p.e_dim, c0, ok, v);
+                            store_split8(v, Xh + (size_t)j * p.xs + p.off_e + c0,
+                                         Xl + (size_t)j * p.ls + (p.off_e + c0 - p.lo_begin));
+                        } else {
+                            *(u32x4 *)(Xh + (size_t)j * p.xs + p.off_e + c0) =
+                                piece_bf16_bits<K>(pc, p.e_dim, c0, ok);
+                        }
+                    });
+            };
+            if (p.e_kind == kF32Vec)
+                edge_fill(std::integral_constant<int, kF32Vec>{});
+            else if (p.e_kind == kBf16Word)
+                edge_fill(std::integral_constant<int, kBf16Word>{});
+            else
+                edge_fill(std::integral_constant<int, kBf16Vec>{});
+        }
+        __syncthreads();
+    } else {
 
     // Inputs: X = [r_other | T-enc(t) | e] and H = r_self; rows m .. R-1
     // are zero.  Units of 8 columns: X's R * kx / 8 first, then H's; the
@@ -396,6 +527,7 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
         }
     }
     __syncthreads();
+    }
 
     const uint32_t d = p.d;
     const uint32_t units = (d + 15) / 16;
@@ -492,7 +624,7 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_clear(unsigned long long *a, 
 // LDS layout of a tile of `rows` pair rows; returns its size in bytes.
 uint32_t gru_layout(GruParams &p, uint32_t rows) {
     p.rows = rows;
-    p.off_xl = align16(kGruMeta + rows * p.xs * 2u);
+    p.off_xl = align16(p.meta + rows * p.xs * 2u);
     p.off_h = align16(p.off_xl + (p.lo_end > p.lo_begin ? rows * p.ls * 2u : 0u));
     p.off_hl = align16(p.off_h + rows * p.hs * 2u);
     return p.off_hl + (p.h_lo ? rows * p.hs * 2u : 0u);
@@ -598,6 +730,11 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     p.hs = p.kd + 8;
     p.gx_m = ceil_2_40_div(p.kx / 8);
     p.gh_m = ceil_2_40_div(p.kd / 8);
+    p.gt_m = p.off_e > p.kd ? ceil_2_40_div((p.off_e - p.kd) / 8) : 0;
+    p.ge_m = p.kx > p.off_e ? ceil_2_40_div((p.kx - p.off_e) / 8) : 0;
+    p.s_kind = piece_kind(p.srb, status, p.s_bf16);
+    p.e_kind = h->efeat ? piece_kind(h->erb, h->efeat, p.e_bf16) : -1;
+    p.meta = align16(kGruMetaRows + 8u * pad32(p.d_time));
     p.w_ih = (const __bf16 *)wts->w_ih;
     p.w_hh = (const __bf16 *)wts->w_hh;
     p.b_ih = wts->b_ih;
