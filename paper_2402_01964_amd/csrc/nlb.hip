@@ -350,32 +350,43 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
 }
 
 // Time encoding of a large first-hop launch as its own stream, after
-// sample_gather has written the timestamp output: one float4 of output per
-// thread in short workgroups.  A tile-looping kernel's write streams reach
-// about 5 TB/s on gfx950; this shape writes at the fill rate (~6.9 TB/s).
-// Slot row j = f / units belongs to query j / s; ts[j] = 0xFFFFFFFF marks an
-// invalid slot (zeros).  Divisions by multiply-high with M = 2^64 / d + 1,
-// exact for 32-bit numerators.
-__global__ __launch_bounds__(256) void tenc_stream(const uint32_t *ts, const uint32_t *tq, uint64_t s_M,
-                                                   uint32_t units, uint64_t u_M, uint32_t total,
-                                                   const float *w, const float *b, float *out) {
-    const uint32_t f = blockIdx.x * 256u + threadIdx.x;
-    if (f >= total) return;
-    const uint32_t j = (uint32_t)__umul64hi(u_M, f);
-    const uint32_t c = f - j * units;
-    const uint32_t t = ts[j];
-    f32x4 r = f32x4(0.0f);
-    if (t != 0xFFFFFFFFu) {
-        const uint32_t i = (uint32_t)__umul64hi(s_M, j);
-        const float dt = (float)(tq[i] - t);
-        const f32x4 w4 = *(const f32x4 *)(w + 4 * c);
-        const f32x4 b4 = *(const f32x4 *)(b + 4 * c);
-        r.x = cos_fp32(__builtin_fmaf(w4.x, dt, b4.x));
-        r.y = cos_fp32(__builtin_fmaf(w4.y, dt, b4.y));
-        r.z = cos_fp32(__builtin_fmaf(w4.z, dt, b4.z));
-        r.w = cos_fp32(__builtin_fmaf(w4.w, dt, b4.w));
+// sample_gather has written the timestamp output.  A tile-looping kernel's
+// write streams reach about 5 TB/s on gfx950, short workgroups with one
+// 16-byte store per thread the fill rate (~6.9 TB/s); here each thread of a
+// 128-thread workgroup computes two float4 outputs (kTencPerThread) whose
+// timestamp and query-time reads are issued together, so one read latency
+// covers two stores.  Slot row j = f / units belongs to query j / s;
+// ts[j] = 0xFFFFFFFF marks an invalid slot (zeros).  Divisions by
+// multiply-high with M = 2^64 / d + 1, exact for 32-bit numerators.
+constexpr uint32_t kTencThreads = 128, kTencPerThread = 2;
+
+__global__ __launch_bounds__(kTencThreads) void tenc_stream(const uint32_t *ts, const uint32_t *tq, uint64_t s_M,
+                                                            uint32_t units, uint64_t u_M, uint32_t total,
+                                                            const float *w, const float *b, float *out) {
+    uint32_t t[kTencPerThread], q[kTencPerThread], cc[kTencPerThread], ff[kTencPerThread];
+#pragma unroll
+    for (uint32_t k = 0; k < kTencPerThread; k++) {
+        ff[k] = (blockIdx.x * kTencPerThread + k) * kTencThreads + threadIdx.x;
+        const uint32_t f = min(ff[k], total - 1u);   // past the end: re-read the last (unused)
+        const uint32_t j = (uint32_t)__umul64hi(u_M, f);
+        cc[k] = f - j * units;
+        t[k] = ts[j];
+        q[k] = tq[(uint32_t)__umul64hi(s_M, j)];
     }
-    __builtin_nontemporal_store(r, (f32x4 *)(out + (size_t)f * 4));
+#pragma unroll
+    for (uint32_t k = 0; k < kTencPerThread; k++) {
+        f32x4 r = f32x4(0.0f);
+        if (t[k] != 0xFFFFFFFFu) {
+            const float dt = (float)(q[k] - t[k]);
+            const f32x4 w4 = *(const f32x4 *)(w + 4 * cc[k]);
+            const f32x4 b4 = *(const f32x4 *)(b + 4 * cc[k]);
+            r.x = cos_fp32(__builtin_fmaf(w4.x, dt, b4.x));
+            r.y = cos_fp32(__builtin_fmaf(w4.y, dt, b4.y));
+            r.z = cos_fp32(__builtin_fmaf(w4.z, dt, b4.z));
+            r.w = cos_fp32(__builtin_fmaf(w4.w, dt, b4.w));
+        }
+        if (ff[k] < total) __builtin_nontemporal_store(r, (f32x4 *)(out + (size_t)ff[k] * 4));
+    }
 }
 
 // ---------------------------------------------------------------- export
@@ -649,7 +660,10 @@ static int launch_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, 
         hipLaunchKernelGGL(sample_gather<false>, grid, dim3(kTileThreads), 0, st, p);
     if (split) {
         const uint64_t sM = ~0ull / h->s + 1, uM = ~0ull / p.tenc_units + 1;
-        hipLaunchKernelGGL(tenc_stream, dim3((unsigned)((tenc_total + 255) / 256)), dim3(256), 0, st,
+        hipLaunchKernelGGL(tenc_stream,
+                           dim3((unsigned)((tenc_total + kTencThreads * kTencPerThread - 1) /
+                                           (kTencThreads * kTencPerThread))),
+                           dim3(kTencThreads), 0, st,
                            (const uint32_t *)out->ts, tq, sM, p.tenc_units, uM, (uint32_t)tenc_total, h->w,
                            h->b, out->tenc);
     }
