@@ -291,32 +291,47 @@ def main():
     torch.cuda.synchronize()
 
     print(f"bench: warm-up done; timing {K} steps", file=sys.stderr, flush=True)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
+    # HIP events on the library's stream time each phase.  A recorded event
+    # costs the stream a few microseconds, so a step records only those it
+    # needs: its start (which also ends the previous step's last phase), the
+    # end of its retrieval, and the end of the second hop / the insertion
+    # only when a second hop / a status update follows.
+    def mk():
+        return torch.cuda.Event(enable_timing=True)
+    e_start = [mk() for _ in range(K + 1)]
+    e_sample = [mk() for _ in range(K)]
+    e_hop2 = [mk() for _ in range(K)] if hop2_out is not None else None
+    e_ins = [mk() for _ in range(K)] if status is not None else None
     qcount = []
     t0 = time.perf_counter()
     for k in range(K):
         b = start + W + k
-        ev[k][0].record()
+        e_start[k].record()
         s_, d_, t_, n = step(b, nbr_all[k])
-        ev[k][1].record()
+        e_sample[k].record()
         if hop2_out is not None:
             _, _, _, _, tq = synth.batch_views(w, nodes, ts, b)
             o2 = {kk: v[:n * w.s] for kk, v in hop2_out.items()}
             table.sample_hop2_into(nbr_all[k, :n], tq, o2)
-        ev[k][2].record()
+            e_hop2[k].record()
         table.insert(s_, d_, t_)
-        ev[k][3].record()
-        update(b, s_, d_, t_)
-        ev[k][4].record()
+        if status is not None:
+            e_ins[k].record()
+            update(b, s_, d_, t_)
         qcount.append(n)
+    e_start[K].record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     assert table.status() == nlb.NLB_OK
 
-    sample_ms = np.array([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)])
-    hop2_ms = np.array([ev[k][1].elapsed_time(ev[k][2]) for k in range(K)])
-    insert_ms = np.array([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)])
-    rnn_ms = np.array([ev[k][3].elapsed_time(ev[k][4]) for k in range(K)])
+    def span(a, b_):
+        return np.array([a[k].elapsed_time(b_[k]) for k in range(K)])
+    ins_from = e_hop2 if e_hop2 is not None else e_sample
+    ins_to = e_ins if e_ins is not None else e_start[1:]
+    sample_ms = span(e_start, e_sample)
+    hop2_ms = span(e_sample, e_hop2) if e_hop2 is not None else np.zeros(K)
+    insert_ms = span(ins_from, ins_to)
+    rnn_ms = span(e_ins, e_start[1:]) if e_ins is not None else np.zeros(K)
     links = sum(n // 3 for n in qcount)
     queries = sum(qcount)
     if agg_w is not None:

@@ -85,16 +85,15 @@ __device__ __forceinline__ bool link_ok(const InsertParams &p, int32_t u, int32_
 // Validation of link i (ranges; timestamps non-decreasing inside the batch
 // and against the last timestamp of the previous batch) and its two offers.
 // Returns false when the link is skipped.
-__device__ __forceinline__ bool link_offers(const InsertParams &p, uint32_t i, uint64_t &ou,
-                                            uint64_t &wu, uint64_t &ov, uint64_t &wv) {
-    const int32_t u = p.src[i];
-    const int32_t v = p.dst[i];
-    const uint32_t t = p.t[i];
+// link_offers_of takes the link's already-loaded u, v, t and the previous
+// link's timestamp.
+__device__ __forceinline__ bool link_offers_of(const InsertParams &p, uint32_t i, int32_t u, int32_t v,
+                                               uint32_t t, uint32_t prev_t, uint64_t &ou, uint64_t &wu,
+                                               uint64_t &ov, uint64_t &wv) {
     uint32_t flags = 0;
     if (u < 0 || v < 0 || (int64_t)u >= p.num_nodes || (int64_t)v >= p.num_nodes)
         flags |= kStatusRange;
     if (t > kTimeMask) flags |= kStatusOrder;
-    const uint32_t prev_t = (i > 0) ? p.t[i - 1] : p.status[1 + (p.parity ^ 1u)];
     if (t < prev_t) flags |= kStatusOrder;
     if (flags) atomicOr(p.status, flags);
     if (i == p.n - 1) p.status[1 + p.parity] = t;
@@ -106,6 +105,15 @@ __device__ __forceinline__ bool link_offers(const InsertParams &p, uint32_t i, u
     wu = offer_word(p, e, 0, t);
     wv = offer_word(p, e, 1, t);
     return true;
+}
+
+__device__ __forceinline__ uint32_t prev_time(const InsertParams &p, uint32_t i) {
+    return (i > 0) ? p.t[i - 1] : p.status[1 + (p.parity ^ 1u)];
+}
+
+__device__ __forceinline__ bool link_offers(const InsertParams &p, uint32_t i, uint64_t &ou,
+                                            uint64_t &wu, uint64_t &ov, uint64_t &wv) {
+    return link_offers_of(p, i, p.src[i], p.dst[i], p.t[i], prev_time(p, i), ou, wu, ov, wv);
 }
 
 __global__ __launch_bounds__(kInsertThreads) void insert_resolve(InsertParams p) {
@@ -125,12 +133,26 @@ __global__ __launch_bounds__(kInsertThreads) void insert_resolve_merged(InsertPa
         merge_word[k] = 0ull;
     }
     __syncthreads();
+    // All of a thread's links are loaded (a link past the batch re-reads
+    // the last one, unused) before any is merged.
+    constexpr int RR = kResolveLinks / kInsertThreads;
     const uint32_t first = blockIdx.x * kResolveLinks;
-    for (uint32_t r = 0; r < kResolveLinks; r += kInsertThreads) {
-        const uint32_t i = first + r + threadIdx.x;
+    int32_t uu[RR], vv[RR];
+    uint32_t tt[RR], pt[RR];
+#pragma unroll
+    for (int r = 0; r < RR; r++) {
+        const uint32_t i = min(first + r * kInsertThreads + threadIdx.x, p.n - 1u);
+        uu[r] = p.src[i];
+        vv[r] = p.dst[i];
+        tt[r] = p.t[i];
+        pt[r] = prev_time(p, i);
+    }
+#pragma unroll
+    for (int r = 0; r < RR; r++) {
+        const uint32_t i = first + r * kInsertThreads + threadIdx.x;
         if (i >= p.n) break;
         uint64_t ou, wu, ov, wv;
-        if (link_offers(p, i, ou, wu, ov, wv)) {
+        if (link_offers_of(p, i, uu[r], vv[r], tt[r], pt[r], ou, wu, ov, wv)) {
             merge_max(merge_off, merge_word, ou, wu);
             merge_max(merge_off, merge_word, ov, wv);
         }
