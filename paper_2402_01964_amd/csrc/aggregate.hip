@@ -335,6 +335,7 @@ constexpr int kRowThreads = 512;    // 8 wavefronts per workgroup
 constexpr uint32_t kMaxGroupQ = 16;  // queries per MLP_out block at most
 constexpr int kRuSteps = 4;         // k-steps of r_u held in registers: node rows up to 128 wide
 constexpr uint32_t kRowsMinQueries = 1;
+constexpr float kLog2eAgg = 1.44269504088896340736f;
 // Blocks with at least this many valid rows compute the time encoding of
 // every row in registers; sparser blocks compute their valid rows only.
 constexpr uint32_t kDenseRows = 12;
@@ -733,7 +734,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
         // Layer 1: a1 = ReLU(W1 x + b1).
         f32x4 acc[4];
 #pragma unroll
-        for (int ub = 0; ub < 4; ub++) acc[ub] = f32x4(0.0f);
+        for (int ub = 0; ub < 4; ub++) acc[ub] = *(const f32x4 *)(b1 + 16 * ub + 4 * g);   // + b1
 #pragma unroll
         for (int ks = 0; ks < NKS; ks++) {
             bf16x8 hi, lo;
@@ -825,7 +826,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
 #pragma unroll
         for (int ub = 0; ub < 4; ub++)
 #pragma unroll
-            for (int i = 0; i < 4; i++) acc[ub][i] = fmaxf(acc[ub][i] + b1[16 * ub + 4 * g + i], 0.0f);
+            for (int i = 0; i < 4; i++) acc[ub][i] = fmaxf(acc[ub][i], 0.0f);
         // The row's logit v . a1 (up to the common shift att . b2).
         float part = 0.0f;
 #pragma unroll
@@ -840,8 +841,10 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
         const float mb = xor16_max(lg);
         if (mb != -INFINITY) {
             const float mn = fmaxf(m, mb);
-            const float sc = (m == -INFINITY) ? 0.0f : expf(m - mn);
-            const float e = valid ? expf(lg - mn) : 0.0f;
+            // exp(x) as the hardware 2^(x log2 e): x <= 0 here, and the
+            // rounding of the product adds a relative error of |x| 2^-24.
+            const float sc = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m - mn) * kLog2eAgg);
+            const float e = valid ? __builtin_amdgcn_exp2f((lg - mn) * kLog2eAgg) : 0.0f;
             den = den * sc + xor16_sum(e);
 #pragma unroll
             for (int ub = 0; ub < 4; ub++)
