@@ -111,6 +111,46 @@ def test_time_encoding_launch_paths_agree():
                        {"nbr": oo["nbr"], "ts": oo["ts"], "tenc": oo["tenc"]}, f"nq={nq}")
 
 
+def test_time_encoding_wide_arguments():
+    """Frequencies scaled by 10^4 put w dt + b far beyond 2^33 for most
+    slots, outside the fast cosine's range: both time-encoding launch paths
+    of nlb_sample stay bit-identical and match the oracle within 1e-5, and
+    the aggregation (whose per-query kernel then takes its general-cosine
+    branch) matches the oracle within its tolerance."""
+    import torch
+    import paper_2402_01964_amd as nlb
+    for k in (4, 1):
+        base = synth.workload(k)
+        w = synth.scaled(base, 20 * base.batch)
+        src, dst, t, neg = synth.host_links(w)
+        fw, fb = synth.time_params(w)
+        fw = (fw * 1.0e4).astype(np.float32)
+        ef = synth.host_features(w, "edge") if w.edge_dim else None
+        g = nlb.Table(w.num_nodes, w.s, w.alpha, w.table_seed, time_w=to_dev(fw), time_b=to_dev(fb),
+                      edge_feat=feat_to_dev(ef, w.edge_dtype) if ef is not None else None)
+        g.insert(to_dev(src), to_dev(dst), to_dev(t))
+        o = make_oracle(w)
+        o.insert(src, dst, t)
+        rng = np.random.default_rng(9 + k)
+        ends = np.concatenate([src, dst])
+        for nq in (30000, 500):
+            q = ends[rng.integers(0, len(ends), nq)].astype(np.int32)
+            tq = rng.integers(0, int(t[-1]) + 2, nq).astype(np.uint32)
+            a = g.sample(to_dev(q), to_dev(tq), want=("nbr", "eid", "ts", "tenc"))
+            b = g.sample(to_dev(q), to_dev(tq), want=("tenc",))
+            assert torch.equal(a["tenc"], b["tenc"]), (k, nq)
+            oo = o.sample(q[:400], tq[:400], fw, fb, None, None, want=("nbr", "ts", "tenc"))
+            compare_sample({"nbr": a["nbr"][:400], "ts": a["ts"][:400], "tenc": a["tenc"][:400]},
+                           {"nbr": oo["nbr"], "ts": oo["ts"], "tenc": oo["tenc"]}, f"wide k={k} nq={nq}")
+            W = synth.agg_weights(w)
+            gz = g.aggregate(to_dev(q), to_dev(tq), _agg_dev(W)).cpu().numpy()
+            oz = o.aggregate(q[:400], tq[:400], fw, fb, ef, None, W)
+            err = agg_error(gz[:400], oz)
+            print(f"aggregate wide arguments, workload {k}, {nq} queries: max scaled error {err:.3e}")
+            assert err <= AGG_TOL
+        assert g.status() == 0
+
+
 # ----------------------------------------------------------------------------- invariance
 def _insert_in_batches(w, src, dst, t, B, **kw):
     g = make_gpu_table(w, time=False, **kw)

@@ -137,6 +137,27 @@ def _small_table(N, d_time=12, edge=None, seed=3):
     return nlb.Table(N, 4, 0.5, 1, time_w=tw, time_b=tb, edge_feat=edge), fw, fb
 
 
+def test_rnn_wide_time_arguments():
+    """Time-encoding frequencies of 10^3 .. 10^5 and link times up to 10^7
+    put the cosine arguments far beyond 2^33, outside the fast cosine's
+    range."""
+    import paper_2402_01964_amd as nlb
+    rng = np.random.default_rng(12)
+    N, d, n, d_time = 2000, 40, 3000, 12
+    fw = (10.0 ** rng.uniform(3, 5, d_time)).astype(np.float32)
+    fb = rng.uniform(-np.pi, np.pi, d_time).astype(np.float32)
+    ef32 = rng.standard_normal((n + 10, 24)).astype(np.float32)
+    g = nlb.Table(N, 4, 0.5, 1, time_w=to_dev(fw), time_b=to_dev(fb), edge_feat=to_dev(ef32))
+    src = rng.integers(0, N, n).astype(np.int32)
+    dst = rng.integers(0, N, n).astype(np.int32)
+    t = np.sort(rng.integers(0, 10**7, n)).astype(np.uint32)
+    st = to_dev(rng.standard_normal((N, d)).astype(np.float32))
+    W = synth.gru_weights_for(d, d_time, 24, seed=6)
+    err, _ = _check_batch(g, st, ef32, W, _weights_dev(W), fw, fb, src, dst, t, 10, "wide arguments")
+    _log(f"wide time arguments: max err {err:.3e}")
+    assert g.status() == 0
+
+
 @pytest.mark.parametrize("n", [1000, 70000])
 def test_rnn_hub_repeats_and_self_loops(n):
     """50 nodes, half of all endpoints on node 0, 5% self-loops: nearly
