@@ -309,20 +309,45 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
     const size_t row0 = (size_t)q0 * s;          // first output slot row
 
     // Phase 1: table read, strict mask (eq. (1)), id outputs, LDS staging.
-    for (uint32_t j = tid; j < ns; j += kTileThreads) {
+    // A thread's slot rows (at most kTileSlots / kTileThreads) are read in
+    // two rounds of unconditional loads -- the query ids and times, then
+    // the slot words (an out-of-range node or a row past the tile reads
+    // slot 0 of node 0, which exists) -- before any is used.
+    constexpr int P1 = kTileSlots / kTileThreads;
+    int32_t nd[P1];
+    uint32_t tqv[P1];
+#pragma unroll
+    for (int r = 0; r < P1; r++) {
+        const uint32_t j = min(tid + r * kTileThreads, ns - 1u);
+        const uint32_t ql = div_small(j, p.s_m);
+        const uint64_t qg = q0 + ql;
+        nd[r] = p.node[qg];
+        tqv[r] = p.tq[HOP2 ? (uint32_t)qg / s : qg];
+    }
+    uint64_t key[P1];
+    int32_t xv[P1];
+#pragma unroll
+    for (int r = 0; r < P1; r++) {
+        const uint32_t j = min(tid + r * kTileThreads, ns - 1u);
         const uint32_t ql = div_small(j, p.s_m);
         const uint32_t a = j - ql * s;
-        const uint64_t qg = q0 + ql;
-        const int32_t node = p.node[qg];
-        const uint32_t tq = p.tq[HOP2 ? (uint32_t)qg / s : qg];
+        const bool in_range = nd[r] >= 0 && (int64_t)nd[r] < p.num_nodes;
+        const uint8_t *bp = p.blocks + (size_t)(in_range ? nd[r] : 0) * p.block_bytes;
+        const uint32_t aa = in_range ? a : 0u;
+        key[r] = ((const uint64_t *)bp)[aa];
+        xv[r] = ((const int32_t *)(bp + 8u * s))[aa];
+    }
+#pragma unroll
+    for (int r = 0; r < P1; r++) {
+        const uint32_t j = tid + r * kTileThreads;
+        if (j >= ns) break;
+        const uint32_t ql = div_small(j, p.s_m);
+        const uint32_t a = j - ql * s;
+        const int32_t node = nd[r];
         const bool in_range = node >= 0 && (int64_t)node < p.num_nodes;
         const bool quiet = HOP2 && node < 0;   // empty first-hop slot
-        SlotLds sl = {-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
-        if (in_range) {
-            sl = read_slot(p.blocks, p.block_bytes, s, node, a, tq);
-        } else if (a == 0 && !quiet) {
-            atomicOr(p.status, kStatusRange);
-        }
+        const SlotLds sl = decode_slot(in_range ? key[r] : 0ull, xv[r], tqv[r]);
+        if (!in_range && a == 0 && !quiet) atomicOr(p.status, kStatusRange);
         if (a == 0) tile_nodes[ql] = in_range ? node : -1;
         slots[j] = sl;
         if (p.o_nbr) p.o_nbr[row0 + j] = sl.x;
