@@ -93,11 +93,22 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_resolve_merged(ResolveParams 
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) *p.count = 0;
     __syncthreads();
+    // All of a thread's links are loaded (a link past the batch re-reads
+    // the last one, unused) before any is merged.
+    constexpr int RR = kResolveLinks / kRnnThreads;
     const uint32_t first = blockIdx.x * kResolveLinks;
-    for (uint32_t r = 0; r < kResolveLinks; r += kRnnThreads) {
-        const uint32_t i = first + r + threadIdx.x;
+    int32_t uu[RR], vv[RR];
+#pragma unroll
+    for (int r = 0; r < RR; r++) {
+        const uint32_t i = min(first + r * kRnnThreads + threadIdx.x, p.n - 1u);
+        uu[r] = p.src[i];
+        vv[r] = p.dst[i];
+    }
+#pragma unroll
+    for (int r = 0; r < RR; r++) {
+        const uint32_t i = first + r * kRnnThreads + threadIdx.x;
         if (i >= p.n) break;
-        const int32_t u = p.src[i], v = p.dst[i];
+        const int32_t u = uu[r], v = vv[r];
         if (!endpoints_ok(u, v, p.num_nodes)) {
             atomicOr(p.status, kStatusRange);
             continue;
@@ -135,18 +146,38 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_select(SelectParams p) {
     const uint32_t lane = threadIdx.x & 63;
     if (threadIdx.x == 0) n_local = 0;
     __syncthreads();
+    // A thread's pair rows: their links' endpoints, then the winner words
+    // of their nodes, are read in two rounds of unconditional loads (rows
+    // past the batch re-read the last link; invalid endpoints read
+    // winner[0]) before any is used.
+    constexpr int RS = kSelectRows / kRnnThreads;
     const uint64_t r0 = (uint64_t)blockIdx.x * kSelectRows;
-    for (uint32_t k = threadIdx.x; k < kSelectRows; k += kRnnThreads) {
+    int32_t su[RS], sv[RS];
+#pragma unroll
+    for (int q = 0; q < RS; q++) {
+        const uint64_t r = min(r0 + q * kRnnThreads + threadIdx.x, 2ull * p.n - 1ull);
+        su[q] = p.src[(uint32_t)(r >> 1)];
+        sv[q] = p.dst[(uint32_t)(r >> 1)];
+    }
+    unsigned long long wv[RS];
+#pragma unroll
+    for (int q = 0; q < RS; q++) {
+        const uint64_t r = min(r0 + q * kRnnThreads + threadIdx.x, 2ull * p.n - 1ull);
+        const int32_t self = (r & 1) ? sv[q] : su[q];
+        wv[q] = p.winner[endpoints_ok(su[q], sv[q], p.num_nodes) ? self : 0];
+    }
+#pragma unroll
+    for (int q = 0; q < RS; q++) {
+        const uint32_t k = q * kRnnThreads + threadIdx.x;
         const uint64_t r = r0 + k;
         bool win = false;
         int32_t self = -1, other = -1;
         if (r < 2ull * p.n) {
-            const uint32_t i = (uint32_t)(r >> 1);
-            const int32_t u = p.src[i], v = p.dst[i];
+            const int32_t u = su[q], v = sv[q];
             if (endpoints_ok(u, v, p.num_nodes)) {
                 self = (r & 1) ? v : u;
                 other = (r & 1) ? u : v;
-                win = p.winner[self] == (p.epoch_hi | (r + 1));
+                win = wv[q] == (p.epoch_hi | (r + 1));
             }
             p.cand_node[r] = win ? self : -1;
         }
