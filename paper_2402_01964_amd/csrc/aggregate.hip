@@ -3,7 +3,10 @@
 //   Z_u = MLP_out(r_u, sum_i alpha_i MLP_in(r_v, e, t')),
 //   {alpha_i} = softmax({w^T MLP_in(r_v, e, t')}) over the valid slots of S_u^t,
 // MLP(x) = W_b ReLU(W_a x + b_a) + b_b.  The retrieved rows and the time
-// encoding never leave the chip: a workgroup reads its tile's table slots,
+// encoding never leave the chip.  Two kernels: aggregate_rows (below), one
+// wavefront per query at a time with every intermediate in registers, for
+// the input shapes it is instantiated for; and aggregate_fused, a tiled
+// kernel for any other shape, whose workgroup reads its tile's table slots,
 // builds the inputs in LDS and runs the four layers on bf16 matrix cores.
 //
 // Numerics.  Every activation is fp32 and enters a matrix product as a pair
@@ -322,15 +325,18 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_fused(AggParams p) {
 // the next product follow without an LDS round trip.
 //
 // Each wavefront takes one query at a time, one 16-row block of its slots
-// at a time (s <= 16: one block): layer 1, layer 2, the attention logits
-// (a reduction over the four lanes of a row) and an online softmax with the
-// weighted sum of the messages (reductions over the 16 rows of a block,
-// combined across blocks with a running maximum).  A group of 16 queries
-// then runs MLP_out as one 16-row block.  The weights of all four layers are
-// staged in LDS once per persistent workgroup; the only other LDS is each
-// wavefront's 16 aggregate vectors.  Wavefronts never wait for each other
-// after the staging, so the latency of one query's gathers is covered by
-// the other wavefronts of the CU.
+// at a time (s <= 16: one block), as a software pipeline: a block's slot
+// words are read two blocks ahead of its computation and its row gathers
+// one block ahead.  Per block: layer 1, the attention logits and an online
+// softmax that sums the softmax-weighted layer-1 outputs (reductions over
+// the 16 rows of a block, combined across blocks with a running maximum).
+// MLP_in's second layer is affine, so it is applied once per query to that
+// sum (the logits use v = W2^T att, the common shift att . b2 cancelling in
+// the softmax).  A group of up to 16 queries then runs MLP_out as one
+// 16-row block.  The weights of all four layers are staged in LDS once per
+// persistent workgroup; the other LDS is each wavefront's time-encoding tile
+// for blocks with few valid rows.  Wavefronts never wait for each other
+// after the staging.
 constexpr int kRowThreads = 512;    // 8 wavefronts per workgroup
 constexpr uint32_t kMaxGroupQ = 16;  // queries per MLP_out block at most
 constexpr int kRuSteps = 4;         // k-steps of r_u held in registers: node rows up to 128 wide
