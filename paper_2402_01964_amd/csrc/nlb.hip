@@ -125,23 +125,23 @@ __global__ __launch_bounds__(kInsertThreads) void insert_resolve(InsertParams p)
     atomicMax((unsigned long long *)(p.blocks + ov), (unsigned long long)wv);
 }
 
-__global__ __launch_bounds__(kInsertThreads) void insert_resolve_merged(InsertParams p) {
+__global__ __launch_bounds__(kMergeThreads) void insert_resolve_merged(InsertParams p) {
     __shared__ unsigned long long merge_off[kMergeEntries];
     __shared__ unsigned long long merge_word[kMergeEntries];
-    for (int k = threadIdx.x; k < kMergeEntries; k += kInsertThreads) {
+    for (int k = threadIdx.x; k < kMergeEntries; k += kMergeThreads) {
         merge_off[k] = 0ull;
         merge_word[k] = 0ull;
     }
     __syncthreads();
     // All of a thread's links are loaded (a link past the batch re-reads
     // the last one, unused) before any is merged.
-    constexpr int RR = kResolveLinks / kInsertThreads;
+    constexpr int RR = kResolveLinks / kMergeThreads;
     const uint32_t first = blockIdx.x * kResolveLinks;
     int32_t uu[RR], vv[RR];
     uint32_t tt[RR], pt[RR];
 #pragma unroll
     for (int r = 0; r < RR; r++) {
-        const uint32_t i = min(first + r * kInsertThreads + threadIdx.x, p.n - 1u);
+        const uint32_t i = min(first + r * kMergeThreads + threadIdx.x, p.n - 1u);
         uu[r] = p.src[i];
         vv[r] = p.dst[i];
         tt[r] = p.t[i];
@@ -149,7 +149,7 @@ __global__ __launch_bounds__(kInsertThreads) void insert_resolve_merged(InsertPa
     }
 #pragma unroll
     for (int r = 0; r < RR; r++) {
-        const uint32_t i = first + r * kInsertThreads + threadIdx.x;
+        const uint32_t i = first + r * kMergeThreads + threadIdx.x;
         if (i >= p.n) break;
         uint64_t ou, wu, ov, wv;
         if (link_offers_of(p, i, uu[r], vv[r], tt[r], pt[r], ou, wu, ov, wv)) {
@@ -158,7 +158,7 @@ __global__ __launch_bounds__(kInsertThreads) void insert_resolve_merged(InsertPa
         }
     }
     __syncthreads();
-    for (int k = threadIdx.x; k < kMergeEntries; k += kInsertThreads) {
+    for (int k = threadIdx.x; k < kMergeEntries; k += kMergeThreads) {
         const unsigned long long tag = merge_off[k];
         if (tag) atomicMax((unsigned long long *)(p.blocks + (tag - 1)), merge_word[k]);
     }
@@ -631,7 +631,7 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const
     const hipStream_t st = (hipStream_t)stream;
     if (n >= kMergeMinBatch)
         hipLaunchKernelGGL(insert_resolve_merged, dim3((n + kResolveLinks - 1) / kResolveLinks),
-                           dim3(kInsertThreads), 0, st, p);
+                           dim3(kMergeThreads), 0, st, p);
     else
         hipLaunchKernelGGL(insert_resolve, dim3((n + kInsertThreads - 1) / kInsertThreads),
                            dim3(kInsertThreads), 0, st, p);

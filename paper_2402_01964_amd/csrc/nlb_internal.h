@@ -121,6 +121,7 @@ __device__ __forceinline__ SlotLds read_slot(const uint8_t *blocks, uint32_t blo
 // atomicMax per distinct address can replace many.  kMergeEntries entries
 // hold up to half as many distinct addresses.
 constexpr int kResolveLinks = 1024;               // links merged per workgroup (two addresses each)
+constexpr int kMergeThreads = 1024;               // threads of a merging workgroup (one link each)
 constexpr int kMergeBits = 12;                    // 2 * kResolveLinks addresses: load <= 1/2
 constexpr int kMergeEntries = 1 << kMergeBits;
 constexpr uint32_t kMergeMinBatch = 65536;        // batches from this size merge in LDS

@@ -84,10 +84,10 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_resolve(ResolveParams p) {
     atomicMax(&p.winner[v], (unsigned long long)(p.epoch_hi | (2ull * i + 2)));
 }
 
-__global__ __launch_bounds__(kRnnThreads) void rnn_resolve_merged(ResolveParams p) {
+__global__ __launch_bounds__(kMergeThreads) void rnn_resolve_merged(ResolveParams p) {
     __shared__ unsigned long long merge_off[kMergeEntries];
     __shared__ unsigned long long merge_word[kMergeEntries];
-    for (int k = threadIdx.x; k < kMergeEntries; k += kRnnThreads) {
+    for (int k = threadIdx.x; k < kMergeEntries; k += kMergeThreads) {
         merge_off[k] = 0ull;
         merge_word[k] = 0ull;
     }
@@ -95,18 +95,18 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_resolve_merged(ResolveParams 
     __syncthreads();
     // All of a thread's links are loaded (a link past the batch re-reads
     // the last one, unused) before any is merged.
-    constexpr int RR = kResolveLinks / kRnnThreads;
+    constexpr int RR = kResolveLinks / kMergeThreads;
     const uint32_t first = blockIdx.x * kResolveLinks;
     int32_t uu[RR], vv[RR];
 #pragma unroll
     for (int r = 0; r < RR; r++) {
-        const uint32_t i = min(first + r * kRnnThreads + threadIdx.x, p.n - 1u);
+        const uint32_t i = min(first + r * kMergeThreads + threadIdx.x, p.n - 1u);
         uu[r] = p.src[i];
         vv[r] = p.dst[i];
     }
 #pragma unroll
     for (int r = 0; r < RR; r++) {
-        const uint32_t i = first + r * kRnnThreads + threadIdx.x;
+        const uint32_t i = first + r * kMergeThreads + threadIdx.x;
         if (i >= p.n) break;
         const int32_t u = uu[r], v = vv[r];
         if (!endpoints_ok(u, v, p.num_nodes)) {
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_resolve_merged(ResolveParams 
         merge_max(merge_off, merge_word, 8ull * (uint32_t)v, p.epoch_hi | (2ull * i + 2));
     }
     __syncthreads();
-    for (int k = threadIdx.x; k < kMergeEntries; k += kRnnThreads) {
+    for (int k = threadIdx.x; k < kMergeEntries; k += kMergeThreads) {
         const unsigned long long tag = merge_off[k];
         if (tag) atomicMax(&p.winner[(tag - 1) >> 3], merge_word[k]);
     }
@@ -806,7 +806,7 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     ResolveParams rp = {src, dst, n, h->num_nodes, h->rnn_winner, epoch_hi, h->status, count};
     if (n >= kMergeMinBatch)
         hipLaunchKernelGGL(rnn_resolve_merged, dim3((n + kResolveLinks - 1) / kResolveLinks),
-                           dim3(kRnnThreads), 0, (hipStream_t)stream, rp);
+                           dim3(kMergeThreads), 0, (hipStream_t)stream, rp);
     else
         hipLaunchKernelGGL(rnn_resolve, dim3((n + kRnnThreads - 1) / kRnnThreads), dim3(kRnnThreads), 0,
                            (hipStream_t)stream, rp);
