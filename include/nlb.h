@@ -123,7 +123,17 @@ typedef struct nlb_info {
     int64_t table_bytes;    /* device bytes owned by the table */
     int32_t block_bytes;    /* bytes of one node's slot block */
     int32_t device;
+    int32_t rnn_form;       /* GRU pass of the last nlb_rnn_update: NLB_RNN_FORM_* */
 } nlb_info;
+
+/* Forms of the GRU pass of nlb_rnn_update: none run yet; tiles of listed
+ * rows with the weights streamed from L2; the weight-stationary form (the
+ * weights held in registers for the whole launch, one workgroup per CU),
+ * used when the statuses have 16-byte rows, pad32(d) <= 128 and
+ * pad32(d) + pad32(d) + pad32(d_time) + pad32(edge_dim) <= 384. */
+#define NLB_RNN_FORM_NONE 0
+#define NLB_RNN_FORM_TILED 1
+#define NLB_RNN_FORM_WEIGHT_STATIONARY 2
 
 /* Create an empty table (Sec. 4.2: fixed-size GPU memory of s slots per
  * node, all empty).  Validates `cfg`, allocates and zeroes the slot blocks on

@@ -28,6 +28,7 @@ ABI_SYMBOLS = ("nlb_create", "nlb_insert_batch", "nlb_sample", "nlb_sample_hop2"
 AGG_HIDDEN = 64
 RNN_MAX_DIM = 1024
 DTYPE_F32, DTYPE_BF16 = 0, 1
+RNN_FORM_NONE, RNN_FORM_TILED, RNN_FORM_WEIGHT_STATIONARY = 0, 1, 2
 
 
 class NLBError(RuntimeError):
@@ -67,7 +68,7 @@ class _Info(ctypes.Structure):
     _fields_ = [("num_nodes", ctypes.c_int64), ("s", ctypes.c_int32), ("key_mode", ctypes.c_int32),
                 ("threshold", ctypes.c_uint64), ("q1", ctypes.c_uint64), ("q2", ctypes.c_uint64),
                 ("interactions", ctypes.c_uint64), ("table_bytes", ctypes.c_int64),
-                ("block_bytes", ctypes.c_int32), ("device", ctypes.c_int32)]
+                ("block_bytes", ctypes.c_int32), ("device", ctypes.c_int32), ("rnn_form", ctypes.c_int32)]
 
 
 _lib = None

@@ -599,6 +599,7 @@ int nlb_get_info(const nlb_table *h, nlb_info *info) {
     info->table_bytes = (int64_t)h->table_bytes;
     info->block_bytes = (int32_t)h->block_bytes;
     info->device = h->device;
+    info->rnn_form = h->rnn_form;
     return NLB_OK;
 }
 

@@ -258,6 +258,7 @@ struct nlb_table {
     // Node-status update (rnn.hip), allocated on first use.
     unsigned long long *rnn_winner;   // [N] latest pair-row code per node
     uint32_t rnn_epoch;               // calls since the winner array was cleared
+    int32_t rnn_form;                 // GRU pass of the last update (NLB_RNN_FORM_*)
     uint8_t *rnn_cand;                // candidate status rows by pair row
     size_t rnn_cand_bytes;
     int32_t *rnn_cand_node;           // winner node per pair row, else -1

@@ -43,6 +43,7 @@
 // (read from global memory, where the whole weight set stays L2-resident)
 // go through a three-slot register ring, so each k-step's loads are issued
 // two steps before their products.
+#include <algorithm>
 #include <cstring>
 
 #include "nlb_internal.h"
@@ -226,6 +227,7 @@ struct GruParams {
     uint64_t gt_m, ge_m;                // ceil(2^40 / ((off_e - kd) / 8)), ceil(2^40 / ((kx - off_e) / 8))
     int32_t s_kind, e_kind;             // piece forms of status / link rows (-1: none applies)
     uint32_t meta;                      // LDS bytes before X: row list, then T-enc w | b (pad32(d_time) each)
+    uint32_t ws_lomask;                 // weight-stationary form: bit s set if X k-step s has a lo plane
     const __bf16 *w_ih, *w_hh;
     const float *b_ih, *b_hh;
 };
@@ -327,21 +329,21 @@ __device__ __forceinline__ void gate_seg(f32x4 (&acc)[4][NB], const __bf16 *Ah, 
 // One input segment of a tile: `units` pieces of 8 columns, piece u of tile
 // row j = u / g at column c0 = 8 (u - j g), from the row row_of(j) (a valid
 // address for every j < R); store(j, c0, piece) writes it to LDS.  F pieces
-// per thread are loaded before any is stored.
-template <int KIND, int F, typename RowOf, typename Store>
+// per thread (of NT) are loaded before any is stored.
+template <int KIND, int F, uint32_t NT = kRnnThreads, typename RowOf, typename Store>
 __device__ __forceinline__ void fill_seg(uint32_t units, uint32_t g, uint64_t g_m, uint32_t dim, RowOf row_of,
                                          Store store) {
-    for (uint32_t base = threadIdx.x; base < units; base += kRnnThreads * F) {
+    for (uint32_t base = threadIdx.x; base < units; base += NT * F) {
         Piece8<KIND> pc[F];
 #pragma unroll
         for (int f = 0; f < F; f++) {
-            const uint32_t u = min(base + f * kRnnThreads, units - 1u);
+            const uint32_t u = min(base + f * NT, units - 1u);
             const uint32_t j = div_small(u, g_m), c0 = (u - j * g) * 8u;
             load_piece<KIND>(row_of(j), dim, c0, pc[f]);
         }
 #pragma unroll
         for (int f = 0; f < F; f++) {
-            const uint32_t u = base + f * kRnnThreads;
+            const uint32_t u = base + f * NT;
             if (u < units) {
                 const uint32_t j = div_small(u, g_m), c0 = (u - j * g) * 8u;
                 store(j, c0, pc[f]);
@@ -350,42 +352,22 @@ __device__ __forceinline__ void fill_seg(uint32_t units, uint32_t g, uint64_t g_
     }
 }
 
+// A tile's inputs X = [r_other | T-enc(t) | e] and H = r_self for tile rows
+// j < m (rows m .. 16 NB - 1 are written as zeros), as bf16 hi planes at Xh
+// and Hh and lo planes at Xl (columns [lo_begin, lo_end)) and Hl (fp32
+// statuses), with row strides xs, ls, hs -- in LDS or in global memory.
+// m_row .. m_t are the tile rows' list entries and link times, s_tw / s_tb
+// the zero-padded time-encoding parameters (LDS).  The caller synchronises.
 template <int NB>
-__global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
+__device__ __forceinline__ void gru_fill(const GruParams &p, uint32_t m, const uint32_t *m_row,
+                                         const int32_t *m_self, const int32_t *m_other, const float *m_t,
+                                         const float *s_tw, const float *s_tb, __bf16 *Xh, __bf16 *Xl,
+                                         __bf16 *Hh, __bf16 *Hl, uint32_t xs, uint32_t ls, uint32_t hs) {
     constexpr uint32_t R = 16 * NB;
     // Input units (8 columns each) whose loads a thread keeps in flight
-    // together: about all of its units for the common widths.
+    // together (generic path): about all of its units for the common widths.
     constexpr int kFill = NB == 4 ? 12 : (NB == 2 ? 8 : 4);
-    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-    uint32_t *m_row = (uint32_t *)smem;          // pair row of tile row j
-    int32_t *m_self = (int32_t *)(m_row + 64);
-    int32_t *m_other = m_self + 64;
-    float *m_t = (float *)(m_other + 64);        // its link's time, as fp32
-    float *s_tw = (float *)(smem + kGruMetaRows), *s_tb = s_tw + ((p.d_time + 31u) & ~31u);
-    __bf16 *Xh = (__bf16 *)(smem + p.meta);
-    __bf16 *Xl = (__bf16 *)(smem + p.off_xl);
-    __bf16 *Hh = (__bf16 *)(smem + p.off_h);
-    __bf16 *Hl = (__bf16 *)(smem + p.off_hl);
-
     const uint32_t tid = threadIdx.x;
-    const uint32_t lane = tid & 63, wave = tid >> 6;
-    const uint32_t count = *p.count;
-    const uint64_t j0 = (uint64_t)blockIdx.x * R;
-    if (j0 >= count) return;
-    const uint32_t m = (uint32_t)min((uint64_t)R, (uint64_t)count - j0);
-    if (tid < m) {
-        const u32x4 e = p.list[j0 + tid];
-        m_row[tid] = e[0];
-        m_self[tid] = (int32_t)e[1];
-        m_other[tid] = (int32_t)e[2];
-        m_t[tid] = (float)p.t[e[0] >> 1];
-    }
-    for (uint32_t u = tid; u < ((p.d_time + 31u) & ~31u); u += kRnnThreads) {
-        s_tw[u] = u < p.d_time ? p.tw[u] : 0.0f;
-        s_tb[u] = u < p.d_time ? p.tb[u] : 0.0f;
-    }
-    __syncthreads();
-
     if (p.s_kind >= 0 && (p.e_kind >= 0 || p.kx == p.off_e)) {
         // Inputs segment by segment, each with its rows' fixed piece form:
         // statuses (H = r_self, then X's r_other), the time encoding, link
@@ -410,13 +392,13 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
                         float v[8];
                         piece_floats<K>(pc, d, c0, ok, v);
                         if (jj < R)
-                            store_split8(v, Hh + (size_t)j * p.hs + c0, Hl + (size_t)j * p.hs + c0);
+                            store_split8(v, Hh + (size_t)j * hs + c0, Hl + (size_t)j * hs + c0);
                         else
-                            store_split8(v, Xh + (size_t)j * p.xs + c0,
-                                         Xl + (size_t)j * p.ls + (c0 - p.lo_begin));
+                            store_split8(v, Xh + (size_t)j * xs + c0,
+                                         Xl + (size_t)j * ls + (c0 - p.lo_begin));
                     } else {
                         const u32x4 w = piece_bf16_bits<K>(pc, d, c0, ok);
-                        *(u32x4 *)(jj < R ? Hh + (size_t)j * p.hs + c0 : Xh + (size_t)j * p.xs + c0) = w;
+                        *(u32x4 *)(jj < R ? Hh + (size_t)j * hs + c0 : Xh + (size_t)j * xs + c0) = w;
                     }
                 });
         };
@@ -442,7 +424,7 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
             }
 #pragma unroll
             for (int i = 0; i < 8; i++) v[i] = (j < m && k + i < p.d_time) ? v[i] : 0.0f;
-            store_split8(v, Xh + (size_t)j * p.xs + p.kd + k, Xl + (size_t)j * p.ls + (p.kd + k - p.lo_begin));
+            store_split8(v, Xh + (size_t)j * xs + p.kd + k, Xl + (size_t)j * ls + (p.kd + k - p.lo_begin));
         }
 
         // Link rows (rows at or past edge_rows are zeros).
@@ -462,10 +444,10 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
                         if constexpr (K == kF32Vec) {
                             float v[8];
                             piece_floats<K>(pc, p.e_dim, c0, ok, v);
-                            store_split8(v, Xh + (size_t)j * p.xs + p.off_e + c0,
-                                         Xl + (size_t)j * p.ls + (p.off_e + c0 - p.lo_begin));
+                            store_split8(v, Xh + (size_t)j * xs + p.off_e + c0,
+                                         Xl + (size_t)j * ls + (p.off_e + c0 - p.lo_begin));
                         } else {
-                            *(u32x4 *)(Xh + (size_t)j * p.xs + p.off_e + c0) =
+                            *(u32x4 *)(Xh + (size_t)j * xs + p.off_e + c0) =
                                 piece_bf16_bits<K>(pc, p.e_dim, c0, ok);
                         }
                     });
@@ -477,7 +459,6 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
             else
                 edge_fill(std::integral_constant<int, kBf16Vec>{});
         }
-        __syncthreads();
     } else {
 
     // Inputs: X = [r_other | T-enc(t) | e] and H = r_self; rows m .. R-1
@@ -544,21 +525,58 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
                 const uint32_t j = div_small(u - ux, p.gh_m);
                 const uint32_t c0 = (u - ux - j * gh) * 8;
                 if (p.h_lo)
-                    store_split8(v[f], Hh + (size_t)j * p.hs + c0, Hl + (size_t)j * p.hs + c0);
+                    store_split8(v[f], Hh + (size_t)j * hs + c0, Hl + (size_t)j * hs + c0);
                 else
-                    store_hi8(v[f], Hh + (size_t)j * p.hs + c0);
+                    store_hi8(v[f], Hh + (size_t)j * hs + c0);
                 continue;
             }
             const uint32_t j = div_small(u, p.gx_m);
             const uint32_t c0 = (u - j * gx) * 8;
             if (c0 >= p.lo_begin && c0 < p.lo_end)
-                store_split8(v[f], Xh + (size_t)j * p.xs + c0, Xl + (size_t)j * p.ls + (c0 - p.lo_begin));
+                store_split8(v[f], Xh + (size_t)j * xs + c0, Xl + (size_t)j * ls + (c0 - p.lo_begin));
             else
-                store_hi8(v[f], Xh + (size_t)j * p.xs + c0);
+                store_hi8(v[f], Xh + (size_t)j * xs + c0);
         }
     }
-    __syncthreads();
     }
+
+}
+
+template <int NB>
+__global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
+    constexpr uint32_t R = 16 * NB;
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    uint32_t *m_row = (uint32_t *)smem;          // pair row of tile row j
+    int32_t *m_self = (int32_t *)(m_row + 64);
+    int32_t *m_other = m_self + 64;
+    float *m_t = (float *)(m_other + 64);        // its link's time, as fp32
+    float *s_tw = (float *)(smem + kGruMetaRows), *s_tb = s_tw + ((p.d_time + 31u) & ~31u);
+    __bf16 *Xh = (__bf16 *)(smem + p.meta);
+    __bf16 *Xl = (__bf16 *)(smem + p.off_xl);
+    __bf16 *Hh = (__bf16 *)(smem + p.off_h);
+    __bf16 *Hl = (__bf16 *)(smem + p.off_hl);
+
+    const uint32_t tid = threadIdx.x;
+    const uint32_t lane = tid & 63, wave = tid >> 6;
+    const uint32_t count = *p.count;
+    const uint64_t j0 = (uint64_t)blockIdx.x * R;
+    if (j0 >= count) return;
+    const uint32_t m = (uint32_t)min((uint64_t)R, (uint64_t)count - j0);
+    if (tid < m) {
+        const u32x4 e = p.list[j0 + tid];
+        m_row[tid] = e[0];
+        m_self[tid] = (int32_t)e[1];
+        m_other[tid] = (int32_t)e[2];
+        m_t[tid] = (float)p.t[e[0] >> 1];
+    }
+    for (uint32_t u = tid; u < ((p.d_time + 31u) & ~31u); u += kRnnThreads) {
+        s_tw[u] = u < p.d_time ? p.tw[u] : 0.0f;
+        s_tb[u] = u < p.d_time ? p.tb[u] : 0.0f;
+    }
+    __syncthreads();
+
+    gru_fill<NB>(p, m, m_row, m_self, m_other, m_t, s_tw, s_tb, Xh, Xl, Hh, Hl, p.xs, p.ls, p.hs);
+    __syncthreads();
 
     const uint32_t d = p.d;
     const uint32_t units = (d + 15) / 16;
@@ -617,6 +635,313 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
                     ((float *)crow)[j] = out;
             }
         }
+    }
+}
+
+// Weight-stationary form of the GRU pass, for status rows with a 16-byte
+// piece form, kd <= 128, kx + kd <= 32 kWsSteps and a time encoding.  One
+// workgroup per CU with kd / 16 wavefronts: wavefront w holds the weight
+// fragments of output units 16 w .. 16 w + 15 (all three gates, every
+// k-step: 12 registers per k-step) for the whole launch, and the workgroup
+// loops over the 32-row tiles blockIdx.x, blockIdx.x + gridDim.x, ...
+//
+// A tile sits in LDS in matrix-operand order: the A operand of k-step s and
+// row block rb is 1 KB at (s NB + rb) KB of its plane, lane l's eight values
+// at 16 l, so that every operand read is one contiguous 16-byte read per
+// lane at a fixed offset.  Planes: X hi, X lo (indexed by the same step;
+// only steps inside [lo_begin, lo_end) are written or read), H hi, H lo
+// (fp32 statuses).  Tiles alternate between two such buffers (two LDS
+// arrays, so that the compiler can tell a write of one from a read of the
+// other): the status rows of the next tile are requested before the
+// products of the current one and land in the other buffer meanwhile --
+// bf16 rows whose width is a multiple of 32 by direct global-to-LDS loads
+// (one operand fragment per wavefront and load), other rows through
+// registers, written after the products (fp32 ones as hi + lo).  The list
+// entries of the tile after that are read meanwhile into the third of three
+// row-list slots.  The time encoding is computed when the next tile is
+// written; link rows, if any, are read then too.  Rows of a tile past the
+// list's end repeat its last entry and are never written out.
+constexpr int kWsSteps = 12;
+constexpr uint32_t kWsRows = 32;
+constexpr int kWsBf16Dma = 0, kWsBf16 = 1, kWsF32 = 2;   // how status rows reach the LDS
+
+template <int KH>
+struct WsLayout {
+    static constexpr uint32_t NB = kWsRows / 16, KXM = kWsSteps - KH;
+    static constexpr uint32_t frag = 1024;   // bytes of one 16 x 32 operand
+    static constexpr uint32_t xh = 0, xl = KXM * NB * frag, hh = 2 * KXM * NB * frag,
+                              hl = hh + KH * NB * frag, buf = hl + KH * NB * frag;
+};
+
+// Byte offset of the eight values at row j, columns c .. c + 7 (c % 8 == 0)
+// of a tile plane in operand order.
+__device__ __forceinline__ uint32_t frag_off(uint32_t j, uint32_t c) {
+    return (((c >> 5) * (kWsRows / 16) + (j >> 4)) * 64u + (j & 15u) + 16u * ((c >> 3) & 3u)) * 16u;
+}
+
+// A uniform value that the compiler re-reads where it is used (keeps loop
+// invariant flags out of long-lived registers).
+__device__ __forceinline__ uint32_t opaque_u32(uint32_t x) {
+    x = __builtin_amdgcn_readfirstlane(x);
+    asm volatile("" : "+s"(x));
+    return x;
+}
+
+typedef __attribute__((address_space(3))) void *lds_ptr;
+
+template <int KH, int MODE>
+__global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
+    using L = WsLayout<KH>;
+    constexpr uint32_t NB = L::NB, R = kWsRows, T = 128 * KH, GH = 4 * KH, FB = L::frag;
+    constexpr int KXM = (int)L::KXM, KS = KXM + KH;
+    constexpr int SK = MODE == kWsF32 ? kF32Vec : kBf16Vec;
+    static_assert(R * GH == T, "one status piece of each input half per thread");
+    static_assert(2 * KH == KH * NB, "one operand fragment of each input half per wavefront");
+    __shared__ __attribute__((aligned(16))) uint8_t buf0[L::buf];
+    __shared__ __attribute__((aligned(16))) uint8_t buf1[L::buf];
+    __shared__ u32x4 meta[3 * R];   // 3 slots x R: {pair row, self, other, 0}
+    extern __shared__ __attribute__((aligned(16))) float s_tw[];   // T-enc w | b, pad32(d_time) each
+    float *s_tb = s_tw + ((p.d_time + 31u) & ~31u);
+
+    const uint32_t tid = threadIdx.x, lane = tid & 63;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t lr = lane & 15, lk = (lane >> 4) * 8;
+    const uint32_t count = *p.count;
+    const uint32_t tiles = (uint32_t)(((uint64_t)count + R - 1) / R);
+    if (blockIdx.x >= tiles) return;
+    const uint32_t d = p.d, kx_steps = p.kx / 32;
+    const bool mma = wave < (d + 15) / 16;
+    const uint32_t j = 16 * wave + lr, jr = j < d ? j : d - 1;
+    const uint32_t gt = (p.off_e - p.kd) / 8, tu = R * gt;
+
+    // This wavefront's weight fragments and biases.
+    bf16x8 bx[KXM][3], bh[KH][3];
+#pragma unroll
+    for (int s = 0; s < KXM; s++)
+#pragma unroll
+        for (int g = 0; g < 3; g++)
+            bx[s][g] = *(const bf16x8 *)(p.w_ih + ((size_t)g * d + jr) * p.kx +
+                                         32u * min((uint32_t)s, kx_steps - 1u) + lk);
+#pragma unroll
+    for (int s = 0; s < KH; s++)
+#pragma unroll
+        for (int g = 0; g < 3; g++)
+            bh[s][g] = *(const bf16x8 *)(p.w_hh + ((size_t)g * d + jr) * p.kd + 32 * s + lk);
+    const float br = p.b_ih[jr] + p.b_hh[jr];
+    const float bz = p.b_ih[d + jr] + p.b_hh[d + jr];
+    const float bin = p.b_ih[2 * d + jr];
+    const float bhn = p.b_hh[2 * d + jr];
+
+    auto list_entry = [&](uint32_t tl) __attribute__((always_inline)) {
+        return p.list[min((uint64_t)tl * R + (tid & (R - 1)), (uint64_t)count - 1)];
+    };
+
+    // Register path: a thread's status pieces, f = 0 of H (self) and f = 1
+    // of X's r_other, both at tile row pj, columns pc0 .. pc0 + 7
+    // (operand-order offset po).  Direct path: wavefront w's operand
+    // fragment w of H and of X's r_other, lane l at tile row dj, column dc.
+    // Both: the thread's first time-encoding unit (row tj, encoding columns
+    // tk .. tk + 7, offset to) and that row's link time.
+    const uint32_t pj = tid / GH, pc0 = 8 * (tid % GH), po = frag_off(pj, pc0);
+    const uint32_t dj = 16 * (wave % NB) + lr, dc = 32 * (wave / NB) + lk;
+    const uint32_t tu0 = min(tid, tu - 1u);
+    const uint32_t tj = div_small(tu0, p.gt_m), tk = (tu0 - tj * gt) * 8u, to = frag_off(tj, p.kd + tk);
+    Piece8<SK> pc[2];
+    uint32_t t0 = 0;   // converted where used: a conversion here would wait for the loads
+    auto request_tile = [&](uint8_t *nb, uint32_t slot) __attribute__((always_inline)) {
+        if constexpr (MODE == kWsBf16Dma) {
+            const u32x4 e = meta[slot * R + dj];
+            __builtin_amdgcn_global_load_lds(p.st + (size_t)e[1] * p.srb + 2u * dc, (lds_ptr)(nb + L::hh + wave * FB),
+                                             16, 0, 0);
+            __builtin_amdgcn_global_load_lds(p.st + (size_t)e[2] * p.srb + 2u * dc, (lds_ptr)(nb + L::xh + wave * FB),
+                                             16, 0, 0);
+        } else {
+            const u32x4 e = meta[slot * R + pj];
+            load_piece<SK>(p.st + (size_t)e[1] * p.srb, d, pc0, pc[0]);
+            load_piece<SK>(p.st + (size_t)e[2] * p.srb, d, pc0, pc[1]);
+        }
+        t0 = p.t[meta[slot * R + tj][0] >> 1];
+    };
+    auto tenc_unit = [&](uint8_t *nb, uint32_t off, uint32_t k, float tf) __attribute__((always_inline)) {
+        const f32x4 w0 = *(const f32x4 *)(s_tw + k), w1 = *(const f32x4 *)(s_tw + k + 4);
+        const f32x4 b0 = *(const f32x4 *)(s_tb + k), b1 = *(const f32x4 *)(s_tb + k + 4);
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            v[i] = cos_fp32(__builtin_fmaf(w0[i], tf, b0[i]));
+            v[4 + i] = cos_fp32(__builtin_fmaf(w1[i], tf, b1[i]));
+        }
+#pragma unroll
+        for (int i = 0; i < 8; i++) v[i] = k + i < p.d_time ? v[i] : 0.0f;
+        store_split8(v, (__bf16 *)(nb + L::xh + off), (__bf16 *)(nb + L::xl + off));
+    };
+    auto write_tile = [&](uint8_t *nb, uint32_t slot) __attribute__((always_inline)) {
+        if constexpr (MODE == kWsF32) {
+            float v[8];
+            piece_floats<SK>(pc[0], d, pc0, true, v);
+            store_split8(v, (__bf16 *)(nb + L::hh + po), (__bf16 *)(nb + L::hl + po));
+            piece_floats<SK>(pc[1], d, pc0, true, v);
+            store_split8(v, (__bf16 *)(nb + L::xh + po), (__bf16 *)(nb + L::xl + po));   // lo_begin == 0
+        } else if constexpr (MODE == kWsBf16) {
+            *(u32x4 *)(nb + L::hh + po) = piece_bf16_bits<SK>(pc[0], d, pc0, true);
+            *(u32x4 *)(nb + L::xh + po) = piece_bf16_bits<SK>(pc[1], d, pc0, true);
+        }
+        if (tid < tu) tenc_unit(nb, to, tk, (float)t0);
+        for (uint32_t u = tid + T; u < tu; u += T) {
+            const uint32_t jj = div_small(u, p.gt_m), k = (u - jj * gt) * 8u;
+            tenc_unit(nb, frag_off(jj, p.kd + k), k, (float)p.t[meta[slot * R + jj][0] >> 1]);
+        }
+        if (p.kx > p.off_e) {
+            const uint32_t ge = (p.kx - p.off_e) / 8;
+            auto edge_fill = [&](auto kind) __attribute__((always_inline)) {
+                constexpr int K = decltype(kind)::value;
+                auto eid_of = [&](uint32_t jj) __attribute__((always_inline)) {
+                    return p.first_eid + (meta[slot * R + jj][0] >> 1);
+                };
+                fill_seg<K, 4, T>(
+                    R * ge, ge, p.ge_m, p.e_dim,
+                    [&](uint32_t jj) __attribute__((always_inline)) {
+                        const uint64_t e = eid_of(jj);
+                        return p.efeat + (size_t)(e < (uint64_t)p.edge_rows ? e : 0u) * p.erb;
+                    },
+                    [&](uint32_t jj, uint32_t c0, const Piece8<K> &q) __attribute__((always_inline)) {
+                        const bool ok = eid_of(jj) < (uint64_t)p.edge_rows;
+                        const uint32_t off = frag_off(jj, p.off_e + c0);
+                        if constexpr (K == kF32Vec) {
+                            float v[8];
+                            piece_floats<K>(q, p.e_dim, c0, ok, v);
+                            store_split8(v, (__bf16 *)(nb + L::xh + off), (__bf16 *)(nb + L::xl + off));
+                        } else {
+                            *(u32x4 *)(nb + L::xh + off) = piece_bf16_bits<K>(q, p.e_dim, c0, ok);
+                        }
+                    });
+            };
+            if (p.e_kind == kF32Vec)
+                edge_fill(std::integral_constant<int, kF32Vec>{});
+            else if (p.e_kind == kBf16Word)
+                edge_fill(std::integral_constant<int, kBf16Word>{});
+            else
+                edge_fill(std::integral_constant<int, kBf16Vec>{});
+        }
+    };
+    // Direct loads into LDS count as outstanding vector-memory operations:
+    // all of this wavefront's must have landed before the workgroup barrier.
+    auto tile_barrier = [&]() __attribute__((always_inline)) {
+        if constexpr (MODE == kWsBf16Dma) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    };
+
+    // Prologue: time-encoding parameters, row lists of the first two tiles,
+    // the first tile's inputs.
+    for (uint32_t u = tid; u < ((p.d_time + 31u) & ~31u); u += T) {
+        s_tw[u] = u < p.d_time ? p.tw[u] : 0.0f;
+        s_tb[u] = u < p.d_time ? p.tb[u] : 0.0f;
+    }
+    const uint32_t stride = gridDim.x;
+    uint32_t tl = blockIdx.x;
+    {
+        const u32x4 e0 = list_entry(tl), e1 = list_entry(tl + stride < tiles ? tl + stride : tl);
+        if (tid < R) {
+            meta[tid] = e0;
+            meta[R + tid] = e1;
+        }
+    }
+    __syncthreads();
+    request_tile(buf0, 0);
+    write_tile(buf0, 0);
+    tile_barrier();
+
+    // One tile: products from cb (row-list slot i % 3) while the next tile
+    // arrives in nb; false after the workgroup's last tile.
+    auto tile = [&](uint8_t *cb, uint8_t *nb, uint32_t i) __attribute__((always_inline)) {
+        const uint32_t ms = i % 3, ns = (i + 1) % 3;
+        const bool has_next = tl + stride < tiles, has_nn = tl + 2 * stride < tiles;
+        // Row list of the tile two strides on and status rows of the next tile
+        // (re-reads of the current tile's when there is none: in bounds, unused).
+        const u32x4 e_nn = list_entry(has_nn ? tl + 2 * stride : tl);
+        if (MODE != kWsBf16Dma || has_next) request_tile(nb, has_next ? ns : ms);
+        if (mma) {
+            const uint32_t lm = opaque_u32(p.ws_lomask), ks = opaque_u32(kx_steps);
+            const uint8_t *b = cb + 16u * lane;
+            f32x4 acc[4][NB];   // r, z, input part of n, hidden part of n
+#pragma unroll
+            for (int g = 0; g < 4; g++)
+#pragma unroll
+                for (int rb = 0; rb < NB; rb++) acc[g][rb] = f32x4(0.0f);
+            auto mfma3 = [&](const bf16x8 (&a)[NB], const bf16x8 (&w)[3], int nidx) __attribute__((always_inline)) {
+#pragma unroll
+                for (int rb = 0; rb < NB; rb++)
+#pragma unroll
+                    for (int g = 0; g < 3; g++) {
+                        const int gi = g == 2 ? nidx : g;
+                        acc[gi][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], w[g], acc[gi][rb], 0, 0, 0);
+                    }
+            };
+            // Operands of step s (X steps, then H steps) into a / al: the hi
+            // plane always, the lo plane where the step has one.
+            auto load_step = [&](int s, bf16x8 (&a)[NB], bf16x8 (&al)[NB]) __attribute__((always_inline)) {
+                const uint32_t ph = s < KXM ? L::xh + s * NB * FB : L::hh + (s - KXM) * NB * FB;
+                const uint32_t pl = s < KXM ? L::xl + s * NB * FB : L::hl + (s - KXM) * NB * FB;
+#pragma unroll
+                for (int rb = 0; rb < NB; rb++) a[rb] = *(const bf16x8 *)(b + ph + rb * FB);
+                if (s < KXM ? ((lm >> s) & 1u) != 0 : MODE == kWsF32) {
+#pragma unroll
+                    for (int rb = 0; rb < NB; rb++) al[rb] = *(const bf16x8 *)(b + pl + rb * FB);
+                }
+            };
+            bf16x8 a[2][NB], al[2][NB];
+            load_step(0, a[0], al[0]);
+#pragma unroll
+            for (int s = 0; s < KS; s++) {
+                if (s + 1 < KS) load_step(s + 1, a[(s + 1) & 1], al[(s + 1) & 1]);
+                if (s < KXM) {
+                    if ((uint32_t)s < ks) mfma3(a[s & 1], bx[s], 2);
+                    if ((lm >> s) & 1u) mfma3(al[s & 1], bx[s], 2);
+                } else {
+                    mfma3(a[s & 1], bh[s - KXM], 3);
+                    if constexpr (MODE == kWsF32) mfma3(al[s & 1], bh[s - KXM], 3);
+                }
+            }
+            float hv[NB][4];
+#pragma unroll
+            for (int rb = 0; rb < NB; rb++)
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    const uint32_t row = 16u * rb + 4u * (lane >> 4) + q;
+                    if constexpr (MODE == kWsF32)
+                        hv[rb][q] = ((const float *)(p.st + (size_t)meta[ms * R + row][1] * p.srb))[jr];
+                    else
+                        hv[rb][q] = (float)*(const __bf16 *)(cb + L::hh + frag_off(row, jr & ~7u) + 2u * (jr & 7u));
+                }
+            const uint32_t m = min(R, count - tl * R);
+            if (j < d) {
+#pragma unroll
+                for (int rb = 0; rb < NB; rb++)
+#pragma unroll
+                    for (int q = 0; q < 4; q++) {
+                        const uint32_t row = 16u * rb + 4u * (lane >> 4) + q;
+                        if (row >= m) continue;
+                        const float rg = sigmoid_f32(acc[0][rb][q] + br);
+                        const float zg = sigmoid_f32(acc[1][rb][q] + bz);
+                        const float ng = tanh_f32(acc[2][rb][q] + bin + rg * (acc[3][rb][q] + bhn));
+                        const float out = (1.0f - zg) * ng + zg * hv[rb][q];
+                        uint8_t *crow = p.cand + (size_t)meta[ms * R + row][0] * p.srb;
+                        if constexpr (MODE == kWsF32)
+                            ((float *)crow)[j] = out;
+                        else
+                            ((uint16_t *)crow)[j] = f32_to_bf16_rne(out);
+                    }
+            }
+        }
+        if (has_next) write_tile(nb, ns);
+        if (has_nn && tid < R) meta[((i + 2) % 3) * R + tid] = e_nn;
+        tile_barrier();
+        tl += stride;
+        return has_next;
+    };
+    for (uint32_t i = 0;; i += 2) {
+        if (!tile(buf0, buf1, i)) break;
+        if (!tile(buf1, buf0, i + 1)) break;
     }
 }
 
@@ -771,21 +1096,41 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     p.b_ih = wts->b_ih;
     p.b_hh = wts->b_hh;
 
-    // Tile of 16 * nb listed rows: as large as the LDS budget of two
-    // workgroups per CU allows, smaller when the batch would give fewer than
-    // kGruTargetTiles tiles (counting all 2n pair rows; the winners are
-    // fewer); a 16-row tile may use a workgroup's whole LDS.
+    // Weight-stationary form when its weight fragments fit the registers and
+    // its two tile buffers the LDS; else tiles of 16 * nb listed rows: as
+    // large as the LDS budget of two workgroups per CU allows, smaller when
+    // the batch would give fewer than kGruTargetTiles tiles (counting all 2n
+    // pair rows; the winners are fewer); a 16-row tile may use a workgroup's
+    // whole LDS.
     const uint64_t pairs = 2ull * n;
-    uint32_t nb = 4;
-    while (nb > 1 && pairs < (uint64_t)kGruTargetTiles * 16u * nb) nb /= 2;
-    uint32_t lds = 0;
-    for (;; nb /= 2) {
-        GruParams trial = p;
-        lds = gru_layout(trial, 16u * nb);
-        if (lds <= (nb == 1 ? kGruLdsMax : kGruLdsBudget)) break;
-        if (nb == 1) return NLB_EINVAL;   // one 16-row tile does not fit the LDS
+    const uint32_t kh = p.kd / 32;
+    // Forms whose registers fit without spills: bf16 rows of a width that is
+    // a multiple of 32 (direct loads into LDS) up to kd = 128, other 16-byte
+    // rows up to kd = 64.
+    const int ws_mode = p.s_kind == kF32Vec ? kWsF32 : (p.d % 32 == 0 ? kWsBf16Dma : kWsBf16);
+    bool ws = (p.s_kind == kBf16Vec || p.s_kind == kF32Vec) && kh <= (ws_mode == kWsBf16Dma ? 4u : 2u) &&
+              p.kx / 32 + kh <= (uint32_t)kWsSteps && p.d_time > 0 && (p.kx == p.off_e || p.e_kind >= 0);
+    uint32_t lds = 0, nb = 4;
+    int cus = 0;
+    if (ws) {
+        // static LDS: two tile buffers and the row-list slots; dynamic: T-enc w | b
+        const uint32_t bufs = kh == 1 ? WsLayout<1>::buf : kh == 2 ? WsLayout<2>::buf
+                            : kh == 3 ? WsLayout<3>::buf : WsLayout<4>::buf;
+        lds = 8u * pad32(p.d_time);
+        ws = 2u * bufs + 3u * 32u * 16u + lds <= kGruLdsMax &&
+             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) == hipSuccess && cus > 0;
+        for (uint32_t st = p.lo_begin / 32; st < p.lo_end / 32; st++) p.ws_lomask |= 1u << st;
     }
-    gru_layout(p, 16u * nb);
+    if (!ws) {
+        while (nb > 1 && pairs < (uint64_t)kGruTargetTiles * 16u * nb) nb /= 2;
+        for (;; nb /= 2) {
+            GruParams trial = p;
+            lds = gru_layout(trial, 16u * nb);
+            if (lds <= (nb == 1 ? kGruLdsMax : kGruLdsBudget)) break;
+            if (nb == 1) return NLB_EINVAL;   // one 16-row tile does not fit the LDS
+        }
+        gru_layout(p, 16u * nb);
+    }
 
     int rc = rnn_reserve(h, pairs, p.srb);
     if (rc != NLB_OK) return rc;
@@ -813,18 +1158,37 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     SelectParams sp = {src, dst, n, h->num_nodes, h->rnn_winner, epoch_hi, h->rnn_cand_node, list, count};
     hipLaunchKernelGGL(rnn_select, dim3((unsigned)((pairs + kSelectRows - 1) / kSelectRows)),
                        dim3(kRnnThreads), 0, (hipStream_t)stream, sp);
-    const void *kern = nb == 4 ? (const void *)rnn_gru<4>
-                     : nb == 2 ? (const void *)rnn_gru<2> : (const void *)rnn_gru<1>;
-    if (lds > 64u * 1024u &&
-        hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGruLdsMax) != hipSuccess)
-        return NLB_EDEVICE;
-    const dim3 grid((unsigned)((pairs + 16u * nb - 1) / (16u * nb)));
-    if (nb == 4)
-        hipLaunchKernelGGL(rnn_gru<4>, grid, dim3(kRnnThreads), lds, (hipStream_t)stream, p);
-    else if (nb == 2)
-        hipLaunchKernelGGL(rnn_gru<2>, grid, dim3(kRnnThreads), lds, (hipStream_t)stream, p);
-    else
-        hipLaunchKernelGGL(rnn_gru<1>, grid, dim3(kRnnThreads), lds, (hipStream_t)stream, p);
+    if (ws) {
+        const void *kern = nullptr;
+        switch (kh * 4 + ws_mode) {
+#define NLB_WS_CASE(KH, MODE) \
+        case KH * 4 + MODE: kern = (const void *)rnn_gru_ws<KH, MODE>; break;
+        NLB_WS_CASE(1, kWsBf16Dma) NLB_WS_CASE(1, kWsBf16) NLB_WS_CASE(1, kWsF32)
+        NLB_WS_CASE(2, kWsBf16Dma) NLB_WS_CASE(2, kWsBf16) NLB_WS_CASE(2, kWsF32)
+        NLB_WS_CASE(3, kWsBf16Dma) NLB_WS_CASE(4, kWsBf16Dma)
+#undef NLB_WS_CASE
+        default: return NLB_EINVAL;
+        }
+        const uint64_t tiles = (pairs + 31) / 32;
+        const dim3 grid((unsigned)std::min<uint64_t>(tiles, (uint64_t)cus));
+        void *args[] = {&p};
+        if (hipLaunchKernel(kern, grid, dim3(128u * kh), args, lds, (hipStream_t)stream) != hipSuccess)
+            return NLB_EDEVICE;
+    } else {
+        const void *kern = nb == 4 ? (const void *)rnn_gru<4>
+                         : nb == 2 ? (const void *)rnn_gru<2> : (const void *)rnn_gru<1>;
+        if (lds > 64u * 1024u &&
+            hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGruLdsMax) != hipSuccess)
+            return NLB_EDEVICE;
+        const dim3 grid((unsigned)((pairs + 16u * nb - 1) / (16u * nb)));
+        if (nb == 4)
+            hipLaunchKernelGGL(rnn_gru<4>, grid, dim3(kRnnThreads), lds, (hipStream_t)stream, p);
+        else if (nb == 2)
+            hipLaunchKernelGGL(rnn_gru<2>, grid, dim3(kRnnThreads), lds, (hipStream_t)stream, p);
+        else
+            hipLaunchKernelGGL(rnn_gru<1>, grid, dim3(kRnnThreads), lds, (hipStream_t)stream, p);
+    }
+    h->rnn_form = ws ? NLB_RNN_FORM_WEIGHT_STATIONARY : NLB_RNN_FORM_TILED;
     uint32_t w = 2;
     for (uint32_t c = 16; c >= 4; c /= 2)
         if (p.srb % c == 0 && (uintptr_t)status % c == 0 && (uintptr_t)h->rnn_cand % c == 0) {

@@ -203,6 +203,53 @@ def test_rnn_status_widths_and_types(d, dtype):
     _log(f"d={d} {dtype}: max err {err:.3e}, bf16 mismatches {frac:.3%}")
 
 
+# d, status dtype, d_time, link-row width, link dtype, links, nodes, form of the GRU pass
+WS, TILED = 2, 1
+GRU_FORMS = [
+    (128, "bf16", 100, 0, None, 6000, 20000, WS),     # direct loads into LDS, kd = 128 (12 k-steps)
+    (96, "bf16", 20, 16, "bf16", 5000, 20000, WS),    # direct, kd = 96, bf16 link rows
+    (64, "bf16", 28, 8, "f32", 40000, 100000, WS),    # direct, fp32 link rows (lo plane); ~7 tiles per CU
+    (64, "bf16", 28, 8, "f32", 1, 100, WS),           # one link
+    (32, "bf16", 64, 40, "bf16", 3000, 5000, WS),     # direct, kd = 32; time encoding and rows over 2 steps each
+    (40, "bf16", 20, 8, "f32", 5000, 20000, WS),      # bf16 rows through registers (width not a multiple of 32)
+    (24, "bf16", 12, 0, None, 3000, 5000, WS),        # same, kd = 32
+    (48, "f32", 20, 16, "bf16", 5000, 20000, WS),     # fp32 statuses: hi + lo planes of X and H
+    (20, "f32", 12, 8, "f32", 3000, 5000, WS),        # fp32, every X step with a lo plane
+    (96, "f32", 20, 0, None, 3000, 5000, TILED),      # fp32 beyond kd = 64: tiled
+    (128, "bf16", 100, 200, "bf16", 2000, 5000, TILED),   # 15 + 4 k-steps: tiled
+]
+
+
+@pytest.mark.parametrize("d,dtype,d_time,e_dim,e_dtype,n,N,form", GRU_FORMS)
+def test_rnn_gru_forms(d, dtype, d_time, e_dim, e_dtype, n, N, form):
+    """Each form of the GRU pass (weight-stationary with direct or register
+    row loads, bf16 or fp32 statuses, link rows of either type; the tiled
+    form where the weight-stationary one does not apply) against the
+    oracle, with the form the update reports."""
+    import paper_2402_01964_amd as nlb
+    rng = np.random.default_rng(1000 + d + n)
+    e0 = 5
+    ef = None
+    edge = None
+    if e_dim:
+        x = rng.standard_normal((n + e0 + 3, e_dim)).astype(np.float32)
+        ef = synth._to_bf16_bits(x) if e_dtype == "bf16" else x
+        edge = feat_to_dev(ef, e_dtype)
+    g, fw, fb = _small_table(N, d_time=d_time, edge=edge, seed=d)
+    x = rng.standard_normal((N, d)).astype(np.float32)
+    st = feat_to_dev(synth._to_bf16_bits(x) if dtype == "bf16" else x, dtype)
+    W = synth.gru_weights_for(d, d_time, e_dim, seed=d + 7)
+    src = rng.integers(0, N, n).astype(np.int32)
+    dst = rng.integers(0, N, n).astype(np.int32)
+    t = np.sort(rng.integers(0, 2**30, n)).astype(np.uint32)
+    what = f"d={d} {dtype} d_time={d_time} e={e_dim} {e_dtype} n={n}"
+    err, frac = _check_batch(g, st, ef, W, _weights_dev(W), fw, fb, src, dst, t, e0, what)
+    got_form = g.info()["rnn_form"]
+    _log(f"{what}: form {got_form}, max err {err:.3e}, bf16 mismatches {frac:.3%}")
+    assert got_form == form
+    assert g.status() == 0
+
+
 def test_rnn_without_time_or_link_rows_and_rows_past_the_end():
     """A table with no time encoding and no link rows (x = r_other only); and
     link rows past the end of the link table read as zeros."""
