@@ -228,6 +228,7 @@ struct GruParams {
     int32_t s_kind, e_kind;             // piece forms of status / link rows (-1: none applies)
     uint32_t meta;                      // LDS bytes before X: row list, then T-enc w | b (pad32(d_time) each)
     uint32_t ws_lomask;                 // weight-stationary form: bit s set if X k-step s has a lo plane
+    uint64_t ws_cpr_m;                  // ceil(2^40 / (srb / 16))
     const __bf16 *w_ih, *w_hh;
     const float *b_ih, *b_hh;
 };
@@ -657,10 +658,14 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
 // bf16 rows whose width is a multiple of 32 by direct global-to-LDS loads
 // (one operand fragment per wavefront and load), other rows through
 // registers, written after the products (fp32 ones as hi + lo).  The list
-// entries of the tile after that are read meanwhile into the third of three
+// entries of the tile after that are read meanwhile into one of four
 // row-list slots.  The time encoding is computed when the next tile is
-// written; link rows, if any, are read then too.  Rows of a tile past the
-// list's end repeat its last entry and are never written out.
+// written; link rows, if any, are read then too.  The new statuses of a
+// tile go to an LDS staging area and, after the tile's barrier, to the
+// candidate rows in whole 16-byte pieces, so that their stores complete
+// under the next tile's products instead of holding up the barrier.  Rows
+// of a tile past the list's end repeat its last entry and are never written
+// out.
 constexpr int kWsSteps = 12;
 constexpr uint32_t kWsRows = 32;
 constexpr int kWsBf16Dma = 0, kWsBf16 = 1, kWsF32 = 2;   // how status rows reach the LDS
@@ -671,6 +676,10 @@ struct WsLayout {
     static constexpr uint32_t frag = 1024;   // bytes of one 16 x 32 operand
     static constexpr uint32_t xh = 0, xl = KXM * NB * frag, hh = 2 * KXM * NB * frag,
                               hl = hh + KH * NB * frag, buf = hl + KH * NB * frag;
+    // output rows of a tile, row-major with a stride of the widest row
+    // (fp32, kd = 32 KH) plus 16 bytes against bank conflicts
+    static constexpr uint32_t ostride = 32 * KH * 4 + 16, ostage = kWsRows * ostride;
+    static constexpr uint32_t fixed = 2 * buf + 2 * ostage + 4 * kWsRows * 16;   // static LDS
 };
 
 // Byte offset of the eight values at row j, columns c .. c + 7 (c % 8 == 0)
@@ -699,7 +708,9 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     static_assert(2 * KH == KH * NB, "one operand fragment of each input half per wavefront");
     __shared__ __attribute__((aligned(16))) uint8_t buf0[L::buf];
     __shared__ __attribute__((aligned(16))) uint8_t buf1[L::buf];
-    __shared__ u32x4 meta[3 * R];   // 3 slots x R: {pair row, self, other, 0}
+    __shared__ __attribute__((aligned(16))) uint8_t ost0[L::ostage];
+    __shared__ __attribute__((aligned(16))) uint8_t ost1[L::ostage];
+    __shared__ u32x4 meta[4 * R];   // 4 slots x R: {pair row, self, other, 0}; tile i in slot i % 4
     extern __shared__ __attribute__((aligned(16))) float s_tw[];   // T-enc w | b, pad32(d_time) each
     float *s_tb = s_tw + ((p.d_time + 31u) & ~31u);
 
@@ -727,8 +738,9 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
 #pragma unroll
         for (int g = 0; g < 3; g++)
             bh[s][g] = *(const bf16x8 *)(p.w_hh + ((size_t)g * d + jr) * p.kd + 32 * s + lk);
-    const float br = p.b_ih[jr] + p.b_hh[jr];
-    const float bz = p.b_ih[d + jr] + p.b_hh[d + jr];
+    // Gate biases, those of r and z pre-scaled for the base-2 exponential.
+    const float nbr = -kLog2e * (p.b_ih[jr] + p.b_hh[jr]);
+    const float nbz = -kLog2e * (p.b_ih[d + jr] + p.b_hh[d + jr]);
     const float bin = p.b_ih[2 * d + jr];
     const float bhn = p.b_hh[2 * d + jr];
 
@@ -851,15 +863,29 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     write_tile(buf0, 0);
     tile_barrier();
 
-    // One tile: products from cb (row-list slot i % 3) while the next tile
-    // arrives in nb; false after the workgroup's last tile.
-    auto tile = [&](uint8_t *cb, uint8_t *nb, uint32_t i) __attribute__((always_inline)) {
-        const uint32_t ms = i % 3, ns = (i + 1) % 3;
+    // Candidate rows of tile tlp (row-list slot `slot`) from its staging
+    // area, 16 bytes per thread and step.
+    auto copy_out = [&](const uint8_t *ob, uint32_t slot, uint32_t tlp) __attribute__((always_inline)) {
+        const uint32_t cpr = p.srb / 16, units = min(R, count - tlp * R) * cpr;
+        for (uint32_t u = tid; u < units; u += T) {
+            const uint32_t row = div_small(u, p.ws_cpr_m), c = 16u * (u - row * cpr);
+            const u32x4 v = *(const u32x4 *)(ob + row * L::ostride + c);
+            *(u32x4 *)(p.cand + (size_t)meta[slot * R + row][0] * p.srb + c) = v;
+        }
+    };
+
+    // One tile: products from cb (row-list slot i % 4) while the next tile
+    // arrives in nb; new statuses to ob, those of the previous tile out of
+    // obp; false after the workgroup's last tile.
+    auto tile = [&](uint8_t *cb, uint8_t *nb, uint8_t *ob, const uint8_t *obp, uint32_t i)
+                    __attribute__((always_inline)) {
+        const uint32_t ms = i & 3, ns = (i + 1) & 3;
         const bool has_next = tl + stride < tiles, has_nn = tl + 2 * stride < tiles;
         // Row list of the tile two strides on and status rows of the next tile
         // (re-reads of the current tile's when there is none: in bounds, unused).
         const u32x4 e_nn = list_entry(has_nn ? tl + 2 * stride : tl);
         if (MODE != kWsBf16Dma || has_next) request_tile(nb, has_next ? ns : ms);
+        if (i > 0) copy_out(obp, (i - 1) & 3, tl - stride);
         if (mma) {
             const uint32_t lm = opaque_u32(p.ws_lomask), ks = opaque_u32(kx_steps);
             const uint8_t *b = cb + 16u * lane;
@@ -889,17 +915,16 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
                     for (int rb = 0; rb < NB; rb++) al[rb] = *(const bf16x8 *)(b + pl + rb * FB);
                 }
             };
-            bf16x8 a[2][NB], al[2][NB];
-            load_step(0, a[0], al[0]);
 #pragma unroll
             for (int s = 0; s < KS; s++) {
-                if (s + 1 < KS) load_step(s + 1, a[(s + 1) & 1], al[(s + 1) & 1]);
+                bf16x8 a[NB], al[NB];
+                load_step(s, a, al);
                 if (s < KXM) {
-                    if ((uint32_t)s < ks) mfma3(a[s & 1], bx[s], 2);
-                    if ((lm >> s) & 1u) mfma3(al[s & 1], bx[s], 2);
+                    if ((uint32_t)s < ks) mfma3(a, bx[s], 2);
+                    if ((lm >> s) & 1u) mfma3(al, bx[s], 2);
                 } else {
-                    mfma3(a[s & 1], bh[s - KXM], 3);
-                    if constexpr (MODE == kWsF32) mfma3(al[s & 1], bh[s - KXM], 3);
+                    mfma3(a, bh[s - KXM], 3);
+                    if constexpr (MODE == kWsF32) mfma3(al, bh[s - KXM], 3);
                 }
             }
             float hv[NB][4];
@@ -913,35 +938,40 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
                     else
                         hv[rb][q] = (float)*(const __bf16 *)(cb + L::hh + frag_off(row, jr & ~7u) + 2u * (jr & 7u));
                 }
-            const uint32_t m = min(R, count - tl * R);
             if (j < d) {
 #pragma unroll
                 for (int rb = 0; rb < NB; rb++)
 #pragma unroll
                     for (int q = 0; q < 4; q++) {
                         const uint32_t row = 16u * rb + 4u * (lane >> 4) + q;
-                        if (row >= m) continue;
-                        const float rg = sigmoid_f32(acc[0][rb][q] + br);
-                        const float zg = sigmoid_f32(acc[1][rb][q] + bz);
-                        const float ng = tanh_f32(acc[2][rb][q] + bin + rg * (acc[3][rb][q] + bhn));
-                        const float out = (1.0f - zg) * ng + zg * hv[rb][q];
-                        uint8_t *crow = p.cand + (size_t)meta[ms * R + row][0] * p.srb;
+                        const float rg = __builtin_amdgcn_rcpf(
+                            1.0f + __builtin_amdgcn_exp2f(__builtin_fmaf(acc[0][rb][q], -kLog2e, nbr)));
+                        const float zg = __builtin_amdgcn_rcpf(
+                            1.0f + __builtin_amdgcn_exp2f(__builtin_fmaf(acc[1][rb][q], -kLog2e, nbz)));
+                        const float ng = tanh_f32(__builtin_fmaf(rg, acc[3][rb][q] + bhn, acc[2][rb][q] + bin));
+                        const float out = __builtin_fmaf(zg, hv[rb][q] - ng, ng);   // (1 - z) n + z h
                         if constexpr (MODE == kWsF32)
-                            ((float *)crow)[j] = out;
+                            ((float *)(ob + row * L::ostride))[j] = out;
                         else
-                            ((uint16_t *)crow)[j] = f32_to_bf16_rne(out);
+                            ((__bf16 *)(ob + row * L::ostride))[j] = (__bf16)out;   // round to nearest even
                     }
             }
         }
         if (has_next) write_tile(nb, ns);
-        if (has_nn && tid < R) meta[((i + 2) % 3) * R + tid] = e_nn;
+        if (has_nn && tid < R) meta[((i + 2) & 3) * R + tid] = e_nn;
         tile_barrier();
         tl += stride;
         return has_next;
     };
     for (uint32_t i = 0;; i += 2) {
-        if (!tile(buf0, buf1, i)) break;
-        if (!tile(buf1, buf0, i + 1)) break;
+        if (!tile(buf0, buf1, ost0, ost1, i)) {
+            copy_out(ost0, i & 3, tl - stride);
+            break;
+        }
+        if (!tile(buf1, buf0, ost1, ost0, i + 1)) {
+            copy_out(ost1, (i + 1) & 3, tl - stride);
+            break;
+        }
     }
 }
 
@@ -1113,11 +1143,12 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     uint32_t lds = 0, nb = 4;
     int cus = 0;
     if (ws) {
-        // static LDS: two tile buffers and the row-list slots; dynamic: T-enc w | b
-        const uint32_t bufs = kh == 1 ? WsLayout<1>::buf : kh == 2 ? WsLayout<2>::buf
-                            : kh == 3 ? WsLayout<3>::buf : WsLayout<4>::buf;
+        // static LDS: tile buffers, staging areas, row-list slots; dynamic: T-enc w | b
+        const uint32_t fixed = kh == 1 ? WsLayout<1>::fixed : kh == 2 ? WsLayout<2>::fixed
+                             : kh == 3 ? WsLayout<3>::fixed : WsLayout<4>::fixed;
         lds = 8u * pad32(p.d_time);
-        ws = 2u * bufs + 3u * 32u * 16u + lds <= kGruLdsMax &&
+        p.ws_cpr_m = ceil_2_40_div(p.srb / 16);
+        ws = fixed + lds <= kGruLdsMax &&
              hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) == hipSuccess && cus > 0;
         for (uint32_t st = p.lo_begin / 32; st < p.lo_end / 32; st++) p.ws_lomask |= 1u << st;
     }
