@@ -78,6 +78,31 @@ __device__ __forceinline__ float cos_fp32_small(float x) {
     return __builtin_amdgcn_cosf(f);
 }
 
+// Bits 1 .. 192 of the binary fraction of 1 / (2 pi) = 0.159154943...,
+// most significant first (derived from Machin's formula for pi in exact
+// integer arithmetic by inv2pi_bits.py).
+__device__ const uint32_t kInv2PiBits[6] = {0x28be60dbu, 0x9391054au, 0x7f09d5f4u,
+                                            0x7d4d3770u, 0x36d8a566u, 0x4f10e410u};
+
+// cos of an fp32 argument with |x| >= kCosFastLimit, or not finite (NaN),
+// inline and in integer arithmetic (the reduction of Payne and Hanek,
+// 1983): x = m 2^e with a 24-bit integer m and e >= 10, so x / (2 pi) mod 1
+// = m * 0.c_{e+1} c_{e+2} ... mod 1 for the bits c_i of 1 / (2 pi); the 64
+// bits c_{e+1} .. c_{e+64} times m, modulo 2^64, give that fraction within
+// m 2^-64 < 2^-40 of a revolution.  Its top 32 bits, read as a signed
+// fraction in [-1/2, 1/2), go to the hardware cosine (as in the fast path).
+__device__ __forceinline__ float cos_fp32_exact_wide(float x) {
+    const uint32_t u = __float_as_uint(x), ex = (u >> 23) & 0xFFu;
+    if (ex == 0xFFu) return __uint_as_float(0x7FC00000u);
+    if (ex < 160u) return cos_fp32_small(x);   // |x| < 2^33: not a wide argument
+    const uint64_t m = (u & 0x7FFFFFu) | 0x800000u;
+    const uint32_t e = ex - 150u, w0 = e >> 5, sh = e & 31u;
+    const uint64_t top = ((uint64_t)kInv2PiBits[w0] << 32) | kInv2PiBits[w0 + 1];
+    const uint64_t w = (top << sh) | ((uint64_t)kInv2PiBits[w0 + 2] >> (32u - sh));
+    const uint64_t q = m * w;
+    return __builtin_amdgcn_cosf((float)(int32_t)(uint32_t)(q >> 32) * 0x1p-32f);
+}
+
 __device__ __forceinline__ float cos_fp32(float x) {
     if (fabsf(x) < kCosFastLimit) return cos_fp32_small(x);
     return cos_fp32_wide(x);

@@ -647,25 +647,29 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
 // loops over the 32-row tiles blockIdx.x, blockIdx.x + gridDim.x, ...
 //
 // A tile sits in LDS in matrix-operand order: the A operand of k-step s and
-// row block rb is 1 KB at (s NB + rb) KB of its plane, lane l's eight values
-// at 16 l, so that every operand read is one contiguous 16-byte read per
-// lane at a fixed offset.  Planes: X hi, X lo (indexed by the same step;
-// only steps inside [lo_begin, lo_end) are written or read), H hi, H lo
-// (fp32 statuses).  Tiles alternate between two such buffers (two LDS
-// arrays, so that the compiler can tell a write of one from a read of the
-// other): the status rows of the next tile are requested before the
-// products of the current one and land in the other buffer meanwhile --
-// bf16 rows whose width is a multiple of 32 by direct global-to-LDS loads
-// (one operand fragment per wavefront and load), other rows through
-// registers, written after the products (fp32 ones as hi + lo).  The list
-// entries of the tile after that are read meanwhile into one of four
-// row-list slots.  The time encoding is computed when the next tile is
-// written; link rows, if any, are read then too.  The new statuses of a
-// tile go to an LDS staging area and, after the tile's barrier, to the
-// candidate rows in whole 16-byte pieces, so that their stores complete
-// under the next tile's products instead of holding up the barrier.  Rows
-// of a tile past the list's end repeat its last entry and are never written
-// out.
+// row block rb is 1 KB, lane l's eight values at 16 l, so that every operand
+// read is one contiguous 16-byte read per lane at a fixed offset.  Each
+// tile buffer is two LDS arrays (so that the compiler can tell a write of
+// one from a read or write of the other): S holds what the status rows
+// fill (H hi, X hi of the r_other steps), T the rest (X hi of the
+// time-encoding and link-row steps, X lo by step, H lo for fp32 statuses;
+// lo planes only at steps inside [lo_begin, lo_end)).  Tiles alternate
+// between two buffers: the status rows of the next tile are requested
+// before the products of the current one and land in its S array meanwhile
+// -- bf16 rows whose width is a multiple of 32 by direct global-to-LDS
+// loads (one operand fragment per wavefront and load), other rows through
+// registers, written after the products (fp32 ones as hi + lo).
+//
+// The two wavefronts that share a SIMD (w and w + KH) work in opposite
+// order, so that one's vector work overlaps the other's products: the
+// second half computes the next tile's time encoding before its products
+// (from link times it read one tile ahead), the first half goes straight to
+// its products; both then apply the gates.  The new statuses of a tile go
+// to an LDS staging area and, after the tile's barrier, to the candidate
+// rows in whole 16-byte pieces, so that their stores complete under the
+// next tile's products.  List entries are read two tiles ahead into one of
+// eight row-list slots.  Rows of a tile past the list's end repeat its last
+// entry and are never written out.
 constexpr int kWsSteps = 12;
 constexpr uint32_t kWsRows = 32;
 constexpr int kWsBf16Dma = 0, kWsBf16 = 1, kWsF32 = 2;   // how status rows reach the LDS
@@ -674,12 +678,16 @@ template <int KH>
 struct WsLayout {
     static constexpr uint32_t NB = kWsRows / 16, KXM = kWsSteps - KH;
     static constexpr uint32_t frag = 1024;   // bytes of one 16 x 32 operand
-    static constexpr uint32_t xh = 0, xl = KXM * NB * frag, hh = 2 * KXM * NB * frag,
-                              hl = hh + KH * NB * frag, buf = hl + KH * NB * frag;
-    // output rows of a tile, row-major with a stride of the widest row
-    // (fp32, kd = 32 KH) plus 16 bytes against bank conflicts
-    static constexpr uint32_t ostride = 32 * KH * 4 + 16, ostage = kWsRows * ostride;
-    static constexpr uint32_t fixed = 2 * buf + 2 * ostage + 4 * kWsRows * 16;   // static LDS
+    // S: X hi steps [0, KH), H hi
+    static constexpr uint32_t sx = 0, sh = KH * NB * frag, s_bytes = 2 * KH * NB * frag;
+    // T: X hi steps [KH, KXM), X lo steps [0, KXM), H lo
+    static constexpr uint32_t tx = 0, tl = (KXM - KH) * NB * frag, th = tl + KXM * NB * frag,
+                              t_bytes = th + KH * NB * frag;
+    // output rows of a tile, row-major with a stride of the row plus 16
+    // bytes against bank conflicts (at most fp32, kd = 32 KH)
+    static constexpr uint32_t ostage = kWsRows * (32 * KH * 4 + 16);
+    static constexpr uint32_t slots = 8;
+    static constexpr uint32_t fixed = 2 * (s_bytes + t_bytes) + 2 * ostage + slots * 1024 + 4 * 32 * KH * 4;
 };
 
 // Byte offset of the eight values at row j, columns c .. c + 7 (c % 8 == 0)
@@ -698,24 +706,43 @@ __device__ __forceinline__ uint32_t opaque_u32(uint32_t x) {
 
 typedef __attribute__((address_space(3))) void *lds_ptr;
 
+// One direct global-to-LDS load of 16 bytes per lane: lane l's bytes from g
+// land at LDS byte address lds + 16 l (lds uniform).  Written as assembly so
+// that the compiler does not make later LDS accesses wait for it (it cannot
+// tell which LDS array such a load writes); the caller waits for it
+// (vmcnt) before the workgroup barrier that publishes the data.
+__device__ __forceinline__ void lds_load16(const void *g, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(g) : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void *p) { return (uint32_t)(uintptr_t)(lds_ptr)p; }
+
 template <int KH, int MODE>
 __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     using L = WsLayout<KH>;
-    constexpr uint32_t NB = L::NB, R = kWsRows, T = 128 * KH, GH = 4 * KH, FB = L::frag;
+    constexpr uint32_t NB = L::NB, R = kWsRows, T = 128 * KH, TB = T / 2, GH = 4 * KH, FB = L::frag;
     constexpr int KXM = (int)L::KXM, KS = KXM + KH;
     constexpr int SK = MODE == kWsF32 ? kF32Vec : kBf16Vec;
     static_assert(R * GH == T, "one status piece of each input half per thread");
     static_assert(2 * KH == KH * NB, "one operand fragment of each input half per wavefront");
-    __shared__ __attribute__((aligned(16))) uint8_t buf0[L::buf];
-    __shared__ __attribute__((aligned(16))) uint8_t buf1[L::buf];
-    __shared__ __attribute__((aligned(16))) uint8_t ost0[L::ostage];
-    __shared__ __attribute__((aligned(16))) uint8_t ost1[L::ostage];
-    __shared__ u32x4 meta[4 * R];   // 4 slots x R: {pair row, self, other, 0}; tile i in slot i % 4
+    __shared__ __attribute__((aligned(16))) uint8_t bs0[L::s_bytes];
+    __shared__ __attribute__((aligned(16))) uint8_t bs1[L::s_bytes];
+    __shared__ __attribute__((aligned(16))) uint8_t bt0[L::t_bytes];
+    __shared__ __attribute__((aligned(16))) uint8_t bt1[L::t_bytes];
+    constexpr uint32_t OSTR = 32 * KH * (MODE == kWsF32 ? 4 : 2) + 16;   // staging row stride
+    __shared__ __attribute__((aligned(16))) uint8_t ost0[R * OSTR];
+    __shared__ __attribute__((aligned(16))) uint8_t ost1[R * OSTR];
+    // Row lists {pair row, self, other, 0} of 1 KB slots (R entries and room
+    // for the duplicates a direct load of R entries writes); tile i in slot i % 8.
+    constexpr uint32_t MS = 64;
+    __shared__ __attribute__((aligned(16))) u32x4 meta[L::slots * MS];
     extern __shared__ __attribute__((aligned(16))) float s_tw[];   // T-enc w | b, pad32(d_time) each
     float *s_tb = s_tw + ((p.d_time + 31u) & ~31u);
 
     const uint32_t tid = threadIdx.x, lane = tid & 63;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const bool second = wave >= (uint32_t)KH;   // shares its SIMD with wavefront wave - KH
     const uint32_t lr = lane & 15, lk = (lane >> 4) * 8;
     const uint32_t count = *p.count;
     const uint32_t tiles = (uint32_t)(((uint64_t)count + R - 1) / R);
@@ -738,77 +765,106 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
 #pragma unroll
         for (int g = 0; g < 3; g++)
             bh[s][g] = *(const bf16x8 *)(p.w_hh + ((size_t)g * d + jr) * p.kd + 32 * s + lk);
-    // Gate biases, those of r and z pre-scaled for the base-2 exponential.
-    const float nbr = -kLog2e * (p.b_ih[jr] + p.b_hh[jr]);
-    const float nbz = -kLog2e * (p.b_ih[d + jr] + p.b_hh[d + jr]);
-    const float bin = p.b_ih[2 * d + jr];
-    const float bhn = p.b_hh[2 * d + jr];
+    // Gate biases by output unit (LDS, read per tile): those of r and z
+    // pre-scaled for the base-2 exponential, then the input and hidden
+    // biases of n.
+    __shared__ float sbias[4][32 * KH];
+    if (lane < 16 && mma) {
+        sbias[0][j] = -kLog2e * (p.b_ih[jr] + p.b_hh[jr]);
+        sbias[1][j] = -kLog2e * (p.b_ih[d + jr] + p.b_hh[d + jr]);
+        sbias[2][j] = p.b_ih[2 * d + jr];
+        sbias[3][j] = p.b_hh[2 * d + jr];
+    }
 
-    auto list_entry = [&](uint32_t tl) __attribute__((always_inline)) {
-        return p.list[min((uint64_t)tl * R + (tid & (R - 1)), (uint64_t)count - 1)];
+    auto list_at = [&](uint32_t tl, uint32_t row) __attribute__((always_inline)) {
+        return min((uint64_t)tl * R + row, (uint64_t)count - 1);
     };
 
     // Register path: a thread's status pieces, f = 0 of H (self) and f = 1
-    // of X's r_other, both at tile row pj, columns pc0 .. pc0 + 7
-    // (operand-order offset po).  Direct path: wavefront w's operand
-    // fragment w of H and of X's r_other, lane l at tile row dj, column dc.
-    // Both: the thread's first time-encoding unit (row tj, encoding columns
-    // tk .. tk + 7, offset to) and that row's link time.
-    const uint32_t pj = tid / GH, pc0 = 8 * (tid % GH), po = frag_off(pj, pc0);
+    // of X's r_other, both at tile row pj, columns pc0 .. pc0 + 7.  Direct
+    // path: wavefront w's operand fragment w of H and of X's r_other, lane l
+    // at tile row dj, column dc.
+    const uint32_t pj = tid / GH, pc0 = 8 * (tid % GH);
     const uint32_t dj = 16 * (wave % NB) + lr, dc = 32 * (wave / NB) + lk;
-    const uint32_t tu0 = min(tid, tu - 1u);
-    const uint32_t tj = div_small(tu0, p.gt_m), tk = (tu0 - tj * gt) * 8u, to = frag_off(tj, p.kd + tk);
     Piece8<SK> pc[2];
-    uint32_t t0 = 0;   // converted where used: a conversion here would wait for the loads
-    auto request_tile = [&](uint8_t *nb, uint32_t slot) __attribute__((always_inline)) {
+    auto request_tile = [&](uint8_t *nbS, uint32_t slot) __attribute__((always_inline)) {
         if constexpr (MODE == kWsBf16Dma) {
-            const u32x4 e = meta[slot * R + dj];
-            __builtin_amdgcn_global_load_lds(p.st + (size_t)e[1] * p.srb + 2u * dc, (lds_ptr)(nb + L::hh + wave * FB),
-                                             16, 0, 0);
-            __builtin_amdgcn_global_load_lds(p.st + (size_t)e[2] * p.srb + 2u * dc, (lds_ptr)(nb + L::xh + wave * FB),
-                                             16, 0, 0);
+            const u32x4 e = meta[slot * MS + dj];
+            lds_load16(p.st + (size_t)e[1] * p.srb + 2u * dc, lds_addr(nbS + L::sh + wave * FB));
+            lds_load16(p.st + (size_t)e[2] * p.srb + 2u * dc, lds_addr(nbS + L::sx + wave * FB));
         } else {
-            const u32x4 e = meta[slot * R + pj];
+            const u32x4 e = meta[slot * MS + pj];
             load_piece<SK>(p.st + (size_t)e[1] * p.srb, d, pc0, pc[0]);
             load_piece<SK>(p.st + (size_t)e[2] * p.srb, d, pc0, pc[1]);
         }
-        t0 = p.t[meta[slot * R + tj][0] >> 1];
     };
-    auto tenc_unit = [&](uint8_t *nb, uint32_t off, uint32_t k, float tf) __attribute__((always_inline)) {
+
+    // Time-encoding unit u of a tile: row u / gt, encoding columns k .. k + 7
+    // (X columns kd + k ..), from the row's link time tf.
+    // Time-encoding unit u of a tile: lane l = u % 64 of operand fragment
+    // f = u / 64 of the encoding's steps (step f / NB, row block f % NB), i.e.
+    // tile row 16 (f % NB) + l % 16 and encoding columns 32 (f / NB) +
+    // 8 (l / 16) .. + 7, so that its eight values sit at byte 16 u of their
+    // plane (a wavefront's writes are contiguous).  Arguments beyond the fast
+    // cosine's range are rare: their units are redone, exactly, only where a
+    // wavefront meets one.
+    auto unit_row = [](uint32_t u) { return 16u * ((u >> 6) % NB) + (u & 15u); };
+    auto unit_col = [](uint32_t u) { return 32u * ((u >> 6) / NB) + 8u * ((u >> 4) & 3u); };
+    auto tenc_unit = [&](uint8_t *nbT, uint32_t u, float tf) __attribute__((always_inline)) {
+        const uint32_t k = unit_col(u);
         const f32x4 w0 = *(const f32x4 *)(s_tw + k), w1 = *(const f32x4 *)(s_tw + k + 4);
         const f32x4 b0 = *(const f32x4 *)(s_tb + k), b1 = *(const f32x4 *)(s_tb + k + 4);
-        float v[8];
+        float x[8], v[8];
+        bool wide = false;
 #pragma unroll
         for (int i = 0; i < 4; i++) {
-            v[i] = cos_fp32(__builtin_fmaf(w0[i], tf, b0[i]));
-            v[4 + i] = cos_fp32(__builtin_fmaf(w1[i], tf, b1[i]));
+            x[i] = __builtin_fmaf(w0[i], tf, b0[i]);
+            x[4 + i] = __builtin_fmaf(w1[i], tf, b1[i]);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; i++) {
+            v[i] = cos_fp32_small(x[i]);
+            wide |= !(__builtin_fabsf(x[i]) < kCosFastLimit);
+        }
+        if (__builtin_expect(__ballot(wide) != 0, 0)) {
+#pragma unroll
+            for (int i = 0; i < 8; i++)
+                if (!(__builtin_fabsf(x[i]) < kCosFastLimit)) v[i] = cos_fp32_exact_wide(x[i]);
         }
 #pragma unroll
         for (int i = 0; i < 8; i++) v[i] = k + i < p.d_time ? v[i] : 0.0f;
-        store_split8(v, (__bf16 *)(nb + L::xh + off), (__bf16 *)(nb + L::xl + off));
+        store_split8(v, (__bf16 *)(nbT + L::tx + 16u * u), (__bf16 *)(nbT + L::tl + KH * NB * FB + 16u * u));
     };
-    auto write_tile = [&](uint8_t *nb, uint32_t slot) __attribute__((always_inline)) {
+    // A thread's time-encoding unit u = tid of every tile (if u < tu), with
+    // the link time of its row for the tile whose encoding it computes next.
+    uint32_t tB = 0;
+    auto t_row = [&](uint32_t tl, uint32_t u) __attribute__((always_inline)) {
+        return ((const uint32_t *)p.list)[4 * list_at(tl, unit_row(min(u, tu - 1u)))];
+    };
+
+    // What is written after the products: status pieces on the register
+    // path, time-encoding units the second half does not cover (u >= T) and
+    // link rows.
+    auto write_tile = [&](uint8_t *nbS, uint8_t *nbT, uint32_t slot) __attribute__((always_inline)) {
+        const uint32_t po = frag_off(pj, pc0);
         if constexpr (MODE == kWsF32) {
             float v[8];
             piece_floats<SK>(pc[0], d, pc0, true, v);
-            store_split8(v, (__bf16 *)(nb + L::hh + po), (__bf16 *)(nb + L::hl + po));
+            store_split8(v, (__bf16 *)(nbS + L::sh + po), (__bf16 *)(nbT + L::th + po));
             piece_floats<SK>(pc[1], d, pc0, true, v);
-            store_split8(v, (__bf16 *)(nb + L::xh + po), (__bf16 *)(nb + L::xl + po));   // lo_begin == 0
+            store_split8(v, (__bf16 *)(nbS + L::sx + po), (__bf16 *)(nbT + L::tl + po));   // lo_begin == 0
         } else if constexpr (MODE == kWsBf16) {
-            *(u32x4 *)(nb + L::hh + po) = piece_bf16_bits<SK>(pc[0], d, pc0, true);
-            *(u32x4 *)(nb + L::xh + po) = piece_bf16_bits<SK>(pc[1], d, pc0, true);
+            *(u32x4 *)(nbS + L::sh + po) = piece_bf16_bits<SK>(pc[0], d, pc0, true);
+            *(u32x4 *)(nbS + L::sx + po) = piece_bf16_bits<SK>(pc[1], d, pc0, true);
         }
-        if (tid < tu) tenc_unit(nb, to, tk, (float)t0);
-        for (uint32_t u = tid + T; u < tu; u += T) {
-            const uint32_t jj = div_small(u, p.gt_m), k = (u - jj * gt) * 8u;
-            tenc_unit(nb, frag_off(jj, p.kd + k), k, (float)p.t[meta[slot * R + jj][0] >> 1]);
-        }
+        for (uint32_t u = tid + T; u < tu; u += T)
+            tenc_unit(nbT, u, (float)p.t[meta[slot * MS + unit_row(u)][0] >> 1]);
         if (p.kx > p.off_e) {
             const uint32_t ge = (p.kx - p.off_e) / 8;
             auto edge_fill = [&](auto kind) __attribute__((always_inline)) {
                 constexpr int K = decltype(kind)::value;
                 auto eid_of = [&](uint32_t jj) __attribute__((always_inline)) {
-                    return p.first_eid + (meta[slot * R + jj][0] >> 1);
+                    return p.first_eid + (meta[slot * MS + jj][0] >> 1);
                 };
                 fill_seg<K, 4, T>(
                     R * ge, ge, p.ge_m, p.e_dim,
@@ -818,13 +874,14 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
                     },
                     [&](uint32_t jj, uint32_t c0, const Piece8<K> &q) __attribute__((always_inline)) {
                         const bool ok = eid_of(jj) < (uint64_t)p.edge_rows;
-                        const uint32_t off = frag_off(jj, p.off_e + c0);
+                        const uint32_t c = p.off_e + c0;
+                        __bf16 *hi = (__bf16 *)(nbT + L::tx + frag_off(jj, c - p.kd));
                         if constexpr (K == kF32Vec) {
                             float v[8];
                             piece_floats<K>(q, p.e_dim, c0, ok, v);
-                            store_split8(v, (__bf16 *)(nb + L::xh + off), (__bf16 *)(nb + L::xl + off));
+                            store_split8(v, hi, (__bf16 *)(nbT + L::tl + frag_off(jj, c)));
                         } else {
-                            *(u32x4 *)(nb + L::xh + off) = piece_bf16_bits<K>(q, p.e_dim, c0, ok);
+                            *(u32x4 *)hi = piece_bf16_bits<K>(q, p.e_dim, c0, ok);
                         }
                     });
             };
@@ -837,14 +894,17 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
         }
     };
     // Direct loads into LDS count as outstanding vector-memory operations:
-    // all of this wavefront's must have landed before the workgroup barrier.
+    // all of this wavefront's must have landed before the workgroup barrier
+    // (the compiler does not know of them).
     auto tile_barrier = [&]() __attribute__((always_inline)) {
-        if constexpr (MODE == kWsBf16Dma) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), seen by the compiler's own wait tracking
         __syncthreads();
     };
 
     // Prologue: time-encoding parameters, row lists of the first two tiles,
-    // the first tile's inputs.
+    // the first tile's inputs (its whole time encoding), the link times of
+    // the second tile's encoding.
     for (uint32_t u = tid; u < ((p.d_time + 31u) & ~31u); u += T) {
         s_tw[u] = u < p.d_time ? p.tw[u] : 0.0f;
         s_tb[u] = u < p.d_time ? p.tb[u] : 0.0f;
@@ -852,44 +912,62 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     const uint32_t stride = gridDim.x;
     uint32_t tl = blockIdx.x;
     {
-        const u32x4 e0 = list_entry(tl), e1 = list_entry(tl + stride < tiles ? tl + stride : tl);
+        const uint32_t t1 = tl + stride < tiles ? tl + stride : tl;
+        const u32x4 e0 = p.list[list_at(tl, tid & (R - 1))], e1 = p.list[list_at(t1, tid & (R - 1))];
         if (tid < R) {
             meta[tid] = e0;
-            meta[R + tid] = e1;
+            meta[MS + tid] = e1;
         }
+        tB = p.t[t_row(t1, tid) >> 1];
     }
     __syncthreads();
-    request_tile(buf0, 0);
-    write_tile(buf0, 0);
+    request_tile(bs0, 0);
+    write_tile(bs0, bt0, 0);
+    for (uint32_t u = tid; u < tu && u < T; u += T)
+        tenc_unit(bt0, u, (float)p.t[meta[unit_row(u)][0] >> 1]);
     tile_barrier();
 
     // Candidate rows of tile tlp (row-list slot `slot`) from its staging
     // area, 16 bytes per thread and step.
     auto copy_out = [&](const uint8_t *ob, uint32_t slot, uint32_t tlp) __attribute__((always_inline)) {
+        constexpr uint32_t CO = MODE == kWsF32 ? 2 : 1;   // >= R * (kd * element size / 16) / T
         const uint32_t cpr = p.srb / 16, units = min(R, count - tlp * R) * cpr;
-        for (uint32_t u = tid; u < units; u += T) {
-            const uint32_t row = div_small(u, p.ws_cpr_m), c = 16u * (u - row * cpr);
-            const u32x4 v = *(const u32x4 *)(ob + row * L::ostride + c);
-            *(u32x4 *)(p.cand + (size_t)meta[slot * R + row][0] * p.srb + c) = v;
+#pragma unroll
+        for (uint32_t k = 0; k < CO; k++) {
+            const uint32_t u = tid + k * T;
+            if (u < units) {
+                const uint32_t row = div_small(u, p.ws_cpr_m), c = 16u * (u - row * cpr);
+                const u32x4 v = *(const u32x4 *)(ob + row * OSTR + c);
+                *(u32x4 *)(p.cand + (size_t)meta[slot * MS + row][0] * p.srb + c) = v;
+            }
         }
     };
 
-    // One tile: products from cb (row-list slot i % 4) while the next tile
-    // arrives in nb; new statuses to ob, those of the previous tile out of
-    // obp; false after the workgroup's last tile.
-    auto tile = [&](uint8_t *cb, uint8_t *nb, uint8_t *ob, const uint8_t *obp, uint32_t i)
-                    __attribute__((always_inline)) {
-        const uint32_t ms = i & 3, ns = (i + 1) & 3;
+    // One tile: products from (cbS, cbT) (row-list slot i % 8) while the
+    // next tile arrives in (nbS, nbT); new statuses to ob, those of the
+    // previous tile out of obp; false after the workgroup's last tile.
+    auto tile = [&](uint8_t *cbS, uint8_t *cbT, uint8_t *nbS, uint8_t *nbT, uint8_t *ob, const uint8_t *obp,
+                    uint32_t i) __attribute__((always_inline)) {
+        const uint32_t ms = i & 7, ns = (i + 1) & 7;
         const bool has_next = tl + stride < tiles, has_nn = tl + 2 * stride < tiles;
-        // Row list of the tile two strides on and status rows of the next tile
-        // (re-reads of the current tile's when there is none: in bounds, unused).
-        const u32x4 e_nn = list_entry(has_nn ? tl + 2 * stride : tl);
-        if (MODE != kWsBf16Dma || has_next) request_tile(nb, has_next ? ns : ms);
-        if (i > 0) copy_out(obp, (i - 1) & 3, tl - stride);
+        const uint32_t tnn = has_nn ? tl + 2 * stride : tl;
+        // Row list of the tile two strides on (straight into its slot; the
+        // list rows of the threads' encoding units too) and status rows of the
+        // next tile (re-reads of the current tile's when there is none: in
+        // bounds, unused).
+        if (has_nn && wave == 0)
+            lds_load16(p.list + list_at(tnn, lane & (R - 1)), lds_addr(meta + ((i + 2) & 7) * MS));
+        const uint32_t rB = t_row(tnn, tid);
+        if (MODE != kWsBf16Dma || has_next) request_tile(nbS, has_next ? ns : ms);
+        if (i > 0) copy_out(obp, (i - 1) & 7, tl - stride);
+        // The second half encodes its units of the next tile now, the first
+        // half after its products.
+        const float tf = (float)tB;
+        if (second && has_next && tid < tu) tenc_unit(nbT, tid, tf);
+        f32x4 acc[4][NB];   // r, z, input part of n, hidden part of n
         if (mma) {
             const uint32_t lm = opaque_u32(p.ws_lomask), ks = opaque_u32(kx_steps);
-            const uint8_t *b = cb + 16u * lane;
-            f32x4 acc[4][NB];   // r, z, input part of n, hidden part of n
+            const uint8_t *bS = cbS + 16u * lane, *bT = cbT + 16u * lane;
 #pragma unroll
             for (int g = 0; g < 4; g++)
 #pragma unroll
@@ -903,30 +981,43 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
                         acc[gi][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], w[g], acc[gi][rb], 0, 0, 0);
                     }
             };
-            // Operands of step s (X steps, then H steps) into a / al: the hi
-            // plane always, the lo plane where the step has one.
+            // Operands of step s (X steps, then H steps): the hi plane
+            // always, the lo plane where the step has one; those of step
+            // s + 1 are read before the products of step s.
             auto load_step = [&](int s, bf16x8 (&a)[NB], bf16x8 (&al)[NB]) __attribute__((always_inline)) {
-                const uint32_t ph = s < KXM ? L::xh + s * NB * FB : L::hh + (s - KXM) * NB * FB;
-                const uint32_t pl = s < KXM ? L::xl + s * NB * FB : L::hl + (s - KXM) * NB * FB;
+                const uint8_t *hi = s < KH ? bS + L::sx + s * NB * FB
+                                  : s < KXM ? bT + L::tx + (s - KH) * NB * FB : bS + L::sh + (s - KXM) * NB * FB;
+                const uint8_t *lo = s < KXM ? bT + L::tl + s * NB * FB : bT + L::th + (s - KXM) * NB * FB;
 #pragma unroll
-                for (int rb = 0; rb < NB; rb++) a[rb] = *(const bf16x8 *)(b + ph + rb * FB);
+                for (int rb = 0; rb < NB; rb++) a[rb] = *(const bf16x8 *)(hi + rb * FB);
                 if (s < KXM ? ((lm >> s) & 1u) != 0 : MODE == kWsF32) {
 #pragma unroll
-                    for (int rb = 0; rb < NB; rb++) al[rb] = *(const bf16x8 *)(b + pl + rb * FB);
+                    for (int rb = 0; rb < NB; rb++) al[rb] = *(const bf16x8 *)(lo + rb * FB);
                 }
             };
+            bf16x8 a[2][NB], al[NB];
+            load_step(0, a[0], al);
 #pragma unroll
             for (int s = 0; s < KS; s++) {
-                bf16x8 a[NB], al[NB];
-                load_step(s, a, al);
+                bf16x8 nal[NB];
+                if (s + 1 < KS) load_step(s + 1, a[(s + 1) & 1], nal);
                 if (s < KXM) {
-                    if ((uint32_t)s < ks) mfma3(a, bx[s], 2);
+                    if ((uint32_t)s < ks) mfma3(a[s & 1], bx[s], 2);
                     if ((lm >> s) & 1u) mfma3(al, bx[s], 2);
                 } else {
-                    mfma3(a, bh[s - KXM], 3);
+                    mfma3(a[s & 1], bh[s - KXM], 3);
                     if constexpr (MODE == kWsF32) mfma3(al, bh[s - KXM], 3);
                 }
+#pragma unroll
+                for (int rb = 0; rb < NB; rb++) al[rb] = nal[rb];
             }
+        }
+        // Link times of the second half's next units, read while the gates
+        // are applied (kept after the products: their addresses come from
+        // loads issued with the direct ones, which a wait here would cover).
+        __builtin_amdgcn_sched_barrier(0);
+        tB = p.t[rB >> 1];
+        if (mma) {
             float hv[NB][4];
 #pragma unroll
             for (int rb = 0; rb < NB; rb++)
@@ -934,11 +1025,12 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
                 for (int q = 0; q < 4; q++) {
                     const uint32_t row = 16u * rb + 4u * (lane >> 4) + q;
                     if constexpr (MODE == kWsF32)
-                        hv[rb][q] = ((const float *)(p.st + (size_t)meta[ms * R + row][1] * p.srb))[jr];
+                        hv[rb][q] = ((const float *)(p.st + (size_t)meta[ms * MS + row][1] * p.srb))[jr];
                     else
-                        hv[rb][q] = (float)*(const __bf16 *)(cb + L::hh + frag_off(row, jr & ~7u) + 2u * (jr & 7u));
+                        hv[rb][q] = (float)*(const __bf16 *)(cbS + L::sh + frag_off(row, jr & ~7u) + 2u * (jr & 7u));
                 }
             if (j < d) {
+                const float nbr = sbias[0][j], nbz = sbias[1][j], bin = sbias[2][j], bhn = sbias[3][j];
 #pragma unroll
                 for (int rb = 0; rb < NB; rb++)
 #pragma unroll
@@ -951,25 +1043,25 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
                         const float ng = tanh_f32(__builtin_fmaf(rg, acc[3][rb][q] + bhn, acc[2][rb][q] + bin));
                         const float out = __builtin_fmaf(zg, hv[rb][q] - ng, ng);   // (1 - z) n + z h
                         if constexpr (MODE == kWsF32)
-                            ((float *)(ob + row * L::ostride))[j] = out;
+                            ((float *)(ob + row * OSTR))[j] = out;
                         else
-                            ((__bf16 *)(ob + row * L::ostride))[j] = (__bf16)out;   // round to nearest even
+                            ((__bf16 *)(ob + row * OSTR))[j] = (__bf16)out;   // round to nearest even
                     }
             }
         }
-        if (has_next) write_tile(nb, ns);
-        if (has_nn && tid < R) meta[((i + 2) & 3) * R + tid] = e_nn;
+        if (!second && has_next && tid < tu) tenc_unit(nbT, tid, tf);
+        if (has_next) write_tile(nbS, nbT, ns);
         tile_barrier();
         tl += stride;
         return has_next;
     };
     for (uint32_t i = 0;; i += 2) {
-        if (!tile(buf0, buf1, ost0, ost1, i)) {
-            copy_out(ost0, i & 3, tl - stride);
+        if (!tile(bs0, bt0, bs1, bt1, ost0, ost1, i)) {
+            copy_out(ost0, i & 7, tl - stride);
             break;
         }
-        if (!tile(buf1, buf0, ost1, ost0, i + 1)) {
-            copy_out(ost1, (i + 1) & 3, tl - stride);
+        if (!tile(bs1, bt1, bs0, bt0, ost1, ost0, i + 1)) {
+            copy_out(ost1, (i + 1) & 7, tl - stride);
             break;
         }
     }
