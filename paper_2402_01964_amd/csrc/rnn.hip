@@ -752,29 +752,11 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     const uint32_t j = 16 * wave + lr, jr = j < d ? j : d - 1;
     const uint32_t gt = (p.off_e - p.kd) / 8, tu = R * gt;
 
-    // This wavefront's weight fragments and biases.
+    // This wavefront's weight fragments (loaded in the prologue, after the
+    // first tile's requests) and the gate biases by output unit (LDS, read
+    // per tile).
     bf16x8 bx[KXM][3], bh[KH][3];
-#pragma unroll
-    for (int s = 0; s < KXM; s++)
-#pragma unroll
-        for (int g = 0; g < 3; g++)
-            bx[s][g] = *(const bf16x8 *)(p.w_ih + ((size_t)g * d + jr) * p.kx +
-                                         32u * min((uint32_t)s, kx_steps - 1u) + lk);
-#pragma unroll
-    for (int s = 0; s < KH; s++)
-#pragma unroll
-        for (int g = 0; g < 3; g++)
-            bh[s][g] = *(const bf16x8 *)(p.w_hh + ((size_t)g * d + jr) * p.kd + 32 * s + lk);
-    // Gate biases by output unit (LDS, read per tile): those of r and z
-    // pre-scaled for the base-2 exponential, then the input and hidden
-    // biases of n.
     __shared__ float sbias[4][32 * KH];
-    if (lane < 16 && mma) {
-        sbias[0][j] = -kLog2e * (p.b_ih[jr] + p.b_hh[jr]);
-        sbias[1][j] = -kLog2e * (p.b_ih[d + jr] + p.b_hh[d + jr]);
-        sbias[2][j] = p.b_ih[2 * d + jr];
-        sbias[3][j] = p.b_hh[2 * d + jr];
-    }
 
     auto list_at = [&](uint32_t tl, uint32_t row) __attribute__((always_inline)) {
         return min((uint64_t)tl * R + row, (uint64_t)count - 1);
@@ -812,28 +794,35 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     auto unit_col = [](uint32_t u) { return 32u * ((u >> 6) / NB) + 8u * ((u >> 4) & 3u); };
     auto tenc_unit = [&](uint8_t *nbT, uint32_t u, float tf) __attribute__((always_inline)) {
         const uint32_t k = unit_col(u);
-        const f32x4 w0 = *(const f32x4 *)(s_tw + k), w1 = *(const f32x4 *)(s_tw + k + 4);
-        const f32x4 b0 = *(const f32x4 *)(s_tb + k), b1 = *(const f32x4 *)(s_tb + k + 4);
-        float x[8], v[8];
-        bool wide = false;
+        // two halves of four values (fewer registers live at once)
 #pragma unroll
-        for (int i = 0; i < 4; i++) {
-            x[i] = __builtin_fmaf(w0[i], tf, b0[i]);
-            x[4 + i] = __builtin_fmaf(w1[i], tf, b1[i]);
+        for (int h = 0; h < 2; h++) {
+            const f32x4 w = *(const f32x4 *)(s_tw + k + 4 * h), b = *(const f32x4 *)(s_tb + k + 4 * h);
+            float x[4], v[4];
+            bool wide = false;
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                x[e] = __builtin_fmaf(w[e], tf, b[e]);
+                v[e] = cos_fp32_small(x[e]);
+                wide |= !(__builtin_fabsf(x[e]) < kCosFastLimit);
+            }
+            if (__builtin_expect(__ballot(wide) != 0, 0)) {
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    if (!(__builtin_fabsf(x[e]) < kCosFastLimit)) v[e] = cos_fp32_exact_wide(x[e]);
+            }
+            u32x2 hi, lo;
+#pragma unroll
+            for (int e = 0; e < 4; e += 2) {
+                float a0 = k + 4 * h + e < p.d_time ? v[e] : 0.0f, a1 = k + 4 * h + e + 1 < p.d_time ? v[e + 1] : 0.0f;
+                const __bf16 h0 = (__bf16)a0, h1 = (__bf16)a1;
+                const __bf16 l0 = (__bf16)(a0 - (float)h0), l1 = (__bf16)(a1 - (float)h1);
+                hi[e / 2] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
+                lo[e / 2] = (uint32_t)__builtin_bit_cast(uint16_t, l0) | ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
+            }
+            *(u32x2 *)(nbT + L::tx + 16u * u + 8u * h) = hi;
+            *(u32x2 *)(nbT + L::tl + KH * NB * FB + 16u * u + 8u * h) = lo;
         }
-#pragma unroll
-        for (int i = 0; i < 8; i++) {
-            v[i] = cos_fp32_small(x[i]);
-            wide |= !(__builtin_fabsf(x[i]) < kCosFastLimit);
-        }
-        if (__builtin_expect(__ballot(wide) != 0, 0)) {
-#pragma unroll
-            for (int i = 0; i < 8; i++)
-                if (!(__builtin_fabsf(x[i]) < kCosFastLimit)) v[i] = cos_fp32_exact_wide(x[i]);
-        }
-#pragma unroll
-        for (int i = 0; i < 8; i++) v[i] = k + i < p.d_time ? v[i] : 0.0f;
-        store_split8(v, (__bf16 *)(nbT + L::tx + 16u * u), (__bf16 *)(nbT + L::tl + KH * NB * FB + 16u * u));
     };
     // A thread's time-encoding unit u = tid of every tile (if u < tu), with
     // the link time of its row for the tile whose encoding it computes next.
@@ -902,9 +891,12 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
         __syncthreads();
     };
 
-    // Prologue: time-encoding parameters, row lists of the first two tiles,
-    // the first tile's inputs (its whole time encoding), the link times of
-    // the second tile's encoding.
+    // Prologue, ordered so that the weights' transfer (about 300 KB per CU,
+    // from L2) overlaps the first tile's dependent loads: time-encoding
+    // parameters, row lists of the first two tiles and the list rows of the
+    // second tile's encoding units; then the first tile's status rows and
+    // the link times of both tiles' encoding units; then the weights and
+    // biases; then the first tile's encoding and barrier.
     for (uint32_t u = tid; u < ((p.d_time + 31u) & ~31u); u += T) {
         s_tw[u] = u < p.d_time ? p.tw[u] : 0.0f;
         s_tb[u] = u < p.d_time ? p.tb[u] : 0.0f;
@@ -914,17 +906,39 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     {
         const uint32_t t1 = tl + stride < tiles ? tl + stride : tl;
         const u32x4 e0 = p.list[list_at(tl, tid & (R - 1))], e1 = p.list[list_at(t1, tid & (R - 1))];
+        const uint32_t r1 = t_row(t1, tid);
         if (tid < R) {
             meta[tid] = e0;
             meta[MS + tid] = e1;
         }
-        tB = p.t[t_row(t1, tid) >> 1];
+        tB = r1;
     }
     __syncthreads();
     request_tile(bs0, 0);
+    const uint32_t t_first = p.t[meta[unit_row(min(tid, tu - 1u))][0] >> 1];
+    tB = p.t[tB >> 1];
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s < KXM; s++)
+#pragma unroll
+        for (int g = 0; g < 3; g++)
+            bx[s][g] = *(const bf16x8 *)(p.w_ih + ((size_t)g * d + jr) * p.kx +
+                                         32u * min((uint32_t)s, kx_steps - 1u) + lk);
+#pragma unroll
+    for (int s = 0; s < KH; s++)
+#pragma unroll
+        for (int g = 0; g < 3; g++)
+            bh[s][g] = *(const bf16x8 *)(p.w_hh + ((size_t)g * d + jr) * p.kd + 32 * s + lk);
+    if (lane < 16 && mma) {
+        // r and z biases pre-scaled for the base-2 exponential, then the
+        // input and hidden biases of n
+        sbias[0][j] = -kLog2e * (p.b_ih[jr] + p.b_hh[jr]);
+        sbias[1][j] = -kLog2e * (p.b_ih[d + jr] + p.b_hh[d + jr]);
+        sbias[2][j] = p.b_ih[2 * d + jr];
+        sbias[3][j] = p.b_hh[2 * d + jr];
+    }
     write_tile(bs0, bt0, 0);
-    for (uint32_t u = tid; u < tu && u < T; u += T)
-        tenc_unit(bt0, u, (float)p.t[meta[unit_row(u)][0] >> 1]);
+    if (tid < tu) tenc_unit(bt0, tid, (float)t_first);
     tile_barrier();
 
     // Candidate rows of tile tlp (row-list slot `slot`) from its staging
