@@ -580,7 +580,6 @@ int nlb_destroy(nlb_table *h) {
         if (hipFree(h->blocks) != hipSuccess) rc = NLB_EDEVICE;
         if (h->rnn_winner && hipFree(h->rnn_winner) != hipSuccess) rc = NLB_EDEVICE;
         if (h->rnn_cand && hipFree(h->rnn_cand) != hipSuccess) rc = NLB_EDEVICE;
-        if (h->rnn_cand_node && hipFree(h->rnn_cand_node) != hipSuccess) rc = NLB_EDEVICE;
         if (h->rnn_list && hipFree(h->rnn_list) != hipSuccess) rc = NLB_EDEVICE;
     }
     delete h;

@@ -286,7 +286,6 @@ struct nlb_table {
     int32_t rnn_form;                 // GRU pass of the last update (NLB_RNN_FORM_*)
     uint8_t *rnn_cand;                // candidate status rows by pair row
     size_t rnn_cand_bytes;
-    int32_t *rnn_cand_node;           // winner node per pair row, else -1
     uint32_t *rnn_list;               // winner count, then the winners' pair rows
     uint64_t rnn_cand_rows;
 };

@@ -21,12 +21,17 @@
 //            to a dense list (one atomic per wavefront).  The list order
 //            varies from run to run; the results do not, because every row
 //            of a matrix product depends on its own inputs only.
-//   gru      a workgroup takes a tile of 16, 32 or 64 listed rows, builds
-//            their inputs in LDS and runs both GRU products on bf16 matrix
-//            cores; the gates, the blend with h and the rounding to the
-//            status type happen in registers, and the new status goes to a
-//            candidate buffer indexed by pair row.
-//   scatter  copies each winner's candidate row over its node's status.
+//   gru      where its registers suffice, the weight-stationary form
+//            (rnn_gru_ws: one workgroup per CU keeps the weights in
+//            registers and loops over 32-row tiles of listed rows);
+//            otherwise a workgroup takes a tile of 16, 32 or 64 listed rows
+//            and reads the weights from L2 (rnn_gru).  Both build the inputs
+//            in LDS and run both GRU products on bf16 matrix cores; the
+//            gates, the blend with h and the rounding to the status type
+//            happen in registers, and the new status goes to a candidate
+//            buffer indexed by pair row.
+//   scatter  copies each listed winner's candidate row over its node's
+//            status.
 // The candidate buffer is what lets the gru pass read only pre-batch
 // statuses: no status is written until every workgroup has read its inputs.
 //
@@ -131,7 +136,6 @@ struct SelectParams {
     int64_t num_nodes;
     const unsigned long long *winner;
     uint64_t epoch_hi;
-    int32_t *cand_node;   // [2n]: winner node of pair row r, else -1
     u32x4 *list;          // winners, dense: {pair row, self, other, 0}
     uint32_t *count;
 };
@@ -180,7 +184,6 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_select(SelectParams p) {
                 other = (r & 1) ? u : v;
                 win = wv[q] == (p.epoch_hi | (r + 1));
             }
-            p.cand_node[r] = win ? self : -1;
         }
         const uint64_t mask = __ballot(win);
         if (mask == 0) continue;
@@ -216,7 +219,6 @@ struct GruParams {
     const uint8_t *st;                  // statuses [N][d]
     uint32_t s_bf16, srb, s_vec;
     uint8_t *cand;                      // [2n][srb] candidate rows by pair row
-    int32_t *cand_node;                 // [2n] node of a winning pair row, else -1
     uint32_t kd, off_e, kx;             // X = [r_other | T-enc | e]: columns [0,kd) [kd,off_e) [off_e,kx)
     uint32_t lo_begin, lo_end;          // X columns with a stored lo plane
     uint32_t h_lo;                      // fp32 statuses: H has a lo plane
@@ -721,7 +723,7 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p) { return (uint32_t)(
 template <int KH, int MODE>
 __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     using L = WsLayout<KH>;
-    constexpr uint32_t NB = L::NB, R = kWsRows, T = 128 * KH, TB = T / 2, GH = 4 * KH, FB = L::frag;
+    constexpr uint32_t NB = L::NB, R = kWsRows, T = 128 * KH, GH = 4 * KH, FB = L::frag;
     constexpr int KXM = (int)L::KXM, KS = KXM + KH;
     constexpr int SK = MODE == kWsF32 ? kF32Vec : kBf16Vec;
     static_assert(R * GH == T, "one status piece of each input half per thread");
@@ -1081,20 +1083,20 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     }
 }
 
-// Status rows of the winners: cand row r -> status row cand_node[r], in
-// units of `w` bytes (upr units per row), grid-stride.
-__global__ __launch_bounds__(kRnnThreads) void rnn_scatter(const uint8_t *cand, const int32_t *cand_node,
-                                                          uint8_t *st, uint64_t rows, uint32_t srb,
-                                                          uint32_t w, uint32_t upr) {
-    const uint64_t units = rows * upr;
-    for (uint64_t u = (uint64_t)blockIdx.x * kRnnThreads + threadIdx.x; u < units;
-         u += (uint64_t)gridDim.x * kRnnThreads) {
-        const uint64_t r = u / upr;
-        const int32_t node = cand_node[r];
-        if (node < 0) continue;
-        const uint32_t c = (uint32_t)(u - r * upr) * w;
-        const uint8_t *from = cand + r * srb + c;
-        uint8_t *to = st + (size_t)node * srb + c;
+// Status rows of the winners: for each listed winner {pair row r, node},
+// candidate row r -> status row node, in units of `w` bytes (upr units per
+// row).  A wavefront pass copies 64 >> lg rows (lg = ceil(log2 upr) <= 6),
+// or one row in passes of 64 units; wavefronts stride over the list.
+__global__ __launch_bounds__(kRnnThreads) void rnn_scatter(const uint8_t *cand, const u32x4 *list,
+                                                          const uint32_t *count, uint8_t *st, uint32_t srb,
+                                                          uint32_t w, uint32_t upr, uint32_t lg) {
+    const uint32_t n = *count, lane = threadIdx.x & 63;
+    const uint64_t gw = ((uint64_t)blockIdx.x * kRnnThreads + threadIdx.x) >> 6;
+    const uint64_t nw = ((uint64_t)gridDim.x * kRnnThreads) >> 6;
+    auto copy = [&](uint64_t k, uint32_t c) {
+        const u32x4 e = list[k];
+        const uint8_t *from = cand + (size_t)e[0] * srb + c * w;
+        uint8_t *to = st + (size_t)e[1] * srb + c * w;
         if (w == 16)
             *(u32x4 *)to = *(const u32x4 *)from;
         else if (w == 8)
@@ -1103,6 +1105,14 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_scatter(const uint8_t *cand, 
             *(uint32_t *)to = *(const uint32_t *)from;
         else
             *(uint16_t *)to = *(const uint16_t *)from;
+    };
+    if (lg <= 6) {
+        const uint32_t per = 64u >> lg, c = lane & ((1u << lg) - 1u);
+        for (uint64_t k = gw * per + (lane >> lg); k < n; k += nw * per)
+            if (c < upr) copy(k, c);
+    } else {
+        for (uint64_t k = gw; k < n; k += nw)
+            for (uint32_t c = lane; c < upr; c += 64) copy(k, c);
     }
 }
 
@@ -1139,22 +1149,18 @@ int rnn_reserve(nlb_table *h, uint64_t pair_rows, uint32_t srb) {
         // Earlier updates may still read the old buffers.
         if (hipDeviceSynchronize() != hipSuccess) return NLB_EDEVICE;
         (void)hipFree(h->rnn_cand);
-        (void)hipFree(h->rnn_cand_node);
         (void)hipFree(h->rnn_list);
         h->rnn_cand = nullptr;
-        h->rnn_cand_node = nullptr;
         h->rnn_list = nullptr;
         h->rnn_cand_bytes = 0;
         h->rnn_cand_rows = 0;
         // list: the winner count in word 0, the winners (4 words each) from word 64 on
         if (hipMalloc((void **)&h->rnn_cand, cbytes) != hipSuccess ||
-            hipMalloc((void **)&h->rnn_cand_node, (size_t)pair_rows * 4u) != hipSuccess ||
             hipMalloc((void **)&h->rnn_list, ((size_t)pair_rows * 4u + 64u) * 4u) != hipSuccess) {
             (void)hipGetLastError();
             (void)hipFree(h->rnn_cand);
-            (void)hipFree(h->rnn_cand_node);
             h->rnn_cand = nullptr;
-            h->rnn_cand_node = nullptr;
+            h->rnn_list = nullptr;
             return NLB_ENOMEM;
         }
         h->rnn_cand_bytes = cbytes;
@@ -1283,7 +1289,6 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     p.list = list;
     p.count = count;
     p.cand = h->rnn_cand;
-    p.cand_node = h->rnn_cand_node;
 
     ResolveParams rp = {src, dst, n, h->num_nodes, h->rnn_winner, epoch_hi, h->status, count};
     if (n >= kMergeMinBatch)
@@ -1292,7 +1297,7 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     else
         hipLaunchKernelGGL(rnn_resolve, dim3((n + kRnnThreads - 1) / kRnnThreads), dim3(kRnnThreads), 0,
                            (hipStream_t)stream, rp);
-    SelectParams sp = {src, dst, n, h->num_nodes, h->rnn_winner, epoch_hi, h->rnn_cand_node, list, count};
+    SelectParams sp = {src, dst, n, h->num_nodes, h->rnn_winner, epoch_hi, list, count};
     hipLaunchKernelGGL(rnn_select, dim3((unsigned)((pairs + kSelectRows - 1) / kSelectRows)),
                        dim3(kRnnThreads), 0, (hipStream_t)stream, sp);
     if (ws) {
@@ -1333,10 +1338,13 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
             break;
         }
     const uint32_t upr = p.srb / w;
-    const uint64_t blocks = (pairs * upr + kRnnThreads - 1) / kRnnThreads;
+    uint32_t lg = 0;
+    while ((1u << lg) < upr) lg++;
+    const uint64_t per = lg <= 6 ? 64u >> lg : 1u;                       // rows per wavefront pass
+    const uint64_t blocks = ((pairs + per - 1) / per * 64u + kRnnThreads - 1) / kRnnThreads;
     hipLaunchKernelGGL(rnn_scatter, dim3((unsigned)(blocks < 65536 ? blocks : 65536)),
                        dim3(kRnnThreads), 0, (hipStream_t)stream, (const uint8_t *)h->rnn_cand,
-                       (const int32_t *)h->rnn_cand_node, (uint8_t *)status, pairs, p.srb, w, upr);
+                       (const u32x4 *)list, (const uint32_t *)count, (uint8_t *)status, p.srb, w, upr, lg);
     if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
     return NLB_OK;
 }
