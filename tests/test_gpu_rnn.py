@@ -299,6 +299,31 @@ def test_rnn_out_of_range_link_is_skipped_and_flagged():
     assert g.status() == 0
 
 
+@pytest.mark.parametrize("d,dtype,form", [(128, "bf16", WS), (48, "f32", WS), (100, "bf16", TILED)])
+def test_rnn_batch_without_valid_links(d, dtype, form):
+    """A batch whose every link has an endpoint out of range has no winners:
+    each form of the GRU pass must write nothing (the weight-stationary
+    workgroups all find an empty list) and the batch is flagged."""
+    import torch
+    import paper_2402_01964_amd as nlb
+    rng = np.random.default_rng(d)
+    N, n = 500, 300
+    g, fw, fb = _small_table(N, d_time=20)
+    x = rng.standard_normal((N, d)).astype(np.float32)
+    st = feat_to_dev(synth._to_bf16_bits(x) if dtype == "bf16" else x, dtype)
+    W = synth.gru_weights_for(d, 20, 0, seed=3)
+    src = rng.integers(0, N, n).astype(np.int32)
+    dst = np.full(n, N, np.int32)            # every link out of range
+    t = np.arange(n, dtype=np.uint32)
+    pre = host_np(st).copy()
+    g.rnn_update(to_dev(src), to_dev(dst), to_dev(t), 0, _weights_dev(W), st)
+    torch.cuda.synchronize()
+    assert np.array_equal(host_np(st), pre)
+    assert g.info()["rnn_form"] == form
+    assert g.status() == nlb.NLB_ERANGE
+    assert g.status() == 0
+
+
 def test_rnn_argument_errors():
     import torch
     import paper_2402_01964_amd as nlb
