@@ -145,12 +145,13 @@ def insert_bytes(links):
     return links * (12 + 2 * (8 + 8 + 4))
 
 
-def cpu_baseline(w, budget_s, max_batches=400):
+def cpu_baseline(w, budget_s, max_batches=400, agg_weights=None):
     """The CPU oracle, single-threaded, over the first batches of the same
-    stream (sample then insert per batch) until the time budget is used.
-    Stream and feature rows are generated outside the timed region; the
-    oracle gathers rows from full-size host tables whose untouched rows stay
-    unmaterialised zero pages."""
+    stream (sample -- or, with agg_weights, the eq. (4) aggregation -- then
+    insert per batch) until the time budget is used.  Stream and feature
+    rows are generated outside the timed region; the oracle gathers rows from
+    full-size host tables whose untouched rows stay unmaterialised zero
+    pages."""
     import numpy as np
 
     import oracle
@@ -186,7 +187,10 @@ def cpu_baseline(w, budget_s, max_batches=400):
                 nf[new] = synth.host_feature_rows(w, "node", new)
                 filled[new] = True
         t0 = time.perf_counter()
-        o.sample(q, tq, fw, fb, ef, nf)
+        if agg_weights is None:
+            o.sample(q, tq, fw, fb, ef, nf)
+        else:
+            o.aggregate(q, tq, fw, fb, ef, nf, agg_weights)
         o.insert(src, dst, t)
         spent += time.perf_counter() - t0
         links += hi - lo
@@ -195,8 +199,53 @@ def cpu_baseline(w, budget_s, max_batches=400):
     return {"value": links / spent, "unit": "links/s", "cores": 1, "kind": "oracle",
             "queries_per_s": queries / spent, "seconds": spent,
             "sample": f"first {b} batches ({links} links, {queries} queries) of the same stream, "
-                      f"sample then insert per batch, one thread; early batches see emptier "
-                      f"tables than the GPU's timed window"}
+                      f"{'sample' if agg_weights is None else 'aggregate (eq. (4))'} then insert per "
+                      f"batch, one thread; early batches see emptier tables than the GPU's timed "
+                      f"window"}
+
+
+def cpu_rnn_baseline(w, first_batch, budget_s, max_batches=50, max_links=20000):
+    """The CPU oracle's node-status update (fp64 GRU), single-threaded, on the
+    batches the GPU times (from first_batch on; at most their first max_links
+    links each) until the time budget is used.  Each batch's endpoints are
+    renumbered onto a compact status array of its distinct nodes (the update
+    reads and writes only those rows); statuses, link rows and renumbering
+    are prepared outside the timed region."""
+    import numpy as np
+
+    import oracle
+    import synth
+    d, dt = synth.status_spec(w)
+    W = synth.gru_weights(w)
+    fw, fb = synth.time_params(w)
+    rng = np.random.default_rng(7000 + w.key)
+    links = updates = 0
+    spent = 0.0
+    b = first_batch
+    while b < min(w.batches, first_batch + max_batches) and spent < budget_s:
+        lo, hi = w.batch_range(b)
+        hi = min(hi, lo + max_links)
+        src, dst, t, _ = synth.host_links(w, lo, hi)
+        nodes, inv = np.unique(np.concatenate([src, dst]), return_inverse=True)
+        s_l, d_l = inv[:len(src)].astype(np.int32), inv[len(src):].astype(np.int32)
+        if w.node_dim and d == w.node_dim and dt == w.node_dtype:
+            st = synth.host_feature_rows(w, "node", nodes)
+        else:
+            x = rng.standard_normal((len(nodes), d)).astype(np.float32)
+            st = synth._to_bf16_bits(x) if dt == "bf16" else x
+        st = np.ascontiguousarray(st)
+        ef = synth.host_feature_rows(w, "edge", np.arange(lo, hi)) if w.edge_dim else None
+        t0 = time.perf_counter()
+        oracle.gru_update(st, s_l, d_l, t, 0, fw, fb, ef, W)
+        spent += time.perf_counter() - t0
+        links += hi - lo
+        updates += len(nodes)
+        b += 1
+    return {"value": links / spent, "unit": "links/s", "cores": 1, "kind": "oracle",
+            "node_updates_per_s": updates / spent, "seconds": spent,
+            "sample": f"batches {first_batch}..{b - 1} of the timed window, at most their first "
+                      f"{max_links} links ({links} links, {updates} node updates), one thread, "
+                      f"each batch's nodes on a compact status array"}
 
 
 def main():
@@ -433,7 +482,12 @@ def main():
         res["value_note"] = "value includes the node-status updates (--rnn)"
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(
+            w, args.cpu_seconds,
+            agg_weights=synth.agg_weights(w) if agg_w is not None else None)
+        if status is not None:
+            print("bench: timing the CPU oracle's status update", file=sys.stderr, flush=True)
+            res["rnn"]["cpu_baseline"] = cpu_rnn_baseline(w, start + W, args.cpu_seconds)
     print(json.dumps(res), flush=True)
 
 
