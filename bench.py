@@ -145,9 +145,10 @@ def insert_bytes(links):
     return links * (12 + 2 * (8 + 8 + 4))
 
 
-def cpu_baseline(w, budget_s, max_batches=400, agg_weights=None):
+def cpu_baseline(w, budget_s, max_batches=400, agg_weights=None, hop2=False):
     """The CPU oracle, single-threaded, over the first batches of the same
-    stream (sample -- or, with agg_weights, the eq. (4) aggregation -- then
+    stream (sample -- or, with agg_weights, the eq. (4) aggregation; with
+    hop2, also the second hop's ids over the first hop's neighbours -- then
     insert per batch) until the time budget is used.  Stream and feature
     rows are generated outside the timed region; the oracle gathers rows from
     full-size host tables whose untouched rows stay unmaterialised zero
@@ -187,10 +188,12 @@ def cpu_baseline(w, budget_s, max_batches=400, agg_weights=None):
                 nf[new] = synth.host_feature_rows(w, "node", new)
                 filled[new] = True
         t0 = time.perf_counter()
-        if agg_weights is None:
-            o.sample(q, tq, fw, fb, ef, nf)
-        else:
+        if agg_weights is not None:
             o.aggregate(q, tq, fw, fb, ef, nf, agg_weights)
+        else:
+            r1 = o.sample(q, tq, fw, fb, ef, nf)
+            if hop2:
+                o.sample_hop2(r1["nbr"], tq, want=("nbr", "eid", "ts"))
         o.insert(src, dst, t)
         spent += time.perf_counter() - t0
         links += hi - lo
@@ -199,7 +202,7 @@ def cpu_baseline(w, budget_s, max_batches=400, agg_weights=None):
     return {"value": links / spent, "unit": "links/s", "cores": 1, "kind": "oracle",
             "queries_per_s": queries / spent, "seconds": spent,
             "sample": f"first {b} batches ({links} links, {queries} queries) of the same stream, "
-                      f"{'sample' if agg_weights is None else 'aggregate (eq. (4))'} then insert per "
+                      f"{'aggregate (eq. (4))' if agg_weights is not None else 'sample, second hop' if hop2 else 'sample'} then insert per "
                       f"batch, one thread; early batches see emptier tables than the GPU's timed "
                       f"window"}
 
@@ -484,7 +487,7 @@ def main():
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(
             w, args.cpu_seconds,
-            agg_weights=synth.agg_weights(w) if agg_w is not None else None)
+            agg_weights=synth.agg_weights(w) if agg_w is not None else None, hop2=hop2_out is not None)
         if status is not None:
             print("bench: timing the CPU oracle's status update", file=sys.stderr, flush=True)
             res["rnn"]["cpu_baseline"] = cpu_rnn_baseline(w, start + W, args.cpu_seconds)
