@@ -473,7 +473,7 @@ def main():
         fl = rnn_flops(w, d_r, winners)
         rb = rnn_bytes(w, d_r, status.element_size(), links, winners)
         t_s = rnn_ms.sum() * 1e-3
-        res["rnn"] = {"kernels": "rnn_resolve(_merged) + rnn_gru + rnn_scatter",
+        res["rnn"] = {"kernels": "rnn_resolve(_merged) + rnn_select + rnn_gru_ws (or rnn_gru) + rnn_scatter",
                       "status": f"{d_r} x {str(status.dtype).replace('torch.', '')}",
                       "links_per_s": links / t_s, "node_updates_per_s": winners / t_s,
                       "ms_avg": float(rnn_ms.mean()), "updates_per_batch": winners / K,
