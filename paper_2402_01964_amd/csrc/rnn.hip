@@ -709,13 +709,15 @@ __device__ __forceinline__ uint32_t opaque_u32(uint32_t x) {
 typedef __attribute__((address_space(3))) void *lds_ptr;
 
 // One direct global-to-LDS load of 16 bytes per lane: lane l's bytes from g
-// land at LDS byte address lds + 16 l (lds uniform).  Written as assembly so
-// that the compiler does not make later LDS accesses wait for it (it cannot
-// tell which LDS array such a load writes); the caller waits for it
-// (vmcnt) before the workgroup barrier that publishes the data.
+// land at LDS byte address lds + 16 l (lds uniform, passed in M0, which the
+// compiler sets; the nop is the wait state a load through M0 needs after
+// M0 is written).  Written as assembly so that the compiler does not make
+// later LDS accesses wait for it (it cannot tell which LDS array such a load
+// writes); the caller waits for it (vmcnt) before the workgroup barrier that
+// publishes the data.
 __device__ __forceinline__ void lds_load16(const void *g, uint32_t lds) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(g) : "memory", "m0");
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(g), "{m0}"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
 }
 
 __device__ __forceinline__ uint32_t lds_addr(const void *p) { return (uint32_t)(uintptr_t)(lds_ptr)p; }
