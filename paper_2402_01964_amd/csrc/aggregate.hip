@@ -467,11 +467,32 @@ __device__ __forceinline__ float xor16_sum(float v) {
     return v;
 }
 
+// max(a, b) and max(x, 0) as medians with +inf: one instruction each for
+// non-NaN operands.  fmaxf on a value the compiler cannot prove canonical (a
+// lane permutation, a matrix-core result) first quiets a possible signalling
+// NaN, which costs a second instruction per value.  The +inf bound passes
+// through an empty asm statement: with a literal bound the compiler folds the
+// median back into fmaxf.
+__device__ __forceinline__ float opaque_inf() {
+    uint32_t u = 0x7F800000u;
+    asm("" : "+s"(u));
+    return __uint_as_float(u);
+}
+__device__ __forceinline__ float max2(float a, float b) { return __builtin_amdgcn_fmed3f(a, b, opaque_inf()); }
+__device__ __forceinline__ float relu(float x) { return __builtin_amdgcn_fmed3f(x, 0.0f, opaque_inf()); }
+
+// A lane permutation with no prior value: every lane of these four patterns
+// has a source lane, so none keeps its old contents.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
 __device__ __forceinline__ float xor16_max(float v) {
-    v = fmaxf(v, dpp<kDppSwap1>(v));
-    v = fmaxf(v, dpp<kDppSwap2>(v));
-    v = fmaxf(v, dpp<kDppHalfMirror>(v));
-    v = fmaxf(v, dpp<kDppMirror>(v));
+    v = max2(v, dpp_mov<kDppSwap1>(v));
+    v = max2(v, dpp_mov<kDppSwap2>(v));
+    v = max2(v, dpp_mov<kDppHalfMirror>(v));
+    v = max2(v, dpp_mov<kDppMirror>(v));
     return v;
 }
 
@@ -832,7 +853,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
 #pragma unroll
         for (int ub = 0; ub < 4; ub++)
 #pragma unroll
-            for (int i = 0; i < 4; i++) acc[ub][i] = fmaxf(acc[ub][i], 0.0f);
+            for (int i = 0; i < 4; i++) acc[ub][i] = relu(acc[ub][i]);
         // The row's logit v . a1 (up to the common shift att . b2).
         float part = 0.0f;
 #pragma unroll
@@ -846,7 +867,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
         const float lg = valid ? part : -INFINITY;
         const float mb = xor16_max(lg);
         if (mb != -INFINITY) {
-            const float mn = fmaxf(m, mb);
+            const float mn = max2(m, mb);
             // exp(x) as the hardware 2^(x log2 e): x <= 0 here, and the
             // rounding of the product adds a relative error of |x| 2^-24.
             const float sc = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m - mn) * kLog2eAgg);
