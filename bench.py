@@ -254,8 +254,8 @@ def cpu_rnn_baseline(w, first_batch, budget_s, max_batches=50, max_links=20000):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (asked for {args.gpus}); "
-              "the tables shard by node, see DESIGN.md", file=sys.stderr)
+        print(f"bench.py: measures one GPU only (asked for {args.gpus}); on several GPUs "
+              "each would hold the table rows of its share of the node ids", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
