@@ -150,8 +150,9 @@ int nlb_create(const nlb_config *cfg, nlb_table **out);
  * non-decreasing across calls; node ids must be in [0, N).  Links with an
  * out-of-range endpoint or timestamp are skipped and flagged for
  * nlb_status, but still consume their arrival index.  n == 0 is a no-op.
- * Errors: NLB_EINVAL (NULL table or array with n > 0), NLB_ERANGE (the
- * arrival index would exceed 2^32-2), NLB_EDEVICE (launch failure). */
+ * Errors: NLB_EINVAL (NULL table or array with n > 0; n >= 2^31),
+ * NLB_ERANGE (the arrival index would exceed 2^32-2), NLB_EDEVICE (launch
+ * failure). */
 int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst,
                      const uint32_t *t, uint32_t n, void *stream);
 

@@ -1142,7 +1142,7 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
         hipFuncSetAttribute((const void *)aggregate_fused, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)kAggLdsMax) != hipSuccess)
         return NLB_EDEVICE;
-    const dim3 grid((unsigned)((nq + tile_q - 1) / tile_q));
+    const dim3 grid((unsigned)(((uint64_t)nq + tile_q - 1) / tile_q));
     hipLaunchKernelGGL(aggregate_fused, grid, dim3(kAggThreads), lds, (hipStream_t)stream, p);
     if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
     return NLB_OK;

@@ -607,6 +607,8 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const
     if (!h) return NLB_EINVAL;
     if (n == 0) return NLB_OK;
     if (!src || !dst || !t) return NLB_EINVAL;
+    // link and thread indices of the kernels are 32-bit
+    if (n >= (1u << 31)) return NLB_EINVAL;
     if (h->interactions + n > 0xFFFFFFFFull) return NLB_ERANGE;
     DeviceGuard guard(h->device);
     if (!guard.ok()) return NLB_EDEVICE;
@@ -694,7 +696,7 @@ static int launch_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, 
     p.tile_q = tile_queries(h->s, nq);
     p.s_m = ceil_2_40_div(h->s);
     const hipStream_t st = (hipStream_t)stream;
-    const dim3 grid((unsigned)((nq + p.tile_q - 1) / p.tile_q));
+    const dim3 grid((unsigned)(((uint64_t)nq + p.tile_q - 1) / p.tile_q));
     // Large first-hop launches that also write timestamps take the time
     // encoding out of sample_gather into tenc_stream.
     const uint64_t tenc_total = (uint64_t)nq * h->s * p.tenc_units;

@@ -305,6 +305,29 @@ def test_feature_row_widths_and_time_dims():
                                       o.sample(q, tq, None, None, ef, None)["efeat"])
 
 
+def test_oversized_calls_are_rejected_before_launch():
+    """Batch sizes whose 32-bit link or thread indices would wrap are refused
+    on the host: nothing is launched, so the tiny buffers are never read,
+    and the table is unchanged."""
+    import ctypes
+    import torch
+    import paper_2402_01964_amd as nlb
+    g = nlb.Table(100, 4, 0.5, 1)
+    z = torch.zeros(8, dtype=torch.int32, device="cuda")
+    p = ctypes.c_void_p(z.data_ptr())
+    lib = nlb.load_library()
+    assert lib.nlb_insert_batch(g._h, p, p, p, 2**31, None) == nlb.NLB_EINVAL
+    assert lib.nlb_insert_batch(g._h, p, p, p, 2**32 - 1, None) == nlb.NLB_EINVAL
+    out = nlb._SampleOut()
+    out.nbr = p
+    # second hop: nq * s must stay below 2^32
+    assert lib.nlb_sample_hop2(g._h, p, p, 2**30, ctypes.byref(out), None) == nlb.NLB_EINVAL
+    torch.cuda.synchronize()
+    assert g.info()["interactions"] == 0
+    assert g.status() == nlb.NLB_OK
+    assert not z.any()
+
+
 def test_errors_are_reported_not_faulted():
     """Out-of-range ids, timestamps >= 2^30 and decreasing timestamps are
     skipped/flagged; the rest of the batch is applied as usual."""
