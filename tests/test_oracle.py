@@ -659,6 +659,71 @@ def test_aggregate_constant_messages_ignore_attention():
     assert np.abs(z[any_valid][0] - z[~any_valid][0]).max() > 1e-6
 
 
+def _bf16_to_f64(bits):
+    return (np.asarray(bits).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def _pad_last(a, to):
+    return np.concatenate([a, np.zeros(a.shape[:-1] + (to - a.shape[-1],))], axis=-1)
+
+
+def test_aggregate_matches_library_attention_pooling():
+    """Eq. (4) rebuilt from library routines in float64 on the oracle's own
+    sample outputs (pinned above): torch's F.linear for the four layers
+    (weights [out][in], as the layouts state) and scaled_dot_product_attention
+    with the attention vector as the single query, the messages as keys and
+    values, scale 1 and the validity mask; a query without a valid slot
+    aggregates the zero vector.  A transposed square weight, a dropped bias,
+    a wrong mask or a wrong order of the input segments fails this."""
+    import torch
+    import torch.nn.functional as F
+    import synth
+    rng = np.random.default_rng(11)
+    N, s, E = 300, 8, 3000
+    src, dst, t = random_stream(rng, N, E, 10**5)
+    w = synth.scaled(synth.workload(3), 10)            # bf16 link and node rows
+    W = synth.agg_weights(w)
+    ef = synth._to_bf16_bits(rng.standard_normal((E, w.edge_dim)).astype(np.float32))
+    nf = synth._to_bf16_bits(rng.standard_normal((N, w.node_dim)).astype(np.float32))
+    fw, fb = synth.time_params(w)
+    o = Oracle(N, s, 0.5, seed=7)
+    o.insert(src, dst, t)
+    q = rng.integers(0, N, 400).astype(np.int32)
+    tq = rng.integers(0, 2 * 10**5, 400).astype(np.uint32)
+    tq[:5] = 0                                          # no entry is older than time 0
+    # queries at the time of one of their node's stored entries: the strict
+    # mask of eq. (1) leaves that entry out
+    _, ts_q, _ = o.export_nodes(q[5:60])
+    at_entry = 0
+    for i, row in enumerate(ts_q):
+        live = row[row != 0xFFFFFFFF]
+        if len(live) >= 2:
+            tq[5 + i] = live.max()
+            at_entry += 1
+    assert at_entry >= 20
+    z = o.aggregate(q, tq, fw, fb, ef, nf, W)
+
+    out = o.sample(q, tq, fw, fb, ef, nf)
+    valid = out["nbr"] >= 0
+    n_valid = valid.sum(axis=1)
+    assert (n_valid == 0).sum() >= 5 and (n_valid >= 2).sum() > 300
+    p32 = lambda d: (d + 31) // 32 * 32
+    x = np.concatenate([_pad_last(_bf16_to_f64(out["nfeat"]), p32(w.node_dim)),
+                        _pad_last(_bf16_to_f64(out["efeat"]), p32(w.edge_dim)),
+                        _pad_last(out["tenc"].astype(np.float64), p32(w.d_time))], axis=-1)
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float64))
+    Wt = {k: T(_bf16_to_f64(v) if k[0] == "w" and k != "att" else v.astype(np.float64))
+          for k, v in W.items()}
+    msg = F.linear(F.relu(F.linear(T(x), Wt["w1"], Wt["b1"])), Wt["w2"], Wt["b2"])   # [nq, s, H]
+    query = Wt["att"].expand(len(q), 1, -1).contiguous()
+    agg = F.scaled_dot_product_attention(query, msg, msg, attn_mask=torch.from_numpy(valid)[:, None, :],
+                                         scale=1.0)[:, 0, :]
+    agg[~torch.from_numpy(valid.any(axis=1))] = 0.0
+    y = torch.cat([T(_pad_last(_bf16_to_f64(out["self"]), p32(w.node_dim))), agg], dim=-1)
+    ref = F.linear(F.relu(F.linear(y, Wt["w3"], Wt["b3"])), Wt["w4"], Wt["b4"]).numpy()
+    np.testing.assert_allclose(z, ref, rtol=1e-9, atol=1e-9)
+
+
 # ----------------------------------------------------------------------------- status RNN (Sec. 4.4)
 def _gru_zero(d, d_t, e_dim):
     kx = oracle_pad32(d) + oracle_pad32(d_t) + oracle_pad32(e_dim)
