@@ -307,8 +307,8 @@ def test_feature_row_widths_and_time_dims():
 
 def test_oversized_calls_are_rejected_before_launch():
     """Batch sizes whose 32-bit link or thread indices would wrap are refused
-    on the host: nothing is launched, so the tiny buffers are never read,
-    and the table is unchanged."""
+    on the host, and empty calls return at once: nothing is launched, so the
+    tiny buffers are never read, and the table is unchanged."""
     import ctypes
     import torch
     import paper_2402_01964_amd as nlb
@@ -322,6 +322,10 @@ def test_oversized_calls_are_rejected_before_launch():
     out.nbr = p
     # second hop: nq * s must stay below 2^32
     assert lib.nlb_sample_hop2(g._h, p, p, 2**30, ctypes.byref(out), None) == nlb.NLB_EINVAL
+    # empty calls are no-ops that touch nothing
+    assert lib.nlb_sample_hop2(g._h, p, p, 0, ctypes.byref(out), None) == nlb.NLB_OK
+    aw = nlb._AggWeights()
+    assert lib.nlb_aggregate(g._h, p, p, 0, ctypes.byref(aw), p, None) == nlb.NLB_OK
     torch.cuda.synchronize()
     assert g.info()["interactions"] == 0
     assert g.status() == nlb.NLB_OK
