@@ -152,7 +152,8 @@ int nlb_create(const nlb_config *cfg, nlb_table **out);
  * nlb_status, but still consume their arrival index.  n == 0 is a no-op.
  * Errors: NLB_EINVAL (NULL table or array with n > 0; n >= 2^31),
  * NLB_ERANGE (the arrival index would exceed 2^32-2), NLB_EDEVICE (launch
- * failure). */
+ * failure).  The arrival indices are assigned on the host at the call, so a
+ * captured insert must not be replayed. */
 int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst,
                      const uint32_t *t, uint32_t n, void *stream);
 
@@ -163,7 +164,9 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst,
  * during the call only.  A query node outside [0, N) yields an all-invalid
  * answer and is flagged for nlb_status.  nq == 0 is a no-op.
  * Errors: NLB_EINVAL (NULL table, out or array with nq > 0; tenc/efeat/nfeat/
- * self requested without the matching configuration), NLB_EDEVICE. */
+ * self requested without the matching configuration), NLB_EDEVICE.
+ * The call only enqueues kernels (no allocation, memset or synchronisation):
+ * it may be captured in a HIP graph and replayed on the same buffers. */
 int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t nq,
                const nlb_sample_out *out, void *stream);
 
@@ -177,7 +180,8 @@ int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t n
  * [nq][s][s][row bytes], self [nq][s][node_row_bytes] (v's node row).  An
  * empty first-hop entry (v < 0) gives an all-invalid answer and a zero self
  * row without an error; v >= N is flagged as in nlb_sample.  nq*s must be
- * below 2^32.  nq == 0 is a no-op.  Errors: as nlb_sample. */
+ * below 2^32.  nq == 0 is a no-op.  Errors: as nlb_sample.  Graph capture:
+ * as nlb_sample. */
 int nlb_sample_hop2(nlb_table *h, const int32_t *hop1_nbr, const uint32_t *tq, uint32_t nq,
                     const nlb_sample_out *out, void *stream);
 
@@ -208,7 +212,8 @@ int nlb_sample_hop2(nlb_table *h, const int32_t *hop1_nbr, const uint32_t *tq, u
  * slot (the logits then use W_b^T w); only the rounding order differs.
  * z is device fp32 [nq][H].  Tables with s > 64 are not supported
  * (NLB_EINVAL).  nq == 0 is a no-op.  Errors: as nlb_sample, and NLB_EINVAL
- * for a bad weight set. */
+ * for a bad weight set.  Graph capture: as nlb_sample (besides its kernels
+ * the call makes only host-side attribute queries and settings). */
 #define NLB_AGG_HIDDEN 64
 #define NLB_DTYPE_F32 0
 #define NLB_DTYPE_BF16 1
@@ -263,7 +268,8 @@ int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_
  * which the first call (and a larger batch) allocates.  n == 0 is a no-op.
  * Errors: NLB_EINVAL (NULL table, weights or array with n > 0; n >= 2^31;
  * bad dtype or dimension; misaligned pointers; a 16-row tile that does not
- * fit the LDS), NLB_ENOMEM, NLB_EDEVICE. */
+ * fit the LDS), NLB_ENOMEM, NLB_EDEVICE.  Not for graph replay: each call
+ * takes a new host-side call number that tags its working buffers. */
 #define NLB_RNN_MAX_DIM 1024
 
 typedef struct nlb_gru_weights {
