@@ -52,7 +52,7 @@ struct AggParams {
     uint32_t tile_q;      // queries per tile
     uint32_t rows;        // slot rows per tile, padded to 16
     uint32_t qrows;       // query rows per tile, padded to 16
-    uint64_t s_m;         // ceil(2^40 / s)
+    uint64_t s_m;         // nlb_div_magic(s)
     uint32_t d_time;
     const float *w;
     const float *b;
@@ -63,7 +63,7 @@ struct AggParams {
     uint32_t n_dim, n_bf16, nrb, n_vec;
     uint32_t k1, off_e, off_t, k3;   // padded widths of w1 / w3 and segment offsets in w1
     uint32_t xs, ys;                 // LDS row strides (bf16 elements) of X and Y
-    uint64_t g1_m, gq_m;             // ceil(2^40 / (k1 / 8)), ceil(2^40 / (pad32(n_dim) / 8))
+    uint64_t g1_m, gq_m;             // nlb_div_magic(k1 / 8), nlb_div_magic(pad32(n_dim) / 8)
     uint32_t region_off, off_h, off_y, off_a3;
     const __bf16 *w1, *w2, *w3, *w4;
     const float *b1, *b2, *b3, *b4, *att;
@@ -131,7 +131,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_fused(AggParams p) {
     for (uint32_t j = tid; j < p.rows; j += kAggThreads) {
         SlotLds sl = {-1, 0xFFFFFFFFu, 0xFFFFFFFFu, 0.0f};
         if (j < ns) {
-            const uint32_t ql = div_small(j, p.s_m);
+            const uint32_t ql = nlb_div(j, p.s_m);
             const uint32_t a = j - ql * s;
             const int32_t node = p.node[q0 + ql];
             const bool in_range = node >= 0 && (int64_t)node < p.num_nodes;
@@ -157,7 +157,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_fused(AggParams p) {
 #pragma unroll
             for (int i = 0; i < 8; i++) v[r][i] = 0.0f;
             if (u >= units) continue;
-            const uint32_t j = div_small(u, p.g1_m);
+            const uint32_t j = nlb_div(u, p.g1_m);
             const uint32_t c0 = (u - j * g1) * 8;
             const SlotLds sl = slots[j];
             if (sl.x < 0) continue;
@@ -179,7 +179,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_fused(AggParams p) {
         for (int r = 0; r < kFillUnroll; r++) {
             const uint32_t u = base + r * kAggThreads;
             if (u >= units) continue;
-            const uint32_t j = div_small(u, p.g1_m);
+            const uint32_t j = nlb_div(u, p.g1_m);
             const uint32_t c0 = (u - j * g1) * 8;
             store_split8(v[r], Xh + (size_t)j * p.xs + c0, Xl + (size_t)j * p.xs + c0);
         }
@@ -267,7 +267,7 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_fused(AggParams p) {
     if (kn) {
         const uint32_t gq = kn / 8;
         for (uint32_t u = tid; u < p.qrows * gq; u += kAggThreads) {
-            const uint32_t q = div_small(u, p.gq_m);
+            const uint32_t q = nlb_div(u, p.gq_m);
             const uint32_t c0 = (u - q * gq) * 8;
             float v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
             if (q < nqt && tnodes[q] >= 0)
@@ -1001,7 +1001,7 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
     p.node = node;
     p.tq = tq;
     p.nq = nq;
-    p.s_m = ceil_2_40_div(h->s);
+    p.s_m = nlb_div_magic(h->s);
     p.d_time = h->d_time;
     p.w = h->w;
     p.b = h->b;
@@ -1023,8 +1023,8 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
     if (p.k1 == 0) return NLB_EINVAL;   // no inputs at all
     p.xs = p.k1 + 8;
     p.ys = p.k3 + 8;
-    p.g1_m = ceil_2_40_div(p.k1 / 8);
-    p.gq_m = ceil_2_40_div(pad32(p.n_dim) / 8 ? pad32(p.n_dim) / 8 : 1);
+    p.g1_m = nlb_div_magic(p.k1 / 8);
+    p.gq_m = nlb_div_magic(pad32(p.n_dim) / 8 ? pad32(p.n_dim) / 8 : 1);
     p.w1 = (const __bf16 *)wts->w1;
     p.w2 = (const __bf16 *)wts->w2;
     p.w3 = (const __bf16 *)wts->w3;

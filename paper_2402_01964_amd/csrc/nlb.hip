@@ -13,13 +13,6 @@ namespace {
 constexpr int kInsertThreads = 256;
 
 // ---------------------------------------------------------------- integer helpers
-// x mod d for 32-bit x and d, by Lemire, Kaser & Kurz, "Faster remainder by
-// direct computation" (2019): M = 2^64 / d + 1.
-__device__ __forceinline__ uint32_t fastmod_u32(uint32_t x, uint64_t M, uint32_t d) {
-    uint64_t low = M * x;
-    return (uint32_t)__umul64hi(low, d);
-}
-
 // Output number n (n >= 1) of SplitMix64 started at `state0`; its mixing
 // function is the one published by Steele, Lea & Flood (OOPSLA 2014).
 __device__ __forceinline__ uint64_t splitmix64_nth(uint64_t state0, uint64_t n) {
@@ -42,7 +35,7 @@ struct InsertParams {
     int64_t num_nodes;
     uint64_t seed;
     uint64_t thr;         // replace when coin < thr
-    uint64_t mod_m;       // Lemire constant for mod s
+    uint64_t mod_m;       // nlb_div_magic(s), for nlb_mod
     uint32_t q1r, q2r;    // q1 mod s, q2 mod s
     uint32_t key_mode;
     uint32_t *status;
@@ -52,10 +45,10 @@ struct InsertParams {
 // Slot of neighbour x at time t: eq. (2) (q1*x + q2*t) mod s, or eq. (3)
 // q1*x mod s, evaluated on residues (exact: both products are < s^2).
 __device__ __forceinline__ uint32_t slot_of(const InsertParams &p, uint32_t x, uint32_t t) {
-    const uint32_t xr = fastmod_u32(x, p.mod_m, p.s);
+    const uint32_t xr = nlb_mod(x, p.mod_m, p.s);
     uint32_t h = p.q1r * xr;
-    if (p.key_mode == NLB_KEY_EDGE) h += p.q2r * fastmod_u32(t, p.mod_m, p.s);
-    return fastmod_u32(h, p.mod_m, p.s);
+    if (p.key_mode == NLB_KEY_EDGE) h += p.q2r * nlb_mod(t, p.mod_m, p.s);
+    return nlb_mod(h, p.mod_m, p.s);
 }
 
 __device__ __forceinline__ uint64_t offer_word(const InsertParams &p, uint32_t e, uint32_t k,
@@ -205,7 +198,7 @@ struct SampleParams {
     const uint32_t *tq;
     uint32_t nq;
     uint32_t tile_q;      // queries per tile; tile_q * s <= kTileSlots
-    uint64_t s_m;         // ceil(2^40 / s)
+    uint64_t s_m;         // nlb_div_magic(s)
     uint32_t d_time;
     const float *w;
     const float *b;
@@ -222,7 +215,7 @@ struct SampleParams {
     uint8_t *o_nfeat;
     uint8_t *o_self;
     uint32_t *status;
-    // copy geometry: units per row and ceil(2^40 / units)
+    // copy geometry: units per row and nlb_div_magic(units)
     uint32_t tenc_units, tenc_vec;  // tenc_vec = 4 (float4 stores) or 1
     uint64_t tenc_m;
     uint32_t e_units, e_width;
@@ -260,7 +253,7 @@ __device__ __forceinline__ void gather_tile(const uint8_t *__restrict__ src, uin
             const uint32_t f = base + r * kTileThreads + tid;
             val[r] = V(0);
             if (f < total) {
-                const uint32_t j = div_small(f, m);
+                const uint32_t j = nlb_div(f, m);
                 const uint32_t c = f - j * units;
                 int64_t row;
                 if (KIND == kRowSelf) {
@@ -319,7 +312,7 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
 #pragma unroll
     for (int r = 0; r < P1; r++) {
         const uint32_t j = min(tid + r * kTileThreads, ns - 1u);
-        const uint32_t ql = div_small(j, p.s_m);
+        const uint32_t ql = nlb_div(j, p.s_m);
         const uint64_t qg = q0 + ql;
         nd[r] = p.node[qg];
         tqv[r] = p.tq[HOP2 ? (uint32_t)qg / s : qg];
@@ -329,7 +322,7 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
 #pragma unroll
     for (int r = 0; r < P1; r++) {
         const uint32_t j = min(tid + r * kTileThreads, ns - 1u);
-        const uint32_t ql = div_small(j, p.s_m);
+        const uint32_t ql = nlb_div(j, p.s_m);
         const uint32_t a = j - ql * s;
         const bool in_range = nd[r] >= 0 && (int64_t)nd[r] < p.num_nodes;
         const uint8_t *bp = p.blocks + (size_t)(in_range ? nd[r] : 0) * p.block_bytes;
@@ -341,7 +334,7 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
     for (int r = 0; r < P1; r++) {
         const uint32_t j = tid + r * kTileThreads;
         if (j >= ns) break;
-        const uint32_t ql = div_small(j, p.s_m);
+        const uint32_t ql = nlb_div(j, p.s_m);
         const uint32_t a = j - ql * s;
         const int32_t node = nd[r];
         const bool in_range = node >= 0 && (int64_t)node < p.num_nodes;
@@ -363,7 +356,7 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
         const uint32_t total = ns * units;
         float *out = p.o_tenc + row0 * p.d_time;
         for (uint32_t f = tid; f < total; f += kTileThreads) {
-            const uint32_t j = div_small(f, p.tenc_m);
+            const uint32_t j = nlb_div(f, p.tenc_m);
             const uint32_t c = f - j * units;
             const SlotLds sl = slots[j];
             if (p.tenc_vec == 4) {
@@ -403,8 +396,8 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
 // 128-thread workgroup computes two float4 outputs (kTencPerThread) whose
 // timestamp and query-time reads are issued together, so one read latency
 // covers two stores.  Slot row j = f / units belongs to query j / s;
-// ts[j] = 0xFFFFFFFF marks an invalid slot (zeros).  Divisions by
-// multiply-high with M = 2^64 / d + 1, exact for 32-bit numerators.
+// ts[j] = 0xFFFFFFFF marks an invalid slot (zeros).  Both divisions are
+// nlb_div (exact for every 32-bit numerator and divisor, 1 included).
 constexpr uint32_t kTencThreads = 128, kTencPerThread = 2;
 
 __global__ __launch_bounds__(kTencThreads) void tenc_stream(const uint32_t *ts, const uint32_t *tq, uint64_t s_M,
@@ -415,10 +408,10 @@ __global__ __launch_bounds__(kTencThreads) void tenc_stream(const uint32_t *ts, 
     for (uint32_t k = 0; k < kTencPerThread; k++) {
         ff[k] = (blockIdx.x * kTencPerThread + k) * kTencThreads + threadIdx.x;
         const uint32_t f = min(ff[k], total - 1u);   // past the end: re-read the last (unused)
-        const uint32_t j = (uint32_t)__umul64hi(u_M, f);
+        const uint32_t j = nlb_div(f, u_M);
         cc[k] = f - j * units;
         t[k] = ts[j];
-        q[k] = tq[(uint32_t)__umul64hi(s_M, j)];
+        q[k] = tq[nlb_div(j, s_M)];
     }
 #pragma unroll
     for (uint32_t k = 0; k < kTencPerThread; k++) {
@@ -624,7 +617,7 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const
     p.num_nodes = h->num_nodes;
     p.seed = h->seed;
     p.thr = h->thr;
-    p.mod_m = UINT64_MAX / h->s + 1;
+    p.mod_m = nlb_div_magic(h->s);
     p.q1r = (uint32_t)(h->q1 % h->s);
     p.q2r = (uint32_t)(h->q2 % h->s);
     p.key_mode = (uint32_t)h->key_mode;
@@ -684,17 +677,17 @@ static int launch_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, 
                       (uintptr_t)h->w % 16 == 0 && (uintptr_t)h->b % 16 == 0;
     p.tenc_vec = vec4 ? 4 : 1;
     p.tenc_units = h->d_time ? (vec4 ? h->d_time / 4 : h->d_time) : 1;
-    p.tenc_m = ceil_2_40_div(p.tenc_units);
+    p.tenc_m = nlb_div_magic(p.tenc_units);
     p.e_width = h->erb ? copy_width(h->erb, h->efeat, out->efeat) : 4;
     p.e_units = h->erb ? h->erb / p.e_width : 1;
-    p.e_m = ceil_2_40_div(p.e_units);
+    p.e_m = nlb_div_magic(p.e_units);
     // the same width serves the neighbour rows and the self row
     const uintptr_t nalign = (uintptr_t)out->nfeat | (uintptr_t)out->self;
     p.n_width = h->nrb ? copy_width(h->nrb, h->nfeat, (const void *)nalign) : 4;
     p.n_units = h->nrb ? h->nrb / p.n_width : 1;
-    p.n_m = ceil_2_40_div(p.n_units);
+    p.n_m = nlb_div_magic(p.n_units);
     p.tile_q = tile_queries(h->s, nq);
-    p.s_m = ceil_2_40_div(h->s);
+    p.s_m = nlb_div_magic(h->s);
     const hipStream_t st = (hipStream_t)stream;
     const dim3 grid((unsigned)(((uint64_t)nq + p.tile_q - 1) / p.tile_q));
     // Large first-hop launches that also write timestamps take the time
@@ -708,7 +701,7 @@ static int launch_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, 
     else
         hipLaunchKernelGGL(sample_gather<false>, grid, dim3(kTileThreads), 0, st, p);
     if (split) {
-        const uint64_t sM = ~0ull / h->s + 1, uM = ~0ull / p.tenc_units + 1;
+        const uint64_t sM = nlb_div_magic(h->s), uM = nlb_div_magic(p.tenc_units);
         hipLaunchKernelGGL(tenc_stream,
                            dim3((unsigned)((tenc_total + kTencThreads * kTencPerThread - 1) /
                                            (kTencThreads * kTencPerThread))),

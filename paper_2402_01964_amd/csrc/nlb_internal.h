@@ -31,6 +31,7 @@
 #include <cstdint>
 
 #include "../../include/nlb.h"
+#include "nlb_divide.h"
 
 namespace {
 
@@ -48,11 +49,6 @@ constexpr size_t kStatusBytes = 256;    // [0] flags, [1..2] last timestamp per 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-// floor(f / d) for f < 2^24, d < 2^16, with m = ceil(2^40 / d).
-__device__ __forceinline__ uint32_t div_small(uint32_t f, uint64_t m) {
-    return (uint32_t)(((uint64_t)f * m) >> 40);
-}
 
 // ---------------------------------------------------------------- cosine
 // Arguments beyond the fast path's range: the device libm's double cos,
@@ -227,8 +223,6 @@ __device__ __forceinline__ void store_split1(float v, __bf16 *hi, __bf16 *lo) {
 inline uint32_t pad16(uint32_t x) { return (x + 15u) & ~15u; }
 inline uint32_t pad32(uint32_t x) { return (x + 31u) & ~31u; }
 inline uint32_t align16(uint32_t x) { return (x + 15u) & ~15u; }
-
-uint64_t ceil_2_40_div(uint32_t d) { return ((1ull << 40) + d - 1) / d; }
 
 class DeviceGuard {
   public:

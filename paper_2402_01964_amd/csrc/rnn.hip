@@ -225,12 +225,12 @@ struct GruParams {
     uint32_t xs, ls, hs;                // LDS row strides (bf16 elements)
     uint32_t rows;                      // listed rows per tile (16, 32 or 64)
     uint32_t off_xl, off_h, off_hl;     // LDS byte offsets
-    uint64_t gx_m, gh_m;                // ceil(2^40 / (kx / 8)), ceil(2^40 / (kd / 8))
-    uint64_t gt_m, ge_m;                // ceil(2^40 / ((off_e - kd) / 8)), ceil(2^40 / ((kx - off_e) / 8))
+    uint64_t gx_m, gh_m;                // nlb_div_magic(kx / 8), nlb_div_magic(kd / 8)
+    uint64_t gt_m, ge_m;                // nlb_div_magic((off_e - kd) / 8), nlb_div_magic((kx - off_e) / 8)
     int32_t s_kind, e_kind;             // piece forms of status / link rows (-1: none applies)
     uint32_t meta;                      // LDS bytes before X: row list, then T-enc w | b (pad32(d_time) each)
     uint32_t ws_lomask;                 // weight-stationary form: bit s set if X k-step s has a lo plane
-    uint64_t ws_cpr_m;                  // ceil(2^40 / (srb / 16))
+    uint64_t ws_cpr_m;                  // nlb_div_magic(srb / 16)
     const __bf16 *w_ih, *w_hh;
     const float *b_ih, *b_hh;
 };
@@ -341,14 +341,14 @@ __device__ __forceinline__ void fill_seg(uint32_t units, uint32_t g, uint64_t g_
 #pragma unroll
         for (int f = 0; f < F; f++) {
             const uint32_t u = min(base + f * NT, units - 1u);
-            const uint32_t j = div_small(u, g_m), c0 = (u - j * g) * 8u;
+            const uint32_t j = nlb_div(u, g_m), c0 = (u - j * g) * 8u;
             load_piece<KIND>(row_of(j), dim, c0, pc[f]);
         }
 #pragma unroll
         for (int f = 0; f < F; f++) {
             const uint32_t u = base + f * NT;
             if (u < units) {
-                const uint32_t j = div_small(u, g_m), c0 = (u - j * g) * 8u;
+                const uint32_t j = nlb_div(u, g_m), c0 = (u - j * g) * 8u;
                 store(j, c0, pc[f]);
             }
         }
@@ -415,7 +415,7 @@ __device__ __forceinline__ void gru_fill(const GruParams &p, uint32_t m, const u
         // Time encoding cos(w_k t + b_k) of each row's link time.
         const uint32_t gt = (p.off_e - p.kd) / 8;
         for (uint32_t u = tid; u < R * gt; u += kRnnThreads) {
-            const uint32_t j = div_small(u, p.gt_m), k = (u - j * gt) * 8u;
+            const uint32_t j = nlb_div(u, p.gt_m), k = (u - j * gt) * 8u;
             const float tf = m_t[j < m ? j : 0];
             const f32x4 w0 = *(const f32x4 *)(s_tw + k), w1 = *(const f32x4 *)(s_tw + k + 4);
             const f32x4 b0 = *(const f32x4 *)(s_tb + k), b1 = *(const f32x4 *)(s_tb + k + 4);
@@ -479,12 +479,12 @@ __device__ __forceinline__ void gru_fill(const GruParams &p, uint32_t m, const u
             for (int i = 0; i < 8; i++) v[f][i] = 0.0f;
             if (u >= ut) continue;
             if (u >= ux) {
-                const uint32_t j = div_small(u - ux, p.gh_m);
+                const uint32_t j = nlb_div(u - ux, p.gh_m);
                 const uint32_t c0 = (u - ux - j * gh) * 8;
                 if (j < m) load8(p.st + (size_t)m_self[j] * p.srb, p.d, p.s_bf16, p.s_vec, c0, v[f]);
                 continue;
             }
-            const uint32_t j = div_small(u, p.gx_m);
+            const uint32_t j = nlb_div(u, p.gx_m);
             const uint32_t c0 = (u - j * gx) * 8;
             if (j >= m) continue;
             const uint32_t link = m_row[j] >> 1;
@@ -525,7 +525,7 @@ __device__ __forceinline__ void gru_fill(const GruParams &p, uint32_t m, const u
             const uint32_t u = base + f * kRnnThreads;
             if (u >= ut) continue;
             if (u >= ux) {
-                const uint32_t j = div_small(u - ux, p.gh_m);
+                const uint32_t j = nlb_div(u - ux, p.gh_m);
                 const uint32_t c0 = (u - ux - j * gh) * 8;
                 if (p.h_lo)
                     store_split8(v[f], Hh + (size_t)j * hs + c0, Hl + (size_t)j * hs + c0);
@@ -533,7 +533,7 @@ __device__ __forceinline__ void gru_fill(const GruParams &p, uint32_t m, const u
                     store_hi8(v[f], Hh + (size_t)j * hs + c0);
                 continue;
             }
-            const uint32_t j = div_small(u, p.gx_m);
+            const uint32_t j = nlb_div(u, p.gx_m);
             const uint32_t c0 = (u - j * gx) * 8;
             if (c0 >= p.lo_begin && c0 < p.lo_end)
                 store_split8(v[f], Xh + (size_t)j * xs + c0, Xl + (size_t)j * ls + (c0 - p.lo_begin));
@@ -954,7 +954,7 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
         for (uint32_t k = 0; k < CO; k++) {
             const uint32_t u = tid + k * T;
             if (u < units) {
-                const uint32_t row = div_small(u, p.ws_cpr_m), c = 16u * (u - row * cpr);
+                const uint32_t row = nlb_div(u, p.ws_cpr_m), c = 16u * (u - row * cpr);
                 const u32x4 v = *(const u32x4 *)(ob + row * OSTR + c);
                 *(u32x4 *)(p.cand + (size_t)meta[slot * MS + row][0] * p.srb + c) = v;
             }
@@ -1228,10 +1228,10 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     p.xs = p.kx + 8;
     p.ls = (p.lo_end - p.lo_begin) + 8;
     p.hs = p.kd + 8;
-    p.gx_m = ceil_2_40_div(p.kx / 8);
-    p.gh_m = ceil_2_40_div(p.kd / 8);
-    p.gt_m = p.off_e > p.kd ? ceil_2_40_div((p.off_e - p.kd) / 8) : 0;
-    p.ge_m = p.kx > p.off_e ? ceil_2_40_div((p.kx - p.off_e) / 8) : 0;
+    p.gx_m = nlb_div_magic(p.kx / 8);
+    p.gh_m = nlb_div_magic(p.kd / 8);
+    p.gt_m = p.off_e > p.kd ? nlb_div_magic((p.off_e - p.kd) / 8) : 0;
+    p.ge_m = p.kx > p.off_e ? nlb_div_magic((p.kx - p.off_e) / 8) : 0;
     p.s_kind = piece_kind(p.srb, status, p.s_bf16);
     p.e_kind = h->efeat ? piece_kind(h->erb, h->efeat, p.e_bf16) : -1;
     p.meta = align16(kGruMetaRows + 8u * pad32(p.d_time));
@@ -1261,7 +1261,7 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
         const uint32_t fixed = kh == 1 ? WsLayout<1>::fixed : kh == 2 ? WsLayout<2>::fixed
                              : kh == 3 ? WsLayout<3>::fixed : WsLayout<4>::fixed;
         lds = 8u * pad32(p.d_time);
-        p.ws_cpr_m = ceil_2_40_div(p.srb / 16);
+        p.ws_cpr_m = nlb_div_magic(p.srb / 16);
         ws = fixed + lds <= kGruLdsMax &&
              hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) == hipSuccess && cus > 0;
         for (uint32_t st = p.lo_begin / 32; st < p.lo_end / 32; st++) p.ws_lomask |= 1u << st;
