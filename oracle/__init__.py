@@ -58,6 +58,10 @@ def _load():
                                ctypes.c_uint64, ctypes.c_double)
     lib.orc_create.restype = P
     lib.orc_create.argtypes = [i64, i32, dbl, u64, u64, u64, i32]
+    lib.orc_create_subset.restype = P
+    lib.orc_create_subset.argtypes = [i64, i32, dbl, u64, u64, u64, i32, P, i64]
+    lib.orc_rows.restype = i64
+    lib.orc_rows.argtypes = [P]
     lib.orc_destroy.argtypes = [P]
     lib.orc_threshold.restype = u64
     lib.orc_threshold.argtypes = [P]
@@ -74,18 +78,19 @@ def _load():
     lib.orc_insert_ids.restype = ctypes.c_int
     lib.orc_insert_ids.argtypes = [P, P, P, P, P, i64]
     lib.orc_export.argtypes = [P, P, P, P]
+    lib.orc_export_nodes.restype = ctypes.c_int
     lib.orc_export_nodes.argtypes = [P, P, i64, P, P, P]
     lib.orc_sample.restype = ctypes.c_int
-    lib.orc_sample.argtypes = [P, P, P, i64, i32, P, P, P, i64, P, i64,
+    lib.orc_sample.argtypes = [P, P, P, i64, i32, P, P, P, i64, i64, P, i64,
                                P, P, P, P, P, P, P]
     lib.orc_sample_hop2.restype = ctypes.c_int
-    lib.orc_sample_hop2.argtypes = [P, P, P, i64, i32, P, P, P, i64, P, i64,
+    lib.orc_sample_hop2.argtypes = [P, P, P, i64, i32, P, P, P, i64, i64, P, i64,
                                     P, P, P, P, P, P, P]
     lib.orc_aggregate.restype = ctypes.c_int
-    lib.orc_aggregate.argtypes = [P, P, P, i64, i32, P, P, P, i32, i32, P, i32, i32, i32,
+    lib.orc_aggregate.argtypes = [P, P, P, i64, i32, P, P, P, i64, i32, i32, P, i32, i32, i32,
                                   P, P, P, P, P, P, P, P, P, P]
     lib.orc_gru_update.restype = ctypes.c_int
-    lib.orc_gru_update.argtypes = [i64, i32, P, i32, P, P, P, i64, u64, i32, P, P, P, i32, i32,
+    lib.orc_gru_update.argtypes = [i64, i32, P, i32, P, P, P, i64, u64, i32, P, P, P, i64, i32, i32,
                                    P, P, P, P]
     lib.orc_tenc.argtypes = [P, i64, i32, P, P, P]
     _lib = lib
@@ -101,16 +106,27 @@ def _c(a, dtype):
 
 
 class Oracle:
-    """Sequential NLB tables for ``num_nodes`` nodes with ``s`` slots each."""
+    """Sequential NLB tables for ``num_nodes`` nodes with ``s`` slots each.
+
+    ``keep``: optional node ids whose tables are kept; offers to every other
+    table are dropped.  Tables are per node (Sec. 4.2), so the kept tables
+    are exactly those of the full structure; queries and exports must name
+    kept nodes."""
 
     def __init__(self, num_nodes: int, s: int, alpha: float, seed: int,
-                 q1: int = DEFAULT_Q1, q2: int = DEFAULT_Q2, key_mode: int = 0):
+                 q1: int = DEFAULT_Q1, q2: int = DEFAULT_Q2, key_mode: int = 0, keep=None):
         lib = _load()
         self._lib = lib
         self.N, self.s, self.alpha, self.seed = int(num_nodes), int(s), float(alpha), int(seed)
         self.key_mode = int(key_mode)
-        self._h = lib.orc_create(self.N, self.s, self.alpha, self.seed & (2**64 - 1),
-                                 int(q1), int(q2), self.key_mode)
+        self.subset = keep is not None
+        if keep is None:
+            self._h = lib.orc_create(self.N, self.s, self.alpha, self.seed & (2**64 - 1),
+                                     int(q1), int(q2), self.key_mode)
+        else:
+            keep = _c(keep, np.int32)
+            self._h = lib.orc_create_subset(self.N, self.s, self.alpha, self.seed & (2**64 - 1),
+                                            int(q1), int(q2), self.key_mode, _ptr(keep), len(keep))
         if not self._h:
             raise ValueError("oracle: invalid parameters or out of memory")
 
@@ -128,6 +144,10 @@ class Oracle:
     @property
     def threshold(self) -> int:
         return int(self._lib.orc_threshold(self._h))
+
+    @property
+    def rows(self) -> int:
+        return int(self._lib.orc_rows(self._h))
 
     @property
     def count(self) -> int:
@@ -153,6 +173,8 @@ class Oracle:
 
     def export(self):
         """Canonical table: (nbr int32, ts uint32, eid uint32), each [N, s]."""
+        if self.subset:
+            raise ValueError("oracle keeps a node subset: use export_nodes")
         n = self.N * self.s
         nbr = np.empty(n, np.int32)
         ts = np.empty(n, np.uint32)
@@ -166,7 +188,8 @@ class Oracle:
         nbr = np.empty((c, self.s), np.int32)
         ts = np.empty((c, self.s), np.uint32)
         eid = np.empty((c, self.s), np.uint32)
-        self._lib.orc_export_nodes(self._h, _ptr(nodes), c, _ptr(nbr), _ptr(ts), _ptr(eid))
+        if self._lib.orc_export_nodes(self._h, _ptr(nodes), c, _ptr(nbr), _ptr(ts), _ptr(eid)) != 0:
+            raise ValueError("oracle: node out of range or its table is not kept")
         return nbr, ts, eid
 
     def sample(self, node, tq, w=None, b=None, efeat=None, nfeat=None,
@@ -174,7 +197,8 @@ class Oracle:
         """Answer queries; returns a dict of numpy outputs (see nlb_oracle.c).
 
         ``efeat``/``nfeat`` are 2-D arrays of any dtype (rows are copied as
-        bytes); outputs keep that dtype.
+        bytes); outputs keep that dtype.  A stored link whose arrival index
+        is not below ``len(efeat)`` gathers a zero row.
         """
         node, tq = _c(node, np.int32), _c(tq, np.uint32)
         nq, s = len(node), self.s
@@ -190,10 +214,10 @@ class Oracle:
             out["ts"] = np.empty((nq, s), np.uint32)
         if "tenc" in want and d_t > 0:
             out["tenc"] = np.empty((nq, s, d_t), np.float32)
-        erb = nrb = 0
+        erb = nrb = erows = 0
         if efeat is not None:
             efeat = np.ascontiguousarray(efeat)
-            erb = efeat.shape[1] * efeat.itemsize
+            erb, erows = efeat.shape[1] * efeat.itemsize, efeat.shape[0]
             if "efeat" in want:
                 out["efeat"] = np.empty((nq, s, efeat.shape[1]), efeat.dtype)
         if nfeat is not None:
@@ -205,7 +229,7 @@ class Oracle:
                 out["self"] = np.empty((nq, nfeat.shape[1]), nfeat.dtype)
         rc = self._lib.orc_sample(
             self._h, _ptr(node), _ptr(tq), nq, d_t, _ptr(w), _ptr(b),
-            _ptr(efeat), erb, _ptr(nfeat), nrb,
+            _ptr(efeat), erows, erb, _ptr(nfeat), nrb,
             _ptr(out.get("nbr")), _ptr(out.get("eid")), _ptr(out.get("ts")),
             _ptr(out.get("tenc")), _ptr(out.get("efeat")), _ptr(out.get("nfeat")),
             _ptr(out.get("self")))
@@ -236,10 +260,10 @@ class Oracle:
             out["ts"] = np.empty((nq, s, s), np.uint32)
         if "tenc" in want and d_t > 0:
             out["tenc"] = np.empty((nq, s, s, d_t), np.float32)
-        erb = nrb = 0
+        erb = nrb = erows = 0
         if efeat is not None:
             efeat = np.ascontiguousarray(efeat)
-            erb = efeat.shape[1] * efeat.itemsize
+            erb, erows = efeat.shape[1] * efeat.itemsize, efeat.shape[0]
             if "efeat" in want:
                 out["efeat"] = np.empty((nq, s, s, efeat.shape[1]), efeat.dtype)
         if nfeat is not None:
@@ -251,7 +275,7 @@ class Oracle:
                 out["self"] = np.empty((nq, s, nfeat.shape[1]), nfeat.dtype)
         rc = self._lib.orc_sample_hop2(
             self._h, _ptr(hop1), _ptr(tq), nq, d_t, _ptr(w), _ptr(b),
-            _ptr(efeat), erb, _ptr(nfeat), nrb,
+            _ptr(efeat), erows, erb, _ptr(nfeat), nrb,
             _ptr(out.get("nbr")), _ptr(out.get("eid")), _ptr(out.get("ts")),
             _ptr(out.get("tenc")), _ptr(out.get("efeat")), _ptr(out.get("nfeat")),
             _ptr(out.get("self")))
@@ -275,6 +299,7 @@ class Oracle:
                 return None, 0, 1
             a = np.ascontiguousarray(a)
             return a, a.shape[1], (0 if a.dtype == np.float32 else 1)
+        erows = 0 if efeat is None else int(np.shape(efeat)[0])
         ef, e_dim, e_dt = feat(efeat)
         nf, n_dim, n_dt = feat(nfeat)
         W = {k: np.ascontiguousarray(weights[k], np.uint16 if k[0] == "w" and k != "att" else np.float32)
@@ -282,7 +307,7 @@ class Oracle:
         z = np.empty((len(node), H), np.float64)
         rc = self._lib.orc_aggregate(
             self._h, _ptr(node), _ptr(tq), len(node), len(w), _ptr(w), _ptr(b),
-            _ptr(ef), e_dim, e_dt, _ptr(nf), n_dim, n_dt, H,
+            _ptr(ef), erows, e_dim, e_dt, _ptr(nf), n_dim, n_dt, H,
             _ptr(W["w1"]), _ptr(W["b1"]), _ptr(W["w2"]), _ptr(W["b2"]), _ptr(W["att"]),
             _ptr(W["w3"]), _ptr(W["b3"]), _ptr(W["w4"]), _ptr(W["b4"]), _ptr(z))
         if rc != 0:
@@ -302,14 +327,14 @@ def gru_update(status, src, dst, t, e0, w, b, efeat, weights):
     w, b = _c(w, np.float32), _c(b, np.float32)
     s_dt = 0 if status.dtype == np.float32 else 1
     if efeat is None:
-        ef, e_dim, e_dt = None, 0, 1
+        ef, e_rows, e_dim, e_dt = None, 0, 0, 1
     else:
         ef = np.ascontiguousarray(efeat)
-        e_dim, e_dt = ef.shape[1], (0 if ef.dtype == np.float32 else 1)
+        e_rows, e_dim, e_dt = ef.shape[0], ef.shape[1], (0 if ef.dtype == np.float32 else 1)
     W = {k: np.ascontiguousarray(weights[k], np.uint16 if k.startswith("w_") else np.float32)
          for k in ("w_ih", "w_hh", "b_ih", "b_hh")}
     rc = lib.orc_gru_update(status.shape[0], status.shape[1], _ptr(status), s_dt, _ptr(src), _ptr(dst),
-                            _ptr(t), len(src), int(e0), len(w), _ptr(w), _ptr(b), _ptr(ef), e_dim, e_dt,
+                            _ptr(t), len(src), int(e0), len(w), _ptr(w), _ptr(b), _ptr(ef), e_rows, e_dim, e_dt,
                             _ptr(W["w_ih"]), _ptr(W["w_hh"]), _ptr(W["b_ih"]), _ptr(W["b_hh"]))
     if rc != 0:
         raise ValueError("oracle: node id out of range")

@@ -50,11 +50,24 @@ typedef struct orc {
     uint64_t thr;       /* floor(alpha * 2^32), 2^32 when alpha == 1 */
     uint64_t seed;
     uint64_t q1, q2;
-    int32_t *nbr;       /* [N*s], -1 = empty */
-    uint32_t *ts;       /* [N*s] */
-    uint32_t *eid;      /* [N*s] */
+    int32_t *row_of;    /* NULL: node n owns table row n; else the row of node n, -1 = not kept */
+    uint64_t *kept;     /* with row_of: bit n set when node n's table is kept (a compact
+                           membership test, so that dropped offers stay cheap) */
+    int64_t rows;       /* table rows kept (N without row_of) */
+    int32_t *nbr;       /* [rows*s], -1 = empty */
+    uint32_t *ts;       /* [rows*s] */
+    uint32_t *eid;      /* [rows*s] */
     uint64_t next_e;    /* arrival index of the next link */
 } orc;
+
+/* Table row of node n, or -1 when the oracle does not keep n's table. */
+static int64_t table_row(const orc *o, int32_t n)
+{
+    if (n < 0 || n >= o->N) return -1;
+    if (!o->row_of) return n;
+    if (!((o->kept[n >> 6] >> (n & 63)) & 1u)) return -1;
+    return (int64_t)o->row_of[n];
+}
 
 /* n-th output (n >= 1) of SplitMix64 whose state starts at `state0`. */
 static uint64_t splitmix64_nth(uint64_t state0, uint64_t n)
@@ -65,10 +78,15 @@ static uint64_t splitmix64_nth(uint64_t state0, uint64_t n)
     return z ^ (z >> 31);
 }
 
-orc *orc_create(int64_t N, int32_t s, double alpha, uint64_t seed,
-                uint64_t q1, uint64_t q2, int32_t key_mode)
+/* Tables of `count` nodes (all N when nodes == NULL).  Sec. 4.2 gives every
+ * node its own table, and an offer to S_u touches no other table, so
+ * keeping only some nodes' tables (and dropping the offers to the others)
+ * leaves the kept tables exactly as in the full structure. */
+orc *orc_create_subset(int64_t N, int32_t s, double alpha, uint64_t seed,
+                       uint64_t q1, uint64_t q2, int32_t key_mode,
+                       const int32_t *nodes, int64_t count)
 {
-    if (N <= 0 || s <= 0 || !(alpha > 0.0 && alpha <= 1.0)) return NULL;
+    if (N <= 0 || N > 2147483647 || s <= 0 || !(alpha > 0.0 && alpha <= 1.0)) return NULL;
     if (key_mode != 0 && key_mode != 1) return NULL;
     /* q1*x + q2*t must not wrap in 64 bits: x < 2^31, t < 2^32. */
     if (q1 >= (1ULL << 31) || q2 >= (1ULL << 31)) return NULL;
@@ -77,12 +95,28 @@ orc *orc_create(int64_t N, int32_t s, double alpha, uint64_t seed,
     o->N = N; o->s = s; o->key_mode = key_mode; o->alpha = alpha;
     o->seed = seed; o->q1 = q1; o->q2 = q2;
     o->thr = (alpha >= 1.0) ? (1ULL << 32) : (uint64_t)floor(alpha * 4294967296.0);
-    size_t n = (size_t)N * (size_t)s;
-    o->nbr = (int32_t *)malloc(n * sizeof(int32_t));
-    o->ts = (uint32_t *)malloc(n * sizeof(uint32_t));
-    o->eid = (uint32_t *)malloc(n * sizeof(uint32_t));
+    o->rows = N;
+    if (nodes) {
+        o->row_of = (int32_t *)malloc((size_t)N * sizeof(int32_t));
+        o->kept = (uint64_t *)calloc((size_t)(N + 63) / 64, sizeof(uint64_t));
+        if (!o->row_of || !o->kept) { free(o->row_of); free(o->kept); free(o); return NULL; }
+        for (int64_t n = 0; n < N; n++) o->row_of[n] = -1;
+        o->rows = 0;
+        for (int64_t i = 0; i < count; i++) {
+            const int32_t n = nodes[i];
+            if (n < 0 || n >= N) { free(o->row_of); free(o->kept); free(o); return NULL; }
+            if (o->row_of[n] < 0) {
+                o->row_of[n] = (int32_t)o->rows++;
+                o->kept[n >> 6] |= 1ull << (n & 63);
+            }
+        }
+    }
+    size_t n = (size_t)o->rows * (size_t)s;
+    o->nbr = (int32_t *)malloc((n ? n : 1) * sizeof(int32_t));
+    o->ts = (uint32_t *)malloc((n ? n : 1) * sizeof(uint32_t));
+    o->eid = (uint32_t *)malloc((n ? n : 1) * sizeof(uint32_t));
     if (!o->nbr || !o->ts || !o->eid) {
-        free(o->nbr); free(o->ts); free(o->eid); free(o);
+        free(o->nbr); free(o->ts); free(o->eid); free(o->row_of); free(o->kept); free(o);
         return NULL;
     }
     for (size_t i = 0; i < n; i++) {
@@ -91,11 +125,19 @@ orc *orc_create(int64_t N, int32_t s, double alpha, uint64_t seed,
     return o;
 }
 
+orc *orc_create(int64_t N, int32_t s, double alpha, uint64_t seed,
+                uint64_t q1, uint64_t q2, int32_t key_mode)
+{
+    return orc_create_subset(N, s, alpha, seed, q1, q2, key_mode, NULL, 0);
+}
+
 void orc_destroy(orc *o)
 {
     if (!o) return;
-    free(o->nbr); free(o->ts); free(o->eid); free(o);
+    free(o->nbr); free(o->ts); free(o->eid); free(o->row_of); free(o->kept); free(o);
 }
+
+int64_t orc_rows(const orc *o) { return o->rows; }
 
 uint64_t orc_threshold(const orc *o) { return o->thr; }
 uint64_t orc_count(const orc *o) { return o->next_e; }
@@ -117,7 +159,9 @@ uint32_t orc_coin(const orc *o, uint64_t e, uint32_t k)
  * slot takes it; an occupied slot is replaced with probability alpha. */
 static void offer(orc *o, int32_t n, int32_t x, uint32_t t, uint64_t e, uint32_t k)
 {
-    size_t idx = (size_t)n * (size_t)o->s + orc_slot(o, (uint32_t)x, t);
+    const int64_t row = table_row(o, n);
+    if (row < 0) return;   /* a table the oracle does not keep */
+    size_t idx = (size_t)row * (size_t)o->s + orc_slot(o, (uint32_t)x, t);
     int empty = (o->nbr[idx] == -1);
     if (empty || (uint64_t)orc_coin(o, e, k) < o->thr) {
         o->nbr[idx] = x;
@@ -159,25 +203,30 @@ int orc_insert_ids(orc *o, const uint64_t *eids, const int32_t *src,
     return 0;
 }
 
+/* The kept tables in row order ([N][s] without a node subset). */
 void orc_export(const orc *o, int32_t *nbr, uint32_t *ts, uint32_t *eid)
 {
-    size_t n = (size_t)o->N * (size_t)o->s;
+    size_t n = (size_t)o->rows * (size_t)o->s;
     memcpy(nbr, o->nbr, n * sizeof(int32_t));
     memcpy(ts, o->ts, n * sizeof(uint32_t));
     memcpy(eid, o->eid, n * sizeof(uint32_t));
 }
 
-/* Export the slots of selected nodes: outputs are [count][s]. */
-void orc_export_nodes(const orc *o, const int32_t *nodes, int64_t count,
-                      int32_t *nbr, uint32_t *ts, uint32_t *eid)
+/* Export the slots of selected nodes: outputs are [count][s].  Returns -1
+ * when a node is out of range or its table is not kept. */
+int orc_export_nodes(const orc *o, const int32_t *nodes, int64_t count,
+                     int32_t *nbr, uint32_t *ts, uint32_t *eid)
 {
     for (int64_t i = 0; i < count; i++) {
-        size_t src = (size_t)nodes[i] * (size_t)o->s;
+        const int64_t row = table_row(o, nodes[i]);
+        if (row < 0) return -1;
+        size_t src = (size_t)row * (size_t)o->s;
         size_t dst = (size_t)i * (size_t)o->s;
         memcpy(nbr + dst, o->nbr + src, (size_t)o->s * sizeof(int32_t));
         memcpy(ts + dst, o->ts + src, (size_t)o->s * sizeof(uint32_t));
         memcpy(eid + dst, o->eid + src, (size_t)o->s * sizeof(uint32_t));
     }
+    return 0;
 }
 
 /* T-encoding of one time gap (App. C, with a phase b per dimension):
@@ -198,11 +247,16 @@ static float tenc_value(float w, float dt, float b)
  *   efeat    = bytes of edge-feature row eid, else zero bytes
  *   nfeat    = bytes of node-feature row nbr, else zero bytes
  *   self     = bytes of node-feature row node[i]
- * Any output pointer may be NULL.  Returns -1 on an out-of-range node.
+ * The link-feature table holds e_rows rows; a stored link with eid >= e_rows
+ * has no row there and contributes zero bytes (the paper gives every link
+ * a feature vector and never meets this case; a caller that keeps only the
+ * first rows gets zeros for the rest).
+ * Any output pointer may be NULL.  Returns -1 on an out-of-range node (or
+ * one whose table is not kept).
  */
 int orc_sample(const orc *o, const int32_t *node, const uint32_t *tq, int64_t nq,
                int32_t d_t, const float *w, const float *b,
-               const uint8_t *efeat, int64_t e_row_bytes,
+               const uint8_t *efeat, int64_t e_rows, int64_t e_row_bytes,
                const uint8_t *nfeat, int64_t n_row_bytes,
                int32_t *nbr_out, uint32_t *eid_out, uint32_t *ts_out,
                float *tenc_out, uint8_t *efeat_out, uint8_t *nfeat_out,
@@ -211,9 +265,10 @@ int orc_sample(const orc *o, const int32_t *node, const uint32_t *tq, int64_t nq
     const int64_t s = o->s;
     for (int64_t i = 0; i < nq; i++) {
         int32_t n = node[i];
-        if (n < 0 || n >= o->N) return -1;
+        const int64_t row = table_row(o, n);
+        if (row < 0) return -1;
         for (int64_t a = 0; a < s; a++) {
-            size_t src = (size_t)n * (size_t)s + (size_t)a;
+            size_t src = (size_t)row * (size_t)s + (size_t)a;
             size_t out = (size_t)i * (size_t)s + (size_t)a;
             int valid = (o->nbr[src] != -1) && (o->ts[src] < tq[i]);
             if (nbr_out) nbr_out[out] = valid ? o->nbr[src] : -1;
@@ -230,7 +285,7 @@ int orc_sample(const orc *o, const int32_t *node, const uint32_t *tq, int64_t nq
             }
             if (efeat_out && e_row_bytes > 0) {
                 uint8_t *dst = efeat_out + out * (size_t)e_row_bytes;
-                if (valid)
+                if (valid && (int64_t)o->eid[src] < e_rows)
                     memcpy(dst, efeat + (size_t)o->eid[src] * (size_t)e_row_bytes, (size_t)e_row_bytes);
                 else
                     memset(dst, 0, (size_t)e_row_bytes);
@@ -260,7 +315,7 @@ int orc_sample(const orc *o, const int32_t *node, const uint32_t *tq, int64_t nq
  */
 int orc_sample_hop2(const orc *o, const int32_t *hop1_nbr, const uint32_t *tq, int64_t nq,
                     int32_t d_t, const float *w, const float *b,
-                    const uint8_t *efeat, int64_t e_row_bytes,
+                    const uint8_t *efeat, int64_t e_rows, int64_t e_row_bytes,
                     const uint8_t *nfeat, int64_t n_row_bytes,
                     int32_t *nbr_out, uint32_t *eid_out, uint32_t *ts_out,
                     float *tenc_out, uint8_t *efeat_out, uint8_t *nfeat_out,
@@ -272,7 +327,7 @@ int orc_sample_hop2(const orc *o, const int32_t *hop1_nbr, const uint32_t *tq, i
             const int64_t r = i * s + a;         /* second-hop query index */
             const int32_t v = hop1_nbr[r];
             if (v >= 0) {
-                int rc = orc_sample(o, &v, &tq[i], 1, d_t, w, b, efeat, e_row_bytes, nfeat,
+                int rc = orc_sample(o, &v, &tq[i], 1, d_t, w, b, efeat, e_rows, e_row_bytes, nfeat,
                                     n_row_bytes,
                                     nbr_out ? nbr_out + r * s : NULL,
                                     eid_out ? eid_out + r * s : NULL,
@@ -352,11 +407,13 @@ static void affine(const uint16_t *W, int64_t ld, int64_t col0, const float *bia
  *   w1: [H][pad32(n_dim) + pad32(e_dim) + pad32(d_t)]  (r_v | e | T-enc)
  *   w2: [H][H]; w3: [H][pad32(n_dim) + H]  (r_u | aggregate); w4: [H][H]
  * Biases and att (the vector w) are fp32 [H].  Feature dtypes: 0 fp32, 1 bf16.
- * z_out is [nq][H].  Returns -1 on an out-of-range query node.
+ * A stored link with eid >= e_rows has no link-feature row: its e is zero
+ * (as in orc_sample).  z_out is [nq][H].  Returns -1 on an out-of-range
+ * query node.
  */
 int orc_aggregate(const orc *o, const int32_t *node, const uint32_t *tq, int64_t nq,
                   int32_t d_t, const float *w, const float *b,
-                  const uint8_t *efeat, int32_t e_dim, int32_t e_dtype,
+                  const uint8_t *efeat, int64_t e_rows, int32_t e_dim, int32_t e_dtype,
                   const uint8_t *nfeat, int32_t n_dim, int32_t n_dtype,
                   int32_t H, const uint16_t *w1, const float *b1, const uint16_t *w2,
                   const float *b2, const float *att, const uint16_t *w3, const float *b3,
@@ -376,10 +433,11 @@ int orc_aggregate(const orc *o, const int32_t *node, const uint32_t *tq, int64_t
     int rc = 0;
     for (int64_t i = 0; i < nq && rc == 0; i++) {
         const int32_t n = node[i];
-        if (n < 0 || n >= o->N) { rc = -1; break; }
+        const int64_t row = table_row(o, n);
+        if (row < 0) { rc = -1; break; }
         int any = 0;
         for (int64_t sl = 0; sl < s; sl++) {
-            const size_t idx = (size_t)n * (size_t)s + (size_t)sl;
+            const size_t idx = (size_t)row * (size_t)s + (size_t)sl;
             valid[sl] = (o->nbr[idx] != -1) && (o->ts[idx] < tq[i]);
             if (!valid[sl]) continue;
             any = 1;
@@ -388,7 +446,8 @@ int orc_aggregate(const orc *o, const int32_t *node, const uint32_t *tq, int64_t
             const float dt = (float)(uint32_t)(tq[i] - o->ts[idx]);
             /* MLP_in on x = [r_v ; e ; T-enc(tq - t')] */
             for (int64_t c = 0; c < n_dim; c++) x[c] = feat_value(nfeat + (size_t)v * n_bytes, n_dtype, c);
-            for (int64_t c = 0; c < e_dim; c++) x[n_dim + c] = feat_value(efeat + (size_t)e * e_bytes, e_dtype, c);
+            for (int64_t c = 0; c < e_dim; c++)
+                x[n_dim + c] = (int64_t)e < e_rows ? feat_value(efeat + (size_t)e * e_bytes, e_dtype, c) : 0.0;
             for (int64_t c = 0; c < d_t; c++) x[n_dim + e_dim + c] = (double)tenc_value(w[c], dt, b[c]);
             for (int64_t j = 0; j < H; j++) {
                 double acc = 0.0;
@@ -465,12 +524,14 @@ static uint16_t bf16_round(double v)
  * Weights (bf16 bits, row-major, input segments zero-padded to 32 columns):
  *   w_ih [3d][pad32(d) + pad32(d_t) + pad32(e_dim)]  rows r | z | n
  *   w_hh [3d][pad32(d)]
- * b_ih, b_hh: fp32 [3d].  Returns -1 on an out-of-range endpoint.
+ * b_ih, b_hh: fp32 [3d].  A link whose arrival index is e_rows or more has
+ * no link-feature row: its e is zero (as in orc_sample).  Returns -1 on an
+ * out-of-range endpoint.
  */
 int orc_gru_update(int64_t N, int32_t d, void *status, int32_t status_dtype,
                    const int32_t *src, const int32_t *dst, const uint32_t *t, int64_t n,
                    uint64_t e0, int32_t d_t, const float *w, const float *b,
-                   const uint8_t *efeat, int32_t e_dim, int32_t e_dtype,
+                   const uint8_t *efeat, int64_t e_rows, int32_t e_dim, int32_t e_dtype,
                    const uint16_t *w_ih, const uint16_t *w_hh, const float *b_ih,
                    const float *b_hh)
 {
@@ -494,8 +555,10 @@ int orc_gru_update(int64_t N, int32_t d, void *status, int32_t status_dtype,
             for (int64_t c = 0; c < d; c++) x[c] = feat_value(ro, status_dtype, c);
             for (int64_t c = 0; c < d_t; c++)
                 x[d + c] = (double)tenc_value(w[c], (float)t[i], b[c]);
+            const uint64_t e = e0 + (uint64_t)i;
             for (int64_t c = 0; c < e_dim; c++)
-                x[d + d_t + c] = feat_value(efeat + (size_t)(e0 + (uint64_t)i) * (size_t)e_bytes, e_dtype, c);
+                x[d + d_t + c] = e < (uint64_t)e_rows ? feat_value(efeat + (size_t)e * (size_t)e_bytes, e_dtype, c)
+                                                      : 0.0;
             for (int64_t c = 0; c < d; c++) hv[c] = feat_value(rs, status_dtype, c);
             double *out = cand + (size_t)(2 * i + k) * (size_t)d;
             for (int64_t j = 0; j < d; j++) {

@@ -1,15 +1,27 @@
 """Full-size parity: workloads 3, 4 and 5 at their real sizes, with the
 inputs resident in HBM and the batch / query launches the benchmark times.
 
-The GPU runs the whole stream.  At checkpoint batches a random subset of the
-batch's queries is kept -- the sampled outputs, and the eq. (4) aggregates
-of the same launch of all the batch's queries (random weights); after the
-stream, the final table rows of those query nodes are kept too.  The oracle then replays, in stream order, only the
-links that touch those nodes (tables are per node, so this is exact -- pinned
-on the CPU by test_filtered_substream_gives_same_rows) and answers the same
-queries at the same points.  Indices and rows must match bit for bit, the
-time encoding within 1e-5, the aggregates within the scaled tolerance of
-nlb_aggregate.
+The GPU runs the whole stream.  At each checkpoint batch it answers all of
+the batch's queries (3 x batch, every output) and keeps: the ids (nbr, eid,
+ts) of every query; every output of a random subset of queries; the eq. (4)
+aggregates of that subset (from one launch over all the batch's queries,
+random weights); the table rows of the tracked nodes; and, at one
+checkpoint, a random subset of the second-hop answers of a launch over all
+the batch's first-hop entries (nq * s second-hop queries, ids only, as the
+benchmark's second-hop mode times it).  After the stream it keeps the final
+rows of the tracked nodes.
+
+Tracked nodes: every node for medium-homogeneous and dense-repeated, whose
+whole tables are compared.  For large-sparse (1.2e9 slots) the tracked set
+is every query node of the checkpoints, 10^6 random nodes, the 1 000
+hottest nodes and the sampled second-hop queries' nodes; the oracle keeps
+only their tables (exact, because tables are per node: pinned on the CPU by
+test_kept_node_subset_gives_the_same_rows).
+
+The oracle then replays the whole stream in order, one link at a time, and
+is compared at the same points.  Indices, tables and rows must match bit
+for bit, the time encoding within 1e-5, the aggregates within the scaled
+tolerance of nlb_aggregate.
 """
 import numpy as np
 import pytest
@@ -22,45 +34,50 @@ AGG_TOL = 2e-4   # see nlb_aggregate in include/nlb.h
 
 pytestmark = pytest.mark.gpu
 
-
-def _host_filtered_links(w, mask, chunk=50_000_000):
-    """Links touching a masked node, with their arrival indices; also the
-    host copy of every query position asked for later is taken from the
-    same host generation."""
-    ids, S, D, T = [], [], [], []
-    if w.stateless:
-        for lo in range(0, w.links, chunk):
-            hi = min(w.links, lo + chunk)
-            src, dst, t, _ = synth.host_links(w, lo, hi)
-            sel = np.nonzero(mask[src] | mask[dst])[0]
-            ids.append(sel + lo)
-            S.append(src[sel]); D.append(dst[sel]); T.append(t[sel])
-    else:
-        src, dst, t, _ = synth.host_links(w)
-        sel = np.nonzero(mask[src] | mask[dst])[0]
-        ids.append(sel); S.append(src[sel]); D.append(dst[sel]); T.append(t[sel])
-    return (np.concatenate(ids).astype(np.uint64), np.concatenate(S), np.concatenate(D),
-            np.concatenate(T))
-
-
-def _host_queries(w, b, positions):
-    """Host-generated (node, tq) of query positions of batch b."""
-    lo, hi = w.batch_range(b)
-    src, dst, t, neg = synth.host_links(w, lo, hi) if w.stateless else \
-        (x[lo:hi] for x in synth.host_links(w))
-    q = np.concatenate([src, dst, neg])
-    tq = np.concatenate([t, t, t])
-    return q[positions], tq[positions]
+CHUNK = 50_000_000
+IDS = ("nbr", "eid", "ts")
 
 
 def _log(*a):
     print("[full-size]", *a, flush=True)
 
 
-def _full_size(k, checks, per_check=400):
+def _u32(a):
+    return a.view(np.uint32) if a.dtype == np.int32 else a
+
+
+def _host_chunks(w):
+    """The host stream in order, as (first arrival index, src, dst, t, neg)."""
+    if not w.stateless:
+        yield (0, *synth.host_links(w))
+        return
+    for lo in range(0, w.links, CHUNK):
+        yield (lo, *synth.host_links(w, lo, min(w.links, lo + CHUNK)))
+
+
+def _assert_ids(g, o, what):
+    for key in IDS:
+        gv, ov = _u32(g[key]), _u32(o[key])
+        if not np.array_equal(gv, ov):
+            bad = np.argwhere(gv != ov)
+            raise AssertionError(f"{what}: {key} differs at {len(bad)} places, first {bad[:3].tolist()}")
+
+
+def _hot_nodes(w, nodes_d, count=1000, links=CHUNK):
+    """The `count` most frequent endpoints among the first `links` links."""
+    import torch
+    nb = min(w.batches, max(1, links // w.batch))
+    v = nodes_d[:3 * nb * w.batch].view(nb, 3, w.batch)[:, :2].reshape(-1).long()
+    deg = torch.bincount(v, minlength=w.num_nodes)
+    return torch.topk(deg, count).indices.int().cpu().numpy()
+
+
+def _full_size(k, checks, per_check=400, hop2_at=None, hop2_rows=2000):
     import torch
     w = synth.workload(k)
-    _log(f"workload {w.name}: {w.links} links, {w.batches} batches, checks {sorted(checks)}")
+    whole = w.num_nodes * w.s <= 10**8           # compare whole tables
+    _log(f"workload {w.name}: {w.links} links, {w.batches} batches, checks {sorted(checks)}, "
+         f"{'whole tables' if whole else 'tracked nodes'}")
     dev = torch.device("cuda", 0)
     nodes_d, ts_d = synth.device_links(w, dev)
     ef_d = synth.device_features(w, "edge", dev)
@@ -72,7 +89,25 @@ def _full_size(k, checks, per_check=400):
         if W is not None else None
     z = torch.empty((3 * w.batch, 64), dtype=torch.float32, device=dev) if W is not None else None
     rng = np.random.default_rng(100 + k)
-    kept = {}
+
+    tracked = None
+    if not whole:
+        parts = [_hot_nodes(w, nodes_d), rng.integers(0, w.num_nodes, 10**6).astype(np.int32)]
+        for b in checks:
+            _, _, _, q, _ = synth.batch_views(w, nodes_d, ts_d, b)
+            parts.append(host_np(q))
+        tracked = np.unique(np.concatenate(parts)).astype(np.int32)
+        _log(f"{len(tracked)} tracked nodes")
+    tracked_d = torch.from_numpy(tracked.astype(np.int64)).to(dev) if tracked is not None else None
+
+    def table_now():
+        """(node list or None for all, nbr, ts, eid) of the tracked rows."""
+        nbr, ts, eid = g.export()
+        if tracked_d is not None:
+            nbr, ts, eid = nbr[tracked_d], ts[tracked_d], eid[tracked_d]
+        return tracked, host_np(nbr), _u32(host_np(ts)), _u32(host_np(eid))
+
+    kept, hop2 = {}, None
     for b in range(w.batches):
         s_, d_, t_, q, tq = synth.batch_views(w, nodes_d, ts_d, b)
         if b in checks:
@@ -85,73 +120,107 @@ def _full_size(k, checks, per_check=400):
             if W is not None:
                 g.aggregate(q, tq, Wd, out=z[:n])
                 zk = host_np(z[pos_d])
-            kept[b] = (pos, host_np(q[pos_d]), {kk: host_np(v[pos_d]) for kk, v in o.items()}, zk)
+            ids = {kk: host_np(o[kk]) for kk in IDS}
+            rows = {kk: host_np(v[pos_d]) for kk, v in o.items() if kk not in IDS}
+            kept[b] = (host_np(q), pos, ids, rows, zk, table_now())
+            if b == hop2_at:
+                h2 = {kk: torch.empty((n * w.s, w.s), dtype=torch.int32, device=dev) for kk in IDS}
+                g.sample_hop2_into(o["nbr"], tq, h2)
+                r = np.sort(rng.choice(n * w.s, hop2_rows, replace=False))
+                r_d = torch.from_numpy(r).to(dev)
+                hop2 = (b, r, ids["nbr"].reshape(-1)[r], host_np(tq).view(np.uint32)[r // w.s],
+                        {kk: host_np(v[r_d]) for kk, v in h2.items()})
+                del h2
         g.insert(s_, d_, t_)
         if b % 1000 == 0:
             _log(f"gpu batch {b}")
     torch.cuda.synchronize()
     assert g.status() == 0
-    qnodes = np.unique(np.concatenate([kept[b][1] for b in kept]))
-    del z
-    nbr_d, ts_dd, eid_d = g.export()
-    idx = torch.from_numpy(qnodes.astype(np.int64)).to(dev)
-    final_gpu = (host_np(nbr_d[idx]), host_np(ts_dd[idx]).view(np.uint32),
-                 host_np(eid_d[idx]).view(np.uint32))
-    del nbr_d, ts_dd, eid_d, out, g, ef_d, nf_d, nodes_d, ts_d
+    if hop2 is not None and tracked is not None:
+        v = hop2[2]
+        tracked = np.unique(np.concatenate([tracked, v[v >= 0]])).astype(np.int32)
+        tracked_d = torch.from_numpy(tracked.astype(np.int64)).to(dev)
+    final_gpu = table_now()
+    del z, out, g, ef_d, nf_d, nodes_d, ts_d, tracked_d
     torch.cuda.empty_cache()
 
-    # ---- oracle side (host only from here)
-    mask = np.zeros(w.num_nodes, bool)
-    mask[qnodes] = True
-    _log(f"gpu done; filtering the host stream for {len(qnodes)} query nodes")
-    eids, S, D, T = _host_filtered_links(w, mask)
-    _log(f"{len(eids)} links touch them; oracle replay")
-    o = oracle.Oracle(w.num_nodes, w.s, w.alpha, w.table_seed)
+    # ---- oracle side (host only from here): the whole stream, link by link
+    o = oracle.Oracle(w.num_nodes, w.s, w.alpha, w.table_seed, keep=tracked)
     fw, fb = synth.time_params(w)
     nf = ef = None
     if w.node_dim:
         nf = np.zeros((w.num_nodes, w.node_dim), np.uint16 if w.elem_bytes("node") == 2 else np.float32)
     if w.edge_dim:
         ef = np.zeros((w.links, w.edge_dim), np.uint16 if w.elem_bytes("edge") == 2 else np.float32)
-    done = 0
-    for b in sorted(kept):
-        lo, _ = w.batch_range(b)
-        upto = int(np.searchsorted(eids, lo))
-        if upto > done:
-            o.insert_ids(eids[done:upto], S[done:upto], D[done:upto], T[done:upto])
-            done = upto
-        pos, gq, gout, gz = kept[b]
-        hq, htq = _host_queries(w, b, pos)
-        np.testing.assert_array_equal(hq, gq)   # host and device streams agree
-        # materialise the feature rows the oracle will copy
-        rn, _, re = o.export_nodes(hq)
+
+    def compare_tables(gtab, what):
+        nodes, gt = gtab[0], gtab[1:]
+        ot = o.export() if nodes is None else o.export_nodes(nodes)
+        for gv, ov, name in zip(gt, ot, ("nbr", "ts", "eid")):
+            assert np.array_equal(gv, ov), (w.name, what, "table", name, int((gv != ov).sum()))
+        return len(gt[0])
+
+    def check(b, q_all):
+        gq, pos, gids, grows, gz, gtab = kept[b]
+        np.testing.assert_array_equal(q_all[0], gq)    # host and device streams agree
+        hq, htq = q_all
+        _assert_ids(gids, o.sample(hq, htq, want=IDS), f"{w.name} batch {b}, all {len(hq)} queries")
+        n_rows = compare_tables(gtab, f"batch {b}")
+        pq, ptq = hq[pos], htq[pos]
+        rn, _, re = o.export_nodes(pq)
         if nf is not None:
-            need = np.unique(np.concatenate([hq, rn[rn >= 0]]))
+            need = np.unique(np.concatenate([pq, rn[rn >= 0]]))
             nf[need] = synth.host_feature_rows(w, "node", need)
         if ef is not None:
             need = np.unique(re[re != 0xFFFFFFFF]).astype(np.int64)
             ef[need] = synth.host_feature_rows(w, "edge", need)
-        oout = o.sample(hq, htq, fw, fb, ef, nf)
-        for key, ov in oout.items():
-            gv = gout[key]
-            if key in ("eid", "ts"):
-                gv = gv.view(np.uint32)
+        oout = o.sample(pq, ptq, fw, fb, ef, nf)
+        _assert_ids({kk: gids[kk][pos] for kk in IDS}, oout, f"{w.name} batch {b}, sampled")
+        for key, gv in grows.items():
+            ov = oout[key]
             if key == "tenc":
                 err = np.abs(gv.astype(np.float64) - ov)
                 assert err.max() <= TENC_TOL, (b, err.max())
             else:
-                assert np.array_equal(gv, ov), (k, b, key, int((gv != ov).sum()))
+                assert np.array_equal(gv, ov), (w.name, b, key, int((gv != ov).sum()))
         if gz is not None:
-            oz = o.aggregate(hq, htq, fw, fb, ef, nf, W)
+            oz = o.aggregate(pq, ptq, fw, fb, ef, nf, W)
             scale = np.sqrt(np.mean(oz ** 2))
             err = float(np.max(np.abs(gz.astype(np.float64) - oz) / (np.abs(oz) + scale)))
-            assert err <= AGG_TOL, (k, b, "aggregate", err)
+            assert err <= AGG_TOL, (w.name, b, "aggregate", err)
             _log(f"checkpoint batch {b}: aggregate scaled error {err:.2e}")
-        _log(f"checkpoint batch {b} matches")
-    o.insert_ids(eids[done:], S[done:], D[done:], T[done:])
-    for gv, ov, name in zip(final_gpu, o.export_nodes(qnodes), ("nbr", "ts", "eid")):
-        assert np.array_equal(gv, ov), (k, "final", name)
-    return len(kept), len(qnodes), len(eids)
+        if hop2 is not None and hop2[0] == b:
+            _, r, v, tq2, g2 = hop2
+            ok = v >= 0
+            o2 = o.sample(v[ok], tq2[ok], want=IDS)
+            _assert_ids({kk: g2[kk][ok] for kk in IDS}, o2, f"{w.name} batch {b}, second hop")
+            assert (g2["nbr"][~ok] == -1).all() and (_u32(g2["eid"][~ok]) == 0xFFFFFFFF).all()
+            _log(f"checkpoint batch {b}: {len(r)} second-hop answers ({int(ok.sum())} valid entries) match")
+        _log(f"checkpoint batch {b} matches: ids of {len(hq)} queries, {len(pos)} full answers, "
+             f"{n_rows} table rows")
+
+    order = sorted(kept)
+    ci = 0
+    for c0, src, dst, t, neg in _host_chunks(w):
+        c1 = c0 + len(src)
+        done = c0
+        while ci < len(order) and w.batch_range(order[ci])[0] < c1:
+            b = order[ci]
+            lo, hi = w.batch_range(b)
+            o.insert(src[done - c0:lo - c0], dst[done - c0:lo - c0], t[done - c0:lo - c0])
+            done = lo
+            if hi > c1:
+                raise AssertionError("a checkpoint batch straddles host chunks")
+            sl = slice(lo - c0, hi - c0)
+            check(b, (np.concatenate([src[sl], dst[sl], neg[sl]]), np.concatenate([t[sl]] * 3)))
+            ci += 1
+        o.insert(src[done - c0:], dst[done - c0:], t[done - c0:])
+        if c0 // CHUNK % 4 == 3:
+            _log(f"oracle at link {c1}")
+    assert ci == len(order) and o.count == w.links
+    n_rows = compare_tables(final_gpu, "final")
+    _log(f"final tables match: {n_rows} nodes x {w.s} slots")
+    return len(kept), n_rows
 
 
 @pytest.mark.timeout(600)
@@ -159,7 +228,7 @@ def test_medium_homogeneous_full_size():
     w = synth.workload(3)
     nb = w.batches
     checks = {0, 1, nb // 3, nb // 2, nb - 1}
-    assert _full_size(3, checks)[0] == len(checks)
+    assert _full_size(3, checks, hop2_at=nb // 2) == (len(checks), w.num_nodes)
 
 
 @pytest.mark.timeout(600)
@@ -167,12 +236,13 @@ def test_dense_repeated_full_size():
     w = synth.workload(4)
     nb = w.batches
     checks = {0, 5, nb // 2, nb - 2, nb - 1}
-    assert _full_size(4, checks)[0] == len(checks)
+    assert _full_size(4, checks, hop2_at=nb // 2) == (len(checks), w.num_nodes)
 
 
-@pytest.mark.timeout(900)
+@pytest.mark.timeout(1200)
 def test_large_sparse_full_size():
     w = synth.workload(5)
     nb = w.batches
     checks = {0, 1000, nb // 2, nb - 1}
-    assert _full_size(5, checks, per_check=300)[0] == len(checks)
+    n_kept, n_rows = _full_size(5, checks, per_check=300, hop2_at=nb // 2)
+    assert n_kept == len(checks) and n_rows >= 10**6

@@ -372,12 +372,14 @@ def test_errors_are_reported_not_faulted():
                       {"tenc": to_dev(np.zeros(300, np.float32))})
 
 
-@pytest.mark.parametrize("k", [1, 3])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
 def test_second_hop_matches_oracle(k):
-    """Sec. 4.4 second-hop retrieval: nlb_sample_hop2 on the first-hop
-    neighbours of a batch equals the oracle's second hop, rows and time
-    encoding included, at several points of the stream."""
-    w = synth.scaled(synth.workload(k), 30 * synth.workload(k).batch)
+    """Sec. 4.4 second-hop retrieval on every workload shape: nlb_sample_hop2
+    on the first-hop neighbours of a batch equals the oracle's second hop,
+    rows and time encoding included, at several points of the stream (30
+    batches of the workload's batch size, at most 200 000 nodes)."""
+    base = synth.workload(k)
+    w = synth.scaled(base, 30 * base.batch, num_nodes=min(base.num_nodes, 200000))
     src, dst, t, neg = synth.host_links(w)
     nodes, ts = synth.blocked(w, src, dst, t, neg)
     nodes_d, ts_d = to_dev(nodes), to_dev(ts)

@@ -268,12 +268,11 @@ def test_rnn_without_time_or_link_rows_and_rows_past_the_end():
     g2, fw2, fb2 = _small_table(N, d_time=4, edge=to_dev(ef32))
     st2 = to_dev(rng.standard_normal((N, d)).astype(np.float32))
     W2 = synth.gru_weights_for(d, 4, 8, seed=3)
-    padded = np.zeros((60 + n, 8), np.float32)   # rows 60 .. 99 real, the rest zero
-    padded[60:100] = ef32[60:100]
     pre = host_np(st2).copy()
     g2.rnn_update(to_dev(src), to_dev(dst), to_dev(t), 60, _weights_dev(W2), st2)
     torch.cuda.synchronize()
-    want = oracle.gru_update(pre, src, dst, t, 60, fw2, fb2, padded, W2)
+    # links 60 .. 99 have rows; links 100 .. 459 are past the 100-row table
+    want = oracle.gru_update(pre, src, dst, t, 60, fw2, fb2, ef32, W2)
     touched = np.unique(np.concatenate([src, dst]))
     compare_status(host_np(st2)[touched], want[touched], "rows past the end")
 

@@ -307,6 +307,37 @@ def test_filtered_substream_gives_same_rows():
 
 
 # ----------------------------------------------------------------------------- invariants
+def test_kept_node_subset_gives_the_same_rows():
+    """Tables are per node (Sec. 4.2): an oracle that keeps only some nodes'
+    tables ends with exactly the rows the full structure has for them, and
+    answers their queries identically; other nodes are refused."""
+    rng = np.random.default_rng(31)
+    N, s, E = 500, 6, 20000
+    src, dst, t = random_stream(rng, N, E, 10**6)
+    keep = np.unique(rng.integers(0, N, 60)).astype(np.int32)[::-1].copy()
+    full = Oracle(N, s, 0.4, seed=5)
+    part = Oracle(N, s, 0.4, seed=5, keep=np.concatenate([keep, keep[:5]]))
+    assert part.rows == len(keep)
+    for lo in range(0, E, 3000):
+        full.insert(src[lo:lo + 3000], dst[lo:lo + 3000], t[lo:lo + 3000])
+        part.insert(src[lo:lo + 3000], dst[lo:lo + 3000], t[lo:lo + 3000])
+        tq = np.full(len(keep), t[min(E, lo + 3000) - 1] + 1, np.uint32)
+        a = full.sample(keep, tq, want=("nbr", "eid", "ts"))
+        b = part.sample(keep, tq, want=("nbr", "eid", "ts"))
+        for k in a:
+            np.testing.assert_array_equal(a[k], b[k])
+    for x, y in zip(full.export_nodes(keep), part.export_nodes(keep)):
+        np.testing.assert_array_equal(x, y)
+    assert (full.export_nodes(keep)[0] >= 0).sum() > 100
+    other = np.setdiff1d(np.arange(N), keep)[:1].astype(np.int32)
+    with pytest.raises(ValueError):
+        part.sample(other, np.ones(1, np.uint32))
+    with pytest.raises(ValueError):
+        part.export_nodes(other)
+    with pytest.raises(ValueError):
+        part.export()
+
+
 def test_invariants_and_strict_query_mask():
     rng = np.random.default_rng(10)
     N, s, E = 100, 10, 6000
@@ -467,6 +498,35 @@ def test_sample_outputs_rows_and_zeros():
                 assert out["ts"][i, a] == 0xFFFFFFFF
                 assert not out["efeat"][i, a].any() and not out["nfeat"][i, a].any()
                 assert not out["tenc"][i, a].any()
+
+
+def test_link_rows_past_the_table_are_zero_rows():
+    """A stored link whose arrival index has no row in the link-feature
+    table (the table keeps only its first rows) gathers an all-zero row in
+    retrieval; it equals the answer for a table padded with zero rows."""
+    rng = np.random.default_rng(21)
+    N, s, E = 30, 4, 400
+    src, dst, t = random_stream(rng, N, E, 10**4)
+    o = Oracle(N, s, 0.7, seed=9)
+    o.insert(src, dst, t)
+    full = rng.standard_normal((E, 6)).astype(np.float32)
+    keep = 250
+    part = full[:keep].copy()
+    padded = np.concatenate([part, np.zeros((E - keep, 6), np.float32)])
+    nodes = rng.integers(0, N, 200).astype(np.int32)
+    tq = np.full(200, 10**4 + 1, np.uint32)
+    got = o.sample(nodes, tq, efeat=part, want=("eid", "efeat"))
+    want = o.sample(nodes, tq, efeat=padded, want=("eid", "efeat"))
+    np.testing.assert_array_equal(got["efeat"], want["efeat"])
+    late = (got["eid"] != 0xFFFFFFFF) & (got["eid"] >= keep)
+    early = (got["eid"] != 0xFFFFFFFF) & (got["eid"] < keep)
+    assert late.sum() > 50 and early.sum() > 50
+    assert not got["efeat"][late].any()
+    np.testing.assert_array_equal(got["efeat"][early], full[got["eid"][early]])
+    hop1 = o.sample(nodes[:20], tq[:20], want=("nbr",))["nbr"]
+    g2 = o.sample_hop2(hop1, tq[:20], efeat=part, want=("efeat",))
+    w2 = o.sample_hop2(hop1, tq[:20], efeat=padded, want=("efeat",))
+    np.testing.assert_array_equal(g2["efeat"], w2["efeat"])
 
 
 def test_theorem2_nlb_node_product_form():
@@ -657,6 +717,41 @@ def test_aggregate_constant_messages_ignore_attention():
     np.testing.assert_allclose(z[~any_valid], np.broadcast_to(z[~any_valid][0], z[~any_valid].shape),
                                rtol=0, atol=1e-12)
     assert np.abs(z[any_valid][0] - z[~any_valid][0]).max() > 1e-6
+
+
+def test_aggregate_and_gru_take_zero_rows_past_the_link_table():
+    """Eq. (4) and the status GRU see a link without a row in the (partial)
+    link-feature table as a zero row: the same result as a zero-padded
+    table."""
+    import synth
+    rng = np.random.default_rng(5)
+    N, s, E = 100, 8, 2000
+    src, dst, t = random_stream(rng, N, E, 10**5)
+    w = synth.scaled(synth.workload(1), 10)
+    W = synth.agg_weights(w)
+    ef = rng.standard_normal((E, w.edge_dim)).astype(np.float32)
+    keep = 1200
+    padded = ef.copy()
+    padded[keep:] = 0.0
+    fw, fb = synth.time_params(w)
+    o = Oracle(N, s, 0.5, seed=2)
+    o.insert(src, dst, t)
+    q = rng.integers(0, N, 200).astype(np.int32)
+    tq = np.full(200, 2 * 10**5, np.uint32)
+    z_part = o.aggregate(q, tq, fw, fb, ef[:keep], None, W)
+    np.testing.assert_array_equal(z_part, o.aggregate(q, tq, fw, fb, padded, None, W))
+    assert np.abs(z_part - o.aggregate(q, tq, fw, fb, ef, None, W)).max() > 1e-6
+    d = 16
+    G = synth.gru_weights_for(d, w.d_time, w.edge_dim, seed=7)
+    st0 = rng.standard_normal((N, d)).astype(np.float32)
+    lo = keep - 100
+    a, b_ = st0.copy(), st0.copy()
+    oracle.gru_update(a, src[lo:lo + 200], dst[lo:lo + 200], t[lo:lo + 200], lo, fw, fb, ef[:keep], G)
+    oracle.gru_update(b_, src[lo:lo + 200], dst[lo:lo + 200], t[lo:lo + 200], lo, fw, fb, padded, G)
+    np.testing.assert_array_equal(a, b_)
+    c = st0.copy()
+    oracle.gru_update(c, src[lo:lo + 200], dst[lo:lo + 200], t[lo:lo + 200], lo, fw, fb, ef, G)
+    assert np.abs(a - c).max() > 1e-6
 
 
 def _bf16_to_f64(bits):
