@@ -61,6 +61,8 @@ extern "C" {
 #define NLB_EDEVICE 3  /* no usable GPU, or a HIP call failed */
 #define NLB_EORDER 4   /* (nlb_status) timestamps decreased, or a timestamp >= 2^30 */
 #define NLB_ERANGE 5   /* node id outside [0, num_nodes), or more than 2^32-1 links */
+#define NLB_ESCRATCH 6 /* nlb_rnn_update_noalloc: the call needs more working memory than the
+                          library's static array holds */
 
 /* Key choice of Sec. 4.2. */
 #define NLB_KEY_EDGE 0 /* key (neighbour, time): slot by eq. (2) */
@@ -284,6 +286,29 @@ typedef struct nlb_gru_weights {
 
 int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, const uint32_t *t, uint32_t n,
                    uint64_t first_eid, const nlb_gru_weights *wts, void *status, void *stream);
+
+/* nlb_rnn_update for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, kernels and results; it allocates and frees nothing
+ * (device memory, host-pinned memory or library workspaces) and sets no
+ * memory with hipMemset: its working memory -- the winner word of each of
+ * the table's N nodes (8 B), a list of 16 B per pair row, and 2 n candidate
+ * status rows -- lives in one static device array of NLB_NOALLOC_SCRATCH
+ * bytes per device, which the library holds until the process ends.  The
+ * call needs align256(8 N) + align256(16 (2 n) + 256) + 2 n * status row
+ * bytes of it, and returns NLB_ESCRATCH when that exceeds the array
+ * (nothing is enqueued then).  Every call on a device shares that device's
+ * array: the call clears what it needs cleared (the winner words, with a
+ * fill kernel) and keeps no state across calls, but calls that overlap in
+ * time on one device -- other streams, other threads, other tables -- race
+ * and must be ordered by the caller.  Besides the NLB_ESCRATCH case, errors
+ * are those of nlb_rnn_update.  The first call on a device looks up the
+ * array's device address (hipGetSymbolAddress) with that device current. */
+#define NLB_NOALLOC_SCRATCH (64u << 20)
+
+int nlb_rnn_update_noalloc(nlb_table *h, const int32_t *src, const int32_t *dst, const uint32_t *t,
+                           uint32_t n, uint64_t first_eid, const nlb_gru_weights *wts, void *status,
+                           void *stream);
 
 /* Free the table's device memory after synchronising its device.  NULL is a
  * no-op.  Borrowed buffers are not touched. */

@@ -17,13 +17,14 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libnlb.so")
 
-NLB_OK, NLB_EINVAL, NLB_ENOMEM, NLB_EDEVICE, NLB_EORDER, NLB_ERANGE = range(6)
+NLB_OK, NLB_EINVAL, NLB_ENOMEM, NLB_EDEVICE, NLB_EORDER, NLB_ERANGE, NLB_ESCRATCH = range(7)
+NOALLOC_SCRATCH = 64 << 20
 KEY_EDGE, KEY_NODE = 0, 1
 MAX_SLOTS = 1024
 
 # Symbols declared in include/nlb.h.
 ABI_SYMBOLS = ("nlb_create", "nlb_insert_batch", "nlb_sample", "nlb_sample_hop2", "nlb_aggregate",
-               "nlb_rnn_update", "nlb_destroy", "nlb_get_info", "nlb_export", "nlb_status",
+               "nlb_rnn_update", "nlb_rnn_update_noalloc", "nlb_destroy", "nlb_get_info", "nlb_export", "nlb_status",
                "nlb_strerror")
 AGG_HIDDEN = 64
 RNN_MAX_DIM = 1024
@@ -102,6 +103,8 @@ def load_library(path: str = LIB_PATH):
     lib.nlb_aggregate.restype = I
     lib.nlb_rnn_update.argtypes = [P, P, P, P, U32, U64, ctypes.POINTER(_GruWeights), P, P]
     lib.nlb_rnn_update.restype = I
+    lib.nlb_rnn_update_noalloc.argtypes = [P, P, P, P, U32, U64, ctypes.POINTER(_GruWeights), P, P]
+    lib.nlb_rnn_update_noalloc.restype = I
     lib.nlb_destroy.argtypes = [P]
     lib.nlb_destroy.restype = I
     lib.nlb_get_info.argtypes = [P, ctypes.POINTER(_Info)]
@@ -279,12 +282,15 @@ class Table:
                "nlb_aggregate")
         return out
 
-    def rnn_update(self, src, dst, t, first_eid: int, weights: dict, status, stream=None):
+    def rnn_update(self, src, dst, t, first_eid: int, weights: dict, status, stream=None,
+                   noalloc: bool = False):
         """Node-status GRU update of Sec. 4.4 after the links (src[i], dst[i],
         t[i]) whose link rows are first_eid + i, in place on ``status`` (a
         CUDA tensor [N, d], fp32 or bf16 -- e.g. this table's node_feat).
         ``weights``: w_ih, w_hh (bf16, or 16-bit ints holding bf16 bits, padded
-        layouts of include/nlb.h) and b_ih, b_hh (fp32)."""
+        layouts of include/nlb.h) and b_ih, b_hh (fp32).  ``noalloc`` calls
+        nlb_rnn_update_noalloc (working memory in the library's static
+        array; NLBError with NLB_ESCRATCH when it does not fit)."""
         import torch
         n = int(src.numel())
         if dst.numel() != n or t.numel() != n:
@@ -302,10 +308,11 @@ class Table:
             setattr(gw, k, _dev_ptr(weights[k], 2, k))
         for k in ("b_ih", "b_hh"):
             setattr(gw, k, _dev_ptr(weights[k], 4, k))
-        _check(self._lib.nlb_rnn_update(self._h, _dev_ptr(src, 4, "src"), _dev_ptr(dst, 4, "dst"),
-                                        _dev_ptr(t, 4, "t"), n, int(first_eid), ctypes.byref(gw),
-                                        _dev_ptr(status, None, "status"), _stream_ptr(stream)),
-               "nlb_rnn_update")
+        fn, name = ((self._lib.nlb_rnn_update_noalloc, "nlb_rnn_update_noalloc") if noalloc
+                    else (self._lib.nlb_rnn_update, "nlb_rnn_update"))
+        _check(fn(self._h, _dev_ptr(src, 4, "src"), _dev_ptr(dst, 4, "dst"), _dev_ptr(t, 4, "t"), n,
+                  int(first_eid), ctypes.byref(gw), _dev_ptr(status, None, "status"), _stream_ptr(stream)),
+               name)
         return status
 
     def alloc_outputs(self, nq: int, want=("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self")):

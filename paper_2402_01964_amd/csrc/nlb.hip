@@ -495,6 +495,7 @@ const char *nlb_strerror(int code) {
         case NLB_EDEVICE: return "no usable GPU or HIP failure";
         case NLB_EORDER: return "timestamp out of order or >= 2^30";
         case NLB_ERANGE: return "node id or arrival index out of range";
+        case NLB_ESCRATCH: return "working memory beyond the static array of the allocation-free call";
         default: return "unknown error";
     }
 }

@@ -50,6 +50,7 @@
 // two steps before their products.
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 
 #include "nlb_internal.h"
 #include "nlb_pieces.h"
@@ -1171,11 +1172,89 @@ int rnn_reserve(nlb_table *h, uint64_t pair_rows, uint32_t srb) {
     return NLB_OK;
 }
 
+// Working memory of one update: the winner word of every node, the winner
+// count and list, and the candidate rows.  Codes in `winner` carry the call
+// number in their high word (epoch_hi), so an array that is not cleared
+// between calls only needs codes of earlier calls to be smaller.
+struct RnnWork {
+    unsigned long long *winner;
+    uint64_t epoch_hi;
+    bool clear_winner;    // zero winner[0 .. N) first (memory shared with other calls)
+    uint8_t *cand;
+    uint32_t *list;       // word 0: winner count; from word 64: the winners, 4 words each
+};
+
+// Working memory of the table, grown on demand (nlb_rnn_update).
+int table_work(nlb_table *h, uint64_t pairs, uint32_t srb, hipStream_t stream, RnnWork *wk) {
+    int rc = rnn_reserve(h, pairs, srb);
+    if (rc != NLB_OK) return rc;
+    if (h->rnn_epoch == 0xFFFFFFFFu) {
+        hipLaunchKernelGGL(rnn_clear, dim3(4096), dim3(kRnnThreads), 0, stream, h->rnn_winner,
+                           (uint64_t)h->num_nodes);
+        h->rnn_epoch = 0;
+    }
+    h->rnn_epoch++;
+    *wk = {h->rnn_winner, (uint64_t)h->rnn_epoch << 32, false, h->rnn_cand, h->rnn_list};
+    return NLB_OK;
+}
+
+// ---------------------------------------------------------------- static working memory
+// nlb_rnn_update_noalloc works in this array instead of memory of the
+// table's: every call on a device shares that device's copy (it keeps the
+// last call's contents, and calls that overlap on one device race).  Each
+// device holds its own copy at its own address, which hipGetSymbolAddress
+// returns with that device current; host code uses only those addresses
+// (the array's name on the host is not a device address).
+constexpr size_t kScratchBytes = NLB_NOALLOC_SCRATCH;
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mutex;
+uint8_t *g_scratch_addr[kScratchDevices];
+
+// Device address of `scratch` on `dev` (the current device), looked up on
+// the first call for that device.
+int scratch_address(int dev, uint8_t **out) {
+    if (dev < 0 || dev >= kScratchDevices) return NLB_EDEVICE;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_addr[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+            (void)hipGetLastError();
+            return NLB_EDEVICE;
+        }
+        g_scratch_addr[dev] = (uint8_t *)ptr;
+    }
+    *out = g_scratch_addr[dev];
+    return NLB_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// The update's working memory carved from `scratch`: winner words of all N
+// nodes, the list, the candidate rows.  The winner words are cleared by a
+// fill kernel at the start of every call.
+int scratch_work(nlb_table *h, uint64_t pairs, uint32_t srb, RnnWork *wk) {
+    const size_t winner_bytes = align256((size_t)h->num_nodes * 8u);
+    const size_t list_bytes = align256(((size_t)pairs * 4u + 64u) * 4u);
+    const size_t cand_bytes = (size_t)pairs * srb;
+    if (winner_bytes + list_bytes + cand_bytes > kScratchBytes) return NLB_ESCRATCH;
+    uint8_t *base = nullptr;
+    const int rc = scratch_address(h->device, &base);
+    if (rc != NLB_OK) return rc;
+    *wk = {(unsigned long long *)base, 1ull << 32, true, base + winner_bytes + list_bytes,
+           (uint32_t *)(base + winner_bytes)};
+    return NLB_OK;
+}
+
 }  // namespace
 
-extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, const uint32_t *t,
-                              uint32_t n, uint64_t first_eid, const nlb_gru_weights *wts, void *status,
-                              void *stream) {
+// Both entry points: argument checks, the GRU form and tile shape, the
+// working memory (the table's own, grown on demand, or the static array),
+// then the four launches.
+static int rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, const uint32_t *t, uint32_t n,
+                      uint64_t first_eid, const nlb_gru_weights *wts, void *status, void *stream,
+                      bool use_scratch) {
     if (!h || !wts) return NLB_EINVAL;
     if (n == 0) return NLB_OK;
     if (!src || !dst || !t || !status) return NLB_EINVAL;
@@ -1277,29 +1356,30 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
         gru_layout(p, 16u * nb);
     }
 
-    int rc = rnn_reserve(h, pairs, p.srb);
+    RnnWork wk;
+    const int rc = use_scratch ? scratch_work(h, pairs, p.srb, &wk)
+                               : table_work(h, pairs, p.srb, (hipStream_t)stream, &wk);
     if (rc != NLB_OK) return rc;
-    if (h->rnn_epoch == 0xFFFFFFFFu) {
-        hipLaunchKernelGGL(rnn_clear, dim3(4096), dim3(kRnnThreads), 0, (hipStream_t)stream, h->rnn_winner,
-                           (uint64_t)h->num_nodes);
-        h->rnn_epoch = 0;
+    if (wk.clear_winner) {
+        const uint64_t blocks = std::min<uint64_t>(4096, ((uint64_t)h->num_nodes + kRnnThreads - 1) / kRnnThreads);
+        hipLaunchKernelGGL(rnn_clear, dim3((unsigned)blocks), dim3(kRnnThreads), 0, (hipStream_t)stream,
+                           wk.winner, (uint64_t)h->num_nodes);
     }
-    h->rnn_epoch++;
-    const uint64_t epoch_hi = (uint64_t)h->rnn_epoch << 32;
-    uint32_t *count = h->rnn_list;
-    u32x4 *list = (u32x4 *)(h->rnn_list + 64);
+    const uint64_t epoch_hi = wk.epoch_hi;
+    uint32_t *count = wk.list;
+    u32x4 *list = (u32x4 *)(wk.list + 64);
     p.list = list;
     p.count = count;
-    p.cand = h->rnn_cand;
+    p.cand = wk.cand;
 
-    ResolveParams rp = {src, dst, n, h->num_nodes, h->rnn_winner, epoch_hi, h->status, count};
+    ResolveParams rp = {src, dst, n, h->num_nodes, wk.winner, epoch_hi, h->status, count};
     if (n >= kMergeMinBatch)
         hipLaunchKernelGGL(rnn_resolve_merged, dim3((n + kResolveLinks - 1) / kResolveLinks),
                            dim3(kMergeThreads), 0, (hipStream_t)stream, rp);
     else
         hipLaunchKernelGGL(rnn_resolve, dim3((n + kRnnThreads - 1) / kRnnThreads), dim3(kRnnThreads), 0,
                            (hipStream_t)stream, rp);
-    SelectParams sp = {src, dst, n, h->num_nodes, h->rnn_winner, epoch_hi, list, count};
+    SelectParams sp = {src, dst, n, h->num_nodes, wk.winner, epoch_hi, list, count};
     hipLaunchKernelGGL(rnn_select, dim3((unsigned)((pairs + kSelectRows - 1) / kSelectRows)),
                        dim3(kRnnThreads), 0, (hipStream_t)stream, sp);
     if (ws) {
@@ -1335,7 +1415,7 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     h->rnn_form = ws ? NLB_RNN_FORM_WEIGHT_STATIONARY : NLB_RNN_FORM_TILED;
     uint32_t w = 2;
     for (uint32_t c = 16; c >= 4; c /= 2)
-        if (p.srb % c == 0 && (uintptr_t)status % c == 0 && (uintptr_t)h->rnn_cand % c == 0) {
+        if (p.srb % c == 0 && (uintptr_t)status % c == 0 && (uintptr_t)wk.cand % c == 0) {
             w = c;
             break;
         }
@@ -1345,8 +1425,20 @@ extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *d
     const uint64_t per = lg <= 6 ? 64u >> lg : 1u;                       // rows per wavefront pass
     const uint64_t blocks = ((pairs + per - 1) / per * 64u + kRnnThreads - 1) / kRnnThreads;
     hipLaunchKernelGGL(rnn_scatter, dim3((unsigned)(blocks < 65536 ? blocks : 65536)),
-                       dim3(kRnnThreads), 0, (hipStream_t)stream, (const uint8_t *)h->rnn_cand,
+                       dim3(kRnnThreads), 0, (hipStream_t)stream, (const uint8_t *)wk.cand,
                        (const u32x4 *)list, (const uint32_t *)count, (uint8_t *)status, p.srb, w, upr, lg);
     if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
     return NLB_OK;
+}
+
+extern "C" int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, const uint32_t *t,
+                              uint32_t n, uint64_t first_eid, const nlb_gru_weights *wts, void *status,
+                              void *stream) {
+    return rnn_update(h, src, dst, t, n, first_eid, wts, status, stream, false);
+}
+
+extern "C" int nlb_rnn_update_noalloc(nlb_table *h, const int32_t *src, const int32_t *dst, const uint32_t *t,
+                                      uint32_t n, uint64_t first_eid, const nlb_gru_weights *wts, void *status,
+                                      void *stream) {
+    return rnn_update(h, src, dst, t, n, first_eid, wts, status, stream, true);
 }

@@ -65,7 +65,7 @@ def test_null_arguments():
 
 def test_strerror():
     assert nlb.strerror(nlb.NLB_OK) == "success"
-    for c in range(1, 6):
+    for c in range(1, 7):
         assert nlb.strerror(c) and nlb.strerror(c) != "unknown error"
     assert nlb.strerror(77) == "unknown error"
 
