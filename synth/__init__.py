@@ -238,9 +238,12 @@ def _host_tables(w: Workload):
 
 
 # ----------------------------------------------------------------------------- streams
-def host_links(w: Workload, i0: int = 0, i1: int | None = None, threads: int | None = None):
+def host_links(w: Workload, i0: int = 0, i1: int | None = None, threads: int | None = None,
+               out=None):
     """Links [i0, i1) as numpy (src, dst, t, neg).  Stateful workloads (2, 3)
-    are only generated whole."""
+    are only generated whole.  ``out``: four contiguous arrays of i1 - i0
+    elements (int32, int32, uint32 or int32 bits, int32) to write into, e.g.
+    views of pinned host memory."""
     i1 = w.links if i1 is None else int(i1)
     if not w.stateless and (i0 != 0 or i1 != w.links):
         raise ValueError("workloads with repeats or bursty time are generated whole")
@@ -248,8 +251,14 @@ def host_links(w: Workload, i0: int = 0, i1: int | None = None, threads: int | N
     a, b = _host_tables(w)
     st = _stream_struct(w, ((_p(a[0]), _p(a[1])), (_p(b[0]), _p(b[1]))))
     n = i1 - i0
-    src, dst, neg = (np.empty(n, np.int32) for _ in range(3))
-    t = np.empty(n, np.uint32)
+    if out is None:
+        src, dst, neg = (np.empty(n, np.int32) for _ in range(3))
+        t = np.empty(n, np.uint32)
+    else:
+        src, dst, t, neg = out
+        for x in out:
+            if len(x) != n or x.itemsize != 4 or not x.flags.c_contiguous:
+                raise ValueError("out: four contiguous 4-byte arrays of the range's length")
     lib.syn_links_host(ctypes.byref(st), i0, i1, _p(src), _p(dst), _p(t), _p(neg),
                        threads or host_threads())
     if w.repeat:
