@@ -428,6 +428,21 @@ __device__ __forceinline__ void mfma4(f32x4 (&acc)[4], const __bf16 *W, uint32_t
     }
 }
 
+// The same product with the activations as the A operand and the weights as
+// B (both operands hold the same registers as in mfma4): D = X W^T, the
+// layer's output transposed -- lane l holds rows 4 (l / 16) + i of unit
+// 16 ub + l % 16.
+__device__ __forceinline__ void mfma4t(f32x4 (&acc)[4], const __bf16 *W, uint32_t ls, uint32_t k0,
+                                       uint32_t r16, uint32_t g, const bf16x8 &hi, const bf16x8 &lo,
+                                       bool use_lo) {
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++) {
+        const bf16x8 a = *(const bf16x8 *)(W + (16u * ub + r16) * ls + k0 + 8u * g);
+        acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, a, acc[ub], 0, 0, 0);
+        if (use_lo) acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, a, acc[ub], 0, 0, 0);
+    }
+}
+
 // act (a layer's output in the D layout, 64 units) -> next layer through
 // weights whose 64 columns from k0 on are in chained order (row stride ls):
 // out[ub] += Wp x act.
@@ -539,7 +554,7 @@ __device__ __forceinline__ void piece_operand(const Piece8<KIND> &r, uint32_t di
 // offset, all k-loops unroll and each segment's loads have one fixed form.
 // Queries are taken in groups of p.gq <= 16 (one MLP_out block each).
 template <int NKS, int EKS, int TKS, int NK, int EK>
-__global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void aggregate_rows(RowParams p) {
     constexpr int GS = NKS + EKS, K1S = GS + TKS, K3S = NKS + 2;
     using L = RowsLayout<K1S, K3S, TKS>;
     static_assert(NKS <= kRuSteps, "shape");
@@ -622,6 +637,14 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
     __bf16 *Tt = (__bf16 *)(smem + L::o_t) + (size_t)wave * 16u * L::ts;
     u32x2 *rl = (u32x2 *)(smem + L::o_rl) + wave * 16u;
     const float *b1 = vec, *b2 = vec + kH, *b3 = vec + 2 * kH, *b4 = vec + 3 * kH, *va = vec + 4 * kH;
+    // This lane's unit column of layer 1 (16 ub + r16): its bias and its
+    // weight in the logits.
+    float b1v[4], vav[4];
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++) {
+        b1v[ub] = b1[16 * ub + r16];
+        vav[ub] = va[16 * ub + r16];
+    }
     const uint32_t gq = p.gq;
     const uint64_t groups = ((uint64_t)p.nq + gq - 1) / gq;
     const uint64_t gstep = (uint64_t)gridDim.x * (kRowThreads / 64);
@@ -719,15 +742,22 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
     uint32_t cq = 0, cb = 0, cnq = group_size(g0);
     // Query ids of the compute group for MLP_out (lanes r16 >= cnq unused).
     int32_t mo_nd = p.node[min(g0 * gq + r16, (uint64_t)p.nq - 1)];
-    float m = -INFINITY, den = 0.0f;
-    // Running softmax sums of the current query, and the group's finished
-    // aggregates sum_s alpha_s a1_s: query q's in the lanes with r16 == q, in
-    // the D layout (units 16 ub + 4 g + i), with ne = 1 where the query had a
-    // valid row (else its aggregate is zero).
-    f32x4 agg[4], aggq[4];
-    float ne = 0.0f;
+    // Layer 1 runs transposed (mfma4t): lane l holds rows 4 g + i of unit
+    // 16 ub + r16.  The online softmax of the current query is kept per lane
+    // group g, over its rows 4 g .. 4 g + 3 of each block: running maximum m,
+    // sum of exponentials den, and agg, the exponential-weighted sums of this
+    // lane's unit column.  At the query's end the four groups are combined
+    // into aggd, the group's finished aggregates sum_s alpha_s a1_s: query
+    // q's in the lanes with r16 == q, in the D layout (units 16 ub + 4 g + i),
+    // with ne = 1 where the query had a valid row (else its aggregate is zero).
+    float m = -INFINITY, den = 0.0f, ne = 0.0f;
+    float agg[4];
+    f32x4 aggd[4];
 #pragma unroll
-    for (int ub = 0; ub < 4; ub++) agg[ub] = aggq[ub] = f32x4(0.0f);
+    for (int ub = 0; ub < 4; ub++) {
+        agg[ub] = 0.0f;
+        aggd[ub] = f32x4(0.0f);
+    }
     while (cg < groups) {
         // Keeps the LDS-resident biases from being hoisted into long-lived
         // registers.
@@ -761,18 +791,18 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
         // Layer 1: a1 = ReLU(W1 x + b1).
         f32x4 acc[4];
 #pragma unroll
-        for (int ub = 0; ub < 4; ub++) acc[ub] = *(const f32x4 *)(b1 + 16 * ub + 4 * g);   // + b1
+        for (int ub = 0; ub < 4; ub++) acc[ub] = f32x4(b1v[ub]);   // + b1
 #pragma unroll
         for (int ks = 0; ks < NKS; ks++) {
             bf16x8 hi, lo;
             piece_operand<NK>(rows_c.n[ks], p.n_dim, 32u * ks + 8u * g, valid, hi, lo);
-            mfma4(acc, W1, L::ls1, 32u * ks, r16, g, hi, lo, NK == kF32Vec);
+            mfma4t(acc, W1, L::ls1, 32u * ks, r16, g, hi, lo, NK == kF32Vec);
         }
 #pragma unroll
         for (int ks = 0; ks < EKS; ks++) {
             bf16x8 hi, lo;
             piece_operand<EK>(rows_c.e[ks], p.e_dim, 32u * ks + 8u * g, ev, hi, lo);
-            mfma4(acc, W1, L::ls1, 32u * (NKS + ks), r16, g, hi, lo, EK == kF32Vec);
+            mfma4t(acc, W1, L::ls1, 32u * (NKS + ks), r16, g, hi, lo, EK == kF32Vec);
         }
         // Time encodings.  A block with few valid rows computes only those:
         // its (valid row, 4-column chunk) items are spread over the 64 lanes,
@@ -819,7 +849,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
                 for (int ks = 0; ks < TKS; ks++) {
                     const bf16x8 hi = *(const bf16x8 *)(Tt + r16 * L::ts + 32u * ks + 8u * g);
                     const bf16x8 lo = *(const bf16x8 *)(Tt + r16 * L::ts + 32u * TKS + 32u * ks + 8u * g);
-                    mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
+                    mfma4t(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
                 }
             } else if (fast) {
 #pragma unroll 1
@@ -835,7 +865,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
                     }
                     bf16x8 hi, lo;
                     split8(t, hi, lo);
-                    mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
+                    mfma4t(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
                 }
             } else {
 #pragma unroll 1
@@ -846,7 +876,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
                     for (int i = 0; i < 8; i++) t[i] = cos_fp32(__builtin_fmaf(tw[k + i], sl.dt, tb[k + i]));
                     bf16x8 hi, lo;
                     split8(t, hi, lo);
-                    mfma4(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
+                    mfma4t(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
                 }
             }
         }
@@ -854,51 +884,71 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
         for (int ub = 0; ub < 4; ub++)
 #pragma unroll
             for (int i = 0; i < 4; i++) acc[ub][i] = relu(acc[ub][i]);
-        // The row's logit v . a1 (up to the common shift att . b2).
-        float part = 0.0f;
+        // The logits v . a1 of rows 4 g + i (up to the common shift att . b2):
+        // this lane's unit column's share, summed over the 16 lanes of its
+        // group.
+        float lg[4];
 #pragma unroll
-        for (int ub = 0; ub < 4; ub++)
+        for (int i = 0; i < 4; i++) {
+            float t = vav[0] * acc[0][i];
 #pragma unroll
-            for (int i = 0; i < 4; i++) part = __builtin_fmaf(va[16 * ub + 4 * g + i], acc[ub][i], part);
-        part += __shfl_xor(part, 16);
-        part += __shfl_xor(part, 32);
-        // Online softmax over the query's valid rows (a block without a valid
-        // row changes nothing; the test is wave-uniform).
-        const float lg = valid ? part : -INFINITY;
-        const float mb = xor16_max(lg);
-        if (mb != -INFINITY) {
-            const float mn = max2(m, mb);
-            // exp(x) as the hardware 2^(x log2 e): x <= 0 here, and the
-            // rounding of the product adds a relative error of |x| 2^-24.
-            const float sc = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m - mn) * kLog2eAgg);
-            const float e = valid ? __builtin_amdgcn_exp2f((lg - mn) * kLog2eAgg) : 0.0f;
-            den = den * sc + xor16_sum(e);
-#pragma unroll
-            for (int ub = 0; ub < 4; ub++)
-#pragma unroll
-                for (int i = 0; i < 4; i++) agg[ub][i] = agg[ub][i] * sc + xor16_sum(e * acc[ub][i]);
-            m = mn;
+            for (int ub = 1; ub < 4; ub++) t = __builtin_fmaf(vav[ub], acc[ub][i], t);
+            lg[i] = xor16_sum(t);
         }
+        // Online softmax over the group's valid rows: an invalid row's logit
+        // is -inf (weight 0), and a group without a valid row so far keeps
+        // m = -inf, den = 0.  exp(x - mn) is the hardware 2^(x log2 e -
+        // mn log2 e), one fused multiply-add: its rounding adds a relative
+        // error of about |mn| 2^-24.
+        const uint32_t nib = ((uint32_t)__builtin_amdgcn_ballot_w64(valid) >> (4u * g)) & 0xFu;
+#pragma unroll
+        for (int i = 0; i < 4; i++) lg[i] = ((nib >> i) & 1u) ? lg[i] : -INFINITY;
+        const float mn = max2(m, max2(max2(lg[0], lg[1]), max2(lg[2], lg[3])));
+        const float shift = (mn == -INFINITY) ? 0.0f : mn * kLog2eAgg;
+        const float sc = __builtin_amdgcn_exp2f(__builtin_fmaf(m, kLog2eAgg, -shift));
+        float e[4];
+#pragma unroll
+        for (int i = 0; i < 4; i++) e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(lg[i], kLog2eAgg, -shift));
+        den = __builtin_fmaf(den, sc, (e[0] + e[1]) + (e[2] + e[3]));
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) {
+            float t = agg[ub] * sc;
+#pragma unroll
+            for (int i = 0; i < 4; i++) t = __builtin_fmaf(e[i], acc[ub][i], t);
+            agg[ub] = t;
+        }
+        m = mn;
         }
         if (last_blk) {
-            // The sums are the same in every lane of a row group: the lanes
-            // of row cq keep them, normalised.
-            if (r16 == cq) {
-                const float inv = den > 0.0f ? 1.0f / den : 0.0f;
+            // The query's four lane groups combined: with M the largest group
+            // maximum, group g's share is r_g = exp(m_g - M) / sum_g' den_g'
+            // exp(m_g' - M), and aggd[ub] += A B with A[unit][k = g] = agg of
+            // lane (g, unit) and B[k = g][n] = r_g for n == cq, else 0.  In
+            // v_mfma_f32_16x16x4f32 lane l holds A[l % 16][l / 16], B[l / 16]
+            // [l % 16] and D[4 (l / 16) + i][l % 16]: the product sums the
+            // groups, normalises, and leaves query cq's aggregate in column cq
+            // of the D layout.
+            float M = max2(m, __shfl_xor(m, 16));
+            M = max2(M, __shfl_xor(M, 32));
+            const float shift = (M == -INFINITY) ? 0.0f : M * kLog2eAgg;
+            const float r = __builtin_amdgcn_exp2f(__builtin_fmaf(m, kLog2eAgg, -shift));
+            float ds = den * r;
+            ds += __shfl_xor(ds, 16);
+            ds += __shfl_xor(ds, 32);
+            const float f = ds > 0.0f ? r * __builtin_amdgcn_rcpf(ds) : 0.0f;
+            const float bq = r16 == cq ? f : 0.0f;
 #pragma unroll
-                for (int ub = 0; ub < 4; ub++)
-#pragma unroll
-                    for (int i = 0; i < 4; i++) aggq[ub][i] = agg[ub][i] * inv;
-                ne = den > 0.0f ? 1.0f : 0.0f;
-            }
+            for (int ub = 0; ub < 4; ub++)
+                aggd[ub] = __builtin_amdgcn_mfma_f32_16x16x4f32(agg[ub], bq, aggd[ub], 0, 0, 0);
+            if (r16 == cq) ne = ds > 0.0f ? 1.0f : 0.0f;
             m = -INFINITY;
             den = 0.0f;
 #pragma unroll
-            for (int ub = 0; ub < 4; ub++) agg[ub] = f32x4(0.0f);
+            for (int ub = 0; ub < 4; ub++) agg[ub] = 0.0f;
         }
         if (group_end) {
             // MLP_out for the group: row r16 = query qb + r16, input
-            // [r_u | aggregate], the aggregate w2 aggq + b2 (zero for a query
+            // [r_u | aggregate], the aggregate w2 aggd + b2 (zero for a query
             // without valid rows).
             const uint64_t qb = cg * gq;
             if (vq && g == 0 && nr < 0) atomicOr(p.status, kStatusRange);   // an out-of-range query
@@ -914,7 +964,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
             f32x4 hq[4];
 #pragma unroll
             for (int ub = 0; ub < 4; ub++) hq[ub] = f32x4(0.0f);
-            chain64(hq, aggq, W2, kPs, 0, r16, g);
+            chain64(hq, aggd, W2, kPs, 0, r16, g);
 #pragma unroll
             for (int ub = 0; ub < 4; ub++)
 #pragma unroll
@@ -937,7 +987,7 @@ __global__ __launch_bounds__(kRowThreads) void aggregate_rows(RowParams p) {
                 }
             }
 #pragma unroll
-            for (int ub = 0; ub < 4; ub++) aggq[ub] = f32x4(0.0f);
+            for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
             ne = 0.0f;
             cg += gstep;
             cq = 0;
