@@ -47,12 +47,17 @@ _lib = None
 
 
 def _load():
+    """The built oracle; NLB_ORACLE_LIB names another build of nlb_oracle.c
+    to load instead (the sanitizer build of tests/test_sanitizers.py)."""
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-        build()
-    lib = ctypes.CDLL(_LIB)
+    path = os.environ.get("NLB_ORACLE_LIB")
+    if path is None:
+        path = _LIB
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+    lib = ctypes.CDLL(path)
     P = ctypes.c_void_p
     i32, i64, u32, u64, dbl = (ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32,
                                ctypes.c_uint64, ctypes.c_double)

@@ -75,12 +75,15 @@ class _Info(ctypes.Structure):
 _lib = None
 
 
-def load_library(path: str = LIB_PATH):
-    """Load libnlb.so.  Fails loudly when it has not been built: there is no
-    other implementation to fall back to."""
+def load_library(path: str | None = None):
+    """Load libnlb.so (or the build named by NLB_LIBRARY, e.g. a sanitizer
+    build of the same sources).  Fails loudly when it has not been built:
+    there is no other implementation to fall back to."""
     global _lib
     if _lib is not None:
         return _lib
+    if path is None:
+        path = os.environ.get("NLB_LIBRARY", LIB_PATH)
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with "
                           f"`python -m paper_2402_01964_amd.build` (hipcc, gfx950)")

@@ -462,6 +462,16 @@ __device__ __forceinline__ void chain64(f32x4 (&out)[4], const f32x4 (&act)[4], 
     }
 }
 
+// cos of an fp32 argument with |x| < kCosFastLimit, as cos_fp32_small but
+// with the revolutions reduced by v_fract_f64 (y - floor(y), exact in
+// double) instead of a rounding and a subtraction: one instruction fewer.
+// The fraction lies in [0, 1); its rounding to fp32 adds at most 2^-25 of a
+// revolution.
+__device__ __forceinline__ float cos_fast(float x) {
+    const double y = (double)x * 0.15915494309189533577;
+    return __builtin_amdgcn_cosf((float)__builtin_amdgcn_fract(y));
+}
+
 // Reductions over the 16 lanes of a DPP row (the 16 rows of a block), with
 // the result in every lane: pair lanes by quad permutations (swap
 // neighbours, then pairs), then mirror within each half-row and the row.
@@ -835,7 +845,7 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
                         const f32x4 wv = *(const f32x4 *)(tw + 4u * c), bv = *(const f32x4 *)(tb + 4u * c);
                         float t[4];
 #pragma unroll
-                        for (int i = 0; i < 4; i++) t[i] = cos_fp32_small(__builtin_fmaf(wv[i], dt, bv[i]));
+                        for (int i = 0; i < 4; i++) t[i] = cos_fast(__builtin_fmaf(wv[i], dt, bv[i]));
                         u32x2 hw, lw;
                         split4(t, hw, lw);
                         *(u32x2 *)(Tt + e[0] * L::ts + 4u * c) = hw;
@@ -860,8 +870,8 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
                     float t[8];
 #pragma unroll
                     for (int i = 0; i < 4; i++) {
-                        t[i] = cos_fp32_small(__builtin_fmaf(w0[i], sl.dt, c0[i]));
-                        t[4 + i] = cos_fp32_small(__builtin_fmaf(w1[i], sl.dt, c1[i]));
+                        t[i] = cos_fast(__builtin_fmaf(w0[i], sl.dt, c0[i]));
+                        t[4 + i] = cos_fast(__builtin_fmaf(w1[i], sl.dt, c1[i]));
                     }
                     bf16x8 hi, lo;
                     split8(t, hi, lo);

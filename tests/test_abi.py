@@ -23,7 +23,7 @@ def test_header_declares_the_binding_symbols():
 
 
 def test_library_exports_every_declared_symbol():
-    lib = ctypes.CDLL(nlb.LIB_PATH)
+    lib = nlb.load_library()
     for name in _declared():
         assert hasattr(lib, name), name
 

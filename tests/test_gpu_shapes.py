@@ -132,3 +132,60 @@ def test_link_rows_past_the_table(k):
     _log(f"workload {k}: aggregate with partial link rows, scaled error {err:.2e}")
     assert err <= 2e-4
     assert g.status() == 0
+
+
+@pytest.mark.parametrize("sweep", ["reduced-domain", "wide-arguments"])
+def test_device_cosine_dense_sweep(sweep):
+    """The library's fp32 cosine against the oracle's cosine in double of
+    the same fp32 argument (App. C time encoding), through nlb_sample, by
+    band of |x|: <= 5e-7 below 1e9; <= 2.5e-6 up to 2^33, where the double
+    product x / (2 pi) is off by up to 2.7e-7 of a revolution; <= 1e-6
+    beyond (the exact wide-argument route); <= 1e-5 (the interface's bound)
+    everywhere.  reduced-domain: w = 0 and 65 532 phases b covering
+    [-pi, pi] densely, so the argument is b itself (the whole reduced domain
+    of [-1/2, 1/2] revolution); wide-arguments: log-spaced frequencies
+    1e-9 .. 10 and 80 time gaps from 1 to 2^32 - 1, arguments up to 4e10
+    (beyond 2^33 the wide-argument route).  Both launch paths: with the
+    timestamp output (time-encoding stream, >= 2^20 float4 outputs) and
+    without it (the sample kernel's own phase)."""
+    import paper_2402_01964_amd as nlb
+    import torch
+    D, nq = 65532, 80                               # 80 x 16 383 float4 >= 2^20
+    rng = np.random.default_rng(77)
+    if sweep == "reduced-domain":
+        fw = np.zeros(D, np.float32)
+        fb = np.linspace(-np.pi, np.pi, D).astype(np.float32)
+        dt = np.arange(1, nq + 1, dtype=np.uint64)
+    else:
+        fw = np.logspace(-9, 1, D).astype(np.float32)
+        fb = rng.uniform(-np.pi, np.pi, D).astype(np.float32)
+        dt = np.unique(np.concatenate([
+            [1, 2, 3, 7, 1000, 65535, 65536, 65537, 10**6 + 3, 2**24 + 1, 10**8 - 1, 2**30 - 1, 2**31,
+             2**32 - 1], rng.integers(1, 2**32, nq)]).astype(np.uint64))[:nq]
+    assert len(dt) == nq
+    g = nlb.Table(2, 1, 1.0, 5, time_w=to_dev(fw), time_b=to_dev(fb))
+    g.insert(to_dev(np.zeros(1, np.int32)), to_dev(np.ones(1, np.int32)), to_dev(np.zeros(1, np.uint32)))
+    q = np.zeros(nq, np.int32)
+    tq = dt.astype(np.uint32)                      # the stored link has t' = 0
+    a = g.sample(to_dev(q), to_dev(tq), want=("ts", "tenc"))
+    b = g.sample(to_dev(q), to_dev(tq), want=("tenc",))
+    torch.cuda.synchronize()
+    o = oracle.Oracle(2, 1, 1.0, 5)
+    o.insert([0], [1], [0])
+    want = o.sample(q, tq, fw, fb, want=("nbr", "tenc"))
+    assert (want["nbr"] >= 0).all()
+    ref = want["tenc"].astype(np.float64)
+    # |x| of each argument (w dt is exact in double for fp32 w and dt)
+    x = np.abs(fw.astype(np.float64)[None, :] * dt.astype(np.float32).astype(np.float64)[:, None]
+               + fb.astype(np.float64)[None, :]).reshape(nq, 1, D)
+    bands = ((0.0, 1e9, 5e-7), (1e9, 2.0**33, 2.5e-6), (2.0**33, np.inf, 1e-6))
+    for name, got in (("stream", a["tenc"]), ("sample kernel", b["tenc"])):
+        err = np.abs(got.cpu().numpy().astype(np.float64) - ref)
+        assert err.max() <= 1e-5, (sweep, name, float(err.max()))
+        for lo, hi, tol in bands:
+            sel = (x >= lo) & (x < hi)
+            if sel.any():
+                e = float(err[sel].max())
+                _log(f"cosine sweep {sweep}, {name} path, {lo:.0e} <= |x| < {hi:.0e}: {int(sel.sum())} "
+                     f"values, max abs error {e:.2e}")
+                assert e <= tol, (sweep, name, lo, e)

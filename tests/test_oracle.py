@@ -393,6 +393,26 @@ def test_survival_law_over_seeds(alpha):
     assert z.max() < 4.5, (z.max(), freq[z.argmax()], p[z.argmax()])
 
 
+@pytest.mark.parametrize("alpha", [0.3, 0.7])
+def test_same_key_offer_is_an_ordinary_collision(alpha):
+    """NLB-node (eq. (3)): a later link with the same neighbour maps to the
+    same slot.  Theorem 2's proof (App. B) inserts every other temporal
+    neighbour with probability alpha, so the second of two links from v to u
+    replaces the first in a fraction alpha of seeds; a same-key-always-
+    overwrites reading would give 1.  Binomial z-test over 20 000 seeds."""
+    K = 20000
+    hits = 0
+    for seed in range(K):
+        o = Oracle(4, 3, alpha, seed=seed, key_mode=1)
+        o.insert([0, 0], [1, 1], [5, 9])
+        nbr, ts, eid = o.export_nodes([0])
+        held = eid[0][nbr[0] == 1]
+        assert len(held) == 1
+        hits += int(held[0] == 1)
+    z = (hits - K * alpha) / math.sqrt(K * alpha * (1 - alpha))
+    assert abs(z) < 4.5, (hits / K, alpha)
+
+
 def test_theorem1_poisson_hub_survival():
     """Theorem 1 (NLB-edge achieves recent sampling): with Poisson(lambda)
     arrivals at a hub, a link that entered S_u at t_i is still there at t
