@@ -121,7 +121,9 @@ typedef struct nlb_info {
     int32_t key_mode;
     uint64_t threshold;     /* floor(alpha * 2^32), or 2^32 for alpha == 1 */
     uint64_t q1, q2;
-    uint64_t interactions;  /* links inserted so far = arrival index of the next link */
+    uint64_t interactions;  /* links inserted so far = arrival index of the next link, as
+                               counted by eager calls; nlb_status refreshes it from the
+                               device count, which also counts graph replays */
     int64_t table_bytes;    /* device bytes owned by the table */
     int32_t block_bytes;    /* bytes of one node's slot block */
     int32_t device;
@@ -154,8 +156,12 @@ int nlb_create(const nlb_config *cfg, nlb_table **out);
  * nlb_status, but still consume their arrival index.  n == 0 is a no-op.
  * Errors: NLB_EINVAL (NULL table or array with n > 0; n >= 2^31),
  * NLB_ERANGE (the arrival index would exceed 2^32-2), NLB_EDEVICE (launch
- * failure).  The arrival indices are assigned on the host at the call, so a
- * captured insert must not be replayed. */
+ * failure).  The kernels take the batch's arrival indices from a link count
+ * kept on the device and advance it (the host keeps its own count for the
+ * NLB_ERANGE test and nlb_get_info), so the call may be captured in a HIP
+ * graph: every replay inserts its links as the next links of the stream
+ * (a replay that would pass 2^32 - 1 links is skipped and flagged for
+ * nlb_status as NLB_ERANGE). */
 int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst,
                      const uint32_t *t, uint32_t n, void *stream);
 
@@ -242,8 +248,12 @@ int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_
  * r_u <- RNN([r_u, r_v, t, e]) and r_v <- RNN([r_v, r_u, t, e]), for a batch
  * of n links (src, dst, t: device arrays of n elements) whose link-feature
  * rows are first_eid .. first_eid + n - 1 of the table's link rows (rows at
- * or past edge_rows read as zeros).  The RNN is a GRU cell with input
- * x = [r_other ; T-enc(t) ; e] and hidden state h = r_self:
+ * or past edge_rows read as zeros); first_eid = NLB_EID_LAST_BATCH takes the
+ * arrival indices of the n links inserted last (the table's device link
+ * count when the update runs, minus n), as a step that inserts a batch and
+ * then updates the statuses needs, also when replayed from a HIP graph.
+ * The RNN is a GRU cell with input x = [r_other ; T-enc(t) ; e] and hidden
+ * state h = r_self:
  *   r = sigmoid(W_ir x + b_ir + W_hr h + b_hr)
  *   z = sigmoid(W_iz x + b_iz + W_hz h + b_hz)
  *   n = tanh(W_in x + b_in + r * (W_hn h + b_hn))
@@ -268,11 +278,16 @@ int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_
  * double, a bf16 one within one bf16 rounding of it.  Calls on one table
  * must be ordered (same stream): they share the table's working buffers,
  * which the first call (and a larger batch) allocates.  n == 0 is a no-op.
+ * Graph capture: a call that allocates (see above) must not be captured;
+ * once an earlier call on the table has sized the working memory for at
+ * least n links, the call only enqueues kernels and may be captured and
+ * replayed (no call number or host-side state is involved; with
+ * first_eid = NLB_EID_LAST_BATCH it follows the inserts replayed before it).
  * Errors: NLB_EINVAL (NULL table, weights or array with n > 0; n >= 2^31;
  * bad dtype or dimension; misaligned pointers; a 16-row tile that does not
- * fit the LDS), NLB_ENOMEM, NLB_EDEVICE.  Not for graph replay: each call
- * takes a new host-side call number that tags its working buffers. */
+ * fit the LDS), NLB_ENOMEM, NLB_EDEVICE. */
 #define NLB_RNN_MAX_DIM 1024
+#define NLB_EID_LAST_BATCH UINT64_MAX
 
 typedef struct nlb_gru_weights {
     int32_t status_dim;      /* d, 1 .. NLB_RNN_MAX_DIM */
@@ -323,8 +338,10 @@ int nlb_get_info(const nlb_table *h, nlb_info *info);
 int nlb_export(nlb_table *h, int32_t *nbr, uint32_t *ts, uint32_t *eid, void *stream);
 
 /* Synchronise `stream`, then return and clear the errors kernels recorded
- * since the last call: NLB_OK, NLB_ERANGE (node id out of range) or
- * NLB_EORDER (timestamp >= 2^30 or decreasing); NLB_ERANGE wins when both. */
+ * since the last call: NLB_OK, NLB_ERANGE (node id out of range, or a
+ * replayed insert past 2^32 - 1 links) or NLB_EORDER (timestamp >= 2^30 or
+ * decreasing); NLB_ERANGE wins when both.  Also refreshes the link count of
+ * nlb_get_info from the device. */
 int nlb_status(nlb_table *h, void *stream);
 
 /* Static description of a return code. */

@@ -30,6 +30,7 @@ AGG_HIDDEN = 64
 RNN_MAX_DIM = 1024
 DTYPE_F32, DTYPE_BF16 = 0, 1
 RNN_FORM_NONE, RNN_FORM_TILED, RNN_FORM_WEIGHT_STATIONARY = 0, 1, 2
+EID_LAST_BATCH = 2**64 - 1   # first_eid of rnn_update: the links inserted last (device count)
 
 
 class NLBError(RuntimeError):

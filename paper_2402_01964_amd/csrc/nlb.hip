@@ -28,7 +28,6 @@ struct InsertParams {
     const int32_t *dst;
     const uint32_t *t;
     uint32_t n;
-    uint32_t e0;          // arrival index of link 0 of the batch
     uint8_t *blocks;
     uint32_t block_bytes;
     uint32_t s;
@@ -38,9 +37,31 @@ struct InsertParams {
     uint64_t mod_m;       // nlb_div_magic(s), for nlb_mod
     uint32_t q1r, q2r;    // q1 mod s, q2 mod s
     uint32_t key_mode;
-    uint32_t *status;
-    uint32_t parity;      // batch counter & 1
+    uint32_t *status;     // device status words (nlb_internal.h)
 };
+
+// The batch's place in the stream, read from the device status words at
+// the start of each insert kernel (the link count by insert_resolve, its copy
+// for the batch in flight by insert_commit): e0 = arrival index of link 0,
+// and whether the batch fits the 32-bit arrival indices (a batch that does
+// not is skipped and flagged).
+struct BatchPos {
+    uint32_t e0;
+    bool ok;
+};
+
+__device__ __forceinline__ BatchPos batch_pos(const InsertParams &p, uint32_t word) {
+    const uint64_t links = *(const uint64_t *)(p.status + word);
+    BatchPos b;
+    b.e0 = (uint32_t)links;
+    b.ok = links + p.n <= 0xFFFFFFFFull;
+    return b;
+}
+
+// insert_resolve's record of the batch in flight, for insert_commit.
+__device__ __forceinline__ void record_batch(const InsertParams &p, const BatchPos &bp) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) *(uint64_t *)(p.status + kWordBatch) = bp.e0;
+}
 
 // Slot of neighbour x at time t: eq. (2) (q1*x + q2*t) mod s, or eq. (3)
 // q1*x mod s, evaluated on residues (exact: both products are < s^2).
@@ -80,18 +101,17 @@ __device__ __forceinline__ bool link_ok(const InsertParams &p, int32_t u, int32_
 // Returns false when the link is skipped.
 // link_offers_of takes the link's already-loaded u, v, t and the previous
 // link's timestamp.
-__device__ __forceinline__ bool link_offers_of(const InsertParams &p, uint32_t i, int32_t u, int32_t v,
-                                               uint32_t t, uint32_t prev_t, uint64_t &ou, uint64_t &wu,
-                                               uint64_t &ov, uint64_t &wv) {
+__device__ __forceinline__ bool link_offers_of(const InsertParams &p, const BatchPos &bp, uint32_t i, int32_t u,
+                                               int32_t v, uint32_t t, uint32_t prev_t, uint64_t &ou,
+                                               uint64_t &wu, uint64_t &ov, uint64_t &wv) {
     uint32_t flags = 0;
     if (u < 0 || v < 0 || (int64_t)u >= p.num_nodes || (int64_t)v >= p.num_nodes)
         flags |= kStatusRange;
     if (t > kTimeMask) flags |= kStatusOrder;
     if (t < prev_t) flags |= kStatusOrder;
     if (flags) atomicOr(p.status, flags);
-    if (i == p.n - 1) p.status[1 + p.parity] = t;
     if (!link_ok(p, u, v, t)) return false;
-    const uint32_t e = p.e0 + i;
+    const uint32_t e = bp.e0 + i;
     // Sec. 4.2: S_u receives (v, t, e); S_v receives (u, t, e).
     ou = (uint64_t)u * p.block_bytes + 8u * slot_of(p, (uint32_t)v, t);
     ov = (uint64_t)v * p.block_bytes + 8u * slot_of(p, (uint32_t)u, t);
@@ -100,20 +120,28 @@ __device__ __forceinline__ bool link_offers_of(const InsertParams &p, uint32_t i
     return true;
 }
 
+// The previous link's timestamp (for link 0, the last of the previous batch,
+// which insert_commit records).
 __device__ __forceinline__ uint32_t prev_time(const InsertParams &p, uint32_t i) {
-    return (i > 0) ? p.t[i - 1] : p.status[1 + (p.parity ^ 1u)];
+    return (i > 0) ? p.t[i - 1] : p.status[kWordLastT];
 }
 
-__device__ __forceinline__ bool link_offers(const InsertParams &p, uint32_t i, uint64_t &ou,
-                                            uint64_t &wu, uint64_t &ov, uint64_t &wv) {
-    return link_offers_of(p, i, p.src[i], p.dst[i], p.t[i], prev_time(p, i), ou, wu, ov, wv);
+__device__ __forceinline__ bool link_offers(const InsertParams &p, const BatchPos &bp, uint32_t i,
+                                            uint64_t &ou, uint64_t &wu, uint64_t &ov, uint64_t &wv) {
+    return link_offers_of(p, bp, i, p.src[i], p.dst[i], p.t[i], prev_time(p, i), ou, wu, ov, wv);
 }
 
 __global__ __launch_bounds__(kInsertThreads) void insert_resolve(InsertParams p) {
     const uint32_t i = blockIdx.x * kInsertThreads + threadIdx.x;
+    const BatchPos bp = batch_pos(p, kWordLinks);
+    record_batch(p, bp);
+    if (!bp.ok) {
+        if (i == 0) atomicOr(p.status, kStatusRange);
+        return;
+    }
     if (i >= p.n) return;
     uint64_t ou, wu, ov, wv;
-    if (!link_offers(p, i, ou, wu, ov, wv)) return;
+    if (!link_offers(p, bp, i, ou, wu, ov, wv)) return;
     atomicMax((unsigned long long *)(p.blocks + ou), (unsigned long long)wu);
     atomicMax((unsigned long long *)(p.blocks + ov), (unsigned long long)wv);
 }
@@ -126,6 +154,12 @@ __global__ __launch_bounds__(kMergeThreads) void insert_resolve_merged(InsertPar
         merge_word[k] = 0ull;
     }
     __syncthreads();
+    const BatchPos bp = batch_pos(p, kWordLinks);
+    record_batch(p, bp);
+    if (!bp.ok) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(p.status, kStatusRange);
+        return;   // uniform over the grid: no workgroup waits at a later barrier
+    }
     // All of a thread's links are loaded (a link past the batch re-reads
     // the last one, unused) before any is merged.
     constexpr int RR = kResolveLinks / kMergeThreads;
@@ -145,7 +179,7 @@ __global__ __launch_bounds__(kMergeThreads) void insert_resolve_merged(InsertPar
         const uint32_t i = first + r * kMergeThreads + threadIdx.x;
         if (i >= p.n) break;
         uint64_t ou, wu, ov, wv;
-        if (link_offers_of(p, i, uu[r], vv[r], tt[r], pt[r], ou, wu, ov, wv)) {
+        if (link_offers_of(p, bp, i, uu[r], vv[r], tt[r], pt[r], ou, wu, ov, wv)) {
             merge_max(merge_off, merge_word, ou, wu);
             merge_max(merge_off, merge_word, ov, wv);
         }
@@ -157,24 +191,32 @@ __global__ __launch_bounds__(kMergeThreads) void insert_resolve_merged(InsertPar
     }
 }
 
+// Pass 2, also the batch's end: it reads the batch position insert_resolve
+// recorded and advances the link count and the last timestamp for the next
+// batch (words no workgroup of this kernel reads).
 __global__ __launch_bounds__(kInsertThreads) void insert_commit(InsertParams p) {
     const uint32_t i = blockIdx.x * kInsertThreads + threadIdx.x;
-    if (i >= p.n) return;
-    const int32_t u = p.src[i];
-    const int32_t v = p.dst[i];
-    const uint32_t t = p.t[i];
-    if (!link_ok(p, u, v, t)) return;
-    const uint32_t e = p.e0 + i;
-    const uint32_t au = slot_of(p, (uint32_t)v, t);
-    const uint32_t av = slot_of(p, (uint32_t)u, t);
-    uint8_t *bu = p.blocks + (size_t)u * p.block_bytes;
-    uint8_t *bv = p.blocks + (size_t)v * p.block_bytes;
-    const uint64_t wu = ((const uint64_t *)bu)[au];
-    const uint64_t wv = ((const uint64_t *)bv)[av];
-    // Exactly one offer owns each surviving word (a self-loop's two offers
-    // may share one; they write the same id).
-    if (wu == offer_word(p, e, 0, t)) ((int32_t *)(bu + 8u * p.s))[au] = v;
-    if (wv == offer_word(p, e, 1, t)) ((int32_t *)(bv + 8u * p.s))[av] = u;
+    const BatchPos bp = batch_pos(p, kWordBatch);
+    if (bp.ok && i == 0) *(uint64_t *)(p.status + kWordLinks) = (uint64_t)bp.e0 + p.n;
+    if (bp.ok && i == p.n - 1) p.status[kWordLastT] = p.t[i];
+    if (bp.ok && i < p.n) {
+        const int32_t u = p.src[i];
+        const int32_t v = p.dst[i];
+        const uint32_t t = p.t[i];
+        if (link_ok(p, u, v, t)) {
+            const uint32_t e = bp.e0 + i;
+            const uint32_t au = slot_of(p, (uint32_t)v, t);
+            const uint32_t av = slot_of(p, (uint32_t)u, t);
+            uint8_t *bu = p.blocks + (size_t)u * p.block_bytes;
+            uint8_t *bv = p.blocks + (size_t)v * p.block_bytes;
+            const uint64_t wu = ((const uint64_t *)bu)[au];
+            const uint64_t wv = ((const uint64_t *)bv)[av];
+            // Exactly one offer owns each surviving word (a self-loop's two
+            // offers may share one; they write the same id).
+            if (wu == offer_word(p, e, 0, t)) ((int32_t *)(bu + 8u * p.s))[au] = v;
+            if (wv == offer_word(p, e, 1, t)) ((int32_t *)(bv + 8u * p.s))[av] = u;
+        }
+    }
 }
 
 // ---------------------------------------------------------------- sample
@@ -603,6 +645,7 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const
     if (!src || !dst || !t) return NLB_EINVAL;
     // link and thread indices of the kernels are 32-bit
     if (n >= (1u << 31)) return NLB_EINVAL;
+    // (the kernels make the same test on the device count, for replays)
     if (h->interactions + n > 0xFFFFFFFFull) return NLB_ERANGE;
     DeviceGuard guard(h->device);
     if (!guard.ok()) return NLB_EDEVICE;
@@ -611,7 +654,6 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const
     p.dst = dst;
     p.t = t;
     p.n = n;
-    p.e0 = (uint32_t)h->interactions;
     p.blocks = h->blocks;
     p.block_bytes = h->block_bytes;
     p.s = h->s;
@@ -623,7 +665,6 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const
     p.q2r = (uint32_t)(h->q2 % h->s);
     p.key_mode = (uint32_t)h->key_mode;
     p.status = h->status;
-    p.parity = (uint32_t)(h->batches & 1);
     const hipStream_t st = (hipStream_t)stream;
     if (n >= kMergeMinBatch)
         hipLaunchKernelGGL(insert_resolve_merged, dim3((n + kResolveLinks - 1) / kResolveLinks),
@@ -635,7 +676,6 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const
                        dim3(kInsertThreads), 0, st, p);
     if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
     h->interactions += n;
-    h->batches += 1;
     return NLB_OK;
 }
 
@@ -747,9 +787,12 @@ int nlb_status(nlb_table *h, void *stream) {
     DeviceGuard guard(h->device);
     if (!guard.ok()) return NLB_EDEVICE;
     if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return NLB_EDEVICE;
-    uint32_t flags = 0;
-    if (hipMemcpy(&flags, h->status, sizeof(flags), hipMemcpyDeviceToHost) != hipSuccess)
+    uint32_t words[8];
+    if (hipMemcpy(words, h->status, sizeof(words), hipMemcpyDeviceToHost) != hipSuccess)
         return NLB_EDEVICE;
+    const uint32_t flags = words[0];
+    // inserts replayed from graphs advance only the device count
+    h->interactions = (uint64_t)words[kWordLinks] | ((uint64_t)words[kWordLinks + 1] << 32);
     if (flags) {
         const uint32_t zero = 0;
         if (hipMemcpy(h->status, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess)

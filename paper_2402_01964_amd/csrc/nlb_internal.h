@@ -41,10 +41,20 @@ constexpr uint32_t kTimeBits = 30;
 constexpr uint32_t kTimeMask = (1u << kTimeBits) - 1u;
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;  // SplitMix64 state increment
 
-// Device status words, kept after the slot blocks.
-constexpr uint32_t kStatusRange = 1u;   // node id out of range
+// Device status words, kept after the slot blocks (32-bit words):
+//   [0]     error flags (kStatusRange | kStatusOrder)
+//   [1]     timestamp of the last link inserted so far
+//   [4..5]  first arrival index of the batch in flight (64-bit; written by
+//           insert_resolve, read by insert_commit)
+//   [6..7]  links inserted so far (64-bit): the next batch's first arrival
+//           index (read by insert_resolve, advanced by insert_commit)
+// No kernel writes a word its own workgroups read, so the two insert kernels
+// keep the stream position on the device without atomics or a last-finisher
+// test, and an insert replayed from a captured HIP graph continues the stream.
+constexpr uint32_t kStatusRange = 1u;   // node id out of range, or the arrival index would pass 2^32 - 2
 constexpr uint32_t kStatusOrder = 2u;   // timestamp >= 2^30 or decreasing
-constexpr size_t kStatusBytes = 256;    // [0] flags, [1..2] last timestamp per batch parity
+constexpr uint32_t kWordLastT = 1, kWordBatch = 4, kWordLinks = 6;
+constexpr size_t kStatusBytes = 256;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -273,11 +283,9 @@ struct nlb_table {
     size_t table_bytes;
     uint32_t block_bytes;
     uint32_t *status;
-    uint64_t interactions;
-    uint64_t batches;
+    uint64_t interactions;            // links enqueued by eager calls (refreshed by nlb_status)
     // Node-status update (rnn.hip), allocated on first use.
-    unsigned long long *rnn_winner;   // [N] latest pair-row code per node
-    uint32_t rnn_epoch;               // calls since the winner array was cleared
+    unsigned long long *rnn_winner;   // [N] latest pair-row code per node, zero between calls
     int32_t rnn_form;                 // GRU pass of the last update (NLB_RNN_FORM_*)
     uint8_t *rnn_cand;                // candidate status rows by pair row
     size_t rnn_cand_bytes;

@@ -12,11 +12,11 @@
 // endpoint's).
 //
 // Four launches per batch:
-//   resolve  each endpoint offers the code epoch << 32 | (2i + k + 1) of its
-//            pair row (link i, endpoint k) to winner[node] with a 64-bit
-//            atomic maximum; codes of earlier calls are smaller, so the array
-//            is never cleared.  Large batches merge their offers per node in
-//            LDS first (merge_max), as the table insertion does.
+//   resolve  each endpoint offers the code 2i + k + 1 of its pair row (link
+//            i, endpoint k) to winner[node] with a 64-bit atomic maximum (the
+//            array is all zero between calls: the scatter clears the words it
+//            has used).  Large batches merge their offers per node in LDS
+//            first (merge_max), as the table insertion does.
 //   select   each pair row checks whether it won; the winners are appended
 //            to a dense list (one atomic per wavefront).  The list order
 //            varies from run to run; the results do not, because every row
@@ -31,7 +31,10 @@
 //            happen in registers, and the new status goes to a candidate
 //            buffer indexed by pair row.
 //   scatter  copies each listed winner's candidate row over its node's
-//            status.
+//            status and clears the node's winner word.  Every node a valid
+//            link touches has exactly one winner, so this restores the all-
+//            zero array; no call number is needed, and a call captured in a
+//            HIP graph can be replayed.
 // The candidate buffer is what lets the gru pass read only pre-batch
 // statuses: no status is written until every workgroup has read its inputs.
 //
@@ -69,7 +72,6 @@ struct ResolveParams {
     uint32_t n;
     int64_t num_nodes;
     unsigned long long *winner;
-    uint64_t epoch_hi;
     uint32_t *status;
     uint32_t *count;      // winners listed by select; zeroed here
 };
@@ -87,8 +89,8 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_resolve(ResolveParams p) {
         atomicOr(p.status, kStatusRange);
         return;
     }
-    atomicMax(&p.winner[u], (unsigned long long)(p.epoch_hi | (2ull * i + 1)));
-    atomicMax(&p.winner[v], (unsigned long long)(p.epoch_hi | (2ull * i + 2)));
+    atomicMax(&p.winner[u], (unsigned long long)(2ull * i + 1));
+    atomicMax(&p.winner[v], (unsigned long long)(2ull * i + 2));
 }
 
 __global__ __launch_bounds__(kMergeThreads) void rnn_resolve_merged(ResolveParams p) {
@@ -120,8 +122,8 @@ __global__ __launch_bounds__(kMergeThreads) void rnn_resolve_merged(ResolveParam
             atomicOr(p.status, kStatusRange);
             continue;
         }
-        merge_max(merge_off, merge_word, 8ull * (uint32_t)u, p.epoch_hi | (2ull * i + 1));
-        merge_max(merge_off, merge_word, 8ull * (uint32_t)v, p.epoch_hi | (2ull * i + 2));
+        merge_max(merge_off, merge_word, 8ull * (uint32_t)u, 2ull * i + 1);
+        merge_max(merge_off, merge_word, 8ull * (uint32_t)v, 2ull * i + 2);
     }
     __syncthreads();
     for (int k = threadIdx.x; k < kMergeEntries; k += kMergeThreads) {
@@ -136,7 +138,6 @@ struct SelectParams {
     uint32_t n;
     int64_t num_nodes;
     const unsigned long long *winner;
-    uint64_t epoch_hi;
     u32x4 *list;          // winners, dense: {pair row, self, other, 0}
     uint32_t *count;
 };
@@ -183,7 +184,7 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_select(SelectParams p) {
             if (endpoints_ok(u, v, p.num_nodes)) {
                 self = (r & 1) ? v : u;
                 other = (r & 1) ? u : v;
-                win = wv[q] == (p.epoch_hi | (r + 1));
+                win = wv[q] == r + 1;
             }
         }
         const uint64_t mask = __ballot(win);
@@ -210,7 +211,8 @@ struct GruParams {
     int64_t num_nodes;
     const u32x4 *list;                  // winners {pair row, self, other, 0} (select)
     const uint32_t *count;
-    uint64_t first_eid;                 // arrival index (link-row index) of link 0
+    uint64_t first_eid;                 // arrival index (link-row index) of link 0, or NLB_EID_LAST_BATCH
+    const uint32_t *table_status;       // the table's device status words (its link count)
     uint32_t d, d_time;
     const float *tw, *tb;               // time encoding
     uint32_t t_vec;                     // tw, tb 16-byte aligned
@@ -235,6 +237,15 @@ struct GruParams {
     const __bf16 *w_ih, *w_hh;
     const float *b_ih, *b_hh;
 };
+
+// Arrival index of link 0 of the batch: given, or (NLB_EID_LAST_BATCH) the
+// table's device link count minus n -- the batch inserted last -- read when
+// the kernel runs, so that a captured update follows the inserts replayed
+// before it.
+__device__ __forceinline__ uint64_t first_eid_of(const GruParams &p) {
+    if (p.first_eid != NLB_EID_LAST_BATCH) return p.first_eid;
+    return *(const uint64_t *)(p.table_status + kWordLinks) - p.n;
+}
 
 __device__ __forceinline__ void store_hi8(const float v[8], __bf16 *hi) {
     bf16x8 h;
@@ -367,6 +378,7 @@ __device__ __forceinline__ void gru_fill(const GruParams &p, uint32_t m, const u
                                          const int32_t *m_self, const int32_t *m_other, const float *m_t,
                                          const float *s_tw, const float *s_tb, __bf16 *Xh, __bf16 *Xl,
                                          __bf16 *Hh, __bf16 *Hl, uint32_t xs, uint32_t ls, uint32_t hs) {
+    const uint64_t first_eid = first_eid_of(p);
     constexpr uint32_t R = 16 * NB;
     // Input units (8 columns each) whose loads a thread keeps in flight
     // together (generic path): about all of its units for the common widths.
@@ -436,7 +448,7 @@ __device__ __forceinline__ void gru_fill(const GruParams &p, uint32_t m, const u
             const uint32_t ge = (p.kx - p.off_e) / 8;
             auto edge_fill = [&](auto kind) {
                 constexpr int K = decltype(kind)::value;
-                auto eid_of = [&](uint32_t j) { return p.first_eid + (m_row[j < m ? j : 0] >> 1); };
+                auto eid_of = [&](uint32_t j) { return first_eid + (m_row[j < m ? j : 0] >> 1); };
                 fill_seg<K, 8>(
                     R * ge, ge, p.ge_m, p.e_dim,
                     [&](uint32_t j) {
@@ -516,7 +528,7 @@ __device__ __forceinline__ void gru_fill(const GruParams &p, uint32_t m, const u
                 for (int i = 0; i < 8; i++)
                     if (k + i < p.d_time) v[f][i] = cos_fp32(__builtin_fmaf(wk[i], tf, bk[i]));
             } else {
-                const uint64_t e = p.first_eid + link;
+                const uint64_t e = first_eid + link;
                 if (e < (uint64_t)p.edge_rows)
                     load8(p.efeat + (size_t)e * p.erb, p.e_dim, p.e_bf16, p.e_vec, c0 - p.off_e, v[f]);
             }
@@ -747,6 +759,7 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
 
     const uint32_t tid = threadIdx.x, lane = tid & 63;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint64_t first_eid = first_eid_of(p);
     const bool second = wave >= (uint32_t)KH;   // shares its SIMD with wavefront wave - KH
     const uint32_t lr = lane & 15, lk = (lane >> 4) * 8;
     const uint32_t count = *p.count;
@@ -858,7 +871,7 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
             auto edge_fill = [&](auto kind) __attribute__((always_inline)) {
                 constexpr int K = decltype(kind)::value;
                 auto eid_of = [&](uint32_t jj) __attribute__((always_inline)) {
-                    return p.first_eid + (meta[slot * MS + jj][0] >> 1);
+                    return first_eid + (meta[slot * MS + jj][0] >> 1);
                 };
                 fill_seg<K, 4, T>(
                     R * ge, ge, p.ge_m, p.e_dim,
@@ -1088,11 +1101,13 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
 
 // Status rows of the winners: for each listed winner {pair row r, node},
 // candidate row r -> status row node, in units of `w` bytes (upr units per
-// row).  A wavefront pass copies 64 >> lg rows (lg = ceil(log2 upr) <= 6),
-// or one row in passes of 64 units; wavefronts stride over the list.
+// row), and winner[node] = 0.  A wavefront pass copies 64 >> lg rows
+// (lg = ceil(log2 upr) <= 6), or one row in passes of 64 units; wavefronts
+// stride over the list.
 __global__ __launch_bounds__(kRnnThreads) void rnn_scatter(const uint8_t *cand, const u32x4 *list,
                                                           const uint32_t *count, uint8_t *st, uint32_t srb,
-                                                          uint32_t w, uint32_t upr, uint32_t lg) {
+                                                          uint32_t w, uint32_t upr, uint32_t lg,
+                                                          unsigned long long *winner) {
     const uint32_t n = *count, lane = threadIdx.x & 63;
     const uint64_t gw = ((uint64_t)blockIdx.x * kRnnThreads + threadIdx.x) >> 6;
     const uint64_t nw = ((uint64_t)gridDim.x * kRnnThreads) >> 6;
@@ -1108,6 +1123,7 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_scatter(const uint8_t *cand, 
             *(uint32_t *)to = *(const uint32_t *)from;
         else
             *(uint16_t *)to = *(const uint16_t *)from;
+        if (c == 0) winner[e[1]] = 0ull;
     };
     if (lg <= 6) {
         const uint32_t per = 64u >> lg, c = lane & ((1u << lg) - 1u);
@@ -1119,7 +1135,7 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_scatter(const uint8_t *cand, 
     }
 }
 
-// Zero fill of the winner array (on the rare wrap of the call counter).
+// Zero fill of a winner array (the static one of the allocation-free call).
 __global__ __launch_bounds__(kRnnThreads) void rnn_clear(unsigned long long *a, uint64_t n) {
     for (uint64_t i = (uint64_t)blockIdx.x * kRnnThreads + threadIdx.x; i < n;
          i += (uint64_t)gridDim.x * kRnnThreads)
@@ -1145,7 +1161,6 @@ int rnn_reserve(nlb_table *h, uint64_t pair_rows, uint32_t srb) {
             return NLB_ENOMEM;
         }
         if (hipMemset(h->rnn_winner, 0, bytes) != hipSuccess) return NLB_EDEVICE;
-        h->rnn_epoch = 0;
     }
     const size_t cbytes = (size_t)pair_rows * srb;
     if (cbytes > h->rnn_cand_bytes || pair_rows > h->rnn_cand_rows) {
@@ -1172,29 +1187,20 @@ int rnn_reserve(nlb_table *h, uint64_t pair_rows, uint32_t srb) {
     return NLB_OK;
 }
 
-// Working memory of one update: the winner word of every node, the winner
-// count and list, and the candidate rows.  Codes in `winner` carry the call
-// number in their high word (epoch_hi), so an array that is not cleared
-// between calls only needs codes of earlier calls to be smaller.
+// Working memory of one update: the winner word of every node (all zero
+// between calls), the winner count and list, and the candidate rows.
 struct RnnWork {
     unsigned long long *winner;
-    uint64_t epoch_hi;
     bool clear_winner;    // zero winner[0 .. N) first (memory shared with other calls)
     uint8_t *cand;
     uint32_t *list;       // word 0: winner count; from word 64: the winners, 4 words each
 };
 
 // Working memory of the table, grown on demand (nlb_rnn_update).
-int table_work(nlb_table *h, uint64_t pairs, uint32_t srb, hipStream_t stream, RnnWork *wk) {
-    int rc = rnn_reserve(h, pairs, srb);
+int table_work(nlb_table *h, uint64_t pairs, uint32_t srb, RnnWork *wk) {
+    const int rc = rnn_reserve(h, pairs, srb);
     if (rc != NLB_OK) return rc;
-    if (h->rnn_epoch == 0xFFFFFFFFu) {
-        hipLaunchKernelGGL(rnn_clear, dim3(4096), dim3(kRnnThreads), 0, stream, h->rnn_winner,
-                           (uint64_t)h->num_nodes);
-        h->rnn_epoch = 0;
-    }
-    h->rnn_epoch++;
-    *wk = {h->rnn_winner, (uint64_t)h->rnn_epoch << 32, false, h->rnn_cand, h->rnn_list};
+    *wk = {h->rnn_winner, false, h->rnn_cand, h->rnn_list};
     return NLB_OK;
 }
 
@@ -1242,8 +1248,7 @@ int scratch_work(nlb_table *h, uint64_t pairs, uint32_t srb, RnnWork *wk) {
     uint8_t *base = nullptr;
     const int rc = scratch_address(h->device, &base);
     if (rc != NLB_OK) return rc;
-    *wk = {(unsigned long long *)base, 1ull << 32, true, base + winner_bytes + list_bytes,
-           (uint32_t *)(base + winner_bytes)};
+    *wk = {(unsigned long long *)base, true, base + winner_bytes + list_bytes, (uint32_t *)(base + winner_bytes)};
     return NLB_OK;
 }
 
@@ -1279,6 +1284,7 @@ static int rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, cons
     p.n = n;
     p.num_nodes = h->num_nodes;
     p.first_eid = first_eid;
+    p.table_status = h->status;
     p.d = (uint32_t)wts->status_dim;
     p.d_time = h->d_time;
     p.tw = h->w;
@@ -1358,28 +1364,27 @@ static int rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, cons
 
     RnnWork wk;
     const int rc = use_scratch ? scratch_work(h, pairs, p.srb, &wk)
-                               : table_work(h, pairs, p.srb, (hipStream_t)stream, &wk);
+                               : table_work(h, pairs, p.srb, &wk);
     if (rc != NLB_OK) return rc;
     if (wk.clear_winner) {
         const uint64_t blocks = std::min<uint64_t>(4096, ((uint64_t)h->num_nodes + kRnnThreads - 1) / kRnnThreads);
         hipLaunchKernelGGL(rnn_clear, dim3((unsigned)blocks), dim3(kRnnThreads), 0, (hipStream_t)stream,
                            wk.winner, (uint64_t)h->num_nodes);
     }
-    const uint64_t epoch_hi = wk.epoch_hi;
     uint32_t *count = wk.list;
     u32x4 *list = (u32x4 *)(wk.list + 64);
     p.list = list;
     p.count = count;
     p.cand = wk.cand;
 
-    ResolveParams rp = {src, dst, n, h->num_nodes, wk.winner, epoch_hi, h->status, count};
+    ResolveParams rp = {src, dst, n, h->num_nodes, wk.winner, h->status, count};
     if (n >= kMergeMinBatch)
         hipLaunchKernelGGL(rnn_resolve_merged, dim3((n + kResolveLinks - 1) / kResolveLinks),
                            dim3(kMergeThreads), 0, (hipStream_t)stream, rp);
     else
         hipLaunchKernelGGL(rnn_resolve, dim3((n + kRnnThreads - 1) / kRnnThreads), dim3(kRnnThreads), 0,
                            (hipStream_t)stream, rp);
-    SelectParams sp = {src, dst, n, h->num_nodes, wk.winner, epoch_hi, list, count};
+    SelectParams sp = {src, dst, n, h->num_nodes, wk.winner, list, count};
     hipLaunchKernelGGL(rnn_select, dim3((unsigned)((pairs + kSelectRows - 1) / kSelectRows)),
                        dim3(kRnnThreads), 0, (hipStream_t)stream, sp);
     if (ws) {
@@ -1426,7 +1431,8 @@ static int rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, cons
     const uint64_t blocks = ((pairs + per - 1) / per * 64u + kRnnThreads - 1) / kRnnThreads;
     hipLaunchKernelGGL(rnn_scatter, dim3((unsigned)(blocks < 65536 ? blocks : 65536)),
                        dim3(kRnnThreads), 0, (hipStream_t)stream, (const uint8_t *)wk.cand,
-                       (const u32x4 *)list, (const uint32_t *)count, (uint8_t *)status, p.srb, w, upr, lg);
+                       (const u32x4 *)list, (const uint32_t *)count, (uint8_t *)status, p.srb, w, upr, lg,
+                       wk.winner);
     if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
     return NLB_OK;
 }

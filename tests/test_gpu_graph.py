@@ -1,12 +1,12 @@
-"""Retrieval and aggregation inside a HIP graph.
+"""Calls inside a HIP graph.
 
-nlb_sample and nlb_aggregate enqueue kernels only (no allocation, no
-memset, no synchronisation), so a caller whose queries land in the same
-device buffers every step can capture them once and replay the graph: the
-launch-bound small workloads then pay one graph launch per step.  Each
-replay here follows eager work on the same buffers and is checked against
-the eager call.  (nlb_insert_batch is not replayable: it assigns arrival
-indices on the host.)"""
+nlb_sample, nlb_aggregate and nlb_insert_batch enqueue kernels only (no
+allocation, no memset, no synchronisation), and the insert keeps the stream's
+link count on the device, as does nlb_rnn_update once its working memory is
+sized; so a caller whose batches land in the same device buffers every step
+can capture a whole step once and replay it: the launch-bound small
+workloads then pay one graph launch per step.  Replays are checked against
+eager calls and against the oracle."""
 import numpy as np
 import pytest
 
@@ -67,4 +67,77 @@ def test_sample_and_aggregate_replay_in_a_hip_graph():
         assert torch.equal(z, ref_z), f"replay {rep}: z"
     del graph
     assert g.status() == nlb.NLB_OK
+    g.close()
+
+
+@pytest.mark.parametrize("k", [1, 2])
+def test_whole_step_replays_against_the_oracle(k):
+    """One whole step -- nlb_sample of the batch's queries (Sec. 4.4), then
+    nlb_insert_batch of its links (Sec. 4.2), then the status update with
+    the arrival indices of the links just inserted (NLB_EID_LAST_BATCH) --
+    captured once and replayed for 40 consecutive batches, each copied into
+    the captured input buffers before its replay.  Every replay's retrieval
+    equals the oracle's at that point of the stream, the statuses its GRU
+    update (within 1e-4, from the GPU's statuses before the step), and the
+    tables and the device link count match at the end."""
+    import torch
+    import oracle
+    import paper_2402_01964_amd as nlb
+    from tests.gpu_helpers import compare_tables, host_np
+    base = synth.workload(k)
+    steps = 41
+    w = synth.scaled(base, steps * base.batch)
+    src, dst, t, neg = synth.host_links(w)
+    nodes, ts = synth.blocked(w, src, dst, t, neg)
+    ef = synth.host_features(w, "edge")
+    g = make_gpu_table(w, feat_to_dev(ef, w.edge_dtype), None)
+    o = make_oracle(w)
+    fw, fb = synth.time_params(w)
+    d, _ = synth.status_spec(w)                      # fp32 statuses (no node rows)
+    status = to_dev(np.random.default_rng(k).standard_normal((w.num_nodes, d)).astype(np.float32))
+    W = synth.gru_weights(w)
+    Wd = _agg_dev(W)
+    B, Q = w.batch, 3 * w.batch
+    q_s = torch.empty(Q, dtype=torch.int32, device="cuda")
+    tq_s = torch.empty(Q, dtype=torch.int32, device="cuda")
+    out = g.alloc_outputs(Q)
+
+    def run_step():
+        g.sample_into(q_s, tq_s, out)
+        g.insert(q_s[:B], q_s[B:2 * B], tq_s[:B])
+        g.rnn_update(q_s[:B], q_s[B:2 * B], tq_s[:B], nlb.EID_LAST_BATCH, Wd, status)
+
+    def check(b, pre):
+        lo, hi = w.batch_range(b)
+        compare_sample(out, o.sample(nodes[3 * lo:3 * hi], ts[3 * lo:3 * hi], fw, fb, ef, None),
+                       f"workload {k} step {b}")
+        o.insert(src[lo:hi], dst[lo:hi], t[lo:hi])
+        want = oracle.gru_update(pre.copy(), src[lo:hi], dst[lo:hi], t[lo:hi], lo, fw, fb, ef, W)
+        err = float(np.abs(host_np(status).astype(np.float64) - want.astype(np.float64)).max())
+        assert err <= 1e-4, (k, b, err)
+
+    def load(b):
+        lo, hi = w.batch_range(b)
+        q_s.copy_(to_dev(nodes[3 * lo:3 * hi]))
+        tq_s.copy_(to_dev(ts[3 * lo:3 * hi]))
+
+    load(0)                                          # eager step: sizes the update's memory
+    pre = host_np(status).copy()
+    run_step()
+    torch.cuda.synchronize()
+    check(0, pre)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run_step()
+    for b in range(1, steps):
+        load(b)
+        torch.cuda.synchronize()
+        pre = host_np(status).copy()
+        graph.replay()
+        torch.cuda.synchronize()
+        check(b, pre)
+    del graph
+    assert g.status() == nlb.NLB_OK
+    assert g.info()["interactions"] == w.links       # the device count, refreshed by nlb_status
+    compare_tables(g, o)
     g.close()
