@@ -67,3 +67,14 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU only" in r.stderr
+
+
+def test_binding_roofline_is_the_slower_peak():
+    # 86 us of bytes at 8 TB/s against 28 us of FLOPs at 2.5 PFLOP/s: HBM binds
+    r = bench.binding_roofline(7.0e10, 6.9e8, 3.9e-4)
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["other"]["bound"] == "mfma"
+    assert abs(r["frac"] - 6.9e8 / 3.9e-4 / 8e12) < 1e-12
+    # 8.7 us of FLOPs against 7.8 us of bytes: the matrix cores bind
+    r = bench.binding_roofline(2.17e10, 6.2e7, 4.8e-5)
+    assert r["bound"] == "mfma" and r["unit"] == "TFLOP/s"
+    assert abs(r["floor_seconds"] - 2.17e10 / 2.5e15) < 1e-15
