@@ -34,7 +34,7 @@ struct InsertParams {
     int64_t num_nodes;
     uint64_t seed;
     uint64_t thr;         // replace when coin < thr
-    uint64_t mod_m;       // nlb_div_magic(s), for nlb_mod
+    uint64_t mod_m;       // nlb_mod_magic(s)
     uint32_t q1r, q2r;    // q1 mod s, q2 mod s
     uint32_t key_mode;
     uint32_t *status;     // device status words (nlb_internal.h)
@@ -240,7 +240,7 @@ struct SampleParams {
     const uint32_t *tq;
     uint32_t nq;
     uint32_t tile_q;      // queries per tile; tile_q * s <= kTileSlots
-    uint64_t s_m;         // nlb_div_magic(s)
+    uint64_t s_m;         // nlb_div12_magic(s): slot rows of a tile (< 2^12) by s (<= 2^12)
     uint32_t d_time;
     const float *w;
     const float *b;
@@ -275,6 +275,25 @@ template <> struct VecOf<4> { typedef uint32_t T; };
 // link's row (kind 1) or the query node's row (kind 2).
 enum RowKind { kRowNeighbour = 0, kRowLink = 1, kRowSelf = 2 };
 
+// A thread's (row, column) in a tile's flattened range, advanced by
+// kTileThreads units per step without a division: with
+// kTileThreads = dq units + dr (dr < units), a step adds dq rows and dr
+// columns and carries at most one row.
+struct RowCursor {
+    uint32_t j, c;
+    __device__ __forceinline__ RowCursor(uint32_t f, uint32_t units, uint64_t m) {
+        j = nlb_div(f, m);
+        c = f - j * units;
+    }
+    __device__ __forceinline__ void step(uint32_t units, uint32_t dq, uint32_t dr) {
+        c += dr;
+        j += dq;
+        const bool carry = c >= units;
+        c = carry ? c - units : c;
+        j += carry ? 1u : 0u;
+    }
+};
+
 // Copy `rows` output rows of `row_bytes` each, laid out contiguously at
 // `out`, from their source rows; unit f of the flattened range is
 // (row f / units, column f % units).  R loads per thread are issued before
@@ -288,15 +307,17 @@ __device__ __forceinline__ void gather_tile(const uint8_t *__restrict__ src, uin
     typedef typename VecOf<W>::T V;
     constexpr int R = (W == 16) ? 4 : (W == 8 ? 6 : 8);
     const uint32_t total = rows * units;
+    const uint32_t dq = nlb_div(kTileThreads, m), dr = kTileThreads - dq * units;
+    RowCursor cur(tid, units, m);
     for (uint32_t base = 0; base < total; base += kTileThreads * R) {
         V val[R];
 #pragma unroll
         for (int r = 0; r < R; r++) {
             const uint32_t f = base + r * kTileThreads + tid;
+            const uint32_t j = cur.j, c = cur.c;
+            cur.step(units, dq, dr);
             val[r] = V(0);
             if (f < total) {
-                const uint32_t j = nlb_div(f, m);
-                const uint32_t c = f - j * units;
                 int64_t row;
                 if (KIND == kRowSelf) {
                     row = tile_nodes[j];
@@ -349,13 +370,21 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
     // the slot words (an out-of-range node or a row past the tile reads
     // slot 0 of node 0, which exists) -- before any is used.
     constexpr int P1 = kTileSlots / kTileThreads;
+    static_assert(kTileSlots <= 4096 && NLB_MAX_SLOTS <= 4096, "slot rows of a tile split by nlb_div12");
+    // Query and slot of each of the thread's rows (rows past the tile take
+    // the tile's last row).
+    uint32_t qlv[P1], av[P1];
+#pragma unroll
+    for (int r = 0; r < P1; r++) {
+        const uint32_t j = min(tid + r * kTileThreads, ns - 1u);
+        qlv[r] = nlb_div12(j, p.s_m);
+        av[r] = j - qlv[r] * s;
+    }
     int32_t nd[P1];
     uint32_t tqv[P1];
 #pragma unroll
     for (int r = 0; r < P1; r++) {
-        const uint32_t j = min(tid + r * kTileThreads, ns - 1u);
-        const uint32_t ql = nlb_div(j, p.s_m);
-        const uint64_t qg = q0 + ql;
+        const uint64_t qg = q0 + qlv[r];
         nd[r] = p.node[qg];
         tqv[r] = p.tq[HOP2 ? (uint32_t)qg / s : qg];
     }
@@ -363,9 +392,7 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
     int32_t xv[P1];
 #pragma unroll
     for (int r = 0; r < P1; r++) {
-        const uint32_t j = min(tid + r * kTileThreads, ns - 1u);
-        const uint32_t ql = nlb_div(j, p.s_m);
-        const uint32_t a = j - ql * s;
+        const uint32_t a = av[r];
         const bool in_range = nd[r] >= 0 && (int64_t)nd[r] < p.num_nodes;
         const uint8_t *bp = p.blocks + (size_t)(in_range ? nd[r] : 0) * p.block_bytes;
         const uint32_t aa = in_range ? a : 0u;
@@ -376,8 +403,7 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
     for (int r = 0; r < P1; r++) {
         const uint32_t j = tid + r * kTileThreads;
         if (j >= ns) break;
-        const uint32_t ql = nlb_div(j, p.s_m);
-        const uint32_t a = j - ql * s;
+        const uint32_t ql = qlv[r], a = av[r];
         const int32_t node = nd[r];
         const bool in_range = node >= 0 && (int64_t)node < p.num_nodes;
         const bool quiet = HOP2 && node < 0;   // empty first-hop slot
@@ -397,9 +423,11 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
         const uint32_t units = p.tenc_units;
         const uint32_t total = ns * units;
         float *out = p.o_tenc + row0 * p.d_time;
+        const uint32_t dq = nlb_div(kTileThreads, p.tenc_m), dr = kTileThreads - dq * units;
+        RowCursor cur(tid, units, p.tenc_m);
         for (uint32_t f = tid; f < total; f += kTileThreads) {
-            const uint32_t j = nlb_div(f, p.tenc_m);
-            const uint32_t c = f - j * units;
+            const uint32_t j = cur.j, c = cur.c;
+            cur.step(units, dq, dr);
             const SlotLds sl = slots[j];
             if (p.tenc_vec == 4) {
                 f32x4 r = f32x4(0.0f);
@@ -660,7 +688,7 @@ int nlb_insert_batch(nlb_table *h, const int32_t *src, const int32_t *dst, const
     p.num_nodes = h->num_nodes;
     p.seed = h->seed;
     p.thr = h->thr;
-    p.mod_m = nlb_div_magic(h->s);
+    p.mod_m = nlb_mod_magic(h->s);
     p.q1r = (uint32_t)(h->q1 % h->s);
     p.q2r = (uint32_t)(h->q2 % h->s);
     p.key_mode = (uint32_t)h->key_mode;
@@ -728,7 +756,7 @@ static int launch_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, 
     p.n_units = h->nrb ? h->nrb / p.n_width : 1;
     p.n_m = nlb_div_magic(p.n_units);
     p.tile_q = tile_queries(h->s, nq);
-    p.s_m = nlb_div_magic(h->s);
+    p.s_m = nlb_div12_magic(h->s);
     const hipStream_t st = (hipStream_t)stream;
     const dim3 grid((unsigned)(((uint64_t)nq + p.tile_q - 1) / p.tile_q));
     // Large first-hop launches that also write timestamps take the time

@@ -6,7 +6,7 @@ kernels split flat output indices into (row, column) and slot rows into
 tests/divide_check.cpp: every row boundary for every divisor up to 65536
 and tiles of up to 1024 rows, every numerator below 2^26 for a set of
 divisors, quotient boundaries over the whole 32-bit range (divisor 1
-included), and random pairs.
+included), every pair of the 12-bit slot-row form, and random pairs.
 """
 import os
 import subprocess
