@@ -557,6 +557,54 @@ __device__ __forceinline__ void piece_operand(const Piece8<KIND> &r, uint32_t di
     }
 }
 
+// MLP_out for a group of up to 16 queries: row r16 = query qb + r16, input
+// [r_u | aggregate], the aggregate w2 aggd + b2 (zero for a query without
+// valid rows, ne = 0); aggd holds the group's finished aggregates
+// sum_s alpha_s a1_s in the D layout (query r16's units 16 ub + 4 g + i in
+// the lanes with that r16).  Writes z for the lanes with vq.
+template <int NKS, int NK, uint32_t LS3>
+__device__ __forceinline__ void mlp_out_group(const RowParams &p, const Piece8<NK> (&ru)[NKS > 0 ? NKS : 1],
+                                              int32_t nr, bool vq, const f32x4 (&aggd)[4], float ne,
+                                              const __bf16 *W2, const __bf16 *W3, const __bf16 *W4,
+                                              const float *b2, const float *b3, const float *b4, uint32_t r16,
+                                              uint32_t g, uint64_t qb) {
+    if (vq && g == 0 && nr < 0) atomicOr(p.status, kStatusRange);   // an out-of-range query
+    f32x4 acc3[4];
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++) acc3[ub] = f32x4(0.0f);
+#pragma unroll
+    for (int ks = 0; ks < NKS; ks++) {
+        bf16x8 hi, lo;
+        piece_operand<NK>(ru[ks], p.n_dim, 32u * ks + 8u * g, nr >= 0, hi, lo);
+        mfma4(acc3, W3, LS3, 32u * ks, r16, g, hi, lo, NK == kF32Vec);
+    }
+    f32x4 hq[4];
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++) hq[ub] = f32x4(0.0f);
+    chain64(hq, aggd, W2, kPs, 0, r16, g);
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+        for (int i = 0; i < 4; i++) hq[ub][i] = ne * (hq[ub][i] + b2[16 * ub + 4 * g + i]);
+    chain64(acc3, hq, W3, LS3, 32u * NKS, r16, g);
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+        for (int i = 0; i < 4; i++) acc3[ub][i] = fmaxf(acc3[ub][i] + b3[16 * ub + 4 * g + i], 0.0f);
+    f32x4 zo[4];
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++) zo[ub] = f32x4(0.0f);
+    chain64(zo, acc3, W4, kPs, 0, r16, g);
+    if (vq) {
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) {
+#pragma unroll
+            for (int i = 0; i < 4; i++) zo[ub][i] += b4[16 * ub + 4 * g + i];
+            *(f32x4 *)(p.z + (qb + r16) * kH + 16 * ub + 4 * g) = zo[ub];
+        }
+    }
+}
+
 // Specialised per input shape: NKS, EKS and TKS k-steps of layer 1 hold r_v,
 // e and the time encoding, NK / EK are the piece forms of the node / link
 // rows; layer 3 has NKS + 2 k-steps (r_u, then the aggregate).  With the
@@ -957,45 +1005,7 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
             for (int ub = 0; ub < 4; ub++) agg[ub] = 0.0f;
         }
         if (group_end) {
-            // MLP_out for the group: row r16 = query qb + r16, input
-            // [r_u | aggregate], the aggregate w2 aggd + b2 (zero for a query
-            // without valid rows).
-            const uint64_t qb = cg * gq;
-            if (vq && g == 0 && nr < 0) atomicOr(p.status, kStatusRange);   // an out-of-range query
-            f32x4 acc3[4];
-#pragma unroll
-            for (int ub = 0; ub < 4; ub++) acc3[ub] = f32x4(0.0f);
-#pragma unroll
-            for (int ks = 0; ks < NKS; ks++) {
-                bf16x8 hi, lo;
-                piece_operand<NK>(ru[ks], p.n_dim, 32u * ks + 8u * g, nr >= 0, hi, lo);
-                mfma4(acc3, W3, L::ls3, 32u * ks, r16, g, hi, lo, NK == kF32Vec);
-            }
-            f32x4 hq[4];
-#pragma unroll
-            for (int ub = 0; ub < 4; ub++) hq[ub] = f32x4(0.0f);
-            chain64(hq, aggd, W2, kPs, 0, r16, g);
-#pragma unroll
-            for (int ub = 0; ub < 4; ub++)
-#pragma unroll
-                for (int i = 0; i < 4; i++) hq[ub][i] = ne * (hq[ub][i] + b2[16 * ub + 4 * g + i]);
-            chain64(acc3, hq, W3, L::ls3, 32u * NKS, r16, g);
-#pragma unroll
-            for (int ub = 0; ub < 4; ub++)
-#pragma unroll
-                for (int i = 0; i < 4; i++) acc3[ub][i] = fmaxf(acc3[ub][i] + b3[16 * ub + 4 * g + i], 0.0f);
-            f32x4 zo[4];
-#pragma unroll
-            for (int ub = 0; ub < 4; ub++) zo[ub] = f32x4(0.0f);
-            chain64(zo, acc3, W4, kPs, 0, r16, g);
-            if (vq) {
-#pragma unroll
-                for (int ub = 0; ub < 4; ub++) {
-#pragma unroll
-                    for (int i = 0; i < 4; i++) zo[ub][i] += b4[16 * ub + 4 * g + i];
-                    *(f32x4 *)(p.z + (qb + r16) * kH + 16 * ub + 4 * g) = zo[ub];
-                }
-            }
+            mlp_out_group<NKS, NK, L::ls3>(p, ru, nr, vq, aggd, ne, W2, W3, W4, b2, b3, b4, r16, g, cg * gq);
 #pragma unroll
             for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
             ne = 0.0f;
@@ -1014,6 +1024,467 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         }
         sl_c = sl_n;
         rows_c = rows_n;
+    }
+}
+
+// ---------------------------------------------------------------- packed rows
+// aggregate_packed: the computation of aggregate_rows with the valid rows of
+// a query group packed into full 16-row blocks, for tables of at most 16
+// slots.  In aggregate_rows every query takes a whole 16-row block, so with
+// s = 10 and two thirds of the slots valid, three fifths of the rows that
+// the matrix cores and the softmax process are empty.
+//
+// Per group of up to 16 queries a wavefront first reads all of the group's
+// slot words (lane (q = l % 16, g = l / 16) slots g, g + 4, g + 8, g + 12 of
+// query q, issued one group ahead), applies eq. (1) and writes the valid
+// slots to a list in LDS, query by query, each query's run padded to a
+// multiple of four rows with empty entries.  The list is then processed in
+// 16-row blocks.  Because runs are padded to four rows, the four rows
+// 4 g .. 4 g + 3 that lane group g holds after the transposed layer 1 belong
+// to one query; the lane group forms its rows' softmax partial (maximum,
+// sum of exponentials, exponential-weighted sum of layer-1 outputs), and one
+// fp32 matrix product per unit block adds the four partials into their
+// queries' columns of the group's running aggregates (the product's B
+// operand holds each partial's weight exp(m_g - M_q) in its query's column;
+// the columns are rescaled first when M_q, the running maximum of query q,
+// grows).  At the group's end every column is divided by its sum of
+// exponentials and MLP_out runs as in aggregate_rows.  Results differ from
+// aggregate_rows by summation order only.
+constexpr uint32_t kPackMaxS = 16;                    // slots per node at most
+constexpr uint32_t kPackMinGroup = 8;                 // queries per group at least
+constexpr uint32_t kScanJ = kPackMaxS / 4;           // slots per lane in the group scan
+constexpr uint32_t kPackList = kMaxGroupQ * kPackMaxS;   // list entries per group at most
+
+// One list entry: a valid slot of query q of the group (x < 0: padding).
+struct PackEntry {
+    int32_t x;
+    uint32_t e;
+    uint32_t q;
+    float dt;
+};
+
+// LDS layout: weights and time-encoding vectors as RowsLayout, then each
+// wavefront's list.
+template <int K1S, int K3S, int TKS>
+struct PackedLayout {
+    static constexpr uint32_t ls1 = 32u * K1S + 8u, ls3 = 32u * K3S + 8u;
+    static constexpr uint32_t o_w1 = 0;
+    static constexpr uint32_t o_w2 = o_w1 + kH * ls1 * 2u;
+    static constexpr uint32_t o_w3 = o_w2 + kH * kPs * 2u;
+    static constexpr uint32_t o_w4 = o_w3 + kH * ls3 * 2u;
+    static constexpr uint32_t o_vec = o_w4 + kH * kPs * 2u;
+    static constexpr uint32_t o_tenc = o_vec + 5u * kH * 4u;
+    static constexpr uint32_t o_list = o_tenc + 2u * 32u * TKS * 4u;
+    static constexpr uint32_t bytes = o_list + (kRowThreads / 64) * kPackList * (uint32_t)sizeof(PackEntry);
+};
+
+// Time-encoding columns in lane-group order: k-step ks, lane group g and
+// element i of a lane's 8-element operand piece hold column 4 (8 ks + i) + g,
+// so with d_time columns every lane group needs elements j = 8 ks + i <
+// ceil(d_time / 4) only -- a bound common to all lanes.
+__device__ __forceinline__ uint32_t tenc_column(uint32_t kk) {
+    const uint32_t ks = kk >> 5, g = (kk >> 3) & 3u, i = kk & 7u;
+    return 4u * (8u * ks + i) + g;
+}
+
+template <int NKS, int EKS, int TKS, int NK, int EK>
+__global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void aggregate_packed(RowParams p) {
+    constexpr int GS = NKS + EKS, K1S = GS + TKS, K3S = NKS + 2;
+    using L = PackedLayout<K1S, K3S, TKS>;
+    static_assert(NKS <= kRuSteps, "shape");
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    __bf16 *W1 = (__bf16 *)(smem + L::o_w1);
+    __bf16 *W2 = (__bf16 *)(smem + L::o_w2);
+    __bf16 *W3 = (__bf16 *)(smem + L::o_w3);
+    __bf16 *W4 = (__bf16 *)(smem + L::o_w4);
+    float *vec = (float *)(smem + L::o_vec);   // b1 | b2 | b3 | b4 | v, 64 each
+
+    // Stage the weights as aggregate_rows does, except that the time-encoding
+    // columns of w1 (and w, b) go in lane-group order (tenc_column).
+    const uint32_t tid = threadIdx.x;
+    for (uint32_t u = tid; u < kH * (GS * 4u); u += kRowThreads) {
+        const uint32_t r = u / (GS * 4u), c = (u % (GS * 4u)) * 8;
+        *(bf16x8 *)(W1 + r * L::ls1 + c) = *(const bf16x8 *)(p.w1 + (size_t)r * (32u * K1S) + c);
+    }
+    for (uint32_t u = tid; u < kH * (32u * TKS); u += kRowThreads) {
+        const uint32_t r = u / (32u * TKS), kk = u % (32u * TKS), c = tenc_column(kk);
+        W1[r * L::ls1 + 32u * GS + kk] =
+            c < p.d_time ? p.w1[(size_t)r * (32u * K1S) + 32u * GS + c] : (__bf16)0.0f;
+    }
+    if constexpr (NKS > 0) {
+        for (uint32_t u = tid; u < kH * (NKS * 4u); u += kRowThreads) {
+            const uint32_t r = u / (NKS * 4u), c = (u % (NKS * 4u)) * 8;
+            *(bf16x8 *)(W3 + r * L::ls3 + c) = *(const bf16x8 *)(p.w3 + (size_t)r * (32u * K3S) + c);
+        }
+    }
+    for (uint32_t u = tid; u < kH * kH; u += kRowThreads) {
+        const uint32_t r = u / kH, c = u % kH;
+        W2[r * kPs + c] = p.w2[r * kH + chain_unit(c)];
+        W4[r * kPs + c] = p.w4[r * kH + chain_unit(c)];
+        W3[r * L::ls3 + 32u * NKS + c] = p.w3[(size_t)r * (32u * K3S) + 32u * NKS + chain_unit(c)];
+    }
+    for (uint32_t u = tid; u < 5u * kH; u += kRowThreads) {
+        const uint32_t k = u / kH, c = u % kH;
+        float val;
+        if (k < 4) {
+            val = (k == 0 ? p.b1 : k == 1 ? p.b2 : k == 2 ? p.b3 : p.b4)[c];
+        } else {
+            val = 0.0f;
+            for (uint32_t r = 0; r < kH; r++) val = __builtin_fmaf(p.att[r], (float)p.w2[r * kH + c], val);
+        }
+        vec[u] = val;
+    }
+    float *tw = (float *)(smem + L::o_tenc), *tb = tw + 32 * TKS;
+    for (uint32_t kk = tid; kk < 32u * TKS; kk += kRowThreads) {
+        const uint32_t c = tenc_column(kk);
+        tw[kk] = c < p.d_time ? p.w[c] : 0.0f;
+        tb[kk] = c < p.d_time ? p.b[c] : 0.0f;
+    }
+    __syncthreads();
+    float wmax = 0.0f, bmax = 0.0f;
+    for (uint32_t u = tid & 63; u < 32u * TKS; u += 64) {
+        wmax = fmaxf(wmax, fabsf(tw[u]));
+        bmax = fmaxf(bmax, fabsf(tb[u]));
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        wmax = fmaxf(wmax, __shfl_xor(wmax, o));
+        bmax = fmaxf(bmax, __shfl_xor(bmax, o));
+    }
+    wmax = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(wmax)));
+    bmax = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(bmax)));
+    // Elements of the last time-encoding k-step that a lane group computes.
+    const uint32_t t_last = TKS > 0 ? (p.d_time + 3u) / 4u - 8u * (uint32_t)(TKS - 1) : 0u;
+
+    const uint32_t lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t r16 = lane & 15, g = lane >> 4;
+    PackEntry *lst = (PackEntry *)(smem + L::o_list) + (size_t)wave * kPackList;
+    const float *b1 = vec, *b2 = vec + kH, *b3 = vec + 2 * kH, *b4 = vec + 3 * kH, *va = vec + 4 * kH;
+    float b1v[4], vav[4];
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++) {
+        b1v[ub] = b1[16 * ub + r16];
+        vav[ub] = va[16 * ub + r16];
+    }
+    const uint32_t gq = p.gq;
+    const uint64_t groups = ((uint64_t)p.nq + gq - 1) / gq;
+    const uint64_t gstep = (uint64_t)gridDim.x * (kRowThreads / 64);
+    const uint64_t g0 = (uint64_t)wave * gridDim.x + blockIdx.x;
+    if (g0 >= groups) return;   // no workgroup barrier follows
+
+    auto group_size = [&](uint64_t grp) -> uint32_t {
+        return grp < groups ? (uint32_t)min((uint64_t)gq, (uint64_t)p.nq - grp * gq) : 0u;
+    };
+    // Query ids of a group: query r16 of it in the lanes with that r16 (lanes
+    // past the group's last query read the launch's last query, unused).
+    auto load_ids = [&](uint64_t grp, int32_t &nd, uint32_t &t) {
+        const uint64_t q = min(grp * gq + r16, (uint64_t)p.nq - 1);
+        nd = p.node[q];
+        t = p.tq[q];
+    };
+    // The group scan's slot words, read unconditionally (a slot past s, a
+    // query past the group or an out-of-range node reads slot 0 of node 0
+    // and is marked not ok).
+    struct ScanRaw {
+        uint64_t key[kScanJ];
+        int32_t x[kScanJ];
+        uint32_t tq, okm;
+    };
+    auto issue_scan = [&](uint64_t grp, int32_t nd, uint32_t t, ScanRaw &sr) {
+        const bool in = r16 < group_size(grp) && nd >= 0 && (int64_t)nd < p.num_nodes;
+        const uint8_t *bp = p.blocks + (size_t)(in ? nd : 0) * p.block_bytes;
+        sr.tq = t;
+        sr.okm = 0;
+#pragma unroll
+        for (uint32_t j = 0; j < kScanJ; j++) {
+            const uint32_t a = g + 4u * j;
+            const bool ok = in && a < p.s;
+            const uint32_t aa = ok ? a : 0u;
+            sr.key[j] = ((const uint64_t *)bp)[aa];
+            sr.x[j] = ((const int32_t *)(bp + 8u * p.s))[aa];
+            sr.okm |= (ok ? 1u : 0u) << j;
+        }
+    };
+    // eq. (1) on the scanned words, then the list: query q's valid slots at
+    // base_q .. base_q + v_q - 1 (lane groups in order), padding up to
+    // base_q + pad4(v_q).  Returns the list length (a multiple of 4).
+    auto build_list = [&](const ScanRaw &sr) -> uint32_t {
+        SlotLds sl[kScanJ];
+        uint32_t c = 0;
+#pragma unroll
+        for (uint32_t j = 0; j < kScanJ; j++) {
+            sl[j] = decode_slot(((sr.okm >> j) & 1u) ? sr.key[j] : 0ull, sr.x[j], sr.tq);
+            c += sl[j].x >= 0 ? 1u : 0u;
+        }
+        // Inclusive prefix over the query's four lane groups, and its total.
+        uint32_t inc = c;
+        const uint32_t u16 = (uint32_t)__shfl_up((int)inc, 16);
+        if (g >= 1) inc += u16;
+        const uint32_t u32 = (uint32_t)__shfl_up((int)inc, 32);
+        if (g >= 2) inc += u32;
+        const uint32_t vq = (uint32_t)__shfl((int)inc, (int)(48u + r16));
+        const uint32_t pq = (vq + 3u) & ~3u;
+        // Exclusive prefix of the padded runs over the 16 queries.
+        uint32_t run = pq;
+#pragma unroll
+        for (uint32_t d = 1; d < 16; d <<= 1) {
+            const uint32_t t = (uint32_t)__shfl_up((int)run, d, 16);
+            if (r16 >= d) run += t;
+        }
+        const uint32_t base = run - pq;
+        const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)run, 15);
+        uint32_t pos = base + (inc - c);
+#pragma unroll
+        for (uint32_t j = 0; j < kScanJ; j++) {
+            if (sl[j].x >= 0) {
+                lst[pos] = PackEntry{sl[j].x, sl[j].e, r16, sl[j].dt};
+                pos++;
+            }
+        }
+        if (g < pq - vq) lst[base + vq + g] = PackEntry{-1, 0u, r16, 0.0f};
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        return total;
+    };
+    // Row r16 of block b of a list of n entries (past the end: empty).
+    auto read_entry = [&](uint32_t n, uint32_t b) -> PackEntry {
+        const uint32_t idx = 16u * b + r16;
+        PackEntry en = lst[min(idx, n - 1u)];
+        if (idx >= n) {
+            en.x = -1;
+            en.dt = 0.0f;
+        }
+        return en;
+    };
+    struct Rows {
+        Piece8<NK> n[NKS > 0 ? NKS : 1];
+        Piece8<EK> e[EKS > 0 ? EKS : 1];
+    };
+    auto issue_rows = [&](const PackEntry &en, Rows &r) {
+        const bool valid = en.x >= 0;
+        if constexpr (NKS > 0) {
+            const uint8_t *nrow = p.nfeat + (size_t)(valid ? en.x : 0) * p.nrb;
+#pragma unroll
+            for (int ks = 0; ks < NKS; ks++) load_piece<NK>(nrow, p.n_dim, 32u * ks + 8u * g, r.n[ks]);
+        }
+        if constexpr (EKS > 0) {
+            const bool ev = valid && (int64_t)en.e < p.edge_rows;
+            const uint8_t *erow = p.efeat + (size_t)(ev ? en.e : 0u) * p.erb;
+#pragma unroll
+            for (int ks = 0; ks < EKS; ks++) load_piece<EK>(erow, p.e_dim, 32u * ks + 8u * g, r.e[ks]);
+        }
+    };
+
+    // Running state of the group: aggd holds, in the D layout, each query's
+    // sum over its merged partials of exp(m - M) times the partial's
+    // exponential-weighted sums, and the lanes with r16 == q hold M_q (mrun)
+    // and the matching sum of exponentials (drun).
+    f32x4 aggd[4];
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
+    float mrun = -INFINITY, drun = 0.0f;
+
+    auto compute_block = [&](const PackEntry &en, const Rows &rc) {
+        const bool valid = en.x >= 0;
+        const bool ev = valid && (int64_t)en.e < p.edge_rows;
+        f32x4 acc[4];
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) acc[ub] = f32x4(b1v[ub]);   // + b1
+#pragma unroll
+        for (int ks = 0; ks < NKS; ks++) {
+            bf16x8 hi, lo;
+            piece_operand<NK>(rc.n[ks], p.n_dim, 32u * ks + 8u * g, valid, hi, lo);
+            mfma4t(acc, W1, L::ls1, 32u * ks, r16, g, hi, lo, NK == kF32Vec);
+        }
+#pragma unroll
+        for (int ks = 0; ks < EKS; ks++) {
+            bf16x8 hi, lo;
+            piece_operand<EK>(rc.e[ks], p.e_dim, 32u * ks + 8u * g, ev, hi, lo);
+            mfma4t(acc, W1, L::ls1, 32u * (NKS + ks), r16, g, hi, lo, EK == kF32Vec);
+        }
+        // Time encodings of the block's rows (an empty row has dt = 0; its
+        // finite values get zero weight in the softmax).
+        const float dtmax =
+            __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(xor16_max(en.dt))));
+        if (wmax * dtmax + bmax < 0.5f * kCosFastLimit) {
+            // Every k-step but the last computes all of its elements; the
+            // last computes the first t_last (the others have zero weight).
+#pragma unroll 1
+            for (int ks = 0; ks < TKS - 1; ks++) {
+                const uint32_t k = 32u * ks + 8u * g;
+                const f32x4 w0 = *(const f32x4 *)(tw + k), w1 = *(const f32x4 *)(tw + k + 4);
+                const f32x4 c0 = *(const f32x4 *)(tb + k), c1 = *(const f32x4 *)(tb + k + 4);
+                float t[8];
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    t[i] = cos_fast(__builtin_fmaf(w0[i], en.dt, c0[i]));
+                    t[4 + i] = cos_fast(__builtin_fmaf(w1[i], en.dt, c1[i]));
+                }
+                bf16x8 hi, lo;
+                split8(t, hi, lo);
+                mfma4t(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
+            }
+            if constexpr (TKS > 0) {
+                const uint32_t k = 32u * (TKS - 1) + 8u * g;
+                float t[8];
+#pragma unroll
+                for (int i = 0; i < 8; i++) {
+                    t[i] = 0.0f;
+                    if ((uint32_t)i < t_last) t[i] = cos_fast(__builtin_fmaf(tw[k + i], en.dt, tb[k + i]));
+                }
+                bf16x8 hi, lo;
+                split8(t, hi, lo);
+                mfma4t(acc, W1, L::ls1, 32u * (GS + TKS - 1), r16, g, hi, lo, true);
+            }
+        } else {
+#pragma unroll 1
+            for (int ks = 0; ks < TKS; ks++) {
+                const uint32_t k = 32u * ks + 8u * g;
+                float t[8];
+#pragma unroll
+                for (int i = 0; i < 8; i++) t[i] = cos_fp32(__builtin_fmaf(tw[k + i], en.dt, tb[k + i]));
+                bf16x8 hi, lo;
+                split8(t, hi, lo);
+                mfma4t(acc, W1, L::ls1, 32u * (GS + ks), r16, g, hi, lo, true);
+            }
+        }
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+            for (int i = 0; i < 4; i++) acc[ub][i] = relu(acc[ub][i]);
+        // Logits of rows 4 g + i, then the lane group's softmax partial.
+        float lg[4];
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            float t = vav[0] * acc[0][i];
+#pragma unroll
+            for (int ub = 1; ub < 4; ub++) t = __builtin_fmaf(vav[ub], acc[ub][i], t);
+            lg[i] = xor16_sum(t);
+        }
+        const uint32_t nib = ((uint32_t)__builtin_amdgcn_ballot_w64(valid) >> (4u * g)) & 0xFu;
+#pragma unroll
+        for (int i = 0; i < 4; i++) lg[i] = ((nib >> i) & 1u) ? lg[i] : -INFINITY;
+        const float mg = max2(max2(lg[0], lg[1]), max2(lg[2], lg[3]));
+        const float sh = (mg == -INFINITY) ? 0.0f : mg * kLog2eAgg;
+        float e[4];
+#pragma unroll
+        for (int i = 0; i < 4; i++) e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(lg[i], kLog2eAgg, -sh));
+        const float dg = (e[0] + e[1]) + (e[2] + e[3]);
+        float agg[4];
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) {
+            float t = e[0] * acc[ub][0];
+#pragma unroll
+            for (int i = 1; i < 4; i++) t = __builtin_fmaf(e[i], acc[ub][i], t);
+            agg[ub] = t;
+        }
+        // Merge the four partials into their queries' columns.  The quad's
+        // query is that of its first row (rows 4 g .. 4 g + 3 hold one query's
+        // run or lie past the list).
+        const uint32_t qg = (uint32_t)__shfl((int)en.q, (int)(4u * g));
+        const bool mine = qg == r16 && mg != -INFINITY;
+        float bm = mine ? mg : -INFINITY;
+        bm = max2(bm, __shfl_xor(bm, 16));
+        bm = max2(bm, __shfl_xor(bm, 32));
+        const float mnew = max2(mrun, bm);
+        const float scl = (mrun == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f((mrun - mnew) * kLog2eAgg);
+        const float r = mine ? __builtin_amdgcn_exp2f((mg - mnew) * kLog2eAgg) : 0.0f;
+        float dc = dg * r;
+        dc += __shfl_xor(dc, 16);
+        dc += __shfl_xor(dc, 32);
+        drun = __builtin_fmaf(drun, scl, dc);
+        mrun = mnew;
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) {
+#pragma unroll
+            for (int i = 0; i < 4; i++) aggd[ub][i] *= scl;
+            aggd[ub] = __builtin_amdgcn_mfma_f32_16x16x4f32(agg[ub], r, aggd[ub], 0, 0, 0);
+        }
+    };
+
+    // Prologue: the first group's list and the next group's scan in flight.
+    // This lane's query node of the current group (mo_nd, for MLP_out) and
+    // of the next (nx_nd); id_nd / id_t: the ids of the group whose scan is
+    // issued next.
+    int32_t mo_nd, nx_nd, id_nd;
+    uint32_t id_t;
+    load_ids(g0, mo_nd, id_t);
+    ScanRaw sr;
+    issue_scan(g0, mo_nd, id_t, sr);
+    load_ids(g0 + gstep, nx_nd, id_t);
+    uint32_t n_cur = build_list(sr);
+    issue_scan(g0 + gstep, nx_nd, id_t, sr);
+    load_ids(g0 + 2 * gstep, id_nd, id_t);
+    PackEntry en_c = n_cur ? read_entry(n_cur, 0) : PackEntry{-1, 0u, 0u, 0.0f};
+    Rows rows_c;
+    issue_rows(en_c, rows_c);
+
+    for (uint64_t cg = g0; cg < groups; cg += gstep) {
+        asm volatile("" ::: "memory");
+        const uint32_t cnq = group_size(cg);
+        const bool vq = r16 < cnq;
+        const int32_t nr = (vq && mo_nd >= 0 && (int64_t)mo_nd < p.num_nodes) ? mo_nd : -1;
+        const uint32_t nb = (n_cur + 15u) / 16u;
+        Piece8<NK> ru[NKS > 0 ? NKS : 1];
+        uint32_t n_next = 0;
+        // The step to the next group, taken at the current group's last block
+        // (or at once for a group without blocks): this group's MLP_out rows
+        // r_u, the next group's list (its scan was issued a group ago) and
+        // the next group's first block of rows.  The scan of the group after
+        // is issued once the blocks are done.
+        auto advance = [&](PackEntry &en_n, Rows &rows_n) {
+            if constexpr (NKS > 0) {
+                const uint8_t *urow = p.nfeat + (size_t)(nr >= 0 ? nr : 0) * p.nrb;
+#pragma unroll
+                for (int ks = 0; ks < NKS; ks++) load_piece<NK>(urow, p.n_dim, 32u * ks + 8u * g, ru[ks]);
+            }
+            n_next = build_list(sr);
+            en_n = n_next ? read_entry(n_next, 0) : PackEntry{-1, 0u, 0u, 0.0f};
+            issue_rows(en_n, rows_n);
+        };
+        if (nb == 0) {
+            PackEntry en_n;
+            Rows rows_n;
+            advance(en_n, rows_n);
+            en_c = en_n;
+            rows_c = rows_n;
+        }
+        for (uint32_t b = 0; b < nb; b++) {
+            // Keeps the LDS-resident weights from being hoisted out of the
+            // loop into long-lived registers.
+            asm volatile("" ::: "memory");
+            PackEntry en_n;
+            Rows rows_n;
+            if (b + 1 < nb) {
+                en_n = read_entry(n_cur, b + 1);
+                issue_rows(en_n, rows_n);
+            } else {
+                advance(en_n, rows_n);
+            }
+            // Keep the scheduler from sinking the loads to their uses.
+            __builtin_amdgcn_sched_barrier(0);
+            compute_block(en_c, rows_c);
+            en_c = en_n;
+            rows_c = rows_n;
+        }
+        issue_scan(cg + 2 * gstep, id_nd, id_t, sr);
+        mo_nd = nx_nd;
+        nx_nd = id_nd;
+        load_ids(cg + 3 * gstep, id_nd, id_t);
+        // The group's aggregates, normalised, then MLP_out.
+        const float ne = drun > 0.0f ? 1.0f : 0.0f;
+        const float inv = drun > 0.0f ? __builtin_amdgcn_rcpf(drun) : 0.0f;
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++)
+#pragma unroll
+            for (int i = 0; i < 4; i++) aggd[ub][i] *= inv;
+        mlp_out_group<NKS, NK, L::ls3>(p, ru, nr, vq, aggd, ne, W2, W3, W4, b2, b3, b4, r16, g, cg * gq);
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
+        mrun = -INFINITY;
+        drun = 0.0f;
+        n_cur = n_next;
     }
 }
 
@@ -1140,13 +1611,32 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
         const void *kern = nullptr;
         uint32_t bytes = 0;
         void (*launch)(dim3, uint32_t, hipStream_t, const RowParams &) = nullptr;
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess || cus < 1)
+            return NLB_EDEVICE;
+        // One persistent workgroup per CU; groups of up to 16 queries, fewer
+        // when that leaves wavefronts without one.
+        const uint64_t waves = (uint64_t)cus * (kRowThreads / 64);
+        r.gq = (uint32_t)std::min<uint64_t>(kMaxGroupQ, std::max<uint64_t>(1, (nq + waves - 1) / waves));
+        // Tables of at most 16 slots take the packed form when the groups
+        // are large enough for packing to fill blocks (small launches are
+        // bound by their per-group steps).
+        const bool packed = h->s <= kPackMaxS && r.gq >= kPackMinGroup;
 #define NLB_ROWS_SHAPE(A, B, C, NK, EK)                                                              \
     if (!kern && nks == A && eks == B && tks == C && (A == 0 || nkind == NK) && (B == 0 || ekind == EK)) { \
-        kern = (const void *)aggregate_rows<A, B, C, NK, EK>;                                         \
-        bytes = RowsLayout<A + B + C, A + 2, C>::bytes;                                               \
-        launch = [](dim3 gr, uint32_t l, hipStream_t st, const RowParams &rp) {                       \
-            hipLaunchKernelGGL((aggregate_rows<A, B, C, NK, EK>), gr, dim3(kRowThreads), l, st, rp);  \
-        };                                                                                            \
+        if (packed) {                                                                                 \
+            kern = (const void *)aggregate_packed<A, B, C, NK, EK>;                                   \
+            bytes = PackedLayout<A + B + C, A + 2, C>::bytes;                                         \
+            launch = [](dim3 gr, uint32_t l, hipStream_t st, const RowParams &rp) {                   \
+                hipLaunchKernelGGL((aggregate_packed<A, B, C, NK, EK>), gr, dim3(kRowThreads), l, st, rp); \
+            };                                                                                        \
+        } else {                                                                                      \
+            kern = (const void *)aggregate_rows<A, B, C, NK, EK>;                                     \
+            bytes = RowsLayout<A + B + C, A + 2, C>::bytes;                                           \
+            launch = [](dim3 gr, uint32_t l, hipStream_t st, const RowParams &rp) {                   \
+                hipLaunchKernelGGL((aggregate_rows<A, B, C, NK, EK>), gr, dim3(kRowThreads), l, st, rp); \
+            };                                                                                        \
+        }                                                                                             \
     }
         // 100 time dims with: bf16 node rows 128 wide and bf16 link rows 128
         // wide or none; no node rows and fp32 link rows 100 or 172 wide, or
@@ -1161,14 +1651,6 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
             if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kAggLdsMax) !=
                 hipSuccess)
                 return NLB_EDEVICE;
-            int cus = 0;
-            if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess ||
-                cus < 1)
-                return NLB_EDEVICE;
-            // One persistent workgroup per CU; groups of up to 16 queries,
-            // fewer when that leaves wavefronts without one.
-            const uint64_t waves = (uint64_t)cus * (kRowThreads / 64);
-            r.gq = (uint32_t)std::min<uint64_t>(kMaxGroupQ, std::max<uint64_t>(1, (nq + waves - 1) / waves));
             const uint64_t groups = ((uint64_t)nq + r.gq - 1) / r.gq;
             launch(dim3((unsigned)std::min<uint64_t>(groups, (uint64_t)cus)), bytes, (hipStream_t)stream, r);
             if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
