@@ -417,14 +417,20 @@ __device__ __forceinline__ void split4(const float v[4], u32x2 &hw, u32x2 &lw) {
 }
 
 // acc[ub] += W[16 ub .. 16 ub + 15][k-step] x (hi + lo) for the four unit blocks.
+// The four hi products are issued before the four lo products, so that no
+// product waits for the one just before it (the lo product of a unit block
+// accumulates onto its hi product's result).
 __device__ __forceinline__ void mfma4(f32x4 (&acc)[4], const __bf16 *W, uint32_t ls, uint32_t k0,
                                       uint32_t r16, uint32_t g, const bf16x8 &hi, const bf16x8 &lo,
                                       bool use_lo) {
+    bf16x8 a[4];
 #pragma unroll
-    for (int ub = 0; ub < 4; ub++) {
-        const bf16x8 a = *(const bf16x8 *)(W + (16u * ub + r16) * ls + k0 + 8u * g);
-        acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, hi, acc[ub], 0, 0, 0);
-        if (use_lo) acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, lo, acc[ub], 0, 0, 0);
+    for (int ub = 0; ub < 4; ub++) a[ub] = *(const bf16x8 *)(W + (16u * ub + r16) * ls + k0 + 8u * g);
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++) acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ub], hi, acc[ub], 0, 0, 0);
+    if (use_lo) {
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ub], lo, acc[ub], 0, 0, 0);
     }
 }
 
@@ -435,11 +441,14 @@ __device__ __forceinline__ void mfma4(f32x4 (&acc)[4], const __bf16 *W, uint32_t
 __device__ __forceinline__ void mfma4t(f32x4 (&acc)[4], const __bf16 *W, uint32_t ls, uint32_t k0,
                                        uint32_t r16, uint32_t g, const bf16x8 &hi, const bf16x8 &lo,
                                        bool use_lo) {
+    bf16x8 a[4];
 #pragma unroll
-    for (int ub = 0; ub < 4; ub++) {
-        const bf16x8 a = *(const bf16x8 *)(W + (16u * ub + r16) * ls + k0 + 8u * g);
-        acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, a, acc[ub], 0, 0, 0);
-        if (use_lo) acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, a, acc[ub], 0, 0, 0);
+    for (int ub = 0; ub < 4; ub++) a[ub] = *(const bf16x8 *)(W + (16u * ub + r16) * ls + k0 + 8u * g);
+#pragma unroll
+    for (int ub = 0; ub < 4; ub++) acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, a[ub], acc[ub], 0, 0, 0);
+    if (use_lo) {
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, a[ub], acc[ub], 0, 0, 0);
     }
 }
 
@@ -521,6 +530,24 @@ __device__ __forceinline__ float xor16_max(float v) {
     return v;
 }
 
+// Sum and maximum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (one lane of
+// each lane group), in every lane, with gfx950's row-swap instructions:
+// v_permlane16_swap on two copies of v leaves rows (0, 0, 2, 2) in one and
+// (1, 1, 3, 3) in the other, v_permlane32_swap halves (lo, lo) and (hi, hi);
+// combining each pair pairs lane l with l ^ 16, then with l ^ 32.
+__device__ __forceinline__ float groups_sum(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+__device__ __forceinline__ float groups_max(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = max2(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return max2(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 // LDS layout of aggregate_rows for K1S / K3S k-steps of layers 1 and 3 and
 // TKS k-steps of time encoding.
 template <int K1S, int K3S, int TKS>
@@ -562,7 +589,7 @@ __device__ __forceinline__ void piece_operand(const Piece8<KIND> &r, uint32_t di
 // valid rows, ne = 0); aggd holds the group's finished aggregates
 // sum_s alpha_s a1_s in the D layout (query r16's units 16 ub + 4 g + i in
 // the lanes with that r16).  Writes z for the lanes with vq.
-template <int NKS, int NK, uint32_t LS3>
+template <int NKS, int NK, uint32_t LS3, uint32_t PS>
 __device__ __forceinline__ void mlp_out_group(const RowParams &p, const Piece8<NK> (&ru)[NKS > 0 ? NKS : 1],
                                               int32_t nr, bool vq, const f32x4 (&aggd)[4], float ne,
                                               const __bf16 *W2, const __bf16 *W3, const __bf16 *W4,
@@ -581,7 +608,7 @@ __device__ __forceinline__ void mlp_out_group(const RowParams &p, const Piece8<N
     f32x4 hq[4];
 #pragma unroll
     for (int ub = 0; ub < 4; ub++) hq[ub] = f32x4(0.0f);
-    chain64(hq, aggd, W2, kPs, 0, r16, g);
+    chain64(hq, aggd, W2, PS, 0, r16, g);
 #pragma unroll
     for (int ub = 0; ub < 4; ub++)
 #pragma unroll
@@ -594,7 +621,7 @@ __device__ __forceinline__ void mlp_out_group(const RowParams &p, const Piece8<N
     f32x4 zo[4];
 #pragma unroll
     for (int ub = 0; ub < 4; ub++) zo[ub] = f32x4(0.0f);
-    chain64(zo, acc3, W4, kPs, 0, r16, g);
+    chain64(zo, acc3, W4, PS, 0, r16, g);
     if (vq) {
 #pragma unroll
         for (int ub = 0; ub < 4; ub++) {
@@ -986,13 +1013,11 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
             // [l % 16] and D[4 (l / 16) + i][l % 16]: the product sums the
             // groups, normalises, and leaves query cq's aggregate in column cq
             // of the D layout.
-            float M = max2(m, __shfl_xor(m, 16));
-            M = max2(M, __shfl_xor(M, 32));
+            const float M = groups_max(m);
             const float shift = (M == -INFINITY) ? 0.0f : M * kLog2eAgg;
             const float r = __builtin_amdgcn_exp2f(__builtin_fmaf(m, kLog2eAgg, -shift));
             float ds = den * r;
-            ds += __shfl_xor(ds, 16);
-            ds += __shfl_xor(ds, 32);
+            ds = groups_sum(ds);
             const float f = ds > 0.0f ? r * __builtin_amdgcn_rcpf(ds) : 0.0f;
             const float bq = r16 == cq ? f : 0.0f;
 #pragma unroll
@@ -1005,7 +1030,7 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
             for (int ub = 0; ub < 4; ub++) agg[ub] = 0.0f;
         }
         if (group_end) {
-            mlp_out_group<NKS, NK, L::ls3>(p, ru, nr, vq, aggd, ne, W2, W3, W4, b2, b3, b4, r16, g, cg * gq);
+            mlp_out_group<NKS, NK, L::ls3, kPs>(p, ru, nr, vq, aggd, ne, W2, W3, W4, b2, b3, b4, r16, g, cg * gq);
 #pragma unroll
             for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
             ne = 0.0f;
@@ -1063,16 +1088,24 @@ struct PackEntry {
     float dt;
 };
 
+// A lane's row of a block, and the query of its lane group's four rows.
+struct PackRow {
+    PackEntry en;
+    uint32_t qg;
+};
+
 // LDS layout: weights and time-encoding vectors as RowsLayout, then each
 // wavefront's list.
 template <int K1S, int K3S, int TKS>
 struct PackedLayout {
-    static constexpr uint32_t ls1 = 32u * K1S + 8u, ls3 = 32u * K3S + 8u;
+    // w2 / w4 rows padded like the others, so that the 16-byte operand reads
+    // of 16 consecutive rows fall on distinct banks.
+    static constexpr uint32_t ls1 = 32u * K1S + 8u, ls3 = 32u * K3S + 8u, ps = kH + 8u;
     static constexpr uint32_t o_w1 = 0;
     static constexpr uint32_t o_w2 = o_w1 + kH * ls1 * 2u;
-    static constexpr uint32_t o_w3 = o_w2 + kH * kPs * 2u;
+    static constexpr uint32_t o_w3 = o_w2 + kH * ps * 2u;
     static constexpr uint32_t o_w4 = o_w3 + kH * ls3 * 2u;
-    static constexpr uint32_t o_vec = o_w4 + kH * kPs * 2u;
+    static constexpr uint32_t o_vec = o_w4 + kH * ps * 2u;
     static constexpr uint32_t o_tenc = o_vec + 5u * kH * 4u;
     static constexpr uint32_t o_list = o_tenc + 2u * 32u * TKS * 4u;
     static constexpr uint32_t bytes = o_list + (kRowThreads / 64) * kPackList * (uint32_t)sizeof(PackEntry);
@@ -1119,8 +1152,8 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     }
     for (uint32_t u = tid; u < kH * kH; u += kRowThreads) {
         const uint32_t r = u / kH, c = u % kH;
-        W2[r * kPs + c] = p.w2[r * kH + chain_unit(c)];
-        W4[r * kPs + c] = p.w4[r * kH + chain_unit(c)];
+        W2[r * L::ps + c] = p.w2[r * kH + chain_unit(c)];
+        W4[r * L::ps + c] = p.w4[r * kH + chain_unit(c)];
         W3[r * L::ls3 + 32u * NKS + c] = p.w3[(size_t)r * (32u * K3S) + 32u * NKS + chain_unit(c)];
     }
     for (uint32_t u = tid; u < 5u * kH; u += kRowThreads) {
@@ -1247,15 +1280,19 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         return total;
     };
-    // Row r16 of block b of a list of n entries (past the end: empty).
-    auto read_entry = [&](uint32_t n, uint32_t b) -> PackEntry {
+    // Row r16 of block b of a list of n entries (past the end: empty), and
+    // the query of rows 4 g .. 4 g + 3 (those of one query's run, or past
+    // the list).
+    auto read_entry = [&](uint32_t n, uint32_t b) -> PackRow {
         const uint32_t idx = 16u * b + r16;
-        PackEntry en = lst[min(idx, n - 1u)];
+        PackRow pr;
+        pr.en = lst[min(idx, n - 1u)];
+        pr.qg = lst[min(16u * b + 4u * g, n - 1u)].q;
         if (idx >= n) {
-            en.x = -1;
-            en.dt = 0.0f;
+            pr.en.x = -1;
+            pr.en.dt = 0.0f;
         }
-        return en;
+        return pr;
     };
     struct Rows {
         Piece8<NK> n[NKS > 0 ? NKS : 1];
@@ -1285,7 +1322,8 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
     float mrun = -INFINITY, drun = 0.0f;
 
-    auto compute_block = [&](const PackEntry &en, const Rows &rc) {
+    auto compute_block = [&](const PackRow &pr, const Rows &rc) {
+        const PackEntry &en = pr.en;
         const bool valid = en.x >= 0;
         const bool ev = valid && (int64_t)en.e < p.edge_rows;
         f32x4 acc[4];
@@ -1379,20 +1417,15 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
             for (int i = 1; i < 4; i++) t = __builtin_fmaf(e[i], acc[ub][i], t);
             agg[ub] = t;
         }
-        // Merge the four partials into their queries' columns.  The quad's
-        // query is that of its first row (rows 4 g .. 4 g + 3 hold one query's
-        // run or lie past the list).
-        const uint32_t qg = (uint32_t)__shfl((int)en.q, (int)(4u * g));
-        const bool mine = qg == r16 && mg != -INFINITY;
+        // Merge the four partials into their queries' columns.
+        const bool mine = pr.qg == r16 && mg != -INFINITY;
         float bm = mine ? mg : -INFINITY;
-        bm = max2(bm, __shfl_xor(bm, 16));
-        bm = max2(bm, __shfl_xor(bm, 32));
+        bm = groups_max(bm);
         const float mnew = max2(mrun, bm);
         const float scl = (mrun == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f((mrun - mnew) * kLog2eAgg);
         const float r = mine ? __builtin_amdgcn_exp2f((mg - mnew) * kLog2eAgg) : 0.0f;
         float dc = dg * r;
-        dc += __shfl_xor(dc, 16);
-        dc += __shfl_xor(dc, 32);
+        dc = groups_sum(dc);
         drun = __builtin_fmaf(drun, scl, dc);
         mrun = mnew;
 #pragma unroll
@@ -1416,9 +1449,9 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     uint32_t n_cur = build_list(sr);
     issue_scan(g0 + gstep, nx_nd, id_t, sr);
     load_ids(g0 + 2 * gstep, id_nd, id_t);
-    PackEntry en_c = n_cur ? read_entry(n_cur, 0) : PackEntry{-1, 0u, 0u, 0.0f};
+    PackRow en_c = n_cur ? read_entry(n_cur, 0) : PackRow{PackEntry{-1, 0u, 0u, 0.0f}, 0u};
     Rows rows_c;
-    issue_rows(en_c, rows_c);
+    issue_rows(en_c.en, rows_c);
 
     for (uint64_t cg = g0; cg < groups; cg += gstep) {
         asm volatile("" ::: "memory");
@@ -1433,18 +1466,18 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         // r_u, the next group's list (its scan was issued a group ago) and
         // the next group's first block of rows.  The scan of the group after
         // is issued once the blocks are done.
-        auto advance = [&](PackEntry &en_n, Rows &rows_n) {
+        auto advance = [&](PackRow &en_n, Rows &rows_n) {
             if constexpr (NKS > 0) {
                 const uint8_t *urow = p.nfeat + (size_t)(nr >= 0 ? nr : 0) * p.nrb;
 #pragma unroll
                 for (int ks = 0; ks < NKS; ks++) load_piece<NK>(urow, p.n_dim, 32u * ks + 8u * g, ru[ks]);
             }
             n_next = build_list(sr);
-            en_n = n_next ? read_entry(n_next, 0) : PackEntry{-1, 0u, 0u, 0.0f};
-            issue_rows(en_n, rows_n);
+            en_n = n_next ? read_entry(n_next, 0) : PackRow{PackEntry{-1, 0u, 0u, 0.0f}, 0u};
+            issue_rows(en_n.en, rows_n);
         };
         if (nb == 0) {
-            PackEntry en_n;
+            PackRow en_n;
             Rows rows_n;
             advance(en_n, rows_n);
             en_c = en_n;
@@ -1454,11 +1487,11 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
             // Keeps the LDS-resident weights from being hoisted out of the
             // loop into long-lived registers.
             asm volatile("" ::: "memory");
-            PackEntry en_n;
+            PackRow en_n;
             Rows rows_n;
             if (b + 1 < nb) {
                 en_n = read_entry(n_cur, b + 1);
-                issue_rows(en_n, rows_n);
+                issue_rows(en_n.en, rows_n);
             } else {
                 advance(en_n, rows_n);
             }
@@ -1479,7 +1512,7 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         for (int ub = 0; ub < 4; ub++)
 #pragma unroll
             for (int i = 0; i < 4; i++) aggd[ub][i] *= inv;
-        mlp_out_group<NKS, NK, L::ls3>(p, ru, nr, vq, aggd, ne, W2, W3, W4, b2, b3, b4, r16, g, cg * gq);
+        mlp_out_group<NKS, NK, L::ls3, L::ps>(p, ru, nr, vq, aggd, ne, W2, W3, W4, b2, b3, b4, r16, g, cg * gq);
 #pragma unroll
         for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
         mrun = -INFINITY;
