@@ -1062,25 +1062,24 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
 // Per group of up to 16 queries a wavefront first reads all of the group's
 // slot words (lane (q = l % 16, g = l / 16) slots g, g + 4, g + 8, g + 12 of
 // query q, issued one group ahead), applies eq. (1) and writes the valid
-// slots to a list in LDS, query by query, each query's run padded to a
-// multiple of four rows with empty entries.  The list is then processed in
-// 16-row blocks.  Because runs are padded to four rows, the four rows
-// 4 g .. 4 g + 3 that lane group g holds after the transposed layer 1 belong
-// to one query; the lane group forms its rows' softmax partial (maximum,
-// sum of exponentials, exponential-weighted sum of layer-1 outputs), and one
-// fp32 matrix product per unit block adds the four partials into their
-// queries' columns of the group's running aggregates (the product's B
-// operand holds each partial's weight exp(m_g - M_q) in its query's column;
-// the columns are rescaled first when M_q, the running maximum of query q,
-// grows).  At the group's end every column is divided by its sum of
-// exponentials and MLP_out runs as in aggregate_rows.  Results differ from
-// aggregate_rows by summation order only.
+// slots to a list in LDS, query by query, with each entry's query in a byte
+// array beside it.  The list is then processed in 16-row blocks, whose rows
+// may belong to several queries.  After the transposed layer 1, lane group g
+// holds rows 4 g + i; each lane keeps the running maximum M_q and sum of
+// exponentials of its column q = l % 16, and the block's rows are added to
+// their queries' columns of the running aggregates by fp32 matrix products:
+// for each i, A holds the rows 4 g + i of layer 1 (unit x lane group) and B
+// the rows' weights exp(logit - M_q) in their queries' columns, so the
+// product sums each row into its own query (the columns are rescaled first
+// when a query's maximum grows).  At the group's end every column is divided
+// by its sum of exponentials and MLP_out runs as in aggregate_rows.  Results
+// differ from aggregate_rows by summation order only.
 constexpr uint32_t kPackMaxS = 16;                    // slots per node at most
 constexpr uint32_t kPackMinGroup = 8;                 // queries per group at least
 constexpr uint32_t kScanJ = kPackMaxS / 4;           // slots per lane in the group scan
 constexpr uint32_t kPackList = kMaxGroupQ * kPackMaxS;   // list entries per group at most
 
-// One list entry: a valid slot of query q of the group (x < 0: padding).
+// One list entry: a valid slot of query q of the group (x < 0: past the list).
 struct PackEntry {
     int32_t x;
     uint32_t e;
@@ -1088,10 +1087,11 @@ struct PackEntry {
     float dt;
 };
 
-// A lane's row of a block, and the query of its lane group's four rows.
+// A lane's row of a block, and the queries of its lane group's four rows
+// (one byte each, 255 past the list).
 struct PackRow {
     PackEntry en;
-    uint32_t qg;
+    uint32_t q4;
 };
 
 // LDS layout: weights and time-encoding vectors as RowsLayout, then each
@@ -1108,7 +1108,8 @@ struct PackedLayout {
     static constexpr uint32_t o_vec = o_w4 + kH * ps * 2u;
     static constexpr uint32_t o_tenc = o_vec + 5u * kH * 4u;
     static constexpr uint32_t o_list = o_tenc + 2u * 32u * TKS * 4u;
-    static constexpr uint32_t bytes = o_list + (kRowThreads / 64) * kPackList * (uint32_t)sizeof(PackEntry);
+    static constexpr uint32_t o_qs = o_list + (kRowThreads / 64) * kPackList * (uint32_t)sizeof(PackEntry);
+    static constexpr uint32_t bytes = o_qs + (kRowThreads / 64) * kPackList;
 };
 
 // Time-encoding columns in lane-group order: k-step ks, lane group g and
@@ -1192,6 +1193,7 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     const uint32_t lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint32_t r16 = lane & 15, g = lane >> 4;
     PackEntry *lst = (PackEntry *)(smem + L::o_list) + (size_t)wave * kPackList;
+    uint8_t *qs = smem + L::o_qs + (size_t)wave * kPackList;
     const float *b1 = vec, *b2 = vec + kH, *b3 = vec + 2 * kH, *b4 = vec + 3 * kH, *va = vec + 4 * kH;
     float b1v[4], vav[4];
 #pragma unroll
@@ -1239,8 +1241,9 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         }
     };
     // eq. (1) on the scanned words, then the list: query q's valid slots at
-    // base_q .. base_q + v_q - 1 (lane groups in order), padding up to
-    // base_q + pad4(v_q).  Returns the list length (a multiple of 4).
+    // base_q .. base_q + v_q - 1 (lane groups in order), and the entries'
+    // queries in qs, with 255 up to the end of the last block.  Returns the
+    // list length.
     auto build_list = [&](const ScanRaw &sr) -> uint32_t {
         SlotLds sl[kScanJ];
         uint32_t c = 0;
@@ -1256,38 +1259,37 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         const uint32_t u32 = (uint32_t)__shfl_up((int)inc, 32);
         if (g >= 2) inc += u32;
         const uint32_t vq = (uint32_t)__shfl((int)inc, (int)(48u + r16));
-        const uint32_t pq = (vq + 3u) & ~3u;
-        // Exclusive prefix of the padded runs over the 16 queries.
-        uint32_t run = pq;
+        // Exclusive prefix of the runs over the 16 queries.
+        uint32_t run = vq;
 #pragma unroll
         for (uint32_t d = 1; d < 16; d <<= 1) {
             const uint32_t t = (uint32_t)__shfl_up((int)run, d, 16);
             if (r16 >= d) run += t;
         }
-        const uint32_t base = run - pq;
+        const uint32_t base = run - vq;
         const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)run, 15);
         uint32_t pos = base + (inc - c);
 #pragma unroll
         for (uint32_t j = 0; j < kScanJ; j++) {
             if (sl[j].x >= 0) {
                 lst[pos] = PackEntry{sl[j].x, sl[j].e, r16, sl[j].dt};
+                qs[pos] = (uint8_t)r16;
                 pos++;
             }
         }
-        if (g < pq - vq) lst[base + vq + g] = PackEntry{-1, 0u, r16, 0.0f};
+        if (lane < 16 && total + lane < ((total + 15u) & ~15u)) qs[total + lane] = 0xFFu;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         return total;
     };
     // Row r16 of block b of a list of n entries (past the end: empty), and
-    // the query of rows 4 g .. 4 g + 3 (those of one query's run, or past
-    // the list).
+    // the queries of rows 4 g .. 4 g + 3.
     auto read_entry = [&](uint32_t n, uint32_t b) -> PackRow {
         const uint32_t idx = 16u * b + r16;
         PackRow pr;
         pr.en = lst[min(idx, n - 1u)];
-        pr.qg = lst[min(16u * b + 4u * g, n - 1u)].q;
+        pr.q4 = *(const uint32_t *)(qs + 16u * b + 4u * g);
         if (idx >= n) {
             pr.en.x = -1;
             pr.en.dt = 0.0f;
@@ -1391,7 +1393,7 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         for (int ub = 0; ub < 4; ub++)
 #pragma unroll
             for (int i = 0; i < 4; i++) acc[ub][i] = relu(acc[ub][i]);
-        // Logits of rows 4 g + i, then the lane group's softmax partial.
+        // Logits of rows 4 g + i (the lane group's rows; -inf where empty).
         float lg[4];
 #pragma unroll
         for (int i = 0; i < 4; i++) {
@@ -1403,37 +1405,38 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         const uint32_t nib = ((uint32_t)__builtin_amdgcn_ballot_w64(valid) >> (4u * g)) & 0xFu;
 #pragma unroll
         for (int i = 0; i < 4; i++) lg[i] = ((nib >> i) & 1u) ? lg[i] : -INFINITY;
-        const float mg = max2(max2(lg[0], lg[1]), max2(lg[2], lg[3]));
-        const float sh = (mg == -INFINITY) ? 0.0f : mg * kLog2eAgg;
-        float e[4];
+        // The block's rows into their queries' columns: the lane's column is
+        // query r16; bm is the largest logit of its rows in the block.
+        bool mine[4];
+        float bm = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < 4; i++) e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(lg[i], kLog2eAgg, -sh));
-        const float dg = (e[0] + e[1]) + (e[2] + e[3]);
-        float agg[4];
-#pragma unroll
-        for (int ub = 0; ub < 4; ub++) {
-            float t = e[0] * acc[ub][0];
-#pragma unroll
-            for (int i = 1; i < 4; i++) t = __builtin_fmaf(e[i], acc[ub][i], t);
-            agg[ub] = t;
+        for (int i = 0; i < 4; i++) {
+            mine[i] = ((pr.q4 >> (8 * i)) & 0xFFu) == r16;
+            bm = max2(bm, mine[i] ? lg[i] : -INFINITY);
         }
-        // Merge the four partials into their queries' columns.
-        const bool mine = pr.qg == r16 && mg != -INFINITY;
-        float bm = mine ? mg : -INFINITY;
         bm = groups_max(bm);
         const float mnew = max2(mrun, bm);
         const float scl = (mrun == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f((mrun - mnew) * kLog2eAgg);
-        const float r = mine ? __builtin_amdgcn_exp2f((mg - mnew) * kLog2eAgg) : 0.0f;
-        float dc = dg * r;
-        dc = groups_sum(dc);
+        const float sh = (mnew == -INFINITY) ? 0.0f : mnew * kLog2eAgg;
+        float wr[4];
+#pragma unroll
+        for (int i = 0; i < 4; i++)
+            wr[i] = mine[i] ? __builtin_amdgcn_exp2f(__builtin_fmaf(lg[i], kLog2eAgg, -sh)) : 0.0f;
+        const float dc = groups_sum((wr[0] + wr[1]) + (wr[2] + wr[3]));
         drun = __builtin_fmaf(drun, scl, dc);
         mrun = mnew;
 #pragma unroll
-        for (int ub = 0; ub < 4; ub++) {
+        for (int ub = 0; ub < 4; ub++)
 #pragma unroll
-            for (int i = 0; i < 4; i++) aggd[ub][i] *= scl;
-            aggd[ub] = __builtin_amdgcn_mfma_f32_16x16x4f32(agg[ub], r, aggd[ub], 0, 0, 0);
-        }
+            for (int j = 0; j < 4; j++) aggd[ub][j] *= scl;
+        // aggd[ub] += A_i B_i over the rows 4 g + i: A_i[unit][k = g] is
+        // layer 1 of row 4 g + i (this lane's acc[ub][i]), B_i[k = g][n] the
+        // row's weight in column n (this lane's wr[i] for n = r16).
+#pragma unroll
+        for (int i = 0; i < 4; i++)
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++)
+                aggd[ub] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[ub][i], wr[i], aggd[ub], 0, 0, 0);
     };
 
     // Prologue: the first group's list and the next group's scan in flight.
@@ -1449,7 +1452,7 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     uint32_t n_cur = build_list(sr);
     issue_scan(g0 + gstep, nx_nd, id_t, sr);
     load_ids(g0 + 2 * gstep, id_nd, id_t);
-    PackRow en_c = n_cur ? read_entry(n_cur, 0) : PackRow{PackEntry{-1, 0u, 0u, 0.0f}, 0u};
+    PackRow en_c = n_cur ? read_entry(n_cur, 0) : PackRow{PackEntry{-1, 0u, 0u, 0.0f}, ~0u};
     Rows rows_c;
     issue_rows(en_c.en, rows_c);
 
@@ -1473,7 +1476,7 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
                 for (int ks = 0; ks < NKS; ks++) load_piece<NK>(urow, p.n_dim, 32u * ks + 8u * g, ru[ks]);
             }
             n_next = build_list(sr);
-            en_n = n_next ? read_entry(n_next, 0) : PackRow{PackEntry{-1, 0u, 0u, 0.0f}, 0u};
+            en_n = n_next ? read_entry(n_next, 0) : PackRow{PackEntry{-1, 0u, 0u, 0.0f}, ~0u};
             issue_rows(en_n.en, rows_n);
         };
         if (nb == 0) {
