@@ -84,31 +84,49 @@ def sample_bytes(w, valid_slots, queries):
     return reads + writes
 
 
-def kernel_source_hash():
-    """sha256 over the sources of the sample kernels (nlb.hip and the shared
-    headers), the key under which counter summaries stay valid."""
+# Per call: the summary file (by workload name) and the sources its kernels
+# are built from.
+COUNTER_SOURCES = {
+    "nlb_sample": ("sample_gather_{}.md", ("nlb.hip", "nlb_internal.h", "nlb_divide.h")),
+    "nlb_aggregate": ("aggregate_packed_{}.md",
+                      ("aggregate.hip", "nlb_internal.h", "nlb_pieces.h", "nlb_divide.h")),
+}
+
+
+def kernel_source_hash(call="nlb_sample"):
+    """sha256 over the sources of a call's kernels, the key under which
+    counter summaries stay valid."""
     import hashlib
     hs = hashlib.sha256()
-    for f in ("nlb.hip", "nlb_internal.h", "nlb_divide.h"):
+    for f in COUNTER_SOURCES[call][1]:
         hs.update(open(os.path.join(ROOT, "paper_2402_01964_amd", "csrc", f), "rb").read())
     return hs.hexdigest()
 
 
-def measured_traffic(w):
-    """HBM bytes per nlb_sample call (all its launches) from the committed
-    rocprofv3 counter summary of this workload, or None when there is none
-    or the kernel sources have changed since the counters were taken."""
+def measured_traffic(w, call="nlb_sample"):
+    """HBM bytes per call (all its launches) from the committed rocprofv3
+    counter summary of this workload, or None when there is none or the
+    kernel sources have changed since the counters were taken."""
     import re
-    path = os.path.join(ROOT, "profiles", f"sample_gather_{w.name}.md")
+    path = os.path.join(ROOT, "profiles", COUNTER_SOURCES[call][0].format(w.name))
     if not os.path.exists(path):
         return None
-    m = re.search(r"counters: workload=(\S+) call=nlb_sample traffic_bytes_per_call=(\S+) "
+    m = re.search(r"counters: workload=(\S+) call=(\S+) traffic_bytes_per_call=(\S+) "
                   r"kernel_source_sha256=([0-9a-f]+)", open(path).read())
-    if not m or m.group(1) != w.name:
+    if not m or m.group(1) != w.name or m.group(2) != call:
         return None
-    if kernel_source_hash() != m.group(3):
+    if kernel_source_hash(call) != m.group(4):
         return None
-    return float(m.group(2))
+    return float(m.group(3))
+
+
+def aggregate_kernel(w, queries, cus):
+    """The eq. (4) kernel a launch of `queries` takes on this workload's
+    shapes (the library's own choice, restated for the record): the packed
+    form for tables of at most 16 slots when its query groups hold at least
+    8 queries, else the per-query form."""
+    gq = min(16, max(1, -(-queries // (cus * 8))))
+    return "aggregate_packed" if w.s <= 16 and gq >= 8 else "aggregate_rows"
 
 
 def hop2_bytes(w, hop1_valid, queries):
@@ -757,8 +775,13 @@ def main():
         fl = aggregate_flops(w, valid, queries)
         ab = aggregate_bytes(w, valid, queries)
         t_s = sample_ms.sum() * 1e-3
-        res["roofline"] = dict(binding_roofline(fl, ab, t_s), traffic=None,
-                               kernel="nlb_aggregate: aggregate_rows", flops_per_launch=fl / K,
+        cus = torch.cuda.get_device_properties(0).multi_processor_count
+        kname = aggregate_kernel(w, 3 * w.batch, cus)
+        agg_traffic = measured_traffic(w, "nlb_aggregate") if kname == "aggregate_packed" else None
+        res["roofline"] = dict(binding_roofline(fl, ab, t_s), traffic=agg_traffic,
+                               traffic_unit="bytes per nlb_aggregate launch (rocprofv3 FETCH_SIZE "
+                                            "+ WRITE_SIZE, reads scaled by a random-gather kernel)",
+                               kernel="nlb_aggregate: " + kname, flops_per_launch=fl / K,
                                bytes_per_launch=ab / K)
         res["aggregate_ms_avg"] = res.pop("sample_ms_avg")
         res["aggregate_kernel_queries_per_s"] = res.pop("sample_kernel_queries_per_s")

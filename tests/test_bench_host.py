@@ -57,9 +57,21 @@ def test_counter_summary_is_used_only_for_the_current_sources(monkeypatch):
     w = synth.workload(5)
     t = bench.measured_traffic(w)
     assert t is not None and 1e9 < t < 1e10
-    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "0" * 64)
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda call="nlb_sample": "0" * 64)
     assert bench.measured_traffic(w) is None
     assert bench.measured_traffic(synth.workload(1)) is None   # no summary for that workload
+
+
+def test_aggregate_counter_summary_and_kernel_choice(monkeypatch):
+    w = synth.workload(5)
+    t = bench.measured_traffic(w, "nlb_aggregate")
+    assert t is not None and 1e8 < t < 1e10
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda call="nlb_sample": "0" * 64)
+    assert bench.measured_traffic(w, "nlb_aggregate") is None
+    # 300 000 queries on 256 CUs: groups of 16 (packed); 600 queries: groups of 1
+    assert bench.aggregate_kernel(w, 300000, 256) == "aggregate_packed"
+    assert bench.aggregate_kernel(synth.workload(1), 600, 256) == "aggregate_rows"
+    assert bench.aggregate_kernel(synth.workload(3), 12000, 256) == "aggregate_rows"   # s = 64
 
 
 def test_more_than_one_gpu_is_refused():
