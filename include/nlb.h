@@ -218,8 +218,13 @@ int nlb_sample_hop2(nlb_table *h, const int32_t *hop1_nbr, const uint32_t *tq, u
  * MLP_in's second layer is affine, so the library may apply it once to the
  * softmax-weighted sum of the first layer's outputs instead of to every
  * slot (the logits then use W_b^T w); only the rounding order differs.
- * z is device fp32 [nq][H].  Tables with s > 64 are not supported
- * (NLB_EINVAL).  nq == 0 is a no-op.  Errors: as nlb_sample, and NLB_EINVAL
+ * z is device fp32 [nq][H].  Tables with s > 64 are supported for the input
+ * shapes the per-query kernel is built for and rejected (NLB_EINVAL) for
+ * others: a time encoding of 97 to 128 dimensions with 16-byte-aligned bf16
+ * node rows of 97 to 128 values and no link rows or such bf16 link rows, or
+ * no node rows and fp32 link rows of 97 to 128 or 161 to 192 values
+ * (16-byte aligned) or bf16 link rows of 161 to 192 values (4-byte aligned).
+ * nq == 0 is a no-op.  Errors: as nlb_sample, and NLB_EINVAL
  * for a bad weight set.  Graph capture: as nlb_sample (besides its kernels
  * the call makes only host-side attribute queries and settings). */
 #define NLB_AGG_HIDDEN 64

@@ -1544,7 +1544,7 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
     if (!h || !wts) return NLB_EINVAL;
     if (nq == 0) return NLB_OK;
     if (!node || !tq || !z) return NLB_EINVAL;
-    if (wts->hidden != kH || h->s > 16u * kMaxBlocks) return NLB_EINVAL;
+    if (wts->hidden != kH) return NLB_EINVAL;
     if (!wts->w1 || !wts->w2 || !wts->w3 || !wts->w4 || !wts->b1 || !wts->b2 || !wts->b3 ||
         !wts->b4 || !wts->att)
         return NLB_EINVAL;
@@ -1694,6 +1694,8 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
         }
     }
 
+    // The tiled kernel holds at most 64 slot rows of one query.
+    if (h->s > 16u * kMaxBlocks) return NLB_EINVAL;
     // Tile: as many queries as fit the LDS budget (at most 128 slot rows),
     // fewer when that leaves too few workgroups to fill the GPU.
     // A tile larger than one query must fit the budget that keeps four

@@ -189,3 +189,48 @@ def test_device_cosine_dense_sweep(sweep):
                 _log(f"cosine sweep {sweep}, {name} path, {lo:.0e} <= |x| < {hi:.0e}: {int(sel.sum())} "
                      f"values, max abs error {e:.2e}")
                 assert e <= tol, (sweep, name, lo, e)
+
+
+@pytest.mark.parametrize("k,s", [(5, 100), (5, 1024), (1, 200)])
+def test_aggregate_tables_wider_than_64_slots(k, s):
+    """eq. (4) on tables of more than 64 slots, which the per-query kernel
+    takes in ceil(s / 16) blocks per query, against the oracle on sampled
+    queries of launches of 3 000 and 70 001 queries; a shape that only the
+    tiled kernel serves is refused for such tables."""
+    import dataclasses
+    import paper_2402_01964_amd as nlb
+    from tests.test_gpu_parity import AGG_TOL, _agg_dev, agg_error
+    base = synth.workload(k)
+    w = dataclasses.replace(synth.scaled(base, 8 * base.batch, num_nodes=min(base.num_nodes, 20000)), s=s)
+    src, dst, t, _ = synth.host_links(w)
+    ef = synth.host_features(w, "edge") if w.edge_dim else None
+    nf = synth.host_features(w, "node") if w.node_dim else None
+    g = make_gpu_table(w, feat_to_dev(ef, w.edge_dtype) if ef is not None else None,
+                       feat_to_dev(nf, w.node_dtype) if nf is not None else None)
+    o = make_oracle(w)
+    g.insert(to_dev(src), to_dev(dst), to_dev(t))
+    o.insert(src, dst, t)
+    W = synth.agg_weights(w)
+    fw, fb = synth.time_params(w)
+    rng = np.random.default_rng(300 + s)
+    ends = np.concatenate([src, dst])
+    for nq in (3000, 70001):
+        q = ends[rng.integers(0, len(ends), nq)].astype(np.int32)
+        tq = rng.integers(0, int(t[-1]) + 2, nq).astype(np.uint32)
+        tq[::9] = 0
+        gz = g.aggregate(to_dev(q), to_dev(tq), _agg_dev(W)).cpu().numpy()
+        pos = np.sort(rng.choice(nq, 400, replace=False))
+        oz = o.aggregate(q[pos], tq[pos], fw, fb, ef, nf, W)
+        err = agg_error(gz[pos], oz)
+        _log(f"aggregate, workload {k} shapes, s={s}, {nq} queries: max scaled error {err:.3e}")
+        assert err <= AGG_TOL, (nq, err)
+    assert g.status() == nlb.NLB_OK
+    g.close()
+    # node rows 200 wide: no per-query instance, so s > 64 is refused
+    w2 = dataclasses.replace(w, node_dim=200, node_dtype="bf16", edge_dim=0)
+    nf2 = synth.host_features(w2, "node")
+    g2 = make_gpu_table(w2, None, feat_to_dev(nf2, "bf16"))
+    with pytest.raises(nlb.NLBError) as err:
+        g2.aggregate(to_dev(q[:10]), to_dev(tq[:10]), _agg_dev(synth.agg_weights(w2)))
+    assert err.value.code == nlb.NLB_EINVAL
+    g2.close()
