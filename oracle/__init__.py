@@ -92,7 +92,7 @@ def _load():
     lib.orc_sample_hop2.argtypes = [P, P, P, i64, i32, P, P, P, i64, i64, P, i64,
                                     P, P, P, P, P, P, P]
     lib.orc_aggregate.restype = ctypes.c_int
-    lib.orc_aggregate.argtypes = [P, P, P, i64, i32, P, P, P, i64, i32, i32, P, i32, i32, i32,
+    lib.orc_aggregate.argtypes = [P, P, P, i64, i32, P, P, P, i64, i32, i32, P, i32, i32, i32, i32,
                                   P, P, P, P, P, P, P, P, P, P]
     lib.orc_gru_update.restype = ctypes.c_int
     lib.orc_gru_update.argtypes = [i64, i32, P, i32, P, P, P, i64, u64, i32, P, P, P, i64, i32, i32,
@@ -289,12 +289,13 @@ class Oracle:
         return out
 
 
-    def aggregate(self, node, tq, w, b, efeat, nfeat, weights):
+    def aggregate(self, node, tq, w, b, efeat, nfeat, weights, heads=1):
         """Eq. (4) attention aggregation (forward, fp64) for queries
         (node[i], tq[i]); ``weights`` holds w1, b1, w2, b2, att, w3, b3, w4, b4
         (bf16 matrices as uint16 bits in the padded layouts of
         nlb_oracle.c).  ``efeat``/``nfeat``: 2-D float32 or bf16-bits (uint16)
-        arrays or None.  Returns z [nq, H] (float64)."""
+        arrays or None.  ``heads`` attention heads, each over its own slice
+        of MLP_in's outputs (App. E uses two).  Returns z [nq, H] (float64)."""
         node, tq = _c(node, np.int32), _c(tq, np.uint32)
         w, b = _c(w, np.float32), _c(b, np.float32)
         H = int(weights["b1"].shape[0])
@@ -312,9 +313,11 @@ class Oracle:
         z = np.empty((len(node), H), np.float64)
         rc = self._lib.orc_aggregate(
             self._h, _ptr(node), _ptr(tq), len(node), len(w), _ptr(w), _ptr(b),
-            _ptr(ef), erows, e_dim, e_dt, _ptr(nf), n_dim, n_dt, H,
+            _ptr(ef), erows, e_dim, e_dt, _ptr(nf), n_dim, n_dt, H, int(heads),
             _ptr(W["w1"]), _ptr(W["b1"]), _ptr(W["w2"]), _ptr(W["b2"]), _ptr(W["att"]),
             _ptr(W["w3"]), _ptr(W["b3"]), _ptr(W["w4"]), _ptr(W["b4"]), _ptr(z))
+        if rc == -2:
+            raise ValueError("oracle: heads must divide the hidden width")
         if rc != 0:
             raise ValueError("oracle: query node out of range")
         return z

@@ -408,18 +408,24 @@ static void affine(const uint16_t *W, int64_t ld, int64_t col0, const float *bia
  *   w2: [H][H]; w3: [H][pad32(n_dim) + H]  (r_u | aggregate); w4: [H][H]
  * Biases and att (the vector w) are fp32 [H].  Feature dtypes: 0 fp32, 1 bf16.
  * A stored link with eid >= e_rows has no link-feature row: its e is zero
- * (as in orc_sample).  z_out is [nq][H].  Returns -1 on an out-of-range
- * query node.
+ * (as in orc_sample).  z_out is [nq][H].
+ * Attention heads (the experiments use two, App. E): with `heads` = A, the
+ * H outputs of MLP_in are split into A consecutive slices of H / A; head a
+ * scores slot i with w[slice a] . MLP_in(...)_i[slice a], takes its own
+ * softmax over the valid slots, and fills slice a of the aggregate with
+ * its weighted sum of slice a of the messages.  A = 1 is the formula above.
+ * Returns -1 on an out-of-range query node, -2 when A does not divide H.
  */
 int orc_aggregate(const orc *o, const int32_t *node, const uint32_t *tq, int64_t nq,
                   int32_t d_t, const float *w, const float *b,
                   const uint8_t *efeat, int64_t e_rows, int32_t e_dim, int32_t e_dtype,
                   const uint8_t *nfeat, int32_t n_dim, int32_t n_dtype,
-                  int32_t H, const uint16_t *w1, const float *b1, const uint16_t *w2,
+                  int32_t H, int32_t heads, const uint16_t *w1, const float *b1, const uint16_t *w2,
                   const float *b2, const float *att, const uint16_t *w3, const float *b3,
                   const uint16_t *w4, const float *b4, double *z_out)
 {
-    const int64_t s = o->s;
+    if (heads < 1 || H % heads != 0) return -2;
+    const int64_t s = o->s, hw = H / heads;   /* units per head */
     const int64_t e_bytes = (int64_t)e_dim * (e_dtype == 0 ? 4 : 2);
     const int64_t n_bytes = (int64_t)n_dim * (n_dtype == 0 ? 4 : 2);
     const int64_t k1 = pad32(n_dim) + pad32(e_dim) + pad32(d_t);
@@ -427,7 +433,7 @@ int orc_aggregate(const orc *o, const int32_t *node, const uint32_t *tq, int64_t
     double *x = (double *)malloc(sizeof(double) * (size_t)(n_dim + e_dim + d_t + 1));
     double *a = (double *)malloc(sizeof(double) * (size_t)H);
     double *h = (double *)malloc(sizeof(double) * (size_t)(s * H));
-    double *logit = (double *)malloc(sizeof(double) * (size_t)s);
+    double *logit = (double *)malloc(sizeof(double) * (size_t)(s * heads));
     double *y = (double *)malloc(sizeof(double) * (size_t)(n_dim + H + 1));
     int *valid = (int *)malloc(sizeof(int) * (size_t)s);
     int rc = 0;
@@ -460,20 +466,25 @@ int orc_aggregate(const orc *o, const int32_t *node, const uint32_t *tq, int64_t
                 a[j] = acc > 0.0 ? acc : 0.0;                  /* ReLU */
             }
             affine(w2, H, 0, b2, a, H, H, h + sl * H);
-            double l = 0.0;                                    /* attention logit w^T h */
-            for (int64_t j = 0; j < H; j++) l += (double)att[j] * h[sl * H + j];
-            logit[sl] = l;
+            for (int64_t hd = 0; hd < heads; hd++) {          /* logit of head hd: w . h on its slice */
+                double l = 0.0;
+                for (int64_t j = hd * hw; j < (hd + 1) * hw; j++) l += (double)att[j] * h[sl * H + j];
+                logit[sl * heads + hd] = l;
+            }
         }
-        /* softmax over the valid slots, then the weighted sum */
+        /* per head: softmax over the valid slots, then the weighted sum of its slice */
         for (int64_t j = 0; j < H; j++) y[n_dim + j] = 0.0;
         if (any) {
-            double m = -INFINITY, den = 0.0;
-            for (int64_t sl = 0; sl < s; sl++) if (valid[sl] && logit[sl] > m) m = logit[sl];
-            for (int64_t sl = 0; sl < s; sl++) if (valid[sl]) den += exp(logit[sl] - m);
-            for (int64_t sl = 0; sl < s; sl++) {
-                if (!valid[sl]) continue;
-                const double alpha = exp(logit[sl] - m) / den;
-                for (int64_t j = 0; j < H; j++) y[n_dim + j] += alpha * h[sl * H + j];
+            for (int64_t hd = 0; hd < heads; hd++) {
+                double m = -INFINITY, den = 0.0;
+                for (int64_t sl = 0; sl < s; sl++)
+                    if (valid[sl] && logit[sl * heads + hd] > m) m = logit[sl * heads + hd];
+                for (int64_t sl = 0; sl < s; sl++) if (valid[sl]) den += exp(logit[sl * heads + hd] - m);
+                for (int64_t sl = 0; sl < s; sl++) {
+                    if (!valid[sl]) continue;
+                    const double alpha = exp(logit[sl * heads + hd] - m) / den;
+                    for (int64_t j = hd * hw; j < (hd + 1) * hw; j++) y[n_dim + j] += alpha * h[sl * H + j];
+                }
             }
         }
         /* MLP_out on y = [r_u ; aggregate] */

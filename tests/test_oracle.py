@@ -782,14 +782,19 @@ def _pad_last(a, to):
     return np.concatenate([a, np.zeros(a.shape[:-1] + (to - a.shape[-1],))], axis=-1)
 
 
-def test_aggregate_matches_library_attention_pooling():
+@pytest.mark.parametrize("heads", [1, 2, 4])
+def test_aggregate_matches_library_attention_pooling(heads):
     """Eq. (4) rebuilt from library routines in float64 on the oracle's own
     sample outputs (pinned above): torch's F.linear for the four layers
     (weights [out][in], as the layouts state) and scaled_dot_product_attention
     with the attention vector as the single query, the messages as keys and
     values, scale 1 and the validity mask; a query without a valid slot
-    aggregates the zero vector.  A transposed square weight, a dropped bias,
-    a wrong mask or a wrong order of the input segments fails this."""
+    aggregates the zero vector.  With several heads (App. E uses two), the
+    library's multi-head layout: query, keys and values split into `heads`
+    consecutive slices of the hidden width, one attention per slice, the
+    outputs concatenated.  A transposed square weight, a dropped bias, a
+    wrong mask, a wrong order of the input segments or a head scored over
+    the wrong slice fails this."""
     import torch
     import torch.nn.functional as F
     import synth
@@ -816,7 +821,7 @@ def test_aggregate_matches_library_attention_pooling():
             tq[5 + i] = live.max()
             at_entry += 1
     assert at_entry >= 20
-    z = o.aggregate(q, tq, fw, fb, ef, nf, W)
+    z = o.aggregate(q, tq, fw, fb, ef, nf, W, heads=heads)
 
     out = o.sample(q, tq, fw, fb, ef, nf)
     valid = out["nbr"] >= 0
@@ -830,9 +835,12 @@ def test_aggregate_matches_library_attention_pooling():
     Wt = {k: T(_bf16_to_f64(v) if k[0] == "w" and k != "att" else v.astype(np.float64))
           for k, v in W.items()}
     msg = F.linear(F.relu(F.linear(T(x), Wt["w1"], Wt["b1"])), Wt["w2"], Wt["b2"])   # [nq, s, H]
-    query = Wt["att"].expand(len(q), 1, -1).contiguous()
-    agg = F.scaled_dot_product_attention(query, msg, msg, attn_mask=torch.from_numpy(valid)[:, None, :],
-                                         scale=1.0)[:, 0, :]
+    nq, H = len(q), msg.shape[-1]
+    kv = msg.reshape(nq, s, heads, H // heads).transpose(1, 2).contiguous()          # [nq, heads, s, H/heads]
+    query = Wt["att"].reshape(1, heads, 1, H // heads).expand(nq, -1, -1, -1).contiguous()
+    mask = torch.from_numpy(valid)[:, None, None, :]
+    agg = F.scaled_dot_product_attention(query, kv, kv, attn_mask=mask, scale=1.0)   # [nq, heads, 1, H/heads]
+    agg = agg[:, :, 0, :].reshape(nq, H).clone()
     agg[~torch.from_numpy(valid.any(axis=1))] = 0.0
     y = torch.cat([T(_pad_last(_bf16_to_f64(out["self"]), p32(w.node_dim))), agg], dim=-1)
     ref = F.linear(F.relu(F.linear(y, Wt["w3"], Wt["b3"])), Wt["w4"], Wt["b4"]).numpy()
