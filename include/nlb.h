@@ -218,6 +218,13 @@ int nlb_sample_hop2(nlb_table *h, const int32_t *hop1_nbr, const uint32_t *tq, u
  * MLP_in's second layer is affine, so the library may apply it once to the
  * softmax-weighted sum of the first layer's outputs instead of to every
  * slot (the logits then use W_b^T w); only the rounding order differs.
+ * Attention heads (the experiments use two, App. E): with heads = A, MLP_in's
+ * H outputs are split into A consecutive slices of H / A; head a scores a
+ * slot with w[slice a] . MLP_in(...)[slice a], takes its own softmax over the
+ * valid slots and fills slice a of the aggregate.  A = 1 is the formula
+ * above.  One head runs in every kernel form, two in the per-query and
+ * tiled forms, four and eight in the tiled form (tables of at most 64
+ * slots); any other count is NLB_EINVAL.
  * z is device fp32 [nq][H].  Tables with s > 64 are supported for the input
  * shapes the per-query kernel is built for and rejected (NLB_EINVAL) for
  * others: a time encoding of 97 to 128 dimensions with 16-byte-aligned bf16
@@ -235,6 +242,7 @@ typedef struct nlb_agg_weights {
     int32_t hidden;          /* must be NLB_AGG_HIDDEN */
     int32_t node_dtype;      /* element type of the table's node rows: NLB_DTYPE_F32 / _BF16 */
     int32_t edge_dtype;      /* element type of the table's link rows */
+    int32_t heads;           /* attention heads A: 0 or 1 for one, else 2, 4 or 8 */
     const uint16_t *w1;      /* bf16 bits */
     const float *b1;
     const uint16_t *w2;

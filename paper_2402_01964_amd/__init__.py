@@ -56,7 +56,7 @@ class _SampleOut(ctypes.Structure):
 
 class _AggWeights(ctypes.Structure):
     _fields_ = [("hidden", ctypes.c_int32), ("node_dtype", ctypes.c_int32),
-                ("edge_dtype", ctypes.c_int32)] + \
+                ("edge_dtype", ctypes.c_int32), ("heads", ctypes.c_int32)] + \
                [(k, ctypes.c_void_p) for k in ("w1", "b1", "w2", "b2", "att", "w3", "b3", "w4", "b4")]
 
 
@@ -260,17 +260,19 @@ class Table:
         self.sample_hop2_into(hop1_nbr, tq, out, stream)
         return {k: v.view(nq, self.s, *v.shape[1:]) for k, v in out.items()}
 
-    def aggregate(self, node, tq, weights: dict, out=None, stream=None):
+    def aggregate(self, node, tq, weights: dict, out=None, stream=None, heads: int = 1):
         """Eq. (4) attention aggregation for queries (node[i], tq[i]).
         ``weights``: device tensors w1..w4 (bf16, or 16-bit ints holding bf16
-        bits, padded layouts of include/nlb.h) and b1..b4, att (fp32).
-        Returns (or fills) z, fp32 [nq, AGG_HIDDEN]."""
+        bits, padded layouts of include/nlb.h) and b1..b4, att (fp32);
+        ``heads`` attention heads, each over its own slice of the hidden
+        width.  Returns (or fills) z, fp32 [nq, AGG_HIDDEN]."""
         import torch
         nq = int(node.numel())
         if tq.numel() != nq:
             raise ValueError("node and tq must have the same length")
         aw = _AggWeights()
         aw.hidden = AGG_HIDDEN
+        aw.heads = int(heads)
 
         def dt(feat):
             return DTYPE_F32 if feat is None or feat.dtype == torch.float32 else DTYPE_BF16

@@ -69,6 +69,7 @@ struct AggParams {
     const float *b1, *b2, *b3, *b4, *att;
     float *z;
     uint32_t *status;
+    uint32_t heads;                  // attention heads, each over H / heads of the messages
 };
 
 // acc[rb] += A_rb (16 x K, from the LDS pair Ah/Al with row stride `as`)
@@ -229,33 +230,35 @@ __global__ __launch_bounds__(kAggThreads) void aggregate_fused(AggParams p) {
     }
     __syncthreads();
 
-    // Attention logits w^T h of the valid slots.
-    for (uint32_t j = tid; j < p.rows; j += kAggThreads) {
+    // Attention logits of the valid slots, one per head over its slice of
+    // the messages: logit[j * heads + a] = w[slice a] . h_j[slice a].
+    const uint32_t heads = p.heads, hw = kH / heads;
+    for (uint32_t u = tid; u < p.rows * heads; u += kAggThreads) {
+        const uint32_t j = u / heads, a = u - j * heads;
         float l = 0.0f;
         if (slots[j].x >= 0) {
             const float *h = Hf + j * kHf;
-#pragma unroll 8
-            for (int n = 0; n < kH; n++) l = __builtin_fmaf(p.att[n], h[n], l);
+            for (uint32_t n = a * hw; n < (a + 1) * hw; n++) l = __builtin_fmaf(p.att[n], h[n], l);
         }
-        logit[j] = l;
+        logit[u] = l;
     }
     __syncthreads();
 
     // MLP_out inputs y = [r_u | softmax-weighted sum of the messages].
     const uint32_t kn = p.k3 - kH;   // pad32(node_dim)
     for (uint32_t t = tid; t < p.qrows * kH; t += kAggThreads) {
-        const uint32_t q = t / kH, n = t % kH;
+        const uint32_t q = t / kH, n = t % kH, hd = n / hw;   // unit n belongs to head hd
         float value = 0.0f;
         if (q < nqt) {
             const uint32_t base = q * s;
             float m = -INFINITY;
             for (uint32_t a = 0; a < s; a++)
-                if (slots[base + a].x >= 0) m = fmaxf(m, logit[base + a]);
+                if (slots[base + a].x >= 0) m = fmaxf(m, logit[(base + a) * heads + hd]);
             if (m > -INFINITY) {
                 float den = 0.0f, num = 0.0f;
                 for (uint32_t a = 0; a < s; a++) {
                     if (slots[base + a].x < 0) continue;
-                    const float ex = expf(logit[base + a] - m);
+                    const float ex = expf(logit[(base + a) * heads + hd] - m);
                     den += ex;
                     num = __builtin_fmaf(ex, Hf[(base + a) * kHf + n], num);
                 }
@@ -420,17 +423,21 @@ __device__ __forceinline__ void split4(const float v[4], u32x2 &hw, u32x2 &lw) {
 // The four hi products are issued before the four lo products, so that no
 // product waits for the one just before it (the lo product of a unit block
 // accumulates onto its hi product's result).
+// Only the unit blocks UB0 <= ub < UB1 are computed.
+template <int UB0 = 0, int UB1 = 4>
 __device__ __forceinline__ void mfma4(f32x4 (&acc)[4], const __bf16 *W, uint32_t ls, uint32_t k0,
                                       uint32_t r16, uint32_t g, const bf16x8 &hi, const bf16x8 &lo,
                                       bool use_lo) {
     bf16x8 a[4];
 #pragma unroll
-    for (int ub = 0; ub < 4; ub++) a[ub] = *(const bf16x8 *)(W + (16u * ub + r16) * ls + k0 + 8u * g);
+    for (int ub = UB0; ub < UB1; ub++) a[ub] = *(const bf16x8 *)(W + (16u * ub + r16) * ls + k0 + 8u * g);
 #pragma unroll
-    for (int ub = 0; ub < 4; ub++) acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ub], hi, acc[ub], 0, 0, 0);
+    for (int ub = UB0; ub < UB1; ub++)
+        acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ub], hi, acc[ub], 0, 0, 0);
     if (use_lo) {
 #pragma unroll
-        for (int ub = 0; ub < 4; ub++) acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ub], lo, acc[ub], 0, 0, 0);
+        for (int ub = UB0; ub < UB1; ub++)
+            acc[ub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ub], lo, acc[ub], 0, 0, 0);
     }
 }
 
@@ -454,7 +461,8 @@ __device__ __forceinline__ void mfma4t(f32x4 (&acc)[4], const __bf16 *W, uint32_
 
 // act (a layer's output in the D layout, 64 units) -> next layer through
 // weights whose 64 columns from k0 on are in chained order (row stride ls):
-// out[ub] += Wp x act.
+// out[ub] += Wp x act, for the output unit blocks UB0 <= ub < UB1.
+template <int UB0 = 0, int UB1 = 4>
 __device__ __forceinline__ void chain64(f32x4 (&out)[4], const f32x4 (&act)[4], const __bf16 *Wp,
                                         uint32_t ls, uint32_t k0, uint32_t r16, uint32_t g) {
 #pragma unroll
@@ -467,7 +475,7 @@ __device__ __forceinline__ void chain64(f32x4 (&out)[4], const f32x4 (&act)[4], 
         }
         bf16x8 hi, lo;
         split8(v, hi, lo);
-        mfma4(out, Wp, ls, k0 + 32u * ks, r16, g, hi, lo, true);
+        mfma4<UB0, UB1>(out, Wp, ls, k0 + 32u * ks, r16, g, hi, lo, true);
     }
 }
 
@@ -558,7 +566,7 @@ struct RowsLayout {
     static constexpr uint32_t o_w3 = o_w2 + kH * kPs * 2u;
     static constexpr uint32_t o_w4 = o_w3 + kH * ls3 * 2u;
     static constexpr uint32_t o_vec = o_w4 + kH * kPs * 2u;
-    static constexpr uint32_t o_tenc = o_vec + 5u * kH * 4u;   // w | b, 32 TKS each, zero-padded
+    static constexpr uint32_t o_tenc = o_vec + 6u * kH * 4u;   // w | b, 32 TKS each, zero-padded
     // Per wavefront: the time encodings of a block's 16 rows, bf16 hi | lo
     // (32 TKS each) plus 8 elements of padding per row, and the list of the
     // block's valid rows (row, dt).
@@ -586,12 +594,13 @@ __device__ __forceinline__ void piece_operand(const Piece8<KIND> &r, uint32_t di
 
 // MLP_out for a group of up to 16 queries: row r16 = query qb + r16, input
 // [r_u | aggregate], the aggregate w2 aggd + b2 (zero for a query without
-// valid rows, ne = 0); aggd holds the group's finished aggregates
-// sum_s alpha_s a1_s in the D layout (query r16's units 16 ub + 4 g + i in
-// the lanes with that r16).  Writes z for the lanes with vq.
-template <int NKS, int NK, uint32_t LS3, uint32_t PS>
+// valid rows, ne = 0); aggd[a] holds head a's finished aggregates
+// sum_s alpha_{s,a} a1_s in the D layout (query r16's units 16 ub + 4 g + i
+// in the lanes with that r16), of which head a's slice of w2's outputs is
+// taken.  Writes z for the lanes with vq.
+template <int NKS, int NK, uint32_t LS3, uint32_t PS, int HEADS>
 __device__ __forceinline__ void mlp_out_group(const RowParams &p, const Piece8<NK> (&ru)[NKS > 0 ? NKS : 1],
-                                              int32_t nr, bool vq, const f32x4 (&aggd)[4], float ne,
+                                              int32_t nr, bool vq, const f32x4 (&aggd)[HEADS][4], float ne,
                                               const __bf16 *W2, const __bf16 *W3, const __bf16 *W4,
                                               const float *b2, const float *b3, const float *b4, uint32_t r16,
                                               uint32_t g, uint64_t qb) {
@@ -605,10 +614,16 @@ __device__ __forceinline__ void mlp_out_group(const RowParams &p, const Piece8<N
         piece_operand<NK>(ru[ks], p.n_dim, 32u * ks + 8u * g, nr >= 0, hi, lo);
         mfma4(acc3, W3, LS3, 32u * ks, r16, g, hi, lo, NK == kF32Vec);
     }
+    static_assert(HEADS == 1 || HEADS == 2, "one or two heads");
     f32x4 hq[4];
 #pragma unroll
     for (int ub = 0; ub < 4; ub++) hq[ub] = f32x4(0.0f);
-    chain64(hq, aggd, W2, PS, 0, r16, g);
+    if constexpr (HEADS == 1) {
+        chain64(hq, aggd[0], W2, PS, 0, r16, g);
+    } else {
+        chain64<0, 2>(hq, aggd[0], W2, PS, 0, r16, g);
+        chain64<2, 4>(hq, aggd[1], W2, PS, 0, r16, g);
+    }
 #pragma unroll
     for (int ub = 0; ub < 4; ub++)
 #pragma unroll
@@ -638,7 +653,7 @@ __device__ __forceinline__ void mlp_out_group(const RowParams &p, const Piece8<N
 // shape fixed at compile time every LDS address is a base plus an immediate
 // offset, all k-loops unroll and each segment's loads have one fixed form.
 // Queries are taken in groups of p.gq <= 16 (one MLP_out block each).
-template <int NKS, int EKS, int TKS, int NK, int EK>
+template <int NKS, int EKS, int TKS, int NK, int EK, int HEADS>
 __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void aggregate_rows(RowParams p) {
     constexpr int GS = NKS + EKS, K1S = GS + TKS, K3S = NKS + 2;
     using L = RowsLayout<K1S, K3S, TKS>;
@@ -648,7 +663,7 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     __bf16 *W2 = (__bf16 *)(smem + L::o_w2);
     __bf16 *W3 = (__bf16 *)(smem + L::o_w3);
     __bf16 *W4 = (__bf16 *)(smem + L::o_w4);
-    float *vec = (float *)(smem + L::o_vec);   // b1 | b2 | b3 | b4 | v, 64 each
+    float *vec = (float *)(smem + L::o_vec);   // b1 | b2 | b3 | b4 | v per head, 64 each
 
     // Stage the weights: w2, w4 and the aggregate columns of w3 in chained
     // order.
@@ -678,15 +693,18 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     // Layer 2 is affine, so the logit att . (w2 a1 + b2) of a row is
     // v . a1 up to a shift common to all rows (which the softmax cancels),
     // with v = w2^T att; and the aggregate sum_s alpha_s (w2 a1_s + b2) is
-    // w2 (sum_s alpha_s a1_s) + b2.  So layer 2 runs once per query.
-    for (uint32_t u = tid; u < 5u * kH; u += kRowThreads) {
+    // w2 (sum_s alpha_s a1_s) + b2.  So layer 2 runs once per query.  With
+    // heads, head a's logit vector is v_a = w2[slice a]^T att[slice a].
+    for (uint32_t u = tid; u < (4u + HEADS) * kH; u += kRowThreads) {
         const uint32_t k = u / kH, c = u % kH;
         float val;
         if (k < 4) {
             val = (k == 0 ? p.b1 : k == 1 ? p.b2 : k == 2 ? p.b3 : p.b4)[c];
         } else {
             val = 0.0f;
-            for (uint32_t r = 0; r < kH; r++) val = __builtin_fmaf(p.att[r], (float)p.w2[r * kH + c], val);
+            const uint32_t r0 = (k - 4u) * (kH / HEADS);
+            for (uint32_t r = r0; r < r0 + kH / HEADS; r++)
+                val = __builtin_fmaf(p.att[r], (float)p.w2[r * kH + c], val);
         }
         vec[u] = val;
     }
@@ -723,12 +741,13 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     u32x2 *rl = (u32x2 *)(smem + L::o_rl) + wave * 16u;
     const float *b1 = vec, *b2 = vec + kH, *b3 = vec + 2 * kH, *b4 = vec + 3 * kH, *va = vec + 4 * kH;
     // This lane's unit column of layer 1 (16 ub + r16): its bias and its
-    // weight in the logits.
-    float b1v[4], vav[4];
+    // weight in each head's logits.
+    float b1v[4], vav[HEADS][4];
 #pragma unroll
     for (int ub = 0; ub < 4; ub++) {
         b1v[ub] = b1[16 * ub + r16];
-        vav[ub] = va[16 * ub + r16];
+#pragma unroll
+        for (int a = 0; a < HEADS; a++) vav[a][ub] = va[a * kH + 16 * ub + r16];
     }
     const uint32_t gq = p.gq;
     const uint64_t groups = ((uint64_t)p.nq + gq - 1) / gq;
@@ -835,13 +854,19 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     // into aggd, the group's finished aggregates sum_s alpha_s a1_s: query
     // q's in the lanes with r16 == q, in the D layout (units 16 ub + 4 g + i),
     // with ne = 1 where the query had a valid row (else its aggregate is zero).
-    float m = -INFINITY, den = 0.0f, ne = 0.0f;
-    float agg[4];
-    f32x4 aggd[4];
+    // Each head keeps its own softmax state and aggregates.
+    float m[HEADS], den[HEADS], ne = 0.0f;
+    float agg[HEADS][4];
+    f32x4 aggd[HEADS][4];
 #pragma unroll
-    for (int ub = 0; ub < 4; ub++) {
-        agg[ub] = 0.0f;
-        aggd[ub] = f32x4(0.0f);
+    for (int a = 0; a < HEADS; a++) {
+        m[a] = -INFINITY;
+        den[a] = 0.0f;
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) {
+            agg[a][ub] = 0.0f;
+            aggd[a][ub] = f32x4(0.0f);
+        }
     }
     while (cg < groups) {
         // Keeps the LDS-resident biases from being hoisted into long-lived
@@ -969,15 +994,18 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         for (int ub = 0; ub < 4; ub++)
 #pragma unroll
             for (int i = 0; i < 4; i++) acc[ub][i] = relu(acc[ub][i]);
-        // The logits v . a1 of rows 4 g + i (up to the common shift att . b2):
-        // this lane's unit column's share, summed over the 16 lanes of its
-        // group.
+        const uint32_t nib = ((uint32_t)__builtin_amdgcn_ballot_w64(valid) >> (4u * g)) & 0xFu;
+#pragma unroll
+        for (int a = 0; a < HEADS; a++) {
+        // Head a's logits v_a . a1 of rows 4 g + i (up to the common shift
+        // att . b2): this lane's unit column's share, summed over the 16 lanes
+        // of its group.
         float lg[4];
 #pragma unroll
         for (int i = 0; i < 4; i++) {
-            float t = vav[0] * acc[0][i];
+            float t = vav[a][0] * acc[0][i];
 #pragma unroll
-            for (int ub = 1; ub < 4; ub++) t = __builtin_fmaf(vav[ub], acc[ub][i], t);
+            for (int ub = 1; ub < 4; ub++) t = __builtin_fmaf(vav[a][ub], acc[ub][i], t);
             lg[i] = xor16_sum(t);
         }
         // Online softmax over the group's valid rows: an invalid row's logit
@@ -985,24 +1013,24 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         // m = -inf, den = 0.  exp(x - mn) is the hardware 2^(x log2 e -
         // mn log2 e), one fused multiply-add: its rounding adds a relative
         // error of about |mn| 2^-24.
-        const uint32_t nib = ((uint32_t)__builtin_amdgcn_ballot_w64(valid) >> (4u * g)) & 0xFu;
 #pragma unroll
         for (int i = 0; i < 4; i++) lg[i] = ((nib >> i) & 1u) ? lg[i] : -INFINITY;
-        const float mn = max2(m, max2(max2(lg[0], lg[1]), max2(lg[2], lg[3])));
+        const float mn = max2(m[a], max2(max2(lg[0], lg[1]), max2(lg[2], lg[3])));
         const float shift = (mn == -INFINITY) ? 0.0f : mn * kLog2eAgg;
-        const float sc = __builtin_amdgcn_exp2f(__builtin_fmaf(m, kLog2eAgg, -shift));
+        const float sc = __builtin_amdgcn_exp2f(__builtin_fmaf(m[a], kLog2eAgg, -shift));
         float e[4];
 #pragma unroll
         for (int i = 0; i < 4; i++) e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(lg[i], kLog2eAgg, -shift));
-        den = __builtin_fmaf(den, sc, (e[0] + e[1]) + (e[2] + e[3]));
+        den[a] = __builtin_fmaf(den[a], sc, (e[0] + e[1]) + (e[2] + e[3]));
 #pragma unroll
         for (int ub = 0; ub < 4; ub++) {
-            float t = agg[ub] * sc;
+            float t = agg[a][ub] * sc;
 #pragma unroll
             for (int i = 0; i < 4; i++) t = __builtin_fmaf(e[i], acc[ub][i], t);
-            agg[ub] = t;
+            agg[a][ub] = t;
         }
-        m = mn;
+        m[a] = mn;
+        }
         }
         if (last_blk) {
             // The query's four lane groups combined: with M the largest group
@@ -1013,26 +1041,32 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
             // [l % 16] and D[4 (l / 16) + i][l % 16]: the product sums the
             // groups, normalises, and leaves query cq's aggregate in column cq
             // of the D layout.
-            const float M = groups_max(m);
-            const float shift = (M == -INFINITY) ? 0.0f : M * kLog2eAgg;
-            const float r = __builtin_amdgcn_exp2f(__builtin_fmaf(m, kLog2eAgg, -shift));
-            float ds = den * r;
-            ds = groups_sum(ds);
-            const float f = ds > 0.0f ? r * __builtin_amdgcn_rcpf(ds) : 0.0f;
-            const float bq = r16 == cq ? f : 0.0f;
 #pragma unroll
-            for (int ub = 0; ub < 4; ub++)
-                aggd[ub] = __builtin_amdgcn_mfma_f32_16x16x4f32(agg[ub], bq, aggd[ub], 0, 0, 0);
-            if (r16 == cq) ne = ds > 0.0f ? 1.0f : 0.0f;
-            m = -INFINITY;
-            den = 0.0f;
+            for (int a = 0; a < HEADS; a++) {
+                const float M = groups_max(m[a]);
+                const float shift = (M == -INFINITY) ? 0.0f : M * kLog2eAgg;
+                const float r = __builtin_amdgcn_exp2f(__builtin_fmaf(m[a], kLog2eAgg, -shift));
+                float ds = den[a] * r;
+                ds = groups_sum(ds);
+                const float f = ds > 0.0f ? r * __builtin_amdgcn_rcpf(ds) : 0.0f;
+                const float bq = r16 == cq ? f : 0.0f;
 #pragma unroll
-            for (int ub = 0; ub < 4; ub++) agg[ub] = 0.0f;
+                for (int ub = 0; ub < 4; ub++)
+                    aggd[a][ub] = __builtin_amdgcn_mfma_f32_16x16x4f32(agg[a][ub], bq, aggd[a][ub], 0, 0, 0);
+                if (a == 0 && r16 == cq) ne = ds > 0.0f ? 1.0f : 0.0f;
+                m[a] = -INFINITY;
+                den[a] = 0.0f;
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++) agg[a][ub] = 0.0f;
+            }
         }
         if (group_end) {
-            mlp_out_group<NKS, NK, L::ls3, kPs>(p, ru, nr, vq, aggd, ne, W2, W3, W4, b2, b3, b4, r16, g, cg * gq);
+            mlp_out_group<NKS, NK, L::ls3, kPs, HEADS>(p, ru, nr, vq, aggd, ne, W2, W3, W4, b2, b3, b4, r16, g,
+                                                       cg * gq);
 #pragma unroll
-            for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
+            for (int a = 0; a < HEADS; a++)
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++) aggd[a][ub] = f32x4(0.0f);
             ne = 0.0f;
             cg += gstep;
             cq = 0;
@@ -1319,7 +1353,8 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     // sum over its merged partials of exp(m - M) times the partial's
     // exponential-weighted sums, and the lanes with r16 == q hold M_q (mrun)
     // and the matching sum of exponentials (drun).
-    f32x4 aggd[4];
+    f32x4 aggdh[1][4];
+    f32x4 (&aggd)[4] = aggdh[0];
 #pragma unroll
     for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
     float mrun = -INFINITY, drun = 0.0f;
@@ -1515,7 +1550,8 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         for (int ub = 0; ub < 4; ub++)
 #pragma unroll
             for (int i = 0; i < 4; i++) aggd[ub][i] *= inv;
-        mlp_out_group<NKS, NK, L::ls3, L::ps>(p, ru, nr, vq, aggd, ne, W2, W3, W4, b2, b3, b4, r16, g, cg * gq);
+        mlp_out_group<NKS, NK, L::ls3, L::ps, 1>(p, ru, nr, vq, aggdh, ne, W2, W3, W4, b2, b3, b4, r16, g,
+                                                 cg * gq);
 #pragma unroll
         for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
         mrun = -INFINITY;
@@ -1531,7 +1567,7 @@ uint32_t agg_layout(AggParams &p, uint32_t rows, uint32_t qrows) {
     p.region_off = align16(16u * rows + 4u * qrows);
     const uint32_t x_bytes = 2u * rows * p.xs * 2u;
     p.off_h = rows * kHs * 2u * 2u;
-    p.off_y = align16(p.off_h + rows * kHf * 4u + rows * 4u);
+    p.off_y = align16(p.off_h + rows * kHf * 4u + rows * 4u * p.heads);
     p.off_a3 = align16(p.off_y + 2u * qrows * p.ys * 2u);
     const uint32_t late = p.off_a3 + 2u * qrows * kHs * 2u;
     return p.region_off + (x_bytes > late ? x_bytes : late);
@@ -1545,6 +1581,8 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
     if (nq == 0) return NLB_OK;
     if (!node || !tq || !z) return NLB_EINVAL;
     if (wts->hidden != kH) return NLB_EINVAL;
+    const uint32_t heads = wts->heads <= 1 ? 1u : (uint32_t)wts->heads;
+    if (heads != 1 && heads != 2 && heads != 4 && heads != 8) return NLB_EINVAL;
     if (!wts->w1 || !wts->w2 || !wts->w3 || !wts->w4 || !wts->b1 || !wts->b2 || !wts->b3 ||
         !wts->b4 || !wts->att)
         return NLB_EINVAL;
@@ -1603,6 +1641,7 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
     p.att = wts->att;
     p.z = z;
     p.status = h->status;
+    p.heads = heads;
 
     // The wavefront-per-query kernel, for the input shapes it is instantiated
     // for (those of the synthetic workloads) when its weights fit one
@@ -1657,9 +1696,12 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
         // Tables of at most 16 slots take the packed form when the groups
         // are large enough for packing to fill blocks (small launches are
         // bound by their per-group steps).
-        const bool packed = h->s <= kPackMaxS && r.gq >= kPackMinGroup;
+        const bool packed = h->s <= kPackMaxS && r.gq >= kPackMinGroup && heads == 1;
+        // One or two heads: the per-query kernel; more heads take the tiled kernel.
+        const bool rows_ok = heads <= 2;
 #define NLB_ROWS_SHAPE(A, B, C, NK, EK)                                                              \
-    if (!kern && nks == A && eks == B && tks == C && (A == 0 || nkind == NK) && (B == 0 || ekind == EK)) { \
+    if (!kern && rows_ok && nks == A && eks == B && tks == C && (A == 0 || nkind == NK) &&          \
+        (B == 0 || ekind == EK)) {                                                                    \
         if (packed) {                                                                                 \
             kern = (const void *)aggregate_packed<A, B, C, NK, EK>;                                   \
             bytes = PackedLayout<A + B + C, A + 2, C>::bytes;                                         \
@@ -1667,11 +1709,18 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
                 hipLaunchKernelGGL((aggregate_packed<A, B, C, NK, EK>), gr, dim3(kRowThreads), l, st, rp); \
             };                                                                                        \
         } else {                                                                                      \
-            kern = (const void *)aggregate_rows<A, B, C, NK, EK>;                                     \
             bytes = RowsLayout<A + B + C, A + 2, C>::bytes;                                           \
-            launch = [](dim3 gr, uint32_t l, hipStream_t st, const RowParams &rp) {                   \
-                hipLaunchKernelGGL((aggregate_rows<A, B, C, NK, EK>), gr, dim3(kRowThreads), l, st, rp); \
-            };                                                                                        \
+            if (heads == 1) {                                                                         \
+                kern = (const void *)aggregate_rows<A, B, C, NK, EK, 1>;                              \
+                launch = [](dim3 gr, uint32_t l, hipStream_t st, const RowParams &rp) {               \
+                    hipLaunchKernelGGL((aggregate_rows<A, B, C, NK, EK, 1>), gr, dim3(kRowThreads), l, st, rp); \
+                };                                                                                    \
+            } else {                                                                                  \
+                kern = (const void *)aggregate_rows<A, B, C, NK, EK, 2>;                              \
+                launch = [](dim3 gr, uint32_t l, hipStream_t st, const RowParams &rp) {               \
+                    hipLaunchKernelGGL((aggregate_rows<A, B, C, NK, EK, 2>), gr, dim3(kRowThreads), l, st, rp); \
+                };                                                                                    \
+            }                                                                                         \
         }                                                                                             \
     }
         // 100 time dims with: bf16 node rows 128 wide and bf16 link rows 128

@@ -529,3 +529,47 @@ def test_aggregate_large_launch_matches_oracle(k):
     print(f"aggregate large launch, workload {k}: max scaled error {err:.3e}")
     assert g.status() == 0
     assert err <= AGG_TOL
+
+
+@pytest.mark.parametrize("k,heads,shape", [(1, 2, None), (2, 2, None), (3, 2, None), (4, 2, None), (5, 2, None),
+                                           (5, 4, None), (3, 8, None), (1, 2, "f32node36-bf16edge90-t50"),
+                                           (1, 4, "bf16node200")])
+def test_aggregate_heads_match_oracle(k, heads, shape):
+    """Eq. (4) with several attention heads (App. E uses two), each over its
+    own slice of the hidden width: two heads in the per-query kernel on
+    every workload shape, four and eight in the tiled kernel, and the tiled
+    shapes with two and four heads; launches of 3 000 and 70 001 queries,
+    sampled queries against the fp64 oracle with the same heads."""
+    import dataclasses
+    base = synth.workload(k)
+    w = synth.scaled(base, 12 * base.batch, num_nodes=min(base.num_nodes, 200000))
+    if shape is not None:
+        w = dataclasses.replace(w, **TILED_SHAPES[shape])
+    src, dst, t, _ = synth.host_links(w)
+    ef = synth.host_features(w, "edge") if w.edge_dim else None
+    nf = synth.host_features(w, "node") if w.node_dim else None
+    g = make_gpu_table(w, feat_to_dev(ef, w.edge_dtype) if ef is not None else None,
+                       feat_to_dev(nf, w.node_dtype) if nf is not None else None)
+    o = make_oracle(w)
+    g.insert(to_dev(src), to_dev(dst), to_dev(t))
+    o.insert(src, dst, t)
+    W = synth.agg_weights(w)
+    fw, fb = synth.time_params(w)
+    rng = np.random.default_rng(40 + 3 * k + heads)
+    ends = np.concatenate([src, dst])
+    worst = 0.0
+    for nq in (3000, 70001):
+        q = ends[rng.integers(0, len(ends), nq)].astype(np.int32)
+        tq = rng.integers(0, int(t[-1]) + 2, nq).astype(np.uint32)
+        tq[::9] = 0
+        gz = g.aggregate(to_dev(q), to_dev(tq), _agg_dev(W), heads=heads).cpu().numpy()
+        pos = np.sort(rng.choice(nq, 800, replace=False))
+        oz = o.aggregate(q[pos], tq[pos], fw, fb, ef, nf, W, heads=heads)
+        worst = max(worst, agg_error(gz[pos], oz))
+        if heads > 1:   # the heads change the result
+            oz1 = o.aggregate(q[pos[:50]], tq[pos[:50]], fw, fb, ef, nf, W, heads=1)
+            assert agg_error(gz[pos[:50]], oz1) > 10 * AGG_TOL
+    print(f"aggregate, workload {k} shapes{'' if shape is None else ' ' + shape}, {heads} heads: "
+          f"max scaled error {worst:.3e}")
+    assert g.status() == 0
+    assert worst <= AGG_TOL
