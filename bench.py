@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--aggregate", action="store_true",
                     help="retrieve with the fused eq. (4) attention aggregation (nlb_aggregate, "
                          "random weights) instead of nlb_sample, and report that kernel")
+    ap.add_argument("--heads", type=int, default=1,
+                    help="attention heads of --aggregate (App. E uses two)")
     ap.add_argument("--rnn", action="store_true",
                     help="also update the node statuses after every batch (Sec. 4.4 GRU, "
                          "nlb_rnn_update, random weights): the node-feature rows when the workload "
@@ -120,13 +122,16 @@ def measured_traffic(w, call="nlb_sample"):
     return float(m.group(3))
 
 
-def aggregate_kernel(w, queries, cus):
+def aggregate_kernel(w, queries, cus, heads=1):
     """The eq. (4) kernel a launch of `queries` takes on this workload's
-    shapes (the library's own choice, restated for the record): the packed
-    form for tables of at most 16 slots when its query groups hold at least
-    8 queries, else the per-query form."""
+    shapes (the library's own choice, restated for the record): with one
+    head, the packed form for tables of at most 16 slots when its query
+    groups hold at least 8 queries, else the per-query form, which also takes
+    two heads; more heads take the tiled form."""
+    if heads > 2:
+        return "aggregate_fused"
     gq = min(16, max(1, -(-queries // (cus * 8))))
-    return "aggregate_packed" if w.s <= 16 and gq >= 8 else "aggregate_rows"
+    return "aggregate_packed" if heads == 1 and w.s <= 16 and gq >= 8 else "aggregate_rows"
 
 
 def hop2_bytes(w, hop1_valid, queries):
@@ -140,15 +145,16 @@ def hop2_bytes(w, hop1_valid, queries):
 PEAK_BF16_TFLOPS = 2500.0
 
 
-def aggregate_flops(w, valid_slots, queries, hidden=64):
+def aggregate_flops(w, valid_slots, queries, hidden=64, heads=1):
     """Algorithmic matrix FLOPs of eq. (4) as computed (no padding, one
-    product per weight): MLP_in's first layer and the attention logit for
-    every valid slot; MLP_in's second layer, which is affine, once on each
-    query's softmax-weighted sum, and MLP_out's two layers, for every query.
-    (Applying the second layer to every slot, in the order the equation is
-    written, would add 2 H^2 per valid slot.)"""
+    product per weight): MLP_in's first layer and each head's attention
+    logit for every valid slot; MLP_in's second layer, which is affine, once
+    on each query's softmax-weighted sums (each head's slice of its outputs),
+    and MLP_out's two layers, for every query.  (Applying the second layer to
+    every slot, in the order the equation is written, would add 2 H^2 per
+    valid slot.)"""
     d_in = w.node_dim + w.edge_dim + w.d_time
-    per_slot = 2 * (d_in * hidden + hidden)
+    per_slot = 2 * (d_in * hidden + heads * hidden)
     per_query = 2 * (hidden * hidden + (w.node_dim + hidden) * hidden + hidden * hidden)
     return valid_slots * per_slot + queries * per_query
 
@@ -269,7 +275,7 @@ def _stream_batches(w, b0, b1):
             yield b, src[a - lo:z - lo], dst[a - lo:z - lo], t[a - lo:z - lo], neg[a - lo:z - lo]
 
 
-def cpu_baseline(w, first, budget_s, agg_weights=None, hop2=False):
+def cpu_baseline(w, first, budget_s, agg_weights=None, hop2=False, heads=1):
     """The CPU oracle, one thread, on the GPU machine's host.  Insertion is
     timed over every link of batches 0 .. first-1 (the replay that brings the
     oracle to the GPU's timed window); then, from batch `first` on, each
@@ -302,7 +308,7 @@ def cpu_baseline(w, first, budget_s, agg_weights=None, hop2=False):
         rows.need(o, q)
         t0 = time.perf_counter()
         if agg_weights is not None:
-            o.aggregate(q, tq, fw, fb, rows.ef, rows.nf, agg_weights)
+            o.aggregate(q, tq, fw, fb, rows.ef, rows.nf, agg_weights, heads=heads)
         else:
             r1 = o.sample(q, tq, fw, fb, rows.ef, rows.nf)
             if hop2:
@@ -653,7 +659,7 @@ def main():
         s_, d_, t_, q, tq = synth.batch_views(w, nodes, ts, b)
         n = q.numel()
         if agg_w is not None:
-            table.aggregate(q, tq, agg_w, out=agg_z[:n])
+            table.aggregate(q, tq, agg_w, out=agg_z[:n], heads=args.heads)
             return s_, d_, t_, n
         o = {k: v[:n] for k, v in out.items()}
         o["nbr"] = nbr_out[:n]
@@ -772,11 +778,11 @@ def main():
         "setup_s": setup_s,
     }
     if agg_w is not None:
-        fl = aggregate_flops(w, valid, queries)
+        fl = aggregate_flops(w, valid, queries, heads=args.heads)
         ab = aggregate_bytes(w, valid, queries)
         t_s = sample_ms.sum() * 1e-3
         cus = torch.cuda.get_device_properties(0).multi_processor_count
-        kname = aggregate_kernel(w, 3 * w.batch, cus)
+        kname = aggregate_kernel(w, 3 * w.batch, cus, args.heads)
         agg_traffic = measured_traffic(w, "nlb_aggregate") if kname == "aggregate_packed" else None
         res["roofline"] = dict(binding_roofline(fl, ab, t_s), traffic=agg_traffic,
                                traffic_unit="bytes per nlb_aggregate launch (rocprofv3 FETCH_SIZE "
@@ -787,6 +793,7 @@ def main():
         res["aggregate_kernel_queries_per_s"] = res.pop("sample_kernel_queries_per_s")
         res["value_note"] = "steps retrieve with nlb_aggregate (eq. (4), random weights)"
         res["dtype"] = "bf16-mfma+f32"
+        res["config"]["heads"] = args.heads
     if hop2_out is not None:
         n_last = qcount[-1] * w.s
         last_valid = int((hop2_out["nbr"][:n_last] >= 0).sum())   # last step, after timing
@@ -833,7 +840,8 @@ def main():
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(
             w, start + W, args.cpu_seconds,
-            agg_weights=synth.agg_weights(w) if agg_w is not None else None, hop2=hop2_out is not None)
+            agg_weights=synth.agg_weights(w) if agg_w is not None else None, hop2=hop2_out is not None,
+            heads=args.heads)
         if status is not None:
             print("bench: timing the CPU oracle's status update", file=sys.stderr, flush=True)
             res["rnn"]["cpu_baseline"] = cpu_rnn_baseline(w, start + W, args.cpu_seconds)
