@@ -141,3 +141,46 @@ def test_whole_step_replays_against_the_oracle(k):
     assert g.info()["interactions"] == w.links       # the device count, refreshed by nlb_status
     compare_tables(g, o)
     g.close()
+
+
+def test_packed_aggregation_replays_in_a_hip_graph():
+    """The packed eq. (4) kernel (groups of at least 8 queries, s = 10) in a
+    HIP graph: 30 000 queries captured once and replayed three times with
+    eager work on the output between replays; every replay equals the eager
+    result bit for bit, which matches the oracle on sampled queries."""
+    import torch
+    import paper_2402_01964_amd as nlb
+    from tests.test_gpu_parity import AGG_TOL, agg_error
+    base = synth.workload(5)
+    w = synth.scaled(base, 4 * base.batch, num_nodes=200000)
+    src, dst, t, neg = synth.host_links(w)
+    nf = synth.host_features(w, "node")
+    g = make_gpu_table(w, None, feat_to_dev(nf, w.node_dtype))
+    o = make_oracle(w)
+    lo, hi = w.batch_range(3)
+    g.insert(to_dev(src[:lo]), to_dev(dst[:lo]), to_dev(t[:lo]))
+    o.insert(src[:lo], dst[:lo], t[:lo])
+    qh = np.concatenate([src[lo:hi], dst[lo:hi], neg[lo:hi]])[:30000]
+    tqh = np.concatenate([t[lo:hi]] * 3)[:30000]
+    q, tq = to_dev(qh), to_dev(tqh)
+    W = synth.agg_weights(w)
+    Wd = _agg_dev(W)
+    z = torch.empty((len(qh), nlb.AGG_HIDDEN), dtype=torch.float32, device="cuda")
+    g.aggregate(q, tq, Wd, out=z)
+    torch.cuda.synchronize()
+    ref = z.clone()
+    fw, fb = synth.time_params(w)
+    pos = np.sort(np.random.default_rng(5).choice(len(qh), 600, replace=False))
+    assert agg_error(ref.cpu().numpy()[pos], o.aggregate(qh[pos], tqh[pos], fw, fb, None, nf, W)) <= AGG_TOL
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        g.aggregate(q, tq, Wd, out=z)
+    for rep in range(3):
+        z.fill_(7.0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(z, ref), f"replay {rep}"
+    del graph
+    assert g.status() == nlb.NLB_OK
+    g.close()
