@@ -233,7 +233,6 @@ struct GruParams {
     int32_t s_kind, e_kind;             // piece forms of status / link rows (-1: none applies)
     uint32_t meta;                      // LDS bytes before X: row list, then T-enc w | b (pad32(d_time) each)
     uint32_t ws_lomask;                 // weight-stationary form: bit s set if X k-step s has a lo plane
-    uint64_t ws_cpr_m;                  // nlb_div_magic(srb / 16)
     const __bf16 *w_ih, *w_hh;
     const float *b_ih, *b_hh;
 };
@@ -661,7 +660,7 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
 // k-step: 12 registers per k-step) for the whole launch, and the workgroup
 // loops over the 32-row tiles blockIdx.x, blockIdx.x + gridDim.x, ...
 //
-// A tile sits in LDS in matrix-operand order: the A operand of k-step s and
+// A tile sits in LDS in matrix-operand order: the operand of k-step s and
 // row block rb is 1 KB, lane l's eight values at 16 l, so that every operand
 // read is one contiguous 16-byte read per lane at a fixed offset.  Each
 // tile buffer is two LDS arrays (so that the compiler can tell a write of
@@ -669,22 +668,32 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
 // fill (H hi, X hi of the r_other steps), T the rest (X hi of the
 // time-encoding and link-row steps, X lo by step, H lo for fp32 statuses;
 // lo planes only at steps inside [lo_begin, lo_end)).  Tiles alternate
-// between two buffers: the status rows of the next tile are requested
-// before the products of the current one and land in its S array meanwhile
-// -- bf16 rows whose width is a multiple of 32 by direct global-to-LDS
-// loads (one operand fragment per wavefront and load), other rows through
-// registers, written after the products (fp32 ones as hi + lo).
+// between two buffers: the status rows of the next tile are requested at
+// the start of the current one and land in its S array meanwhile -- bf16
+// rows whose width is a multiple of 32 by direct global-to-LDS loads (one
+// operand fragment per load), other rows through registers, written before
+// the tile's barrier (fp32 ones as hi + lo).
 //
-// The two wavefronts that share a SIMD (w and w + KH) work in opposite
-// order, so that one's vector work overlaps the other's products: the
-// second half computes the next tile's time encoding before its products
-// (from link times it read one tile ahead), the first half goes straight to
-// its products; both then apply the gates.  The new statuses of a tile go
-// to an LDS staging area and, after the tile's barrier, to the candidate
-// rows in whole 16-byte pieces, so that their stores complete under the
-// next tile's products.  List entries are read two tiles ahead into one of
-// eight row-list slots.  Rows of a tile past the list's end repeat its last
-// entry and are never written out.
+// The products are taken as W X^T (the weight fragment is the first
+// operand), so that a lane's four accumulator values are four consecutive
+// output units of one tile row: the accumulators start from the gate
+// biases, the gates read the units' h values with one 8-byte LDS read (a
+// 16-byte global read for fp32 statuses), and the new statuses go straight
+// from registers to the candidate rows, 8 or 16 bytes per lane, with no
+// exchange between wavefronts.
+//
+// The two wavefronts that share a SIMD (w and w + KH) alternate between
+// matrix and vector work, which the SIMD runs side by side.  After a tile's
+// barrier the first half starts on that tile's products at once, while the
+// second half issues the loads of the tiles ahead, applies the gates of the
+// previous tile (its accumulators and h values kept in registers across the
+// barrier) and encodes its share of the next tile's time columns; then the
+// second half takes its products while the first half applies its gates and
+// encodes its share.  Row
+// lists are read three tiles ahead into one of eight row-list slots, the
+// link times of a tile's rows two tiles ahead into one of four LDS rows.
+// Rows of a tile past the list's end repeat its last entry and are never
+// written out.
 constexpr int kWsSteps = 12;
 constexpr uint32_t kWsRows = 32;
 constexpr int kWsBf16Dma = 0, kWsBf16 = 1, kWsF32 = 2;   // how status rows reach the LDS
@@ -698,11 +707,9 @@ struct WsLayout {
     // T: X hi steps [KH, KXM), X lo steps [0, KXM), H lo
     static constexpr uint32_t tx = 0, tl = (KXM - KH) * NB * frag, th = tl + KXM * NB * frag,
                               t_bytes = th + KH * NB * frag;
-    // output rows of a tile, row-major with a stride of the row plus 16
-    // bytes against bank conflicts (at most fp32, kd = 32 KH)
-    static constexpr uint32_t ostage = kWsRows * (32 * KH * 4 + 16);
-    static constexpr uint32_t slots = 8;
-    static constexpr uint32_t fixed = 2 * (s_bytes + t_bytes) + 2 * ostage + slots * 1024 + 4 * 32 * KH * 4;
+    static constexpr uint32_t slots = 8, tslots = 4;
+    // tile buffers, row-list slots, link-time rows, gate biases
+    static constexpr uint32_t fixed = 2 * (s_bytes + t_bytes) + slots * 1024 + tslots * 256 + 4 * 32 * KH * 4;
 };
 
 // Byte offset of the eight values at row j, columns c .. c + 7 (c % 8 == 0)
@@ -733,12 +740,45 @@ __device__ __forceinline__ void lds_load16(const void *g, uint32_t lds) {
                  :: "v"(g), "{m0}"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
 }
 
+// The same with 4 bytes per lane (lane l's word at lds + 4 l).
+__device__ __forceinline__ void lds_load4(const void *g, uint32_t lds) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dword %0, off"
+                 :: "v"(g), "{m0}"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void *p) { return (uint32_t)(uintptr_t)(lds_ptr)p; }
 
-template <int KH, int MODE>
+// Candidate-row stores, written as assembly: the compiler would otherwise
+// make the next write of their source registers wait until the stores have
+// completed (vmcnt), which stalls the loop for a memory round trip; the
+// hardware has read the sources one wait state after issue (the nop).
+__device__ __forceinline__ void store_b64_async(void *g, u32x2 v) {
+    asm volatile("global_store_dwordx2 %0, %1, off\n\ts_nop 1" :: "v"(g), "v"(v) : "memory");
+}
+__device__ __forceinline__ void store_b128_async(void *g, u32x4 v) {
+    asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 1" :: "v"(g), "v"(v) : "memory");
+}
+
+// Workgroup barriers of the tile loop.  The first half has no direct loads
+// in flight and nothing in global memory that another wavefront reads, so it
+// waits for its LDS accesses only (its candidate-row stores complete in the
+// background); the second half also waits for its direct loads (vmcnt), which
+// the compiler does not count.
+__device__ __forceinline__ void barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+__device__ __forceinline__ void barrier_loads() {
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// FULL: every X step is in use and exactly the steps KH .. KXM - 1 have a lo
+// plane (kx = 32 KXM; the time encoding, and fp32 link rows if any, fill the
+// steps after the status): the products then run without branches.
+template <int KH>
+constexpr uint32_t ws_full_lomask() { return ((1u << (kWsSteps - KH)) - 1u) & ~((1u << KH) - 1u); }
+
+template <int KH, int MODE, bool FULL>
 __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     using L = WsLayout<KH>;
-    constexpr uint32_t NB = L::NB, R = kWsRows, T = 128 * KH, GH = 4 * KH, FB = L::frag;
+    constexpr uint32_t NB = L::NB, R = kWsRows, T = 128 * KH, TH = T / 2, GH = 4 * KH, FB = L::frag;
     constexpr int KXM = (int)L::KXM, KS = KXM + KH;
     constexpr int SK = MODE == kWsF32 ? kF32Vec : kBf16Vec;
     static_assert(R * GH == T, "one status piece of each input half per thread");
@@ -747,13 +787,15 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     __shared__ __attribute__((aligned(16))) uint8_t bs1[L::s_bytes];
     __shared__ __attribute__((aligned(16))) uint8_t bt0[L::t_bytes];
     __shared__ __attribute__((aligned(16))) uint8_t bt1[L::t_bytes];
-    constexpr uint32_t OSTR = 32 * KH * (MODE == kWsF32 ? 4 : 2) + 16;   // staging row stride
-    __shared__ __attribute__((aligned(16))) uint8_t ost0[R * OSTR];
-    __shared__ __attribute__((aligned(16))) uint8_t ost1[R * OSTR];
     // Row lists {pair row, self, other, 0} of 1 KB slots (R entries and room
-    // for the duplicates a direct load of R entries writes); tile i in slot i % 8.
+    // for the duplicates a direct load of R entries writes); tile i in slot
+    // i % 8.  Link times of the rows of tile i in row i % 4 of tt (words
+    // R .. 63 of a row: room for the duplicates a direct load writes).
     constexpr uint32_t MS = 64;
     __shared__ __attribute__((aligned(16))) u32x4 meta[L::slots * MS];
+    __shared__ __attribute__((aligned(16))) uint32_t tt[L::tslots][64];
+    // gate biases by output unit: b_ir + b_hr, b_iz + b_hz, b_in, b_hn
+    __shared__ __attribute__((aligned(16))) float sbias[4][32 * KH];
     extern __shared__ __attribute__((aligned(16))) float s_tw[];   // T-enc w | b, pad32(d_time) each
     float *s_tb = s_tw + ((p.d_time + 31u) & ~31u);
 
@@ -768,39 +810,52 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     const uint32_t d = p.d, kx_steps = p.kx / 32;
     const bool mma = wave < (d + 15) / 16;
     const uint32_t j = 16 * wave + lr, jr = j < d ? j : d - 1;
+    // Accumulator value q of row block rb of this lane: output unit u0 + q,
+    // tile row 16 rb + lr.
+    const uint32_t u0 = 16 * wave + 4 * (lane >> 4);
     const uint32_t gt = (p.off_e - p.kd) / 8, tu = R * gt;
 
     // This wavefront's weight fragments (loaded in the prologue, after the
-    // first tile's requests) and the gate biases by output unit (LDS, read
-    // per tile).
+    // first tile's requests): lane l holds unit 16 w + l % 16, columns
+    // 32 s + 8 (l / 16) .. + 7 of step s.
     bf16x8 bx[KXM][3], bh[KH][3];
-    __shared__ float sbias[4][32 * KH];
 
     auto list_at = [&](uint32_t tl, uint32_t row) __attribute__((always_inline)) {
         return min((uint64_t)tl * R + row, (uint64_t)count - 1);
     };
 
-    // Register path: a thread's status pieces, f = 0 of H (self) and f = 1
-    // of X's r_other, both at tile row pj, columns pc0 .. pc0 + 7.  Direct
-    // path: wavefront w's operand fragment w of H and of X's r_other, lane l
-    // at tile row dj, column dc.
+    // Direct path: operand fragment f (< 2 KH) of H and of X's r_other for
+    // the tile in row-list slot `slot`, lane l from tile row 16 (f % NB) +
+    // l % 16, columns 32 (f / NB) + 8 (l / 16) .. + 7.  Register path: a
+    // thread's status pieces, f = 0 of H (self) and f = 1 of X's r_other,
+    // both at tile row pj, columns pc0 .. pc0 + 7, written to LDS later.
+    auto request_frag = [&](uint8_t *nbS, uint32_t slot, uint32_t f) __attribute__((always_inline)) {
+        const uint32_t dj = 16 * (f % NB) + lr, dc = 32 * (f / NB) + lk;
+        const u32x4 e = meta[slot * MS + dj];
+        lds_load16(p.st + (size_t)e[1] * p.srb + 2u * dc, lds_addr(nbS + L::sh + f * FB));
+        lds_load16(p.st + (size_t)e[2] * p.srb + 2u * dc, lds_addr(nbS + L::sx + f * FB));
+    };
     const uint32_t pj = tid / GH, pc0 = 8 * (tid % GH);
-    const uint32_t dj = 16 * (wave % NB) + lr, dc = 32 * (wave / NB) + lk;
     Piece8<SK> pc[2];
-    auto request_tile = [&](uint8_t *nbS, uint32_t slot) __attribute__((always_inline)) {
-        if constexpr (MODE == kWsBf16Dma) {
-            const u32x4 e = meta[slot * MS + dj];
-            lds_load16(p.st + (size_t)e[1] * p.srb + 2u * dc, lds_addr(nbS + L::sh + wave * FB));
-            lds_load16(p.st + (size_t)e[2] * p.srb + 2u * dc, lds_addr(nbS + L::sx + wave * FB));
-        } else {
-            const u32x4 e = meta[slot * MS + pj];
-            load_piece<SK>(p.st + (size_t)e[1] * p.srb, d, pc0, pc[0]);
-            load_piece<SK>(p.st + (size_t)e[2] * p.srb, d, pc0, pc[1]);
+    auto request_pieces = [&](uint32_t slot) __attribute__((always_inline)) {
+        const u32x4 e = meta[slot * MS + pj];
+        load_piece<SK>(p.st + (size_t)e[1] * p.srb, d, pc0, pc[0]);
+        load_piece<SK>(p.st + (size_t)e[2] * p.srb, d, pc0, pc[1]);
+    };
+    auto write_pieces = [&](uint8_t *nbS, uint8_t *nbT) __attribute__((always_inline)) {
+        const uint32_t po = frag_off(pj, pc0);
+        if constexpr (MODE == kWsF32) {
+            float v[8];
+            piece_floats<SK>(pc[0], d, pc0, true, v);
+            store_split8(v, (__bf16 *)(nbS + L::sh + po), (__bf16 *)(nbT + L::th + po));
+            piece_floats<SK>(pc[1], d, pc0, true, v);
+            store_split8(v, (__bf16 *)(nbS + L::sx + po), (__bf16 *)(nbT + L::tl + po));   // lo_begin == 0
+        } else if constexpr (MODE == kWsBf16) {
+            *(u32x4 *)(nbS + L::sh + po) = piece_bf16_bits<SK>(pc[0], d, pc0, true);
+            *(u32x4 *)(nbS + L::sx + po) = piece_bf16_bits<SK>(pc[1], d, pc0, true);
         }
     };
 
-    // Time-encoding unit u of a tile: row u / gt, encoding columns k .. k + 7
-    // (X columns kd + k ..), from the row's link time tf.
     // Time-encoding unit u of a tile: lane l = u % 64 of operand fragment
     // f = u / 64 of the encoding's steps (step f / NB, row block f % NB), i.e.
     // tile row 16 (f % NB) + l % 16 and encoding columns 32 (f / NB) +
@@ -842,38 +897,17 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
             *(u32x2 *)(nbT + L::tl + KH * NB * FB + 16u * u + 8u * h) = lo;
         }
     };
-    // A thread's time-encoding unit u = tid of every tile (if u < tu), with
-    // the link time of its row for the tile whose encoding it computes next.
-    uint32_t tB = 0;
-    auto t_row = [&](uint32_t tl, uint32_t u) __attribute__((always_inline)) {
-        return ((const uint32_t *)p.list)[4 * list_at(tl, unit_row(min(u, tu - 1u)))];
-    };
 
-    // What is written after the products: status pieces on the register
-    // path, time-encoding units the second half does not cover (u >= T) and
-    // link rows.
-    auto write_tile = [&](uint8_t *nbS, uint8_t *nbT, uint32_t slot) __attribute__((always_inline)) {
-        const uint32_t po = frag_off(pj, pc0);
-        if constexpr (MODE == kWsF32) {
-            float v[8];
-            piece_floats<SK>(pc[0], d, pc0, true, v);
-            store_split8(v, (__bf16 *)(nbS + L::sh + po), (__bf16 *)(nbT + L::th + po));
-            piece_floats<SK>(pc[1], d, pc0, true, v);
-            store_split8(v, (__bf16 *)(nbS + L::sx + po), (__bf16 *)(nbT + L::tl + po));   // lo_begin == 0
-        } else if constexpr (MODE == kWsBf16) {
-            *(u32x4 *)(nbS + L::sh + po) = piece_bf16_bits<SK>(pc[0], d, pc0, true);
-            *(u32x4 *)(nbS + L::sx + po) = piece_bf16_bits<SK>(pc[1], d, pc0, true);
-        }
-        for (uint32_t u = tid + T; u < tu; u += T)
-            tenc_unit(nbT, u, (float)p.t[meta[slot * MS + unit_row(u)][0] >> 1]);
-        if (p.kx > p.off_e) {
+    // The link rows of a tile (first half only).
+    auto write_edges = [&](uint8_t *nbT, uint32_t slot) __attribute__((always_inline)) {
+        if (!second && p.kx > p.off_e) {
             const uint32_t ge = (p.kx - p.off_e) / 8;
             auto edge_fill = [&](auto kind) __attribute__((always_inline)) {
                 constexpr int K = decltype(kind)::value;
                 auto eid_of = [&](uint32_t jj) __attribute__((always_inline)) {
                     return first_eid + (meta[slot * MS + jj][0] >> 1);
                 };
-                fill_seg<K, 4, T>(
+                fill_seg<K, 4, TH>(
                     R * ge, ge, p.ge_m, p.e_dim,
                     [&](uint32_t jj) __attribute__((always_inline)) {
                         const uint64_t e = eid_of(jj);
@@ -898,43 +932,34 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
                 edge_fill(std::integral_constant<int, kBf16Word>{});
             else
                 edge_fill(std::integral_constant<int, kBf16Vec>{});
+            // The fill's last loads may go unused; waiting for them here keeps
+            // the compiler from waiting for them (and for every store issued
+            // since) at the next write of their registers.
+            __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
         }
-    };
-    // Direct loads into LDS count as outstanding vector-memory operations:
-    // all of this wavefront's must have landed before the workgroup barrier
-    // (the compiler does not know of them).
-    auto tile_barrier = [&]() __attribute__((always_inline)) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), seen by the compiler's own wait tracking
-        __syncthreads();
     };
 
     // Prologue, ordered so that the weights' transfer (about 300 KB per CU,
     // from L2) overlaps the first tile's dependent loads: time-encoding
-    // parameters, row lists of the first two tiles and the list rows of the
-    // second tile's encoding units; then the first tile's status rows and
-    // the link times of both tiles' encoding units; then the weights and
-    // biases; then the first tile's encoding and barrier.
+    // parameters and the row lists of the first three tiles; then the link
+    // times of the first two tiles' rows and the first tile's status rows;
+    // then the weights and biases; then the first tile's inputs and barrier.
     for (uint32_t u = tid; u < ((p.d_time + 31u) & ~31u); u += T) {
         s_tw[u] = u < p.d_time ? p.tw[u] : 0.0f;
         s_tb[u] = u < p.d_time ? p.tb[u] : 0.0f;
     }
     const uint32_t stride = gridDim.x;
     uint32_t tl = blockIdx.x;
-    {
-        const uint32_t t1 = tl + stride < tiles ? tl + stride : tl;
-        const u32x4 e0 = p.list[list_at(tl, tid & (R - 1))], e1 = p.list[list_at(t1, tid & (R - 1))];
-        const uint32_t r1 = t_row(t1, tid);
-        if (tid < R) {
-            meta[tid] = e0;
-            meta[MS + tid] = e1;
-        }
-        tB = r1;
+    if (tid < 3 * R) {
+        const uint32_t k = tid / R, tk = tl + k * stride < tiles ? tl + k * stride : tl;
+        meta[k * MS + tid % R] = p.list[list_at(tk, tid % R)];
     }
     __syncthreads();
-    request_tile(bs0, 0);
-    const uint32_t t_first = p.t[meta[unit_row(min(tid, tu - 1u))][0] >> 1];
-    tB = p.t[tB >> 1];
+    if (tid < 2 * R) tt[tid / R][tid % R] = p.t[meta[(tid / R) * MS + tid % R][0] >> 1];
+    if constexpr (MODE == kWsBf16Dma)
+        request_frag(bs0, 0, wave);
+    else
+        request_pieces(0);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int s = 0; s < KXM; s++)
@@ -948,154 +973,219 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
         for (int g = 0; g < 3; g++)
             bh[s][g] = *(const bf16x8 *)(p.w_hh + ((size_t)g * d + jr) * p.kd + 32 * s + lk);
     if (lane < 16 && mma) {
-        // r and z biases pre-scaled for the base-2 exponential, then the
-        // input and hidden biases of n
-        sbias[0][j] = -kLog2e * (p.b_ih[jr] + p.b_hh[jr]);
-        sbias[1][j] = -kLog2e * (p.b_ih[d + jr] + p.b_hh[d + jr]);
+        sbias[0][j] = p.b_ih[jr] + p.b_hh[jr];
+        sbias[1][j] = p.b_ih[d + jr] + p.b_hh[d + jr];
         sbias[2][j] = p.b_ih[2 * d + jr];
         sbias[3][j] = p.b_hh[2 * d + jr];
     }
-    write_tile(bs0, bt0, 0);
-    if (tid < tu) tenc_unit(bt0, tid, (float)t_first);
-    tile_barrier();
+    __syncthreads();
+    if constexpr (MODE != kWsBf16Dma) write_pieces(bs0, bt0);
+    for (uint32_t u = tid; u < tu; u += T) tenc_unit(bt0, u, (float)tt[0][unit_row(u)]);
+    write_edges(bt0, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), seen by the compiler's own wait tracking
+    __syncthreads();
 
-    // Candidate rows of tile tlp (row-list slot `slot`) from its staging
-    // area, 16 bytes per thread and step.
-    auto copy_out = [&](const uint8_t *ob, uint32_t slot, uint32_t tlp) __attribute__((always_inline)) {
-        constexpr uint32_t CO = MODE == kWsF32 ? 2 : 1;   // >= R * (kd * element size / 16) / T
-        const uint32_t cpr = p.srb / 16, units = min(R, count - tlp * R) * cpr;
+    // The products of a tile (buffers cbS, cbT) into acc, from the biases.
+    f32x4 acc[4][NB];   // r, z, input part of n, hidden part of n
+    auto products = [&](const uint8_t *cbS, const uint8_t *cbT) __attribute__((always_inline)) {
+        {
+            const f32x4 b0 = *(const f32x4 *)&sbias[0][u0], b1 = *(const f32x4 *)&sbias[1][u0],
+                        b2 = *(const f32x4 *)&sbias[2][u0], b3 = *(const f32x4 *)&sbias[3][u0];
 #pragma unroll
-        for (uint32_t k = 0; k < CO; k++) {
-            const uint32_t u = tid + k * T;
-            if (u < units) {
-                const uint32_t row = nlb_div(u, p.ws_cpr_m), c = 16u * (u - row * cpr);
-                const u32x4 v = *(const u32x4 *)(ob + row * OSTR + c);
-                *(u32x4 *)(p.cand + (size_t)meta[slot * MS + row][0] * p.srb + c) = v;
+            for (int rb = 0; rb < NB; rb++) {
+                acc[0][rb] = b0;
+                acc[1][rb] = b1;
+                acc[2][rb] = b2;
+                acc[3][rb] = b3;
             }
         }
-    };
-
-    // One tile: products from (cbS, cbT) (row-list slot i % 8) while the
-    // next tile arrives in (nbS, nbT); new statuses to ob, those of the
-    // previous tile out of obp; false after the workgroup's last tile.
-    auto tile = [&](uint8_t *cbS, uint8_t *cbT, uint8_t *nbS, uint8_t *nbT, uint8_t *ob, const uint8_t *obp,
-                    uint32_t i) __attribute__((always_inline)) {
-        const uint32_t ms = i & 7, ns = (i + 1) & 7;
-        const bool has_next = tl + stride < tiles, has_nn = tl + 2 * stride < tiles;
-        const uint32_t tnn = has_nn ? tl + 2 * stride : tl;
-        // Row list of the tile two strides on (straight into its slot; the
-        // list rows of the threads' encoding units too) and status rows of the
-        // next tile (re-reads of the current tile's when there is none: in
-        // bounds, unused).
-        if (has_nn && wave == 0)
-            lds_load16(p.list + list_at(tnn, lane & (R - 1)), lds_addr(meta + ((i + 2) & 7) * MS));
-        const uint32_t rB = t_row(tnn, tid);
-        if (MODE != kWsBf16Dma || has_next) request_tile(nbS, has_next ? ns : ms);
-        if (i > 0) copy_out(obp, (i - 1) & 7, tl - stride);
-        // The second half encodes its units of the next tile now, the first
-        // half after its products.
-        const float tf = (float)tB;
-        if (second && has_next && tid < tu) tenc_unit(nbT, tid, tf);
-        f32x4 acc[4][NB];   // r, z, input part of n, hidden part of n
-        if (mma) {
-            const uint32_t lm = opaque_u32(p.ws_lomask), ks = opaque_u32(kx_steps);
-            const uint8_t *bS = cbS + 16u * lane, *bT = cbT + 16u * lane;
-#pragma unroll
-            for (int g = 0; g < 4; g++)
-#pragma unroll
-                for (int rb = 0; rb < NB; rb++) acc[g][rb] = f32x4(0.0f);
-            auto mfma3 = [&](const bf16x8 (&a)[NB], const bf16x8 (&w)[3], int nidx) __attribute__((always_inline)) {
-#pragma unroll
-                for (int rb = 0; rb < NB; rb++)
-#pragma unroll
-                    for (int g = 0; g < 3; g++) {
-                        const int gi = g == 2 ? nidx : g;
-                        acc[gi][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rb], w[g], acc[gi][rb], 0, 0, 0);
-                    }
-            };
-            // Operands of step s (X steps, then H steps): the hi plane
-            // always, the lo plane where the step has one; those of step
-            // s + 1 are read before the products of step s.
-            auto load_step = [&](int s, bf16x8 (&a)[NB], bf16x8 (&al)[NB]) __attribute__((always_inline)) {
-                const uint8_t *hi = s < KH ? bS + L::sx + s * NB * FB
-                                  : s < KXM ? bT + L::tx + (s - KH) * NB * FB : bS + L::sh + (s - KXM) * NB * FB;
-                const uint8_t *lo = s < KXM ? bT + L::tl + s * NB * FB : bT + L::th + (s - KXM) * NB * FB;
-#pragma unroll
-                for (int rb = 0; rb < NB; rb++) a[rb] = *(const bf16x8 *)(hi + rb * FB);
-                if (s < KXM ? ((lm >> s) & 1u) != 0 : MODE == kWsF32) {
-#pragma unroll
-                    for (int rb = 0; rb < NB; rb++) al[rb] = *(const bf16x8 *)(lo + rb * FB);
-                }
-            };
-            bf16x8 a[2][NB], al[NB];
-            load_step(0, a[0], al);
-#pragma unroll
-            for (int s = 0; s < KS; s++) {
-                bf16x8 nal[NB];
-                if (s + 1 < KS) load_step(s + 1, a[(s + 1) & 1], nal);
-                if (s < KXM) {
-                    if ((uint32_t)s < ks) mfma3(a[s & 1], bx[s], 2);
-                    if ((lm >> s) & 1u) mfma3(al, bx[s], 2);
-                } else {
-                    mfma3(a[s & 1], bh[s - KXM], 3);
-                    if constexpr (MODE == kWsF32) mfma3(al, bh[s - KXM], 3);
-                }
-#pragma unroll
-                for (int rb = 0; rb < NB; rb++) al[rb] = nal[rb];
-            }
-        }
-        // Link times of the second half's next units, read while the gates
-        // are applied (kept after the products: their addresses come from
-        // loads issued with the direct ones, which a wait here would cover).
-        __builtin_amdgcn_sched_barrier(0);
-        tB = p.t[rB >> 1];
-        if (mma) {
-            float hv[NB][4];
+        const uint32_t lm = FULL ? ws_full_lomask<KH>() : opaque_u32(p.ws_lomask),
+                       ks = FULL ? (uint32_t)KXM : opaque_u32(kx_steps);
+        const uint8_t *bS = cbS + 16u * lane, *bT = cbT + 16u * lane;
+        auto mfma3 = [&](const bf16x8 (&a)[NB], const bf16x8 (&w)[3], int nidx) __attribute__((always_inline)) {
 #pragma unroll
             for (int rb = 0; rb < NB; rb++)
 #pragma unroll
-                for (int q = 0; q < 4; q++) {
-                    const uint32_t row = 16u * rb + 4u * (lane >> 4) + q;
-                    if constexpr (MODE == kWsF32)
-                        hv[rb][q] = ((const float *)(p.st + (size_t)meta[ms * MS + row][1] * p.srb))[jr];
-                    else
-                        hv[rb][q] = (float)*(const __bf16 *)(cbS + L::sh + frag_off(row, jr & ~7u) + 2u * (jr & 7u));
+                for (int g = 0; g < 3; g++) {
+                    const int gi = g == 2 ? nidx : g;
+                    acc[gi][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[g], a[rb], acc[gi][rb], 0, 0, 0);
                 }
-            if (j < d) {
-                const float nbr = sbias[0][j], nbz = sbias[1][j], bin = sbias[2][j], bhn = sbias[3][j];
+        };
+        // Operands of step s (X steps, then H steps): the hi plane always,
+        // the lo plane where the step has one.  Hi operands are read AH steps
+        // before their products (two where the registers allow), lo operands
+        // one step before.
+        constexpr int AH = 1;
+        auto load_hi = [&](int s, bf16x8 (&a)[NB]) __attribute__((always_inline)) {
+            const uint8_t *hi = s < KH ? bS + L::sx + s * NB * FB
+                              : s < KXM ? bT + L::tx + (s - KH) * NB * FB : bS + L::sh + (s - KXM) * NB * FB;
 #pragma unroll
-                for (int rb = 0; rb < NB; rb++)
+            for (int rb = 0; rb < NB; rb++) a[rb] = *(const bf16x8 *)(hi + rb * FB);
+        };
+        auto load_lo = [&](int s, bf16x8 (&al)[NB]) __attribute__((always_inline)) {
+            const uint8_t *lo = s < KXM ? bT + L::tl + s * NB * FB : bT + L::th + (s - KXM) * NB * FB;
+            if (s < KXM ? ((lm >> s) & 1u) != 0 : MODE == kWsF32) {
 #pragma unroll
-                    for (int q = 0; q < 4; q++) {
-                        const uint32_t row = 16u * rb + 4u * (lane >> 4) + q;
-                        const float rg = __builtin_amdgcn_rcpf(
-                            1.0f + __builtin_amdgcn_exp2f(__builtin_fmaf(acc[0][rb][q], -kLog2e, nbr)));
-                        const float zg = __builtin_amdgcn_rcpf(
-                            1.0f + __builtin_amdgcn_exp2f(__builtin_fmaf(acc[1][rb][q], -kLog2e, nbz)));
-                        const float ng = tanh_f32(__builtin_fmaf(rg, acc[3][rb][q] + bhn, acc[2][rb][q] + bin));
-                        const float out = __builtin_fmaf(zg, hv[rb][q] - ng, ng);   // (1 - z) n + z h
-                        if constexpr (MODE == kWsF32)
-                            ((float *)(ob + row * OSTR))[j] = out;
-                        else
-                            ((__bf16 *)(ob + row * OSTR))[j] = (__bf16)out;   // round to nearest even
-                    }
+                for (int rb = 0; rb < NB; rb++) al[rb] = *(const bf16x8 *)(lo + rb * FB);
+            }
+        };
+        bf16x8 a[AH + 1][NB], al[NB];
+#pragma unroll
+        for (int s = 0; s < AH; s++) load_hi(s, a[s]);
+        load_lo(0, al);
+#pragma unroll
+        for (int s = 0; s < KS; s++) {
+            bf16x8 nal[NB];
+            if (s + AH < KS) load_hi(s + AH, a[(s + AH) % (AH + 1)]);
+            if (s + 1 < KS) load_lo(s + 1, nal);
+            // (the loads stay ahead of this step's products: without branches
+            // between the steps the scheduler would otherwise sink each read
+            // to its first use and wait for it there)
+            __builtin_amdgcn_sched_barrier(0);
+            const bf16x8 (&as)[NB] = a[s % (AH + 1)];
+            if (s < KXM) {
+                if ((uint32_t)s < ks) mfma3(as, bx[s], 2);
+                if ((lm >> s) & 1u) mfma3(al, bx[s], 2);
+            } else {
+                mfma3(as, bh[s - KXM], 3);
+                if constexpr (MODE == kWsF32) mfma3(al, bh[s - KXM], 3);
+            }
+#pragma unroll
+            for (int rb = 0; rb < NB; rb++) al[rb] = nal[rb];
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    // h values of this lane's units u0 .. u0 + 3 in the tile's rows: from the
+    // tile's H plane (bf16 statuses, packed pairs) or the status rows (fp32).
+    using HvT = std::conditional_t<MODE == kWsF32, f32x4, u32x2>;
+    HvT hv[NB];
+    auto read_hv = [&](const uint8_t *cbS, uint32_t ms) __attribute__((always_inline)) {
+#pragma unroll
+        for (int rb = 0; rb < NB; rb++) {
+            const uint32_t row = 16u * rb + lr;
+            if constexpr (MODE == kWsF32)
+                hv[rb] = u0 < d ? *(const f32x4 *)(p.st + (size_t)meta[ms * MS + row][1] * p.srb + 4u * u0) : f32x4(0.0f);
+            else
+                hv[rb] = *(const u32x2 *)(cbS + L::sh + frag_off(row, u0 & ~7u) + 2u * (u0 & 7u));
+        }
+    };
+    auto h_at = [&](int rb, int q) __attribute__((always_inline)) {
+        if constexpr (MODE == kWsF32)
+            return hv[rb][q];
+        else
+            return __uint_as_float(q & 1 ? hv[rb][q >> 1] & 0xFFFF0000u : hv[rb][q >> 1] << 16);
+    };
+    // The gates of the tile in row-list slot ms (tile tlg of the launch)
+    // from acc and hv; new statuses of its listed rows to their candidate
+    // rows.
+    auto gates = [&](uint32_t ms, uint32_t tlg) __attribute__((always_inline)) {
+        const uint32_t nrows = min(R, count - tlg * R);
+#pragma unroll
+        for (int rb = 0; rb < NB; rb++) {
+            const uint32_t row = 16u * rb + lr;
+            float out[4];
+#pragma unroll
+            for (int q = 0; q < 4; q++) {
+                const float rg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(acc[0][rb][q] * -kLog2e));
+                const float zg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(acc[1][rb][q] * -kLog2e));
+                const float ng = tanh_f32(__builtin_fmaf(rg, acc[3][rb][q], acc[2][rb][q]));
+                out[q] = __builtin_fmaf(zg, h_at(rb, q) - ng, ng);   // (1 - z) n + z h
+            }
+            if (u0 < d && row < nrows) {
+                uint8_t *dst = p.cand + (size_t)meta[ms * MS + row][0] * p.srb;
+                if constexpr (MODE == kWsF32) {
+                    store_b128_async(dst + 4u * u0, u32x4{__float_as_uint(out[0]), __float_as_uint(out[1]),
+                                                          __float_as_uint(out[2]), __float_as_uint(out[3])});
+                } else {
+                    u32x2 o;
+#pragma unroll
+                    for (int q = 0; q < 4; q += 2)   // round to nearest even
+                        o[q / 2] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)out[q]) |
+                                   ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)out[q + 1]) << 16);
+                    store_b64_async(dst + 2u * u0, o);
+                }
             }
         }
-        if (!second && has_next && tid < tu) tenc_unit(nbT, tid, tf);
-        if (has_next) write_tile(nbS, nbT, ns);
-        tile_barrier();
+    };
+
+    // Tile i of the workgroup (launch tile tl, buffers i % 2, row-list slot
+    // i % 8) in the first half: products, gates, then its share of the next
+    // tile's time encoding (units tid, tid + T, ..., as in the second half)
+    // and the link rows; false after the workgroup's last tile.  (No loads here
+    // on the direct path: a wait for one would also wait for the last tile's
+    // candidate-row stores.)
+    auto tile_first = [&](uint8_t *cbS, uint8_t *cbT, uint8_t *nbS, uint8_t *nbT, uint32_t i)
+                          __attribute__((always_inline)) {
+        const uint32_t ms = i & 7;
+        const bool has_next = tl + stride < tiles;
+        if (MODE != kWsBf16Dma && has_next) request_pieces((i + 1) & 7);
+        if (mma) {
+            products(cbS, cbT);
+            read_hv(cbS, ms);
+            gates(ms, tl);
+        }
+        if (has_next) {
+            for (uint32_t u = tid; u < tu; u += T) tenc_unit(nbT, u, (float)tt[(i + 1) & 3][unit_row(u)]);
+            if (MODE != kWsBf16Dma) write_pieces(nbS, nbT);
+            write_edges(nbT, (i + 1) & 7);
+        }
+        barrier_lds();
         tl += stride;
         return has_next;
     };
-    for (uint32_t i = 0;; i += 2) {
-        if (!tile(bs0, bt0, bs1, bt1, ost0, ost1, i)) {
-            copy_out(ost0, i & 7, tl - stride);
-            break;
+    // The same tile in the second half: the loads of the tiles ahead, the
+    // gates of the previous tile, its share of the next tile's time encoding,
+    // then the products and h values, kept for the next tile.  Wavefront KH reads
+    // the row lists and link times.
+    auto tile_second = [&](uint8_t *cbS, uint8_t *cbT, uint8_t *nbS, uint8_t *nbT, uint32_t i)
+                           __attribute__((always_inline)) {
+        const uint32_t ms = i & 7, ns = (i + 1) & 7;
+        const bool has_next = tl + stride < tiles, has_nn = tl + 2 * stride < tiles,
+                   has_n3 = tl + 3 * stride < tiles;
+        if (wave == (uint32_t)KH && has_n3)   // row list of the tile three on, straight into its slot
+            lds_load16(p.list + list_at(tl + 3 * stride, lane & (R - 1)), lds_addr(meta + ((i + 3) & 7) * MS));
+        // link times of the rows of the tile two on (its row list arrived with
+        // the last barrier), straight into their row of tt
+        if (wave == (uint32_t)KH && has_nn)
+            lds_load4(p.t + (meta[((i + 2) & 7) * MS + (lane & (R - 1))][0] >> 1), lds_addr(tt[(i + 2) & 3]));
+        if (has_next) {
+            if constexpr (MODE == kWsBf16Dma) {
+                request_frag(nbS, ns, wave - KH);
+                request_frag(nbS, ns, wave);
+            } else {
+                request_pieces(ns);
+            }
         }
-        if (!tile(bs1, bt1, bs0, bt0, ost1, ost0, i + 1)) {
-            copy_out(ost1, (i + 1) & 7, tl - stride);
-            break;
+        if (i > 0 && mma) gates((i - 1) & 7, tl - stride);
+        if (has_next) {
+            for (uint32_t u = tid; u < tu; u += T) tenc_unit(nbT, u, (float)tt[(i + 1) & 3][unit_row(u)]);
+            if (MODE != kWsBf16Dma) write_pieces(nbS, nbT);
         }
+        if (mma) {
+            products(cbS, cbT);
+            read_hv(cbS, ms);
+        }
+        barrier_loads();
+        tl += stride;
+        return has_next;
+    };
+    if (!second) {
+        for (uint32_t i = 0;; i += 2) {
+            if (!tile_first(bs0, bt0, bs1, bt1, i)) break;
+            if (!tile_first(bs1, bt1, bs0, bt0, i + 1)) break;
+        }
+    } else {
+        uint32_t i = 0;
+        for (;; i += 2) {
+            if (!tile_second(bs0, bt0, bs1, bt1, i)) break;
+            if (!tile_second(bs1, bt1, bs0, bt0, i + 1)) {
+                i++;
+                break;
+            }
+        }
+        if (mma) gates(i & 7, tl - stride);   // the workgroup's last tile
     }
 }
 
@@ -1342,11 +1432,10 @@ static int rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, cons
     uint32_t lds = 0, nb = 4;
     int cus = 0;
     if (ws) {
-        // static LDS: tile buffers, staging areas, row-list slots; dynamic: T-enc w | b
+        // static LDS: tile buffers, row-list slots, link times, biases; dynamic: T-enc w | b
         const uint32_t fixed = kh == 1 ? WsLayout<1>::fixed : kh == 2 ? WsLayout<2>::fixed
                              : kh == 3 ? WsLayout<3>::fixed : WsLayout<4>::fixed;
         lds = 8u * pad32(p.d_time);
-        p.ws_cpr_m = nlb_div_magic(p.srb / 16);
         ws = fixed + lds <= kGruLdsMax &&
              hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) == hipSuccess && cus > 0;
         for (uint32_t st = p.lo_begin / 32; st < p.lo_end / 32; st++) p.ws_lomask |= 1u << st;
@@ -1389,15 +1478,18 @@ static int rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, cons
                        dim3(kRnnThreads), 0, (hipStream_t)stream, sp);
     if (ws) {
         const void *kern = nullptr;
+        const bool full = ws_mode == kWsBf16Dma && kh == 4 && p.kx == 32u * (kWsSteps - 4) &&
+                          p.ws_lomask == ws_full_lomask<4>();
         switch (kh * 4 + ws_mode) {
 #define NLB_WS_CASE(KH, MODE) \
-        case KH * 4 + MODE: kern = (const void *)rnn_gru_ws<KH, MODE>; break;
+        case KH * 4 + MODE: kern = (const void *)rnn_gru_ws<KH, MODE, false>; break;
         NLB_WS_CASE(1, kWsBf16Dma) NLB_WS_CASE(1, kWsBf16) NLB_WS_CASE(1, kWsF32)
         NLB_WS_CASE(2, kWsBf16Dma) NLB_WS_CASE(2, kWsBf16) NLB_WS_CASE(2, kWsF32)
         NLB_WS_CASE(3, kWsBf16Dma) NLB_WS_CASE(4, kWsBf16Dma)
 #undef NLB_WS_CASE
         default: return NLB_EINVAL;
         }
+        if (full) kern = (const void *)rnn_gru_ws<4, kWsBf16Dma, true>;
         const uint64_t tiles = (pairs + 31) / 32;
         const dim3 grid((unsigned)std::min<uint64_t>(tiles, (uint64_t)cus));
         void *args[] = {&p};
