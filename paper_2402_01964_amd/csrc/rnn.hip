@@ -140,6 +140,15 @@ struct SelectParams {
     const unsigned long long *winner;
     u32x4 *list;          // winners, dense: {pair row, self, other, 0}
     uint32_t *count;
+    // Weights for the weight-stationary GRU pass, repacked here in operand-
+    // fragment order (wpack null: not needed): fragment (unit block b, k-step
+    // s, gate g) is 64 lanes x 16 bytes at ((b * ks + s) * 3 + g) * 64, lane l
+    // holding unit 16 b + l % 16 (clamped to d - 1), columns 32 s' + 8 (l / 16)
+    // .. + 7 of W_i (steps s < kxm, s' = min(s, kx_steps - 1)) or of W_h (s' =
+    // s - kxm).
+    const __bf16 *w_ih, *w_hh;
+    u32x4 *wpack;
+    uint32_t d, kx, kd, kx_steps, kxm, ks, pieces;
 };
 
 // A workgroup checks kSelectRows consecutive pair rows, collects its
@@ -201,6 +210,17 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_select(SelectParams p) {
     if (threadIdx.x == 0) base = n_local ? atomicAdd(p.count, n_local) : 0;
     __syncthreads();
     for (uint32_t k = threadIdx.x; k < n_local; k += kRnnThreads) p.list[base + k] = rows[k];
+    // The weight pack: each 16-byte piece read once (row reads of 64 bytes)
+    // and written once, contiguous in the order the GRU pass loads them.
+    if (p.wpack) {
+        for (uint32_t q = blockIdx.x * kRnnThreads + threadIdx.x; q < p.pieces; q += gridDim.x * kRnnThreads) {
+            const uint32_t l = q & 63u, f = q >> 6, g = f % 3u, s = (f / 3u) % p.ks, b = f / (3u * p.ks);
+            const uint32_t jr = min(16u * b + (l & 15u), p.d - 1u), lk = (l >> 4) * 8u;
+            const __bf16 *src = s < p.kxm ? p.w_ih + ((size_t)g * p.d + jr) * p.kx + 32u * min(s, p.kx_steps - 1u) + lk
+                                          : p.w_hh + ((size_t)g * p.d + jr) * p.kd + 32u * (s - p.kxm) + lk;
+            p.wpack[q] = *(const u32x4 *)src;
+        }
+    }
 }
 
 struct GruParams {
@@ -235,6 +255,7 @@ struct GruParams {
     uint32_t ws_lomask;                 // weight-stationary form: bit s set if X k-step s has a lo plane
     const __bf16 *w_ih, *w_hh;
     const float *b_ih, *b_hh;
+    const u32x4 *wpack;                 // weight-stationary form: the weights in fragment order (rnn_select)
 };
 
 // Arrival index of link 0 of the batch: given, or (NLB_EID_LAST_BATCH) the
@@ -940,47 +961,85 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     };
 
     // Prologue, ordered so that the weights' transfer (about 300 KB per CU,
-    // from L2) overlaps the first tile's dependent loads: time-encoding
-    // parameters and the row lists of the first three tiles; then the link
-    // times of the first two tiles' rows and the first tile's status rows;
-    // then the weights and biases; then the first tile's inputs and barrier.
-    for (uint32_t u = tid; u < ((p.d_time + 31u) & ~31u); u += T) {
-        s_tw[u] = u < p.d_time ? p.tw[u] : 0.0f;
-        s_tb[u] = u < p.d_time ? p.tb[u] : 0.0f;
-    }
+    // from L2) overlaps the first tile's dependent loads and its time
+    // encoding: the row lists of the first three tiles, the time-encoding
+    // parameters and the biases, all issued before any is used; then the
+    // link times of the first two tiles' rows (direct loads into tt), the
+    // weights and the first tile's status rows; then, once the link times
+    // are in, the first tile's time encoding, and one wait for everything
+    // before the barrier.
     const uint32_t stride = gridDim.x;
     uint32_t tl = blockIdx.x;
-    if (tid < 3 * R) {
-        const uint32_t k = tid / R, tk = tl + k * stride < tiles ? tl + k * stride : tl;
-        meta[k * MS + tid % R] = p.list[list_at(tk, tid % R)];
+    {
+        constexpr uint32_t TW = (32u * (kWsSteps - 2 * KH) + T - 1) / T;   // pad32(d_time) <= 32 (KXM - KH)
+        const uint32_t padt = (p.d_time + 31u) & ~31u;
+        u32x4 le = {};
+        if (tid < 3 * R) {
+            const uint32_t k = tid / R, tk = tl + k * stride < tiles ? tl + k * stride : tl;
+            le = p.list[list_at(tk, tid % R)];
+        }
+        float twv[TW], tbv[TW], bv[6];
+#pragma unroll
+        for (uint32_t k = 0; k < TW; k++) {
+            const uint32_t u = tid + k * T;
+            twv[k] = u < p.d_time ? p.tw[u] : 0.0f;
+            tbv[k] = u < p.d_time ? p.tb[u] : 0.0f;
+        }
+        if (lane < 16 && mma) {
+#pragma unroll
+            for (int g = 0; g < 3; g++) {
+                bv[2 * g] = p.b_ih[g * d + jr];
+                bv[2 * g + 1] = p.b_hh[g * d + jr];
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (tid < 3 * R) meta[(tid / R) * MS + tid % R] = le;
+#pragma unroll
+        for (uint32_t k = 0; k < TW; k++) {
+            const uint32_t u = tid + k * T;
+            if (u < padt) {
+                s_tw[u] = twv[k];
+                s_tb[u] = tbv[k];
+            }
+        }
+        if (lane < 16 && mma) {
+            sbias[0][j] = bv[0] + bv[1];
+            sbias[1][j] = bv[2] + bv[3];
+            sbias[2][j] = bv[4];
+            sbias[3][j] = bv[5];
+        }
     }
     __syncthreads();
-    if (tid < 2 * R) tt[tid / R][tid % R] = p.t[meta[(tid / R) * MS + tid % R][0] >> 1];
+    {   // link times of the first two tiles' rows, straight into tt rows 0 and 1 (every
+        // wavefront loads the same words, so each needs to wait for its own loads only,
+        // and no branch makes the compiler wait for them at its join)
+        lds_load4(p.t + (meta[lane & (R - 1)][0] >> 1), lds_addr(tt[0]));
+        lds_load4(p.t + (meta[MS + (lane & (R - 1))][0] >> 1), lds_addr(tt[1]));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    {   // this wavefront's fragments, 1 KB each, contiguous (packed by rnn_select)
+        const u32x4 *wf = p.wpack + (size_t)wave * KS * 3 * 64 + lane;
+#pragma unroll
+        for (int s = 0; s < KXM; s++)
+#pragma unroll
+            for (int g = 0; g < 3; g++) bx[s][g] = __builtin_bit_cast(bf16x8, wf[(s * 3 + g) * 64]);
+#pragma unroll
+        for (int s = 0; s < KH; s++)
+#pragma unroll
+            for (int g = 0; g < 3; g++) bh[s][g] = __builtin_bit_cast(bf16x8, wf[((KXM + s) * 3 + g) * 64]);
+    }
     if constexpr (MODE == kWsBf16Dma)
         request_frag(bs0, 0, wave);
     else
         request_pieces(0);
     __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int s = 0; s < KXM; s++)
-#pragma unroll
-        for (int g = 0; g < 3; g++)
-            bx[s][g] = *(const bf16x8 *)(p.w_ih + ((size_t)g * d + jr) * p.kx +
-                                         32u * min((uint32_t)s, kx_steps - 1u) + lk);
-#pragma unroll
-    for (int s = 0; s < KH; s++)
-#pragma unroll
-        for (int g = 0; g < 3; g++)
-            bh[s][g] = *(const bf16x8 *)(p.w_hh + ((size_t)g * d + jr) * p.kd + 32 * s + lk);
-    if (lane < 16 && mma) {
-        sbias[0][j] = p.b_ih[jr] + p.b_hh[jr];
-        sbias[1][j] = p.b_ih[d + jr] + p.b_hh[d + jr];
-        sbias[2][j] = p.b_ih[2 * d + jr];
-        sbias[3][j] = p.b_hh[2 * d + jr];
-    }
+    // Wait for the two link-time loads only: at least the 36 weight loads
+    // were issued after them, and loads complete in order.
+    static_assert(3 * (KXM + KH) == 36, "weight loads per lane");
+    asm volatile("s_waitcnt vmcnt(36)" ::: "memory");
     __syncthreads();
-    if constexpr (MODE != kWsBf16Dma) write_pieces(bs0, bt0);
     for (uint32_t u = tid; u < tu; u += T) tenc_unit(bt0, u, (float)tt[0][unit_row(u)]);
+    if constexpr (MODE != kWsBf16Dma) write_pieces(bs0, bt0);
     write_edges(bt0, 0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), seen by the compiler's own wait tracking
@@ -1242,7 +1301,19 @@ uint32_t gru_layout(GruParams &p, uint32_t rows) {
 }
 
 // Per-table working memory of the update, grown on demand.
-int rnn_reserve(nlb_table *h, uint64_t pair_rows, uint32_t srb) {
+int rnn_reserve(nlb_table *h, uint64_t pair_rows, uint32_t srb, size_t wpack_bytes) {
+    if (wpack_bytes > h->rnn_wpack_bytes) {
+        if (hipDeviceSynchronize() != hipSuccess) return NLB_EDEVICE;
+        (void)hipFree(h->rnn_wpack);
+        h->rnn_wpack = nullptr;
+        h->rnn_wpack_bytes = 0;
+        if (hipMalloc((void **)&h->rnn_wpack, wpack_bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            h->rnn_wpack = nullptr;
+            return NLB_ENOMEM;
+        }
+        h->rnn_wpack_bytes = wpack_bytes;
+    }
     if (!h->rnn_winner) {
         const size_t bytes = (size_t)h->num_nodes * 8u;
         if (hipMalloc((void **)&h->rnn_winner, bytes) != hipSuccess) {
@@ -1284,13 +1355,14 @@ struct RnnWork {
     bool clear_winner;    // zero winner[0 .. N) first (memory shared with other calls)
     uint8_t *cand;
     uint32_t *list;       // word 0: winner count; from word 64: the winners, 4 words each
+    uint8_t *wpack;       // packed weights (weight-stationary form), or null
 };
 
 // Working memory of the table, grown on demand (nlb_rnn_update).
-int table_work(nlb_table *h, uint64_t pairs, uint32_t srb, RnnWork *wk) {
-    const int rc = rnn_reserve(h, pairs, srb);
+int table_work(nlb_table *h, uint64_t pairs, uint32_t srb, size_t wpack_bytes, RnnWork *wk) {
+    const int rc = rnn_reserve(h, pairs, srb, wpack_bytes);
     if (rc != NLB_OK) return rc;
-    *wk = {h->rnn_winner, false, h->rnn_cand, h->rnn_list};
+    *wk = {h->rnn_winner, false, h->rnn_cand, h->rnn_list, wpack_bytes ? h->rnn_wpack : nullptr};
     return NLB_OK;
 }
 
@@ -1328,17 +1400,20 @@ int scratch_address(int dev, uint8_t **out) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // The update's working memory carved from `scratch`: winner words of all N
-// nodes, the list, the candidate rows.  The winner words are cleared by a
-// fill kernel at the start of every call.
-int scratch_work(nlb_table *h, uint64_t pairs, uint32_t srb, RnnWork *wk) {
+// nodes, the list, the packed weights (weight-stationary form), the
+// candidate rows.  The winner words are cleared by a fill kernel at the
+// start of every call.
+int scratch_work(nlb_table *h, uint64_t pairs, uint32_t srb, size_t wpack_bytes, RnnWork *wk) {
     const size_t winner_bytes = align256((size_t)h->num_nodes * 8u);
     const size_t list_bytes = align256(((size_t)pairs * 4u + 64u) * 4u);
+    const size_t pack_bytes = align256(wpack_bytes);
     const size_t cand_bytes = (size_t)pairs * srb;
-    if (winner_bytes + list_bytes + cand_bytes > kScratchBytes) return NLB_ESCRATCH;
+    if (winner_bytes + list_bytes + pack_bytes + cand_bytes > kScratchBytes) return NLB_ESCRATCH;
     uint8_t *base = nullptr;
     const int rc = scratch_address(h->device, &base);
     if (rc != NLB_OK) return rc;
-    *wk = {(unsigned long long *)base, true, base + winner_bytes + list_bytes, (uint32_t *)(base + winner_bytes)};
+    *wk = {(unsigned long long *)base, true, base + winner_bytes + list_bytes + pack_bytes,
+           (uint32_t *)(base + winner_bytes), wpack_bytes ? base + winner_bytes + list_bytes : nullptr};
     return NLB_OK;
 }
 
@@ -1451,10 +1526,13 @@ static int rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, cons
         gru_layout(p, 16u * nb);
     }
 
+    // weight fragments of the weight-stationary form: 2 kh unit blocks x kWsSteps k-steps x 3 gates, 1 KB each
+    const size_t wpack_bytes = ws ? (size_t)2 * kh * kWsSteps * 3 * 1024 : 0;
     RnnWork wk;
-    const int rc = use_scratch ? scratch_work(h, pairs, p.srb, &wk)
-                               : table_work(h, pairs, p.srb, &wk);
+    const int rc = use_scratch ? scratch_work(h, pairs, p.srb, wpack_bytes, &wk)
+                               : table_work(h, pairs, p.srb, wpack_bytes, &wk);
     if (rc != NLB_OK) return rc;
+    p.wpack = (const u32x4 *)wk.wpack;
     if (wk.clear_winner) {
         const uint64_t blocks = std::min<uint64_t>(4096, ((uint64_t)h->num_nodes + kRnnThreads - 1) / kRnnThreads);
         hipLaunchKernelGGL(rnn_clear, dim3((unsigned)blocks), dim3(kRnnThreads), 0, (hipStream_t)stream,
@@ -1473,7 +1551,9 @@ static int rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, cons
     else
         hipLaunchKernelGGL(rnn_resolve, dim3((n + kRnnThreads - 1) / kRnnThreads), dim3(kRnnThreads), 0,
                            (hipStream_t)stream, rp);
-    SelectParams sp = {src, dst, n, h->num_nodes, wk.winner, list, count};
+    SelectParams sp = {src, dst, n, h->num_nodes, wk.winner, list, count,
+                       p.w_ih, p.w_hh, (u32x4 *)wk.wpack, p.d, p.kx, p.kd, p.kx / 32, kWsSteps - kh, kWsSteps,
+                       (uint32_t)(wpack_bytes / 16)};
     hipLaunchKernelGGL(rnn_select, dim3((unsigned)((pairs + kSelectRows - 1) / kSelectRows)),
                        dim3(kRnnThreads), 0, (hipStream_t)stream, sp);
     if (ws) {
