@@ -645,7 +645,6 @@ int nlb_destroy(nlb_table *h) {
         if (h->rnn_winner && hipFree(h->rnn_winner) != hipSuccess) rc = NLB_EDEVICE;
         if (h->rnn_cand && hipFree(h->rnn_cand) != hipSuccess) rc = NLB_EDEVICE;
         if (h->rnn_list && hipFree(h->rnn_list) != hipSuccess) rc = NLB_EDEVICE;
-        if (h->rnn_wpack && hipFree(h->rnn_wpack) != hipSuccess) rc = NLB_EDEVICE;
     }
     delete h;
     return rc;

@@ -291,7 +291,5 @@ struct nlb_table {
     size_t rnn_cand_bytes;
     uint32_t *rnn_list;               // winner count, then the winners' pair rows
     uint64_t rnn_cand_rows;
-    uint8_t *rnn_wpack;               // GRU weights in operand-fragment order (weight-stationary form)
-    size_t rnn_wpack_bytes;
 };
 

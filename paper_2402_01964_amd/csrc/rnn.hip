@@ -1300,20 +1300,12 @@ uint32_t gru_layout(GruParams &p, uint32_t rows) {
     return p.off_hl + (p.h_lo ? rows * p.hs * 2u : 0u);
 }
 
-// Per-table working memory of the update, grown on demand.
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Per-table working memory of the update, grown on demand: the winner
+// words, the list, and one buffer for the candidate rows followed (at a
+// 256-byte boundary) by the packed GRU weights.
 int rnn_reserve(nlb_table *h, uint64_t pair_rows, uint32_t srb, size_t wpack_bytes) {
-    if (wpack_bytes > h->rnn_wpack_bytes) {
-        if (hipDeviceSynchronize() != hipSuccess) return NLB_EDEVICE;
-        (void)hipFree(h->rnn_wpack);
-        h->rnn_wpack = nullptr;
-        h->rnn_wpack_bytes = 0;
-        if (hipMalloc((void **)&h->rnn_wpack, wpack_bytes) != hipSuccess) {
-            (void)hipGetLastError();
-            h->rnn_wpack = nullptr;
-            return NLB_ENOMEM;
-        }
-        h->rnn_wpack_bytes = wpack_bytes;
-    }
     if (!h->rnn_winner) {
         const size_t bytes = (size_t)h->num_nodes * 8u;
         if (hipMalloc((void **)&h->rnn_winner, bytes) != hipSuccess) {
@@ -1323,7 +1315,7 @@ int rnn_reserve(nlb_table *h, uint64_t pair_rows, uint32_t srb, size_t wpack_byt
         }
         if (hipMemset(h->rnn_winner, 0, bytes) != hipSuccess) return NLB_EDEVICE;
     }
-    const size_t cbytes = (size_t)pair_rows * srb;
+    const size_t cbytes = align256((size_t)pair_rows * srb) + wpack_bytes;
     if (cbytes > h->rnn_cand_bytes || pair_rows > h->rnn_cand_rows) {
         // Earlier updates may still read the old buffers.
         if (hipDeviceSynchronize() != hipSuccess) return NLB_EDEVICE;
@@ -1362,7 +1354,8 @@ struct RnnWork {
 int table_work(nlb_table *h, uint64_t pairs, uint32_t srb, size_t wpack_bytes, RnnWork *wk) {
     const int rc = rnn_reserve(h, pairs, srb, wpack_bytes);
     if (rc != NLB_OK) return rc;
-    *wk = {h->rnn_winner, false, h->rnn_cand, h->rnn_list, wpack_bytes ? h->rnn_wpack : nullptr};
+    *wk = {h->rnn_winner, false, h->rnn_cand, h->rnn_list,
+           wpack_bytes ? h->rnn_cand + align256((size_t)pairs * srb) : nullptr};
     return NLB_OK;
 }
 
@@ -1396,8 +1389,6 @@ int scratch_address(int dev, uint8_t **out) {
     *out = g_scratch_addr[dev];
     return NLB_OK;
 }
-
-size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // The update's working memory carved from `scratch`: winner words of all N
 // nodes, the list, the packed weights (weight-stationary form), the
