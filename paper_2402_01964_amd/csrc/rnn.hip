@@ -289,6 +289,15 @@ __device__ __forceinline__ float tanh_f32(float a) {
     return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(2.0f * kLog2e * a));
 }
 
+// cos of an fp32 argument with |x| < kCosFastLimit: the revolutions y =
+// x / (2 pi) in double, reduced to [0, 1) by v_fract_f64 (exact), then the
+// hardware cosine; as cos_fp32_small with one instruction fewer, the
+// fraction's rounding to fp32 adding at most 2^-25 of a revolution.
+__device__ __forceinline__ float cos_fract(float x) {
+    const double y = (double)x * 0.15915494309189533577;
+    return __builtin_amdgcn_cosf((float)__builtin_amdgcn_fract(y));
+}
+
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     const uint32_t u = __float_as_uint(f);
     return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
@@ -817,6 +826,7 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     __shared__ __attribute__((aligned(16))) uint32_t tt[L::tslots][64];
     // gate biases by output unit: b_ir + b_hr, b_iz + b_hz, b_in, b_hn
     __shared__ __attribute__((aligned(16))) float sbias[4][32 * KH];
+    __shared__ float s_wb[2];   // largest |w| and |b| of the time encoding
     extern __shared__ __attribute__((aligned(16))) float s_tw[];   // T-enc w | b, pad32(d_time) each
     float *s_tb = s_tw + ((p.d_time + 31u) & ~31u);
 
@@ -886,29 +896,34 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     // wavefront meets one.
     auto unit_row = [](uint32_t u) { return 16u * ((u >> 6) % NB) + (u & 15u); };
     auto unit_col = [](uint32_t u) { return 32u * ((u >> 6) / NB) + 8u * ((u >> 4) & 3u); };
+    // Columns past d_time have w = b = 0 here, so their (finite) values meet
+    // the weights' zero padding.  Where no argument of the wavefront's units
+    // can reach the fast cosine's limit (|w| t + |b| below half of it for the
+    // largest |w| and |b| of the encoding, wmax and bmax) the values take the
+    // fast path with no per-value test.
+    float wmax = 0.0f, bmax = 0.0f;   // set after the prologue
     auto tenc_unit = [&](uint8_t *nbT, uint32_t u, float tf) __attribute__((always_inline)) {
         const uint32_t k = unit_col(u);
+        const bool fast = __ballot(!(__builtin_fmaf(wmax, tf, bmax) < 0.5f * kCosFastLimit)) == 0;
         // two halves of four values (fewer registers live at once)
 #pragma unroll
         for (int h = 0; h < 2; h++) {
             const f32x4 w = *(const f32x4 *)(s_tw + k + 4 * h), b = *(const f32x4 *)(s_tb + k + 4 * h);
-            float x[4], v[4];
-            bool wide = false;
+            float v[4];
+            if (__builtin_expect(fast, 1)) {
 #pragma unroll
-            for (int e = 0; e < 4; e++) {
-                x[e] = __builtin_fmaf(w[e], tf, b[e]);
-                v[e] = cos_fp32_small(x[e]);
-                wide |= !(__builtin_fabsf(x[e]) < kCosFastLimit);
-            }
-            if (__builtin_expect(__ballot(wide) != 0, 0)) {
+                for (int e = 0; e < 4; e++) v[e] = cos_fract(__builtin_fmaf(w[e], tf, b[e]));
+            } else {
 #pragma unroll
-                for (int e = 0; e < 4; e++)
-                    if (!(__builtin_fabsf(x[e]) < kCosFastLimit)) v[e] = cos_fp32_exact_wide(x[e]);
+                for (int e = 0; e < 4; e++) {
+                    const float x = __builtin_fmaf(w[e], tf, b[e]);
+                    v[e] = __builtin_fabsf(x) < kCosFastLimit ? cos_fp32_small(x) : cos_fp32_exact_wide(x);
+                }
             }
             u32x2 hi, lo;
 #pragma unroll
             for (int e = 0; e < 4; e += 2) {
-                float a0 = k + 4 * h + e < p.d_time ? v[e] : 0.0f, a1 = k + 4 * h + e + 1 < p.d_time ? v[e + 1] : 0.0f;
+                const float a0 = v[e], a1 = v[e + 1];
                 const __bf16 h0 = (__bf16)a0, h1 = (__bf16)a1;
                 const __bf16 l0 = (__bf16)(a0 - (float)h0), l1 = (__bf16)(a1 - (float)h1);
                 hi[e / 2] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
@@ -1010,6 +1025,22 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
         }
     }
     __syncthreads();
+    if (wave == 0) {
+        float mw = 0.0f, mb = 0.0f;
+        for (uint32_t u = lane; u < ((p.d_time + 31u) & ~31u); u += 64) {
+            mw = fmaxf(mw, __builtin_fabsf(s_tw[u]));
+            mb = fmaxf(mb, __builtin_fabsf(s_tb[u]));
+        }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            mw = fmaxf(mw, __shfl_xor(mw, o));
+            mb = fmaxf(mb, __shfl_xor(mb, o));
+        }
+        if (lane == 0) {
+            s_wb[0] = mw;
+            s_wb[1] = mb;
+        }
+    }
     {   // link times of the first two tiles' rows, straight into tt rows 0 and 1 (every
         // wavefront loads the same words, so each needs to wait for its own loads only,
         // and no branch makes the compiler wait for them at its join)
@@ -1038,6 +1069,8 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     static_assert(3 * (KXM + KH) == 36, "weight loads per lane");
     asm volatile("s_waitcnt vmcnt(36)" ::: "memory");
     __syncthreads();
+    wmax = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(s_wb[0])));
+    bmax = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(s_wb[1])));
     for (uint32_t u = tid; u < tu; u += T) tenc_unit(bt0, u, (float)tt[0][unit_row(u)]);
     if constexpr (MODE != kWsBf16Dma) write_pieces(bs0, bt0);
     write_edges(bt0, 0);
