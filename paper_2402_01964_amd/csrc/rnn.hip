@@ -1153,6 +1153,7 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
     // tile's H plane (bf16 statuses, packed pairs) or the status rows (fp32).
     using HvT = std::conditional_t<MODE == kWsF32, f32x4, u32x2>;
     HvT hv[NB];
+    uint32_t prow[NB];   // second half: pair rows of the tile whose gates are pending
     auto read_hv = [&](const uint8_t *cbS, uint32_t ms) __attribute__((always_inline)) {
 #pragma unroll
         for (int rb = 0; rb < NB; rb++) {
@@ -1169,10 +1170,14 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
         else
             return __uint_as_float(q & 1 ? hv[rb][q >> 1] & 0xFFFF0000u : hv[rb][q >> 1] << 16);
     };
-    // The gates of the tile in row-list slot ms (tile tlg of the launch)
-    // from acc and hv; new statuses of its listed rows to their candidate
-    // rows.
-    auto gates = [&](uint32_t ms, uint32_t tlg) __attribute__((always_inline)) {
+    // The gates of tile tlg of the launch from acc and hv; new statuses of
+    // its listed rows to their candidate rows (pair rows pr of the lane's
+    // tile rows 16 rb + lr, read from the tile's row-list slot).
+    auto pair_rows = [&](uint32_t ms, uint32_t (&pr)[NB]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int rb = 0; rb < NB; rb++) pr[rb] = meta[ms * MS + 16u * rb + lr][0];
+    };
+    auto gates = [&](const uint32_t (&pr)[NB], uint32_t tlg) __attribute__((always_inline)) {
         const uint32_t nrows = min(R, count - tlg * R);
 #pragma unroll
         for (int rb = 0; rb < NB; rb++) {
@@ -1186,7 +1191,7 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
                 out[q] = __builtin_fmaf(zg, h_at(rb, q) - ng, ng);   // (1 - z) n + z h
             }
             if (u0 < d && row < nrows) {
-                uint8_t *dst = p.cand + (size_t)meta[ms * MS + row][0] * p.srb;
+                uint8_t *dst = p.cand + (size_t)pr[rb] * p.srb;
                 if constexpr (MODE == kWsF32) {
                     store_b128_async(dst + 4u * u0, u32x4{__float_as_uint(out[0]), __float_as_uint(out[1]),
                                                           __float_as_uint(out[2]), __float_as_uint(out[3])});
@@ -1216,7 +1221,9 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
         if (mma) {
             products(cbS, cbT);
             read_hv(cbS, ms);
-            gates(ms, tl);
+            uint32_t pr[NB];
+            pair_rows(ms, pr);
+            gates(pr, tl);
         }
         if (has_next) {
             for (uint32_t u = tid; u < tu; u += T) tenc_unit(nbT, u, (float)tt[(i + 1) & 3][unit_row(u)]);
@@ -1250,7 +1257,7 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
                 request_pieces(ns);
             }
         }
-        if (i > 0 && mma) gates((i - 1) & 7, tl - stride);
+        if (i > 0 && mma) gates(prow, tl - stride);
         if (has_next) {
             for (uint32_t u = tid; u < tu; u += T) tenc_unit(nbT, u, (float)tt[(i + 1) & 3][unit_row(u)]);
             if (MODE != kWsBf16Dma) write_pieces(nbS, nbT);
@@ -1258,6 +1265,7 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
         if (mma) {
             products(cbS, cbT);
             read_hv(cbS, ms);
+            pair_rows(ms, prow);
         }
         barrier_loads();
         tl += stride;
@@ -1277,7 +1285,7 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
                 break;
             }
         }
-        if (mma) gates(i & 7, tl - stride);   // the workgroup's last tile
+        if (mma) gates(prow, tl - stride);   // the workgroup's last tile
     }
 }
 
