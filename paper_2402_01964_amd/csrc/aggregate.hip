@@ -379,10 +379,14 @@ struct RowParams {
 // per query group only.
 constexpr uint32_t kPs = kH;
 
-// Input unit feeding slot (ks, g, i) of a chained layer's B operand.
-__device__ __forceinline__ uint32_t chain_unit(uint32_t c) {
-    const uint32_t ks = c >> 5, r = c & 31, g = r >> 3, i = r & 7;
-    return 32u * ks + (i < 4 ? 4u * g + i : 16u + 4u * g + (i - 4u));
+// Chained layers take their weights' columns permuted: slot (ks, g, i) of a
+// k-step's B operand (LDS column c = 32 ks + 8 g + i) holds input unit
+// 32 ks + 4 g + i for i < 4 and 32 ks + 16 + 4 g + (i - 4) otherwise.
+// chain_pos is the inverse, the LDS column of input unit gc; units gc0 ..
+// gc0 + 3 (gc0 % 4 == 0) land on four consecutive LDS columns.
+__device__ __forceinline__ uint32_t chain_pos(uint32_t gc) {
+    const uint32_t b = gc & 31u;
+    return (gc & ~31u) + 8u * ((b & 15u) >> 2) + (b & 3u) + (b >= 16u ? 4u : 0u);
 }
 
 // v = hi + lo (bf16 each, hi rounded to nearest).  Pairs are converted
@@ -666,10 +670,12 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     float *vec = (float *)(smem + L::o_vec);   // b1 | b2 | b3 | b4 | v per head, 64 each
 
     // Stage the weights: w2, w4 and the aggregate columns of w3 in chained
-    // order.
+    // order.  (Each loop is unrolled so that several iterations' loads are in
+    // flight before their LDS stores: the staging is latency-bound otherwise.)
     const uint32_t tid = threadIdx.x;
     // The time-encoding columns past d_time are staged as zeros: the rows'
     // time encodings are then used unmasked (finite values, zero weight).
+#pragma unroll 4
     for (uint32_t u = tid; u < kH * (K1S * 4u); u += kRowThreads) {
         const uint32_t r = u / (K1S * 4u), c = (u % (K1S * 4u)) * 8;
         bf16x8 v = *(const bf16x8 *)(p.w1 + (size_t)r * (32u * K1S) + c);
@@ -679,16 +685,26 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         *(bf16x8 *)(W1 + r * L::ls1 + c) = v;
     }
     if constexpr (NKS > 0) {
+#pragma unroll 4
         for (uint32_t u = tid; u < kH * (NKS * 4u); u += kRowThreads) {
             const uint32_t r = u / (NKS * 4u), c = (u % (NKS * 4u)) * 8;
             *(bf16x8 *)(W3 + r * L::ls3 + c) = *(const bf16x8 *)(p.w3 + (size_t)r * (32u * K3S) + c);
         }
     }
-    for (uint32_t u = tid; u < kH * kH; u += kRowThreads) {
-        const uint32_t r = u / kH, c = u % kH;
-        W2[r * kPs + c] = p.w2[r * kH + chain_unit(c)];
-        W4[r * kPs + c] = p.w4[r * kH + chain_unit(c)];
-        W3[r * L::ls3 + 32u * NKS + c] = p.w3[(size_t)r * (32u * K3S) + 32u * NKS + chain_unit(c)];
+    // A 16-byte piece of 8 columns gc0 + e lands as two 8-byte halves, at the
+    // LDS columns of gc0 and gc0 + 4.
+#pragma unroll 4
+    for (uint32_t u = tid; u < kH * (kH / 8u); u += kRowThreads) {
+        const uint32_t r = u / (kH / 8u), gc0 = (u % (kH / 8u)) * 8u;
+        const u32x4 v2 = *(const u32x4 *)(p.w2 + r * kH + gc0), v4 = *(const u32x4 *)(p.w4 + r * kH + gc0),
+                    v3 = *(const u32x4 *)(p.w3 + (size_t)r * (32u * K3S) + 32u * NKS + gc0);
+        const uint32_t c0 = chain_pos(gc0), c1 = chain_pos(gc0 + 4u);
+        *(u32x2 *)(W2 + r * kPs + c0) = u32x2{v2[0], v2[1]};
+        *(u32x2 *)(W2 + r * kPs + c1) = u32x2{v2[2], v2[3]};
+        *(u32x2 *)(W4 + r * kPs + c0) = u32x2{v4[0], v4[1]};
+        *(u32x2 *)(W4 + r * kPs + c1) = u32x2{v4[2], v4[3]};
+        *(u32x2 *)(W3 + r * L::ls3 + 32u * NKS + c0) = u32x2{v3[0], v3[1]};
+        *(u32x2 *)(W3 + r * L::ls3 + 32u * NKS + c1) = u32x2{v3[2], v3[3]};
     }
     // Layer 2 is affine, so the logit att . (w2 a1 + b2) of a row is
     // v . a1 up to a shift common to all rows (which the softmax cancels),
@@ -703,8 +719,9 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         } else {
             val = 0.0f;
             const uint32_t r0 = (k - 4u) * (kH / HEADS);
-            for (uint32_t r = r0; r < r0 + kH / HEADS; r++)
-                val = __builtin_fmaf(p.att[r], (float)p.w2[r * kH + c], val);
+#pragma unroll
+            for (uint32_t r = 0; r < kH / HEADS; r++)
+                val = __builtin_fmaf(p.att[r0 + r], (float)p.w2[(r0 + r) * kH + c], val);
         }
         vec[u] = val;
     }
@@ -1169,27 +1186,51 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
 
     // Stage the weights as aggregate_rows does, except that the time-encoding
     // columns of w1 (and w, b) go in lane-group order (tenc_column).
+    // (Each loop unrolled so that several iterations' loads are in flight
+    // before their LDS stores: the staging is latency-bound otherwise.)
     const uint32_t tid = threadIdx.x;
+#pragma unroll 8
     for (uint32_t u = tid; u < kH * (GS * 4u); u += kRowThreads) {
         const uint32_t r = u / (GS * 4u), c = (u % (GS * 4u)) * 8;
         *(bf16x8 *)(W1 + r * L::ls1 + c) = *(const bf16x8 *)(p.w1 + (size_t)r * (32u * K1S) + c);
     }
-    for (uint32_t u = tid; u < kH * (32u * TKS); u += kRowThreads) {
-        const uint32_t r = u / (32u * TKS), kk = u % (32u * TKS), c = tenc_column(kk);
-        W1[r * L::ls1 + 32u * GS + kk] =
-            c < p.d_time ? p.w1[(size_t)r * (32u * K1S) + 32u * GS + c] : (__bf16)0.0f;
+    // Time-encoding columns: 16-byte pieces of 8 columns c0 + e (c0 = 32 ks +
+    // 8 j), element e to position kk = 32 ks + 8 (e % 4) + 2 j + e / 4, so
+    // elements e and e + 4 form one 4-byte word (columns past d_time zero).
+#pragma unroll 4
+    for (uint32_t u = tid; u < kH * (4u * TKS); u += kRowThreads) {
+        const uint32_t r = u / (4u * TKS), c0 = (u % (4u * TKS)) * 8u;
+        const u32x4 v = *(const u32x4 *)(p.w1 + (size_t)r * (32u * K1S) + 32u * GS + c0);
+        uint32_t el[8];
+#pragma unroll
+        for (int e = 0; e < 8; e++)
+            el[e] = c0 + e < p.d_time ? (v[e >> 1] >> (16 * (e & 1))) & 0xFFFFu : 0u;
+        const uint32_t kb = 32u * (c0 >> 5) + 2u * ((c0 & 31u) >> 3);
+#pragma unroll
+        for (int g = 0; g < 4; g++)
+            *(uint32_t *)(W1 + r * L::ls1 + 32u * GS + kb + 8u * g) = el[g] | (el[g + 4] << 16);
     }
     if constexpr (NKS > 0) {
+#pragma unroll 8
         for (uint32_t u = tid; u < kH * (NKS * 4u); u += kRowThreads) {
             const uint32_t r = u / (NKS * 4u), c = (u % (NKS * 4u)) * 8;
             *(bf16x8 *)(W3 + r * L::ls3 + c) = *(const bf16x8 *)(p.w3 + (size_t)r * (32u * K3S) + c);
         }
     }
-    for (uint32_t u = tid; u < kH * kH; u += kRowThreads) {
-        const uint32_t r = u / kH, c = u % kH;
-        W2[r * L::ps + c] = p.w2[r * kH + chain_unit(c)];
-        W4[r * L::ps + c] = p.w4[r * kH + chain_unit(c)];
-        W3[r * L::ls3 + 32u * NKS + c] = p.w3[(size_t)r * (32u * K3S) + 32u * NKS + chain_unit(c)];
+    // Chain-ordered columns: a 16-byte piece of 8 columns gc0 + e lands as two
+    // 8-byte halves, at the LDS columns of gc0 and gc0 + 4.
+#pragma unroll 4
+    for (uint32_t u = tid; u < kH * (kH / 8u); u += kRowThreads) {
+        const uint32_t r = u / (kH / 8u), gc0 = (u % (kH / 8u)) * 8u;
+        const u32x4 v2 = *(const u32x4 *)(p.w2 + r * kH + gc0), v4 = *(const u32x4 *)(p.w4 + r * kH + gc0),
+                    v3 = *(const u32x4 *)(p.w3 + (size_t)r * (32u * K3S) + 32u * NKS + gc0);
+        const uint32_t c0 = chain_pos(gc0), c1 = chain_pos(gc0 + 4u);
+        *(u32x2 *)(W2 + r * L::ps + c0) = u32x2{v2[0], v2[1]};
+        *(u32x2 *)(W2 + r * L::ps + c1) = u32x2{v2[2], v2[3]};
+        *(u32x2 *)(W4 + r * L::ps + c0) = u32x2{v4[0], v4[1]};
+        *(u32x2 *)(W4 + r * L::ps + c1) = u32x2{v4[2], v4[3]};
+        *(u32x2 *)(W3 + r * L::ls3 + 32u * NKS + c0) = u32x2{v3[0], v3[1]};
+        *(u32x2 *)(W3 + r * L::ls3 + 32u * NKS + c1) = u32x2{v3[2], v3[3]};
     }
     for (uint32_t u = tid; u < 5u * kH; u += kRowThreads) {
         const uint32_t k = u / kH, c = u % kH;
@@ -1198,6 +1239,7 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
             val = (k == 0 ? p.b1 : k == 1 ? p.b2 : k == 2 ? p.b3 : p.b4)[c];
         } else {
             val = 0.0f;
+#pragma unroll
             for (uint32_t r = 0; r < kH; r++) val = __builtin_fmaf(p.att[r], (float)p.w2[r * kH + c], val);
         }
         vec[u] = val;
