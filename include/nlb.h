@@ -321,12 +321,13 @@ int nlb_rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, const u
  * (device memory, host-pinned memory or library workspaces) and sets no
  * memory with hipMemset: its working memory -- the winner word of each of
  * the table's N nodes (8 B), a list of 16 B per pair row, the GRU weights
- * repacked for the weight-stationary form (72 KiB per 32 status columns,
- * when that form runs), and 2 n candidate status rows -- lives in one static
- * device array of NLB_NOALLOC_SCRATCH bytes per device, which the library
- * holds until the process ends.  The call needs align256(8 N) +
- * align256(16 (2 n) + 256) + (73728 pad32(d) / 32 in the weight-stationary
- * form) + 2 n * status row bytes of it, and returns NLB_ESCRATCH when that exceeds the array
+ * repacked in matrix-operand fragments (3 KiB per 16 status columns and
+ * 32 input columns of w_ih and w_hh together), and 2 n candidate status
+ * rows -- lives in one static device array of NLB_NOALLOC_SCRATCH bytes per
+ * device, which the library holds until the process ends.  The call needs
+ * align256(8 N) + align256(16 (2 n) + 256) + align256(3072 (pad32(d) / 16)
+ * ((k_x + pad32(d)) / 32)) + 2 n * status row bytes of it (k_x: the row
+ * width of w_ih), and returns NLB_ESCRATCH when that exceeds the array
  * (nothing is enqueued then).  Every call on a device shares that device's
  * array: the call clears what it needs cleared (the winner words, with a
  * fill kernel) and keeps no state across calls, but calls that overlap in

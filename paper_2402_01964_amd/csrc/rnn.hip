@@ -20,7 +20,9 @@
 //   select   each pair row checks whether it won; the winners are appended
 //            to a dense list (one atomic per wavefront).  The list order
 //            varies from run to run; the results do not, because every row
-//            of a matrix product depends on its own inputs only.
+//            of a matrix product depends on its own inputs only.  The same
+//            launch repacks the weights into matrix-operand fragments, so
+//            that the gru pass reads each with one contiguous 1 KB load.
 //   gru      where its registers suffice, the weight-stationary form
 //            (rnn_gru_ws: one workgroup per CU keeps the weights in
 //            registers and loops over 32-row tiles of listed rows);
@@ -48,9 +50,9 @@
 // block -- r and z (input and hidden products summed), the input part of n
 // and the hidden part of n -- so a unit's three gates meet in one lane and
 // the cell finishes without another LDS round trip.  The weight fragments
-// (read from global memory, where the whole weight set stays L2-resident)
-// go through a three-slot register ring, so each k-step's loads are issued
-// two steps before their products.
+// (packed, read from global memory, where the whole weight set stays
+// L2-resident) go through a three-slot register ring, so each k-step's
+// loads are issued two steps before their products.
 #include <algorithm>
 #include <cstring>
 #include <mutex>
@@ -140,15 +142,14 @@ struct SelectParams {
     const unsigned long long *winner;
     u32x4 *list;          // winners, dense: {pair row, self, other, 0}
     uint32_t *count;
-    // Weights for the weight-stationary GRU pass, repacked here in operand-
-    // fragment order (wpack null: not needed): fragment (unit block b, k-step
-    // s, gate g) is 64 lanes x 16 bytes at ((b * ks + s) * 3 + g) * 64, lane l
-    // holding unit 16 b + l % 16 (clamped to d - 1), columns 32 s' + 8 (l / 16)
-    // .. + 7 of W_i (steps s < kxm, s' = min(s, kx_steps - 1)) or of W_h (s' =
-    // s - kxm).
+    // The GRU weights, repacked here in operand-fragment order for the GRU
+    // pass: fragment (unit block b < kd / 16, k-step s < ks, gate g) is 64
+    // lanes x 16 bytes at ((b * ks + s) * 3 + g) * 64, lane l holding unit
+    // 16 b + l % 16 (clamped to d - 1), columns 32 s' + 8 (l / 16) .. + 7 of
+    // W_i (steps s < kxm = kx / 32, s' = s) or of W_h (s' = s - kxm).
     const __bf16 *w_ih, *w_hh;
     u32x4 *wpack;
-    uint32_t d, kx, kd, kx_steps, kxm, ks, pieces;
+    uint32_t d, kx, kd, kxm, ks, pieces;
 };
 
 // A workgroup checks kSelectRows consecutive pair rows, collects its
@@ -216,7 +217,7 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_select(SelectParams p) {
         for (uint32_t q = blockIdx.x * kRnnThreads + threadIdx.x; q < p.pieces; q += gridDim.x * kRnnThreads) {
             const uint32_t l = q & 63u, f = q >> 6, g = f % 3u, s = (f / 3u) % p.ks, b = f / (3u * p.ks);
             const uint32_t jr = min(16u * b + (l & 15u), p.d - 1u), lk = (l >> 4) * 8u;
-            const __bf16 *src = s < p.kxm ? p.w_ih + ((size_t)g * p.d + jr) * p.kx + 32u * min(s, p.kx_steps - 1u) + lk
+            const __bf16 *src = s < p.kxm ? p.w_ih + ((size_t)g * p.d + jr) * p.kx + 32u * s + lk
                                           : p.w_hh + ((size_t)g * p.d + jr) * p.kd + 32u * (s - p.kxm) + lk;
             p.wpack[q] = *(const u32x4 *)src;
         }
@@ -255,7 +256,7 @@ struct GruParams {
     uint32_t ws_lomask;                 // weight-stationary form: bit s set if X k-step s has a lo plane
     const __bf16 *w_ih, *w_hh;
     const float *b_ih, *b_hh;
-    const u32x4 *wpack;                 // weight-stationary form: the weights in fragment order (rnn_select)
+    const u32x4 *wpack;                 // the weights in operand-fragment order (rnn_select)
 };
 
 // Arrival index of link 0 of the batch: given, or (NLB_EID_LAST_BATCH) the
@@ -305,20 +306,21 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 
 // acc[g'][rb] += A_rb (16 x 32 blocks of the LDS pair Ah/Al, row stride
 // `as`; the lo plane starts at column lo_b with its own stride `ls`)
-//              * W_g^T for the three gate row blocks W_g = w0 + g * gstep,
-// over the k-steps kb, kb + 32, .. < ke; g' = g for the r and z gates and
-// g' = NIDX for the n gate.  LO adds the lo-plane products.
+//              * W_g^T for the three gates, over the k-steps kb, kb + 32, ..
+// < ke; g' = g for the r and z gates and g' = NIDX for the n gate.  LO adds
+// the lo-plane products.  The weights come packed (rnn_select): wp points at
+// this lane's word of the fragment (k-step 0, gate 0) of the matrix and unit
+// block; fragment (k-step s, gate g) is 192 s + 64 g words on.
 template <int NB, bool LO, int NIDX>
 __device__ __forceinline__ void gate_seg(f32x4 (&acc)[4][NB], const __bf16 *Ah, const __bf16 *Al,
-                                         uint32_t as, uint32_t ls, uint32_t lo_b, const __bf16 *w0,
-                                         size_t gstep, uint32_t kb, uint32_t ke, uint32_t lr,
-                                         uint32_t lk) {
+                                         uint32_t as, uint32_t ls, uint32_t lo_b, const u32x4 *wp,
+                                         uint32_t kb, uint32_t ke, uint32_t lr, uint32_t lk) {
     if (kb >= ke) return;
     const uint32_t last = ke - 32;
     bf16x8 r0[3], r1[3], r2[3];
     auto load = [&](bf16x8 (&b)[3], uint32_t k) {
 #pragma unroll
-        for (int g = 0; g < 3; g++) b[g] = *(const bf16x8 *)(w0 + g * gstep + k);
+        for (int g = 0; g < 3; g++) b[g] = __builtin_bit_cast(bf16x8, wp[(k >> 5) * 192u + g * 64u]);
     };
     auto step = [&](const bf16x8 (&b)[3], uint32_t k0) {
         bf16x8 a[NB], al[NB];
@@ -646,18 +648,15 @@ __global__ __launch_bounds__(kRnnThreads) void rnn_gru(GruParams p) {
         for (int g = 0; g < 4; g++)
 #pragma unroll
             for (int rb = 0; rb < NB; rb++) acc[g][rb] = f32x4(0.0f);
-        const __bf16 *wx = p.w_ih + (size_t)jr * p.kx + lk;
-        const size_t gx_step = (size_t)d * p.kx;
-        gate_seg<NB, false, 2>(acc, Xh, Xl, p.xs, p.ls, p.lo_begin, wx, gx_step, 0, p.lo_begin, lr, lk);
-        gate_seg<NB, true, 2>(acc, Xh, Xl, p.xs, p.ls, p.lo_begin, wx, gx_step, p.lo_begin, p.lo_end, lr,
-                              lk);
-        gate_seg<NB, false, 2>(acc, Xh, Xl, p.xs, p.ls, p.lo_begin, wx, gx_step, p.lo_end, p.kx, lr, lk);
-        const __bf16 *wh = p.w_hh + (size_t)jr * p.kd + lk;
-        const size_t gh_step = (size_t)d * p.kd;
+        const u32x4 *wx = p.wpack + (size_t)ub * ((p.kx + p.kd) / 32u) * 192u + lane;
+        gate_seg<NB, false, 2>(acc, Xh, Xl, p.xs, p.ls, p.lo_begin, wx, 0, p.lo_begin, lr, lk);
+        gate_seg<NB, true, 2>(acc, Xh, Xl, p.xs, p.ls, p.lo_begin, wx, p.lo_begin, p.lo_end, lr, lk);
+        gate_seg<NB, false, 2>(acc, Xh, Xl, p.xs, p.ls, p.lo_begin, wx, p.lo_end, p.kx, lr, lk);
+        const u32x4 *wh = wx + (p.kx / 32u) * 192u;
         if (p.h_lo)
-            gate_seg<NB, true, 3>(acc, Hh, Hl, p.hs, p.hs, 0, wh, gh_step, 0, p.kd, lr, lk);
+            gate_seg<NB, true, 3>(acc, Hh, Hl, p.hs, p.hs, 0, wh, 0, p.kd, lr, lk);
         else
-            gate_seg<NB, false, 3>(acc, Hh, Hl, p.hs, p.hs, 0, wh, gh_step, 0, p.kd, lr, lk);
+            gate_seg<NB, false, 3>(acc, Hh, Hl, p.hs, p.hs, 0, wh, 0, p.kd, lr, lk);
         if (j >= d) continue;
         const float br = p.b_ih[j] + p.b_hh[j];
         const float bz = p.b_ih[d + j] + p.b_hh[d + j];
@@ -1048,16 +1047,18 @@ __global__ __launch_bounds__(128 * KH) void rnn_gru_ws(GruParams p) {
         lds_load4(p.t + (meta[MS + (lane & (R - 1))][0] >> 1), lds_addr(tt[1]));
     }
     __builtin_amdgcn_sched_barrier(0);
-    {   // this wavefront's fragments, 1 KB each, contiguous (packed by rnn_select)
-        const u32x4 *wf = p.wpack + (size_t)wave * KS * 3 * 64 + lane;
+    {   // this wavefront's fragments, 1 KB each, contiguous (packed by rnn_select;
+        // X steps past kx_steps re-read the last one, unused)
+        const u32x4 *wf = p.wpack + (size_t)wave * (kx_steps + KH) * 192u + lane;
 #pragma unroll
         for (int s = 0; s < KXM; s++)
 #pragma unroll
-            for (int g = 0; g < 3; g++) bx[s][g] = __builtin_bit_cast(bf16x8, wf[(s * 3 + g) * 64]);
+            for (int g = 0; g < 3; g++)
+                bx[s][g] = __builtin_bit_cast(bf16x8, wf[(min((uint32_t)s, kx_steps - 1u) * 3u + g) * 64u]);
 #pragma unroll
         for (int s = 0; s < KH; s++)
 #pragma unroll
-            for (int g = 0; g < 3; g++) bh[s][g] = __builtin_bit_cast(bf16x8, wf[((KXM + s) * 3 + g) * 64]);
+            for (int g = 0; g < 3; g++) bh[s][g] = __builtin_bit_cast(bf16x8, wf[((kx_steps + s) * 3u + g) * 64u]);
     }
     if constexpr (MODE == kWsBf16Dma)
         request_frag(bs0, 0, wave);
@@ -1388,7 +1389,7 @@ struct RnnWork {
     bool clear_winner;    // zero winner[0 .. N) first (memory shared with other calls)
     uint8_t *cand;
     uint32_t *list;       // word 0: winner count; from word 64: the winners, 4 words each
-    uint8_t *wpack;       // packed weights (weight-stationary form), or null
+    uint8_t *wpack;       // the weights in operand-fragment order
 };
 
 // Working memory of the table, grown on demand (nlb_rnn_update).
@@ -1432,8 +1433,7 @@ int scratch_address(int dev, uint8_t **out) {
 }
 
 // The update's working memory carved from `scratch`: winner words of all N
-// nodes, the list, the packed weights (weight-stationary form), the
-// candidate rows.  The winner words are cleared by a fill kernel at the
+// nodes, the list, the packed weights, the candidate rows.  The winner words are cleared by a fill kernel at the
 // start of every call.
 int scratch_work(nlb_table *h, uint64_t pairs, uint32_t srb, size_t wpack_bytes, RnnWork *wk) {
     const size_t winner_bytes = align256((size_t)h->num_nodes * 8u);
@@ -1558,8 +1558,8 @@ static int rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, cons
         gru_layout(p, 16u * nb);
     }
 
-    // weight fragments of the weight-stationary form: 2 kh unit blocks x kWsSteps k-steps x 3 gates, 1 KB each
-    const size_t wpack_bytes = ws ? (size_t)2 * kh * kWsSteps * 3 * 1024 : 0;
+    // packed weight fragments: kd / 16 unit blocks x (kx + kd) / 32 k-steps x 3 gates, 1 KB each
+    const size_t wpack_bytes = (size_t)(p.kd / 16) * ((p.kx + p.kd) / 32) * 3 * 1024;
     RnnWork wk;
     const int rc = use_scratch ? scratch_work(h, pairs, p.srb, wpack_bytes, &wk)
                                : table_work(h, pairs, p.srb, wpack_bytes, &wk);
@@ -1584,10 +1584,13 @@ static int rnn_update(nlb_table *h, const int32_t *src, const int32_t *dst, cons
         hipLaunchKernelGGL(rnn_resolve, dim3((n + kRnnThreads - 1) / kRnnThreads), dim3(kRnnThreads), 0,
                            (hipStream_t)stream, rp);
     SelectParams sp = {src, dst, n, h->num_nodes, wk.winner, list, count,
-                       p.w_ih, p.w_hh, (u32x4 *)wk.wpack, p.d, p.kx, p.kd, p.kx / 32, kWsSteps - kh, kWsSteps,
+                       p.w_ih, p.w_hh, (u32x4 *)wk.wpack, p.d, p.kx, p.kd, p.kx / 32, (p.kx + p.kd) / 32,
                        (uint32_t)(wpack_bytes / 16)};
-    hipLaunchKernelGGL(rnn_select, dim3((unsigned)((pairs + kSelectRows - 1) / kSelectRows)),
-                       dim3(kRnnThreads), 0, (hipStream_t)stream, sp);
+    // (at least enough workgroups for the weight pack at 8 pieces per thread:
+    // workgroups past the pair rows select nothing)
+    const uint64_t sel_blocks = std::max<uint64_t>((pairs + kSelectRows - 1) / kSelectRows,
+                                                   (sp.pieces + 8u * kRnnThreads - 1) / (8u * kRnnThreads));
+    hipLaunchKernelGGL(rnn_select, dim3((unsigned)sel_blocks), dim3(kRnnThreads), 0, (hipStream_t)stream, sp);
     if (ws) {
         const void *kern = nullptr;
         const bool full = ws_mode == kWsBf16Dma && kh == 4 && p.kx == 32u * (kWsSteps - 4) &&
