@@ -65,6 +65,10 @@ def parse():
                     help="capture the K timed steps (each batch's sample, insert and, with --rnn, "
                          "status update, at their own stream offsets) in one HIP graph and time one "
                          "replay of it: the step without host launch costs")
+    ap.add_argument("--serial-encode", action="store_true",
+                    help="compute each retrieval's time encoding inside nlb_sample on the one "
+                         "stream, instead of with nlb_time_encode on a second stream beside the "
+                         "insert that follows")
     ap.add_argument("--streamed-steps", type=int, default=500,
                     help="steps of the host-streamed legs (0: skip them)")
     ap.add_argument("--cpu-plan", action="store_true",
@@ -379,7 +383,35 @@ def cpu_plan(w):
             "wall_seconds": time.perf_counter() - t_start}
 
 
-def streamed_leg(w, table, b0, n, out, nbr, dev, live, host_slots=8, dev_slots=4):
+class EncodeStream:
+    """The time encoding of each retrieval on a second stream.  The table
+    reads (nlb_sample without its tenc output) stay on the current stream;
+    nlb_time_encode runs on this stream after them, beside the insert that
+    follows on the current stream (the encoding reads only the timestamp
+    output and the query times).  join() makes the current stream wait for
+    the encoding before anything reuses the retrieval's buffers."""
+
+    def __init__(self, dev):
+        import torch
+        self.stream = torch.cuda.Stream(device=dev)
+        self.gathered = torch.cuda.Event()
+        self.encoded = torch.cuda.Event()
+
+    def sample_into(self, table, q, tq, o):
+        o = dict(o)
+        tenc = o.pop("tenc")
+        table.sample_into(q, tq, o)
+        self.gathered.record()
+        self.stream.wait_event(self.gathered)
+        table.time_encode_into(o["ts"], tq, tenc, stream=self.stream)
+        self.encoded.record(self.stream)
+
+    def join(self):
+        import torch
+        torch.cuda.current_stream().wait_event(self.encoded)
+
+
+def streamed_leg(w, table, b0, n, out, nbr, dev, live, host_slots=8, dev_slots=4, enc=None):
     """Steps b0 .. b0+n-1 with each batch arriving from host memory: the
     batch (queries [src | dst | neg] and times, the blocked layout) sits in a
     pinned host buffer, a second stream copies it to one of `dev_slots`
@@ -451,8 +483,13 @@ def streamed_leg(w, table, b0, n, out, nbr, dev, live, host_slots=8, dev_slots=4
         q, tq = d_buf[r, 0, :3 * m], d_buf[r, 1, :3 * m]
         o = {kk: v[:3 * m] for kk, v in out.items()}
         o["nbr"] = nbr[:3 * m]
-        table.sample_into(q, tq, o)
-        table.insert(q[:m], q[m:2 * m], tq[:m])
+        if enc is None:
+            table.sample_into(q, tq, o)
+            table.insert(q[:m], q[m:2 * m], tq[:m])
+        else:
+            enc.sample_into(table, q, tq, o)
+            table.insert(q[:m], q[m:2 * m], tq[:m])
+            enc.join()
         ev_free[r].record(compute)
         if live:
             pending.append(ev_copied[k])
@@ -518,7 +555,7 @@ def cpu_rnn_baseline(w, first_batch, budget_s, max_batches=50, max_links=20000):
                       f"each batch's nodes on a compact status array"}
 
 
-def graph_mode(args, w, table, start, W, K, step, update, nbr_all, nodes, ts, setup_s):
+def graph_mode(args, w, table, start, W, K, step, update, nbr_all, nodes, ts, setup_s, enc=None):
     """The K timed steps captured in one HIP graph (every call enqueues
     kernels only; the insert and the status update keep their stream state on
     the device), then one replay timed with events on the replay stream and
@@ -537,6 +574,8 @@ def graph_mode(args, w, table, start, W, K, step, update, nbr_all, nodes, ts, se
             s_, d_, t_, n = step(b, nbr_all[k])
             table.insert(s_, d_, t_)
             update(b, s_, d_, t_)
+            if enc is not None:
+                enc.join()
             qcount.append(n)
     capture_s = time.perf_counter() - t_cap
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -568,6 +607,7 @@ def graph_mode(args, w, table, start, W, K, step, update, nbr_all, nodes, ts, se
         "capture_s": capture_s, "setup_s": setup_s,
         "value_note": "the K timed steps captured in one HIP graph and replayed once"
                       + (" (with the status update)" if args.rnn else ""),
+        "encode_stream": enc is not None,
     }
     print(json.dumps(res), flush=True)
 
@@ -635,6 +675,7 @@ def main():
     Qmax = 3 * w.batch
     out = table.alloc_outputs(Qmax, want=("eid", "ts", "tenc", "efeat", "nfeat", "self"))
     nbr_all = torch.empty((K, Qmax, w.s), dtype=torch.int32, device=dev)
+    enc = None if args.aggregate or args.serial_encode else EncodeStream(dev)
     agg_w = agg_z = None
     if args.aggregate:
         agg_w = {k: (torch.from_numpy(v.view(np.int16)) if v.dtype == np.uint16 else
@@ -663,7 +704,10 @@ def main():
             return s_, d_, t_, n
         o = {k: v[:n] for k, v in out.items()}
         o["nbr"] = nbr_out[:n]
-        table.sample_into(q, tq, o)
+        if enc is not None:
+            enc.sample_into(table, q, tq, o)
+        else:
+            table.sample_into(q, tq, o)
         return s_, d_, t_, n
 
     def update(b, s_, d_, t_):
@@ -674,11 +718,13 @@ def main():
         s_, d_, t_, _ = step(start + k, nbr_all[0])
         table.insert(s_, d_, t_)
         update(start + k, s_, d_, t_)
+        if enc is not None:
+            enc.join()
     torch.cuda.synchronize()
 
     print(f"bench: warm-up done; timing {K} steps", file=sys.stderr, flush=True)
     if args.graph:
-        return graph_mode(args, w, table, start, W, K, step, update, nbr_all, nodes, ts, setup_s)
+        return graph_mode(args, w, table, start, W, K, step, update, nbr_all, nodes, ts, setup_s, enc)
     # HIP events on the library's stream time each phase.  A recorded event
     # costs the stream a few microseconds, so a step records only those it
     # needs: its start (which also ends the previous step's last phase), the
@@ -690,6 +736,10 @@ def main():
     e_sample = [mk() for _ in range(K)]
     e_hop2 = [mk() for _ in range(K)] if hop2_out is not None else None
     e_ins = [mk() for _ in range(K)] if status is not None else None
+    # with the encoding on its own stream: its end, and the end of the
+    # current stream's own work before it waits for the encoding
+    e_enc = [mk() for _ in range(K)] if enc is not None else None
+    e_main = [mk() for _ in range(K)] if enc is not None else None
     qcount = []
     import gc
     gc.disable()
@@ -699,6 +749,8 @@ def main():
         e_start[k].record()
         s_, d_, t_, n = step(b, nbr_all[k])
         e_sample[k].record()
+        if enc is not None:
+            e_enc[k].record(enc.stream)
         if hop2_out is not None:
             _, _, _, _, tq = synth.batch_views(w, nodes, ts, b)
             o2 = {kk: v[:n * w.s] for kk, v in hop2_out.items()}
@@ -708,6 +760,9 @@ def main():
         if status is not None:
             e_ins[k].record()
             update(b, s_, d_, t_)
+        if enc is not None:
+            e_main[k].record()
+            enc.join()
         qcount.append(n)
     e_start[K].record()
     torch.cuda.synchronize()
@@ -717,12 +772,14 @@ def main():
 
     def span(a, b_):
         return np.array([a[k].elapsed_time(b_[k]) for k in range(K)])
+    step_end = e_main if e_main is not None else e_start[1:]
     ins_from = e_hop2 if e_hop2 is not None else e_sample
-    ins_to = e_ins if e_ins is not None else e_start[1:]
-    sample_ms = span(e_start, e_sample)
+    ins_to = e_ins if e_ins is not None else step_end
+    # the retrieval ends with its time encoding (on its own stream if split)
+    sample_ms = span(e_start, e_enc if e_enc is not None else e_sample)
     hop2_ms = span(e_sample, e_hop2) if e_hop2 is not None else np.zeros(K)
     insert_ms = span(ins_from, ins_to)
-    rnn_ms = span(e_ins, e_start[1:]) if e_ins is not None else np.zeros(K)
+    rnn_ms = span(e_ins, step_end) if e_ins is not None else np.zeros(K)
     links = sum(n // 3 for n in qcount)
     queries = sum(qcount)
     if agg_w is not None:
@@ -771,11 +828,14 @@ def main():
                                      "of its launches, scaled by a copy kernel)",
                      "traffic_rate_gbps": (traffic / (sample_ms.mean() * 1e-3) / 1e9
                                            if traffic else None),
-                     "kernel": "nlb_sample: sample_gather (+ tenc_stream on large launches "
-                               "that write timestamps)",
+                     "kernel": ("nlb_sample (sample_gather) + nlb_time_encode (tenc_stream, on a "
+                                "second stream beside the insert)" if enc is not None else
+                                "nlb_sample: sample_gather (+ tenc_stream on large launches "
+                                "that write timestamps)"),
                      "bytes_per_launch": s_bytes / K,
                      "bytes_per_query_full_occupancy": full_bytes_per_query},
         "setup_s": setup_s,
+        "encode_stream": enc is not None,
     }
     if agg_w is not None:
         fl = aggregate_flops(w, valid, queries, heads=args.heads)
@@ -830,8 +890,9 @@ def main():
         if n_s > 0:
             print(f"bench: host-streamed legs, {n_s} steps each", file=sys.stderr, flush=True)
             res["streamed"] = {
-                "live_generator": streamed_leg(w, table, b0, n_s, out, nbr_all[0], dev, live=True),
-                "staged_pinned": streamed_leg(w, table, b0 + n_s, n_s, out, nbr_all[0], dev, live=False),
+                "live_generator": streamed_leg(w, table, b0, n_s, out, nbr_all[0], dev, live=True, enc=enc),
+                "staged_pinned": streamed_leg(w, table, b0 + n_s, n_s, out, nbr_all[0], dev, live=False,
+                                              enc=enc),
                 "note": "same step (nlb_sample + nlb_insert_batch) with each batch copied host to "
                         "device (pinned buffers, second stream, event-ordered) instead of resident "
                         "in HBM; not the headline value"}

@@ -193,6 +193,24 @@ int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t n
 int nlb_sample_hop2(nlb_table *h, const int32_t *hop1_nbr, const uint32_t *tq, uint32_t nq,
                     const nlb_sample_out *out, void *stream);
 
+/* Time encoding (App. C) of an nlb_sample answer from its timestamp output:
+ *   tenc[i][a][k] = cos(fmaf(w_k, (float)(tq[i] - ts[i*s + a]), b_k)),
+ *   0 where ts[i*s + a] == 0xFFFFFFFF (an invalid slot),
+ * the values nlb_sample writes to its own tenc output, to the same bits.
+ * With it a caller splits a retrieval into its table reads (nlb_sample with
+ * out->tenc NULL and out->ts set) and the encoding, and runs the encoding on
+ * a second stream, ordered after the sample by an event the caller records:
+ * the encoding reads neither the tables nor the feature rows, so it may run
+ * beside the next nlb_insert_batch.  ts: device uint32 [nq][s] (an nlb_sample
+ * ts output); tq: the device array of the nq query times of that call; tenc:
+ * device fp32 [nq][s][d_time].  All three are read or written during the
+ * call's kernels only and must be 4-byte aligned (16-byte aligned output
+ * and d_time % 4 == 0 take the vector form).  nq == 0 is a no-op.
+ * Errors: NLB_EINVAL (NULL table or array with nq > 0, a table without a time
+ * encoding, misaligned arrays), NLB_EDEVICE.  Graph capture: as nlb_sample. */
+int nlb_time_encode(nlb_table *h, const uint32_t *ts, const uint32_t *tq, uint32_t nq, float *tenc,
+                    void *stream);
+
 /* Attention aggregation of eq. (4) (Sec. 4.4), forward:
  *   Z_u = MLP_out(r_u, sum_i alpha_i MLP_in(r_v, e, t')),
  *   {alpha_i} = softmax({w^T MLP_in(r_v, e, t')}) over the valid slots of S_u^t,

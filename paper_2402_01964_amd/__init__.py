@@ -23,7 +23,7 @@ KEY_EDGE, KEY_NODE = 0, 1
 MAX_SLOTS = 1024
 
 # Symbols declared in include/nlb.h.
-ABI_SYMBOLS = ("nlb_create", "nlb_insert_batch", "nlb_sample", "nlb_sample_hop2", "nlb_aggregate",
+ABI_SYMBOLS = ("nlb_create", "nlb_insert_batch", "nlb_sample", "nlb_sample_hop2", "nlb_time_encode", "nlb_aggregate",
                "nlb_rnn_update", "nlb_rnn_update_noalloc", "nlb_destroy", "nlb_get_info", "nlb_export", "nlb_status",
                "nlb_strerror")
 AGG_HIDDEN = 64
@@ -103,6 +103,8 @@ def load_library(path: str | None = None):
     lib.nlb_sample.restype = I
     lib.nlb_sample_hop2.argtypes = [P, P, P, U32, ctypes.POINTER(_SampleOut), P]
     lib.nlb_sample_hop2.restype = I
+    lib.nlb_time_encode.argtypes = [P, P, P, U32, P, P]
+    lib.nlb_time_encode.restype = I
     lib.nlb_aggregate.argtypes = [P, P, P, U32, ctypes.POINTER(_AggWeights), P, P]
     lib.nlb_aggregate.restype = I
     lib.nlb_rnn_update.argtypes = [P, P, P, P, U32, U64, ctypes.POINTER(_GruWeights), P, P]
@@ -250,6 +252,21 @@ class Table:
                                          _dev_ptr(tq, 4, "tq"), nq, ctypes.byref(so),
                                          _stream_ptr(stream)), "nlb_sample_hop2")
         return out
+
+    def time_encode_into(self, ts, tq, tenc, stream=None):
+        """App. C time encoding of a first-hop answer from its timestamp
+        output ``ts`` [nq, s] and query times ``tq`` [nq] into ``tenc``
+        [nq, s, d_time]: the values ``sample_into`` writes to its own tenc
+        output.  The caller orders it after the sample that wrote ``ts``."""
+        nq = int(tq.numel())
+        if ts.numel() != nq * self.s:
+            raise ValueError("ts must hold s entries per query")
+        if tenc.numel() != nq * self.s * self.d_time:
+            raise ValueError("tenc must hold s * d_time values per query")
+        _check(self._lib.nlb_time_encode(self._h, _dev_ptr(ts, 4, "ts"), _dev_ptr(tq, 4, "tq"), nq,
+                                         _dev_ptr(tenc, 4, "tenc"), _stream_ptr(stream)),
+               "nlb_time_encode")
+        return tenc
 
     def sample_hop2(self, hop1_nbr, tq, want=("nbr", "eid", "ts", "tenc", "efeat", "nfeat", "self"),
                     stream=None):

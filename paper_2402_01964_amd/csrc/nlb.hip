@@ -459,17 +459,20 @@ __global__ __launch_bounds__(kTileThreads) void sample_gather(SampleParams p) {
                                 tile_nodes, p.o_self + q0 * p.nrb, tid);
 }
 
-// Time encoding of a large first-hop launch as its own stream, after
-// sample_gather has written the timestamp output.  A tile-looping kernel's
-// write streams reach about 5 TB/s on gfx950, short workgroups with one
-// 16-byte store per thread the fill rate (~6.9 TB/s); here each thread of a
-// 128-thread workgroup computes two float4 outputs (kTencPerThread) whose
-// timestamp and query-time reads are issued together, so one read latency
-// covers two stores.  Slot row j = f / units belongs to query j / s;
-// ts[j] = 0xFFFFFFFF marks an invalid slot (zeros).  Both divisions are
-// nlb_div (exact for every 32-bit numerator and divisor, 1 included).
+// Time encoding as its own stream, computed from an answer's timestamp output
+// (the large first-hop launches of nlb_sample, and nlb_time_encode).  A
+// tile-looping kernel's write streams reach about 5 TB/s on gfx950, short
+// workgroups with one 16-byte store per thread the fill rate (~6.9 TB/s);
+// here each thread of a 128-thread workgroup computes two outputs of V
+// floats (kTencPerThread) whose timestamp and query-time reads are issued
+// together, so one read latency covers two stores.  Slot row j = f / units
+// belongs to query j / s; ts[j] = 0xFFFFFFFF marks an invalid slot (zeros).
+// Both divisions are nlb_div (exact for every 32-bit numerator and divisor,
+// 1 included).  V = 4 needs d_time % 4 == 0 and 16-byte aligned w, b and
+// output; V = 1 takes any width and 4-byte alignment.
 constexpr uint32_t kTencThreads = 128, kTencPerThread = 2;
 
+template <uint32_t V>
 __global__ __launch_bounds__(kTencThreads) void tenc_stream(const uint32_t *ts, const uint32_t *tq, uint64_t s_M,
                                                             uint32_t units, uint64_t u_M, uint32_t total,
                                                             const float *w, const float *b, float *out) {
@@ -485,17 +488,23 @@ __global__ __launch_bounds__(kTencThreads) void tenc_stream(const uint32_t *ts, 
     }
 #pragma unroll
     for (uint32_t k = 0; k < kTencPerThread; k++) {
-        f32x4 r = f32x4(0.0f);
-        if (t[k] != 0xFFFFFFFFu) {
-            const float dt = (float)(q[k] - t[k]);
-            const f32x4 w4 = *(const f32x4 *)(w + 4 * cc[k]);
-            const f32x4 b4 = *(const f32x4 *)(b + 4 * cc[k]);
-            r.x = cos_fp32(__builtin_fmaf(w4.x, dt, b4.x));
-            r.y = cos_fp32(__builtin_fmaf(w4.y, dt, b4.y));
-            r.z = cos_fp32(__builtin_fmaf(w4.z, dt, b4.z));
-            r.w = cos_fp32(__builtin_fmaf(w4.w, dt, b4.w));
+        if constexpr (V == 4) {
+            f32x4 r = f32x4(0.0f);
+            if (t[k] != 0xFFFFFFFFu) {
+                const float dt = (float)(q[k] - t[k]);
+                const f32x4 w4 = *(const f32x4 *)(w + 4 * cc[k]);
+                const f32x4 b4 = *(const f32x4 *)(b + 4 * cc[k]);
+                r.x = cos_fp32(__builtin_fmaf(w4.x, dt, b4.x));
+                r.y = cos_fp32(__builtin_fmaf(w4.y, dt, b4.y));
+                r.z = cos_fp32(__builtin_fmaf(w4.z, dt, b4.z));
+                r.w = cos_fp32(__builtin_fmaf(w4.w, dt, b4.w));
+            }
+            if (ff[k] < total) __builtin_nontemporal_store(r, (f32x4 *)(out + (size_t)ff[k] * 4));
+        } else {
+            float r = 0.0f;
+            if (t[k] != 0xFFFFFFFFu) r = cos_fp32(__builtin_fmaf(w[cc[k]], (float)(q[k] - t[k]), b[cc[k]]));
+            if (ff[k] < total) __builtin_nontemporal_store(r, out + ff[k]);
         }
-        if (ff[k] < total) __builtin_nontemporal_store(r, (f32x4 *)(out + (size_t)ff[k] * 4));
     }
 }
 
@@ -551,6 +560,32 @@ uint32_t tile_queries(uint32_t s, uint32_t nq) {
     if (want >= 32) want = (want + 15) / 16 * 16;
     if (want < 1) want = 1;
     return want < cap ? want : cap;
+}
+
+// The time encoding of nq answered queries from their timestamp output
+// [nq][s] into tenc [nq][s][d_time], in launches of fewer than 2^31 output
+// units (whole queries each; s * d_time < 2^31 by the limits of nlb_create).
+bool launch_tenc(const nlb_table *h, const uint32_t *ts, const uint32_t *tq, uint32_t nq, float *tenc,
+                 bool vec4, hipStream_t st) {
+    const uint32_t units = vec4 ? h->d_time / 4 : h->d_time;
+    const uint64_t per_q = (uint64_t)h->s * units;
+    const uint64_t chunk = ((1ull << 31) - 1) / per_q;
+    const uint64_t sM = nlb_div_magic(h->s), uM = nlb_div_magic(units);
+    constexpr uint32_t kPerBlock = kTencThreads * kTencPerThread;
+    for (uint64_t q0 = 0; q0 < nq; q0 += chunk) {
+        const uint64_t n = nq - q0 < chunk ? nq - q0 : chunk;
+        const uint32_t total = (uint32_t)(n * per_q);
+        const dim3 grid((total + kPerBlock - 1) / kPerBlock);
+        const uint32_t *t = ts + q0 * h->s;
+        float *o = tenc + q0 * h->s * h->d_time;
+        if (vec4)
+            hipLaunchKernelGGL(tenc_stream<4>, grid, dim3(kTencThreads), 0, st, t, tq + q0, sM, units, uM,
+                               total, h->w, h->b, o);
+        else
+            hipLaunchKernelGGL(tenc_stream<1>, grid, dim3(kTencThreads), 0, st, t, tq + q0, sM, units, uM,
+                               total, h->w, h->b, o);
+    }
+    return hipGetLastError() == hipSuccess;
 }
 
 }  // namespace
@@ -762,23 +797,14 @@ static int launch_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, 
     // Large first-hop launches that also write timestamps take the time
     // encoding out of sample_gather into tenc_stream.
     const uint64_t tenc_total = (uint64_t)nq * h->s * p.tenc_units;
-    const bool split = !hop2 && out->tenc && out->ts && vec4 && tenc_total >= kTencStreamMin &&
-                       tenc_total < (1ull << 32);
+    const bool split = !hop2 && out->tenc && out->ts && vec4 && tenc_total >= kTencStreamMin;
     if (split) p.o_tenc = nullptr;
     if (hop2)
         hipLaunchKernelGGL(sample_gather<true>, grid, dim3(kTileThreads), 0, st, p);
     else
         hipLaunchKernelGGL(sample_gather<false>, grid, dim3(kTileThreads), 0, st, p);
-    if (split) {
-        const uint64_t sM = nlb_div_magic(h->s), uM = nlb_div_magic(p.tenc_units);
-        hipLaunchKernelGGL(tenc_stream,
-                           dim3((unsigned)((tenc_total + kTencThreads * kTencPerThread - 1) /
-                                           (kTencThreads * kTencPerThread))),
-                           dim3(kTencThreads), 0, st,
-                           (const uint32_t *)out->ts, tq, sM, p.tenc_units, uM, (uint32_t)tenc_total, h->w,
-                           h->b, out->tenc);
-    }
     if (hipGetLastError() != hipSuccess) return NLB_EDEVICE;
+    if (split && !launch_tenc(h, out->ts, tq, nq, out->tenc, true, st)) return NLB_EDEVICE;
     return NLB_OK;
 }
 
@@ -788,6 +814,19 @@ int nlb_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, uint32_t n
     if (nq == 0) return NLB_OK;
     if (!node || !tq) return NLB_EINVAL;
     return launch_sample(h, node, tq, nq, 0, out, stream);
+}
+
+int nlb_time_encode(nlb_table *h, const uint32_t *ts, const uint32_t *tq, uint32_t nq, float *tenc,
+                    void *stream) {
+    if (!h) return NLB_EINVAL;
+    if (nq == 0) return NLB_OK;
+    if (!ts || !tq || !tenc || h->d_time == 0) return NLB_EINVAL;
+    if ((uintptr_t)ts % 4 || (uintptr_t)tq % 4 || (uintptr_t)tenc % 4) return NLB_EINVAL;
+    DeviceGuard guard(h->device);
+    if (!guard.ok()) return NLB_EDEVICE;
+    const bool vec4 = h->d_time % 4 == 0 && (uintptr_t)tenc % 16 == 0 && (uintptr_t)h->w % 16 == 0 &&
+                      (uintptr_t)h->b % 16 == 0;
+    return launch_tenc(h, ts, tq, nq, tenc, vec4, (hipStream_t)stream) ? NLB_OK : NLB_EDEVICE;
 }
 
 int nlb_sample_hop2(nlb_table *h, const int32_t *hop1_nbr, const uint32_t *tq, uint32_t nq,
