@@ -69,6 +69,9 @@ def parse():
                     help="compute each retrieval's time encoding inside nlb_sample on the one "
                          "stream, instead of with nlb_time_encode on a second stream beside the "
                          "insert that follows")
+    ap.add_argument("--encode-depth", type=int, default=2,
+                    help="sets of retrieval output buffers the steps take turns over: with 2, a "
+                         "batch's time encoding also runs beside the next batch's table reads")
     ap.add_argument("--streamed-steps", type=int, default=500,
                     help="steps of the host-streamed legs (0: skip them)")
     ap.add_argument("--cpu-plan", action="store_true",
@@ -386,16 +389,26 @@ def cpu_plan(w):
 class EncodeStream:
     """The time encoding of each retrieval on a second stream.  The table
     reads (nlb_sample without its tenc output) stay on the current stream;
-    nlb_time_encode runs on this stream after them, beside the insert that
-    follows on the current stream (the encoding reads only the timestamp
-    output and the query times).  join() makes the current stream wait for
-    the encoding before anything reuses the retrieval's buffers."""
+    nlb_time_encode runs on this stream after them, beside what follows on
+    the current stream (the encoding reads only the timestamp output and the
+    query times).  Retrievals take turns over ``depth`` sets of output
+    buffers: join() makes the current stream wait for the encoding that last
+    used the set the next retrieval will write, so with two sets a batch's
+    encoding also runs beside the next batch's table reads."""
 
-    def __init__(self, dev):
+    def __init__(self, dev, depth=1):
         import torch
         self.stream = torch.cuda.Stream(device=dev)
+        self.depth = depth
         self.gathered = torch.cuda.Event()
-        self.encoded = torch.cuda.Event()
+        self.encoded = [torch.cuda.Event() for _ in range(depth)]
+        self.used = [False] * depth
+        self.count = 0
+
+    @property
+    def slot(self):
+        """The output set the next retrieval writes."""
+        return self.count % self.depth
 
     def sample_into(self, table, q, tq, o):
         o = dict(o)
@@ -404,11 +417,26 @@ class EncodeStream:
         self.gathered.record()
         self.stream.wait_event(self.gathered)
         table.time_encode_into(o["ts"], tq, tenc, stream=self.stream)
-        self.encoded.record(self.stream)
+        self.encoded[self.slot].record(self.stream)
+        self.used[self.slot] = True
+        self.count += 1
 
     def join(self):
         import torch
-        torch.cuda.current_stream().wait_event(self.encoded)
+        if self.used[self.slot]:
+            torch.cuda.current_stream().wait_event(self.encoded[self.slot])
+
+    def forget(self):
+        """Drop the record of earlier encodings once the device has finished
+        them (after a synchronisation), so that no later join waits on an
+        event recorded outside a graph being captured."""
+        self.used = [False] * self.depth
+
+    def join_all(self):
+        import torch
+        for k in range(self.depth):
+            if self.used[k]:
+                torch.cuda.current_stream().wait_event(self.encoded[k])
 
 
 def streamed_leg(w, table, b0, n, out, nbr, dev, live, host_slots=8, dev_slots=4, enc=None):
@@ -489,7 +517,7 @@ def streamed_leg(w, table, b0, n, out, nbr, dev, live, host_slots=8, dev_slots=4
         else:
             enc.sample_into(table, q, tq, o)
             table.insert(q[:m], q[m:2 * m], tq[:m])
-            enc.join()
+            enc.join_all()
         ev_free[r].record(compute)
         if live:
             pending.append(ev_copied[k])
@@ -567,6 +595,9 @@ def graph_mode(args, w, table, start, W, K, step, update, nbr_all, nodes, ts, se
     import synth
     graph = torch.cuda.CUDAGraph()
     qcount = []
+    torch.cuda.synchronize()
+    if enc is not None:
+        enc.forget()
     t_cap = time.perf_counter()
     with torch.cuda.graph(graph):
         for k in range(K):
@@ -577,6 +608,8 @@ def graph_mode(args, w, table, start, W, K, step, update, nbr_all, nodes, ts, se
             if enc is not None:
                 enc.join()
             qcount.append(n)
+        if enc is not None:
+            enc.join_all()
     capture_s = time.perf_counter() - t_cap
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -608,6 +641,7 @@ def graph_mode(args, w, table, start, W, K, step, update, nbr_all, nodes, ts, se
         "value_note": "the K timed steps captured in one HIP graph and replayed once"
                       + (" (with the status update)" if args.rnn else ""),
         "encode_stream": enc is not None,
+        "encode_depth": enc.depth if enc is not None else 0,
     }
     print(json.dumps(res), flush=True)
 
@@ -675,7 +709,9 @@ def main():
     Qmax = 3 * w.batch
     out = table.alloc_outputs(Qmax, want=("eid", "ts", "tenc", "efeat", "nfeat", "self"))
     nbr_all = torch.empty((K, Qmax, w.s), dtype=torch.int32, device=dev)
-    enc = None if args.aggregate or args.serial_encode else EncodeStream(dev)
+    enc = None if args.aggregate or args.serial_encode else EncodeStream(dev, args.encode_depth)
+    outs = [out] + [table.alloc_outputs(Qmax, want=("eid", "ts", "tenc", "efeat", "nfeat", "self"))
+                    for _ in range(1, enc.depth if enc is not None else 1)]
     agg_w = agg_z = None
     if args.aggregate:
         agg_w = {k: (torch.from_numpy(v.view(np.int16)) if v.dtype == np.uint16 else
@@ -702,7 +738,7 @@ def main():
         if agg_w is not None:
             table.aggregate(q, tq, agg_w, out=agg_z[:n], heads=args.heads)
             return s_, d_, t_, n
-        o = {k: v[:n] for k, v in out.items()}
+        o = {k: v[:n] for k, v in outs[enc.slot if enc is not None else 0].items()}
         o["nbr"] = nbr_out[:n]
         if enc is not None:
             enc.sample_into(table, q, tq, o)
@@ -764,6 +800,8 @@ def main():
             e_main[k].record()
             enc.join()
         qcount.append(n)
+    if enc is not None:
+        enc.join_all()
     e_start[K].record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
@@ -795,7 +833,13 @@ def main():
         replay.close()
     valid = int(sum(int((nbr_all[k, :qcount[k]] >= 0).sum()) for k in range(K)))
     s_bytes = sum(sample_bytes(w, 0, n) for n in qcount) + valid * (w.row_bytes("edge") + w.row_bytes("node"))
-    achieved = s_bytes / (sample_ms.sum() * 1e-3) / 1e9
+    # With two output sets a batch's encoding overlaps the next batch's table
+    # reads, so a retrieval has no span of its own: its rate is then taken
+    # over the event-timed span of all K steps, inserts included (a lower
+    # bound on the retrieval's own rate).
+    pipelined = enc is not None and enc.depth > 1
+    ret_s = (e_start[0].elapsed_time(e_start[K]) if pipelined else sample_ms.sum()) * 1e-3
+    achieved = s_bytes / ret_s / 1e9
     full_bytes_per_query = sample_bytes(w, w.s, 1)
     traffic = measured_traffic(w)
     res = {
@@ -826,8 +870,10 @@ def main():
                      "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic,
                      "traffic_unit": "bytes per nlb_sample call (rocprofv3 FETCH_SIZE + WRITE_SIZE "
                                      "of its launches, scaled by a copy kernel)",
-                     "traffic_rate_gbps": (traffic / (sample_ms.mean() * 1e-3) / 1e9
-                                           if traffic else None),
+                     "traffic_rate_gbps": (traffic / (ret_s / K) / 1e9 if traffic else None),
+                     "time_basis": ("event-timed span of the K steps (the retrievals overlap each "
+                                    "other and the inserts)" if pipelined else
+                                    "summed event-timed spans of the K retrievals"),
                      "kernel": ("nlb_sample (sample_gather) + nlb_time_encode (tenc_stream, on a "
                                 "second stream beside the insert)" if enc is not None else
                                 "nlb_sample: sample_gather (+ tenc_stream on large launches "
@@ -836,6 +882,7 @@ def main():
                      "bytes_per_query_full_occupancy": full_bytes_per_query},
         "setup_s": setup_s,
         "encode_stream": enc is not None,
+        "encode_depth": enc.depth if enc is not None else 0,
     }
     if agg_w is not None:
         fl = aggregate_flops(w, valid, queries, heads=args.heads)
