@@ -18,17 +18,21 @@ from tests.gpu_helpers import compare_sample, make_gpu_table, make_oracle, to_de
 
 pytestmark = pytest.mark.gpu
 
-# (workload whose stream is used, d_time, output at a 4-byte offset)
-CASES = [(4, 100, False), (4, 97, False), (1, 100, True), (5, 128, False)]
+# (workload whose stream is used, d_time, output at a 4-byte offset, s or
+# None for the workload's own); s = 1 with one float4 or one float per slot
+# makes both divisors of the kernel 1
+CASES = [(4, 100, False, None), (4, 97, False, None), (1, 100, True, None), (5, 128, False, None),
+         (4, 4, False, 1), (4, 1, True, 1)]
 
 
-@pytest.mark.parametrize("case", CASES, ids=lambda c: f"w{c[0]}-d{c[1]}" + ("-offset" if c[2] else ""))
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"w{c[0]}-d{c[1]}" + ("-offset" if c[2] else "")
+                         + (f"-s{c[3]}" if c[3] else ""))
 def test_time_encode_matches_sample_and_oracle(case):
     import torch
-    k, d_time, offset = case
+    k, d_time, offset, s_slots = case
     base = synth.workload(k)
     w = dataclasses.replace(synth.scaled(base, 20 * base.batch, num_nodes=min(base.num_nodes, 50000)),
-                            d_time=d_time)
+                            d_time=d_time, s=s_slots or base.s)
     src, dst, t, _ = synth.host_links(w)
     fw, fb = synth.time_params(w)
     g = make_gpu_table(w)
