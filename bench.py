@@ -30,6 +30,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
+# Batches whose time encoding is at least this large run it on a second
+# stream (nlb_time_encode) beside the insert (and status update); smaller
+# ones keep nlb_sample's one-stream form.
+ENCODE_STREAM_MIN_BYTES = 256 << 20
 
 
 def parse():
@@ -68,8 +72,14 @@ def parse():
     ap.add_argument("--serial-encode", action="store_true",
                     help="compute each retrieval's time encoding inside nlb_sample on the one "
                          "stream, instead of with nlb_time_encode on a second stream beside the "
-                         "insert that follows")
-    ap.add_argument("--encode-depth", type=int, default=2,
+                         "insert (and status update) that follow")
+    ap.add_argument("--encode-stream", action="store_true",
+                    help="use the second stream for the time encoding also when a batch's "
+                         "encoding is under 256 MiB or with --hop2 (by default such steps keep "
+                         "the one-stream form: for small batches the extra launch and events cost "
+                         "more than the overlap saves, and the second hop's table reads and the "
+                         "encoding slow each other down)")
+    ap.add_argument("--encode-depth", type=int, default=1,
                     help="sets of retrieval output buffers the steps take turns over: with 2, a "
                          "batch's time encoding also runs beside the next batch's table reads")
     ap.add_argument("--streamed-steps", type=int, default=500,
@@ -709,7 +719,12 @@ def main():
     Qmax = 3 * w.batch
     out = table.alloc_outputs(Qmax, want=("eid", "ts", "tenc", "efeat", "nfeat", "self"))
     nbr_all = torch.empty((K, Qmax, w.s), dtype=torch.int32, device=dev)
-    enc = None if args.aggregate or args.serial_encode else EncodeStream(dev, args.encode_depth)
+    enc_bytes = 4 * Qmax * w.s * w.d_time        # time encoding of one batch's retrieval
+    # (not with a second hop: that launch's random table reads and the
+    # encoding's write stream slow each other down more than they overlap)
+    use_enc = args.encode_stream or (enc_bytes >= ENCODE_STREAM_MIN_BYTES and not args.hop2)
+    enc = (EncodeStream(dev, args.encode_depth)
+           if use_enc and not (args.aggregate or args.serial_encode) else None)
     outs = [out] + [table.alloc_outputs(Qmax, want=("eid", "ts", "tenc", "efeat", "nfeat", "self"))
                     for _ in range(1, enc.depth if enc is not None else 1)]
     agg_w = agg_z = None
@@ -930,6 +945,12 @@ def main():
                       "ms_avg": float(rnn_ms.mean()), "updates_per_batch": winners / K,
                       "roofline": dict(binding_roofline(fl, rb, t_s), flops_per_launch=fl / K,
                                        bytes_per_launch=rb / K)}
+        if enc is not None:
+            res["rnn"]["timing_note"] = (
+                "the update is timed from the end of the insert while the time encoding runs "
+                "beside it on its own stream: its GRU pass waits for the encoding's workgroups to "
+                "leave the CUs, so ms_avg and the roofline understate the update; --serial-encode "
+                "times it alone")
         res["value_note"] = "value includes the node-status updates (--rnn)"
     if agg_w is None and hop2_out is None and status is None and args.streamed_steps > 0:
         b0 = start + W + K
