@@ -33,7 +33,7 @@ PEAK_HBM_GBPS = 8000.0
 # Batches whose time encoding is at least this large run it on a second
 # stream (nlb_time_encode) beside the insert (and status update); smaller
 # ones keep nlb_sample's one-stream form.
-ENCODE_STREAM_MIN_BYTES = 256 << 20
+ENCODE_STREAM_MIN_BYTES = 1 << 30
 
 
 def parse():
@@ -75,7 +75,7 @@ def parse():
                          "insert (and status update) that follow")
     ap.add_argument("--encode-stream", action="store_true",
                     help="use the second stream for the time encoding also when a batch's "
-                         "encoding is under 256 MiB or with --hop2 (by default such steps keep "
+                         "encoding is under 1 GiB or with --hop2 (by default such steps keep "
                          "the one-stream form: for small batches the extra launch and events cost "
                          "more than the overlap saves, and the second hop's table reads and the "
                          "encoding slow each other down)")
