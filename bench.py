@@ -141,14 +141,14 @@ def measured_traffic(w, call="nlb_sample"):
 
 def aggregate_kernel(w, queries, cus, heads=1):
     """The eq. (4) kernel a launch of `queries` takes on this workload's
-    shapes (the library's own choice, restated for the record): with one
-    head, the packed form for tables of at most 16 slots when its query
-    groups hold at least 8 queries, else the per-query form, which also takes
-    two heads; more heads take the tiled form."""
+    shapes (the library's own choice, restated for the record): with one or
+    two heads, the packed form for tables of at most 16 slots when its query
+    groups hold at least 8 queries, else the per-query form; more heads take
+    the tiled form."""
     if heads > 2:
         return "aggregate_fused"
     gq = min(16, max(1, -(-queries // (cus * 8))))
-    return "aggregate_packed" if heads == 1 and w.s <= 16 and gq >= 8 else "aggregate_rows"
+    return "aggregate_packed" if w.s <= 16 and gq >= 8 else "aggregate_rows"
 
 
 def hop2_bytes(w, hop1_valid, queries):
@@ -905,7 +905,8 @@ def main():
         t_s = sample_ms.sum() * 1e-3
         cus = torch.cuda.get_device_properties(0).multi_processor_count
         kname = aggregate_kernel(w, 3 * w.batch, cus, args.heads)
-        agg_traffic = measured_traffic(w, "nlb_aggregate") if kname == "aggregate_packed" else None
+        agg_traffic = (measured_traffic(w, "nlb_aggregate")
+                       if kname == "aggregate_packed" and args.heads == 1 else None)
         res["roofline"] = dict(binding_roofline(fl, ab, t_s), traffic=agg_traffic,
                                traffic_unit="bytes per nlb_aggregate launch (rocprofv3 FETCH_SIZE "
                                             "+ WRITE_SIZE, reads scaled by a random-gather kernel)",

@@ -240,9 +240,8 @@ int nlb_time_encode(nlb_table *h, const uint32_t *ts, const uint32_t *tq, uint32
  * H outputs are split into A consecutive slices of H / A; head a scores a
  * slot with w[slice a] . MLP_in(...)[slice a], takes its own softmax over the
  * valid slots and fills slice a of the aggregate.  A = 1 is the formula
- * above.  One head runs in every kernel form, two in the per-query and
- * tiled forms, four and eight in the tiled form (tables of at most 64
- * slots); any other count is NLB_EINVAL.
+ * above.  One or two heads run in every kernel form, four and eight in the
+ * tiled form (tables of at most 64 slots); any other count is NLB_EINVAL.
  * z is device fp32 [nq][H].  Tables with s > 64 are supported for the input
  * shapes the per-query kernel is built for and rejected (NLB_EINVAL) for
  * others: a time encoding of 97 to 128 dimensions with 16-byte-aligned bf16

@@ -1124,7 +1124,10 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
 // product sums each row into its own query (the columns are rescaled first
 // when a query's maximum grows).  At the group's end every column is divided
 // by its sum of exponentials and MLP_out runs as in aggregate_rows.  Results
-// differ from aggregate_rows by summation order only.
+// differ from aggregate_rows by summation order only.  With two heads every
+// row has one logit per head (v_a . a1 over all 64 units of layer 1), and
+// each head keeps its own M_q, sum of exponentials and running aggregates;
+// MLP_out takes head a's slice of w2's outputs from head a's aggregates.
 constexpr uint32_t kPackMaxS = 16;                    // slots per node at most
 constexpr uint32_t kPackMinGroup = 8;                 // queries per group at least
 constexpr uint32_t kScanJ = kPackMaxS / 4;           // slots per lane in the group scan
@@ -1145,9 +1148,9 @@ struct PackRow {
     uint32_t q4;
 };
 
-// LDS layout: weights and time-encoding vectors as RowsLayout, then each
-// wavefront's list.
-template <int K1S, int K3S, int TKS>
+// LDS layout: weights and time-encoding vectors as RowsLayout (biases and
+// the HEADS logit vectors in vec), then each wavefront's list.
+template <int K1S, int K3S, int TKS, int HEADS>
 struct PackedLayout {
     // w2 / w4 rows padded like the others, so that the 16-byte operand reads
     // of 16 consecutive rows fall on distinct banks.
@@ -1157,7 +1160,7 @@ struct PackedLayout {
     static constexpr uint32_t o_w3 = o_w2 + kH * ps * 2u;
     static constexpr uint32_t o_w4 = o_w3 + kH * ls3 * 2u;
     static constexpr uint32_t o_vec = o_w4 + kH * ps * 2u;
-    static constexpr uint32_t o_tenc = o_vec + 5u * kH * 4u;
+    static constexpr uint32_t o_tenc = o_vec + (4u + HEADS) * kH * 4u;
     static constexpr uint32_t o_list = o_tenc + 2u * 32u * TKS * 4u;
     static constexpr uint32_t o_qs = o_list + (kRowThreads / 64) * kPackList * (uint32_t)sizeof(PackEntry);
     static constexpr uint32_t bytes = o_qs + (kRowThreads / 64) * kPackList;
@@ -1172,17 +1175,18 @@ __device__ __forceinline__ uint32_t tenc_column(uint32_t kk) {
     return 4u * (8u * ks + i) + g;
 }
 
-template <int NKS, int EKS, int TKS, int NK, int EK>
+template <int NKS, int EKS, int TKS, int NK, int EK, int HEADS>
 __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void aggregate_packed(RowParams p) {
     constexpr int GS = NKS + EKS, K1S = GS + TKS, K3S = NKS + 2;
-    using L = PackedLayout<K1S, K3S, TKS>;
+    using L = PackedLayout<K1S, K3S, TKS, HEADS>;
+    static_assert(HEADS == 1 || HEADS == 2, "one or two heads");
     static_assert(NKS <= kRuSteps, "shape");
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     __bf16 *W1 = (__bf16 *)(smem + L::o_w1);
     __bf16 *W2 = (__bf16 *)(smem + L::o_w2);
     __bf16 *W3 = (__bf16 *)(smem + L::o_w3);
     __bf16 *W4 = (__bf16 *)(smem + L::o_w4);
-    float *vec = (float *)(smem + L::o_vec);   // b1 | b2 | b3 | b4 | v, 64 each
+    float *vec = (float *)(smem + L::o_vec);   // b1 | b2 | b3 | b4 | v_0 (| v_1), 64 each
 
     // Stage the weights as aggregate_rows does, except that the time-encoding
     // columns of w1 (and w, b) go in lane-group order (tenc_column).
@@ -1232,15 +1236,17 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         *(u32x2 *)(W3 + r * L::ls3 + 32u * NKS + c0) = u32x2{v3[0], v3[1]};
         *(u32x2 *)(W3 + r * L::ls3 + 32u * NKS + c1) = u32x2{v3[2], v3[3]};
     }
-    for (uint32_t u = tid; u < 5u * kH; u += kRowThreads) {
+    for (uint32_t u = tid; u < (4u + HEADS) * kH; u += kRowThreads) {
         const uint32_t k = u / kH, c = u % kH;
         float val;
         if (k < 4) {
             val = (k == 0 ? p.b1 : k == 1 ? p.b2 : k == 2 ? p.b3 : p.b4)[c];
         } else {
             val = 0.0f;
+            const uint32_t r0 = (k - 4u) * (kH / HEADS);
 #pragma unroll
-            for (uint32_t r = 0; r < kH; r++) val = __builtin_fmaf(p.att[r], (float)p.w2[r * kH + c], val);
+            for (uint32_t r = 0; r < kH / HEADS; r++)
+                val = __builtin_fmaf(p.att[r0 + r], (float)p.w2[(r0 + r) * kH + c], val);
         }
         vec[u] = val;
     }
@@ -1271,11 +1277,11 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
     PackEntry *lst = (PackEntry *)(smem + L::o_list) + (size_t)wave * kPackList;
     uint8_t *qs = smem + L::o_qs + (size_t)wave * kPackList;
     const float *b1 = vec, *b2 = vec + kH, *b3 = vec + 2 * kH, *b4 = vec + 3 * kH, *va = vec + 4 * kH;
-    float b1v[4], vav[4];
+    float b1v[4], vav1[4];
 #pragma unroll
     for (int ub = 0; ub < 4; ub++) {
         b1v[ub] = b1[16 * ub + r16];
-        vav[ub] = va[16 * ub + r16];
+        vav1[ub] = va[16 * ub + r16];
     }
     const uint32_t gq = p.gq;
     const uint64_t groups = ((uint64_t)p.nq + gq - 1) / gq;
@@ -1391,15 +1397,19 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         }
     };
 
-    // Running state of the group: aggd holds, in the D layout, each query's
-    // sum over its merged partials of exp(m - M) times the partial's
-    // exponential-weighted sums, and the lanes with r16 == q hold M_q (mrun)
-    // and the matching sum of exponentials (drun).
-    f32x4 aggdh[1][4];
-    f32x4 (&aggd)[4] = aggdh[0];
+    // Running state of the group, per head a: aggd[a] holds, in the D
+    // layout, each query's sum over its merged partials of exp(m - M) times
+    // the partial's exponential-weighted sums, and the lanes with r16 == q
+    // hold M_q (mrun[a]) and the matching sum of exponentials (drun[a]).
+    f32x4 aggd[HEADS][4];
+    float mrun[HEADS], drun[HEADS];
 #pragma unroll
-    for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
-    float mrun = -INFINITY, drun = 0.0f;
+    for (int a = 0; a < HEADS; a++) {
+#pragma unroll
+        for (int ub = 0; ub < 4; ub++) aggd[a][ub] = f32x4(0.0f);
+        mrun[a] = -INFINITY;
+        drun[a] = 0.0f;
+    }
 
     auto compute_block = [&](const PackRow &pr, const Rows &rc) {
         const PackEntry &en = pr.en;
@@ -1470,50 +1480,59 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         for (int ub = 0; ub < 4; ub++)
 #pragma unroll
             for (int i = 0; i < 4; i++) acc[ub][i] = relu(acc[ub][i]);
-        // Logits of rows 4 g + i (the lane group's rows; -inf where empty).
-        float lg[4];
-#pragma unroll
-        for (int i = 0; i < 4; i++) {
-            float t = vav[0] * acc[0][i];
-#pragma unroll
-            for (int ub = 1; ub < 4; ub++) t = __builtin_fmaf(vav[ub], acc[ub][i], t);
-            lg[i] = xor16_sum(t);
-        }
         const uint32_t nib = ((uint32_t)__builtin_amdgcn_ballot_w64(valid) >> (4u * g)) & 0xFu;
-#pragma unroll
-        for (int i = 0; i < 4; i++) lg[i] = ((nib >> i) & 1u) ? lg[i] : -INFINITY;
         // The block's rows into their queries' columns: the lane's column is
-        // query r16; bm is the largest logit of its rows in the block.
+        // query r16.
         bool mine[4];
-        float bm = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < 4; i++) {
-            mine[i] = ((pr.q4 >> (8 * i)) & 0xFFu) == r16;
-            bm = max2(bm, mine[i] ? lg[i] : -INFINITY);
-        }
-        bm = groups_max(bm);
-        const float mnew = max2(mrun, bm);
-        const float scl = (mrun == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f((mrun - mnew) * kLog2eAgg);
-        const float sh = (mnew == -INFINITY) ? 0.0f : mnew * kLog2eAgg;
-        float wr[4];
+        for (int i = 0; i < 4; i++) mine[i] = ((pr.q4 >> (8 * i)) & 0xFFu) == r16;
 #pragma unroll
-        for (int i = 0; i < 4; i++)
-            wr[i] = mine[i] ? __builtin_amdgcn_exp2f(__builtin_fmaf(lg[i], kLog2eAgg, -sh)) : 0.0f;
-        const float dc = groups_sum((wr[0] + wr[1]) + (wr[2] + wr[3]));
-        drun = __builtin_fmaf(drun, scl, dc);
-        mrun = mnew;
+        for (int a = 0; a < HEADS; a++) {
+            // Head a's logits of rows 4 g + i (the lane group's rows; -inf
+            // where empty); bm is the largest of its rows in the block.
+            // (one head: the logit vector kept in registers; two: read from
+            // LDS per block, the registers being taken by the aggregates)
+            float vav[4];
 #pragma unroll
-        for (int ub = 0; ub < 4; ub++)
+            for (int ub = 0; ub < 4; ub++) vav[ub] = HEADS == 1 ? vav1[ub] : va[a * kH + 16 * ub + r16];
+            float lg[4];
 #pragma unroll
-            for (int j = 0; j < 4; j++) aggd[ub][j] *= scl;
-        // aggd[ub] += A_i B_i over the rows 4 g + i: A_i[unit][k = g] is
-        // layer 1 of row 4 g + i (this lane's acc[ub][i]), B_i[k = g][n] the
-        // row's weight in column n (this lane's wr[i] for n = r16).
+            for (int i = 0; i < 4; i++) {
+                float t = vav[0] * acc[0][i];
 #pragma unroll
-        for (int i = 0; i < 4; i++)
+                for (int ub = 1; ub < 4; ub++) t = __builtin_fmaf(vav[ub], acc[ub][i], t);
+                lg[i] = xor16_sum(t);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; i++) lg[i] = ((nib >> i) & 1u) ? lg[i] : -INFINITY;
+            float bm = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < 4; i++) bm = max2(bm, mine[i] ? lg[i] : -INFINITY);
+            bm = groups_max(bm);
+            const float mnew = max2(mrun[a], bm);
+            const float scl =
+                (mrun[a] == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f((mrun[a] - mnew) * kLog2eAgg);
+            const float sh = (mnew == -INFINITY) ? 0.0f : mnew * kLog2eAgg;
+            float wr[4];
+#pragma unroll
+            for (int i = 0; i < 4; i++)
+                wr[i] = mine[i] ? __builtin_amdgcn_exp2f(__builtin_fmaf(lg[i], kLog2eAgg, -sh)) : 0.0f;
+            const float dc = groups_sum((wr[0] + wr[1]) + (wr[2] + wr[3]));
+            drun[a] = __builtin_fmaf(drun[a], scl, dc);
+            mrun[a] = mnew;
 #pragma unroll
             for (int ub = 0; ub < 4; ub++)
-                aggd[ub] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[ub][i], wr[i], aggd[ub], 0, 0, 0);
+#pragma unroll
+                for (int j = 0; j < 4; j++) aggd[a][ub][j] *= scl;
+            // aggd[a][ub] += A_i B_i over the rows 4 g + i: A_i[unit][k = g]
+            // is layer 1 of row 4 g + i (this lane's acc[ub][i]), B_i[k = g][n]
+            // the row's weight in column n (this lane's wr[i] for n = r16).
+#pragma unroll
+            for (int i = 0; i < 4; i++)
+#pragma unroll
+                for (int ub = 0; ub < 4; ub++)
+                    aggd[a][ub] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[ub][i], wr[i], aggd[a][ub], 0, 0, 0);
+        }
     };
 
     // Prologue: the first group's list and the next group's scan in flight.
@@ -1586,18 +1605,26 @@ __global__ __launch_bounds__(kRowThreads) __attribute__((amdgpu_waves_per_eu(2, 
         nx_nd = id_nd;
         load_ids(cg + 3 * gstep, id_nd, id_t);
         // The group's aggregates, normalised, then MLP_out.
-        const float ne = drun > 0.0f ? 1.0f : 0.0f;
-        const float inv = drun > 0.0f ? __builtin_amdgcn_rcpf(drun) : 0.0f;
+        // (every head has the same valid rows: drun[0] > 0 iff the query
+        // has one)
+        const float ne = drun[0] > 0.0f ? 1.0f : 0.0f;
 #pragma unroll
-        for (int ub = 0; ub < 4; ub++)
+        for (int a = 0; a < HEADS; a++) {
+            const float inv = drun[a] > 0.0f ? __builtin_amdgcn_rcpf(drun[a]) : 0.0f;
 #pragma unroll
-            for (int i = 0; i < 4; i++) aggd[ub][i] *= inv;
-        mlp_out_group<NKS, NK, L::ls3, L::ps, 1>(p, ru, nr, vq, aggdh, ne, W2, W3, W4, b2, b3, b4, r16, g,
-                                                 cg * gq);
+            for (int ub = 0; ub < 4; ub++)
 #pragma unroll
-        for (int ub = 0; ub < 4; ub++) aggd[ub] = f32x4(0.0f);
-        mrun = -INFINITY;
-        drun = 0.0f;
+                for (int i = 0; i < 4; i++) aggd[a][ub][i] *= inv;
+        }
+        mlp_out_group<NKS, NK, L::ls3, L::ps, HEADS>(p, ru, nr, vq, aggd, ne, W2, W3, W4, b2, b3, b4, r16, g,
+                                                     cg * gq);
+#pragma unroll
+        for (int a = 0; a < HEADS; a++) {
+#pragma unroll
+            for (int ub = 0; ub < 4; ub++) aggd[a][ub] = f32x4(0.0f);
+            mrun[a] = -INFINITY;
+            drun[a] = 0.0f;
+        }
         n_cur = n_next;
     }
 }
@@ -1738,17 +1765,23 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
         // Tables of at most 16 slots take the packed form when the groups
         // are large enough for packing to fill blocks (small launches are
         // bound by their per-group steps).
-        const bool packed = h->s <= kPackMaxS && r.gq >= kPackMinGroup && heads == 1;
+        const bool packed = h->s <= kPackMaxS && r.gq >= kPackMinGroup && heads <= 2;
         // One or two heads: the per-query kernel; more heads take the tiled kernel.
         const bool rows_ok = heads <= 2;
 #define NLB_ROWS_SHAPE(A, B, C, NK, EK)                                                              \
     if (!kern && rows_ok && nks == A && eks == B && tks == C && (A == 0 || nkind == NK) &&          \
         (B == 0 || ekind == EK)) {                                                                    \
-        if (packed) {                                                                                 \
-            kern = (const void *)aggregate_packed<A, B, C, NK, EK>;                                   \
-            bytes = PackedLayout<A + B + C, A + 2, C>::bytes;                                         \
+        if (packed && heads == 1) {                                                                   \
+            kern = (const void *)aggregate_packed<A, B, C, NK, EK, 1>;                                \
+            bytes = PackedLayout<A + B + C, A + 2, C, 1>::bytes;                                      \
             launch = [](dim3 gr, uint32_t l, hipStream_t st, const RowParams &rp) {                   \
-                hipLaunchKernelGGL((aggregate_packed<A, B, C, NK, EK>), gr, dim3(kRowThreads), l, st, rp); \
+                hipLaunchKernelGGL((aggregate_packed<A, B, C, NK, EK, 1>), gr, dim3(kRowThreads), l, st, rp); \
+            };                                                                                        \
+        } else if (packed) {                                                                          \
+            kern = (const void *)aggregate_packed<A, B, C, NK, EK, 2>;                                \
+            bytes = PackedLayout<A + B + C, A + 2, C, 2>::bytes;                                      \
+            launch = [](dim3 gr, uint32_t l, hipStream_t st, const RowParams &rp) {                   \
+                hipLaunchKernelGGL((aggregate_packed<A, B, C, NK, EK, 2>), gr, dim3(kRowThreads), l, st, rp); \
             };                                                                                        \
         } else {                                                                                      \
             bytes = RowsLayout<A + B + C, A + 2, C>::bytes;                                           \

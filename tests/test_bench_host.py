@@ -72,7 +72,8 @@ def test_aggregate_counter_summary_and_kernel_choice(monkeypatch):
     assert bench.aggregate_kernel(w, 300000, 256) == "aggregate_packed"
     assert bench.aggregate_kernel(synth.workload(1), 600, 256) == "aggregate_rows"
     assert bench.aggregate_kernel(synth.workload(3), 12000, 256) == "aggregate_rows"   # s = 64
-    assert bench.aggregate_kernel(w, 300000, 256, heads=2) == "aggregate_rows"
+    assert bench.aggregate_kernel(w, 300000, 256, heads=2) == "aggregate_packed"
+    assert bench.aggregate_kernel(w, 3000, 256, heads=2) == "aggregate_rows"
     assert bench.aggregate_kernel(w, 300000, 256, heads=4) == "aggregate_fused"
 
 
