@@ -412,7 +412,7 @@ class EncodeStream:
         self.depth = depth
         self.gathered = torch.cuda.Event()
         self.encoded = [torch.cuda.Event() for _ in range(depth)]
-        self.used = [False] * depth
+        self.used = [None] * depth    # the event that marks each set's last encoding
         self.count = 0
 
     @property
@@ -420,33 +420,38 @@ class EncodeStream:
         """The output set the next retrieval writes."""
         return self.count % self.depth
 
-    def sample_into(self, table, q, tq, o):
+    def sample_into(self, table, q, tq, o, events=None):
+        """``events``: (gathered, encoded) events to record instead of this
+        object's own (timing events of the caller: one record serves both
+        the ordering and the timing, and every record costs the stream a
+        few microseconds)."""
         o = dict(o)
         tenc = o.pop("tenc")
         table.sample_into(q, tq, o)
-        self.gathered.record()
-        self.stream.wait_event(self.gathered)
+        gathered, encoded = events if events is not None else (self.gathered, self.encoded[self.slot])
+        gathered.record()
+        self.stream.wait_event(gathered)
         table.time_encode_into(o["ts"], tq, tenc, stream=self.stream)
-        self.encoded[self.slot].record(self.stream)
-        self.used[self.slot] = True
+        encoded.record(self.stream)
+        self.used[self.slot] = encoded
         self.count += 1
 
     def join(self):
         import torch
-        if self.used[self.slot]:
-            torch.cuda.current_stream().wait_event(self.encoded[self.slot])
+        if self.used[self.slot] is not None:
+            torch.cuda.current_stream().wait_event(self.used[self.slot])
 
     def forget(self):
         """Drop the record of earlier encodings once the device has finished
         them (after a synchronisation), so that no later join waits on an
         event recorded outside a graph being captured."""
-        self.used = [False] * self.depth
+        self.used = [None] * self.depth
 
     def join_all(self):
         import torch
         for k in range(self.depth):
-            if self.used[k]:
-                torch.cuda.current_stream().wait_event(self.encoded[k])
+            if self.used[k] is not None:
+                torch.cuda.current_stream().wait_event(self.used[k])
 
 
 def streamed_leg(w, table, b0, n, out, nbr, dev, live, host_slots=8, dev_slots=4, enc=None):
@@ -747,7 +752,7 @@ def main():
             status.normal_(generator=torch.Generator(device=dev).manual_seed(7000 + w.key))
     setup_s = time.perf_counter() - t_setup
 
-    def step(b, nbr_out):
+    def step(b, nbr_out, events=None):
         s_, d_, t_, q, tq = synth.batch_views(w, nodes, ts, b)
         n = q.numel()
         if agg_w is not None:
@@ -756,7 +761,7 @@ def main():
         o = {k: v[:n] for k, v in outs[enc.slot if enc is not None else 0].items()}
         o["nbr"] = nbr_out[:n]
         if enc is not None:
-            enc.sample_into(table, q, tq, o)
+            enc.sample_into(table, q, tq, o, events)
         else:
             table.sample_into(q, tq, o)
         return s_, d_, t_, n
@@ -798,10 +803,13 @@ def main():
     for k in range(K):
         b = start + W + k
         e_start[k].record()
-        s_, d_, t_, n = step(b, nbr_all[k])
-        e_sample[k].record()
         if enc is not None:
-            e_enc[k].record(enc.stream)
+            # the encoder records e_sample (end of the table reads) and
+            # e_enc (end of the encoding) as its ordering events
+            s_, d_, t_, n = step(b, nbr_all[k], (e_sample[k], e_enc[k]))
+        else:
+            s_, d_, t_, n = step(b, nbr_all[k])
+            e_sample[k].record()
         if hop2_out is not None:
             _, _, _, _, tq = synth.batch_views(w, nodes, ts, b)
             o2 = {kk: v[:n * w.s] for kk, v in hop2_out.items()}
