@@ -1766,7 +1766,8 @@ extern "C" int nlb_aggregate(nlb_table *h, const int32_t *node, const uint32_t *
         // are large enough for packing to fill blocks (small launches are
         // bound by their per-group steps).
         const bool packed = h->s <= kPackMaxS && r.gq >= kPackMinGroup && heads <= 2;
-        // One or two heads: the per-query kernel; more heads take the tiled kernel.
+        // One or two heads: the packed or the per-query kernel; more heads take
+        // the tiled kernel.
         const bool rows_ok = heads <= 2;
 #define NLB_ROWS_SHAPE(A, B, C, NK, EK)                                                              \
     if (!kern && rows_ok && nks == A && eks == B && tks == C && (A == 0 || nkind == NK) &&          \
