@@ -137,3 +137,47 @@ def test_time_encode_errors():
     assert g.status() == 0
     g.close()
     no_t.close()
+
+
+def test_split_retrieval_replays_in_a_hip_graph():
+    """The split retrieval captured in one HIP graph, the encoding on a
+    second stream forked and joined by events inside the capture (as the
+    benchmark's graph mode runs it): replayed three times with eager work on
+    the outputs between replays, every replay equals the eager call."""
+    import torch
+    base = synth.workload(4)
+    w = synth.scaled(base, 6 * base.batch)
+    src, dst, t, neg = synth.host_links(w)
+    g = make_gpu_table(w)
+    B = w.batch
+    g.insert(to_dev(src[:4 * B]), to_dev(dst[:4 * B]), to_dev(t[:4 * B]))
+    sl = slice(4 * B, 5 * B)
+    q = to_dev(np.concatenate([src[sl], dst[sl], neg[sl]]).astype(np.int32))
+    tq = to_dev(np.concatenate([t[sl]] * 3).astype(np.uint32))
+    nq = 3 * B
+    out = g.alloc_outputs(nq, want=("nbr", "eid", "ts", "tenc"))
+    g.sample_into(q, tq, out)                        # eager reference, one call
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in out.items()}
+    side = torch.cuda.Stream()
+    ev, done = torch.cuda.Event(), torch.cuda.Event()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        ids = {k: out[k] for k in ("nbr", "eid", "ts")}
+        g.sample_into(q, tq, ids)
+        ev.record()
+        side.wait_event(ev)
+        g.time_encode_into(out["ts"], tq, out["tenc"], stream=side)
+        done.record(side)
+        torch.cuda.current_stream().wait_event(done)
+    for rep in range(3):
+        for v in out.values():
+            v.fill_(7)                               # eager work on the same buffers
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k, v in out.items():
+            assert torch.equal(v, ref[k]), f"replay {rep}: {k}"
+    del graph
+    assert g.status() == 0
+    g.close()
