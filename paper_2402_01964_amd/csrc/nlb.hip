@@ -270,6 +270,30 @@ template <int W> struct VecOf;
 template <> struct VecOf<16> { typedef u32x4 T; };
 template <> struct VecOf<8> { typedef u32x2 T; };
 template <> struct VecOf<4> { typedef uint32_t T; };
+// Three dwords, moved as three 4-byte accesses (which the compiler may join
+// into one 12-byte access): a three-element vector type would be widened to
+// 16 bytes and touch the next row's first word.
+struct U32x3 {
+    uint32_t x, y, z;
+};
+template <> struct VecOf<12> { typedef U32x3 T; };
+
+template <typename V> __device__ __forceinline__ V unit_zero() { return V(0); }
+template <> __device__ __forceinline__ U32x3 unit_zero<U32x3>() { return U32x3{0u, 0u, 0u}; }
+template <typename V> __device__ __forceinline__ V unit_load(const uint8_t *p) { return *(const V *)p; }
+template <> __device__ __forceinline__ U32x3 unit_load<U32x3>(const uint8_t *p) {
+    const uint32_t *q = (const uint32_t *)p;
+    return U32x3{q[0], q[1], q[2]};
+}
+template <typename V> __device__ __forceinline__ void unit_store(V v, uint8_t *p) {
+    __builtin_nontemporal_store(v, (V *)p);
+}
+template <> __device__ __forceinline__ void unit_store<U32x3>(U32x3 v, uint8_t *p) {
+    uint32_t *q = (uint32_t *)p;
+    __builtin_nontemporal_store(v.x, q);
+    __builtin_nontemporal_store(v.y, q + 1);
+    __builtin_nontemporal_store(v.z, q + 2);
+}
 
 // Row source of output row j: the neighbour's node row (kind 0), the
 // link's row (kind 1) or the query node's row (kind 2).
@@ -305,7 +329,7 @@ __device__ __forceinline__ void gather_tile(const uint8_t *__restrict__ src, uin
                                             const int32_t *tile_nodes, uint8_t *__restrict__ out,
                                             uint32_t tid) {
     typedef typename VecOf<W>::T V;
-    constexpr int R = (W == 16) ? 4 : (W == 8 ? 6 : 8);
+    constexpr int R = (W == 16) ? 4 : (W == 4 ? 8 : 6);
     const uint32_t total = rows * units;
     const uint32_t dq = nlb_div(kTileThreads, m), dr = kTileThreads - dq * units;
     RowCursor cur(tid, units, m);
@@ -316,7 +340,7 @@ __device__ __forceinline__ void gather_tile(const uint8_t *__restrict__ src, uin
             const uint32_t f = base + r * kTileThreads + tid;
             const uint32_t j = cur.j, c = cur.c;
             cur.step(units, dq, dr);
-            val[r] = V(0);
+            val[r] = unit_zero<V>();
             if (f < total) {
                 int64_t row;
                 if (KIND == kRowSelf) {
@@ -326,13 +350,13 @@ __device__ __forceinline__ void gather_tile(const uint8_t *__restrict__ src, uin
                     row = (sl.x < 0) ? -1 : (KIND == kRowNeighbour ? (int64_t)sl.x : (int64_t)sl.e);
                 }
                 if (row >= 0 && row < src_rows)
-                    val[r] = *(const V *)(src + (size_t)row * row_bytes + (size_t)c * W);
+                    val[r] = unit_load<V>(src + (size_t)row * row_bytes + (size_t)c * W);
             }
         }
 #pragma unroll
         for (int r = 0; r < R; r++) {
             const uint32_t f = base + r * kTileThreads + tid;
-            if (f < total) __builtin_nontemporal_store(val[r], (V *)(out + (size_t)f * W));
+            if (f < total) unit_store<V>(val[r], out + (size_t)f * W);
         }
     }
 }
@@ -345,6 +369,8 @@ __device__ __forceinline__ void gather_tile_w(uint32_t width, const uint8_t *src
                                               uint32_t tid) {
     if (width == 16)
         gather_tile<16, KIND>(src, row_bytes, units, m, rows, src_rows, slots, tile_nodes, out, tid);
+    else if (width == 12)
+        gather_tile<12, KIND>(src, row_bytes, units, m, rows, src_rows, slots, tile_nodes, out, tid);
     else if (width == 8)
         gather_tile<8, KIND>(src, row_bytes, units, m, rows, src_rows, slots, tile_nodes, out, tid);
     else
@@ -542,6 +568,13 @@ uint32_t block_bytes_for(uint32_t s) {
         return b;
     }
     return (need + 127u) / 128u * 128u;
+}
+
+// Copy unit of the sample's row gathers: copy_width's 16 or 8 bytes, else 12
+// for rows of a multiple of 12 bytes (e.g. 186 bf16 values), else 4.
+uint32_t row_copy_width(uint32_t row_bytes, const void *src, const void *dst_or_null) {
+    const uint32_t w = copy_width(row_bytes, src, dst_or_null);
+    return w == 4 && row_bytes % 12 == 0 ? 12u : w;
 }
 
 // Queries per sample tile.  Large launches use as many queries as fit
@@ -782,12 +815,12 @@ static int launch_sample(nlb_table *h, const int32_t *node, const uint32_t *tq, 
     p.tenc_vec = vec4 ? 4 : 1;
     p.tenc_units = h->d_time ? (vec4 ? h->d_time / 4 : h->d_time) : 1;
     p.tenc_m = nlb_div_magic(p.tenc_units);
-    p.e_width = h->erb ? copy_width(h->erb, h->efeat, out->efeat) : 4;
+    p.e_width = h->erb ? row_copy_width(h->erb, h->efeat, out->efeat) : 4;
     p.e_units = h->erb ? h->erb / p.e_width : 1;
     p.e_m = nlb_div_magic(p.e_units);
     // the same width serves the neighbour rows and the self row
     const uintptr_t nalign = (uintptr_t)out->nfeat | (uintptr_t)out->self;
-    p.n_width = h->nrb ? copy_width(h->nrb, h->nfeat, (const void *)nalign) : 4;
+    p.n_width = h->nrb ? row_copy_width(h->nrb, h->nfeat, (const void *)nalign) : 4;
     p.n_units = h->nrb ? h->nrb / p.n_width : 1;
     p.n_m = nlb_div_magic(p.n_units);
     p.tile_q = tile_queries(h->s, nq);
