@@ -226,7 +226,7 @@ __global__ __launch_bounds__(kInsertThreads) void insert_commit(InsertParams p) 
 // row), writes the id outputs and stages each slot's (neighbour, arrival
 // index, timestamp, gap) in LDS.  The later phases walk the flattened output
 // ranges (time encoding, link rows, neighbour rows, self rows) with every
-// thread taking consecutive 16-, 8- or 4-byte units; they look up their slot
+// thread taking consecutive 16-, 12-, 8- or 4-byte units; they look up their slot
 // in LDS and keep several row loads in flight before storing.
 constexpr int kTileThreads = 256;
 constexpr int kTileSlots = 1024;   // slot rows staged per tile (16 B each in LDS)
